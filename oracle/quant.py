@@ -1,0 +1,189 @@
+"""Block quantizer Q(X) and reconstruction for CurveFP (oracle; test infrastructure only).
+
+Plain numpy in float64.  Each function follows the paper's definition directly:
+
+* reconstruction  x_hat = (-1)^s 2^{a_b} r^{e+k/K}             (Eq. curvefp-value)
+* quantization    keep the sign, take the magnitude nearest to |x| in absolute
+                  error, saturate at the endpoints                 (Sec. 3.1)
+* block scale     dynamic operands use ceil-absmax scaling         (Sec. 3.1, App. A.2)
+
+Readings taken where the paper is silent (each is listed in the design doc):
+
+* ceil-absmax: a_b is the smallest integer a with amax <= 2^a * fl32(L_max),
+  L_max = r^{n_max/K} the largest positive level.  fl32(L_max) is the value the
+  top code actually reconstructs to, so a block that holds its own top code
+  keeps its scale (quantize(dequantize(c)) == c).  All-zero block -> a_b = 0.
+  a_b is stored as int8, clamped to [-127, 127].
+* non-finite inputs: a block holding NaN or +-Inf gets scale -128 and all-zero
+  codes; it reconstructs to NaN.
+* the zero sentinel is the only zero: every zero result is code 0x00 (the
+  source sign of a zero result is not kept).
+* the candidate set for the nearest search is {0} U {levels}: a tiny value goes
+  to zero when it is nearer to zero than to the smallest level.
+* reconstruction to fp32 is the fp32 value nearest to the real x_hat.
+* E3C3 codes are packed 7 bits each, LSB first: code i of a 32-element block
+  occupies bits [7i, 7i+7) of a 224-bit little-endian string (28 bytes).
+"""
+
+import numpy as np
+
+from .formats import Format
+
+POISON_SCALE = -128
+SCALE_MIN = -127
+SCALE_MAX = 127
+
+
+def _sig_table(fmt: Format) -> np.ndarray:
+    """S[r] = 2^{r/N} for r in [0, N), N = qK: the fractional part of every level."""
+    N = fmt.N
+    return np.array([2.0 ** (r / N) for r in range(N)], dtype=np.float64)
+
+
+def level_value_f64(fmt: Format, n):
+    """r^{n/K} = 2^{p n / (qK)} in float64 (Sec. 3.2: r^{e+k/K} = 2^{p(eK+k)/(qK)}).
+
+    Written as ldexp(S[u mod N], floor(u / N)) with u = p*n, so levels one
+    octave apart differ by exactly a factor of two in float64 as well.
+    """
+    n = np.asarray(n, dtype=np.int64)
+    u = fmt.p * n
+    N = fmt.N
+    frac = np.mod(u, N)
+    whole = np.floor_divide(u, N)
+    return np.ldexp(_sig_table(fmt)[frac], whole.astype(np.int64))
+
+
+def top_level_fp32(fmt: Format) -> float:
+    """fl32(L_max): the fp32 value of the largest level at scale 0."""
+    return float(np.float32(level_value_f64(fmt, fmt.n_max)))
+
+
+def scale_exponents(amax: np.ndarray, fmt: Format) -> np.ndarray:
+    """Ceil-absmax block scale: smallest integer a with amax <= 2^a * fl32(L_max).
+
+    ``amax`` holds the block maxima of |x| in float64 (exact copies of fp32
+    values).  Zero blocks get 0, non-finite blocks get POISON_SCALE, the rest is
+    clamped to [-127, 127].  Returns int64.
+    """
+    amax = np.asarray(amax, dtype=np.float64)
+    lm = top_level_fp32(fmt)
+    finite = np.isfinite(amax)
+    pos = finite & (amax > 0)
+    safe = np.where(pos, amax, 1.0)
+    a = np.ceil(np.log2(safe) - np.log2(lm)).astype(np.int64)
+    # make a exact with two-sided checks (ldexp by an integer is exact in fp64)
+    for _ in range(3):
+        a = np.where(safe > np.ldexp(lm, a), a + 1, a)
+        a = np.where(safe <= np.ldexp(lm, a - 1), a - 1, a)
+    assert np.all(safe[pos] <= np.ldexp(lm, a[pos]))
+    assert np.all(safe[pos] > np.ldexp(lm, a[pos] - 1))
+    a = np.where(pos, a, 0)
+    a = np.clip(a, SCALE_MIN, SCALE_MAX)
+    a = np.where(finite, a, POISON_SCALE)
+    return a.astype(np.int64)
+
+
+def _nearest_index(y: np.ndarray, fmt: Format):
+    """Nearest element of {0} U {r^{n/K}: n_min <= n <= n_max} to y >= 0.
+
+    Returns (is_zero, n).  Candidates: zero, and the four levels around the
+    continuous index floor(log_r(y) * K); the nearest is found by comparing
+    absolute errors |y - level| (Sec. 3.1).  Values above the top level end up
+    on n_max and values below the smallest level on n_min or zero, which is the
+    saturation the paper asks for.
+    """
+    y = np.asarray(y, dtype=np.float64)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        cont = np.floor(np.log2(np.where(y > 0, y, 1.0)) * fmt.N / fmt.p)
+    cont = np.where(y > 0, cont, fmt.n_min).astype(np.int64)
+    best_n = np.full(y.shape, fmt.n_min, dtype=np.int64)
+    best_d = np.full(y.shape, np.inf)
+    for d in (-1, 0, 1, 2):
+        cand = np.clip(cont + d, fmt.n_min, fmt.n_max)
+        dist = np.abs(y - level_value_f64(fmt, cand))
+        take = dist < best_d
+        best_n = np.where(take, cand, best_n)
+        best_d = np.where(take, dist, best_d)
+    is_zero = y < best_d  # |y - 0| < |y - nearest level|
+    return is_zero, best_n
+
+
+def quantize(x: np.ndarray, fmt: Format, block: int = 32):
+    """Q(X) along the last axis in blocks of ``block`` consecutive elements.
+
+    x: float32 array [outer, k] (bf16 sources are passed widened to fp32).
+    Returns (codes uint8 [outer, k], scales int8 [outer, k // block]); codes
+    are unpacked, one per byte, for every format.
+    """
+    x = np.asarray(x)
+    assert x.dtype == np.float32 and x.ndim == 2
+    outer, k = x.shape
+    assert k % block == 0
+    xb = x.astype(np.float64).reshape(outer, k // block, block)
+    mag = np.abs(xb)
+    with np.errstate(invalid="ignore"):
+        finite_block = np.all(np.isfinite(xb), axis=-1)
+    amax = np.where(finite_block, np.max(np.where(np.isfinite(mag), mag, 0.0), axis=-1), np.inf)
+    a = scale_exponents(amax, fmt)
+    a_safe = np.where(finite_block, a, 0)
+    y = np.ldexp(np.where(np.isfinite(mag), mag, 0.0), -a_safe[..., None])
+    is_zero, n = _nearest_index(y, fmt)
+    sign = np.signbit(xb).astype(np.int64)
+    m = n + fmt.B
+    codes = (sign << (fmt.E + fmt.C)) | m
+    codes = np.where(is_zero, 0, codes)
+    codes = np.where(finite_block[..., None], codes, 0)
+    return codes.reshape(outer, k).astype(np.uint8), a.astype(np.int8)
+
+
+def quantize_axis0(x: np.ndarray, fmt: Format, block: int = 32):
+    """Blocks along the rows of x: quantizes x^T, giving codes [cols, rows]."""
+    return quantize(np.ascontiguousarray(np.asarray(x).T), fmt, block)
+
+
+def code_fields(codes: np.ndarray, fmt: Format):
+    """Split element codes into (nonzero, sign, n) with n = m - B (Sec. 3.1)."""
+    codes = np.asarray(codes).astype(np.int64)
+    m = codes & ((1 << (fmt.E + fmt.C)) - 1)
+    s = (codes >> (fmt.E + fmt.C)) & 1
+    return m != 0, s, m - fmt.B
+
+
+def dequantize(codes: np.ndarray, scales: np.ndarray, fmt: Format, block: int = 32) -> np.ndarray:
+    """x_hat = (-1)^s 2^{a_b} r^{n/K} rounded to the nearest fp32 (Eq. curvefp-value).
+
+    codes uint8 [outer, k] (unpacked), scales int8 [outer, k // block].
+    Zero codes give +0.0; poisoned blocks (scale -128) give NaN.
+    """
+    codes = np.asarray(codes)
+    outer, k = codes.shape
+    nz, s, n = code_fields(codes, fmt)
+    a = np.repeat(np.asarray(scales).astype(np.int64), block, axis=1)
+    mag = np.ldexp(level_value_f64(fmt, np.where(nz, n, 0)), a)
+    val = np.where(s == 1, -mag, mag)
+    val = np.where(nz, val, 0.0)
+    out = val.astype(np.float32)
+    out = np.where(a == POISON_SCALE, np.float32(np.nan), out)
+    return out.astype(np.float32)
+
+
+def pack7(codes: np.ndarray, block: int = 32) -> np.ndarray:
+    """Pack 7-bit codes [outer, k] into [outer, k // 32, 28] bytes, LSB first."""
+    codes = np.asarray(codes, dtype=np.uint8)
+    assert block == 32
+    outer, k = codes.shape
+    assert np.all(codes < 128)
+    bits = np.unpackbits(codes[..., None], axis=-1, bitorder="little")[..., :7]
+    bits = bits.reshape(outer, k // 32, 32 * 7)
+    return np.packbits(bits, axis=-1, bitorder="little")  # 224 bits -> 28 bytes
+
+
+def unpack7(packed: np.ndarray, k: int) -> np.ndarray:
+    """Inverse of pack7: [outer, k // 32, 28] bytes -> codes [outer, k]."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    outer = packed.shape[0]
+    packed = packed.reshape(outer, k // 32, 28)
+    bits = np.unpackbits(packed, axis=-1, bitorder="little").reshape(outer, k // 32, 32, 7)
+    weights = (1 << np.arange(7)).astype(np.uint16)
+    return (bits.astype(np.uint16) * weights).sum(-1).reshape(outer, k).astype(np.uint8)

@@ -1,0 +1,456 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+CPU only.  Every check here uses a route independent of the code it checks:
+paper-printed values (tests/golden/paper_tables.json), rigorous integer
+brackets (tests/exact_ref.py), mpmath, exact rationals, or numpy float64
+matmul of reconstructed values.
+"""
+
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import formats as F
+from tests import exact_ref as X
+
+GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_tables.json")))
+FMT_NAMES = ("E4C3", "E5C2", "E3C3")
+
+
+# ------------------------------------------------------------------ tables
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_format_table(name):
+    """Tab. curvefp-formats: bits, E, C, positive levels and H."""
+    g = GOLD["formats"][name]
+    f = oracle.get_format(name)
+    assert (f.bits, f.E, f.C, f.positive_levels, f.H) == (g["bits"], g["E"], g["C"], g["positive"], g["H"])
+    # every canonical magnitude is a distinct level and the codes use exactly bits
+    ranks = np.arange(1, 2 ** (f.E + f.C))
+    nz, s, n = oracle.code_fields(ranks, f)
+    assert nz.all() and len(set(n.tolist())) == g["positive"]
+    assert (2 ** (f.E + f.C + 1) - 1) < 2 ** g["bits"]
+
+
+def test_e5c2_moves_one_bit():
+    """Sec. 3.3: E4C3 -> E5C2 keeps 127 levels, phases 8 -> 4."""
+    g = GOLD["e5c2_vs_e4c3"]
+    a, b = oracle.get_format("E4C3"), oracle.get_format("E5C2")
+    assert a.positive_levels == b.positive_levels == g["levels"]
+    assert (a.H, b.H) == (g["H_from"], g["H_to"])
+
+
+def _occupied_phases(f):
+    """Phases actually hit by all nonzero code pairs (brute force over the codebook)."""
+    seen = set()
+    mags = range(1, 2 ** (f.E + f.C))
+    for mx in mags:
+        for mw in mags:
+            d, h, t = oracle.product_address(mx, 0, mw, 0, f)
+            seen.add(h)
+    return seen
+
+
+@pytest.mark.parametrize("case", GOLD["radix_phases"]["cases"], ids=lambda c: f"p{c['p']}q{c['q']}")
+def test_phase_count_rational_radix(case):
+    """Tab. radix-frontier: 8 / 9 / 32 phases; brute-force occupancy equals H."""
+    f = oracle.rational_format(case["E"], case["C"], case["p"], case["q"])
+    assert f.H == case["H"]
+    assert _occupied_phases(f) == set(range(case["H"]))
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_phase_count_principal(name):
+    f = oracle.get_format(name)
+    assert _occupied_phases(f) == set(range(GOLD["formats"][name]["H"]))
+
+
+def test_storage_rates():
+    """Sec. 4.2 / Eq. effective-rate: printed E3C3 rates are met with integer S."""
+    f = oracle.get_format(GOLD["storage_rates"]["format"])
+    for c in GOLD["storage_rates"]["cases"]:
+        ok = [S for S in range(1, 9) if round(f.storage_rate(c["G"], S), 3) == c["printed"]]
+        assert ok, c
+
+
+def test_e4c3_tile_encoding():
+    """App. C.1: q = m - 64 and q_p = m_a + m_b - 128 = 8e + k for every pair."""
+    g = GOLD["tile_encoding"]
+    f = oracle.get_format("E4C3")
+    for ma in range(1, 128):
+        for sa in (0, 1):
+            code_a = (sa << g["sign_bit"]) | ma
+            nz, s, n = (int(v[0]) for v in oracle.code_fields(np.array([code_a]), f))
+            assert nz and s == sa and n == ma - g["q_offset"]
+    for ma in range(1, 128):
+        for mb in range(1, 128):
+            d, h, t = oracle.product_address(ma, 0, mb | 0x80, 0, f)
+            qp = ma + mb - g["product_offset"]
+            e, k = divmod(qp, g["curves"])
+            assert (h, t, d) == (k, e, -1)
+
+
+# ------------------------------------------------------------------ closure
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_closed_product_all_pairs(name):
+    """Eq. curve-index-product vs the bin address of App. A.1, and the value.
+
+    For every pair of nonzero codes (both signs) and a few scale pairs:
+    l = (i + j) mod K, c = floor((i + j) / K), exponent e_x + e_w + c and sign
+    xor must equal (h, t, delta) of the general addressing, and
+    delta 2^t 2^(h/H) must equal the product of the two reconstructed values
+    computed from their (s, e, k) fields with mpmath.
+    """
+    import mpmath
+    mpmath.mp.dps = 40
+    f = oracle.get_format(name)
+    K = f.K
+    mags = np.arange(1, 2 ** (f.E + f.C))
+    codes = np.concatenate([mags, mags | (1 << (f.E + f.C))])
+    nz, s, n = oracle.code_fields(codes, f)
+    e, k = np.floor_divide(n, K), np.mod(n, K)
+    rng = np.random.default_rng(0)
+    scale_pairs = [(0, 0), (-5, 3)]
+    for ax, aw in scale_pairs:
+        for ix in range(len(codes)):
+            for iw in range(len(codes)):
+                d, h, t = oracle.product_address(int(codes[ix]), ax, int(codes[iw]), aw, f)
+                l = (k[ix] + k[iw]) % K
+                c = (k[ix] + k[iw]) // K
+                assert h == l
+                assert t == ax + aw + e[ix] + e[iw] + c
+                assert d == (-1 if s[ix] ^ s[iw] else 1)
+        # numeric value on a random subset (mpmath is slow)
+        for _ in range(300):
+            ix, iw = rng.integers(0, len(codes), 2)
+            d, h, t = oracle.product_address(int(codes[ix]), ax, int(codes[iw]), aw, f)
+            vx = (-1) ** int(s[ix]) * mpmath.power(2, ax) * mpmath.power(2, int(e[ix]) + mpmath.mpf(int(k[ix])) / K)
+            vw = (-1) ** int(s[iw]) * mpmath.power(2, aw) * mpmath.power(2, int(e[iw]) + mpmath.mpf(int(k[iw])) / K)
+            got = d * mpmath.power(2, t) * mpmath.power(2, mpmath.mpf(h) / f.H)
+            assert abs(got - vx * vw) <= mpmath.mpf(10) ** -30 * abs(vx * vw)
+
+
+def test_zero_short_circuits():
+    f = oracle.get_format("E4C3")
+    for c in (0x00, 0x80):
+        assert oracle.product_address(c, 0, 0x45, 0, f) is None
+        assert oracle.product_address(0x45, 0, c, 0, f) is None
+
+
+# ------------------------------------------------------------------ quantizer
+
+def _blocks_with_scale0(values, f):
+    """Blocks of 32 whose first element is fl32(L_max), so the block scale is 0."""
+    lm = np.float32(oracle.level_value_f64(f, f.n_max))
+    per = 31
+    nb = -(-len(values) // per)
+    buf = np.zeros(nb * per, np.float32)
+    buf[: len(values)] = values
+    blocks = np.concatenate([np.full((nb, 1), lm, np.float32), buf.reshape(nb, per)], axis=1)
+    return blocks.reshape(1, -1), nb
+
+
+def _rigorous_codes(Ms, j, f):
+    out = []
+    for M in Ms:
+        n = X.nearest_binary_radix(int(M), j, f.E, f.C)
+        out.append(0 if n is None else n + f.B)
+    return np.array(out)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_nearest_level_exhaustive_octave(name):
+    """Every fp32 significand of an interior octave: oracle == rigorous decision.
+
+    The rigorous decision brackets each midpoint (2^(c/K) + 2^((c+1)/K)) / 2 with
+    integer K-th roots.  Decisions only depend on the significand within an
+    octave (the rule is the same in every octave), so this covers every
+    interior element exactly.
+    """
+    f = oracle.get_format(name)
+    j = 0
+    Ms = np.arange(1 << 23, 1 << 24, dtype=np.int64)
+    vals = np.ldexp(Ms.astype(np.float64), j - 23).astype(np.float32)
+    x, nb = _blocks_with_scale0(vals, f)
+    codes, scales = oracle.quantize(x, f)
+    assert np.all(scales == 0)
+    got = codes.reshape(nb, 32)[:, 1:].reshape(-1)[: len(Ms)].astype(np.int64)
+    # rigorous thresholds: the decision changes only at K integer thresholds
+    K = f.K
+    thr = []
+    for c in range(K):
+        lo, hi = (1 << 23), (1 << 24) - 1
+        # find the largest M that is NOT above threshold c (binary search on the rigorous rule)
+        def above(M):
+            n = X.nearest_binary_radix(M, j, f.E, f.C)
+            return n is not None and n - K * j > c
+        while lo < hi:
+            mid = (lo + hi + 1) // 2
+            if above(mid):
+                hi = mid - 1
+            else:
+                lo = mid
+        thr.append(lo)
+    expect_c = np.zeros(len(Ms), np.int64)
+    for t in thr:
+        expect_c += (Ms > t)
+    expect = K * j + expect_c + f.B
+    assert np.array_equal(got, expect)
+    # spot-check the rigorous rule itself on the neighbours of each threshold
+    for t in thr:
+        for M in (t - 1, t, t + 1, t + 2):
+            if (1 << 23) <= M < (1 << 24):
+                assert _rigorous_codes([M], j, f)[0] == expect[M - (1 << 23)]
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_nearest_level_edges(name):
+    """Octaves around the zero threshold, the smallest level and the top level."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(1)
+    e_min = math.floor(f.n_min / f.K)
+    e_max = math.floor(f.n_max / f.K)
+    for j in (e_min - 3, e_min - 2, e_min - 1, e_min, e_min + 1, e_max):
+        Ms = np.unique(np.concatenate([
+            rng.integers(1 << 23, 1 << 24, 20000),
+            np.array([1 << 23, (1 << 24) - 1]),
+        ]))
+        vals = np.ldexp(Ms.astype(np.float64), j - 23).astype(np.float32)
+        # values above fl32(L_max) would raise the block scale; they are not in scope here
+        lm = float(np.float32(oracle.level_value_f64(f, f.n_max)))
+        keep = vals.astype(np.float64) <= lm
+        Ms, vals = Ms[keep], vals[keep]
+        x, nb = _blocks_with_scale0(vals, f)
+        codes, scales = oracle.quantize(x, f)
+        assert np.all(scales == 0)
+        got = codes.reshape(nb, 32)[:, 1:].reshape(-1)[: len(Ms)].astype(np.int64)
+        exp = _rigorous_codes(Ms, j, f)
+        assert np.array_equal(got, exp), j
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_scale_rule_and_error_bound(name):
+    """Ceil-absmax: the block max lands in (fl32(L_max)/2, fl32(L_max)] after scaling,
+    and interior elements obey |x - x_hat| <= |x| (2^(1/K) - 1) / (2^(1/K) + 1)."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(2)
+    x = (rng.standard_normal((64, 1024)) * np.exp2(rng.uniform(-30, 30, (64, 1)))).astype(np.float32)
+    codes, scales = oracle.quantize(x, f)
+    lm = float(np.float32(oracle.level_value_f64(f, f.n_max)))
+    amax = np.abs(x.astype(np.float64)).reshape(64, 32, 32).max(-1)
+    y = np.ldexp(amax, -scales.astype(np.int64))
+    assert np.all(y <= lm) and np.all(y > lm / 2)
+    deq = oracle.dequantize(codes, scales, f).astype(np.float64)
+    xd = x.astype(np.float64)
+    bound = (2 ** (1 / f.K) - 1) / (2 ** (1 / f.K) + 1)
+    a = np.repeat(scales.astype(np.int64), 32, axis=1)
+    interior = (np.abs(xd) >= np.ldexp(oracle.level_value_f64(f, f.n_min), a))
+    rel = np.abs(xd - deq)[interior] / np.abs(xd)[interior]
+    assert rel.max() <= bound * (1 + 1e-6)
+    # saturation never fires under this scale rule: no element beyond the top level
+    nz, s, n = oracle.code_fields(codes, f)
+    assert np.all(n[nz] <= f.n_max)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+@pytest.mark.parametrize("a", [-100, -20, 0, 7, 100])
+def test_round_trip_all_codes(name, a):
+    """quantize(dequantize(c)) == c for every canonical code (blocks holding the top code)."""
+    f = oracle.get_format(name)
+    EC = f.E + f.C
+    mags = np.arange(1, 2 ** EC)
+    allc = np.concatenate([mags, mags | (1 << EC)]).astype(np.uint8)
+    top = np.uint8(2 ** EC - 1)
+    per = 31
+    nb = -(-len(allc) // per)
+    body = np.zeros(nb * per, np.uint8)
+    body[: len(allc)] = allc
+    codes = np.concatenate([np.full((nb, 1), top, np.uint8), body.reshape(nb, per)], axis=1).reshape(1, -1)
+    scales = np.full((1, nb), a, np.int8)
+    deq = oracle.dequantize(codes, scales, f)
+    c2, s2 = oracle.quantize(deq, f)
+    assert np.array_equal(s2, scales)
+    assert np.array_equal(c2, codes)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_dequantize_rigorous_all_codes_all_scales(name):
+    """fp32 reconstruction == rigorously rounded 2^(a + n/K), every code and scale."""
+    f = oracle.get_format(name)
+    EC = f.E + f.C
+    mags = np.arange(1, 2 ** EC)
+    scales = np.arange(-127, 128)
+    codes = np.tile(mags, (len(scales), 1)).astype(np.uint8)
+    codes = np.repeat(codes, 1, axis=1)
+    # one block per (scale, 32 codes): lay codes out so each block has one scale
+    nmag = len(mags)
+    pad = (-nmag) % 32
+    cpad = np.concatenate([codes, np.zeros((len(scales), pad), np.uint8)], axis=1)
+    sc = np.repeat(scales[:, None], cpad.shape[1] // 32, axis=1).astype(np.int8)
+    got = oracle.dequantize(cpad, sc, f)[:, :nmag]
+    for ia, a in enumerate(scales):
+        for im, m in enumerate(mags):
+            exp = X.rn_f32_pow2(int(a), int(m) - f.B, f.K)
+            g = float(got[ia, im])
+            assert X.f32_bits(g) == X.f32_bits(exp), (a, m, g, exp)
+    neg = oracle.dequantize(cpad | np.uint8(1 << EC), sc, f)[:, :nmag]
+    assert np.array_equal(neg, -got)
+    zero = oracle.dequantize(np.zeros_like(cpad), sc, f)
+    assert np.all(zero == 0) and not np.any(np.signbit(zero))
+
+
+def test_nonfinite_blocks_poison():
+    f = oracle.get_format("E4C3")
+    x = np.ones((2, 64), np.float32)
+    x[0, 3] = np.nan
+    x[1, 40] = -np.inf
+    codes, scales = oracle.quantize(x, f)
+    assert scales[0, 0] == oracle.POISON_SCALE and scales[1, 1] == oracle.POISON_SCALE
+    assert scales[0, 1] != oracle.POISON_SCALE and scales[1, 0] != oracle.POISON_SCALE
+    assert np.all(codes[0, :32] == 0) and np.all(codes[1, 32:] == 0)
+    d = oracle.dequantize(codes, scales, f)
+    assert np.all(np.isnan(d[0, :32])) and np.all(np.isnan(d[1, 32:]))
+
+
+def test_zero_block_and_sign_of_zero():
+    f = oracle.get_format("E5C2")
+    x = np.zeros((1, 64), np.float32)
+    x[0, 32:] = -0.0
+    codes, scales = oracle.quantize(x, f)
+    assert np.all(codes == 0) and np.all(scales == 0)
+
+
+def test_pack7_layout():
+    """7-bit packing: code i at bits [7i, 7i+7) of a 224-bit little-endian string."""
+    rng = np.random.default_rng(3)
+    codes = rng.integers(0, 128, (5, 96)).astype(np.uint8)
+    packed = oracle.pack7(codes)
+    assert packed.shape == (5, 3, 28)
+    for r in range(5):
+        for b in range(3):
+            big = sum(int(c) << (7 * i) for i, c in enumerate(codes[r, 32 * b: 32 * b + 32]))
+            assert bytes(packed[r, b]) == big.to_bytes(28, "little")
+    assert np.array_equal(oracle.unpack7(packed, 96), codes)
+
+
+# ------------------------------------------------------------------ GEMM
+
+def _deq_exact64(codes, scales, f):
+    nz, s, n = oracle.code_fields(codes, f)
+    a = np.repeat(scales.astype(np.int64), 32, axis=1)
+    v = np.ldexp(oracle.level_value_f64(f, np.where(nz, n, 0)), a)
+    return np.where(nz, np.where(s == 1, -v, v), 0.0)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_gemm_matches_float64_matmul(name):
+    """Phase-binned exact GEMM vs numpy float64 matmul of reconstructed values."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(4)
+    A = (rng.standard_normal((48, 256)) * np.exp2(rng.uniform(-8, 8, (48, 1)))).astype(np.float32)
+    B = (rng.standard_normal((40, 256)) * 0.02).astype(np.float32)
+    ca, sa = oracle.quantize(A, f)
+    cb, sb = oracle.quantize(B, f)
+    C = oracle.gemm_exact(ca, sa, cb, sb, f)
+    ref = _deq_exact64(ca, sa, f) @ _deq_exact64(cb, sb, f).T
+    absmm = np.abs(_deq_exact64(ca, sa, f)) @ np.abs(_deq_exact64(cb, sb, f)).T
+    assert np.all(np.abs(C - ref) <= 1e-13 * absmm)
+    # transposed operands would not even have the right shape or values
+    assert C.shape == (48, 40)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_gemm_matches_python_mini_oracle(name):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(5)
+    A = rng.standard_normal((3, 64)).astype(np.float32)
+    B = rng.standard_normal((4, 64)).astype(np.float32)
+    ca, sa = oracle.quantize(A, f)
+    cb, sb = oracle.quantize(B, f)
+    C = oracle.gemm_exact(ca, sa, cb, sb, f)
+    P = oracle.gemm_exact_python(ca, sa, cb, sb, f)
+    assert np.allclose(C, P, rtol=1e-15, atol=0)
+
+
+def test_gemm_powers_of_two_exact():
+    """All curve indices zero: every product is +-2^t, so the dot is an exact rational."""
+    f = oracle.get_format("E5C2")
+    rng = np.random.default_rng(6)
+    M, N, K = 4, 5, 96
+    e_a = rng.integers(-15, 16, (M, K))   # n = 4e >= n_min = -63
+    e_b = rng.integers(-15, 16, (N, K))
+    ca = ((rng.integers(0, 2, (M, K)) << 7) | (e_a * f.K + f.B)).astype(np.uint8)
+    cb = ((rng.integers(0, 2, (N, K)) << 7) | (e_b * f.K + f.B)).astype(np.uint8)
+    sa = rng.integers(-100, 100, (M, K // 32)).astype(np.int8)
+    sb = rng.integers(-100, 100, (N, K // 32)).astype(np.int8)
+    C = oracle.gemm_exact(ca, sa, cb, sb, f)
+    for i in range(M):
+        for j in range(N):
+            tot = Fraction(0)
+            for k in range(K):
+                sgn = -1 if ((ca[i, k] >> 7) ^ (cb[j, k] >> 7)) & 1 else 1
+                ex = int(e_a[i, k] + e_b[j, k] + sa[i, k // 32] + sb[j, k // 32])
+                tot += sgn * Fraction(2) ** ex
+            assert C[i, j] == float(tot)
+
+
+@pytest.mark.parametrize("name", FMT_NAMES)
+def test_gemm_sign_identity_and_zero(name):
+    f = oracle.get_format(name)
+    EC = f.E + f.C
+    rng = np.random.default_rng(7)
+    A = rng.standard_normal((8, 64)).astype(np.float32)
+    ca, sa = oracle.quantize(A, f)
+    # identity-like B: row j has the level 1.0 (n = 0) at column j, zeros elsewhere
+    cb = np.zeros((64, 64), np.uint8)
+    cb[np.arange(64), np.arange(64)] = f.B          # m = B  <=> n = 0  <=> value 1 at scale 0
+    sb = np.zeros((64, 2), np.int8)
+    C = oracle.gemm_exact(ca, sa, cb, sb, f)
+    assert np.array_equal(C, _deq_exact64(ca, sa, f))
+    neg = np.where(ca != 0, ca ^ np.uint8(1 << EC), 0).astype(np.uint8)
+    Cn = oracle.gemm_exact(neg, sa, cb, sb, f)
+    assert np.array_equal(Cn, -C)
+    Cz = oracle.gemm_exact(np.zeros_like(ca), sa, cb, sb, f)
+    assert np.all(Cz == 0)
+
+
+def test_counter_width_bound():
+    """Sec. 3.2: |A[h][t]| <= D, and D fits a 1 + ceil(log2(D+1)) bit signed counter."""
+    f = oracle.get_format("E4C3")
+    for D in (32, 4096):
+        a = np.full(D, 0x55, np.uint8)
+        b = np.full(D, 0x41, np.uint8)
+        s = np.zeros(D // 32, np.int8)
+        ph, val, mc = oracle.phase_bins_one(a, s, b, s, f)
+        assert mc == D                       # all products land in one bin: the bound is tight
+        width = 1 + math.ceil(math.log2(D + 1))
+        assert -(2 ** (width - 1)) <= -D and D <= 2 ** (width - 1) - 1
+    assert [1 + math.ceil(math.log2(D + 1)) for D in (32, 4096, 11008, 14336)] == [7, 14, 15, 15]
+    # a random dot never exceeds the bound either
+    rng = np.random.default_rng(8)
+    A = rng.standard_normal((4, 4096)).astype(np.float32)
+    ca, sa = oracle.quantize(A, f)
+    _, mc = oracle.gemm_exact(ca, sa, ca, sa, f, return_max_count=True)
+    assert mc <= 4096
+
+
+def test_phase_sums_recombine():
+    """sum_h 2^(h/H) N_h reproduces the returned value; N_h are integers times 2^t."""
+    f = oracle.get_format("E3C3")
+    rng = np.random.default_rng(9)
+    x = rng.standard_normal((1, 256)).astype(np.float32)
+    w = rng.standard_normal((1, 256)).astype(np.float32)
+    ca, sa = oracle.quantize(x, f)
+    cb, sb = oracle.quantize(w, f)
+    ph, val, mc = oracle.phase_bins_one(ca, sa, cb, sb, f)
+    assert len(ph) == f.H
+    v2 = sum(2 ** (h / f.H) * ph[h] for h in range(f.H))
+    assert abs(v2 - val) <= 1e-12 * abs(val)
+    ref = (_deq_exact64(ca, sa, f) @ _deq_exact64(cb, sb, f).T)[0, 0]
+    assert abs(val - ref) <= 1e-12 * abs(ref)
