@@ -1,0 +1,235 @@
+"""Benchmark of the CurveFP hot path on one MI355X.
+
+One step = one pass of the whole path over one batch of the CurveFP7 E3C3
+inference workload (activations 2048 x 4096 bf16, Student-t(4) * 0.5 with 0.1 %
+outlier channels x20; weights 4096 x 4096 bf16 N(0, 0.02), both block 32):
+
+    quantize(activations) -> quantize(weights) -> CurveFP GEMM -> dequantize(activation codes)
+
+Prints one JSON line.  `value` is whole-step throughput in GEMM TFLOP/s
+(2 M N K per step over the measured step time, inputs resident in HBM).
+Per-kernel times come from HIP events recorded on the stream the library
+launches on.  The roofline object is for the GEMM kernel (the dominant one).
+A separate streaming quantize case (1 GiB bf16 source, larger than the 256 MB
+Infinity Cache) gives the HBM figure for the quantizer.  The CPU oracle is timed
+on a bounded row sample of the same workload as `cpu_baseline`.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "CurveFP GEMM TFLOP/s + quantize GB/s (1×MI355X, % roofline), oracle-exact"
+HBM_PEAK_GBS = 8000.0
+F16_DENSE_PEAK_TFLOPS = 2500.0   # MI355X dense fp16/bf16 MFMA
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--workload", default="inference")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-stream", action="store_true")
+    p.add_argument("--cpu-seconds", type=float, default=15.0)
+    return p.parse_args()
+
+
+def quantize_bytes_per_elem(fmt: str, dtype: str) -> float:
+    src = 2.0 if dtype == "bf16" else 4.0
+    code = 7.0 / 8.0 if fmt == "E3C3" else 1.0
+    return src + code + 1.0 / 32.0
+
+
+def dequantize_bytes_per_elem(fmt: str) -> float:
+    return (7.0 / 8.0 if fmt == "E3C3" else 1.0) + 1.0 / 32.0 + 4.0
+
+
+def cpu_baseline(w, seconds: float):
+    """The oracle, as it stands, on a row sample of the same step (quantize both
+    sampled operands, exact GEMM, dequantize); scaled to GEMM TFLOP/s."""
+    import numpy as np
+    import oracle
+
+    f = oracle.get_format(w.fmt)
+    A, B = w.operand("a"), w.operand("b")
+    A = A if w.a.axis == 1 else np.ascontiguousarray(A.T)
+    B = B if w.b.axis == 1 else np.ascontiguousarray(B.T)
+    nthreads = oracle.load_library().oracle_max_threads()
+
+    def run(ra, rb):
+        t0 = time.perf_counter()
+        ca, sa = oracle.quantize(np.ascontiguousarray(A[:ra]), f)
+        cb, sb = oracle.quantize(np.ascontiguousarray(B[:rb]), f)
+        oracle.gemm_exact(ca, sa, cb, sb, f)
+        oracle.dequantize(ca, sa, f)
+        return time.perf_counter() - t0
+
+    ra, rb = 16, 64
+    t = run(ra, rb)
+    scale = max(1.0, (seconds / max(t, 1e-3)) ** 0.5)
+    ra = int(min(w.M, max(16, ra * scale)))
+    rb = int(min(w.N, max(64, rb * scale)))
+    t = run(ra, rb)
+    flops = 2.0 * ra * rb * w.K
+    return {
+        "value": flops / t / 1e12,
+        "unit": "TFLOP/s",
+        "cores": nthreads,
+        "kind": "oracle",
+        "sample": f"{ra} activation rows x {rb} weight rows of {w.name} (K={w.K}): oracle quantize "
+                  f"of both samples, exact phase-binned GEMM, dequantize; {t:.1f} s wall on "
+                  f"{nthreads} threads; value = 2*{ra}*{rb}*{w.K} flop / wall",
+        "seconds": t,
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_10010_amd import curvefp as cf
+    from paper_2608_10010_amd import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = W.get(args.workload)
+    A = w.operand("a")
+    B = w.operand("b")
+    ta = torch.from_numpy(A).to(torch.bfloat16 if w.dtype == "bf16" else torch.float32).to(dev)
+    tb = torch.from_numpy(B).to(torch.bfloat16 if w.dtype == "bf16" else torch.float32).to(dev)
+    outer_a = w.M
+    ka = w.K
+    stream = torch.cuda.current_stream()
+    ca, sa = cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis)
+    cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
+    C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    D = torch.empty((outer_a, ka), dtype=torch.float32, device=dev)
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa)
+        if ev is not None:
+            ev[1].record(stream)
+        cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb)
+        if ev is not None:
+            ev[2].record(stream)
+        cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
+        if ev is not None:
+            ev[3].record(stream)
+        cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region: exactly `steps` steps, synchronized on both sides; HIP events are
+    # recorded on the stream the library launches on, around every kernel of every step
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+    names = ["quantize_a", "quantize_b", "gemm", "dequantize"]
+    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
+           for j, n in enumerate(names)}
+
+    flops = w.flops()
+    gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
+    qa_bytes = outer_a * ka * quantize_bytes_per_elem(w.fmt, w.dtype)
+    qb_bytes = w.N * w.K * quantize_bytes_per_elem(w.fmt, w.dtype)
+    dq_bytes = outer_a * ka * dequantize_bytes_per_elem(w.fmt)
+
+    result = {
+        "metric": METRIC,
+        "value": flops / (ms_per_step * 1e-3) / 1e12,
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": w.name,
+            "format": w.fmt,
+            "source_dtype": w.dtype,
+            "M": w.M, "N": w.N, "K": w.K, "block": 32,
+            "step": "quantize(act) + quantize(weight) + gemm + dequantize(act codes)",
+            "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
+            "parallelism": "single GPU",
+        },
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "gemm",
+            "achieved": gemm_tflops,
+            "peak": F16_DENSE_PEAK_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": gemm_tflops / F16_DENSE_PEAK_TFLOPS,
+            "traffic": None,
+            "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
+        },
+        "kernels_us": {n: per[n] * 1e3 for n in names},
+        "gemm_tflops": gemm_tflops,
+        "quantize_gbps": {
+            "act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
+            "weight": qb_bytes / (per["quantize_b"] * 1e-3) / 1e9,
+        },
+        "dequantize_gbps": dq_bytes / (per["dequantize"] * 1e-3) / 1e9,
+    }
+
+    if not args.no_stream:
+        # streaming quantize: 32768 x 16384 bf16 (1 GiB source) -> E4C3, larger than the MALL
+        g = torch.Generator(device=dev)
+        g.manual_seed(77)
+        xs = torch.randn((32768, 16384), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+        cs, ss = cf.curvefp_quantize(xs, "E4C3")
+        torch.cuda.synchronize()
+        reps = 10
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            cf.curvefp_quantize(xs, "E4C3", codes=cs, scales=ss)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        t_q = e0.elapsed_time(e1) / reps * 1e-3
+        nbytes = xs.numel() * quantize_bytes_per_elem("E4C3", "bf16")
+        gbs = nbytes / t_q / 1e9
+        result["quantize_stream"] = {
+            "shape": [32768, 16384], "format": "E4C3", "source_dtype": "bf16",
+            "us": t_q * 1e6, "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "bytes_per_elem": quantize_bytes_per_elem("E4C3", "bf16"),
+        }
+        del xs, cs, ss
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

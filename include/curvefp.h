@@ -1,0 +1,146 @@
+/*
+ * curvefp.h -- C ABI of libcurvefp: CurveFP block quantization, reconstruction
+ * and the CurveFP GEMM on AMD Instinct MI355X (gfx950).
+ *
+ * CurveFP (arXiv 2608.10010) stores a block of G values with one signed
+ * power-of-two scale exponent a_b and one (1+E+C)-bit code per element; a
+ * nonzero element is (-1)^s 2^{a_b} 2^{e + k/K}, K = 2^C (Sec. 3.1,
+ * Eq. curvefp-value).  The formats are those of Tab. curvefp-formats:
+ * CurveFP8 E4C3 (forward operands), CurveFP8 E5C2 (gradients) and CurveFP7
+ * E3C3 (compact inference), all with binary radix.
+ *
+ * Conventions shared by every entry point
+ *   - All data pointers are device pointers owned by the caller.  The library
+ *     never allocates, frees or keeps them.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
+ *     is asynchronous on that stream and never synchronizes it.  Constant
+ *     tables are uploaded on the first call on each device (or by
+ *     curvefp_init); that first call is synchronous.
+ *   - Argument errors are detected before any HIP call and returned as a
+ *     negative curvefp_status; nothing is launched then.  Launch failures
+ *     return CURVEFP_ERR_HIP.  Data-dependent conditions (non-finite inputs)
+ *     are encoded in the outputs, never in the status.
+ *   - block must be 32 (blocks of 32 consecutive elements along the
+ *     contraction axis); the blocked extent must be a multiple of 32.
+ *   - Code, output and (for blocks along rows) source pointers must be 16-byte
+ *     aligned, and leading dimensions (in elements) must keep every row 16-byte
+ *     aligned; the quantize-transpose source only needs element alignment.
+ *
+ * Element code layout (one byte per code for E4C3/E5C2, 7-bit packed for E3C3)
+ *   code = s << (E+C) | m,  m = n + 2^{E+C-1},  n = e*K + k in [-(2^{E+C-1}-1), 2^{E+C-1}-1],
+ *   m = 0 is the zero sentinel (the paper reserves magnitude index zero and drops
+ *   the smallest exponent/curve combination, Sec. 3.1; App. C.1 gives the same
+ *   rank layout for E4C3: sign in bit 7, rank in bits 6:0, q = m - 64).
+ *   E3C3 codes are packed LSB first: code i of a block of 32 occupies bits
+ *   [7i, 7i+7) of a 224-bit little-endian string, i.e. 28 bytes per block.
+ *
+ * Scales: int8 power-of-two exponents, one per block, row-major
+ *   [outer][k / 32]; -128 marks a block that held a NaN or an infinity.
+ */
+#ifndef CURVEFP_H
+#define CURVEFP_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CURVEFP_E4C3 = 0,   /* 8 bits, E=4, C=3, 127 levels, H=8 */
+    CURVEFP_E5C2 = 1,   /* 8 bits, E=5, C=2, 127 levels, H=4 */
+    CURVEFP_E3C3 = 2    /* 7 bits, E=3, C=3,  63 levels, H=8 */
+} curvefp_format;
+
+typedef enum {
+    CURVEFP_F32 = 0,
+    CURVEFP_BF16 = 1
+} curvefp_dtype;
+
+typedef enum {
+    CURVEFP_OK = 0,
+    CURVEFP_ERR_NULL = -1,     /* a required pointer is NULL */
+    CURVEFP_ERR_SHAPE = -2,    /* non-positive or inconsistent sizes, ld too small, blocked extent % 32 != 0 */
+    CURVEFP_ERR_FORMAT = -3,   /* unknown format or dtype */
+    CURVEFP_ERR_BLOCK = -4,    /* block != 32, or block_axis not 0/1 */
+    CURVEFP_ERR_ALIGN = -5,    /* pointer or row not 16-byte aligned */
+    CURVEFP_ERR_HIP = -6       /* a HIP call failed (launch, device query, table upload) */
+} curvefp_status;
+
+/* Format parameters from Tab. curvefp-formats: element bits, E, C and the phase
+ * count H = qK/gcd(p, qK) of Eq. phase-count (binary radix: H = K).  Any output
+ * pointer may be NULL.  Returns CURVEFP_OK or CURVEFP_ERR_FORMAT. */
+int curvefp_format_info(int format, int* bits, int* E, int* C, int* phases);
+
+/* Bytes of the code array for `outer` rows of `k` elements each
+ * (outer*k for E4C3/E5C2, outer*(k/32)*28 for E3C3); negative status on bad input. */
+int64_t curvefp_codes_bytes(int format, int64_t outer, int64_t k, int block);
+
+/* Number of int8 scales: outer * (k / block); negative status on bad input. */
+int64_t curvefp_scales_count(int64_t outer, int64_t k, int block);
+
+/* Upload the constant tables to the current device.  Optional: every entry
+ * point does it on its first call on a device.  Synchronous. */
+int curvefp_init(void);
+
+/*
+ * Block quantization Q(X) (Sec. 3.1).
+ *   src     [rows][ld_src] elements of `dtype` (fp32 or bf16), row-major.
+ *   block_axis = 1: blocks of 32 run along each row; codes are [rows][cols]
+ *                   (E3C3: [rows][cols/32][28] bytes), scales [rows][cols/32].
+ *   block_axis = 0: blocks run down the columns (quantize-transpose); codes are
+ *                   [cols][rows] (E3C3: [cols][rows/32][28]), scales [cols][rows/32].
+ * Scale (dynamic, ceil-absmax): a_b is the smallest integer with
+ *   max|x| <= 2^{a_b} * fl32(2^{n_max/K}), clamped to [-127, 127]; 0 for an
+ *   all-zero block; -128 (and all-zero codes) for a block holding NaN/Inf.
+ * Element: the magnitude nearest to |x| 2^{-a_b} in absolute error among zero
+ *   and the levels 2^{n/K}, saturating at the endpoints; the sign is kept,
+ *   except that every zero result is the code 0.
+ */
+int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                     int block_axis, int format, int block,
+                     void* codes, int8_t* scales, void* stream);
+
+/*
+ * Reconstruction x_hat = (-1)^s 2^{a_b} 2^{n/K} (Eq. curvefp-value), written as
+ * the nearest fp32 value (ties to even).  codes/scales as produced by
+ * curvefp_quantize with block_axis = 1 for an [outer][k] tensor;
+ * dst [outer][ld_dst] fp32.  Zero codes give +0.0; poisoned blocks give NaN.
+ */
+int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
+                       int64_t outer, int64_t k, int block,
+                       float* dst, int64_t ld_dst, void* stream);
+
+/*
+ * CurveFP GEMM: C[M][N] = deq(A)[M][K] . deq(B)[N][K]^T in fp32, the forward
+ * contract Q_A(X) Q_W(W)^T of Sec. 3.3 with both operands K-contiguous
+ * (A codes [M][K], B codes [N][K], scales [.][K/32], one format for both).
+ * c is [M][ldc] fp32, overwritten.
+ *
+ * Every nonzero product is, in the code domain, a sign xor, a curve-index sum
+ * with carry into the exponent, an exponent sum and a scale sum
+ * (Eq. curve-index-product); the dot product is the fixed-coefficient
+ * reduction sum_h 2^{h/H} N_h of its phase sums (Eq. binned-accumulation).
+ * The kernel evaluates that sum on the matrix cores: each code is expanded to
+ * an fp16 high/low pair (22 significant bits) carrying its block scale
+ * relative to the row's largest block scale, three f16 MFMA products
+ * (hi.hi + hi.lo + lo.hi) accumulate in fp32, and the epilogue applies the
+ * row and column scale offsets exactly.  Error: each product is represented
+ * to about 2^-21 relative; elements more than ~2^-29 below their row's largest
+ * element are flushed; accumulation is fp32.  Relative Frobenius error against
+ * the exact phase-binned sum is about 1e-7 on the benchmark workloads.
+ * Blocks with scale -128 contribute zero.
+ */
+int curvefp_gemm(const void* a_codes, const int8_t* a_scales,
+                 const void* b_codes, const int8_t* b_scales,
+                 int64_t M, int64_t N, int64_t K, int format, int block,
+                 float* c, int64_t ldc, void* stream);
+
+/* Static description of a status code. */
+const char* curvefp_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* CURVEFP_H */

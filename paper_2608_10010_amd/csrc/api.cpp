@@ -1,0 +1,139 @@
+// C ABI of libcurvefp: argument validation, per-device table upload, dispatch.
+// Validation runs before any HIP call, so every argument error is reported
+// without touching the device.
+#include <mutex>
+#include <vector>
+
+#include "../../include/curvefp.h"
+#include "curvefp_internal.hpp"
+
+using namespace curvefp;
+
+namespace {
+
+constexpr int kBits[3] = {8, 8, 7};
+constexpr int kE[3] = {4, 5, 3};
+constexpr int kC[3] = {3, 2, 3};
+
+bool fmt_ok(int f) { return f >= 0 && f <= 2; }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+std::mutex g_mu;
+std::vector<char> g_ready;   // per device: tables uploaded
+AllTables* g_tables = nullptr;
+bool g_tables_bad = false;
+
+int ensure_tables() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return CURVEFP_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_mu);
+    if ((int)g_ready.size() > dev && g_ready[dev]) return CURVEFP_OK;
+    if (g_tables_bad) return CURVEFP_ERR_HIP;
+    if (!g_tables) {
+        g_tables = new AllTables();
+        if (!build_tables(g_tables)) {
+            g_tables_bad = true;
+            return CURVEFP_ERR_HIP;
+        }
+    }
+    if (quantize_upload(*g_tables) != hipSuccess || dequantize_upload(*g_tables) != hipSuccess ||
+        gemm_upload(*g_tables) != hipSuccess)
+        return CURVEFP_ERR_HIP;
+    if (hipDeviceSynchronize() != hipSuccess) return CURVEFP_ERR_HIP;
+    if ((int)g_ready.size() <= dev) g_ready.resize(dev + 1, 0);
+    g_ready[dev] = 1;
+    return CURVEFP_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? CURVEFP_OK : CURVEFP_ERR_HIP; }
+
+}  // namespace
+
+#pragma GCC visibility push(default)
+extern "C" {
+
+int curvefp_format_info(int format, int* bits, int* E, int* C, int* phases) {
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (bits) *bits = kBits[format];
+    if (E) *E = kE[format];
+    if (C) *C = kC[format];
+    if (phases) *phases = 1 << kC[format];   // binary radix: H = qK / gcd(p, qK) = K
+    return CURVEFP_OK;
+}
+
+int64_t curvefp_codes_bytes(int format, int64_t outer, int64_t k, int block) {
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (block != 32) return CURVEFP_ERR_BLOCK;
+    if (outer < 0 || k < 0 || k % 32) return CURVEFP_ERR_SHAPE;
+    return format == CURVEFP_E3C3 ? outer * (k / 32) * 28 : outer * k;
+}
+
+int64_t curvefp_scales_count(int64_t outer, int64_t k, int block) {
+    if (block != 32) return CURVEFP_ERR_BLOCK;
+    if (outer < 0 || k < 0 || k % block) return CURVEFP_ERR_SHAPE;
+    return outer * (k / block);
+}
+
+int curvefp_init(void) { return ensure_tables(); }
+
+int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                     int block_axis, int format, int block, void* codes, int8_t* scales,
+                     void* stream) {
+    if (!src || !codes || !scales) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
+    if (block != 32 || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || cols <= 0 || ld_src < cols) return CURVEFP_ERR_SHAPE;
+    if ((block_axis == 1 ? cols : rows) % 32) return CURVEFP_ERR_SHAPE;
+    const int esz = dtype == CURVEFP_F32 ? 4 : 2;
+    // blocks along rows are read with 16-byte vector loads; the transpose path reads elements
+    if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_quantize(src, dtype, rows, cols, ld_src, block_axis, format, codes, scales,
+                                      reinterpret_cast<hipStream_t>(stream)));
+}
+
+int curvefp_dequantize(const void* codes, const int8_t* scales, int format, int64_t outer, int64_t k,
+                       int block, float* dst, int64_t ld_dst, void* stream) {
+    if (!codes || !scales || !dst) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (block != 32) return CURVEFP_ERR_BLOCK;
+    if (outer <= 0 || k <= 0 || k % 32 || ld_dst < k) return CURVEFP_ERR_SHAPE;
+    if (!aligned16(codes) || !aligned16(dst) || (ld_dst * 4) % 16) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_dequantize(codes, scales, format, outer, k, dst, ld_dst,
+                                        reinterpret_cast<hipStream_t>(stream)));
+}
+
+int curvefp_gemm(const void* a_codes, const int8_t* a_scales, const void* b_codes, const int8_t* b_scales,
+                 int64_t M, int64_t N, int64_t K, int format, int block, float* c, int64_t ldc,
+                 void* stream) {
+    if (!a_codes || !a_scales || !b_codes || !b_scales || !c) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (block != 32) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_gemm(a_codes, a_scales, b_codes, b_scales, M, N, K, format, c, ldc,
+                                  reinterpret_cast<hipStream_t>(stream)));
+}
+
+const char* curvefp_status_string(int status) {
+    switch (status) {
+        case CURVEFP_OK: return "ok";
+        case CURVEFP_ERR_NULL: return "null pointer argument";
+        case CURVEFP_ERR_SHAPE: return "invalid shape, leading dimension, or blocked extent not a multiple of 32";
+        case CURVEFP_ERR_FORMAT: return "unknown format or dtype";
+        case CURVEFP_ERR_BLOCK: return "unsupported block size or block axis";
+        case CURVEFP_ERR_ALIGN: return "pointer or row not 16-byte aligned";
+        case CURVEFP_ERR_HIP: return "HIP error (launch, device query or table upload)";
+        default: return "unknown status";
+    }
+}
+
+}  // extern "C"
+#pragma GCC visibility pop

@@ -1,0 +1,134 @@
+// CurveFP reconstruction x_hat = (-1)^s 2^{a_b} 2^{e + k/K} (Eq. curvefp-value),
+// written as the nearest fp32 value.
+//
+// In the normal range the result is exact bit assembly: the fp32 exponent is
+// e + a_b and the mantissa is that of fl32(2^{k/K}) (scaling by a power of two
+// commutes with rounding there).  Below 2^-126 the 62-bit significand of
+// 2^{k/K} is rounded once at the subnormal position.  HBM-bound: one byte (or 7
+// bits) and 1/32 scale byte read, four bytes written per element.
+#include "curvefp_internal.hpp"
+
+#include <cstring>
+
+namespace curvefp {
+
+__device__ uint32_t g_mant[3][8];
+__device__ uint64_t g_sig62[3][8];
+
+hipError_t dequantize_upload(const AllTables& t) {
+    uint32_t m[3][8];
+    uint64_t s[3][8];
+    for (int f = 0; f < 3; f++) {
+        memcpy(m[f], t.f[f].mant, sizeof(m[f]));
+        memcpy(s[f], t.f[f].sig62, sizeof(s[f]));
+    }
+    hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_mant), m, sizeof(m));
+    if (e != hipSuccess) return e;
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_sig62), s, sizeof(s));
+}
+
+namespace {
+
+template <class F>
+__device__ __forceinline__ uint32_t value_bits(uint32_t code, int a, const uint32_t* mant, const uint64_t* sig) {
+    const uint32_t m = code & F::MAG_MASK;
+    if (m == 0) return 0u;
+    const uint32_t s = (code >> F::EC) & 1u;
+    const int n = (int)m - F::B;
+    const int e = n >> F::C;                 // floor(n / K)
+    const int k = n & (F::K - 1);
+    const int ex = e + a;
+    uint32_t bits;
+    if (ex > 127) {
+        bits = 0x7F800000u;                  // beyond FLT_MAX: rounds to infinity
+    } else if (ex >= -126) {
+        bits = ((uint32_t)(ex + 127) << 23) | mant[k];
+    } else {
+        const int sh = -87 - ex;             // 62 - (ex + 149), in [40, 56]
+        const uint64_t v = sig[k];
+        uint64_t q = v >> sh;
+        const uint64_t rem = v & ((1ull << sh) - 1);
+        const uint64_t half = 1ull << (sh - 1);
+        q += (rem > half || (rem == half && (q & 1))) ? 1 : 0;
+        bits = (uint32_t)q;
+    }
+    return bits | (s << 31);
+}
+
+template <class F>
+__global__ __launch_bounds__(256) void dequantize_kernel(
+    const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, int64_t outer, int64_t k,
+    float* __restrict__ dst, int64_t ld, int fidx) {
+    __shared__ uint32_t mant[8];
+    __shared__ uint64_t sig[8];
+    if (threadIdx.x < 8) {
+        mant[threadIdx.x] = g_mant[fidx][threadIdx.x];
+        sig[threadIdx.x] = g_sig62[fidx][threadIdx.x];
+    }
+    __syncthreads();
+    const int64_t bpr = k / 32;
+    const int64_t nthreads = outer * bpr * 4;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nthreads; g += stride) {
+        const int64_t b = g >> 2;
+        const int part = (int)(g & 3);
+        const int64_t r = b / bpr;
+        const int64_t cb = b - r * bpr;
+        const int a = scales[b];
+        uint32_t c[8];
+        if (!F::PACKED7) {
+            const uint2 w = *reinterpret_cast<const uint2*>(codes + r * k + cb * 32 + part * 8);
+#pragma unroll
+            for (int i = 0; i < 4; i++) {
+                c[i] = (w.x >> (8 * i)) & 0xFFu;
+                c[4 + i] = (w.y >> (8 * i)) & 0xFFu;
+            }
+        } else {
+            // bytes [7 part, 7 part + 7) of this block's 28 bytes
+            const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + b * 28);
+            const int d0 = (7 * part) >> 2, off = 7 * part - 4 * d0;
+            const int d_end = (7 * part + 6) >> 2;
+            const uint64_t lo = (uint64_t)base[d0] | ((uint64_t)base[d0 + 1] << 32);
+            const uint64_t hi = (d_end >= d0 + 2) ? (uint64_t)base[d0 + 2] : 0ull;
+            const uint64_t chunk = off ? ((lo >> (8 * off)) | (hi << (64 - 8 * off))) : lo;
+#pragma unroll
+            for (int i = 0; i < 8; i++) c[i] = (uint32_t)(chunk >> (7 * i)) & 0x7Fu;
+        }
+        uint32_t o[8];
+        if (a == -128) {
+#pragma unroll
+            for (int i = 0; i < 8; i++) o[i] = 0x7FC00000u;   // poisoned block
+        } else {
+#pragma unroll
+            for (int i = 0; i < 8; i++) o[i] = value_bits<F>(c[i], a, mant, sig);
+        }
+        uint4* out = reinterpret_cast<uint4*>(dst + r * ld + cb * 32 + part * 8);
+        out[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        out[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    }
+}
+
+template <class F>
+hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, int64_t k, float* dst,
+                      int64_t ld, int fidx, hipStream_t s) {
+    const int threads = 256;
+    int64_t blocks = (outer * (k / 32) * 4 + threads - 1) / threads;
+    blocks = blocks < 8192 ? blocks : 8192;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL((dequantize_kernel<F>), dim3(blocks), dim3(threads), 0, s,
+                       reinterpret_cast<const uint8_t*>(codes), scales, outer, k, dst, ld, fidx);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format, int64_t outer,
+                             int64_t k, float* dst, int64_t ld_dst, hipStream_t s) {
+    switch (format) {
+        case 0: return launch_fmt<FmtE4C3>(codes, scales, outer, k, dst, ld_dst, 0, s);
+        case 1: return launch_fmt<FmtE5C2>(codes, scales, outer, k, dst, ld_dst, 1, s);
+        default: return launch_fmt<FmtE3C3>(codes, scales, outer, k, dst, ld_dst, 2, s);
+    }
+}
+
+}  // namespace curvefp

@@ -1,0 +1,153 @@
+"""Python binding of libcurvefp (argument marshalling only).
+
+The functions carry the names of the C ABI in ``include/curvefp.h``.  Tensors
+are torch tensors on a ROCm device; their data pointers and the current HIP
+stream are handed to the library, which runs every step of the computation in
+its own HIP kernels.  There is no fallback: if the library cannot be loaded the
+call raises.
+"""
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+from . import build as _build
+
+FORMATS = {"E4C3": 0, "E5C2": 1, "E3C3": 2}
+DTYPES = {torch.float32: 0, torch.bfloat16: 1}
+STATUS = {0: "ok", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_FORMAT", -4: "ERR_BLOCK",
+          -5: "ERR_ALIGN", -6: "ERR_HIP"}
+
+_lib = None
+
+
+class CurveFPError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what} failed: {STATUS.get(status, status)} "
+                         f"({lib().curvefp_status_string(status).decode()})")
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def lib() -> ctypes.CDLL:
+    """Load libcurvefp.so (building it first only if it has never been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB)
+        P, I, I64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+        IP = ctypes.POINTER(ctypes.c_int)
+        L.curvefp_format_info.argtypes = [I, IP, IP, IP, IP]
+        L.curvefp_format_info.restype = I
+        L.curvefp_codes_bytes.argtypes = [I, I64, I64, I]
+        L.curvefp_codes_bytes.restype = I64
+        L.curvefp_scales_count.argtypes = [I64, I64, I]
+        L.curvefp_scales_count.restype = I64
+        L.curvefp_init.argtypes = []
+        L.curvefp_init.restype = I
+        L.curvefp_quantize.argtypes = [P, I, I64, I64, I64, I, I, I, P, P, P]
+        L.curvefp_quantize.restype = I
+        L.curvefp_dequantize.argtypes = [P, P, I, I64, I64, I, P, I64, P]
+        L.curvefp_dequantize.restype = I
+        L.curvefp_gemm.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
+        L.curvefp_gemm.restype = I
+        L.curvefp_status_string.argtypes = [I]
+        L.curvefp_status_string.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+def _fmt(fmt) -> int:
+    return FORMATS[fmt] if isinstance(fmt, str) else int(fmt)
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(st: int, what: str):
+    if st != 0:
+        raise CurveFPError(st, what)
+
+
+def curvefp_format_info(fmt) -> Tuple[int, int, int, int]:
+    b, e, c, h = (ctypes.c_int() for _ in range(4))
+    _check(lib().curvefp_format_info(_fmt(fmt), ctypes.byref(b), ctypes.byref(e), ctypes.byref(c),
+                                     ctypes.byref(h)), "curvefp_format_info")
+    return b.value, e.value, c.value, h.value
+
+
+def curvefp_codes_bytes(fmt, outer: int, k: int, block: int = 32) -> int:
+    n = lib().curvefp_codes_bytes(_fmt(fmt), outer, k, block)
+    if n < 0:
+        raise CurveFPError(int(n), "curvefp_codes_bytes")
+    return n
+
+
+def curvefp_scales_count(outer: int, k: int, block: int = 32) -> int:
+    n = lib().curvefp_scales_count(outer, k, block)
+    if n < 0:
+        raise CurveFPError(int(n), "curvefp_scales_count")
+    return n
+
+
+def curvefp_init():
+    _check(lib().curvefp_init(), "curvefp_init")
+
+
+def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 32,
+                     codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
+                     stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Q(X) of a 2-D fp32/bf16 device tensor (row stride may exceed its width).
+
+    block_axis=1: codes [rows, cols] (E3C3: [rows, cols/32, 28] bytes), scales [rows, cols/32].
+    block_axis=0: quantize-transpose, codes [cols, rows], scales [cols, rows/32].
+    """
+    assert src.dim() == 2 and src.stride(1) == 1
+    rows, cols = src.shape
+    outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
+    f = _fmt(fmt)
+    if codes is None:
+        nbytes = curvefp_codes_bytes(f, outer, k, block)
+        shape = (outer, k // 32, 28) if f == 2 else (outer, k)
+        codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
+        assert codes.numel() == nbytes
+    if scales is None:
+        scales = torch.empty((outer, k // block), dtype=torch.int8, device=src.device)
+    st = lib().curvefp_quantize(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0),
+                                block_axis, f, block, codes.data_ptr(), scales.data_ptr(),
+                                _stream(stream))
+    _check(st, "curvefp_quantize")
+    return codes, scales
+
+
+def curvefp_dequantize(codes: torch.Tensor, scales: torch.Tensor, fmt, outer: int, k: int,
+                       block: int = 32, dst: Optional[torch.Tensor] = None,
+                       stream=None) -> torch.Tensor:
+    if dst is None:
+        dst = torch.empty((outer, k), dtype=torch.float32, device=codes.device)
+    st = lib().curvefp_dequantize(codes.data_ptr(), scales.data_ptr(), _fmt(fmt), outer, k, block,
+                                  dst.data_ptr(), dst.stride(0), _stream(stream))
+    _check(st, "curvefp_dequantize")
+    return dst
+
+
+def curvefp_gemm(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.Tensor,
+                 b_scales: torch.Tensor, M: int, N: int, K: int, fmt, block: int = 32,
+                 c: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T in fp32."""
+    if c is None:
+        c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    st = lib().curvefp_gemm(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
+                            b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
+                            _stream(stream))
+    _check(st, "curvefp_gemm")
+    return c

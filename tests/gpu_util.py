@@ -1,0 +1,94 @@
+"""Helpers for the GPU parity tests: device transfer and oracle-side references.
+
+Oracle inputs always come from the seeded generators, never from the HIP path.
+"""
+
+import sys
+
+import numpy as np
+import torch
+
+import oracle
+from paper_2608_10010_amd import curvefp as cf
+
+DEV = "cuda:0"
+FMTS = ("E4C3", "E5C2", "E3C3")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def to_dev(x: np.ndarray, dtype: str) -> torch.Tensor:
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    if dtype == "bf16":
+        t = t.to(torch.bfloat16)       # exact: the generator already rounded to bf16
+    return t.to(DEV)
+
+
+def oracle_quantize(x: np.ndarray, fmt: str, axis: int):
+    f = oracle.get_format(fmt)
+    if axis == 1:
+        return oracle.quantize(x, f)
+    return oracle.quantize_axis0(x, f)
+
+
+def layout_codes(codes: np.ndarray, fmt: str) -> np.ndarray:
+    """Oracle codes (one per byte) in the library's storage layout."""
+    return oracle.pack7(codes) if fmt == "E3C3" else codes
+
+
+def unpack_dev_codes(codes: torch.Tensor, fmt: str, k: int) -> np.ndarray:
+    c = codes.cpu().numpy()
+    if fmt == "E3C3":
+        return oracle.unpack7(c.reshape(c.shape[0], -1), k)
+    return c
+
+
+def exact_values(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.ndarray:
+    """float64 reconstructed values 2^{a + n/K} (the oracle's level function)."""
+    f = oracle.get_format(fmt)
+    nz, s, n = oracle.code_fields(codes, f)
+    a = np.repeat(scales.astype(np.int64), 32, axis=1)
+    a = np.where(a == oracle.POISON_SCALE, 0, a)
+    v = np.ldexp(oracle.level_value_f64(f, np.where(nz, n, 0)), a)
+    return np.where(nz, np.where(s == 1, -v, v), 0.0)
+
+
+def row_tops(codes, scales, fmt):
+    """2^{alpha + e_max + 1}: the top of the range a row's block scales allow."""
+    f = oracle.get_format(fmt)
+    e_max = 2 ** (f.E - 1) - 1
+    sc = scales.astype(np.int64)
+    alpha = np.max(np.where(sc == oracle.POISON_SCALE, -127, sc), axis=1)
+    return np.ldexp(1.0, alpha + e_max + 1)
+
+
+def gemm_tolerance(ca, sa, cb, sb, fmt):
+    """Element-wise bound for the MFMA GEMM against the exact sum.
+
+    * 1e-5 sum_k |a_ik b_jk| covers the 22-bit fp16 high/low operand splits
+      (about 3 * 2^-22 per product) and fp32 accumulation;
+    * 2^-38 (top_i ||b_j||_1 + top_j ||a_i||_1) covers elements that fall below
+      fp16's normal range when expressed relative to the top of their row's
+      scale range top = 2^{alpha + e_max + 1} (absolute error <= 2^-40 top);
+    * 2^-148 covers an exact result that underflows fp32.
+    """
+    va, vb = np.abs(exact_values(ca, sa, fmt)), np.abs(exact_values(cb, sb, fmt))
+    S = va @ vb.T
+    ta, tb = row_tops(ca, sa, fmt), row_tops(cb, sb, fmt)
+    flush = ta[:, None] * vb.sum(1)[None, :] + va.sum(1)[:, None] * tb[None, :]
+    return 1e-5 * S + 2.0 ** -38 * flush + 2.0 ** -148
+
+
+def check_gemm(C_dev: np.ndarray, V: np.ndarray, tol: np.ndarray, what: str):
+    err = np.abs(C_dev.astype(np.float64) - V)
+    bad = err > tol
+    assert not bad.any(), f"{what}: {bad.sum()} elements beyond bound; worst {np.max(err - tol)}"
+    nv = np.linalg.norm(V)
+    if nv > 0:
+        rel = np.linalg.norm(C_dev.astype(np.float64) - V) / nv
+        assert rel <= 1e-5, f"{what}: relative Frobenius error {rel}"
+        return rel
+    return 0.0

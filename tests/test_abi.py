@@ -1,0 +1,126 @@
+"""CPU-only checks of the C ABI: the library loads, exports every symbol the
+header declares, reports sizes and format parameters, and rejects bad
+arguments before touching the device (so no GPU is needed here)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2608_10010_amd import build as B
+from paper_2608_10010_amd import curvefp as cf
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "curvefp.h")
+
+OK, ENULL, ESHAPE, EFMT, EBLOCK, EALIGN, EHIP = 0, -1, -2, -3, -4, -5, -6
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(curvefp_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB):
+        B.build()
+    return cf.lib()
+
+
+def test_exports_every_declared_symbol(L):
+    names = declared_functions()
+    assert len(names) == 8
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
+    for n in names:
+        assert n in exported, n
+        assert hasattr(L, n)
+    # nothing but the C ABI is exported under the library's prefix
+    assert exported == set(names)
+
+
+def test_format_info(L):
+    # Tab. curvefp-formats
+    assert cf.curvefp_format_info("E4C3") == (8, 4, 3, 8)
+    assert cf.curvefp_format_info("E5C2") == (8, 5, 2, 4)
+    assert cf.curvefp_format_info("E3C3") == (7, 3, 3, 8)
+    assert L.curvefp_format_info(3, None, None, None, None) == EFMT
+    assert L.curvefp_format_info(-1, None, None, None, None) == EFMT
+
+
+def test_sizes(L):
+    assert cf.curvefp_codes_bytes("E4C3", 10, 64) == 640
+    assert cf.curvefp_codes_bytes("E5C2", 3, 32) == 96
+    assert cf.curvefp_codes_bytes("E3C3", 10, 64) == 10 * 2 * 28
+    assert cf.curvefp_scales_count(10, 64) == 20
+    assert L.curvefp_codes_bytes(0, 10, 33, 32) == ESHAPE
+    assert L.curvefp_codes_bytes(0, 10, 64, 16) == EBLOCK
+    assert L.curvefp_codes_bytes(5, 10, 64, 32) == EFMT
+    assert L.curvefp_scales_count(10, 48, 32) == ESHAPE
+    assert L.curvefp_scales_count(10, 64, 64) == EBLOCK
+
+
+def test_status_strings(L):
+    for st in (OK, ENULL, ESHAPE, EFMT, EBLOCK, EALIGN, EHIP, 99):
+        s = L.curvefp_status_string(st)
+        assert isinstance(s, bytes) and len(s) > 0
+
+
+FAKE = 1 << 20          # 16-byte aligned, never dereferenced: validation fails first
+MIS = FAKE + 8          # 8-byte aligned only
+
+
+def test_quantize_validation(L):
+    q = L.curvefp_quantize
+    assert q(None, 0, 4, 32, 32, 1, 0, 32, FAKE, FAKE, None) == ENULL
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 32, None, FAKE, None) == ENULL
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 32, FAKE, None, None) == ENULL
+    assert q(FAKE, 2, 4, 32, 32, 1, 0, 32, FAKE, FAKE, None) == EFMT       # dtype
+    assert q(FAKE, 0, 4, 32, 32, 1, 7, 32, FAKE, FAKE, None) == EFMT       # format
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 64, FAKE, FAKE, None) == EBLOCK     # block
+    assert q(FAKE, 0, 4, 32, 32, 2, 0, 32, FAKE, FAKE, None) == EBLOCK     # axis
+    assert q(FAKE, 0, 0, 32, 32, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # rows
+    assert q(FAKE, 0, 4, 40, 40, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # cols % 32
+    assert q(FAKE, 0, 40, 32, 32, 0, 0, 32, FAKE, FAKE, None) == ESHAPE    # rows % 32 on axis 0
+    assert q(FAKE, 0, 4, 32, 16, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # ld < cols
+    assert q(MIS, 0, 4, 32, 32, 1, 0, 32, FAKE, FAKE, None) == EALIGN
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 32, MIS, FAKE, None) == EALIGN
+    assert q(FAKE, 1, 4, 32, 36, 1, 0, 32, FAKE, FAKE, None) == EALIGN     # bf16 row not 16 B
+    assert q(FAKE + 2, 0, 32, 3, 3, 0, 0, 32, FAKE, FAKE, None) == EALIGN  # f32 element misaligned
+
+
+def test_dequantize_validation(L):
+    d = L.curvefp_dequantize
+    assert d(None, FAKE, 0, 4, 32, 32, FAKE, 32, None) == ENULL
+    assert d(FAKE, None, 0, 4, 32, 32, FAKE, 32, None) == ENULL
+    assert d(FAKE, FAKE, 0, 4, 32, 32, None, 32, None) == ENULL
+    assert d(FAKE, FAKE, 3, 4, 32, 32, FAKE, 32, None) == EFMT
+    assert d(FAKE, FAKE, 0, 4, 32, 16, FAKE, 32, None) == EBLOCK
+    assert d(FAKE, FAKE, 0, 4, 48, 32, FAKE, 48, None) == ESHAPE
+    assert d(FAKE, FAKE, 0, 4, 32, 32, FAKE, 16, None) == ESHAPE
+    assert d(FAKE, FAKE, 0, -1, 32, 32, FAKE, 32, None) == ESHAPE
+    assert d(FAKE, FAKE, 0, 4, 32, 32, MIS, 32, None) == EALIGN
+    assert d(FAKE, FAKE, 0, 4, 32, 32, FAKE, 33, None) == EALIGN
+
+
+def test_gemm_validation(L):
+    g = L.curvefp_gemm
+    args = [FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 32, FAKE, 64, None]
+    for i in (0, 1, 2, 3, 9):
+        a = list(args)
+        a[i] = None
+        assert g(*a) == ENULL, i
+    bad = list(args); bad[7] = 9
+    assert g(*bad) == EFMT
+    bad = list(args); bad[8] = 16
+    assert g(*bad) == EBLOCK
+    for i, v in ((4, 0), (5, -3), (6, 0), (6, 48), (10, 32)):
+        bad = list(args); bad[i] = v
+        assert g(*bad) == ESHAPE, (i, v)
+    for i in (0, 2, 9):
+        bad = list(args); bad[i] = MIS
+        assert g(*bad) == EALIGN, i

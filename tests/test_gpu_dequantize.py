@@ -1,0 +1,84 @@
+"""GPU parity: curvefp_dequantize is bit-exact against the oracle's nearest-fp32 reconstruction."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_10010_amd import curvefp as cf
+from paper_2608_10010_amd import workloads as W
+from tests.gpu_util import DEV, FMTS, layout_codes, oracle_quantize, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def dequant_compare(codes_u: np.ndarray, scales: np.ndarray, fmt: str, what: str):
+    outer, k = codes_u.shape
+    say(f"[dequantize] {what} fmt={fmt} shape={codes_u.shape}")
+    c = torch.from_numpy(np.ascontiguousarray(layout_codes(codes_u, fmt))).to(DEV)
+    s = torch.from_numpy(np.ascontiguousarray(scales)).to(DEV)
+    out = cf.curvefp_dequantize(c, s, fmt, outer, k)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    with np.errstate(over="ignore"):
+        exp = oracle.dequantize(codes_u, scales, oracle.get_format(fmt))
+    nan_g, nan_e = np.isnan(got), np.isnan(exp)
+    assert np.array_equal(nan_g, nan_e), f"{what}: NaN positions differ"
+    diff = got.view(np.uint32)[~nan_e] != exp.view(np.uint32)[~nan_e]
+    assert not diff.any(), f"{what}: {diff.sum()} values differ"
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_all_codes_all_scales(fmt):
+    f = oracle.get_format(fmt)
+    EC = f.E + f.C
+    allc = np.arange(0, 2 ** (EC + 1), dtype=np.uint8)        # both signs, zero, the unused -0 code
+    reps = -(-len(allc) // 32) * 32
+    row = np.resize(allc, reps)
+    scales = np.arange(-127, 128, dtype=np.int64)
+    codes = np.tile(row, (len(scales), 1)).astype(np.uint8)
+    sc = np.repeat(scales[:, None], reps // 32, axis=1).astype(np.int8)
+    dequant_compare(codes, sc, fmt, "all_codes_all_scales")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_poisoned_blocks_are_nan(fmt):
+    rng = np.random.default_rng(13)
+    f = oracle.get_format(fmt)
+    codes = rng.integers(0, 2 ** (f.E + f.C + 1), (8, 128)).astype(np.uint8)
+    sc = rng.integers(-20, 20, (8, 4)).astype(np.int8)
+    sc[2, 1] = -128
+    sc[5, 3] = -128
+    dequant_compare(codes, sc, fmt, "poison")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_roundtrip_from_gpu_quantize(fmt, dtype):
+    rng = np.random.default_rng(14)
+    x = (rng.standard_normal((48, 320)) * np.exp2(rng.uniform(-60, 60, (48, 1)))).astype(np.float32)
+    if dtype == "bf16":
+        x = W.bf16_round(x)
+    say(f"[dequantize] roundtrip fmt={fmt} dtype={dtype}")
+    codes, scales = cf.curvefp_quantize(to_dev(x, dtype), fmt)
+    out = cf.curvefp_dequantize(codes, scales, fmt, 48, 320)
+    torch.cuda.synchronize()
+    oc, os_ = oracle_quantize(x, fmt, 1)
+    exp = oracle.dequantize(oc, os_, oracle.get_format(fmt))
+    assert np.array_equal(out.cpu().numpy().view(np.uint32), exp.view(np.uint32))
+
+
+def test_output_row_stride():
+    rng = np.random.default_rng(15)
+    f = oracle.get_format("E4C3")
+    codes = rng.integers(0, 256, (6, 64)).astype(np.uint8)
+    sc = rng.integers(-5, 5, (6, 2)).astype(np.int8)
+    dst = torch.full((6, 100), 3.0, device=DEV)
+    c = torch.from_numpy(codes).to(DEV)
+    s = torch.from_numpy(sc).to(DEV)
+    say("[dequantize] row stride 100")
+    cf.curvefp_dequantize(c, s, "E4C3", 6, 64, dst=dst[:, :64])
+    torch.cuda.synchronize()
+    got = dst.cpu().numpy()
+    assert np.array_equal(got[:, :64].view(np.uint32), oracle.dequantize(codes, sc, f).view(np.uint32))
+    assert np.all(got[:, 64:] == 3.0)

@@ -1,0 +1,113 @@
+"""GPU parity: curvefp_quantize codes and scales are bit-exact against the oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2608_10010_amd import curvefp as cf
+from paper_2608_10010_amd import workloads as W
+from tests.gpu_util import FMTS, layout_codes, oracle_quantize, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def run_and_compare(x: np.ndarray, fmt: str, dtype: str, axis: int, what: str, ld_pad: int = 0):
+    if dtype == "bf16":
+        x = W.bf16_round(x)
+    say(f"[quantize] {what} fmt={fmt} dtype={dtype} axis={axis} shape={x.shape}")
+    xs = x
+    if ld_pad:
+        xs = np.concatenate([x, np.full((x.shape[0], ld_pad), 7.0, np.float32)], axis=1)
+    t = to_dev(xs, dtype)
+    if ld_pad:
+        t = t[:, : x.shape[1]]
+    codes, scales = cf.curvefp_quantize(t, fmt, block_axis=axis)
+    torch.cuda.synchronize()
+    oc, os_ = oracle_quantize(x, fmt, axis)
+    got_c = codes.cpu().numpy()
+    exp_c = layout_codes(oc, fmt)
+    assert np.array_equal(scales.cpu().numpy(), os_), f"{what}: scales differ"
+    assert np.array_equal(got_c.reshape(exp_c.shape), exp_c), \
+        f"{what}: {np.sum(got_c.reshape(exp_c.shape) != exp_c)} code bytes differ"
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("axis", [1, 0])
+def test_random(fmt, dtype, axis):
+    rng = np.random.default_rng(11)
+    shape = (37, 352) if axis == 1 else (160, 45)
+    x = (rng.standard_normal(shape) * np.exp2(rng.uniform(-30, 30, (shape[0], 1)))).astype(np.float32)
+    run_and_compare(x, fmt, dtype, axis, "random")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("kind", W.EDGE_KINDS)
+def test_edges(fmt, dtype, kind):
+    x = W.edge_tensor(kind, (64, 256))
+    run_and_compare(x, fmt, dtype, 1, kind)
+    run_and_compare(np.ascontiguousarray(x.T), fmt, dtype, 0, kind + "_T")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_nonfinite_poison(fmt):
+    x = W.edge_tensor("nonfinite", (32, 512))
+    run_and_compare(x, fmt, "f32", 1, "nonfinite")
+    run_and_compare(x, fmt, "bf16", 1, "nonfinite")
+    run_and_compare(np.ascontiguousarray(x[:, :64].T.copy()), fmt, "f32", 0, "nonfinite_T")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_row_stride(fmt):
+    rng = np.random.default_rng(12)
+    x = rng.standard_normal((19, 96)).astype(np.float32)
+    run_and_compare(x, fmt, "f32", 1, "ld_padded", ld_pad=32)
+    run_and_compare(x, fmt, "bf16", 1, "ld_padded", ld_pad=64)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_single_block(fmt):
+    x = np.linspace(-3, 3, 32, dtype=np.float32).reshape(1, 32)
+    run_and_compare(x, fmt, "f32", 1, "one_block")
+    run_and_compare(x.T.copy(), fmt, "f32", 0, "one_block_T")
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+def test_all_fp32_significands_one_octave(fmt):
+    """Every fp32 significand of one octave, in blocks pinned to scale 0."""
+    import oracle
+    f = oracle.get_format(fmt)
+    lm = np.float32(oracle.level_value_f64(f, f.n_max))
+    Ms = np.arange(1 << 23, 1 << 24, dtype=np.int64)
+    vals = np.ldexp(Ms.astype(np.float64), -23).astype(np.float32)
+    nb = -(-len(vals) // 31)
+    nb = -(-nb // 32) * 32            # whole rows of 1024 elements
+    body = np.zeros(nb * 31, np.float32)
+    body[: len(vals)] = vals
+    x = np.concatenate([np.full((nb, 1), lm, np.float32), body.reshape(nb, 31)], axis=1).reshape(-1, 1024)
+    run_and_compare(x, fmt, "f32", 1, "octave_sweep")
+
+
+WL_SAMPLED = ["tiny", "inference", "fwd", "dgrad", "wgrad", "sweep_gateup_E4C3", "sweep_down_E3C3"]
+
+
+@pytest.mark.parametrize("name", WL_SAMPLED)
+def test_workload_full_size_sampled(name):
+    """Full-size operands of each workload in the launch shape the benchmark uses;
+    every 61st output row is checked against the oracle (quantization is row-local)."""
+    w = W.get(name)
+    for which in ("a", "b"):
+        op = w.a if which == "a" else w.b
+        x = w.operand(which)
+        say(f"[quantize] workload={name} operand={op.name} fmt={w.fmt} shape={x.shape} axis={op.axis}")
+        t = to_dev(x, w.dtype)
+        codes, scales = cf.curvefp_quantize(t, w.fmt, block_axis=op.axis)
+        torch.cuda.synchronize()
+        src_rows = x if op.axis == 1 else np.ascontiguousarray(x.T)
+        rows = np.arange(0, src_rows.shape[0], 61)
+        oc, os_ = oracle_quantize(np.ascontiguousarray(src_rows[rows]), w.fmt, 1)
+        gc = codes.cpu().numpy()[rows]
+        assert np.array_equal(scales.cpu().numpy()[rows], os_)
+        assert np.array_equal(gc.reshape(gc.shape[0], -1), layout_codes(oc, w.fmt).reshape(len(rows), -1))
+        del t, codes, scales
