@@ -42,10 +42,9 @@ using FmtE3C3 = Fmt<3, 3>;
 static_assert(FmtE4C3::OZ == -9 && FmtE5C2::OZ == -17 && FmtE3C3::OZ == -5, "zero-threshold octaves");
 static_assert(FmtE4C3::OHI == 7 && FmtE5C2::OHI == 15 && FmtE3C3::OHI == 3, "top octaves");
 
-// GEMM decode table: one row per scale offset D = alpha_row - a_block in [0, GEMM_DMAX];
-// offsets above GEMM_DMAX use the all-zero row GEMM_DMAX + 1.
-constexpr int GEMM_DMAX = 40;
-constexpr int GEMM_DROWS = GEMM_DMAX + 2;
+// GEMM expansion table: one (lo16 << 16) | hi16 fp16 pair per code byte (sign included),
+// for a block whose scale equals its row's largest; other blocks are scaled by 2^-D in fp16.
+constexpr int GEMM_DEC_ENTRIES = 256;
 
 constexpr int QLUT_MAX = FmtE5C2::QLUT_SIZE;   // largest of the three
 
@@ -57,7 +56,7 @@ struct FormatTables {
     uint32_t lmax_mant = 0;         // mantissa field of fl32(2^{(K-1)/K})
     uint32_t mant[8];               // mantissa field of fl32(2^{k/K}), k < K
     uint64_t sig62[8];              // floor(2^{k/K} * 2^62)
-    uint32_t dec[GEMM_DROWS * 128]; // (lo16 << 16) | hi16 fp16 pair for (D, magnitude rank)
+    uint32_t dec[GEMM_DEC_ENTRIES];  // (lo16 << 16) | hi16 fp16 pair per code byte
 };
 
 struct AllTables {

@@ -146,25 +146,26 @@ bool build_format(int E, int C, FormatTables* ft) {
         }
     }
     ft->lmax_mant = ft->mant[K - 1];
-    // GEMM decode pairs: value 2^{x} 2^{k/K}, x = e - D + bias
+    // GEMM expansion pairs: value (-1)^s 2^{e + bias} 2^{k/K}, hi = RN16(v), lo = RN16(v - hi)
     const int EMAX = (1 << (E - 1)) - 1;
     const int bias = 15 - EMAX;
-    const int nmag = 1 << (E + C);
+    const int EC = E + C;
     memset(ft->dec, 0, sizeof(ft->dec));
-    for (int D = 0; D <= GEMM_DMAX; D++) {
-        for (int m = 1; m < nmag; m++) {
-            int n = m - r.B;
-            int e = (n >= 0) ? n / K : -((-n + K - 1) / K);
-            int k = n - e * K;
-            long double v = ldexpl(pow2frac(k, K), e - D + bias);
-            uint16_t hb, lb;
-            if (!rn_fp16(v, &hb)) return false;
-            long double rest = v - fp16_value(hb);
-            uint16_t sgn = rest < 0 ? 0x8000 : 0;
-            if (!rn_fp16(fabsl(rest), &lb)) return false;
-            if (lb) lb |= sgn;
-            ft->dec[D * 128 + m] = ((uint32_t)lb << 16) | hb;
-        }
+    for (int code = 0; code < (1 << (EC + 1)); code++) {
+        const int m = code & ((1 << EC) - 1);
+        const int sgn = (code >> EC) & 1;
+        if (m == 0) continue;
+        int n = m - r.B;
+        int e = (n >= 0) ? n / K : -((-n + K - 1) / K);
+        int k = n - e * K;
+        long double v = ldexpl(pow2frac(k, K), e + bias);
+        uint16_t hb, lb;
+        if (!rn_fp16(v, &hb)) return false;
+        long double rest = v - fp16_value(hb);
+        if (!rn_fp16(fabsl(rest), &lb)) return false;
+        if (lb && rest < 0) lb |= 0x8000;
+        if (sgn) { hb ^= 0x8000; if (lb) lb ^= 0x8000; }
+        ft->dec[code] = ((uint32_t)lb << 16) | hb;
     }
     return true;
 }
