@@ -12,21 +12,26 @@
 //
 // Expansion: a 256-entry table (sign included) gives the pair for a block at
 // its row's largest scale; a block D = alpha_row - a_b binades lower is then
-// scaled by 2^-D with one packed fp16 multiply per pair (exact while the
-// result stays normal, correctly rounded below; D > 24 takes a second
-// multiply).  The table is replicated 16 times in LDS so the lanes of a wave
-// gather from different banks.
+// scaled by 2^-min(D, 24) with one packed fp16 multiply per pair (exact while
+// the result stays normal, correctly rounded below).  Blocks with D > 24 get a
+// second multiply in a separate pass before the step's barrier (rare: only
+// rows whose block scales spread over more than 24 binades).  The table is
+// replicated 16 times in LDS so the lanes of a wave gather from 16 banks.
 //
-// Tiling: BM x BN output tile (256 x 256 or 256 x 128) per 512-thread
-// workgroup, eight waves of WM x WN (MFMA 32x32x16 tiles), K step 32 = one
-// scale block.  Expansion work is split into tasks of 8 codes (one 16-byte
-// chunk of one row's hi and lo planes), BM+BN rows x 4 chunks spread evenly
-// over the 512 threads.  Expanded tiles are double-buffered in LDS; the codes
-// are fetched from HBM two steps ahead.  In every step the waves on a SIMD
-// run in opposite order -- one runs its MFMAs while the other expands the
-// next step -- and one barrier closes the step.  Tile rows are 64 bytes with
-// the four 16-byte chunks XOR-swizzled by ((row >> 1) ^ (row >> 3)) & 3, so
-// fragment reads and expansion writes spread over the banks.
+// Tiling: 256 x 256 output tile per 256-thread workgroup, four waves of
+// 128 x 128 (4 x 4 MFMA 32x32x16 tiles), K step 32 = one scale block.  The
+// expansion of step kb+1 (8 tasks of 8 codes per thread: one 16-byte chunk of
+// one row's hi and lo planes) is interleaved with the 96 MFMAs of step kb;
+// operand fragments are double-buffered in registers and the codes are
+// fetched from HBM two steps ahead, so the matrix pipe, the VALU, LDS and HBM
+// work at the same time.  Expanded tiles are double-buffered in LDS with one
+// barrier per step.  Tile rows are 64 bytes with the four 16-byte chunks
+// XOR-swizzled by ((row >> 1) ^ (row >> 3)) & 3, so fragment reads and
+// expansion writes spread over the banks.
+//
+// Small problems split K in two (grid.z = 2) so the grid covers the 256
+// compute units; the two partial sums land in C through fp32 atomic adds on
+// a zero-filled C, which is order-independent for two terms.
 #include "curvefp_internal.hpp"
 
 #include <cstring>
@@ -47,32 +52,24 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int BM = 256;
-constexpr int BK = 32;
-constexpr int NTHREADS = 512;
+constexpr int BM = 256, BN = 256, BK = 32;
+constexpr int NTHREADS = 256;
+constexpr int WM = 128, WN = 128, TM = 4, TN = 4;
 constexpr int LUT_COPIES = 16;
 constexpr int LUT_BYTES = GEMM_DEC_ENTRIES * LUT_COPIES * 4;
-constexpr int ROW_BYTES = BK * 2;          // one fp16 plane row: 32 halves
+constexpr int ROW_BYTES = BK * 2;                 // one fp16 plane row: 32 halves
+constexpr int PLANE = BM * ROW_BYTES;             // 16 KB: one hi or lo plane of A or B
+constexpr int STAGE = 4 * PLANE;                  // Ahi, Alo, Bhi, Blo
+constexpr int SMEM = LUT_BYTES + 2 * STAGE + (BM + BN) * 4;
+constexpr int TASKS = (BM + BN) * 4 / NTHREADS;   // 8 expansion tasks per thread per step
+constexpr int MFMA_PER_SUB = TM * TN * 3;         // 48
+static_assert(SMEM <= 160 * 1024, "LDS budget");
+static_assert(TASKS == 8, "task split");
 
-template <int BN>
-struct Tile {
-    static constexpr int WM = (BN == 256) ? 128 : 64;    // wave tile rows
-    static constexpr int WN = 64;                          // wave tile cols
-    static constexpr int WAVES_N = BN / WN;
-    static constexpr int TM = WM / 32, TN = WN / 32;       // MFMA tiles per wave
-    static constexpr int PLANE_A = BM * ROW_BYTES;         // bytes of one A plane (hi or lo)
-    static constexpr int PLANE_B = BN * ROW_BYTES;
-    static constexpr int STAGE = 2 * PLANE_A + 2 * PLANE_B;
-    static constexpr int SMEM = LUT_BYTES + 2 * STAGE + (BM + BN) * 4;
-    static constexpr int TASKS_A = BM / 128;               // expansion tasks per thread
-    static constexpr int TASKS = (BM + BN) / 128;
-    static_assert((BM / WM) * WAVES_N == 8, "eight waves");
-    static_assert(SMEM <= 160 * 1024, "LDS");
-};
+// sched_group_barrier masks
+constexpr int SG_VALU = 0x002, SG_MFMA = 0x008, SG_DS_RD = 0x100;
 
 // byte offset of 16-byte chunk q (k = 8q .. 8q+7) of tile row r
-// (the row term ((r >> 1) ^ (r >> 3)) & 3 spreads 16 consecutive rows over 64 banks and
-// 8 consecutive rows over 32 banks for the 16-byte fragment reads)
 __device__ __forceinline__ int swz(int r, int q) { return r * ROW_BYTES + 16 * (q ^ (((r >> 1) ^ (r >> 3)) & 3)); }
 
 __device__ __forceinline__ uint32_t f16_pow2_neg(int d) {
@@ -80,249 +77,406 @@ __device__ __forceinline__ uint32_t f16_pow2_neg(int d) {
     return d <= 14 ? (uint32_t)(15 - d) << 10 : 1u << (24 - d);
 }
 
-// raw codes of one 8-code chunk: 8-bit formats read 8 bytes; E3C3 reads the
-// dwords that hold bytes [7q, 7q+7) of the block's 28 bytes and aligns the 56
-// code bits to bit 0
 template <class F>
 struct Raw {
+    uint32_t w[F::PACKED7 ? 3 : 2];   // the loaded code dwords, not yet unpacked
+    uint32_t a;                       // the aligned scale dword that holds the block scale byte
+};
+
+// a task's 8 codes (E3C3: 56 bits aligned to bit 0) and its block scale
+struct Chunk {
     uint32_t w[2];
     int a;
 };
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// one task's codes and scale; codes/scales are buffer descriptors over this tile's rows,
+// so rows past the matrix edge read as zero codes
 template <class F>
-__device__ __forceinline__ void load_raw(const uint8_t* row_codes, int64_t kb, int q, const int8_t* row_scl,
+__device__ __forceinline__ void load_raw(__amdgpu_buffer_rsrc_t codes, __amdgpu_buffer_rsrc_t scl,
+                                         int voff_code, int soff_code, int voff_scl, int soff_scl, int q,
                                          Raw<F>& r) {
     if (!F::PACKED7) {
-        const uint2 v = *reinterpret_cast<const uint2*>(row_codes + kb * 32 + q * 8);
+        const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(codes, voff_code, soff_code, 0);
         r.w[0] = v.x;
         r.w[1] = v.y;
     } else {
-        const uint32_t* p = reinterpret_cast<const uint32_t*>(row_codes + kb * 28);
-        const int d0 = (7 * q) >> 2;
-        const int sh = 8 * ((7 * q) & 3);
-        const uint64_t lo = (uint64_t)p[d0] | ((uint64_t)p[d0 + 1] << 32);
-        const uint64_t hi = sh > 8 ? (uint64_t)p[d0 + 2] : 0ull;
-        const uint64_t v = sh ? ((lo >> sh) | (hi << (64 - sh))) : lo;
-        r.w[0] = (uint32_t)v;
-        r.w[1] = (uint32_t)(v >> 32);
+        // bytes [7q, 7q + 7) of the block's 28 bytes: voff_code points at dword (7q) >> 2
+        r.w[0] = __builtin_amdgcn_raw_buffer_load_b32(codes, voff_code, soff_code, 0);
+        r.w[1] = __builtin_amdgcn_raw_buffer_load_b32(codes, voff_code + 4, soff_code, 0);
+        r.w[2] = __builtin_amdgcn_raw_buffer_load_b32(codes, voff_code + 8, soff_code, 0);
     }
-    r.a = row_scl[kb];
+    r.a = __builtin_amdgcn_raw_buffer_load_b32(scl, voff_scl, soff_scl, 0);
+}
+
+// unpack a task at the step that expands it.  The empty asm makes the loaded words opaque, so
+// the compiler cannot pull the unpacking up to the loads, which sit two steps earlier: that
+// would make each step wait for the codes it has just started to fetch.
+template <class F>
+__device__ __forceinline__ Chunk settle(Raw<F> r, int q, int ash) {
+    Chunk c;
+    if (!F::PACKED7) {
+        asm volatile("" : "+v"(r.w[0]), "+v"(r.w[1]), "+v"(r.a));
+        c.w[0] = r.w[0];
+        c.w[1] = r.w[1];
+    } else {
+        asm volatile("" : "+v"(r.w[0]), "+v"(r.w[1]), "+v"(r.w[2]), "+v"(r.a));
+        // bytes [7q, 7q + 7) of the block's 28: the dwords start at byte 4 floor(7q / 4)
+        const int sh = 8 * ((7 * q) & 3);
+        const uint64_t lo = (uint64_t)r.w[0] | ((uint64_t)r.w[1] << 32);
+        const uint64_t v = sh ? ((lo >> sh) | ((uint64_t)r.w[2] << (64 - sh))) : lo;
+        c.w[0] = (uint32_t)v;
+        c.w[1] = (uint32_t)(v >> 32);
+    }
+    c.a = (int)__builtin_amdgcn_sbfe(r.a, ash, 8);
+    return c;
 }
 
 template <class F>
-__device__ __forceinline__ uint32_t chunk_code(const Raw<F>& r, int i) {
+__device__ __forceinline__ uint32_t chunk_code(const Chunk& r, int i) {
     if (!F::PACKED7) return (r.w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
     const uint64_t v = (uint64_t)r.w[0] | ((uint64_t)r.w[1] << 32);
     return (uint32_t)(v >> (7 * i)) & 0x7Fu;
 }
 
+__device__ __forceinline__ uint32_t pk_mul(uint32_t x, half2v m) {
+    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, x) * m);
+}
+
+// expansion of one task, in two parts so the table gathers of the next task can be in flight
+// while this one is packed: gather -> 8 table entries (lo16 << 16 | hi16)
 template <class F>
-__device__ __forceinline__ void expand_chunk(const Raw<F>& r, int alpha, const uint32_t* lut,
-                                             int copy4, char* hi_dst, char* lo_dst) {
-    uint32_t e[8];
+__device__ __forceinline__ void gather_chunk(const Chunk& r, const char* lut, int copy4, uint32_t* e) {
 #pragma unroll
     for (int i = 0; i < 8; i++) {
         const uint32_t c = chunk_code<F>(r, i);
-        e[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(lut) + (c << 6) + copy4);
+        e[i] = *reinterpret_cast<const uint32_t*>(lut + (c << 6) + copy4);
     }
+}
+
+// pack the 8 entries into hi/lo pairs, scale by 2^-min(D, 24), store 16 B to each plane
+__device__ __forceinline__ void finish_chunk(const uint32_t* e, int D, char* hi_dst, char* lo_dst) {
+    const half2v m1 = __builtin_bit_cast(half2v, f16_pow2_neg(min(max(D, 0), 24)) * 0x10001u);
     uint32_t hv[4], lv[4];
 #pragma unroll
     for (int p = 0; p < 4; p++) {
-        hv[p] = __builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x05040100u);
-        lv[p] = __builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x07060302u);
-    }
-    const int D = alpha - r.a;      // >= 0
-    if (D != 0) {
-        const int d1 = D < 24 ? D : 24;
-        const uint32_t s1 = f16_pow2_neg(d1) * 0x10001u;
-        const half2v m1 = __builtin_bit_cast(half2v, s1);
-#pragma unroll
-        for (int p = 0; p < 4; p++) {
-            hv[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, hv[p]) * m1);
-            lv[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, lv[p]) * m1);
-        }
-        if (D > 24) {
-            const int d2 = D - 24 < 24 ? D - 24 : 24;
-            const half2v m2 = __builtin_bit_cast(half2v, f16_pow2_neg(d2) * 0x10001u);
-#pragma unroll
-            for (int p = 0; p < 4; p++) {
-                hv[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, hv[p]) * m2);
-                lv[p] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, lv[p]) * m2);
-            }
-        }
+        hv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x05040100u), m1);
+        lv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x07060302u), m1);
     }
     *reinterpret_cast<uint4*>(hi_dst) = make_uint4(hv[0], hv[1], hv[2], hv[3]);
     *reinterpret_cast<uint4*>(lo_dst) = make_uint4(lv[0], lv[1], lv[2], lv[3]);
 }
 
-template <class F, int BN>
-struct Tasks {
-    using T = Tile<BN>;
-    const uint8_t* codes[T::TASKS];     // row base of this task's operand row (null if outside)
-    const int8_t* scl[T::TASKS];
-    int alpha[T::TASKS];
-    int hi_off[T::TASKS], lo_off[T::TASKS];
+// second scaling for a chunk whose block lies more than 24 binades below its row's top
+__device__ __forceinline__ void rescale_chunk(char* dst, int D) {
+    const int d2 = min(D - 24, 24);
+    const half2v m2 = __builtin_bit_cast(half2v, f16_pow2_neg(d2) * 0x10001u);
+    uint4 v = *reinterpret_cast<uint4*>(dst);
+    v.x = pk_mul(v.x, m2);
+    v.y = pk_mul(v.y, m2);
+    v.z = pk_mul(v.z, m2);
+    v.w = pk_mul(v.w, m2);
+    *reinterpret_cast<uint4*>(dst) = v;
+}
+
+struct Frag {
+    half8 ah[TM], al[TM], bh[TN], bl[TN];
 };
 
-template <class F, int BN>
+template <class F>
 __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     const uint8_t* __restrict__ A, const int8_t* __restrict__ As,
     const uint8_t* __restrict__ B, const int8_t* __restrict__ Bs,
     int64_t M, int64_t N, int64_t K, float* __restrict__ C, int64_t ldc, int fidx) {
-    using T = Tile<BN>;
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    uint32_t* lut = reinterpret_cast<uint32_t*>(smem);
+    const char* lut = smem;
     char* stage0 = smem + LUT_BYTES;
-    int* sAlpha = reinterpret_cast<int*>(smem + LUT_BYTES + 2 * T::STAGE);
+    char* stage1 = stage0 + STAGE;
+    int* sAlpha = reinterpret_cast<int*>(smem + LUT_BYTES + 2 * STAGE);
     int* sBeta = sAlpha + BM;
 
     const int tid = threadIdx.x;
-    for (int i = tid; i < GEMM_DEC_ENTRIES * LUT_COPIES; i += NTHREADS) lut[i] = g_dec[fidx][i / LUT_COPIES];
+    {
+        uint32_t* l = reinterpret_cast<uint32_t*>(smem);
+        for (int i = tid; i < GEMM_DEC_ENTRIES * LUT_COPIES; i += NTHREADS) l[i] = g_dec[fidx][i / LUT_COPIES];
+    }
 
     const int64_t m0 = (int64_t)blockIdx.y * BM, n0 = (int64_t)blockIdx.x * BN;
     const int64_t nkb = K / 32;
-    const int64_t code_row_bytes = F::PACKED7 ? nkb * 28 : K;
+    // this workgroup's share of the K blocks (split-K over grid.z)
+    const int64_t per = (nkb + gridDim.z - 1) / gridDim.z;
+    const int64_t kb0 = (int64_t)blockIdx.z * per;
+    const int64_t kb1 = min(nkb, kb0 + per);
+    const int64_t nsteps = kb1 - kb0;
+    const int64_t row_bytes = F::PACKED7 ? nkb * 28 : K;
 
-    // largest block scale of every A and B row of the tile
-    if (tid < BM + BN) {
-        const bool isA = tid < BM;
-        const int lrow = isA ? tid : tid - BM;
-        const int64_t grow = (isA ? m0 : n0) + lrow;
-        int alpha = -128;
-        if (grow < (isA ? M : N)) {
-            const int8_t* s = (isA ? As : Bs) + grow * nkb;
-            for (int64_t kb = 0; kb < nkb; kb++) alpha = max(alpha, (int)s[kb]);
+    // largest block scale of every A and B row of the tile (over all of K); 0 for rows past the
+    // edge.  Eight independent 8-byte loads per round keep the scale reads from serializing.
+#pragma unroll
+    for (int h = 0; h < 2; h++) {
+        const int64_t grow = (h == 0 ? m0 : n0) + tid;
+        int alpha = 0;
+        if (grow < (h == 0 ? M : N)) {
+            const int8_t* sp = (h == 0 ? As : Bs) + grow * nkb;
+            alpha = -128;
+            int64_t kb = 0;
+            if ((reinterpret_cast<uintptr_t>(sp) & 7) == 0) {
+                for (; kb + 64 <= nkb; kb += 64) {
+                    uint2 v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; u++) v[u] = *reinterpret_cast<const uint2*>(sp + kb + 8 * u);
+#pragma unroll
+                    for (int u = 0; u < 8; u++)
+#pragma unroll
+                        for (int b = 0; b < 4; b++) {
+                            alpha = max(alpha, (int)(int8_t)(v[u].x >> (8 * b)));
+                            alpha = max(alpha, (int)(int8_t)(v[u].y >> (8 * b)));
+                        }
+                }
+            }
+            for (; kb < nkb; kb++) alpha = max(alpha, (int)sp[kb]);
         }
-        (isA ? sAlpha : sBeta)[lrow] = alpha;
+        (h == 0 ? sAlpha : sBeta)[tid] = alpha;
     }
     __syncthreads();
 
-    // expansion tasks: rows (tid >> 2) + 128 j of A (j < TASKS_A) then of B; chunk q = tid & 3
-    const int q = tid & 3;
-    const int copy4 = (tid & (LUT_COPIES - 1)) * 4;
-    Tasks<F, BN> tk;
-#pragma unroll
-    for (int j = 0; j < T::TASKS; j++) {
-        const bool isA = j < T::TASKS_A;
-        const int lrow = (tid >> 2) + 128 * (isA ? j : j - T::TASKS_A);
-        const int64_t grow = (isA ? m0 : n0) + lrow;
-        const bool valid = grow < (isA ? M : N);
-        tk.codes[j] = valid ? (isA ? A : B) + grow * code_row_bytes : nullptr;
-        tk.scl[j] = valid ? (isA ? As : Bs) + grow * nkb : nullptr;
-        tk.alpha[j] = isA ? sAlpha[lrow] : sBeta[lrow];
-        const int off = isA ? swz(lrow, q) : 2 * T::PLANE_A + swz(lrow, q);
-        tk.hi_off[j] = off;
-        tk.lo_off[j] = off + (isA ? T::PLANE_A : T::PLANE_B);
-    }
+    // buffer descriptors over the tile's rows (reads past the last row return zero)
+    const int64_t rowsA = min((int64_t)BM, M - m0), rowsB = min((int64_t)BN, N - n0);
+    const __amdgpu_buffer_rsrc_t rcA = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(A + m0 * row_bytes), (short)0, (int)(rowsA * row_bytes), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rcB = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(B + n0 * row_bytes), (short)0, (int)(rowsB * row_bytes), 0x00020000);
+    // scales are read as the aligned dword that holds the byte (a 32-bit result keeps the
+    // compiler from extending the byte early): the descriptors start at the dword below the
+    // tile's first scale and end at the dword that holds its last one, all inside mapped pages
+    const uintptr_t sa0 = reinterpret_cast<uintptr_t>(As + m0 * nkb), sb0 = reinterpret_cast<uintptr_t>(Bs + n0 * nkb);
+    const int dA = (int)(sa0 & 3), dB = (int)(sb0 & 3);
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(sa0 - dA), (short)0, (int)((dA + rowsA * nkb + 3) & ~3), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(sb0 - dB), (short)0, (int)((dB + rowsB * nkb + 3) & ~3), 0x00020000);
 
-    Raw<F> rawA[T::TASKS], rawB[T::TASKS];   // two register sets, indexed only at compile time
-    auto fetch = [&](int64_t kb, Raw<F>* dst) {
+    // expansion tasks: rows (tid >> 2) + 64 j of A (j < 4) and of B (j >= 4), chunk q = tid & 3
+    const int q = tid & 3;
+    const int r0 = tid >> 2;
+    const int copy4 = (tid & (LUT_COPIES - 1)) * 4;
+    const int off0 = swz(r0, q);                 // swz(r0 + 64 j, q) = off0 + 64 j * ROW_BYTES
+    const int voff_code = (int)(r0 * row_bytes) + (F::PACKED7 ? 4 * ((7 * q) >> 2) : 8 * q);
+    // byte offset of task j's scale of block kb: xA/xB + 64 (j & 3) nkb + kb, where the middle
+    // term is a multiple of 4 and so moves only the dword
+    const int xA = dA + (int)(r0 * nkb), xB = dB + (int)(r0 * nkb);
+    // the 8 row maxima of this thread's tasks, one byte each (scales lie in [-128, 127])
+    uint32_t alpha_pk[2] = {0u, 0u};
 #pragma unroll
-        for (int j = 0; j < T::TASKS; j++)
-            if (tk.codes[j]) load_raw<F>(tk.codes[j], kb, q, tk.scl[j], dst[j]);
+    for (int j = 0; j < TASKS; j++) {
+        const int al = j < 4 ? sAlpha[r0 + 64 * j] : sBeta[r0 + 64 * (j - 4)];
+        alpha_pk[j >> 2] |= ((uint32_t)al & 0xFFu) << (8 * (j & 3));
+    }
+    auto alpha_of = [&](int j) { return (int)__builtin_amdgcn_sbfe(alpha_pk[j >> 2], 8 * (j & 3), 8); };
+    auto task_dst_hi = [&](char* stage, int j) {
+        return stage + (j < 4 ? 0 : 2 * PLANE) + off0 + 64 * (j & 3) * ROW_BYTES;
     };
-    auto expand = [&](const Raw<F>* src, char* stage) {
+
+    // one register set of codes in flight: task j's codes of block kb+1 are loaded right after
+    // its codes of block kb have been read, so each load has a whole step to arrive.  Loads are
+    // unconditional (a block past the workgroup's range reads the next row, or zero past the
+    // tile, and is never expanded).
+    Raw<F> raw[TASKS];
+    // per step: the block whose codes are read (cur) and the one requested (next)
+    struct Blocks {
+        int64_t next;
+        int vA, vB;       // scale dword offsets of the next block, rows r0 of A and B
+        int shA, shB;     // bit position of the scale byte in its dword, current block
+    };
+    auto blocks = [&](int64_t kb_cur) {
+        Blocks b;
+        b.next = kb_cur + 1;
+        b.vA = (xA + (int)b.next) & ~3;
+        b.vB = (xB + (int)b.next) & ~3;
+        b.shA = 8 * ((xA + (int)kb_cur) & 3);
+        b.shB = 8 * ((xB + (int)kb_cur) & 3);
+        return b;
+    };
+    auto fetch = [&](int j, int64_t kb, int vscl) {
+        const int ro = 64 * (j & 3);
+        load_raw<F>(j < 4 ? rcA : rcB, j < 4 ? rsA : rsB, voff_code,
+                    (int)(ro * row_bytes + kb * (F::PACKED7 ? 28 : 32)), vscl, (int)(ro * nkb), q, raw[j]);
+    };
+    // gather: task j's table entries into e, then the load of its next block; returns
+    // D = (row maximum) - (block scale), and files min(D, 48) for the fixup pass
+    uint32_t dpk[2];
+    auto gather_task = [&](int j, const Blocks& b, uint32_t* e) {
+        const Chunk c = settle<F>(raw[j], q, j < 4 ? b.shA : b.shB);
+        fetch(j, b.next, j < 4 ? b.vA : b.vB);
+        gather_chunk<F>(c, lut, copy4, e);
+        const int D = alpha_of(j) - c.a;
+        const uint32_t db = (uint32_t)min(D, 48) << (8 * (j & 3));
+        dpk[j >> 2] = (j & 3) ? (dpk[j >> 2] | db) : db;
+        return D;
+    };
+    // pack and scale; `need` collects blocks that the 24-binade multiplier cannot reach
+    auto finish_task = [&](int D, char* stage, int j, const uint32_t* e, bool& need) {
+        char* hd = task_dst_hi(stage, j);
+        need |= D > 24;
+        finish_chunk(e, D, hd, hd + PLANE);
+    };
+    // rare second scaling pass (block more than 24 binades below its row's top)
+    auto fixup = [&](char* stage, bool need) {
+        if (__any(need)) {   // wave-uniform: taken only when some lane has such a block
 #pragma unroll
-        for (int j = 0; j < T::TASKS; j++) {
-            if (tk.codes[j]) {
-                expand_chunk<F>(src[j], tk.alpha[j], lut, copy4, stage + tk.hi_off[j], stage + tk.lo_off[j]);
-            } else {
-                *reinterpret_cast<uint4*>(stage + tk.hi_off[j]) = make_uint4(0, 0, 0, 0);
-                *reinterpret_cast<uint4*>(stage + tk.lo_off[j]) = make_uint4(0, 0, 0, 0);
+            for (int j = 0; j < TASKS; j++) {
+                const int D = (int)((dpk[j >> 2] >> (8 * (j & 3))) & 0xFFu);
+                if (D > 24) {
+                    char* hd = task_dst_hi(stage, j);
+                    rescale_chunk(hd, D);
+                    rescale_chunk(hd + PLANE, D);
+                }
             }
         }
     };
-
-    char* stage1 = stage0 + T::STAGE;
-    fetch(0, rawA);
-    if (nkb > 1) fetch(1, rawB);
-    expand(rawA, stage0);
 
     const int lane = tid & 63, wave = tid >> 6;
-    const int wm = wave / T::WAVES_N, wn = wave % T::WAVES_N;
-    const bool mfma_first = (wave & 4) == 0;   // the two waves of a SIMD take opposite orders
-    f32x16 acc[T::TM][T::TN];
+    const int wm = wave >> 1, wn = wave & 1;
+    // lane part of a fragment address: row (lane & 31) of a 32-row tile, chunk 2 kq + (lane >> 5);
+    // the swizzle only depends on bits 1..3 of the row, which the tile bases leave alone
+    const int lr = lane & 31;
+    const int fsw = ((lr >> 1) ^ (lr >> 3)) & 3;
+    const int foff0 = lr * ROW_BYTES + 16 * ((0 + (lane >> 5)) ^ fsw);
+    const int foff1 = lr * ROW_BYTES + 16 * ((2 + (lane >> 5)) ^ fsw);
+    const int abase = wm * WM * ROW_BYTES, bbase = 2 * PLANE + wn * WN * ROW_BYTES;
+    auto load_frag = [&](Frag& f, const char* st, int kq) {
+        const char* pa = st + abase + (kq ? foff1 : foff0);
+        const char* pb = st + bbase + (kq ? foff1 : foff0);
 #pragma unroll
-    for (int i = 0; i < T::TM; i++)
+        for (int t = 0; t < TM; t++) {
+            f.ah[t] = *reinterpret_cast<const half8*>(pa + t * 32 * ROW_BYTES);
+            f.al[t] = *reinterpret_cast<const half8*>(pa + PLANE + t * 32 * ROW_BYTES);
+        }
 #pragma unroll
-        for (int j = 0; j < T::TN; j++)
+        for (int t = 0; t < TN; t++) {
+            f.bh[t] = *reinterpret_cast<const half8*>(pb + t * 32 * ROW_BYTES);
+            f.bl[t] = *reinterpret_cast<const half8*>(pb + PLANE + t * 32 * ROW_BYTES);
+        }
+    };
+
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
 #pragma unroll
             for (int v = 0; v < 16; v++) acc[i][j][v] = 0.f;
-    __syncthreads();
 
-    auto mfma_step = [&](const char* st) {
-        const char* sAh = st;
-        const char* sAl = st + T::PLANE_A;
-        const char* sBh = st + 2 * T::PLANE_A;
-        const char* sBl = sBh + T::PLANE_B;
-#pragma unroll
-        for (int kq = 0; kq < 2; kq++) {
-            const int qq = 2 * kq + (lane >> 5);
-            half8 ah[T::TM], al[T::TM], bh[T::TN], bl[T::TN];
-#pragma unroll
-            for (int t = 0; t < T::TM; t++) {
-                const int r = wm * T::WM + t * 32 + (lane & 31);
-                ah[t] = *reinterpret_cast<const half8*>(sAh + swz(r, qq));
-                al[t] = *reinterpret_cast<const half8*>(sAl + swz(r, qq));
-            }
-#pragma unroll
-            for (int t = 0; t < T::TN; t++) {
-                const int r = wn * T::WN + t * 32 + (lane & 31);
-                bh[t] = *reinterpret_cast<const half8*>(sBh + swz(r, qq));
-                bl[t] = *reinterpret_cast<const half8*>(sBl + swz(r, qq));
-            }
-#pragma unroll
-            for (int i = 0; i < T::TM; i++)
-#pragma unroll
-                for (int j = 0; j < T::TN; j++) {
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[i], bh[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(ah[i], bl[j], acc[i][j], 0, 0, 0);
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(al[i], bh[j], acc[i][j], 0, 0, 0);
-                }
-        }
+    // MFMA number idx (0..47) of a half step: product p = idx / 16 over the 4 x 4 tiles
+    auto mfma = [&](const Frag& f, int idx) {
+        const int p = idx / 16, i = (idx / 4) % 4, j = idx % 4;
+        const half8& a = (p == 2) ? f.al[i] : f.ah[i];
+        const half8& b = (p == 1) ? f.bl[j] : f.bh[j];
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[i][j], 0, 0, 0);
     };
 
-    // one step: MFMAs on `cur` (step kb), expansion of step kb+1 from `ex` into `nxt`,
-    // codes of step kb+2 fetched into `fx` (the set step kb was expanded from)
-    auto step = [&](int64_t kb, const char* cur, char* nxt, Raw<F>* fx, const Raw<F>* ex) {
-        const bool more = kb + 1 < nkb;
-        if (kb + 2 < nkb) fetch(kb + 2, fx);
-        if (mfma_first) {
-            mfma_step(cur);
-            if (more) expand(ex, nxt);
-        } else {
-            if (more) expand(ex, nxt);
-            mfma_step(cur);
+    // prologue: codes of block 0 (and 1), expand block 0, fragments of its first half
+    Frag f0, f1;
+    {
+        const Blocks b0 = blocks(kb0);
+#pragma unroll
+        for (int j = 0; j < TASKS; j++) fetch(j, kb0, j < 4 ? (xA + (int)kb0) & ~3 : (xB + (int)kb0) & ~3);
+        bool need = false;
+#pragma unroll
+        for (int j = 0; j < TASKS; j++) {
+            uint32_t e[8];
+            const int D = gather_task(j, b0, e);
+            finish_task(D, stage0, j, e, need);
         }
-        __syncthreads();
-    };
-    for (int64_t kb = 0; kb < nkb; kb += 2) {
-        step(kb, stage0, stage1, rawA, rawB);
-        if (kb + 1 < nkb) step(kb + 1, stage1, stage0, rawB, rawA);
+        fixup(stage0, need);
     }
+    __syncthreads();
+    load_frag(f0, stage0, 0);
+
+    // one step with a successor: MFMAs of step s from `cur` (f0 already loaded); step s+1 is
+    // expanded into `nxt` while the MFMAs run, and the codes of step s+2 are requested
+    auto step = [&](int64_t s, const char* cur, char* nxt) {
+        const Blocks b = blocks(kb0 + s + 1);
+        load_frag(f1, cur, 1);
+        uint32_t e0[8], e1[8];
+        int D0, D1;
+        bool need = false;
+        D0 = gather_task(0, b, e0);
+        // 8 groups of 12 MFMAs (f0 for groups 0..3, f1 for 4..7); group g gathers task g+1 and
+        // packs task g; the barrier sits before the last group so the next step's fragments
+        // load behind its MFMAs
+#pragma unroll
+        for (int g = 0; g < 7; g++) {
+#pragma unroll
+            for (int m = 0; m < 12; m++) mfma(g < 4 ? f0 : f1, 12 * (g & 3) + m);
+            ((g & 1) ? D0 : D1) = gather_task(g + 1, b, (g & 1) ? e0 : e1);
+            finish_task((g & 1) ? D1 : D0, nxt, g, (g & 1) ? e1 : e0, need);
+#pragma unroll
+            for (int m = 0; m < 12; m++) {
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_VALU, 3, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_DS_RD, 1, 0);
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        finish_task(D1, nxt, 7, e1, need);
+        fixup(nxt, need);
+        __syncthreads();
+        load_frag(f0, nxt, 0);
+#pragma unroll
+        for (int m = 36; m < 48; m++) mfma(f1, m);
+    };
+
+    char* cur = stage0;
+    char* nxt = stage1;
+    for (int64_t s = 0; s + 1 < nsteps; s++) {
+        step(s, cur, nxt);
+        char* t = cur;
+        cur = nxt;
+        nxt = t;
+    }
+    // the last step: MFMAs only
+    load_frag(f1, cur, 1);
+#pragma unroll
+    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f0, m);
+#pragma unroll
+    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f1, m);
 
     // epilogue: D[i][j], j = lane % 32, i = 8 (v / 4) + 4 (lane / 32) + v % 4
+    const bool split = gridDim.z > 1;
 #pragma unroll
-    for (int ti = 0; ti < T::TM; ti++)
+    for (int ti = 0; ti < TM; ti++)
 #pragma unroll
-        for (int tj = 0; tj < T::TN; tj++) {
-            const int lj = wn * T::WN + tj * 32 + (lane & 31);
+        for (int tj = 0; tj < TN; tj++) {
+            const int lj = wn * WN + tj * 32 + (lane & 31);
             const int64_t gj = n0 + lj;
             const int beta = sBeta[lj];
 #pragma unroll
             for (int v = 0; v < 16; v++) {
-                const int li = wm * T::WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                const int li = wm * WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
                 const int64_t gi = m0 + li;
-                if (gi < M && gj < N)
-                    C[gi * ldc + gj] = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                if (gi < M && gj < N) {
+                    const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                    if (split) unsafeAtomicAdd(C + gi * ldc + gj, val);
+                    else C[gi * ldc + gj] = val;
+                }
             }
         }
 }
 
-template <class F, int BN>
-hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                       int64_t N, int64_t K, float* c, int64_t ldc, int fidx, hipStream_t s) {
-    using T = Tile<BN>;
+// zero-fill of the output rows (split-K accumulates into C)
+__global__ __launch_bounds__(256) void zero_rows_kernel(float* __restrict__ C, int64_t M, int64_t N, int64_t ldc) {
+    const int64_t total = M * N;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < total; i += (int64_t)gridDim.x * 256) {
+        const int64_t r = i / N;
+        C[r * ldc + (i - r * N)] = 0.f;
+    }
+}
+
+template <class F>
+hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
+                      int64_t N, int64_t K, float* c, int64_t ldc, int fidx, hipStream_t s) {
     // the dynamic-LDS limit is a per-function, per-device attribute: raise it once per device
     static bool attr_set[64] = {};
     int dev = 0;
@@ -330,26 +484,27 @@ hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int
     if (e != hipSuccess) return e;
     if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
     if (!attr_set[dev]) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<F, BN>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, T::SMEM);
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<F>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, SMEM);
         if (e != hipSuccess) return e;
         attr_set[dev] = true;
     }
-    dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM));
-    hipLaunchKernelGGL((gemm_kernel<F, BN>), grid, dim3(NTHREADS), T::SMEM, s,
+    const int64_t tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int64_t nkb = K / 32;
+    // split K in two when the tiles cover less than the 256 compute units (and K is long enough)
+    const int splits = (tiles < 256 && nkb >= 16) ? 2 : 1;
+    if (splits > 1) {
+        int64_t zb = (M * N + 255) / 256;
+        zb = zb < 4096 ? zb : 4096;
+        hipLaunchKernelGGL(zero_rows_kernel, dim3((unsigned)zb), dim3(256), 0, s, c, M, N, ldc);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    dim3 grid((unsigned)((N + BN - 1) / BN), (unsigned)((M + BM - 1) / BM), (unsigned)splits);
+    hipLaunchKernelGGL((gemm_kernel<F>), grid, dim3(NTHREADS), SMEM, s,
                        reinterpret_cast<const uint8_t*>(a), as, reinterpret_cast<const uint8_t*>(b), bs,
                        M, N, K, c, ldc, fidx);
     return hipGetLastError();
-}
-
-template <class F>
-hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                      int64_t N, int64_t K, float* c, int64_t ldc, int fidx, hipStream_t s) {
-    // 256 x 256 tiles when they fill the 256 compute units at least twice, else 256 x 128
-    const int64_t tiles256 = ((M + BM - 1) / BM) * ((N + 255) / 256);
-    if (tiles256 >= 512)
-        return launch_tile<F, 256>(a, as, b, bs, M, N, K, c, ldc, fidx, s);
-    return launch_tile<F, 128>(a, as, b, bs, M, N, K, c, ldc, fidx, s);
 }
 
 }  // namespace
