@@ -400,7 +400,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
         const Blocks b = blocks(kb0 + s + 1);
         load_frag(f1, cur, 1);
         uint32_t e0[8], e1[8];
-        int D0, D1;
+        int D0 = 0, D1 = 0;
         bool need = false;
         D0 = gather_task(0, b, e0);
         // 8 groups of 12 MFMAs (f0 for groups 0..3, f1 for 4..7); group g gathers task g+1 and

@@ -15,20 +15,28 @@
 #include "device_util.hpp"
 
 #include <cstring>
+#include <type_traits>
 
 namespace curvefp {
 
 __device__ uint32_t g_qlut[3][QLUT_MAX];
+// bfloat16 sources: the low 16 bits of every scaled magnitude are zero, so the bucket's
+// decision point is never passed and the rank is the bucket's base rank alone (one byte)
+__device__ __attribute__((aligned(16))) uint8_t g_qlut8[3][QLUT_MAX];
 __device__ uint32_t g_lmax_mant[3];
 
 hipError_t quantize_upload(const AllTables& t) {
     static uint32_t h[3][QLUT_MAX];
+    static uint8_t h8[3][QLUT_MAX];
     uint32_t lm[3];
     for (int f = 0; f < 3; f++) {
         memcpy(h[f], t.f[f].qlut, sizeof(h[f]));
+        for (int i = 0; i < QLUT_MAX; i++) h8[f][i] = (uint8_t)(t.f[f].qlut[i] >> 16);
         lm[f] = t.f[f].lmax_mant;
     }
     hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut), h, sizeof(h));
+    if (e != hipSuccess) return e;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut8), h8, sizeof(h8));
     if (e != hipSuccess) return e;
     return hipMemcpyToSymbol(HIP_SYMBOL(g_lmax_mant), lm, sizeof(lm));
 }
@@ -54,15 +62,23 @@ __device__ __forceinline__ uint32_t rank_lookup(int32_t yb, const uint32_t* lut)
     return (e >> 16) + ((((uint32_t)yb & 0xFFFFu) > (e & 0xFFFFu)) ? 1u : 0u);
 }
 
-// fast path: a >= A_FAST_MIN, where subnormal or zero inputs can only reach rank 0
+// the same for a yb whose low 16 bits are zero, with the one-byte table
 template <class F>
-__device__ __forceinline__ uint32_t rank_fast(uint32_t mag, int a, const uint32_t* lut) {
+__device__ __forceinline__ uint32_t rank_lookup(int32_t yb, const uint8_t* lut) {
+    int32_t idx = (yb >> 16) - ((127 + F::OZ) << 7);
+    if (idx < 0) return 0;
+    return lut[min(idx, F::QLUT_SIZE - 1)];
+}
+
+// fast path: a >= A_FAST_MIN, where subnormal or zero inputs can only reach rank 0
+template <class F, class T>
+__device__ __forceinline__ uint32_t rank_fast(uint32_t mag, int a, const T* lut) {
     return rank_lookup<F>((int32_t)mag - (a << 23), lut);
 }
 
 // exact path for blocks with tiny scales: normalize subnormal inputs first
-template <class F>
-__device__ __forceinline__ uint32_t rank_exact(uint32_t mag, int a, const uint32_t* lut) {
+template <class F, class T>
+__device__ __forceinline__ uint32_t rank_exact(uint32_t mag, int a, const T* lut) {
     if (mag == 0) return 0;
     int32_t yb;
     if ((mag >> 23) == 0) {
@@ -75,9 +91,8 @@ __device__ __forceinline__ uint32_t rank_exact(uint32_t mag, int a, const uint32
     return rank_lookup<F>(yb, lut);
 }
 
-template <class F>
-__device__ __forceinline__ void ranks_of(const uint32_t* mag, int n, int a, const uint32_t* lut,
-                                         uint32_t* r) {
+template <class F, class T>
+__device__ __forceinline__ void ranks_of(const uint32_t* mag, int n, int a, const T* lut, uint32_t* r) {
     if (a == -128) {
         for (int i = 0; i < n; i++) r[i] = 0;
     } else if (a >= F::A_FAST_MIN) {
@@ -92,11 +107,11 @@ __device__ __forceinline__ int scale_of(uint32_t amax, uint32_t lmax_mant) {
     return (amax >= 0x7F800000u) ? -128 : block_scale<F>(amax, lmax_mant);
 }
 
+// unpack 8 consecutive source elements into magnitude bits (as fp32) and sign bits
 template <bool BF16>
-__device__ __forceinline__ void load8(const void* src, int64_t elem, uint32_t* mag, uint32_t* sgn) {
+__device__ __forceinline__ void unpack8(const uint4* v, uint32_t* mag, uint32_t* sgn) {
     if (BF16) {
-        const uint4 v = *reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(src) + elem);
-        const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+        const uint32_t w[4] = {v[0].x, v[0].y, v[0].z, v[0].w};
 #pragma unroll
         for (int i = 0; i < 4; i++) {
             mag[2 * i] = (w[i] << 16) & 0x7FFF0000u;
@@ -105,9 +120,7 @@ __device__ __forceinline__ void load8(const void* src, int64_t elem, uint32_t* m
             sgn[2 * i + 1] = w[i] >> 31;
         }
     } else {
-        const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(src) + elem);
-        const uint4 v0 = p[0], v1 = p[1];
-        const uint32_t w[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+        const uint32_t w[8] = {v[0].x, v[0].y, v[0].z, v[0].w, v[1].x, v[1].y, v[1].z, v[1].w};
 #pragma unroll
         for (int i = 0; i < 8; i++) {
             mag[i] = w[i] & 0x7FFFFFFFu;
@@ -116,62 +129,163 @@ __device__ __forceinline__ void load8(const void* src, int64_t elem, uint32_t* m
     }
 }
 
-// 4 threads per block of 32 along a row; each thread owns 8 consecutive elements
-template <class F, bool BF16>
+// quotient by an invariant divisor d >= 1 (Granlund and Montgomery, "Division by invariant
+// integers using multiplication", 1994): l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1,
+// n / d = (mulhi(n, m) + n) >> l for every 32-bit n
+struct Div32 {
+    uint32_t m;
+    int l;
+};
+
+__device__ __forceinline__ uint32_t div32(uint32_t n, Div32 d) {
+    return (uint32_t)(((uint64_t)__umulhi(n, d.m) + n) >> d.l);
+}
+
+Div32 make_div32(uint32_t d) {
+    int l = 0;
+    while ((1ull << l) < d) l++;
+    Div32 r;
+    r.m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+    r.l = l;
+    return r;
+}
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+template <bool NT>
+__device__ __forceinline__ uint4 ld16(const uint4* p) {
+    if (!NT) return *p;
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
+template <bool NT>
+__device__ __forceinline__ void st4(uint32_t* p, uint32_t x) {
+    if (!NT) *p = x;
+    else __builtin_nontemporal_store(x, p);
+}
+
+template <bool NT>
+__device__ __forceinline__ void st8(uint8_t* p, uint32_t x, uint32_t y) {
+    if (!NT) {
+        *reinterpret_cast<uint2*>(p) = make_uint2(x, y);
+    } else {
+        u32x2 v;
+        v.x = x;
+        v.y = y;
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
+    }
+}
+
+// quantize one chunk of 8 consecutive elements; four lanes (a quad) hold one block of 32
+template <class F, bool BF16, bool NTS, class T>
+__device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const T* lut,
+                                               uint32_t lmax_mant, uint8_t* __restrict__ codes,
+                                               int8_t* __restrict__ scales) {
+    const int part = (int)(g & 3);
+    uint32_t mag[8], sgn[8];
+    unpack8<BF16>(v, mag, sgn);
+    uint32_t amax = 0;
+#pragma unroll
+    for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+    amax = quad_max_u32(amax);
+    const int a = scale_of<F>(amax, lmax_mant);
+    uint32_t rk[8];
+    ranks_of<F>(mag, 8, a, lut, rk);
+    uint32_t c[8];
+#pragma unroll
+    for (int i = 0; i < 8; i++) c[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
+    const uint32_t b = g >> 2;   // block index (blocks are contiguous in the output)
+    if (!F::PACKED7) {
+        st8<NTS>(codes + (uint64_t)g * 8, c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
+                 c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
+    } else {
+        // 56-bit chunk of this lane; the block string is chunk0 | chunk1 << 56 | ...
+        uint64_t chunk = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) chunk |= (uint64_t)c[i] << (7 * i);
+        const uint32_t nlo = dpp_u32<QP_NEXT>((uint32_t)chunk);
+        const uint32_t nhi = dpp_u32<QP_NEXT>((uint32_t)(chunk >> 32));
+        const uint64_t next = ((uint64_t)nhi << 32) | nlo;
+        uint32_t* base = reinterpret_cast<uint32_t*>(codes + (uint64_t)b * 28);
+        if (part < 3) {
+            const uint64_t lo64 = chunk | (next << 56);
+            const uint64_t hi64 = next >> 8;
+            const int sh = 8 * part;
+            const uint64_t w = sh ? ((lo64 >> sh) | (hi64 << (64 - sh))) : lo64;
+            st4<NTS>(base + 2 * part, (uint32_t)w);
+            st4<NTS>(base + 2 * part + 1, (uint32_t)(w >> 32));
+        } else {
+            st4<NTS>(base + 6, (uint32_t)(chunk >> 24));
+        }
+    }
+    if (part == 0) scales[b] = (int8_t)a;
+}
+
+// blocks along rows: chunk g (8 elements) is chunk g mod cpr of row g / cpr; four consecutive
+// chunks form a block.  Each thread has U chunks in flight, 256 chunks apart, so every load
+// instruction of a wave reads one contiguous span.
+template <class F, bool BF16, int U, bool NT, bool NTS>
 __global__ __launch_bounds__(256) void quantize_rows_kernel(
-    const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld,
+    const void* __restrict__ src, uint32_t nchunks, uint32_t cpr, Div32 dcpr, int64_t ld,
     uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
-    __shared__ uint32_t lut[F::QLUT_SIZE];
-    for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
+    using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
+    __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int NV = BF16 ? 1 : 2;   // 16-byte loads per chunk
+    const bool dense = ld == (int64_t)cpr * 8;
+    const char* s8 = reinterpret_cast<const char*>(src);
+    auto load = [&](uint32_t g0, uint4 (*v)[NV]) {
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const uint32_t g = g0 + 256u * u;
+            if (g < nchunks) {
+                int64_t e;
+                if (dense) {
+                    e = (int64_t)g * 8;
+                } else {
+                    const uint32_t r = div32(g, dcpr);
+                    e = (int64_t)r * ld + (int64_t)(g - r * cpr) * 8;
+                }
+                const uint4* p = reinterpret_cast<const uint4*>(s8 + e * ESZ);
+#pragma unroll
+                for (int t = 0; t < NV; t++) v[u][t] = ld16<NT>(p + t);
+            }
+        }
+    };
+    const uint32_t step = gridDim.x * (256u * U);
+    uint32_t g0 = blockIdx.x * (256u * U) + threadIdx.x;
+    // the first chunks are requested before the table is filled, so both latencies overlap
+    uint4 v[U][NV];
+    load(g0, v);
+    if (BF16) {
+        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(g_qlut8[fidx]);
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lut);
+        for (int i = threadIdx.x; i < F::QLUT_SIZE / 4; i += blockDim.x) l32[i] = s32[i];
+    } else {
+        for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = (T)g_qlut[fidx][i];
+    }
     const uint32_t lmax_mant = g_lmax_mant[fidx];
     __syncthreads();
 
-    const int64_t bpr = cols / 32;
-    const int64_t nthreads = rows * bpr * 4;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nthreads; g += stride) {
-        const int64_t b = g >> 2;
-        const int part = (int)(g & 3);
-        const int64_t r = b / bpr;
-        const int64_t cb = b - r * bpr;
-        uint32_t mag[8], sgn[8];
-        load8<BF16>(src, r * ld + cb * 32 + part * 8, mag, sgn);
-        uint32_t amax = 0;
+    while (g0 < nchunks) {
+        // next chunks in flight while these are quantized
+        const uint32_t g1 = g0 + step;
+        uint4 w[U][NV];
+        const bool more = g1 < nchunks && g1 > g0;
+        if (more) load(g1, w);
 #pragma unroll
-        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
-        amax = quad_max_u32(amax);
-        const int a = scale_of<F>(amax, lmax_mant);
-        uint32_t rk[8];
-        ranks_of<F>(mag, 8, a, lut, rk);
-        uint32_t c[8];
-#pragma unroll
-        for (int i = 0; i < 8; i++) c[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
-        if (!F::PACKED7) {
-            uint2 o;
-            o.x = c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24);
-            o.y = c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24);
-            *reinterpret_cast<uint2*>(codes + r * cols + cb * 32 + part * 8) = o;
-        } else {
-            // 56-bit chunk of this thread; the block string is chunk0 | chunk1 << 56 | ...
-            uint64_t chunk = 0;
-#pragma unroll
-            for (int i = 0; i < 8; i++) chunk |= (uint64_t)c[i] << (7 * i);
-            const uint32_t nlo = dpp_u32<QP_NEXT>((uint32_t)chunk);
-            const uint32_t nhi = dpp_u32<QP_NEXT>((uint32_t)(chunk >> 32));
-            const uint64_t next = ((uint64_t)nhi << 32) | nlo;
-            uint32_t* base = reinterpret_cast<uint32_t*>(codes + (r * bpr + cb) * 28);
-            if (part < 3) {
-                const uint64_t lo64 = chunk | (next << 56);
-                const uint64_t hi64 = next >> 8;
-                const int sh = 8 * part;
-                const uint64_t w = sh ? ((lo64 >> sh) | (hi64 << (64 - sh))) : lo64;
-                base[2 * part] = (uint32_t)w;
-                base[2 * part + 1] = (uint32_t)(w >> 32);
-            } else {
-                base[6] = (uint32_t)(chunk >> 24);
-            }
+        for (int u = 0; u < U; u++) {
+            const uint32_t g = g0 + 256u * u;
+            if (g < nchunks) quantize_chunk<F, BF16, NTS>(v[u], g, lut, lmax_mant, codes, scales);
         }
-        if (part == 0) scales[r * bpr + cb] = (int8_t)a;
+        if (!more) break;
+#pragma unroll
+        for (int u = 0; u < U; u++)
+#pragma unroll
+            for (int t = 0; t < NV; t++) v[u][t] = w[u][t];
+        g0 = g1;
     }
 }
 
@@ -236,26 +350,48 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(
     }
 }
 
+template <class F, bool BF16>
+hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
+                       int8_t* scales, hipStream_t s) {
+    // 128 (bf16) or 64 (fp32) bytes in flight per thread, streaming (non-temporal) loads and
+    // stores, at most 32768 workgroups: the shape that measured fastest on a 1 GiB stream
+    constexpr int U = BF16 ? 8 : 2;
+    const int64_t cpr = cols / 8;
+    // 32-bit chunk indices: slabs of at most 2^31 chunks
+    const int64_t slab = ((int64_t)1 << 31) / cpr;
+    for (int64_t r0 = 0; r0 < rows; r0 += slab) {
+        const int64_t nr = rows - r0 < slab ? rows - r0 : slab;
+        const int64_t nchunks = nr * cpr;
+        int64_t blocks = (nchunks + 256 * U - 1) / (256 * U);
+        blocks = blocks < 32768 ? blocks : 32768;
+        const void* sp = reinterpret_cast<const char*>(src) + r0 * ld * (BF16 ? 2 : 4);
+        uint8_t* cp = codes + (F::PACKED7 ? r0 * (cols / 32) * 28 : r0 * cols);
+        int8_t* scp = scales + r0 * (cols / 32);
+        hipLaunchKernelGGL((quantize_rows_kernel<F, BF16, U, true, true>), dim3(blocks), dim3(256), 0, s, sp,
+                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, cp, scp, fidx);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <class F>
 hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                       int fidx, void* codes, int8_t* scales, hipStream_t s) {
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    if (axis == 1) {
+        return dtype == 1 ? launch_rows<F, true>(src, rows, cols, ld, fidx, cp, scales, s)
+                          : launch_rows<F, false>(src, rows, cols, ld, fidx, cp, scales, s);
+    }
     const int threads = 256;
-    const int64_t work = axis == 1 ? rows * (cols / 32) * 4 : (rows / 32) * cols;
+    const int64_t work = (rows / 32) * cols;
     int64_t blocks = (work + threads - 1) / threads;
     blocks = blocks < 8192 ? blocks : 8192;
     if (blocks < 1) blocks = 1;
-    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
-    if (axis == 1) {
-        if (dtype == 1)
-            hipLaunchKernelGGL((quantize_rows_kernel<F, true>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-        else
-            hipLaunchKernelGGL((quantize_rows_kernel<F, false>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-    } else {
-        if (dtype == 1)
-            hipLaunchKernelGGL((quantize_cols_kernel<F, true>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-        else
-            hipLaunchKernelGGL((quantize_cols_kernel<F, false>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-    }
+    if (dtype == 1)
+        hipLaunchKernelGGL((quantize_cols_kernel<F, true>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
+    else
+        hipLaunchKernelGGL((quantize_cols_kernel<F, false>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
     return hipGetLastError();
 }
 
