@@ -38,7 +38,124 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 256 MiB device copy three times (counter calibration)")
+    p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="print the traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
+                        "of this script with --copy-calibration, then exit")
     return p.parse_args()
+
+
+COPY_BYTES = 256 << 20
+KERNEL_SOURCES = ("gemm.hip", "curvefp_internal.hpp", "device_util.hpp")
+
+
+def kernel_source_digest() -> str:
+    """sha256 over the GEMM kernel's sources: the traffic figure is void once they change."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_10010_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", f"gemm_{workload}_traffic.md")
+
+
+def pmc_per_dispatch(d: str, counter: str):
+    """Mean per dispatch of `counter` (summed over its instances) for the GEMM and copy kernels."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    per = {}
+    copy_grid = 0
+    rows = []
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            kind = "gemm" if "gemm_kernel" in name else ("copy" if "copyBuffer" in name else None)
+            if kind is None:
+                continue
+            rows.append((kind, r))
+            if kind == "copy":
+                copy_grid = max(copy_grid, int(r["Grid_Size"]))
+    # the calibration copies are the largest copy dispatches (the others stage small inputs)
+    seen = set()
+    for kind, r in rows:
+        if kind == "copy" and int(r["Grid_Size"]) != copy_grid:
+            continue
+        key = (kind, r["Dispatch_Id"])
+        inst = (key, r.get("Counter_Value"), r.get("Start_Timestamp"))
+        if inst in seen:      # the same record repeated
+            continue
+        seen.add(inst)
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for kind in ("gemm", "copy"):
+        vals = [v for (k, _), v in per.items() if k == kind]
+        if not vals:
+            raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
+        out[kind] = (sum(vals) / len(vals), len(vals))
+    return out
+
+
+def summarize_pmc(args):
+    fetch = pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE")
+    write = pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE")
+    # KiB the counter reads per byte a plain copy moves (read and written once each)
+    f_fetch = fetch["copy"][0] * 1024.0 / COPY_BYTES
+    f_write = write["copy"][0] * 1024.0 / COPY_BYTES
+    gemm_fetch = fetch["gemm"][0] * 1024.0 / f_fetch
+    gemm_write = write["gemm"][0] * 1024.0 / f_write
+    lines = [
+        f"# HBM traffic of the CurveFP GEMM kernel, {args.workload} workload",
+        "",
+        "Commands (from the repository root on one MI355X; each pass is its own run):",
+        "",
+        "```",
+        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o pmc -- "
+        "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration",
+        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o pmc -- "
+        "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration",
+        "python bench.py --summarize-pmc gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        "```",
+        "",
+        "| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |",
+        "|---|---|---|---|",
+        f"| `gemm_kernel` | {fetch['gemm'][1]} | {fetch['gemm'][0]:.1f} | {write['gemm'][0]:.1f} |",
+        f"| `__amd_rocclr_copyBuffer` ({COPY_BYTES >> 20} MiB copy) | {fetch['copy'][1]} | "
+        f"{fetch['copy'][0]:.1f} | {write['copy'][0]:.1f} |",
+        "",
+        f"Calibration: the copy reads and writes {COPY_BYTES >> 20} MiB once each; the counters "
+        f"report {f_fetch:.4f}x (FETCH_SIZE) and {f_write:.4f}x (WRITE_SIZE) those bytes, and the "
+        f"GEMM's counts are divided by the same factors.",
+        f"GEMM HBM traffic per launch: {gemm_fetch / 1e6:.2f} MB read + {gemm_write / 1e6:.2f} MB written.",
+        "",
+        f"traffic_bytes_per_launch={gemm_fetch + gemm_write:.0f}",
+        f"fetch_bytes_per_launch={gemm_fetch:.0f}",
+        f"write_bytes_per_launch={gemm_write:.0f}",
+        f"kernel_source_sha256={kernel_source_digest()}",
+    ]
+    print("\n".join(lines))
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per GEMM launch from the committed counter summary, or None when there is none
+    or the kernel sources changed since it was taken."""
+    try:
+        text = open(traffic_file(workload)).read()
+    except OSError:
+        return None
+    kv = dict(l.split("=", 1) for l in text.splitlines() if "=" in l and " " not in l.split("=", 1)[0])
+    if kv.get("kernel_source_sha256") != kernel_source_digest():
+        return None
+    return float(kv["traffic_bytes_per_launch"])
 
 
 def quantize_bytes_per_elem(fmt: str, dtype: str) -> float:
@@ -71,12 +188,16 @@ def cpu_baseline(w, seconds: float):
         oracle.dequantize(ca, sa, f)
         return time.perf_counter() - t0
 
+    # grow the sample until one run takes about `seconds` (at most the whole workload)
     ra, rb = 16, 64
     t = run(ra, rb)
-    scale = max(1.0, (seconds / max(t, 1e-3)) ** 0.5)
-    ra = int(min(w.M, max(16, ra * scale)))
-    rb = int(min(w.N, max(64, rb * scale)))
-    t = run(ra, rb)
+    for _ in range(4):
+        if t >= 0.6 * seconds or (ra >= w.M and rb >= w.N):
+            break
+        scale = min(8.0, max(1.2, (seconds / max(t, 1e-3)) ** 0.5))
+        ra = int(min(w.M, max(16, ra * scale)))
+        rb = int(min(w.N, max(64, rb * scale)))
+        t = run(ra, rb)
     flops = 2.0 * ra * rb * w.K
     return {
         "value": flops / t / 1e12,
@@ -92,6 +213,9 @@ def cpu_baseline(w, seconds: float):
 
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(args)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
@@ -189,7 +313,7 @@ def main():
             "peak": F16_DENSE_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": gemm_tflops / F16_DENSE_PEAK_TFLOPS,
-            "traffic": None,
+            "traffic": measured_traffic(args.workload),
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
@@ -200,6 +324,14 @@ def main():
         },
         "dequantize_gbps": dq_bytes / (per["dequantize"] * 1e-3) / 1e9,
     }
+
+    if args.copy_calibration:
+        xc = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)
+        yc = torch.empty_like(xc)
+        for _ in range(3):
+            yc.copy_(xc)
+        torch.cuda.synchronize()
+        del xc, yc
 
     if not args.no_stream:
         # streaming quantize: 32768 x 16384 bf16 (1 GiB source) -> E4C3, larger than the MALL

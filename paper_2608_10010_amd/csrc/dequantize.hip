@@ -7,6 +7,7 @@
 // 2^{k/K} is rounded once at the subnormal position.  HBM-bound: one byte (or 7
 // bits) and 1/32 scale byte read, four bytes written per element.
 #include "curvefp_internal.hpp"
+#include "device_util.hpp"
 
 #include <cstring>
 
@@ -55,69 +56,105 @@ __device__ __forceinline__ uint32_t value_bits(uint32_t code, int a, const uint3
     return bits | (s << 31);
 }
 
-template <class F>
+// chunk g = 8 consecutive codes: chunk g mod cpr of row g / cpr, block g / 4 (blocks are
+// contiguous in the code and scale arrays).  U chunks per thread, 256 chunks apart.
+template <class F, int U>
 __global__ __launch_bounds__(256) void dequantize_kernel(
-    const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, int64_t outer, int64_t k,
-    float* __restrict__ dst, int64_t ld, int fidx) {
+    const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
+    Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx) {
     __shared__ uint32_t mant[8];
     __shared__ uint64_t sig[8];
     if (threadIdx.x < 8) {
         mant[threadIdx.x] = g_mant[fidx][threadIdx.x];
         sig[threadIdx.x] = g_sig62[fidx][threadIdx.x];
     }
+    const bool dense = ld == (int64_t)cpr * 8;
+    const uint32_t g0 = blockIdx.x * (256u * U) + threadIdx.x;
+    // the codes and scales of all U chunks are requested before the table barrier
+    uint32_t w[U][3];
+    int a[U];
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+        const uint32_t g = g0 + 256u * u;
+        if (g < nchunks) {
+            const uint32_t b = g >> 2;
+            if (!F::PACKED7) {
+                const uint2 v = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
+                w[u][0] = v.x;
+                w[u][1] = v.y;
+                w[u][2] = 0;
+            } else {
+                // bytes [7 part, 7 part + 7) of the block's 28 bytes, from the dwords that hold them
+                const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + (uint64_t)b * 28);
+                const int part = (int)(g & 3);
+                const int d0 = (7 * part) >> 2;
+                w[u][0] = base[d0];
+                w[u][1] = base[d0 + 1];
+                // parts 1 and 2 (bytes 7..13 and 14..20) straddle three dwords, parts 0 and 3 two
+                w[u][2] = (part == 1 || part == 2) ? base[d0 + 2] : 0u;
+            }
+            a[u] = scales[b];
+        }
+    }
     __syncthreads();
-    const int64_t bpr = k / 32;
-    const int64_t nthreads = outer * bpr * 4;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < nthreads; g += stride) {
-        const int64_t b = g >> 2;
-        const int part = (int)(g & 3);
-        const int64_t r = b / bpr;
-        const int64_t cb = b - r * bpr;
-        const int a = scales[b];
+#pragma unroll
+    for (int u = 0; u < U; u++) {
+        const uint32_t g = g0 + 256u * u;
+        if (g >= nchunks) continue;
         uint32_t c[8];
         if (!F::PACKED7) {
-            const uint2 w = *reinterpret_cast<const uint2*>(codes + r * k + cb * 32 + part * 8);
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                c[i] = (w.x >> (8 * i)) & 0xFFu;
-                c[4 + i] = (w.y >> (8 * i)) & 0xFFu;
+                c[i] = (w[u][0] >> (8 * i)) & 0xFFu;
+                c[4 + i] = (w[u][1] >> (8 * i)) & 0xFFu;
             }
         } else {
-            // bytes [7 part, 7 part + 7) of this block's 28 bytes
-            const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + b * 28);
-            const int d0 = (7 * part) >> 2, off = 7 * part - 4 * d0;
-            const int d_end = (7 * part + 6) >> 2;
-            const uint64_t lo = (uint64_t)base[d0] | ((uint64_t)base[d0 + 1] << 32);
-            const uint64_t hi = (d_end >= d0 + 2) ? (uint64_t)base[d0 + 2] : 0ull;
+            const int part = (int)(g & 3);
+            const int off = 7 * part - 4 * ((7 * part) >> 2);
+            const uint64_t lo = (uint64_t)w[u][0] | ((uint64_t)w[u][1] << 32);
+            const uint64_t hi = w[u][2];
             const uint64_t chunk = off ? ((lo >> (8 * off)) | (hi << (64 - 8 * off))) : lo;
 #pragma unroll
             for (int i = 0; i < 8; i++) c[i] = (uint32_t)(chunk >> (7 * i)) & 0x7Fu;
         }
         uint32_t o[8];
-        if (a == -128) {
+        if (a[u] == -128) {
 #pragma unroll
             for (int i = 0; i < 8; i++) o[i] = 0x7FC00000u;   // poisoned block
         } else {
 #pragma unroll
-            for (int i = 0; i < 8; i++) o[i] = value_bits<F>(c[i], a, mant, sig);
+            for (int i = 0; i < 8; i++) o[i] = value_bits<F>(c[i], a[u], mant, sig);
         }
-        uint4* out = reinterpret_cast<uint4*>(dst + r * ld + cb * 32 + part * 8);
-        out[0] = make_uint4(o[0], o[1], o[2], o[3]);
-        out[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        int64_t e;
+        if (dense) {
+            e = (int64_t)g * 8;
+        } else {
+            const uint32_t r = div32(g, dcpr);
+            e = (int64_t)r * ld + (int64_t)(g - r * cpr) * 8;
+        }
+        st16<true>(dst + e, o[0], o[1], o[2], o[3]);
+        st16<true>(dst + e + 4, o[4], o[5], o[6], o[7]);
     }
 }
 
 template <class F>
 hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, int64_t k, float* dst,
                       int64_t ld, int fidx, hipStream_t s) {
-    const int threads = 256;
-    int64_t blocks = (outer * (k / 32) * 4 + threads - 1) / threads;
-    blocks = blocks < 8192 ? blocks : 8192;
-    if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((dequantize_kernel<F>), dim3(blocks), dim3(threads), 0, s,
-                       reinterpret_cast<const uint8_t*>(codes), scales, outer, k, dst, ld, fidx);
-    return hipGetLastError();
+    constexpr int U = 2;
+    const int64_t cpr = k / 8;
+    const int64_t slab = ((int64_t)1 << 31) / cpr;   // 32-bit chunk indices per launch
+    const uint8_t* cp = reinterpret_cast<const uint8_t*>(codes);
+    for (int64_t r0 = 0; r0 < outer; r0 += slab) {
+        const int64_t nr = outer - r0 < slab ? outer - r0 : slab;
+        const int64_t nchunks = nr * cpr;
+        const int64_t blocks = (nchunks + 256 * U - 1) / (256 * U);
+        hipLaunchKernelGGL((dequantize_kernel<F, U>), dim3((unsigned)blocks), dim3(256), 0, s,
+                           cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / 32),
+                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 }  // namespace

@@ -73,8 +73,9 @@ constexpr int SG_VALU = 0x002, SG_MFMA = 0x008, SG_DS_RD = 0x100;
 __device__ __forceinline__ int swz(int r, int q) { return r * ROW_BYTES + 16 * (q ^ (((r >> 1) ^ (r >> 3)) & 3)); }
 
 __device__ __forceinline__ uint32_t f16_pow2_neg(int d) {
-    // bits of the fp16 value 2^-d for 0 <= d <= 24 (subnormal below 2^-14)
-    return d <= 14 ? (uint32_t)(15 - d) << 10 : 1u << (24 - d);
+    // bits of the fp16 value 2^-d for 0 <= d <= 24 (exact: subnormal below 2^-14)
+    const _Float16 m = __builtin_amdgcn_ldexph((_Float16)1.0f, -d);
+    return (uint32_t)__builtin_bit_cast(uint16_t, m);
 }
 
 template <class F>

@@ -129,55 +129,6 @@ __device__ __forceinline__ void unpack8(const uint4* v, uint32_t* mag, uint32_t*
     }
 }
 
-// quotient by an invariant divisor d >= 1 (Granlund and Montgomery, "Division by invariant
-// integers using multiplication", 1994): l = ceil(log2 d), m = floor(2^32 (2^l - d) / d) + 1,
-// n / d = (mulhi(n, m) + n) >> l for every 32-bit n
-struct Div32 {
-    uint32_t m;
-    int l;
-};
-
-__device__ __forceinline__ uint32_t div32(uint32_t n, Div32 d) {
-    return (uint32_t)(((uint64_t)__umulhi(n, d.m) + n) >> d.l);
-}
-
-Div32 make_div32(uint32_t d) {
-    int l = 0;
-    while ((1ull << l) < d) l++;
-    Div32 r;
-    r.m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
-    r.l = l;
-    return r;
-}
-
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
-template <bool NT>
-__device__ __forceinline__ uint4 ld16(const uint4* p) {
-    if (!NT) return *p;
-    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
-    return make_uint4(v.x, v.y, v.z, v.w);
-}
-
-template <bool NT>
-__device__ __forceinline__ void st4(uint32_t* p, uint32_t x) {
-    if (!NT) *p = x;
-    else __builtin_nontemporal_store(x, p);
-}
-
-template <bool NT>
-__device__ __forceinline__ void st8(uint8_t* p, uint32_t x, uint32_t y) {
-    if (!NT) {
-        *reinterpret_cast<uint2*>(p) = make_uint2(x, y);
-    } else {
-        u32x2 v;
-        v.x = x;
-        v.y = y;
-        __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
-    }
-}
-
 // quantize one chunk of 8 consecutive elements; four lanes (a quad) hold one block of 32
 template <class F, bool BF16, bool NTS, class T>
 __device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const T* lut,
@@ -350,12 +301,9 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(
     }
 }
 
-template <class F, bool BF16>
-hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
-                       int8_t* scales, hipStream_t s) {
-    // 128 (bf16) or 64 (fp32) bytes in flight per thread, streaming (non-temporal) loads and
-    // stores, at most 32768 workgroups: the shape that measured fastest on a 1 GiB stream
-    constexpr int U = BF16 ? 8 : 2;
+template <class F, bool BF16, int U>
+hipError_t launch_rows_u(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
+                         int8_t* scales, hipStream_t s) {
     const int64_t cpr = cols / 8;
     // 32-bit chunk indices: slabs of at most 2^31 chunks
     const int64_t slab = ((int64_t)1 << 31) / cpr;
@@ -373,6 +321,19 @@ hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, 
         if (e != hipSuccess) return e;
     }
     return hipSuccess;
+}
+
+// Streams of at least 2048 workgroups at 128 (bf16) or 64 (fp32) bytes in flight per thread use
+// that depth (the shape that measured fastest on a 1 GiB stream); smaller tensors use 32 bytes
+// per thread, so that they still spread over every compute unit.
+template <class F, bool BF16>
+hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
+                       int8_t* scales, hipStream_t s) {
+    constexpr int UBIG = BF16 ? 8 : 2;
+    const int64_t nchunks = rows * (cols / 8);
+    if (nchunks >= (int64_t)2048 * 256 * UBIG)
+        return launch_rows_u<F, BF16, UBIG>(src, rows, cols, ld, fidx, codes, scales, s);
+    return launch_rows_u<F, BF16, BF16 ? 2 : 1>(src, rows, cols, ld, fidx, codes, scales, s);
 }
 
 template <class F>
