@@ -57,8 +57,9 @@ __device__ __forceinline__ uint32_t value_bits(uint32_t code, int a, const uint3
 }
 
 // chunk g = 8 consecutive codes: chunk g mod cpr of row g / cpr, block g / 4 (blocks are
-// contiguous in the code and scale arrays).  U chunks per thread, 256 chunks apart.
-template <class F, int U>
+// contiguous in the code and scale arrays); a grid-stride loop over the chunks, one per thread
+// per round (a capped grid with plain stores measured fastest for this write-heavy stream)
+template <class F>
 __global__ __launch_bounds__(256) void dequantize_kernel(
     const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
     Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx) {
@@ -68,62 +69,39 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
         mant[threadIdx.x] = g_mant[fidx][threadIdx.x];
         sig[threadIdx.x] = g_sig62[fidx][threadIdx.x];
     }
-    const bool dense = ld == (int64_t)cpr * 8;
-    const uint32_t g0 = blockIdx.x * (256u * U) + threadIdx.x;
-    // the codes and scales of all U chunks are requested before the table barrier
-    uint32_t w[U][3];
-    int a[U];
-#pragma unroll
-    for (int u = 0; u < U; u++) {
-        const uint32_t g = g0 + 256u * u;
-        if (g < nchunks) {
-            const uint32_t b = g >> 2;
-            if (!F::PACKED7) {
-                const uint2 v = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
-                w[u][0] = v.x;
-                w[u][1] = v.y;
-                w[u][2] = 0;
-            } else {
-                // bytes [7 part, 7 part + 7) of the block's 28 bytes, from the dwords that hold them
-                const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + (uint64_t)b * 28);
-                const int part = (int)(g & 3);
-                const int d0 = (7 * part) >> 2;
-                w[u][0] = base[d0];
-                w[u][1] = base[d0 + 1];
-                // parts 1 and 2 (bytes 7..13 and 14..20) straddle three dwords, parts 0 and 3 two
-                w[u][2] = (part == 1 || part == 2) ? base[d0 + 2] : 0u;
-            }
-            a[u] = scales[b];
-        }
-    }
     __syncthreads();
-#pragma unroll
-    for (int u = 0; u < U; u++) {
-        const uint32_t g = g0 + 256u * u;
-        if (g >= nchunks) continue;
+    const bool dense = ld == (int64_t)cpr * 8;
+    const uint32_t stride = gridDim.x * 256u;
+    for (uint32_t g = blockIdx.x * 256u + threadIdx.x; g < nchunks; g += stride) {
+        const uint32_t b = g >> 2;
+        const int a = scales[b];
         uint32_t c[8];
         if (!F::PACKED7) {
+            const uint2 w = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
 #pragma unroll
             for (int i = 0; i < 4; i++) {
-                c[i] = (w[u][0] >> (8 * i)) & 0xFFu;
-                c[4 + i] = (w[u][1] >> (8 * i)) & 0xFFu;
+                c[i] = (w.x >> (8 * i)) & 0xFFu;
+                c[4 + i] = (w.y >> (8 * i)) & 0xFFu;
             }
         } else {
+            // bytes [7 part, 7 part + 7) of the block's 28 bytes; parts 1 and 2 (bytes 7..13 and
+            // 14..20) straddle three dwords, parts 0 and 3 two
+            const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + (uint64_t)b * 28);
             const int part = (int)(g & 3);
-            const int off = 7 * part - 4 * ((7 * part) >> 2);
-            const uint64_t lo = (uint64_t)w[u][0] | ((uint64_t)w[u][1] << 32);
-            const uint64_t hi = w[u][2];
+            const int d0 = (7 * part) >> 2, off = 7 * part - 4 * d0;
+            const uint64_t lo = (uint64_t)base[d0] | ((uint64_t)base[d0 + 1] << 32);
+            const uint64_t hi = (part == 1 || part == 2) ? (uint64_t)base[d0 + 2] : 0ull;
             const uint64_t chunk = off ? ((lo >> (8 * off)) | (hi << (64 - 8 * off))) : lo;
 #pragma unroll
             for (int i = 0; i < 8; i++) c[i] = (uint32_t)(chunk >> (7 * i)) & 0x7Fu;
         }
         uint32_t o[8];
-        if (a[u] == -128) {
+        if (a == -128) {
 #pragma unroll
             for (int i = 0; i < 8; i++) o[i] = 0x7FC00000u;   // poisoned block
         } else {
 #pragma unroll
-            for (int i = 0; i < 8; i++) o[i] = value_bits<F>(c[i], a[u], mant, sig);
+            for (int i = 0; i < 8; i++) o[i] = value_bits<F>(c[i], a, mant, sig);
         }
         int64_t e;
         if (dense) {
@@ -132,23 +110,24 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
             const uint32_t r = div32(g, dcpr);
             e = (int64_t)r * ld + (int64_t)(g - r * cpr) * 8;
         }
-        st16<true>(dst + e, o[0], o[1], o[2], o[3]);
-        st16<true>(dst + e + 4, o[4], o[5], o[6], o[7]);
+        uint4* out = reinterpret_cast<uint4*>(dst + e);
+        out[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        out[1] = make_uint4(o[4], o[5], o[6], o[7]);
     }
 }
 
 template <class F>
 hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, int64_t k, float* dst,
                       int64_t ld, int fidx, hipStream_t s) {
-    constexpr int U = 2;
     const int64_t cpr = k / 8;
     const int64_t slab = ((int64_t)1 << 31) / cpr;   // 32-bit chunk indices per launch
     const uint8_t* cp = reinterpret_cast<const uint8_t*>(codes);
     for (int64_t r0 = 0; r0 < outer; r0 += slab) {
         const int64_t nr = outer - r0 < slab ? outer - r0 : slab;
         const int64_t nchunks = nr * cpr;
-        const int64_t blocks = (nchunks + 256 * U - 1) / (256 * U);
-        hipLaunchKernelGGL((dequantize_kernel<F, U>), dim3((unsigned)blocks), dim3(256), 0, s,
+        int64_t blocks = (nchunks + 255) / 256;
+        blocks = blocks < 8192 ? blocks : 8192;
+        hipLaunchKernelGGL((dequantize_kernel<F>), dim3((unsigned)blocks), dim3(256), 0, s,
                            cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / 32),
                            (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx);
         const hipError_t e = hipGetLastError();

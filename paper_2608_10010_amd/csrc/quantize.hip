@@ -240,28 +240,32 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
     }
 }
 
-// quantize-transpose: one thread per (column, block of 32 rows)
-template <class F, bool BF16>
+// quantize-transpose: thread g takes column g mod cols and R consecutive blocks of 32 rows
+// (row group g / cols), so the loads of a wave read one contiguous span of a source row and
+// each thread writes R * 32 contiguous code bytes (R * 28 for E3C3) and R scales
+template <class F, bool BF16, int R>
 __global__ __launch_bounds__(256) void quantize_cols_kernel(
-    const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld,
+    const void* __restrict__ src, uint32_t nthreads, uint32_t cols, Div32 dcols, int64_t rows, int64_t ld,
     uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
     __shared__ uint32_t lut[F::QLUT_SIZE];
     for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
     const uint32_t lmax_mant = g_lmax_mant[fidx];
     __syncthreads();
 
+    const uint32_t g = blockIdx.x * 256u + threadIdx.x;
+    if (g >= nthreads) return;
+    const uint32_t rg = div32(g, dcols);
+    const uint32_t c = g - rg * cols;
     const int64_t rblocks = rows / 32;
-    const int64_t total = rblocks * cols;
-    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; g < total; g += stride) {
-        const int64_t rb = g / cols;
-        const int64_t c = g - rb * cols;
+#pragma unroll 1
+    for (int t = 0; t < R; t++) {
+        const int64_t rb = (int64_t)rg * R + t;
         uint32_t mag[32], sgn[32];
 #pragma unroll
         for (int i = 0; i < 32; i++) {
             const int64_t e = (rb * 32 + i) * ld + c;
-            uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[e] << 16)
-                              : reinterpret_cast<const uint32_t*>(src)[e];
+            const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[e] << 16)
+                                    : reinterpret_cast<const uint32_t*>(src)[e];
             mag[i] = w & 0x7FFFFFFFu;
             sgn[i] = w >> 31;
         }
@@ -275,29 +279,28 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(
 #pragma unroll
         for (int i = 0; i < 32; i++) cc[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
         if (!F::PACKED7) {
-            uint4* o = reinterpret_cast<uint4*>(codes + c * rows + rb * 32);
+            uint8_t* o = codes + (int64_t)c * rows + rb * 32;
 #pragma unroll
             for (int q = 0; q < 2; q++) {
-                uint4 v;
-                v.x = cc[16 * q + 0] | (cc[16 * q + 1] << 8) | (cc[16 * q + 2] << 16) | (cc[16 * q + 3] << 24);
-                v.y = cc[16 * q + 4] | (cc[16 * q + 5] << 8) | (cc[16 * q + 6] << 16) | (cc[16 * q + 7] << 24);
-                v.z = cc[16 * q + 8] | (cc[16 * q + 9] << 8) | (cc[16 * q + 10] << 16) | (cc[16 * q + 11] << 24);
-                v.w = cc[16 * q + 12] | (cc[16 * q + 13] << 8) | (cc[16 * q + 14] << 16) | (cc[16 * q + 15] << 24);
-                o[q] = v;
+                const uint32_t* k = cc + 16 * q;
+                st16<true>(o + 16 * q, k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24),
+                           k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24),
+                           k[8] | (k[9] << 8) | (k[10] << 16) | (k[11] << 24),
+                           k[12] | (k[13] << 8) | (k[14] << 16) | (k[15] << 24));
             }
         } else {
             uint32_t w[7] = {0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
             for (int i = 0; i < 32; i++) {
-                const int bit = 7 * i, d = bit >> 5, s = bit & 31;
-                w[d] |= cc[i] << s;
-                if (s > 25) w[d + 1] |= cc[i] >> (32 - s);
+                const int bit = 7 * i, d = bit >> 5, sh = bit & 31;
+                w[d] |= cc[i] << sh;
+                if (sh > 25) w[d + 1] |= cc[i] >> (32 - sh);
             }
-            uint32_t* o = reinterpret_cast<uint32_t*>(codes + (c * rblocks + rb) * 28);
+            uint32_t* o = reinterpret_cast<uint32_t*>(codes + ((int64_t)c * rblocks + rb) * 28);
 #pragma unroll
-            for (int d = 0; d < 7; d++) o[d] = w[d];
+            for (int d = 0; d < 7; d++) st4<true>(o + d, w[d]);
         }
-        scales[c * rblocks + rb] = (int8_t)a;
+        scales[(int64_t)c * rblocks + rb] = (int8_t)a;
     }
 }
 
@@ -336,6 +339,144 @@ hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, 
     return launch_rows_u<F, BF16, BF16 ? 2 : 1>(src, rows, cols, ld, fidx, codes, scales, s);
 }
 
+// quantize-transpose through LDS: a workgroup takes 128 rows (four blocks) x 64 columns.  The
+// tile is read with 16-byte loads along the source rows, each thread then quantizes one
+// column's block of 32 from LDS (a wave reads one contiguous row segment per step), and the
+// codes go back through LDS so every column's 128 code bytes (112 for E3C3) leave as whole
+// 16-byte stores.  Needs rows % 128 == 0, cols % 8 == 0 and a 16-byte aligned source.
+constexpr int TT_ROWS = 128, TT_COLS = 64;
+constexpr int TT_OUT_STRIDE = 144;   // 128 code bytes + 16: the 16-byte writes of a wave spread over the banks
+
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
+    const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld,
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int SEG = TT_COLS * ESZ / 16;            // 16-byte pieces per tile row
+    __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
+    __shared__ __attribute__((aligned(16))) char tile[TT_ROWS * TT_COLS * ESZ];
+    __shared__ __attribute__((aligned(16))) uint8_t outb[TT_COLS * TT_OUT_STRIDE];
+    __shared__ int8_t scl[TT_COLS * 4];
+
+    const int tid = threadIdx.x;
+    const int64_t c0 = (int64_t)blockIdx.x * TT_COLS, r0 = (int64_t)blockIdx.y * TT_ROWS;
+    const char* s8 = reinterpret_cast<const char*>(src);
+    // phase 1: the tile, 16 bytes per load (columns past the end are not read)
+    uint4 v[TT_ROWS * SEG / 256];
+#pragma unroll
+    for (int k = 0; k < TT_ROWS * SEG / 256; k++) {
+        const int piece = tid + 256 * k, row = piece / SEG, seg = piece % SEG;
+        const int64_t col = c0 + seg * (16 / ESZ);
+        v[k] = col < cols ? ld16<true>(reinterpret_cast<const uint4*>(s8 + ((r0 + row) * ld + col) * ESZ))
+                          : make_uint4(0, 0, 0, 0);
+    }
+    if (BF16) {
+        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(g_qlut8[fidx]);
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lut);
+        for (int i = tid; i < F::QLUT_SIZE / 4; i += 256) l32[i] = s32[i];
+    } else {
+        for (int i = tid; i < F::QLUT_SIZE; i += 256) lut[i] = (T)g_qlut[fidx][i];
+    }
+    const uint32_t lmax_mant = g_lmax_mant[fidx];
+#pragma unroll
+    for (int k = 0; k < TT_ROWS * SEG / 256; k++)
+        *reinterpret_cast<uint4*>(tile + (tid + 256 * k) * 16) = v[k];
+    __syncthreads();
+
+    // phase 2: thread = (column j, block b)
+    const int j = tid & (TT_COLS - 1), b = tid >> 6;
+    uint32_t mag[32], sgn[32];
+#pragma unroll
+    for (int i = 0; i < 32; i++) {
+        const int e = (b * 32 + i) * TT_COLS + j;
+        const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(tile)[e] << 16)
+                                : reinterpret_cast<const uint32_t*>(tile)[e];
+        mag[i] = w & 0x7FFFFFFFu;
+        sgn[i] = w >> 31;
+    }
+    uint32_t amax = 0;
+#pragma unroll
+    for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
+    const int a = scale_of<F>(amax, lmax_mant);
+    uint32_t rk[32];
+    ranks_of<F>(mag, 32, a, lut, rk);
+    uint32_t cc[32];
+#pragma unroll
+    for (int i = 0; i < 32; i++) cc[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
+    uint8_t* ob = outb + j * TT_OUT_STRIDE;
+    if (!F::PACKED7) {
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+            const uint32_t* k = cc + 16 * q;
+            *reinterpret_cast<uint4*>(ob + b * 32 + 16 * q) =
+                make_uint4(k[0] | (k[1] << 8) | (k[2] << 16) | (k[3] << 24),
+                           k[4] | (k[5] << 8) | (k[6] << 16) | (k[7] << 24),
+                           k[8] | (k[9] << 8) | (k[10] << 16) | (k[11] << 24),
+                           k[12] | (k[13] << 8) | (k[14] << 16) | (k[15] << 24));
+        }
+    } else {
+        uint32_t w[7] = {0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < 32; i++) {
+            const int bit = 7 * i, d = bit >> 5, sh = bit & 31;
+            w[d] |= cc[i] << sh;
+            if (sh > 25) w[d + 1] |= cc[i] >> (32 - sh);
+        }
+#pragma unroll
+        for (int d = 0; d < 7; d++) *reinterpret_cast<uint32_t*>(ob + b * 28 + 4 * d) = w[d];
+    }
+    scl[j * 4 + b] = (int8_t)a;
+    __syncthreads();
+
+    // phase 3: each column's code bytes for the four blocks are contiguous in the output
+    constexpr int CB = F::PACKED7 ? 4 * 28 : 128;   // code bytes per column and tile
+    const int64_t rblocks = rows / 32;
+#pragma unroll
+    for (int k = 0; k < (TT_COLS * CB / 16 + 255) / 256; k++) {
+        const int piece = tid + 256 * k;
+        if (piece < TT_COLS * CB / 16) {
+            const int jj = piece / (CB / 16), qq = piece % (CB / 16);
+            const int64_t col = c0 + jj;
+            if (col < cols) {
+                const uint4 x = *reinterpret_cast<const uint4*>(outb + jj * TT_OUT_STRIDE + 16 * qq);
+                uint8_t* dst = F::PACKED7 ? codes + (col * rblocks + r0 / 32) * 28 : codes + col * rows + r0;
+                st16<true>(dst + 16 * qq, x.x, x.y, x.z, x.w);
+            }
+        }
+    }
+    {
+        const int jj = tid >> 2, bb = tid & 3;
+        if (c0 + jj < cols) scales[(c0 + jj) * rblocks + r0 / 32 + bb] = scl[jj * 4 + bb];
+    }
+}
+
+template <class F, int R>
+hipError_t launch_cols(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int fidx,
+                       uint8_t* codes, int8_t* scales, hipStream_t s) {
+    // column slabs keep the thread count of one launch below 2^31
+    const int64_t groups = rows / (32 * R);
+    const int64_t slab = ((int64_t)1 << 31) / groups;
+    for (int64_t c0 = 0; c0 < cols; c0 += slab) {
+        const int64_t nc = cols - c0 < slab ? cols - c0 : slab;
+        const int64_t nthreads = groups * nc;
+        const int64_t blocks = (nthreads + 255) / 256;
+        const int64_t esz = dtype == 1 ? 2 : 4;
+        const void* sp = reinterpret_cast<const char*>(src) + c0 * esz;
+        uint8_t* cp = codes + (F::PACKED7 ? c0 * (rows / 32) * 28 : c0 * rows);
+        int8_t* scp = scales + c0 * (rows / 32);
+        if (dtype == 1)
+            hipLaunchKernelGGL((quantize_cols_kernel<F, true, R>), dim3((unsigned)blocks), dim3(256), 0, s, sp,
+                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx);
+        else
+            hipLaunchKernelGGL((quantize_cols_kernel<F, false, R>), dim3((unsigned)blocks), dim3(256), 0, s, sp,
+                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+}
+
 template <class F>
 hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                       int fidx, void* codes, int8_t* scales, hipStream_t s) {
@@ -344,16 +485,18 @@ hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, in
         return dtype == 1 ? launch_rows<F, true>(src, rows, cols, ld, fidx, cp, scales, s)
                           : launch_rows<F, false>(src, rows, cols, ld, fidx, cp, scales, s);
     }
-    const int threads = 256;
-    const int64_t work = (rows / 32) * cols;
-    int64_t blocks = (work + threads - 1) / threads;
-    blocks = blocks < 8192 ? blocks : 8192;
-    if (blocks < 1) blocks = 1;
-    if (dtype == 1)
-        hipLaunchKernelGGL((quantize_cols_kernel<F, true>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-    else
-        hipLaunchKernelGGL((quantize_cols_kernel<F, false>), dim3(blocks), dim3(threads), 0, s, src, rows, cols, ld, cp, scales, fidx);
-    return hipGetLastError();
+    const int64_t esz = dtype == 1 ? 2 : 4;
+    const bool tiled = rows % TT_ROWS == 0 && cols % 8 == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                       (ld * esz) % 16 == 0 && rows / TT_ROWS <= 65535;
+    if (tiled) {
+        const dim3 grid((unsigned)((cols + TT_COLS - 1) / TT_COLS), (unsigned)(rows / TT_ROWS));
+        if (dtype == 1)
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, cp, scales, fidx);
+        else
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, cp, scales, fidx);
+        return hipGetLastError();
+    }
+    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, s);
 }
 
 }  // namespace

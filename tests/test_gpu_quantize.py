@@ -33,10 +33,11 @@ def run_and_compare(x: np.ndarray, fmt: str, dtype: str, axis: int, what: str, l
 
 @pytest.mark.parametrize("fmt", FMTS)
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("axis", [1, 0])
-def test_random(fmt, dtype, axis):
+@pytest.mark.parametrize("axis,shape", [(1, (37, 352)), (0, (160, 45)), (0, (384, 45)), (0, (256, 72))])
+def test_random(fmt, dtype, axis, shape):
+    # axis 0: (160, 45) and (384, 45) take the one-thread-per-block path; (256, 72) the LDS-tiled
+    # one (rows % 128 == 0, cols % 8 == 0), with a last tile of 8 columns
     rng = np.random.default_rng(11)
-    shape = (37, 352) if axis == 1 else (160, 45)
     x = (rng.standard_normal(shape) * np.exp2(rng.uniform(-30, 30, (shape[0], 1)))).astype(np.float32)
     run_and_compare(x, fmt, dtype, axis, "random")
 
