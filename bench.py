@@ -8,8 +8,11 @@ outlier channels x20; weights 4096 x 4096 bf16 N(0, 0.02), both block 32):
 
 Prints one JSON line.  `value` is whole-step throughput in GEMM TFLOP/s
 (2 M N K per step over the measured step time, inputs resident in HBM).
-Per-kernel times come from HIP events recorded on the stream the library
-launches on.  The roofline object is for the GEMM kernel (the dominant one).
+The GEMM is curvefp_gemm_ws by default (codes expanded once into a workspace
+that is allocated before the timed region, like C); --gemm fused times the
+allocation-free curvefp_gemm instead.  Per-call times come from HIP events
+recorded on the stream the library launches on.  The roofline object is for the
+GEMM call (the dominant part: its expansion and GEMM kernels together).
 A separate streaming quantize case (1 GiB bf16 source, larger than the 256 MB
 Infinity Cache) gives the HBM figure for the quantizer.  The CPU oracle is timed
 on a bounded row sample of the same workload as `cpu_baseline`.
@@ -35,6 +38,10 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default="inference")
+    p.add_argument("--gemm", choices=["ws", "fused"], default="ws",
+                   help="ws: curvefp_gemm_ws with a workspace allocated before the timed region "
+                        "(codes expanded once, then the GEMM); fused: curvefp_gemm (expansion inside "
+                        "the GEMM kernel, no workspace)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -60,12 +67,18 @@ def kernel_source_digest() -> str:
     return h.hexdigest()
 
 
-def traffic_file(workload: str) -> str:
-    return os.path.join(ROOT, "profiles", f"gemm_{workload}_traffic.md")
+def traffic_file(workload: str, path: str = "ws") -> str:
+    return os.path.join(ROOT, "profiles", f"gemm_{path}_{workload}_traffic.md")
 
 
-def pmc_per_dispatch(d: str, counter: str):
-    """Mean per dispatch of `counter` (summed over its instances) for the GEMM and copy kernels."""
+# the kernels one GEMM call launches, by path
+CALL_KERNELS = {"ws": ("prep_kernel", "expand_kernel", "gemm_ws_kernel"),
+                "fused": ("zero_rows_kernel", "gemm_kernel")}
+
+
+def pmc_per_dispatch(d: str, counter: str, path: str):
+    """Mean per dispatch of `counter` (summed over its instances) for each kernel of one GEMM call
+    and for the calibration copy; "gemm" is their sum (bytes of one whole call)."""
     import csv
     import glob
     files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
@@ -79,7 +92,9 @@ def pmc_per_dispatch(d: str, counter: str):
             if r["Counter_Name"] != counter:
                 continue
             name = r["Kernel_Name"]
-            kind = "gemm" if "gemm_kernel" in name else ("copy" if "copyBuffer" in name else None)
+            kind = next((k for k in CALL_KERNELS[path] if k + "<" in name or k + "(" in name), None)
+            if kind is None and "copyBuffer" in name:
+                kind = "copy"
             if kind is None:
                 continue
             rows.append((kind, r))
@@ -97,45 +112,55 @@ def pmc_per_dispatch(d: str, counter: str):
         seen.add(inst)
         per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
     out = {}
-    for kind in ("gemm", "copy"):
+    for kind in CALL_KERNELS[path] + ("copy",):
         vals = [v for (k, _), v in per.items() if k == kind]
         if not vals:
+            if kind == "zero_rows_kernel":      # launched only when K is split
+                out[kind] = (0.0, 0)
+                continue
             raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
         out[kind] = (sum(vals) / len(vals), len(vals))
+    out["gemm"] = (sum(out[k][0] for k in CALL_KERNELS[path]), max(out[k][1] for k in CALL_KERNELS[path]))
     return out
 
 
 def summarize_pmc(args):
-    fetch = pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE")
-    write = pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE")
+    fetch = pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE", args.gemm)
+    write = pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE", args.gemm)
     # KiB the counter reads per byte a plain copy moves (read and written once each)
     f_fetch = fetch["copy"][0] * 1024.0 / COPY_BYTES
     f_write = write["copy"][0] * 1024.0 / COPY_BYTES
     gemm_fetch = fetch["gemm"][0] * 1024.0 / f_fetch
     gemm_write = write["gemm"][0] * 1024.0 / f_write
+    kernels = CALL_KERNELS[args.gemm]
+    flag = "" if args.gemm == "ws" else " --gemm fused"
     lines = [
-        f"# HBM traffic of the CurveFP GEMM kernel, {args.workload} workload",
+        f"# HBM traffic of one CurveFP GEMM call ({args.gemm} path), {args.workload} workload",
         "",
         "Commands (from the repository root on one MI355X; each pass is its own run):",
         "",
         "```",
-        "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o pmc -- "
-        "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration",
-        "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o pmc -- "
-        "python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration",
-        "python bench.py --summarize-pmc gpurun_out/pmc_fetch gpurun_out/pmc_write",
+        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_{args.gemm} -o pmc -- "
+        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration --gemm {args.gemm}",
+        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_{args.gemm} -o pmc -- "
+        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration --gemm {args.gemm}",
+        f"python bench.py --summarize-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}{flag}",
         "```",
         "",
         "| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |",
         "|---|---|---|---|",
-        f"| `gemm_kernel` | {fetch['gemm'][1]} | {fetch['gemm'][0]:.1f} | {write['gemm'][0]:.1f} |",
+    ]
+    for k in kernels:
+        lines.append(f"| `{k}` | {fetch[k][1]} | {fetch[k][0]:.1f} | {write[k][0]:.1f} |")
+    lines += [
+        f"| one GEMM call (sum) | {fetch['gemm'][1]} | {fetch['gemm'][0]:.1f} | {write['gemm'][0]:.1f} |",
         f"| `__amd_rocclr_copyBuffer` ({COPY_BYTES >> 20} MiB copy) | {fetch['copy'][1]} | "
         f"{fetch['copy'][0]:.1f} | {write['copy'][0]:.1f} |",
         "",
         f"Calibration: the copy reads and writes {COPY_BYTES >> 20} MiB once each; the counters "
         f"report {f_fetch:.4f}x (FETCH_SIZE) and {f_write:.4f}x (WRITE_SIZE) those bytes, and the "
         f"GEMM's counts are divided by the same factors.",
-        f"GEMM HBM traffic per launch: {gemm_fetch / 1e6:.2f} MB read + {gemm_write / 1e6:.2f} MB written.",
+        f"HBM traffic per GEMM call: {gemm_fetch / 1e6:.2f} MB read + {gemm_write / 1e6:.2f} MB written.",
         "",
         f"traffic_bytes_per_launch={gemm_fetch + gemm_write:.0f}",
         f"fetch_bytes_per_launch={gemm_fetch:.0f}",
@@ -145,11 +170,11 @@ def summarize_pmc(args):
     print("\n".join(lines))
 
 
-def measured_traffic(workload: str):
-    """HBM bytes per GEMM launch from the committed counter summary, or None when there is none
+def measured_traffic(workload: str, path: str):
+    """HBM bytes per GEMM call from the committed counter summary, or None when there is none
     or the kernel sources changed since it was taken."""
     try:
-        text = open(traffic_file(workload)).read()
+        text = open(traffic_file(workload, path)).read()
     except OSError:
         return None
     kv = dict(l.split("=", 1) for l in text.splitlines() if "=" in l and " " not in l.split("=", 1)[0])
@@ -243,6 +268,14 @@ def main():
     cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
     C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
     D = torch.empty((outer_a, ka), dtype=torch.float32, device=dev)
+    # the workspace is allocated once, like C: the timed calls only use it
+    ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if args.gemm == "ws" else None
+
+    def gemm():
+        if args.gemm == "ws":
+            cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws)
+        else:
+            cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
     def step(ev=None):
         if ev is not None:
@@ -253,7 +286,7 @@ def main():
         cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb)
         if ev is not None:
             ev[2].record(stream)
-        cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
+        gemm()
         if ev is not None:
             ev[3].record(stream)
         cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D)
@@ -304,16 +337,18 @@ def main():
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
             "step": "quantize(act) + quantize(weight) + gemm + dequantize(act codes)",
             "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
+            "gemm_path": ("curvefp_gemm_ws: codes expanded once into a workspace, then the GEMM"
+                          if args.gemm == "ws" else "curvefp_gemm: expansion inside the GEMM kernel"),
             "parallelism": "single GPU",
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm",
+            "kernel": "gemm call (" + ", ".join(CALL_KERNELS[args.gemm]) + ")",
             "achieved": gemm_tflops,
             "peak": F16_DENSE_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": gemm_tflops / F16_DENSE_PEAK_TFLOPS,
-            "traffic": measured_traffic(args.workload),
+            "traffic": measured_traffic(args.workload, args.gemm),
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},

@@ -127,14 +127,45 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
  * (hi.hi + hi.lo + lo.hi) accumulate in fp32, and the epilogue applies the
  * row and column scale offsets exactly.  Error: each product is represented
  * to about 2^-21 relative; elements more than ~2^-29 below their row's largest
- * element are flushed; accumulation is fp32.  Relative Frobenius error against
- * the exact phase-binned sum is about 1e-7 on the benchmark workloads.
+ * element keep fewer bits (fp16 subnormals) and those more than ~2^-39 below
+ * it are flushed; accumulation is fp32.  Relative Frobenius error against the
+ * exact phase-binned sum is about 1e-7 on the benchmark workloads.
  * Blocks with scale -128 contribute zero.
+ *
+ * This entry point allocates nothing: the expansion happens inside the GEMM
+ * kernel, once per workgroup that needs a code.  curvefp_gemm_ws below does the
+ * expansion once per code and is faster; both give the same C bit for bit.
  */
 int curvefp_gemm(const void* a_codes, const int8_t* a_scales,
                  const void* b_codes, const int8_t* b_scales,
                  int64_t M, int64_t N, int64_t K, int format, int block,
                  float* c, int64_t ldc, void* stream);
+
+/*
+ * Bytes of device workspace curvefp_gemm_ws needs for an M x N x K product
+ * (4 bytes per element of A and B with rows padded to multiples of 256, plus
+ * one int32 per padded row).  Returns CURVEFP_ERR_SHAPE for non-positive
+ * sizes or K not a multiple of 32.
+ */
+int64_t curvefp_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * The same product as curvefp_gemm (Sec. 3.3, Eq. binned-accumulation, same
+ * arguments and result, bit for bit), through a caller-owned device workspace
+ * of at least curvefp_gemm_workspace_bytes(M, N, K) bytes, 256-byte aligned.
+ * The codes of A and B are first expanded once into fp16 high/low planes in
+ * the workspace; the GEMM kernel then streams those planes into LDS and spends
+ * its main loop on the matrix cores.  The workspace contents are scratch:
+ * calls that share a workspace must be ordered (same stream, or synchronized).
+ * Errors as curvefp_gemm, plus CURVEFP_ERR_NULL for a null workspace,
+ * CURVEFP_ERR_SHAPE if workspace_bytes is too small and CURVEFP_ERR_ALIGN if
+ * the workspace is not 256-byte aligned.
+ */
+int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
+                    const void* b_codes, const int8_t* b_scales,
+                    int64_t M, int64_t N, int64_t K, int format, int block,
+                    float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
+                    void* stream);
 
 /* Static description of a status code. */
 const char* curvefp_status_string(int status);

@@ -75,6 +75,10 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
                            int axis, int format, void* codes, int8_t* scales, hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
                              int64_t outer, int64_t k, float* dst, int64_t ld_dst, hipStream_t s);
+// workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)
+int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
+hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
+                          int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s);
 hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int8_t* bs,
                        int64_t M, int64_t N, int64_t K, int format, float* c, int64_t ldc,
                        hipStream_t s);

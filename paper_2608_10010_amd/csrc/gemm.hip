@@ -198,6 +198,89 @@ struct Frag {
     half8 ah[TM], al[TM], bh[TN], bl[TN];
 };
 
+// epilogue of a 256 x BN_ tile: D[i][j] of MFMA tile (ti, tj) is register v of lane l with
+// j = l % 32 and i = 8 (v / 4) + 4 (l / 32) + v % 4; C = ldexp(D, alpha_i + beta_j - 2 bias)
+// (exact), stored, or added with fp32 atomics when K is split
+template <class F, int BN_>
+__device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], const int* sAlpha, const int* sBeta,
+                                           float* C, int64_t ldc, int64_t M, int64_t N, int64_t m0, int64_t n0,
+                                           int wm, int wn, int lane, bool split) {
+    constexpr int BN = BN_, WN = Tile<BN_>::WN, TN = Tile<BN_>::TN;
+    const int64_t rowsC = min((int64_t)BM, M - m0), colsC = min((int64_t)BN, N - n0);
+    if ((int64_t)BM * ldc <= ((int64_t)1 << 28)) {
+        // buffer descriptor over the tile's rows of C: stores to rows past M fall outside it and
+        // are dropped; columns past N are masked per lane (edge tiles only)
+        const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(C + m0 * ldc + n0), (short)0, (int)(((rowsC - 1) * ldc + colsC) * 4), 0x00020000);
+        const int lrow = wm * WM + 4 * (lane >> 5);
+        const int lcol = wn * WN + (lane & 31);
+        const int voff = (lrow * (int)ldc + lcol) * 4;
+        int beta[TN];
+        bool colok[TN];
+#pragma unroll
+        for (int tj = 0; tj < TN; tj++) {
+            beta[tj] = sBeta[lcol + 32 * tj] - 2 * F::GEMM_BIAS;
+            colok[tj] = lcol + 32 * tj < colsC;
+        }
+        // one straight-line store sequence per case (split or not, edge columns or not)
+        auto store_all = [&](auto split_c, auto edge_c) {
+            constexpr bool SPLIT = decltype(split_c)::value, EDGE = decltype(edge_c)::value;
+#pragma unroll
+            for (int ti = 0; ti < TM; ti++)
+#pragma unroll
+                for (int g = 0; g < 4; g++) {
+                    // row exponents of v = 4 g .. 4 g + 3 (four consecutive rows)
+                    const int4 al = *reinterpret_cast<const int4*>(sAlpha + lrow + 32 * ti + 8 * g);
+                    const int alr[4] = {al.x, al.y, al.z, al.w};
+#pragma unroll
+                    for (int r = 0; r < 4; r++) {
+                        const int soff = (32 * ti + 8 * g + r) * (int)ldc * 4;
+#pragma unroll
+                        for (int tj = 0; tj < TN; tj++) {
+                            if (EDGE && !colok[tj]) continue;
+                            const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta[tj]);
+                            if (SPLIT)
+                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(val, rc, voff + 128 * tj, soff, 0);
+                            else
+                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rc,
+                                                                      voff + 128 * tj, soff, 0);
+                        }
+                    }
+                }
+        };
+        using T = std::true_type;
+        using Fa = std::false_type;
+        const bool edge = colsC < BN;
+        if (split) {
+            if (edge) store_all(T(), T());
+            else store_all(T(), Fa());
+        } else {
+            if (edge) store_all(Fa(), T());
+            else store_all(Fa(), Fa());
+        }
+    } else {
+        // very wide C (ldc beyond 2^20): 64-bit addressing
+#pragma unroll
+        for (int ti = 0; ti < TM; ti++)
+#pragma unroll
+            for (int tj = 0; tj < TN; tj++) {
+                const int lj = wn * WN + tj * 32 + (lane & 31);
+                const int64_t gj = n0 + lj;
+                const int beta = sBeta[lj];
+#pragma unroll
+                for (int v = 0; v < 16; v++) {
+                    const int li = wm * WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+                    const int64_t gi = m0 + li;
+                    if (gi < M && gj < N) {
+                        const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                        if (split) unsafeAtomicAdd(C + gi * ldc + gj, val);
+                        else C[gi * ldc + gj] = val;
+                    }
+                }
+            }
+    }
+}
+
 template <class F, int BN_>
 __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     const uint8_t* __restrict__ A, const int8_t* __restrict__ As,
@@ -479,82 +562,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
 #pragma unroll
     for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f1, m);
 
-    // epilogue: D[i][j] of MFMA tile (ti, tj) is register v of lane l with j = l % 32 and
-    // i = 8 (v / 4) + 4 (l / 32) + v % 4; C = ldexp(D, alpha_i + beta_j - 2 bias) (exact)
-    const bool split = gridDim.z > 1;
-    const int64_t rowsC = min((int64_t)BM, M - m0), colsC = min((int64_t)BN, N - n0);
-    if ((int64_t)BM * ldc <= ((int64_t)1 << 28)) {
-        // buffer descriptor over the tile's rows of C: stores to rows past M fall outside it and
-        // are dropped; columns past N are masked per lane (edge tiles only)
-        const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
-            (void*)(C + m0 * ldc + n0), (short)0, (int)(((rowsC - 1) * ldc + colsC) * 4), 0x00020000);
-        const int lrow = wm * WM + 4 * (lane >> 5);
-        const int lcol = wn * WN + (lane & 31);
-        const int voff = (lrow * (int)ldc + lcol) * 4;
-        int beta[TN];
-        bool colok[TN];
-#pragma unroll
-        for (int tj = 0; tj < TN; tj++) {
-            beta[tj] = sBeta[lcol + 32 * tj] - 2 * F::GEMM_BIAS;
-            colok[tj] = lcol + 32 * tj < colsC;
-        }
-        // one straight-line store sequence per case (split or not, edge columns or not)
-        auto store_all = [&](auto split_c, auto edge_c) {
-            constexpr bool SPLIT = decltype(split_c)::value, EDGE = decltype(edge_c)::value;
-#pragma unroll
-            for (int ti = 0; ti < TM; ti++)
-#pragma unroll
-                for (int g = 0; g < 4; g++) {
-                    // row exponents of v = 4 g .. 4 g + 3 (four consecutive rows)
-                    const int4 al = *reinterpret_cast<const int4*>(sAlpha + lrow + 32 * ti + 8 * g);
-                    const int alr[4] = {al.x, al.y, al.z, al.w};
-#pragma unroll
-                    for (int r = 0; r < 4; r++) {
-                        const int soff = (32 * ti + 8 * g + r) * (int)ldc * 4;
-#pragma unroll
-                        for (int tj = 0; tj < TN; tj++) {
-                            if (EDGE && !colok[tj]) continue;
-                            const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta[tj]);
-                            if (SPLIT)
-                                __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(val, rc, voff + 128 * tj, soff, 0);
-                            else
-                                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, val), rc,
-                                                                      voff + 128 * tj, soff, 0);
-                        }
-                    }
-                }
-        };
-        using T = std::true_type;
-        using Fa = std::false_type;
-        const bool edge = colsC < BN;
-        if (split) {
-            if (edge) store_all(T(), T());
-            else store_all(T(), Fa());
-        } else {
-            if (edge) store_all(Fa(), T());
-            else store_all(Fa(), Fa());
-        }
-    } else {
-        // very wide C (ldc beyond 2^20): 64-bit addressing
-#pragma unroll
-        for (int ti = 0; ti < TM; ti++)
-#pragma unroll
-            for (int tj = 0; tj < TN; tj++) {
-                const int lj = wn * WN + tj * 32 + (lane & 31);
-                const int64_t gj = n0 + lj;
-                const int beta = sBeta[lj];
-#pragma unroll
-                for (int v = 0; v < 16; v++) {
-                    const int li = wm * WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-                    const int64_t gi = m0 + li;
-                    if (gi < M && gj < N) {
-                        const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
-                        if (split) unsafeAtomicAdd(C + gi * ldc + gj, val);
-                        else C[gi * ldc + gj] = val;
-                    }
-                }
-            }
-    }
+    store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, gridDim.z > 1);
 }
 
 // zero-fill of the output rows (split-K accumulates into C)
@@ -564,6 +572,325 @@ __global__ __launch_bounds__(256) void zero_rows_kernel(float* __restrict__ C, i
         const int64_t r = i / N;
         C[r * ldc + (i - r * N)] = 0.f;
     }
+}
+
+// ---------------------------------------------------------------------------------------------
+// Workspace path.  The codes of A and B are expanded once, by their own kernels, into fp16
+// (hi, lo) planes laid out exactly like the LDS stages above; the GEMM then streams each
+// 64 KB stage into LDS with buffer-to-LDS loads and its main loop is left to the MFMAs.
+// The expanded values are those of the fused kernel, and the MFMA order is the same, so both
+// paths give the same C bit for bit.
+
+// workspace of one GEMM: per operand with R rows, RT = ceil(R / 256) row tiles, nkb = K / 32
+//   planes [nkb][RT][hi, lo][256 rows][64 B] (32 KB per (kb, rt), rows swizzled as in a stage,
+//          zero past R)
+//   maxima [RT * 256] int32 (largest block scale of each row, 0 past R)
+struct WsLayout {
+    int64_t rta, rtb, planes_a, planes_b, max_a, max_b, bytes;
+};
+
+WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
+    WsLayout w;
+    const int64_t nkb = K / 32;
+    w.rta = (M + BM - 1) / BM;
+    w.rtb = (N + BM - 1) / BM;
+    w.planes_a = 0;
+    w.planes_b = w.planes_a + nkb * w.rta * 2 * PLANE;
+    w.max_a = w.planes_b + nkb * w.rtb * 2 * PLANE;
+    w.max_b = w.max_a + w.rta * BM * 4;
+    w.bytes = w.max_b + w.rtb * BM * 4;
+    return w;
+}
+
+// one launch before the expansion: row maxima of the block scales of A (workgroups
+// [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th scale of the row;
+// the remaining workgroups clear C when K is split (its halves are added into it)
+__global__ __launch_bounds__(256) void prep_kernel(const int8_t* __restrict__ as, const int8_t* __restrict__ bs,
+                                                   int64_t M, int64_t N, int64_t nkb, int ga, int gb,
+                                                   int* __restrict__ maxA, int* __restrict__ maxB,
+                                                   float* __restrict__ C, int64_t ldc) {
+    const int bid = (int)blockIdx.x;
+    if (bid >= ga + gb) {
+        const int64_t total = M * N, nz = (int64_t)gridDim.x - ga - gb;
+        for (int64_t i = (int64_t)(bid - ga - gb) * 256 + threadIdx.x; i < total; i += nz * 256) {
+            const int64_t r = i / N;
+            C[r * ldc + (i - r * N)] = 0.f;
+        }
+        return;
+    }
+    const bool isA = bid < ga;
+    const int8_t* s = isA ? as : bs;
+    const int64_t R = isA ? M : N;
+    int* out = isA ? maxA : maxB;
+    const int64_t row = (int64_t)(isA ? bid : bid - ga) * 16 + (threadIdx.x >> 4);
+    const int part = threadIdx.x & 15;
+    int m = -128;
+    if (row < R) {
+        const int8_t* sp = s + row * nkb;
+#pragma unroll 8
+        for (int64_t kb = part; kb < nkb; kb += 16) m = max(m, (int)sp[kb]);
+    }
+#pragma unroll
+    for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
+    if (part == 0) out[row] = row < R ? m : 0;   // the grid covers exactly the padded rows
+}
+
+// expansion of 64 rows x 4 K-blocks per workgroup: thread = (row (t >> 2) of the group, chunk
+// q = t & 3), one task per block; the same table values and multipliers as the fused kernel
+struct ExpandOperand {
+    const uint8_t* codes;
+    const int8_t* scales;
+    int64_t rows, tiles;      // rows, and row tiles of 256
+    const int* rmax;
+    char* planes;
+};
+
+// both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B
+template <class F>
+__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb, int fidx) {
+    __shared__ uint32_t lut[GEMM_DEC_ENTRIES];
+    lut[threadIdx.x] = g_dec[fidx][threadIdx.x];
+    const bool isA = (int64_t)blockIdx.x < 4 * opA.tiles;
+    const ExpandOperand& op = isA ? opA : opB;
+    const uint8_t* X = op.codes;
+    const int8_t* Xs = op.scales;
+    const int64_t R = op.rows, RT = op.tiles;
+    const int* rmax = op.rmax;
+    char* planes = op.planes;
+    const int64_t row_bytes = F::PACKED7 ? nkb * 28 : nkb * 32;
+    const int64_t r0 = (int64_t)(isA ? blockIdx.x : blockIdx.x - 4 * opA.tiles) * 64;
+    const int64_t kbase = (int64_t)blockIdx.y * 4;
+    const int lr = threadIdx.x >> 2, q = threadIdx.x & 3;
+    const int64_t row = r0 + lr;
+    // buffer descriptors over the group's rows (none past R: those tasks read zeros)
+    const int64_t rg = max((int64_t)0, min((int64_t)64, R - r0));
+    const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(X + min(r0, R) * row_bytes), (short)0, (int)(rg * row_bytes), 0x00020000);
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(Xs + min(r0, R) * nkb);
+    const int ds = (int)(s0 & 3);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void*>(s0 - ds), (short)0, (int)((ds + rg * nkb + 3) & ~3), 0x00020000);
+    const int voff_code = (int)(lr * row_bytes) + (F::PACKED7 ? 4 * ((7 * q) >> 2) : 8 * q);
+    const int x = ds + (int)(lr * nkb);   // byte offset of the row's scales in rs
+    Raw<F> raw[4];
+#pragma unroll
+    for (int t = 0; t < 4; t++)
+        load_raw<F>(rc, rs, voff_code, (int)((kbase + t) * (F::PACKED7 ? 28 : 32)), (x + (int)(kbase + t)) & ~3, 0, q,
+                    raw[t]);
+    const int alpha = rmax[row];
+    __syncthreads();
+#pragma unroll
+    for (int t = 0; t < 4; t++) {
+        const int64_t kb = kbase + t;
+        if (kb >= nkb) break;
+        const Chunk c = settle<F>(raw[t], q, 8 * ((x + (int)kb) & 3));
+        uint32_t e[8];
+#pragma unroll
+        for (int i = 0; i < 8; i++) e[i] = lut[chunk_code<F>(c, i)];
+        const int D = alpha - c.a;
+        const half2v m1 = __builtin_bit_cast(half2v, f16_pow2_neg(min(max(D, 0), 24)) * 0x10001u);
+        uint32_t hv[4], lv[4];
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            hv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x05040100u), m1);
+            lv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x07060302u), m1);
+        }
+        if (D > 24) {   // a block more than 24 binades below its row's top: second multiply
+            const half2v m2 = __builtin_bit_cast(half2v, f16_pow2_neg(min(D - 24, 24)) * 0x10001u);
+#pragma unroll
+            for (int p = 0; p < 4; p++) {
+                hv[p] = pk_mul(hv[p], m2);
+                lv[p] = pk_mul(lv[p], m2);
+            }
+        }
+        char* dst = planes + (kb * RT + row / BM) * (2 * PLANE) + swz((int)(row % BM), q);
+        *reinterpret_cast<uint4*>(dst) = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+        *reinterpret_cast<uint4*>(dst + PLANE) = make_uint4(lv[0], lv[1], lv[2], lv[3]);
+    }
+}
+
+// Work item of a workgroup on 8 XCDs.  Workgroups go to the XCDs round robin (linear id mod 8),
+// and each XCD has its own L2: XCD x takes the x-th eighth of the work items, in an order that
+// walks groups of 4 tile rows column by column, so the workgroups resident on one XCD at a time
+// cover a compact block of tiles and share their A and B stages in its L2.
+struct WorkItem {
+    int ty, tx, split;
+    bool valid;
+};
+
+__device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int splits) {
+    constexpr int XCDS = 8, GROUP = 4;
+    const int total = tiles_y * tiles_x * splits;
+    const int share = (total + XCDS - 1) / XCDS;
+    const int lin = (int)blockIdx.x;
+    const int u = (lin % XCDS) * share + lin / XCDS;
+    WorkItem w;
+    w.valid = u < total;
+    const int t = u / splits;
+    w.split = u - t * splits;
+    const int g = t / (GROUP * tiles_x);
+    const int gh = min(GROUP, tiles_y - g * GROUP);
+    const int local = t - g * GROUP * tiles_x;
+    w.ty = g * GROUP + local % gh;
+    w.tx = local / gh;
+    return w;
+}
+
+// GEMM on expanded planes: 256 x 256 tile per 256-thread workgroup as in the fused kernel; the
+// stage of block kb+1 is copied from the workspace by buffer-to-LDS loads (16 per thread)
+// while the MFMAs of block kb run
+template <class F>
+__global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
+    const char* __restrict__ PA, const char* __restrict__ PB, const int* __restrict__ maxA,
+    const int* __restrict__ maxB, int64_t M, int64_t N, int64_t K, int64_t RTA, int64_t RTB,
+    float* __restrict__ C, int64_t ldc, int splits) {
+    using TL = Tile<256>;
+    constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE;
+    constexpr int MFMA_PER_SUB = TL::MFMA_PER_SUB;
+    extern __shared__ __attribute__((aligned(16))) char smem[];
+    char* stage0 = smem;
+    char* stage1 = smem + STAGE;
+    int* sAlpha = reinterpret_cast<int*>(smem + 2 * STAGE);
+    int* sBeta = sAlpha + BM;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const WorkItem wi = work_item((int)RTA, (int)RTB, splits);
+    if (!wi.valid) return;   // the last XCD's share can run past the end (uniform per workgroup)
+    const int64_t m0 = (int64_t)wi.ty * BM, n0 = (int64_t)wi.tx * BN;
+    const int64_t nkb = K / 32;
+    const int64_t per = (nkb + splits - 1) / splits;
+    const int64_t kb0 = (int64_t)wi.split * per;
+    const int64_t kb1 = min(nkb, kb0 + per);
+    const int64_t nsteps = kb1 - kb0;
+    sAlpha[tid] = maxA[m0 + tid];
+    sBeta[tid] = maxB[n0 + tid];
+
+    // stage of block kb: A's 32 KB then B's 32 KB, each a contiguous workspace block; wave w
+    // copies kilobytes 8 w .. 8 w + 7 of each (lane l moves bytes 16 l .. 16 l + 15 of a kilobyte)
+    auto dma = [&](int64_t kb, char* st) {
+        const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(PA + (kb * RTA + wi.ty) * (2 * PLANE)), (short)0, 2 * PLANE, 0x00020000);
+        const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(PB + (kb * RTB + wi.tx) * (2 * PLANE)), (short)0, 2 * PLANE, 0x00020000);
+#pragma unroll
+        for (int i = 0; i < 8; i++) {
+            const int kbyte = (wave * 8 + i) * 1024;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                ra, (__attribute__((address_space(3))) void*)(st + kbyte), 16, kbyte + 16 * lane, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rb, (__attribute__((address_space(3))) void*)(st + 2 * PLANE + kbyte), 16, kbyte + 16 * lane, 0, 0, 0);
+        }
+    };
+    // this wave's copies have landed (vmcnt 0; the other counters left alone)
+    auto dma_wait = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
+
+    const int wm = wave >> 1, wn = wave & 1;
+    const int lr = lane & 31;
+    const int fsw = ((lr >> 1) ^ (lr >> 3)) & 3;
+    const int foff0 = lr * ROW_BYTES + 16 * ((0 + (lane >> 5)) ^ fsw);
+    const int foff1 = lr * ROW_BYTES + 16 * ((2 + (lane >> 5)) ^ fsw);
+    const int abase = wm * WM * ROW_BYTES, bbase = 2 * PLANE + wn * WN * ROW_BYTES;
+    auto load_frag = [&](Frag<TN>& f, const char* st, int kq) {
+        const char* pa = st + abase + (kq ? foff1 : foff0);
+        const char* pb = st + bbase + (kq ? foff1 : foff0);
+#pragma unroll
+        for (int t = 0; t < TM; t++) {
+            f.ah[t] = *reinterpret_cast<const half8*>(pa + t * 32 * ROW_BYTES);
+            f.al[t] = *reinterpret_cast<const half8*>(pa + PLANE + t * 32 * ROW_BYTES);
+        }
+#pragma unroll
+        for (int t = 0; t < TN; t++) {
+            f.bh[t] = *reinterpret_cast<const half8*>(pb + t * 32 * ROW_BYTES);
+            f.bl[t] = *reinterpret_cast<const half8*>(pb + TL::PLANE_B + t * 32 * ROW_BYTES);
+        }
+    };
+    f32x16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; i++)
+#pragma unroll
+        for (int j = 0; j < TN; j++)
+#pragma unroll
+            for (int v = 0; v < 16; v++) acc[i][j][v] = 0.f;
+    auto mfma = [&](const Frag<TN>& f, int idx) {
+        const int p = idx / (TM * TN), i = (idx / TN) % TM, j = idx % TN;
+        const half8& a = (p == 2) ? f.al[i] : f.ah[i];
+        const half8& b = (p == 1) ? f.bl[j] : f.bh[j];
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[i][j], 0, 0, 0);
+    };
+
+    Frag<TN> f0, f1;
+    dma(kb0, stage0);
+    dma_wait();
+    __syncthreads();
+    load_frag(f0, stage0, 0);
+    char* cur = stage0;
+    char* nxt = stage1;
+    // the barrier sits after slice 0 and a quarter of slice 1, so the next stage's first
+    // fragments load behind the last 36 MFMAs (slice 0's registers are free by then)
+    constexpr int PRE = 12;
+    for (int64_t s = 0; s + 1 < nsteps; s++) {
+        dma(kb0 + s + 1, nxt);
+        load_frag(f1, cur, 1);
+#pragma unroll
+        for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f0, m);
+#pragma unroll
+        for (int m = 0; m < PRE; m++) mfma(f1, m);
+        dma_wait();
+        __syncthreads();
+        load_frag(f0, nxt, 0);
+#pragma unroll
+        for (int m = PRE; m < MFMA_PER_SUB; m++) mfma(f1, m);
+        char* t = cur;
+        cur = nxt;
+        nxt = t;
+    }
+    load_frag(f1, cur, 1);
+#pragma unroll
+    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f0, m);
+#pragma unroll
+    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f1, m);
+
+    store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, splits > 1);
+}
+
+constexpr int WS_SMEM = 2 * Tile<256>::STAGE + 2 * BM * 4;
+
+template <class F>
+hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
+                         int64_t N, int64_t K, float* c, int64_t ldc, char* ws, int fidx, hipStream_t s) {
+    static bool attr_set[64] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    if (!attr_set[dev]) {
+        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_ws_kernel<F>),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, WS_SMEM);
+        if (e != hipSuccess) return e;
+        attr_set[dev] = true;
+    }
+    const WsLayout w = ws_layout(M, N, K);
+    const int64_t nkb = K / 32;
+    int* maxA = reinterpret_cast<int*>(ws + w.max_a);
+    int* maxB = reinterpret_cast<int*>(ws + w.max_b);
+    const int64_t tiles = w.rta * w.rtb;
+    const int splits = (tiles < 256 && nkb >= 16) ? 2 : 1;
+    const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
+    int64_t zb = splits > 1 ? (M * N + 255) / 256 : 0;
+    zb = zb < 2048 ? zb : 2048;
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + zb)), dim3(256), 0, s, as, bs, M, N, nkb, ga, gb,
+                       maxA, maxB, c, ldc);
+    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a};
+    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b};
+    hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
+                       dim3(256), 0, s, opA, opB, nkb, fidx);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int64_t items = w.rta * w.rtb * splits;
+    const int64_t grid = (items + 7) / 8 * 8;   // whole XCD shares; surplus workgroups return at once
+    hipLaunchKernelGGL((gemm_ws_kernel<F>), dim3((unsigned)grid), dim3(NTHREADS), WS_SMEM, s, ws + w.planes_a,
+                       ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits);
+    return hipGetLastError();
 }
 
 template <class F, int BN_>
@@ -608,6 +935,18 @@ hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8
 }
 
 }  // namespace
+
+int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout(M, N, K).bytes; }
+
+hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
+                          int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s) {
+    char* w = reinterpret_cast<char*>(ws);
+    switch (format) {
+        case 0: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, w, 0, s);
+        case 1: return launch_ws_fmt<FmtE5C2>(a, as, b, bs, M, N, K, c, ldc, w, 1, s);
+        default: return launch_ws_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, w, 2, s);
+    }
+}
 
 hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                        int64_t N, int64_t K, int format, float* c, int64_t ldc, hipStream_t s) {

@@ -57,6 +57,10 @@ def lib() -> ctypes.CDLL:
         L.curvefp_dequantize.restype = I
         L.curvefp_gemm.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
         L.curvefp_gemm.restype = I
+        L.curvefp_gemm_workspace_bytes.argtypes = [I64, I64, I64]
+        L.curvefp_gemm_workspace_bytes.restype = I64
+        L.curvefp_gemm_ws.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P, I64, P]
+        L.curvefp_gemm_ws.restype = I
         L.curvefp_status_string.argtypes = [I]
         L.curvefp_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -150,4 +154,33 @@ def curvefp_gemm(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.T
                             b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
                             _stream(stream))
     _check(st, "curvefp_gemm")
+    return c
+
+
+def curvefp_gemm_workspace_bytes(M: int, N: int, K: int) -> int:
+    n = lib().curvefp_gemm_workspace_bytes(M, N, K)
+    if n < 0:
+        raise CurveFPError(n, "curvefp_gemm_workspace_bytes")
+    return n
+
+
+def gemm_workspace(M: int, N: int, K: int, device) -> torch.Tensor:
+    """A device buffer large enough for curvefp_gemm_ws (torch allocations are 256-byte aligned)."""
+    return torch.empty(curvefp_gemm_workspace_bytes(M, N, K), dtype=torch.uint8, device=device)
+
+
+def curvefp_gemm_ws(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.Tensor,
+                    b_scales: torch.Tensor, M: int, N: int, K: int, fmt, block: int = 32,
+                    c: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                    stream=None) -> torch.Tensor:
+    """The product of curvefp_gemm, through a workspace (codes expanded once)."""
+    if c is None:
+        c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    if workspace is None:
+        workspace = gemm_workspace(M, N, K, a_codes.device)
+    st = lib().curvefp_gemm_ws(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
+                               b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
+                               workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                               _stream(stream))
+    _check(st, "curvefp_gemm_ws")
     return c

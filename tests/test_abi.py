@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 8
+    assert len(names) == 10
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -124,3 +124,26 @@ def test_gemm_validation(L):
     for i in (0, 2, 9):
         bad = list(args); bad[i] = MIS
         assert g(*bad) == EALIGN, i
+
+
+def test_gemm_ws_validation(L):
+    assert L.curvefp_gemm_workspace_bytes(0, 64, 64) == ESHAPE
+    assert L.curvefp_gemm_workspace_bytes(64, 64, 48) == ESHAPE
+    # rows padded to 256: (256 + 256) rows x K x 4 bytes of planes + one int32 per padded row
+    assert L.curvefp_gemm_workspace_bytes(10, 300, 64) == (256 + 512) * 64 * 4 + (256 + 512) * 4
+    need = L.curvefp_gemm_workspace_bytes(64, 64, 64)
+    WS = 1 << 24                     # 256-byte aligned, never dereferenced
+    g = L.curvefp_gemm_ws
+    args = [FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 32, FAKE, 64, WS, need, None]
+    for i in (0, 1, 2, 3, 9, 11):
+        a = list(args)
+        a[i] = None
+        assert g(*a) == ENULL, i
+    bad = list(args); bad[12] = need - 1
+    assert g(*bad) == ESHAPE
+    bad = list(args); bad[11] = WS + 128
+    assert g(*bad) == EALIGN
+    bad = list(args); bad[7] = 5
+    assert g(*bad) == EFMT
+    bad = list(args); bad[6] = 40
+    assert g(*bad) == ESHAPE
