@@ -82,13 +82,18 @@ def gemm_tolerance(ca, sa, cb, sb, fmt):
     return 1e-5 * S + 2.0 ** -38 * flush + 2.0 ** -148
 
 
-def check_gemm(C_dev: np.ndarray, V: np.ndarray, tol: np.ndarray, what: str):
+def check_gemm(C_dev: np.ndarray, V: np.ndarray, tol: np.ndarray, what: str, frobenius: bool = True):
+    """Element-wise bound `tol` everywhere; relative Frobenius error <= 1e-5 (the workloads'
+    bar) unless `frobenius` is off: with K far beyond the workloads' lengths and terms that
+    cancel, fp32 accumulation alone can exceed 1e-5 of |C| while staying inside the
+    element-wise bound, which scales with sum |a b|."""
     err = np.abs(C_dev.astype(np.float64) - V)
     bad = err > tol
     assert not bad.any(), f"{what}: {bad.sum()} elements beyond bound; worst {np.max(err - tol)}"
     nv = np.linalg.norm(V)
     if nv > 0:
         rel = np.linalg.norm(C_dev.astype(np.float64) - V) / nv
-        assert rel <= 1e-5, f"{what}: relative Frobenius error {rel}"
+        if frobenius:
+            assert rel <= 1e-5, f"{what}: relative Frobenius error {rel}"
         return rel
     return 0.0
