@@ -144,7 +144,9 @@ int curvefp_gemm(const void* a_codes, const int8_t* a_scales,
 /*
  * Bytes of device workspace curvefp_gemm_ws needs for an M x N x K product
  * (4 bytes per element of A and B with rows padded to multiples of 256, plus
- * one int32 per padded row).  Returns CURVEFP_ERR_SHAPE for non-positive
+ * one int32 per padded row; when K is split in two -- fewer than 256 output
+ * tiles of 256 x 256 and K >= 512 -- also 512 KiB of partial sums and one
+ * arrival counter per tile).  Returns CURVEFP_ERR_SHAPE for non-positive
  * sizes or K not a multiple of 32.
  */
 int64_t curvefp_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);

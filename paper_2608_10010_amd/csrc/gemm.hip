@@ -52,6 +52,8 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 256, BK = 32;
 constexpr int NTHREADS = 256;
@@ -193,6 +195,11 @@ __device__ __forceinline__ void rescale_chunk(char* dst, int D) {
     *reinterpret_cast<uint4*>(dst) = v;
 }
 
+// cache policy of buffer accesses that must be coherent across the XCDs' L2 caches (sc1:
+// device scope): stores reach the device's point of coherence before they count as done,
+// and loads do not hit lines another XCD may hold stale
+constexpr int AUX_DEVICE_COHERENT = 16;
+
 template <int TN>
 struct Frag {
     half8 ah[TM], al[TM], bh[TN], bl[TN];
@@ -201,12 +208,18 @@ struct Frag {
 // epilogue of a 256 x BN_ tile: D[i][j] of MFMA tile (ti, tj) is register v of lane l with
 // j = l % 32 and i = 8 (v / 4) + 4 (l / 32) + v % 4; C = ldexp(D, alpha_i + beta_j - 2 bias)
 // (exact), stored, or added with fp32 atomics when K is split
-template <class F, int BN_>
+// (ADD: each value is added to the other K half's value of the same element, read from its
+// partial-tile slot at `other`, at wbase in the layout the workspace kernel writes, with
+// device-coherent loads)
+template <class F, int BN_, bool ADD = false>
 __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], const int* sAlpha, const int* sBeta,
                                            float* C, int64_t ldc, int64_t M, int64_t N, int64_t m0, int64_t n0,
-                                           int wm, int wn, int lane, bool split) {
+                                           int wm, int wn, int lane, bool split,
+                                           const char* other_slot = nullptr, int wbase = 0) {
     constexpr int BN = BN_, WN = Tile<BN_>::WN, TN = Tile<BN_>::TN;
     const int64_t rowsC = min((int64_t)BM, M - m0), colsC = min((int64_t)BN, N - n0);
+    const __amdgpu_buffer_rsrc_t rq =
+        __builtin_amdgcn_make_buffer_rsrc((void*)other_slot, (short)0, ADD ? (int)BM * BN * 4 : 0, 0x00020000);
     if ((int64_t)BM * ldc <= ((int64_t)1 << 28)) {
         // buffer descriptor over the tile's rows of C: stores to rows past M fall outside it and
         // are dropped; columns past N are masked per lane (edge tiles only)
@@ -232,13 +245,22 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
                     // row exponents of v = 4 g .. 4 g + 3 (four consecutive rows)
                     const int4 al = *reinterpret_cast<const int4*>(sAlpha + lrow + 32 * ti + 8 * g);
                     const int alr[4] = {al.x, al.y, al.z, al.w};
+                    f32x4 other[TN];
+                    if (ADD) {
+#pragma unroll
+                        for (int tj = 0; tj < TN; tj++)
+                            other[tj] = __builtin_bit_cast(
+                                f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, wbase + ((ti * 4 + tj) * 4 + g) * 1024,
+                                                                             0, AUX_DEVICE_COHERENT));
+                    }
 #pragma unroll
                     for (int r = 0; r < 4; r++) {
                         const int soff = (32 * ti + 8 * g + r) * (int)ldc * 4;
 #pragma unroll
                         for (int tj = 0; tj < TN; tj++) {
                             if (EDGE && !colok[tj]) continue;
-                            const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta[tj]);
+                            float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta[tj]);
+                            if (ADD) val += other[tj][r];
                             if (SPLIT)
                                 __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(val, rc, voff + 128 * tj, soff, 0);
                             else
@@ -272,7 +294,12 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
                     const int li = wm * WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
                     const int64_t gi = m0 + li;
                     if (gi < M && gj < N) {
-                        const float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                        float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                        if (ADD)
+                            val += __builtin_bit_cast(
+                                float, __builtin_amdgcn_raw_buffer_load_b32(
+                                           rq, wbase + ((ti * 4 + tj) * 4 + v / 4) * 1024 + 4 * (v % 4), 0,
+                                           AUX_DEVICE_COHERENT));
                         if (split) unsafeAtomicAdd(C + gi * ldc + gj, val);
                         else C[gi * ldc + gj] = val;
                     }
@@ -585,8 +612,14 @@ __global__ __launch_bounds__(256) void zero_rows_kernel(float* __restrict__ C, i
 //   planes [nkb][RT][hi, lo][256 rows][64 B] (32 KB per (kb, rt), rows swizzled as in a stage,
 //          zero past R)
 //   maxima [RT * 256] int32 (largest block scale of each row, 0 past R)
+// K is split in two when the tiles cover fewer than the 256 compute units and K is long enough:
+// each half writes its scaled 256 x 256 partial tile to the workspace, and the half that
+// finishes last adds the other's to its own and stores C (a per-tile arrival counter decides)
+constexpr int64_t PART_BYTES = (int64_t)BM * 256 * 4;
+
 struct WsLayout {
-    int64_t rta, rtb, planes_a, planes_b, max_a, max_b, bytes;
+    int64_t rta, rtb, planes_a, planes_b, max_a, max_b, cnt, part, bytes;
+    int splits;
 };
 
 WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
@@ -594,28 +627,33 @@ WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
     const int64_t nkb = K / 32;
     w.rta = (M + BM - 1) / BM;
     w.rtb = (N + BM - 1) / BM;
+    const int64_t tiles = w.rta * w.rtb;
+    w.splits = (tiles < 256 && nkb >= 16) ? 2 : 1;
     w.planes_a = 0;
     w.planes_b = w.planes_a + nkb * w.rta * 2 * PLANE;
     w.max_a = w.planes_b + nkb * w.rtb * 2 * PLANE;
     w.max_b = w.max_a + w.rta * BM * 4;
-    w.bytes = w.max_b + w.rtb * BM * 4;
+    int64_t end = w.max_b + w.rtb * BM * 4;
+    w.cnt = w.part = end;
+    if (w.splits > 1) {
+        w.cnt = (end + 255) & ~(int64_t)255;
+        w.part = w.cnt + ((tiles * 4 + 255) & ~(int64_t)255);
+        end = w.part + tiles * w.splits * PART_BYTES;
+    }
+    w.bytes = end;
     return w;
 }
 
 // one launch before the expansion: row maxima of the block scales of A (workgroups
 // [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th scale of the row;
-// the remaining workgroups clear C when K is split (its halves are added into it)
+// one more workgroup zeroes the per-tile arrival counters when K is split
 __global__ __launch_bounds__(256) void prep_kernel(const int8_t* __restrict__ as, const int8_t* __restrict__ bs,
                                                    int64_t M, int64_t N, int64_t nkb, int ga, int gb,
                                                    int* __restrict__ maxA, int* __restrict__ maxB,
-                                                   float* __restrict__ C, int64_t ldc) {
+                                                   int* __restrict__ cnt, int ncnt) {
     const int bid = (int)blockIdx.x;
     if (bid >= ga + gb) {
-        const int64_t total = M * N, nz = (int64_t)gridDim.x - ga - gb;
-        for (int64_t i = (int64_t)(bid - ga - gb) * 256 + threadIdx.x; i < total; i += nz * 256) {
-            const int64_t r = i / N;
-            C[r * ldc + (i - r * N)] = 0.f;
-        }
+        for (int i = threadIdx.x; i < ncnt; i += 256) cnt[i] = 0;
         return;
     }
     const bool isA = bid < ga;
@@ -736,24 +774,30 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
     return w;
 }
 
-// GEMM on expanded planes: 256 x 256 tile per 256-thread workgroup as in the fused kernel; the
-// stage of block kb+1 is copied from the workspace by buffer-to-LDS loads (16 per thread)
-// while the MFMAs of block kb run
+// GEMM on expanded planes: 256 x 256 tile per 256-thread workgroup as in the fused kernel (the
+// same MFMA order, so the same C bit for bit).  Two LDS stages; a step (one K block) is
+//   phase 1: the block's second fragment slice is read from LDS under the first slice's MFMAs;
+//   barrier: every wave is done with the stage of this block, and the copy of the next block
+//            into the other stage has landed;
+//   phase 2: the copy of block s+2 into the stage just freed (buffer-to-LDS loads, 16 per
+//            thread) and the reads of block s+1's first slice go out under the second slice's MFMAs.
+// So each copy has a whole step to land, and the scheduler is held to this interleaving.
 template <class F>
 __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     const char* __restrict__ PA, const char* __restrict__ PB, const int* __restrict__ maxA,
     const int* __restrict__ maxB, int64_t M, int64_t N, int64_t K, int64_t RTA, int64_t RTB,
-    float* __restrict__ C, int64_t ldc, int splits) {
+    float* __restrict__ C, int64_t ldc, int splits, char* __restrict__ part, int* __restrict__ cnt) {
     using TL = Tile<256>;
     constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE;
-    constexpr int MFMA_PER_SUB = TL::MFMA_PER_SUB;
+    constexpr int MPS = TL::MFMA_PER_SUB;   // 48 MFMAs per 16-wide K slice
+    static_assert(TM == 4 && TN == 4 && MPS == 48, "the interleaving below assumes 4 x 4 MFMA tiles");
     extern __shared__ __attribute__((aligned(16))) char smem[];
-    char* stage0 = smem;
-    char* stage1 = smem + STAGE;
     int* sAlpha = reinterpret_cast<int*>(smem + 2 * STAGE);
     int* sBeta = sAlpha + BM;
+    int* sLast = sBeta + BN;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const WorkItem wi = work_item((int)RTA, (int)RTB, splits);
     if (!wi.valid) return;   // the last XCD's share can run past the end (uniform per workgroup)
     const int64_t m0 = (int64_t)wi.ty * BM, n0 = (int64_t)wi.tx * BN;
@@ -765,9 +809,12 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     sAlpha[tid] = maxA[m0 + tid];
     sBeta[tid] = maxB[n0 + tid];
 
-    // stage of block kb: A's 32 KB then B's 32 KB, each a contiguous workspace block; wave w
-    // copies kilobytes 8 w .. 8 w + 7 of each (lane l moves bytes 16 l .. 16 l + 15 of a kilobyte)
-    auto dma = [&](int64_t kb, char* st) {
+    // stage of block kb at LDS offset st: A's 32 KB then B's 32 KB, each a contiguous workspace
+    // block; wave w copies kilobytes 8 w .. 8 w + 7 of each (lane l moves bytes 16 l .. 16 l + 15
+    // of a kilobyte; the LDS address is M0 + 16 l)
+    using lds_ptr = __attribute__((address_space(3))) void*;
+    const int voff = 16 * lane;
+    auto dma = [&](int64_t kb, int st) {
         const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(PA + (kb * RTA + wi.ty) * (2 * PLANE)), (short)0, 2 * PLANE, 0x00020000);
         const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
@@ -775,34 +822,34 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
 #pragma unroll
         for (int i = 0; i < 8; i++) {
             const int kbyte = (wave * 8 + i) * 1024;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                ra, (__attribute__((address_space(3))) void*)(st + kbyte), 16, kbyte + 16 * lane, 0, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rb, (__attribute__((address_space(3))) void*)(st + 2 * PLANE + kbyte), 16, kbyte + 16 * lane, 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(smem + st + kbyte), 16, voff, kbyte, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(smem + st + 2 * PLANE + kbyte), 16, voff,
+                                                     kbyte, 0, 0);
         }
     };
     // this wave's copies have landed (vmcnt 0; the other counters left alone)
     auto dma_wait = [] { __builtin_amdgcn_s_waitcnt(0x0F70); };
 
-    const int wm = wave >> 1, wn = wave & 1;
+    const int wm = (tid >> 6) >> 1, wn = (tid >> 6) & 1;
     const int lr = lane & 31;
     const int fsw = ((lr >> 1) ^ (lr >> 3)) & 3;
     const int foff0 = lr * ROW_BYTES + 16 * ((0 + (lane >> 5)) ^ fsw);
     const int foff1 = lr * ROW_BYTES + 16 * ((2 + (lane >> 5)) ^ fsw);
     const int abase = wm * WM * ROW_BYTES, bbase = 2 * PLANE + wn * WN * ROW_BYTES;
-    auto load_frag = [&](Frag<TN>& f, const char* st, int kq) {
-        const char* pa = st + abase + (kq ? foff1 : foff0);
-        const char* pb = st + bbase + (kq ? foff1 : foff0);
+    // fragment reads in the order the MFMAs consume them (hi x hi by rows of A, then B lo, then A lo)
+    auto load_frag = [&](Frag<TN>& f, int st, int kq) {
+        const char* pa = smem + st + abase + (kq ? foff1 : foff0);
+        const char* pb = smem + st + bbase + (kq ? foff1 : foff0);
+        f.ah[0] = *reinterpret_cast<const half8*>(pa);
 #pragma unroll
-        for (int t = 0; t < TM; t++) {
-            f.ah[t] = *reinterpret_cast<const half8*>(pa + t * 32 * ROW_BYTES);
-            f.al[t] = *reinterpret_cast<const half8*>(pa + PLANE + t * 32 * ROW_BYTES);
-        }
+        for (int t = 0; t < TN; t++) f.bh[t] = *reinterpret_cast<const half8*>(pb + t * 32 * ROW_BYTES);
 #pragma unroll
-        for (int t = 0; t < TN; t++) {
-            f.bh[t] = *reinterpret_cast<const half8*>(pb + t * 32 * ROW_BYTES);
+        for (int t = 1; t < TM; t++) f.ah[t] = *reinterpret_cast<const half8*>(pa + t * 32 * ROW_BYTES);
+#pragma unroll
+        for (int t = 0; t < TN; t++)
             f.bl[t] = *reinterpret_cast<const half8*>(pb + TL::PLANE_B + t * 32 * ROW_BYTES);
-        }
+#pragma unroll
+        for (int t = 0; t < TM; t++) f.al[t] = *reinterpret_cast<const half8*>(pa + PLANE + t * 32 * ROW_BYTES);
     };
     f32x16 acc[TM][TN];
 #pragma unroll
@@ -817,43 +864,134 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
         const half8& b = (p == 1) ? f.bl[j] : f.bh[j];
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, acc[i][j], 0, 0, 0);
     };
+    // scheduling masks: MFMA, VMEM, DS read
+    constexpr int SG_MFMA = 0x008, SG_VMEM = 0x010, SG_DSR = 0x100;
 
-    Frag<TN> f0, f1;
-    dma(kb0, stage0);
-    dma_wait();
-    __syncthreads();
-    load_frag(f0, stage0, 0);
-    char* cur = stage0;
-    char* nxt = stage1;
-    // the barrier sits after slice 0 and a quarter of slice 1, so the next stage's first
-    // fragments load behind the last 36 MFMAs (slice 0's registers are free by then)
-    constexpr int PRE = 12;
-    for (int64_t s = 0; s + 1 < nsteps; s++) {
-        dma(kb0 + s + 1, nxt);
-        load_frag(f1, cur, 1);
+    // phase 1 of the step on the stage at st: one fragment read per two MFMAs over the first 32
+    auto phase1 = [&](Frag<TN>& fa, Frag<TN>& fb, int st) {
+        // fa's reads went out a phase ago: waiting for them here costs nothing, and tells the
+        // compiler that none is outstanding (else it waits for the first read below as well)
+        __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+        load_frag(fb, st, 1);
 #pragma unroll
-        for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f0, m);
+        for (int m = 0; m < MPS; m++) mfma(fa, m);
 #pragma unroll
-        for (int m = 0; m < PRE; m++) mfma(f1, m);
+        for (int i = 0; i < 16; i++) {
+            __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 2, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 32, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // the barrier between the phases
+    auto handover = [&] {
         dma_wait();
         __syncthreads();
-        load_frag(f0, nxt, 0);
+        __builtin_amdgcn_sched_barrier(0);
+    };
+    // phase 2: the next block's first slice read from the stage at nx, one read per MFMA over
+    // the first 16, then (with copy) block kb copied into the stage at st, one copy per MFMA over
+    // the next 16 (the copies follow the reads: the compiler keeps LDS writes after LDS reads
+    // it cannot tell apart from them)
+    auto phase2 = [&](Frag<TN>& fa, Frag<TN>& fb, int nx, bool copy, int64_t kb, int st) {
+        load_frag(fa, nx, 0);
+        if (copy) dma(kb, st);
 #pragma unroll
-        for (int m = PRE; m < MFMA_PER_SUB; m++) mfma(f1, m);
-        char* t = cur;
+        for (int m = 0; m < MPS; m++) mfma(fb, m);
+#pragma unroll
+        for (int i = 0; i < 16; i++) {
+            __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+        }
+        if (copy) {
+#pragma unroll
+            for (int i = 0; i < 16; i++) {
+                __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);
+                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            }
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 32, 0);
+        } else {
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 16, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+    };
+
+    Frag<TN> f0, f1;
+    int cur = 0, nxt = STAGE;
+    dma(kb0, cur);
+    dma_wait();
+    __syncthreads();
+    if (nsteps > 1) dma(kb0 + 1, nxt);
+    load_frag(f0, cur, 0);
+    // steps 0 .. nsteps-3 copy block s+2; the last two copy nothing
+    for (int64_t s = 0; s + 2 < nsteps; s++) {
+        phase1(f0, f1, cur);
+        handover();
+        phase2(f0, f1, nxt, true, kb0 + s + 2, cur);
+        const int t = cur;
         cur = nxt;
         nxt = t;
     }
-    load_frag(f1, cur, 1);
+    if (nsteps > 1) {
+        phase1(f0, f1, cur);
+        handover();
+        phase2(f0, f1, nxt, false, 0, 0);
+        cur = nxt;
+    }
+    phase1(f0, f1, cur);
 #pragma unroll
-    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f0, m);
-#pragma unroll
-    for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f1, m);
+    for (int m = 0; m < MPS; m++) mfma(f1, m);
 
-    store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, splits > 1);
+    if (splits == 1) {
+        store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
+        return;
+    }
+    // K split in two: each half publishes its scaled values (C = ldexp(D, alpha_i + beta_j -
+    // 2 bias), exact) in the tile's slot for that half and counts its arrival; the half that
+    // arrives second adds the other's values to its own (the same fp32 sum as two atomic adds
+    // into zero) and stores C.  Slot layout: thread t's acc[ti][tj] quarter q (four floats) at
+    // ((((t / 64) * 16 + ti * 4 + tj) * 4 + q) * 1024 + (t % 64) * 16), coalesced 1 KB per store.
+    // The slots are written and read with device-coherent accesses, so no cache write-back or
+    // invalidation is needed: every thread waits for its stores to complete, the barrier orders
+    // that before the arrival (a device-scope atomic), and the second half's reads are issued
+    // only after it has seen the first half's arrival.
+    const int64_t tile = (int64_t)wi.ty * RTB + wi.tx;
+    char* slots = part + tile * 2 * PART_BYTES;
+    const int wbase = (tid >> 6) * 16 * 4096 + lane * 16;
+    {
+        const int lcol = wn * WN + (lane & 31), lrow = wm * WM + 4 * (lane >> 5);
+        const __amdgpu_buffer_rsrc_t rp = __builtin_amdgcn_make_buffer_rsrc(
+            (void*)(slots + wi.split * PART_BYTES), (short)0, (int)PART_BYTES, 0x00020000);
+#pragma unroll
+        for (int ti = 0; ti < TM; ti++)
+#pragma unroll
+            for (int tj = 0; tj < TN; tj++) {
+                const int beta = sBeta[lcol + 32 * tj] - 2 * F::GEMM_BIAS;
+#pragma unroll
+                for (int q = 0; q < 4; q++) {
+                    const int4 al = *reinterpret_cast<const int4*>(sAlpha + lrow + 32 * ti + 8 * q);
+                    f32x4 v;
+                    v[0] = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * q], al.x + beta);
+                    v[1] = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * q + 1], al.y + beta);
+                    v[2] = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * q + 2], al.z + beta);
+                    v[3] = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * q + 3], al.w + beta);
+                    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), rp,
+                                                           wbase + ((ti * 4 + tj) * 4 + q) * 1024, 0,
+                                                           AUX_DEVICE_COHERENT);
+                }
+            }
+    }
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's slot stores are complete
+    __syncthreads();
+    if (tid == 0)
+        sLast[0] = __hip_atomic_fetch_add(cnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
+    __syncthreads();
+    if (!sLast[0]) return;   // uniform: the other half arrives later and finishes the tile
+    store_tile<F, BN, true>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false,
+                            slots + (1 - wi.split) * PART_BYTES, wbase);
 }
 
-constexpr int WS_SMEM = 2 * Tile<256>::STAGE + 2 * BM * 4;
+constexpr int WS_SMEM = 2 * Tile<256>::STAGE + 2 * BM * 4 + 16;
 
 template <class F>
 hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
@@ -874,12 +1012,11 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     int* maxA = reinterpret_cast<int*>(ws + w.max_a);
     int* maxB = reinterpret_cast<int*>(ws + w.max_b);
     const int64_t tiles = w.rta * w.rtb;
-    const int splits = (tiles < 256 && nkb >= 16) ? 2 : 1;
+    const int splits = w.splits;
+    int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
-    int64_t zb = splits > 1 ? (M * N + 255) / 256 : 0;
-    zb = zb < 2048 ? zb : 2048;
-    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + zb)), dim3(256), 0, s, as, bs, M, N, nkb, ga, gb,
-                       maxA, maxB, c, ldc);
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
+                       nkb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
     const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a};
     const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
@@ -889,7 +1026,7 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     const int64_t items = w.rta * w.rtb * splits;
     const int64_t grid = (items + 7) / 8 * 8;   // whole XCD shares; surplus workgroups return at once
     hipLaunchKernelGGL((gemm_ws_kernel<F>), dim3((unsigned)grid), dim3(NTHREADS), WS_SMEM, s, ws + w.planes_a,
-                       ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits);
+                       ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt);
     return hipGetLastError();
 }
 
