@@ -791,10 +791,15 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE;
     constexpr int MPS = TL::MFMA_PER_SUB;   // 48 MFMAs per 16-wide K slice
     static_assert(TM == 4 && TN == 4 && MPS == 48, "the interleaving below assumes 4 x 4 MFMA tiles");
-    extern __shared__ __attribute__((aligned(16))) char smem[];
-    int* sAlpha = reinterpret_cast<int*>(smem + 2 * STAGE);
-    int* sBeta = sAlpha + BM;
-    int* sLast = sBeta + BN;
+    // two stages as separate arrays: the loop below is unrolled so that every access names its
+    // stage statically, and the compiler can see that copies into one stage and fragment reads
+    // from the other do not overlap (so it may interleave them freely)
+    __shared__ __attribute__((aligned(16))) char st0[STAGE];
+    __shared__ __attribute__((aligned(16))) char st1[STAGE];
+    __shared__ __attribute__((aligned(16))) int sAB[BM + BN + 4];
+    int* sAlpha = sAB;
+    int* sBeta = sAB + BM;
+    int* sLast = sAB + BM + BN;
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -809,12 +814,12 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     sAlpha[tid] = maxA[m0 + tid];
     sBeta[tid] = maxB[n0 + tid];
 
-    // stage of block kb at LDS offset st: A's 32 KB then B's 32 KB, each a contiguous workspace
+    // stage of block kb in st: A's 32 KB then B's 32 KB, each a contiguous workspace
     // block; wave w copies kilobytes 8 w .. 8 w + 7 of each (lane l moves bytes 16 l .. 16 l + 15
     // of a kilobyte; the LDS address is M0 + 16 l)
     using lds_ptr = __attribute__((address_space(3))) void*;
     const int voff = 16 * lane;
-    auto dma = [&](int64_t kb, int st) {
+    auto dma = [&](int64_t kb, char* st) {
         const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(
             (void*)(PA + (kb * RTA + wi.ty) * (2 * PLANE)), (short)0, 2 * PLANE, 0x00020000);
         const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc(
@@ -822,9 +827,8 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
 #pragma unroll
         for (int i = 0; i < 8; i++) {
             const int kbyte = (wave * 8 + i) * 1024;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(smem + st + kbyte), 16, voff, kbyte, 0, 0);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(smem + st + 2 * PLANE + kbyte), 16, voff,
-                                                     kbyte, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr)(st + kbyte), 16, voff, kbyte, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_ptr)(st + 2 * PLANE + kbyte), 16, voff, kbyte, 0, 0);
         }
     };
     // this wave's copies have landed (vmcnt 0; the other counters left alone)
@@ -837,9 +841,9 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     const int foff1 = lr * ROW_BYTES + 16 * ((2 + (lane >> 5)) ^ fsw);
     const int abase = wm * WM * ROW_BYTES, bbase = 2 * PLANE + wn * WN * ROW_BYTES;
     // fragment reads in the order the MFMAs consume them (hi x hi by rows of A, then B lo, then A lo)
-    auto load_frag = [&](Frag<TN>& f, int st, int kq) {
-        const char* pa = smem + st + abase + (kq ? foff1 : foff0);
-        const char* pb = smem + st + bbase + (kq ? foff1 : foff0);
+    auto load_frag = [&](Frag<TN>& f, const char* st, int kq) {
+        const char* pa = st + abase + (kq ? foff1 : foff0);
+        const char* pb = st + bbase + (kq ? foff1 : foff0);
         f.ah[0] = *reinterpret_cast<const half8*>(pa);
 #pragma unroll
         for (int t = 0; t < TN; t++) f.bh[t] = *reinterpret_cast<const half8*>(pb + t * 32 * ROW_BYTES);
@@ -868,7 +872,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     constexpr int SG_MFMA = 0x008, SG_VMEM = 0x010, SG_DSR = 0x100;
 
     // phase 1 of the step on the stage at st: one fragment read per two MFMAs over the first 32
-    auto phase1 = [&](Frag<TN>& fa, Frag<TN>& fb, int st) {
+    auto phase1 = [&](Frag<TN>& fa, Frag<TN>& fb, char* st) {
         // fa's reads went out a phase ago: waiting for them here costs nothing, and tells the
         // compiler that none is outstanding (else it waits for the first read below as well)
         __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
@@ -889,58 +893,67 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
         __syncthreads();
         __builtin_amdgcn_sched_barrier(0);
     };
-    // phase 2: the next block's first slice read from the stage at nx, one read per MFMA over
-    // the first 16, then (with copy) block kb copied into the stage at st, one copy per MFMA over
-    // the next 16 (the copies follow the reads: the compiler keeps LDS writes after LDS reads
-    // it cannot tell apart from them)
-    auto phase2 = [&](Frag<TN>& fa, Frag<TN>& fb, int nx, bool copy, int64_t kb, int st) {
-        load_frag(fa, nx, 0);
+    // phase 2: (with copy) block kb copied into the stage st and the next block's first slice
+    // read from nx, one copy and one read per two MFMAs over the first 32
+    auto phase2 = [&](Frag<TN>& fa, Frag<TN>& fb, char* nx, bool copy, int64_t kb, char* st) {
         if (copy) dma(kb, st);
+        load_frag(fa, nx, 0);
 #pragma unroll
         for (int m = 0; m < MPS; m++) mfma(fb, m);
 #pragma unroll
         for (int i = 0; i < 16; i++) {
+            if (copy) __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);
             __builtin_amdgcn_sched_group_barrier(SG_DSR, 1, 0);
-            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(SG_MFMA, 2, 0);
         }
-        if (copy) {
-#pragma unroll
-            for (int i = 0; i < 16; i++) {
-                __builtin_amdgcn_sched_group_barrier(SG_VMEM, 1, 0);
-                __builtin_amdgcn_sched_group_barrier(SG_MFMA, 1, 0);
-            }
-            __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 32, 0);
-        } else {
-            __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 16, 0);
-        }
+        __builtin_amdgcn_sched_group_barrier(SG_MFMA, MPS - 32, 0);
         __builtin_amdgcn_sched_barrier(0);
     };
-
+    // a step that copies block kb into its own stage once done with it; one that copies
+    // nothing; the last step (no barrier)
     Frag<TN> f0, f1;
-    int cur = 0, nxt = STAGE;
-    dma(kb0, cur);
+    auto step_copy = [&](char* cur, char* nxt, int64_t kb) {
+        phase1(f0, f1, cur);
+        handover();
+        phase2(f0, f1, nxt, true, kb, cur);
+    };
+    auto step_nocopy = [&](char* cur, char* nxt) {
+        phase1(f0, f1, cur);
+        handover();
+        phase2(f0, f1, nxt, false, 0, cur);
+    };
+    auto step_final = [&](char* cur) {
+        phase1(f0, f1, cur);
+#pragma unroll
+        for (int m = 0; m < MPS; m++) mfma(f1, m);
+    };
+
+    // stages alternate, and the last two steps always run on st0 then st1: with an odd step
+    // count the first block goes to st1, and one step runs before the paired loop
+    const bool odd = (nsteps & 1) != 0;
+    char* first = odd ? st1 : st0;
+    char* second = odd ? st0 : st1;
+    dma(kb0, first);
     dma_wait();
     __syncthreads();
-    if (nsteps > 1) dma(kb0 + 1, nxt);
-    load_frag(f0, cur, 0);
-    // steps 0 .. nsteps-3 copy block s+2; the last two copy nothing
-    for (int64_t s = 0; s + 2 < nsteps; s++) {
-        phase1(f0, f1, cur);
-        handover();
-        phase2(f0, f1, nxt, true, kb0 + s + 2, cur);
-        const int t = cur;
-        cur = nxt;
-        nxt = t;
+    if (nsteps > 1) dma(kb0 + 1, second);
+    load_frag(f0, first, 0);
+    if (nsteps == 1) {
+        step_final(first);
+    } else {
+        int64_t s = 0;
+        if (odd) {   // nsteps >= 3: block kb0 + 2 exists
+            step_copy(st1, st0, kb0 + 2);
+            s = 1;
+        }
+        // block kb0 + s is in st0 here
+        for (; s + 3 < nsteps; s += 2) {
+            step_copy(st0, st1, kb0 + s + 2);
+            step_copy(st1, st0, kb0 + s + 3);
+        }
+        step_nocopy(st0, st1);
+        step_final(st1);
     }
-    if (nsteps > 1) {
-        phase1(f0, f1, cur);
-        handover();
-        phase2(f0, f1, nxt, false, 0, 0);
-        cur = nxt;
-    }
-    phase1(f0, f1, cur);
-#pragma unroll
-    for (int m = 0; m < MPS; m++) mfma(f1, m);
 
     if (splits == 1) {
         store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
@@ -991,22 +1004,10 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
                             slots + (1 - wi.split) * PART_BYTES, wbase);
 }
 
-constexpr int WS_SMEM = 2 * Tile<256>::STAGE + 2 * BM * 4 + 16;
-
 template <class F>
 hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                          int64_t N, int64_t K, float* c, int64_t ldc, char* ws, int fidx, hipStream_t s) {
-    static bool attr_set[64] = {};
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (!attr_set[dev]) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_ws_kernel<F>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, WS_SMEM);
-        if (e != hipSuccess) return e;
-        attr_set[dev] = true;
-    }
+    hipError_t e = hipSuccess;
     const WsLayout w = ws_layout(M, N, K);
     const int64_t nkb = K / 32;
     int* maxA = reinterpret_cast<int*>(ws + w.max_a);
@@ -1025,7 +1026,7 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     if (e != hipSuccess) return e;
     const int64_t items = w.rta * w.rtb * splits;
     const int64_t grid = (items + 7) / 8 * 8;   // whole XCD shares; surplus workgroups return at once
-    hipLaunchKernelGGL((gemm_ws_kernel<F>), dim3((unsigned)grid), dim3(NTHREADS), WS_SMEM, s, ws + w.planes_a,
+    hipLaunchKernelGGL((gemm_ws_kernel<F>), dim3((unsigned)grid), dim3(NTHREADS), 0, s, ws + w.planes_a,
                        ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt);
     return hipGetLastError();
 }
