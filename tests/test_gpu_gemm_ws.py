@@ -98,9 +98,28 @@ def test_workload_full_size(name):
     A, B = w.operand("a"), w.operand("b")
     say(f"[gemm_ws] workload={name} M={w.M} N={w.N} K={w.K} fmt={w.fmt}")
     Cw, Cf = both(A, B, w.fmt, w.dtype, w.a.axis, w.b.axis)
-    same_bits(Cw, Cf, name)
     rows = np.arange(0, w.M, max(1, w.M // 16))
     cols = np.unique(np.concatenate([np.arange(0, w.N, max(1, w.N // 256)), np.arange(w.N - 32, w.N)]))
     V, tol = oracle_gemm(A, B, w.fmt, w.a.axis, w.b.axis, rows=rows, cols=cols)
     rel = check_gemm(Cw[rows][:, cols], V, tol, name)
     say(f"[gemm_ws] workload={name} rel_frob={rel:.3e}")
+    same_bits(Cw, Cf, name)
+
+
+@pytest.mark.parametrize("shape", [(4352, 4096, 1024), (4300, 4000, 1056), (8192, 2304, 2048)])
+def test_partial_last_round(shape):
+    """More tiles than compute units with a partial last round (272, 272 and 288 tiles of
+    256 x 256; ragged edges and an odd K-block count in the second).  Rows are sampled across
+    every tile row, columns across every tile column and the ragged edge."""
+    M, N, K = shape
+    rng = np.random.default_rng(M + N + K)
+    A = (rng.standard_normal((M, K)) * np.exp2(rng.uniform(-4, 4, (M, 1)))).astype(np.float32)
+    B = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    say(f"[gemm_ws] partial last round M={M} N={N} K={K}")
+    Cw, Cf = both(A, B, "E4C3", "f32")
+    rows = np.unique(np.concatenate([np.arange(0, M, 37), np.arange(M - 8, M)]))
+    cols = np.unique(np.concatenate([np.arange(0, N, 29), np.arange(N - 8, N)]))
+    V, tol = oracle_gemm(A, B, "E4C3", rows=rows, cols=cols)
+    rel = check_gemm(Cw[rows][:, cols], V, tol, f"partial last round {shape}")
+    same_bits(Cw, Cf, f"partial last round {shape}")
+    say(f"[gemm_ws] partial last round rel_frob={rel:.3e}")
