@@ -57,11 +57,16 @@ COPY_BYTES = 256 << 20
 KERNEL_SOURCES = ("gemm.hip", "curvefp_internal.hpp", "device_util.hpp")
 
 
-def kernel_source_digest() -> str:
-    """sha256 over the GEMM kernel's sources: the traffic figure is void once they change."""
+QUANTIZE_SOURCES = ("quantize.hip", "curvefp_internal.hpp", "device_util.hpp")
+STREAM_TRAFFIC = os.path.join(ROOT, "profiles", "quantize_stream_e4c3_1gib_traffic.md")
+
+
+def kernel_source_digest(sources=None) -> str:
+    """sha256 over a kernel's sources (the GEMM's by default): a traffic figure is void once
+    they change."""
     import hashlib
     h = hashlib.sha256()
-    for name in KERNEL_SOURCES:
+    for name in (sources or KERNEL_SOURCES):
         with open(os.path.join(ROOT, "paper_2608_10010_amd", "csrc", name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
@@ -181,6 +186,19 @@ def measured_traffic(workload: str, path: str):
     if kv.get("kernel_source_sha256") != kernel_source_digest():
         return None
     return float(kv["traffic_bytes_per_launch"])
+
+
+def measured_stream_traffic():
+    """HBM bytes of one streaming-quantize launch from the committed counter summary, or None
+    when there is none or the quantize sources changed since it was taken."""
+    try:
+        text = open(STREAM_TRAFFIC).read()
+    except OSError:
+        return None
+    kv = dict(l.split("=", 1) for l in text.splitlines() if "=" in l and " " not in l.split("=", 1)[0])
+    if kv.get("kernel_source_sha256") != kernel_source_digest(QUANTIZE_SOURCES):
+        return None
+    return float(kv["fetch_bytes"]) + float(kv["write_bytes"])
 
 
 def quantize_bytes_per_elem(fmt: str, dtype: str) -> float:
@@ -389,6 +407,7 @@ def main():
             "shape": [32768, 16384], "format": "E4C3", "source_dtype": "bf16",
             "us": t_q * 1e6, "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": gbs / HBM_PEAK_GBS, "bytes_per_elem": quantize_bytes_per_elem("E4C3", "bf16"),
+            "traffic": measured_stream_traffic(),
         }
         del xs, cs, ss
 
