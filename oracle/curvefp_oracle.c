@@ -232,4 +232,67 @@ int oracle_dot_phase_sums(const uint8_t* a, const int8_t* as, const uint8_t* b, 
     return 0;
 }
 
+/*
+ * Mixed-format GEMM (the backward recipe of Sec. 3.3: E5C2 output gradients times reused
+ * E4C3 forward operands).  The paper states the closed product for one K; with binary radix
+ * and curve counts K_x, K_w (powers of two) both indices are lifted to the finer lattice
+ * L = max(K_x, K_w): n'_x = (L / K_x) n_x, n'_w = (L / K_w) n_w, so that each magnitude is
+ * 2^(n' / L) exactly, and the product address is
+ *   u = n'_x + n'_w,  h = u mod L,  t = a_x + a_w + floor(u / L),  delta = (-1)^(s_x xor s_w),
+ * the single-format rule when K_x = K_w.  Scales are per element here (a_scales [M][kd],
+ * b_scales [N][kd]): callers whose blocks lie along k expand them, and operands whose blocks
+ * lie along the other axis (forward codes reused in a backward GEMM) are passed the same way.
+ */
+static void dot_bins_mixed(const fmt_t* fx, const fmt_t* fw, int L, hist_t* hs,
+                           const uint8_t* a, const int8_t* as, const uint8_t* b, const int8_t* bs, int64_t kd) {
+    const int ECx = fx->E + fx->C, ECw = fw->E + fw->C;
+    const int lx = L / fx->K, lw = L / fw->K;
+    for (int64_t k = 0; k < kd; k++) {
+        int ma = a[k] & fx->mag_mask, mb = b[k] & fw->mag_mask;
+        if (ma == 0 || mb == 0) continue;
+        int sx = (a[k] >> ECx) & 1, sw = (b[k] >> ECw) & 1;
+        int u = lx * (ma - fx->B) + lw * (mb - fw->B);
+        int h = floor_mod(u, L);
+        int t = as[k] + bs[k] + floor_div(u, L);
+        int rel = t - hs->t_min;
+        hs->cnt[(size_t)h * hs->t_span + rel] += (sx ^ sw) ? -1 : 1;
+        if (rel < hs->lo) hs->lo = rel;
+        if (rel > hs->hi) hs->hi = rel;
+    }
+}
+
+int oracle_gemm_exact_mixed(const uint8_t* a_codes, const int8_t* a_scales, int Ea, int Ca,
+                            const uint8_t* b_codes, const int8_t* b_scales, int Eb, int Cb,
+                            int64_t M, int64_t N, int64_t kd, double* out, int nthreads, int32_t* max_count) {
+    fmt_t fx, fw, fl;
+    if (make_fmt(Ea, Ca, 1, 1, &fx) || make_fmt(Eb, Cb, 1, 1, &fw) || M < 0 || N < 0 || kd < 0) return -1;
+    const int L = fx.K > fw.K ? fx.K : fw.K;
+    /* bins sized for the lifted lattice: |u| <= lx (B_x - 1) + lw (B_w - 1) */
+    fl.E = 0; fl.C = 0; fl.p = 1; fl.q = 1; fl.K = L; fl.QK = L; fl.g = 1; fl.H = L; fl.mag_mask = 0;
+    fl.B = ((L / fx.K) * (fx.B - 1) + (L / fw.K) * (fw.B - 1) + 1) / 2 + 1;
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+    int32_t gmax = 0;
+    #pragma omp parallel
+    {
+        hist_t hs;
+        hist_init(&hs, &fl);
+        int32_t lmax = 0;
+        #pragma omp for schedule(dynamic, 1)
+        for (int64_t i = 0; i < M; i++) {
+            for (int64_t j = 0; j < N; j++) {
+                dot_bins_mixed(&fx, &fw, L, &hs, a_codes + i * kd, a_scales + i * kd,
+                               b_codes + j * kd, b_scales + j * kd, kd);
+                __float128 v = reduce_bins(&fl, &hs, &lmax, NULL);
+                out[i * N + j] = (double)v;
+                hist_clear(&hs);
+            }
+        }
+        #pragma omp critical
+        { if (lmax > gmax) gmax = lmax; }
+        free(hs.cnt);
+    }
+    if (max_count) *max_count = gmax;
+    return 0;
+}
+
 int oracle_max_threads(void) { return omp_get_max_threads(); }

@@ -55,6 +55,8 @@ def load_library():
         lib.oracle_gemm_exact.restype = I
         lib.oracle_dot_phase_sums.argtypes = [P, P, P, P, I64, I, I, I, I, I, P, P, P]
         lib.oracle_dot_phase_sums.restype = I
+        lib.oracle_gemm_exact_mixed.argtypes = [P, P, I, I, P, P, I, I, I64, I64, I64, P, I, P]
+        lib.oracle_gemm_exact_mixed.restype = I
         lib.oracle_max_threads.restype = I
         _lib = lib
     return _lib
@@ -86,6 +88,56 @@ def gemm_exact(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: int = 3
     if return_max_count:
         return out, int(mc[0])
     return out
+
+
+def gemm_exact_mixed(a_codes, a_scales, fmt_a: Format, b_codes, b_scales, fmt_b: Format,
+                     nthreads: int = 0, return_max_count: bool = False):
+    """Exact GEMM of two operands in different binary-radix formats (the backward recipe of
+    Sec. 3.3), per-element scales: A codes/scales [M, K], B codes/scales [N, K] -> float64
+    [M, N].  Indices are lifted to the finer curve lattice L = max(K_a, K_b) and products
+    are binned at h = u mod L, t = a_x + a_w + floor(u / L) (see curvefp_oracle.c)."""
+    assert fmt_a.p == fmt_a.q == 1 and fmt_b.p == fmt_b.q == 1
+    lib = load_library()
+    a_codes = np.ascontiguousarray(a_codes, dtype=np.uint8)
+    b_codes = np.ascontiguousarray(b_codes, dtype=np.uint8)
+    a_scales = np.ascontiguousarray(a_scales, dtype=np.int8)
+    b_scales = np.ascontiguousarray(b_scales, dtype=np.int8)
+    M, kd = a_codes.shape
+    N, kd2 = b_codes.shape
+    assert kd == kd2 and a_scales.shape == (M, kd) and b_scales.shape == (N, kd)
+    out = np.empty((M, N), dtype=np.float64)
+    mc = np.zeros(1, dtype=np.int32)
+    rc = lib.oracle_gemm_exact_mixed(_ptr(a_codes), _ptr(a_scales), fmt_a.E, fmt_a.C,
+                                     _ptr(b_codes), _ptr(b_scales), fmt_b.E, fmt_b.C,
+                                     M, N, kd, _ptr(out), int(nthreads), _ptr(mc))
+    if rc != 0:
+        raise ValueError("oracle_gemm_exact_mixed rejected its arguments")
+    if return_max_count:
+        return out, int(mc[0])
+    return out
+
+
+def expand_scales(scales, block: int = 32, axis: int = 1):
+    """Per-element scales from block scales: axis 1 repeats each scale `block` times along
+    the last axis (blocks along k); axis 0 takes scales of the transposed operand,
+    [k][rows / block], and returns them as [rows][k] (blocks along the rows)."""
+    s = np.asarray(scales, dtype=np.int8)
+    if axis == 1:
+        return np.repeat(s, block, axis=1)
+    return np.ascontiguousarray(np.repeat(s, block, axis=1).T)
+
+
+def product_address_mixed(code_x: int, a_x: int, fmt_x: Format, code_w: int, a_w: int, fmt_w: Format):
+    """(delta, h, t) of one product of two binary-radix formats on the lattice L = max(K_x,
+    K_w), or None for a zero operand."""
+    L = max(fmt_x.K, fmt_w.K)
+    ex, ew = fmt_x.E + fmt_x.C, fmt_w.E + fmt_w.C
+    mx, mw = code_x & ((1 << ex) - 1), code_w & ((1 << ew) - 1)
+    if mx == 0 or mw == 0:
+        return None
+    sx, sw = (code_x >> ex) & 1, (code_w >> ew) & 1
+    u = (L // fmt_x.K) * (mx - fmt_x.B) + (L // fmt_w.K) * (mw - fmt_w.B)
+    return (-1 if (sx ^ sw) else 1), u % L, a_x + a_w + u // L
 
 
 def phase_bins_one(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: int = 32):

@@ -454,3 +454,106 @@ def test_phase_sums_recombine():
     assert abs(v2 - val) <= 1e-12 * abs(val)
     ref = (_deq_exact64(ca, sa, f) @ _deq_exact64(cb, sb, f).T)[0, 0]
     assert abs(val - ref) <= 1e-12 * abs(ref)
+
+
+# ------------------------------------------------------------------ mixed formats (backward recipe)
+
+MIXED = [("E5C2", "E4C3"), ("E4C3", "E5C2"), ("E5C2", "E3C3")]
+
+
+@pytest.mark.parametrize("pair", MIXED, ids=lambda p: f"{p[0]}x{p[1]}")
+def test_mixed_product_closure_all_pairs(pair):
+    """Sec. 3.3 training protocol (E5C2 gradients x E4C3 forward operands): every pair of
+    nonzero codes of the two formats, both signs, a few scale pairs.  The address on the
+    lattice L = max(K_x, K_w) must give delta 2^t 2^(h/L) equal to the product of the two
+    values built from their own (s, e, k) fields with mpmath; every one of the L phases is
+    occupied."""
+    import mpmath
+    mpmath.mp.dps = 40
+    fx, fw = oracle.get_format(pair[0]), oracle.get_format(pair[1])
+    L = max(fx.K, fw.K)
+
+    def fields(f):
+        mags = np.arange(1, 2 ** (f.E + f.C))
+        codes = np.concatenate([mags, mags | (1 << (f.E + f.C))])
+        nz, s, n = oracle.code_fields(codes, f)
+        return codes, s, np.floor_divide(n, f.K), np.mod(n, f.K)
+
+    cx, sx, ex, kx = fields(fx)
+    cw, sw, ew, kw = fields(fw)
+    phases = set()
+    rng = np.random.default_rng(11)
+    for ax, aw in [(0, 0), (-7, 4)]:
+        for i in range(len(cx)):
+            for j in range(len(cw)):
+                d, h, t = oracle.product_address_mixed(int(cx[i]), ax, fx, int(cw[j]), aw, fw)
+                # independent form: exponents and curve fractions added as rationals
+                q = Fraction(int(ex[i])) + Fraction(int(kx[i]), fx.K) + Fraction(int(ew[j])) + Fraction(int(kw[j]), fw.K)
+                assert Fraction(t - ax - aw) + Fraction(h, L) == q
+                assert 0 <= h < L and d == (-1 if sx[i] ^ sw[j] else 1)
+                phases.add(h)
+        for _ in range(200):
+            i, j = int(rng.integers(0, len(cx))), int(rng.integers(0, len(cw)))
+            d, h, t = oracle.product_address_mixed(int(cx[i]), ax, fx, int(cw[j]), aw, fw)
+            vx = (-1) ** int(sx[i]) * mpmath.power(2, ax + int(ex[i]) + mpmath.mpf(int(kx[i])) / fx.K)
+            vw = (-1) ** int(sw[j]) * mpmath.power(2, aw + int(ew[j]) + mpmath.mpf(int(kw[j])) / fw.K)
+            got = d * mpmath.power(2, t) * mpmath.power(2, mpmath.mpf(h) / L)
+            assert abs(got - vx * vw) <= mpmath.mpf(10) ** -30 * abs(vx * vw)
+    assert phases == set(range(L))
+    assert oracle.product_address_mixed(0, 0, fx, int(cw[5]), 0, fw) is None
+    assert oracle.product_address_mixed(int(cx[5]), 0, fx, 0, 0, fw) is None
+
+
+def test_mixed_equals_single_format_when_formats_agree():
+    """With both operands in one format the lifted rule is the paper's single-format rule:
+    the mixed oracle (per-element scales) must reproduce gemm_exact bit for bit."""
+    rng = np.random.default_rng(12)
+    for name in FMT_NAMES:
+        f = oracle.get_format(name)
+        A = (rng.standard_normal((9, 96)) * np.exp2(rng.uniform(-5, 5, (9, 1)))).astype(np.float32)
+        B = rng.standard_normal((7, 96)).astype(np.float32)
+        ca, sa = oracle.quantize(A, f)
+        cb, sb = oracle.quantize(B, f)
+        C1 = oracle.gemm_exact(ca, sa, cb, sb, f)
+        C2 = oracle.gemm_exact_mixed(ca, oracle.expand_scales(sa), f, cb, oracle.expand_scales(sb), f)
+        assert np.array_equal(C1, C2)
+
+
+@pytest.mark.parametrize("pair", MIXED, ids=lambda p: f"{p[0]}x{p[1]}")
+def test_mixed_gemm_matches_float64_matmul(pair):
+    """Mixed exact GEMM vs numpy float64 matmul of each operand reconstructed in its own
+    format (a textbook route that shares no binning logic)."""
+    fa, fb = oracle.get_format(pair[0]), oracle.get_format(pair[1])
+    rng = np.random.default_rng(13)
+    A = (rng.standard_normal((40, 192)) * np.exp(rng.normal(0, 3, (40, 1)))).astype(np.float32)
+    B = (rng.standard_normal((36, 192)) * 0.02).astype(np.float32)
+    ca, sa = oracle.quantize(A, fa)
+    cb, sb = oracle.quantize(B, fb)
+    C = oracle.gemm_exact_mixed(ca, oracle.expand_scales(sa), fa, cb, oracle.expand_scales(sb), fb)
+    da, db = _deq_exact64(ca, sa, fa), _deq_exact64(cb, sb, fb)
+    ref = da @ db.T
+    absmm = np.abs(da) @ np.abs(db).T
+    assert np.all(np.abs(C - ref) <= 1e-13 * absmm)
+    # the single-format oracle in either format is a different product
+    assert not np.allclose(oracle.gemm_exact(ca, sa, cb, sb, fa), ref, rtol=1e-6, atol=0)
+
+
+def test_mixed_gemm_with_reused_forward_codes():
+    """The backward GEMMs reuse forward codes whose blocks lie along the non-contraction axis
+    (dgrad: W [d_out, d_in] blocked along d_in, contracted over d_out).  B is given as the
+    codes of B^T quantized along B's rows; per-element scales follow the other axis."""
+    fg, fw = oracle.get_format("E5C2"), oracle.get_format("E4C3")
+    rng = np.random.default_rng(14)
+    dY = (rng.standard_normal((24, 128)) * np.exp(rng.normal(0, 2, (24, 1)))).astype(np.float32)   # [tokens, d_out]
+    W = (rng.standard_normal((128, 96)) * 0.02).astype(np.float32)                                  # [d_out, d_in]
+    cg, sg = oracle.quantize(dY, fg)            # blocks along d_out (the contraction)
+    cw, sw = oracle.quantize(W, fw)             # forward codes: blocks along d_in
+    Bc = np.ascontiguousarray(cw.T)             # B = W^T [d_in, d_out] for dX = dY W
+    Bs = oracle.expand_scales(sw, axis=0)       # [d_in, d_out]: scale of the block along d_in
+    C = oracle.gemm_exact_mixed(cg, oracle.expand_scales(sg), fg, Bc, Bs, fw)
+    dg = _deq_exact64(cg, sg, fg)
+    dw = _deq_exact64(cw, sw, fw)               # [d_out, d_in], reconstructed in its own layout
+    ref = dg @ dw
+    absmm = np.abs(dg) @ np.abs(dw)
+    assert C.shape == (24, 96)
+    assert np.all(np.abs(C - ref) <= 1e-13 * absmm)
