@@ -169,6 +169,46 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
                     float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
                     void* stream);
 
+/*
+ * Bytes of device workspace curvefp_gemm_mixed needs for an M x N x K product:
+ * curvefp_gemm_workspace_bytes(M, N, K) plus, per operand, 4 bytes per
+ * (256-row slab of K, 32 padded GEMM rows) for the column maxima of a reused
+ * operand's scales.  CURVEFP_ERR_SHAPE for non-positive sizes or K % 32 != 0.
+ */
+int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * CurveFP GEMM of two operands that may differ in format and in how their
+ * codes are stored: the backward GEMMs of Sec. 3.3, which multiply E5C2 output
+ * gradients Q_G(dY) with the E4C3 codes kept from the forward pass,
+ *   dX = Q_G(dY) Q_W(W)      (A = dY codes, B = the forward W codes, b_trans = 1)
+ *   dW = Q_G(dY)^T Q_A(X)    (A = dY codes, a_trans = 1; B = the forward X codes, b_trans = 1).
+ *   C[M][N] = deq(A)[M][K] . deq(B)[N][K]^T in fp32, c [M][ldc], overwritten.
+ * Operand layouts (per operand, X = A with R = M or X = B with R = N):
+ *   x_trans = 0: the codes and scales curvefp_quantize(block_axis = 1) makes of an
+ *                [R][K] tensor: codes [R][K] (E3C3 [R][K/32][28]), scales [R][K/32];
+ *   x_trans = 1: those it makes of a [K][R] tensor: codes [K][R] (E3C3 [K][R/32][28]),
+ *                scales [K][R/32]; the blocks lie along R, so R % 32 == 0.
+ * Formats a_format, b_format are any of the three.  The product of two curve
+ * values with curve counts K_a, K_b (both powers of two) is a value of the finer
+ * lattice L = max(K_a, K_b): indices lift as n' = (L / K) n, the phase is
+ * h = (n'_a + n'_b) mod L and the carry joins the exponent (Eq. curve-index-product
+ * with one lattice for both); the sum is sum_h 2^{h/L} N_h.  Evaluated on the matrix
+ * cores as in curvefp_gemm_ws: every element is expanded once to an fp16 high/low
+ * pair carrying its own scale relative to its row's largest, with the error bound
+ * stated for curvefp_gemm.  With a_trans = b_trans = 0 and a_format == b_format the
+ * result equals curvefp_gemm_ws's bit for bit.
+ * Errors: as curvefp_gemm_ws, plus CURVEFP_ERR_BLOCK for a trans flag other than
+ * 0/1 and CURVEFP_ERR_SHAPE for a reused operand with R % 32 != 0, more than
+ * 65535 256-row tiles of reused operands, or a workspace smaller than
+ * curvefp_gemm_mixed_workspace_bytes(M, N, K).  The workspace (256-byte aligned)
+ * is scratch: calls that share it must be ordered.
+ */
+int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format, int a_trans,
+                       const void* b_codes, const int8_t* b_scales, int b_format, int b_trans,
+                       int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc,
+                       void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Static description of a status code. */
 const char* curvefp_status_string(int status);
 

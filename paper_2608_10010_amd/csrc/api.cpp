@@ -143,6 +143,32 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
+int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K <= 0 || K % 32) return CURVEFP_ERR_SHAPE;
+    return gemm_mixed_workspace_bytes(M, N, K);
+}
+
+int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format, int a_trans,
+                       const void* b_codes, const int8_t* b_scales, int b_format, int b_trans,
+                       int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc,
+                       void* workspace, int64_t workspace_bytes, void* stream) {
+    if (!a_codes || !a_scales || !b_codes || !b_scales || !c || !workspace) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(a_format) || !fmt_ok(b_format)) return CURVEFP_ERR_FORMAT;
+    if (block != 32 || (a_trans != 0 && a_trans != 1) || (b_trans != 0 && b_trans != 1)) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    // a reused operand has its blocks along its GEMM rows; the expansion grid has one
+    // workgroup row per 256 GEMM rows of each reused operand (at most 65535 in all)
+    if ((a_trans && M % 32) || (b_trans && N % 32)) return CURVEFP_ERR_SHAPE;
+    if ((a_trans ? (M + 255) / 256 : 0) + (b_trans ? (N + 255) / 256 : 0) > 65535) return CURVEFP_ERR_SHAPE;
+    if (workspace_bytes < gemm_mixed_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
+    if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
+    if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_gemm_mixed(a_codes, a_scales, a_format, a_trans, b_codes, b_scales, b_format, b_trans,
+                                        M, N, K, c, ldc, workspace, reinterpret_cast<hipStream_t>(stream)));
+}
+
 const char* curvefp_status_string(int status) {
     switch (status) {
         case CURVEFP_OK: return "ok";

@@ -206,12 +206,13 @@ struct Frag {
 };
 
 // epilogue of a 256 x BN_ tile: D[i][j] of MFMA tile (ti, tj) is register v of lane l with
-// j = l % 32 and i = 8 (v / 4) + 4 (l / 32) + v % 4; C = ldexp(D, alpha_i + beta_j - 2 bias)
-// (exact), stored, or added with fp32 atomics when K is split
+// j = l % 32 and i = 8 (v / 4) + 4 (l / 32) + v % 4; C = ldexp(D, alpha_i + beta_j - BIAS2)
+// (exact; BIAS2 = bias_A + bias_B, the fp16 exponent offsets of the two operands' expansions),
+// stored, or added with fp32 atomics when K is split
 // (ADD: each value is added to the other K half's value of the same element, read from its
 // partial-tile slot at `other`, at wbase in the layout the workspace kernel writes, with
 // device-coherent loads)
-template <class F, int BN_, bool ADD = false>
+template <int BIAS2, int BN_, bool ADD = false>
 __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], const int* sAlpha, const int* sBeta,
                                            float* C, int64_t ldc, int64_t M, int64_t N, int64_t m0, int64_t n0,
                                            int wm, int wn, int lane, bool split,
@@ -232,7 +233,7 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
         bool colok[TN];
 #pragma unroll
         for (int tj = 0; tj < TN; tj++) {
-            beta[tj] = sBeta[lcol + 32 * tj] - 2 * F::GEMM_BIAS;
+            beta[tj] = sBeta[lcol + 32 * tj] - BIAS2;
             colok[tj] = lcol + 32 * tj < colsC;
         }
         // one straight-line store sequence per case (split or not, edge columns or not)
@@ -294,7 +295,7 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
                     const int li = wm * WM + ti * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
                     const int64_t gi = m0 + li;
                     if (gi < M && gj < N) {
-                        float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - 2 * F::GEMM_BIAS);
+                        float val = __builtin_amdgcn_ldexpf(acc[ti][tj][v], sAlpha[li] + beta - BIAS2);
                         if (ADD)
                             val += __builtin_bit_cast(
                                 float, __builtin_amdgcn_raw_buffer_load_b32(
@@ -589,7 +590,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
 #pragma unroll
     for (int m = 0; m < MFMA_PER_SUB; m++) mfma(f1, m);
 
-    store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, gridDim.z > 1);
+    store_tile<2 * F::GEMM_BIAS, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, gridDim.z > 1);
 }
 
 // zero-fill of the output rows (split-K accumulates into C)
@@ -681,15 +682,17 @@ struct ExpandOperand {
     int64_t rows, tiles;      // rows, and row tiles of 256
     const int* rmax;
     char* planes;
+    int fidx;                 // format: which expansion table
 };
 
-// both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B
+// both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B (F fixes the code
+// packing, which both share; each operand brings its own table)
 template <class F>
-__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb, int fidx) {
+__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb) {
     __shared__ uint32_t lut[GEMM_DEC_ENTRIES];
-    lut[threadIdx.x] = g_dec[fidx][threadIdx.x];
     const bool isA = (int64_t)blockIdx.x < 4 * opA.tiles;
     const ExpandOperand& op = isA ? opA : opB;
+    lut[threadIdx.x] = g_dec[op.fidx][threadIdx.x];
     const uint8_t* X = op.codes;
     const int8_t* Xs = op.scales;
     const int64_t R = op.rows, RT = op.tiles;
@@ -782,7 +785,7 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
 //   phase 2: the copy of block s+2 into the stage just freed (buffer-to-LDS loads, 16 per
 //            thread) and the reads of block s+1's first slice go out under the second slice's MFMAs.
 // So each copy has a whole step to land, and the scheduler is held to this interleaving.
-template <class F>
+template <int BIAS2>
 __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     const char* __restrict__ PA, const char* __restrict__ PB, const int* __restrict__ maxA,
     const int* __restrict__ maxB, int64_t M, int64_t N, int64_t K, int64_t RTA, int64_t RTB,
@@ -956,11 +959,11 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     }
 
     if (splits == 1) {
-        store_tile<F, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
+        store_tile<BIAS2, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
         return;
     }
     // K split in two: each half publishes its scaled values (C = ldexp(D, alpha_i + beta_j -
-    // 2 bias), exact) in the tile's slot for that half and counts its arrival; the half that
+    // BIAS2), exact) in the tile's slot for that half and counts its arrival; the half that
     // arrives second adds the other's values to its own (the same fp32 sum as two atomic adds
     // into zero) and stores C.  Slot layout: thread t's acc[ti][tj] quarter q (four floats) at
     // ((((t / 64) * 16 + ti * 4 + tj) * 4 + q) * 1024 + (t % 64) * 16), coalesced 1 KB per store.
@@ -979,7 +982,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
         for (int ti = 0; ti < TM; ti++)
 #pragma unroll
             for (int tj = 0; tj < TN; tj++) {
-                const int beta = sBeta[lcol + 32 * tj] - 2 * F::GEMM_BIAS;
+                const int beta = sBeta[lcol + 32 * tj] - BIAS2;
 #pragma unroll
                 for (int q = 0; q < 4; q++) {
                     const int4 al = *reinterpret_cast<const int4*>(sAlpha + lrow + 32 * ti + 8 * q);
@@ -1000,8 +1003,200 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
         sLast[0] = __hip_atomic_fetch_add(cnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
     __syncthreads();
     if (!sLast[0]) return;   // uniform: the other half arrives later and finishes the tile
-    store_tile<F, BN, true>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false,
+    store_tile<BIAS2, BN, true>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false,
                             slots + (1 - wi.split) * PART_BYTES, wbase);
+}
+
+// ---------------------------------------------------------------------------------------------
+// Mixed formats and reused forward operands (the backward recipe of Sec. 3.3: E5C2 output
+// gradients times the E4C3 codes kept from the forward pass).
+//
+// An operand is either the codes of an [R][K] tensor quantized along K (as above), or the codes
+// of a [K][R] tensor quantized along R: a forward operand reused by a backward GEMM, whose
+// block scales then run along the GEMM's rows, so the scale changes from element to element
+// along k.  The expansion is the same but for the multiplier 2^-D, D = alpha_row - a, which is
+// taken per element; the planes, and so the GEMM kernel, do not change.  Two formats need
+// nothing else: each operand goes through its own format's table, the matrix cores multiply
+// the values (the lift of both curve indices to the finer lattice is implicit in the values),
+// and the epilogue removes the sum of the two operands' exponent offsets.
+//
+// Workspace: the single-format layout, then per operand the partial column maxima of a
+// [K][R/32] scale matrix over slabs of 256 k-rows, [ceil(K/256)][RT * 8] int32.
+constexpr int PREP_SLAB = 256;
+
+struct MixedLayout {
+    WsLayout w;
+    int64_t nslab, colpart_a, colpart_b, bytes;
+};
+
+MixedLayout mixed_layout(int64_t M, int64_t N, int64_t K) {
+    MixedLayout x;
+    x.w = ws_layout(M, N, K);
+    x.nslab = (K + PREP_SLAB - 1) / PREP_SLAB;
+    x.colpart_a = (x.w.bytes + 255) & ~(int64_t)255;
+    x.colpart_b = x.colpart_a + ((x.nslab * x.w.rta * 8 * 4 + 255) & ~(int64_t)255);
+    x.bytes = x.colpart_b + x.nslab * x.w.rtb * 8 * 4;
+    return x;
+}
+
+struct PrepOperand {
+    const int8_t* scales;
+    int64_t rows, tiles, K;
+    int trans;
+    int groups;     // workgroups of this operand
+    int cgroups;    // trans: groups of 64 scale columns covering the tiles' tiles * 8 columns
+    int* rmax;      // not trans: row maxima [tiles * 256], 0 past the last row
+    int* colpart;   // trans: partial column maxima [nslab][tiles * 8]
+};
+
+// one launch before the expansion: for an operand quantized along K, the row maxima of its block
+// scales (16 lanes per row, as prep_kernel); for a reused operand, the maxima of each scale
+// column over a slab of 256 k-rows (64 columns x 4 parts of 64 k-rows per workgroup, a wave
+// reading 64 consecutive scale bytes of one k-row).  One more workgroup zeroes the per-tile
+// arrival counters when K is split.
+__global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOperand pb, int* __restrict__ cnt,
+                                                         int ncnt) {
+    __shared__ int red[256];
+    const int bid = (int)blockIdx.x, t = (int)threadIdx.x;
+    if (bid >= pa.groups + pb.groups) {
+        for (int i = t; i < ncnt; i += 256) cnt[i] = 0;
+        return;
+    }
+    const bool isA = bid < pa.groups;
+    const PrepOperand& p = isA ? pa : pb;
+    const int g = isA ? bid : bid - pa.groups;
+    if (!p.trans) {
+        const int64_t nkb = p.K / 32;
+        const int64_t row = (int64_t)g * 16 + (t >> 4);
+        const int part = t & 15;
+        int m = -128;
+        if (row < p.rows) {
+            const int8_t* sp = p.scales + row * nkb;
+#pragma unroll 8
+            for (int64_t kb = part; kb < nkb; kb += 16) m = max(m, (int)sp[kb]);
+        }
+#pragma unroll
+        for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
+        if (part == 0) p.rmax[row] = row < p.rows ? m : 0;   // the grid covers exactly the padded rows
+        return;
+    }
+    const int64_t J = p.rows / 32, J8 = p.tiles * 8;
+    const int cg = g % p.cgroups, slab = g / p.cgroups;
+    const int64_t j = (int64_t)cg * 64 + (t & 63);
+    const int64_t k0 = (int64_t)slab * PREP_SLAB + (t >> 6) * 64;
+    int m = -128;
+    if (j < J) {
+        const int8_t* sp = p.scales + j;
+        const int64_t kend = min(k0 + 64, p.K);
+#pragma unroll 8
+        for (int64_t k = k0; k < kend; k++) m = max(m, (int)sp[k * J]);
+    }
+    red[t] = m;
+    __syncthreads();
+    if (t < 64 && j < J8)
+        p.colpart[(int64_t)slab * J8 + j] = max(max(red[t], red[t + 64]), max(red[t + 128], red[t + 192]));
+}
+
+struct ExpandTOperand {
+    const uint8_t* codes;    // [K][ld] bytes: codes of a [K][R] tensor quantized along R
+    const int8_t* scales;    // [K][R / 32]
+    int64_t rows, tiles, ld; // R, row tiles of 256, bytes per k-row (R, or R / 32 * 28 packed)
+    const int* colpart;      // partial column maxima [nslab][tiles * 8]
+    int64_t nslab;
+    int* rmax;               // row maxima [tiles * 256], written by the first K block's workgroups
+    char* planes;
+    int fidx;
+};
+
+// expansion of a reused operand: one workgroup per (K block, tile of 256 rows).  The 32 k-rows
+// x 256 codes are read with coalesced dword loads into LDS (pitch one dword over the row, so the
+// four 8-wide k-chunks a wave reads fall on different banks), the block scales transposed into
+// [8 scale columns][32 k].  Thread t then writes chunk q = t % 4 (k = 8q .. 8q + 7) of rows
+// t / 4 + 64 i, i < 4, into both planes: each store of a wave covers 16 whole 64-byte rows.
+// Every element is scaled by 2^-min(D, 24) and then by 2^-min(max(D - 24, 0), 24) (a multiply
+// by one when D <= 24), the two multiplies of the K-layout expansion with D taken per element.
+template <bool P7>
+__global__ __launch_bounds__(256) void expand_t_kernel(ExpandTOperand opA, ExpandTOperand opB) {
+    constexpr int TB = P7 ? 224 : 256;   // code bytes of one k-row of a 256-row tile
+    constexpr int DPR = TB / 4;          // dwords per k-row
+    constexpr int PITCH = DPR + 1;
+    __shared__ uint32_t lut[GEMM_DEC_ENTRIES];
+    __shared__ uint32_t tile[32 * PITCH];
+    __shared__ __attribute__((aligned(16))) int8_t scT[8 * 32];
+    __shared__ int alpha_s[8];
+    const int t = (int)threadIdx.x;
+    const bool isA = (int64_t)blockIdx.y < opA.tiles;
+    const ExpandTOperand& op = isA ? opA : opB;
+    lut[t] = g_dec[op.fidx][t];
+    const int64_t rt = isA ? (int64_t)blockIdx.y : (int64_t)blockIdx.y - opA.tiles;
+    const int64_t kb = blockIdx.x;
+    const int64_t R = op.rows, J = R / 32, J8 = op.tiles * 8;
+    const int vrows = (int)min((int64_t)256, R - rt * 256);   // a multiple of 32
+    const int vdw = P7 ? vrows / 32 * 7 : vrows / 4;           // valid dwords of a k-row
+    const uint8_t* src = op.codes + kb * 32 * op.ld + rt * TB;
+#pragma unroll
+    for (int i = 0; i < 32 * DPR / 256; i++) {
+        const int d = t + 256 * i;
+        const int k = d / DPR, c = d - k * DPR;
+        uint32_t v = 0;
+        if (c < vdw) v = *reinterpret_cast<const uint32_t*>(src + k * op.ld + 4 * c);
+        tile[k * PITCH + c] = v;
+    }
+    {
+        const int k = t >> 3, j = t & 7;
+        int s = -128;
+        if (32 * j < vrows) s = op.scales[(kb * 32 + k) * J + rt * 8 + j];
+        scT[j * 32 + k] = (int8_t)s;
+    }
+    {
+        // the row maxima of this tile's 8 scale columns, finished from the slab partials
+        const int j = t >> 5, l = t & 31;
+        int m = -128;
+        for (int64_t sl = l; sl < op.nslab; sl += 32) m = max(m, op.colpart[sl * J8 + rt * 8 + j]);
+#pragma unroll
+        for (int o = 16; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 32));
+        if (l == 0) alpha_s[j] = 32 * j < vrows ? m : 0;
+    }
+    __syncthreads();
+    if (kb == 0) op.rmax[rt * 256 + t] = alpha_s[t >> 5];
+    const int q = t & 3, rb = t >> 2;
+    const uint8_t* tb = reinterpret_cast<const uint8_t*>(tile);
+    char* base = op.planes + (kb * op.tiles + rt) * (2 * PLANE);
+#pragma unroll
+    for (int i = 0; i < 4; i++) {
+        const int r = rb + 64 * i, j = r >> 5;
+        const int alpha = alpha_s[j];
+        const uint2 sv = *reinterpret_cast<const uint2*>(scT + j * 32 + 8 * q);
+        uint32_t e[8], m1[8], m2[8];
+#pragma unroll
+        for (int x = 0; x < 8; x++) {
+            const int k = 8 * q + x;
+            uint32_t code;
+            if (!P7) {
+                code = tb[k * PITCH * 4 + r];
+            } else {
+                const int bit = 224 * j + 7 * (r & 31);
+                const int byte = k * PITCH * 4 + (bit >> 3);
+                code = ((uint32_t)tb[byte] | ((uint32_t)tb[byte + 1] << 8)) >> (bit & 7) & 0x7Fu;
+            }
+            e[x] = lut[code];
+            const int a = (int)__builtin_amdgcn_sbfe(x < 4 ? sv.x : sv.y, 8 * (x & 3), 8);
+            const int D = alpha - a;
+            m1[x] = f16_pow2_neg(min(max(D, 0), 24));
+            m2[x] = f16_pow2_neg(min(max(D - 24, 0), 24));
+        }
+        uint32_t hv[4], lv[4];
+#pragma unroll
+        for (int p = 0; p < 4; p++) {
+            const half2v s1 = __builtin_bit_cast(half2v, m1[2 * p] | (m1[2 * p + 1] << 16));
+            const half2v s2 = __builtin_bit_cast(half2v, m2[2 * p] | (m2[2 * p + 1] << 16));
+            hv[p] = pk_mul(pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x05040100u), s1), s2);
+            lv[p] = pk_mul(pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x07060302u), s1), s2);
+        }
+        char* dst = base + swz(r, q);
+        *reinterpret_cast<uint4*>(dst) = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+        *reinterpret_cast<uint4*>(dst + PLANE) = make_uint4(lv[0], lv[1], lv[2], lv[3]);
+    }
 }
 
 template <class F>
@@ -1018,17 +1213,113 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
     hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
                        nkb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
-    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a};
-    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b};
+    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx};
+    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
-                       dim3(256), 0, s, opA, opB, nkb, fidx);
+                       dim3(256), 0, s, opA, opB, nkb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t items = w.rta * w.rtb * splits;
     const int64_t grid = (items + 7) / 8 * 8;   // whole XCD shares; surplus workgroups return at once
-    hipLaunchKernelGGL((gemm_ws_kernel<F>), dim3((unsigned)grid), dim3(NTHREADS), 0, s, ws + w.planes_a,
+    hipLaunchKernelGGL((gemm_ws_kernel<2 * F::GEMM_BIAS>), dim3((unsigned)grid), dim3(NTHREADS), 0, s, ws + w.planes_a,
                        ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt);
     return hipGetLastError();
+}
+
+// fp16 exponent offset of a format's expansion (the row's largest element lands near 2^15)
+int gemm_bias(int f) { return f == 0 ? FmtE4C3::GEMM_BIAS : f == 1 ? FmtE5C2::GEMM_BIAS : FmtE3C3::GEMM_BIAS; }
+
+hipError_t launch_gemm_ws_bias(int bias2, dim3 grid, hipStream_t s, const char* pa, const char* pb, const int* maxA,
+                               const int* maxB, int64_t M, int64_t N, int64_t K, int64_t rta, int64_t rtb, float* c,
+                               int64_t ldc, int splits, char* part, int* cnt) {
+    constexpr int E4 = FmtE4C3::GEMM_BIAS, E5 = FmtE5C2::GEMM_BIAS, E3 = FmtE3C3::GEMM_BIAS;
+#define CURVEFP_WS_GEMM(B2)                                                                                     \
+    case B2:                                                                                                  \
+        hipLaunchKernelGGL((gemm_ws_kernel<B2>), grid, dim3(NTHREADS), 0, s, pa, pb, maxA, maxB, M, N, K, rta, \
+                           rtb, c, ldc, splits, part, cnt);                                                   \
+        break;
+    static_assert(E4 + E5 != 2 * E4 && E4 + E3 != 2 * E3 && E5 + E3 != 2 * E5 && E4 + E5 != E5 + E3 &&
+                      E4 + E3 != 2 * E5 && E5 + E3 != 2 * E4,
+                  "distinct bias sums");
+    switch (bias2) {
+        CURVEFP_WS_GEMM(2 * E4)
+        CURVEFP_WS_GEMM(2 * E5)
+        CURVEFP_WS_GEMM(2 * E3)
+        CURVEFP_WS_GEMM(E4 + E5)
+        CURVEFP_WS_GEMM(E4 + E3)
+        CURVEFP_WS_GEMM(E5 + E3)
+        default: return hipErrorInvalidValue;
+    }
+#undef CURVEFP_WS_GEMM
+    return hipGetLastError();
+}
+
+hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
+                        int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, char* ws, hipStream_t s) {
+    const MixedLayout x = mixed_layout(M, N, K);
+    const WsLayout& w = x.w;
+    const int64_t nkb = K / 32;
+    int* maxA = reinterpret_cast<int*>(ws + w.max_a);
+    int* maxB = reinterpret_cast<int*>(ws + w.max_b);
+    int* cnt = reinterpret_cast<int*>(ws + w.cnt);
+    const int64_t tiles = w.rta * w.rtb;
+    const int splits = w.splits;
+    auto prep_op = [&](const int8_t* sc, int64_t R, int64_t RT, int tr, int* rmax, int64_t colpart) {
+        PrepOperand p;
+        p.scales = sc;
+        p.rows = R;
+        p.tiles = RT;
+        p.K = K;
+        p.trans = tr;
+        p.cgroups = (int)((RT * 8 + 63) / 64);
+        p.groups = tr ? (int)(p.cgroups * x.nslab) : (int)(RT * 16);
+        p.rmax = rmax;
+        p.colpart = reinterpret_cast<int*>(ws + colpart);
+        return p;
+    };
+    const PrepOperand pa = prep_op(as, M, w.rta, ta, maxA, x.colpart_a);
+    const PrepOperand pb = prep_op(bs, N, w.rtb, tb, maxB, x.colpart_b);
+    hipLaunchKernelGGL(prep_mixed_kernel, dim3((unsigned)(pa.groups + pb.groups + (splits > 1 ? 1 : 0))), dim3(256), 0,
+                       s, pa, pb, cnt, (int)(splits > 1 ? tiles : 0));
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+
+    // expansions: operands that share a kind (along K, or reused) and a code packing share a launch
+    const bool p7a = fa == 2, p7b = fb == 2;
+    const ExpandOperand ka = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fa};
+    const ExpandOperand kbo = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fb};
+    auto ld_of = [](int f, int64_t R) { return f == 2 ? R / 32 * 28 : R; };
+    const ExpandTOperand xa = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, ld_of(fa, M),
+                               reinterpret_cast<const int*>(ws + x.colpart_a), x.nslab, maxA, ws + w.planes_a, fa};
+    const ExpandTOperand xb = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, ld_of(fb, N),
+                               reinterpret_cast<const int*>(ws + x.colpart_b), x.nslab, maxB, ws + w.planes_b, fb};
+    auto expand_k = [&](const ExpandOperand& o1, const ExpandOperand& o2, bool p7) {
+        const dim3 grid((unsigned)(4 * (o1.tiles + o2.tiles)), (unsigned)((nkb + 3) / 4));
+        if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb);
+        else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, o1, o2, nkb);
+        return hipGetLastError();
+    };
+    auto expand_t = [&](const ExpandTOperand& o1, const ExpandTOperand& o2, bool p7) {
+        const dim3 grid((unsigned)nkb, (unsigned)(o1.tiles + o2.tiles));
+        if (p7) hipLaunchKernelGGL((expand_t_kernel<true>), grid, dim3(256), 0, s, o1, o2);
+        else hipLaunchKernelGGL((expand_t_kernel<false>), grid, dim3(256), 0, s, o1, o2);
+        return hipGetLastError();
+    };
+    ExpandOperand kn = ka;
+    kn.tiles = 0;   // an absent second operand: no workgroups
+    ExpandTOperand xn = xa;
+    xn.tiles = 0;
+    if (ta == tb && p7a == p7b) {
+        e = ta ? expand_t(xa, xb, p7a) : expand_k(ka, kbo, p7a);
+    } else {
+        e = ta ? expand_t(xa, xn, p7a) : expand_k(ka, kn, p7a);
+        if (e == hipSuccess) e = tb ? expand_t(xb, xn, p7b) : expand_k(kbo, kn, p7b);
+    }
+    if (e != hipSuccess) return e;
+    const int64_t items = tiles * splits;
+    const dim3 grid((unsigned)((items + 7) / 8 * 8));
+    return launch_gemm_ws_bias(gemm_bias(fa) + gemm_bias(fb), grid, s, ws + w.planes_a, ws + w.planes_b, maxA, maxB,
+                               M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt);
 }
 
 template <class F, int BN_>
@@ -1075,6 +1366,13 @@ hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8
 }  // namespace
 
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout(M, N, K).bytes; }
+
+int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) { return mixed_layout(M, N, K).bytes; }
+
+hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
+                             int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, void* ws, hipStream_t s) {
+    return launch_mixed(a, as, fa, ta, b, bs, fb, tb, M, N, K, c, ldc, reinterpret_cast<char*>(ws), s);
+}
 
 hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                           int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s) {

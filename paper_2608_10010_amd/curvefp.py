@@ -61,6 +61,10 @@ def lib() -> ctypes.CDLL:
         L.curvefp_gemm_workspace_bytes.restype = I64
         L.curvefp_gemm_ws.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P, I64, P]
         L.curvefp_gemm_ws.restype = I
+        L.curvefp_gemm_mixed_workspace_bytes.argtypes = [I64, I64, I64]
+        L.curvefp_gemm_mixed_workspace_bytes.restype = I64
+        L.curvefp_gemm_mixed.argtypes = [P, P, I, I, P, P, I, I, I64, I64, I64, I, P, I64, P, I64, P]
+        L.curvefp_gemm_mixed.restype = I
         L.curvefp_status_string.argtypes = [I]
         L.curvefp_status_string.restype = ctypes.c_char_p
         _lib = L
@@ -183,4 +187,35 @@ def curvefp_gemm_ws(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torc
                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                _stream(stream))
     _check(st, "curvefp_gemm_ws")
+    return c
+
+
+def curvefp_gemm_mixed_workspace_bytes(M: int, N: int, K: int) -> int:
+    n = lib().curvefp_gemm_mixed_workspace_bytes(M, N, K)
+    if n < 0:
+        raise CurveFPError(n, "curvefp_gemm_mixed_workspace_bytes")
+    return n
+
+
+def gemm_mixed_workspace(M: int, N: int, K: int, device) -> torch.Tensor:
+    """A device buffer large enough for curvefp_gemm_mixed."""
+    return torch.empty(curvefp_gemm_mixed_workspace_bytes(M, N, K), dtype=torch.uint8, device=device)
+
+
+def curvefp_gemm_mixed(a_codes: torch.Tensor, a_scales: torch.Tensor, fmt_a, a_trans: int,
+                       b_codes: torch.Tensor, b_scales: torch.Tensor, fmt_b, b_trans: int,
+                       M: int, N: int, K: int, block: int = 32, c: Optional[torch.Tensor] = None,
+                       workspace: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T for operands of any two formats.  x_trans = 0:
+    codes/scales of an [R, K] tensor quantized along K; x_trans = 1: those of a [K, R] tensor
+    quantized along R (forward codes reused by a backward GEMM)."""
+    if c is None:
+        c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    if workspace is None:
+        workspace = gemm_mixed_workspace(M, N, K, a_codes.device)
+    st = lib().curvefp_gemm_mixed(a_codes.data_ptr(), a_scales.data_ptr(), _fmt(fmt_a), int(a_trans),
+                                  b_codes.data_ptr(), b_scales.data_ptr(), _fmt(fmt_b), int(b_trans),
+                                  M, N, K, block, c.data_ptr(), c.stride(0), workspace.data_ptr(),
+                                  workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, "curvefp_gemm_mixed")
     return c

@@ -71,6 +71,7 @@ class Operand:
     make: Callable[[int], np.ndarray]
     seed: int
     axis: int = 1                   # 1: blocks along cols; 0: blocks along rows (transpose)
+    trans: int = 0                  # 1: the quantized codes are [K][rows of the GEMM] (reused forward codes)
 
 
 @dataclass
@@ -84,6 +85,7 @@ class Workload:
     N: int
     K: int
     note: str = ""
+    fmt_b: Optional[str] = None     # B's format when it differs from A's (mixed backward GEMMs)
     _cache: Dict[str, np.ndarray] = field(default_factory=dict, repr=False)
 
     def operand(self, which: str) -> np.ndarray:
@@ -96,6 +98,10 @@ class Workload:
                 x = bf16_round(x)
             self._cache[which] = x
         return self._cache[which]
+
+    def fmt_of(self, which: str) -> str:
+        """Format of operand "a" or "b"."""
+        return self.fmt if which == "a" else (self.fmt_b or self.fmt)
 
     def flops(self) -> float:
         return 2.0 * self.M * self.N * self.K
@@ -141,6 +147,30 @@ def _wgrad():
               4096, 11008, 4096, "dW = X^T . dY; both quantized along tokens (axis 0)")
 
 
+def _dgrad_mixed():
+    # the paper's backward recipe: E5C2 output gradients times the E4C3 forward codes of W
+    # (the 7B up-projection's W, quantized along K = 4096 in the forward pass, reused)
+    w = _w("dgrad_mixed_e5c2xe4c3_4096x4096x11008", "E5C2", "bf16",
+           Operand("dY", (4096, 11008), lambda s: lognormal_rows((4096, 11008), s), 4001),
+           Operand("W", (4096, 11008), lambda s: normal((4096, 11008), 0.02, s), 3002, axis=0, trans=1),
+           4096, 4096, 11008,
+           "dX = Q_G(dY) Q_W(W); dY E5C2 along its rows; W's forward E4C3 codes [11008][4096] reused")
+    w.fmt_b = "E4C3"
+    return w
+
+
+def _wgrad_mixed():
+    # dW = Q_G(dY)^T Q_A(X): dY quantized once (E5C2, along its rows, as for dX), X's forward
+    # E4C3 codes reused; both contract over the 4096 tokens
+    w = _w("wgrad_mixed_e5c2xe4c3_11008x4096x4096", "E5C2", "bf16",
+           Operand("dY", (4096, 11008), lambda s: lognormal_rows((4096, 11008), s), 4001, trans=1),
+           Operand("X", (4096, 4096), lambda s: normal((4096, 4096), 1.0, s), 3001, trans=1),
+           11008, 4096, 4096,
+           "dW = Q_G(dY)^T Q_A(X); both codes [tokens][rows of the GEMM], blocks along the rows")
+    w.fmt_b = "E4C3"
+    return w
+
+
 _SWEEP = {  # name: (N, K) for 8192 tokens
     "qkv": (6144, 4096),
     "o": (4096, 4096),
@@ -164,6 +194,8 @@ def all_workloads() -> Dict[str, Callable[[], Workload]]:
         "fwd": _fwd,
         "dgrad": _dgrad,
         "wgrad": _wgrad,
+        "dgrad_mixed": _dgrad_mixed,
+        "wgrad_mixed": _wgrad_mixed,
     }
     for layer in _SWEEP:
         for fmt in ("E4C3", "E5C2", "E3C3"):

@@ -97,3 +97,34 @@ def check_gemm(C_dev: np.ndarray, V: np.ndarray, tol: np.ndarray, what: str, fro
             assert rel <= 1e-5, f"{what}: relative Frobenius error {rel}"
         return rel
     return 0.0
+
+
+# ---------------------------------------------------------------- mixed formats, per-element scales
+
+def exact_values_elem(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.ndarray:
+    """float64 values 2^{a + n/K} of codes [R][K] with per-element scales [R][K]."""
+    f = oracle.get_format(fmt)
+    nz, s, n = oracle.code_fields(codes, f)
+    a = scales.astype(np.int64)
+    a = np.where(a == oracle.POISON_SCALE, 0, a)
+    v = np.ldexp(oracle.level_value_f64(f, np.where(nz, n, 0)), a)
+    return np.where(nz, np.where(s == 1, -v, v), 0.0)
+
+
+def row_tops_elem(scales: np.ndarray, fmt: str) -> np.ndarray:
+    f = oracle.get_format(fmt)
+    e_max = 2 ** (f.E - 1) - 1
+    sc = scales.astype(np.int64)
+    alpha = np.max(np.where(sc == oracle.POISON_SCALE, -127, sc), axis=1)
+    return np.ldexp(1.0, alpha + e_max + 1)
+
+
+def gemm_tolerance_mixed(ca, sa, fa, cb, sb, fb):
+    """gemm_tolerance for operands of two formats with per-element scales: each operand's
+    elements are expanded relative to the top of its own row's scale range, with its own
+    format's largest exponent."""
+    va, vb = np.abs(exact_values_elem(ca, sa, fa)), np.abs(exact_values_elem(cb, sb, fb))
+    S = va @ vb.T
+    ta, tb = row_tops_elem(sa, fa), row_tops_elem(sb, fb)
+    flush = ta[:, None] * vb.sum(1)[None, :] + va.sum(1)[:, None] * tb[None, :]
+    return 1e-5 * S + 2.0 ** -38 * flush + 2.0 ** -148

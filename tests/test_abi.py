@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 10
+    assert len(names) == 12
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -147,3 +147,46 @@ def test_gemm_ws_validation(L):
     assert g(*bad) == EFMT
     bad = list(args); bad[6] = 40
     assert g(*bad) == ESHAPE
+
+
+def test_gemm_mixed_validation(L):
+    assert L.curvefp_gemm_mixed_workspace_bytes(0, 64, 64) == ESHAPE
+    assert L.curvefp_gemm_mixed_workspace_bytes(64, 64, 48) == ESHAPE
+    base = L.curvefp_gemm_workspace_bytes(10, 300, 64)
+    mixed = L.curvefp_gemm_mixed_workspace_bytes(10, 300, 64)
+    # the single-format layout, 256-aligned, then one slab (K <= 256) of column maxima per
+    # operand: 8 columns per 256-row tile, int32 (A: 1 tile, padded to 256 bytes; B: 2 tiles)
+    assert mixed == ((base + 255) // 256) * 256 + 256 + 2 * 8 * 4
+    assert L.curvefp_gemm_mixed_workspace_bytes(256, 256, 1024) >= L.curvefp_gemm_workspace_bytes(256, 256, 1024)
+    need = L.curvefp_gemm_mixed_workspace_bytes(64, 64, 64)
+    WS = 1 << 24
+    g = L.curvefp_gemm_mixed
+    #       a     as    fa tA b     bs    fb tB  M   N   K  blk c     ldc ws  bytes  stream
+    args = [FAKE, FAKE, 1, 0, FAKE, FAKE, 0, 1, 64, 64, 64, 32, FAKE, 64, WS, need, None]
+    for i in (0, 1, 4, 5, 12, 14):
+        a = list(args)
+        a[i] = None
+        assert g(*a) == ENULL, i
+    for i, v in ((2, 3), (6, -1)):
+        bad = list(args); bad[i] = v
+        assert g(*bad) == EFMT, (i, v)
+    for i, v in ((3, 2), (7, -1), (11, 16)):
+        bad = list(args); bad[i] = v
+        assert g(*bad) == EBLOCK, (i, v)
+    for i, v in ((8, 0), (9, -1), (10, 48), (13, 32), (15, need - 1)):
+        bad = list(args); bad[i] = v
+        assert g(*bad) == ESHAPE, (i, v)
+    # a reused operand (trans) needs its rows in whole blocks of 32
+    bad = list(args); bad[9] = 40
+    assert g(*bad) == ESHAPE
+    bad = list(args); bad[3] = 1; bad[8] = 48
+    assert g(*bad) == ESHAPE
+    ok = list(args); ok[8] = 48                       # M % 32 != 0 is fine when A is not reused
+    ok[15] = L.curvefp_gemm_mixed_workspace_bytes(48, 64, 64)
+    ok[0] = MIS
+    assert g(*ok) == EALIGN                           # ... and reaches the alignment checks
+    for i in (0, 4, 12):
+        bad = list(args); bad[i] = MIS
+        assert g(*bad) == EALIGN, i
+    bad = list(args); bad[14] = WS + 64
+    assert g(*bad) == EALIGN
