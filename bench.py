@@ -14,8 +14,11 @@ allocation-free curvefp_gemm instead.  Per-call times come from HIP events
 recorded on the stream the library launches on.  The roofline object is for the
 GEMM call (the dominant part: its expansion and GEMM kernels together).
 A separate streaming quantize case (1 GiB bf16 source, larger than the 256 MB
-Infinity Cache) gives the HBM figure for the quantizer.  The CPU oracle is timed
-on a bounded row sample of the same workload as `cpu_baseline`.
+Infinity Cache) gives the HBM figure for the quantizer, and the two backward
+GEMMs of the 7B up-projection as the paper runs them (E5C2 output gradients
+times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
+`backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
+workload as `cpu_baseline`.
 """
 
 import argparse
@@ -44,6 +47,8 @@ def parse():
                         "the GEMM kernel, no workspace)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-stream", action="store_true")
+    p.add_argument("--no-backward", action="store_true",
+                   help="skip the mixed-format backward GEMMs (E5C2 gradients x reused E4C3 codes)")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 256 MiB device copy three times (counter calibration)")
@@ -146,9 +151,11 @@ def summarize_pmc(args):
         "",
         "```",
         f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_{args.gemm} -o pmc -- "
-        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration --gemm {args.gemm}",
+        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --no-backward --copy-calibration "
+        f"--gemm {args.gemm}",
         f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_{args.gemm} -o pmc -- "
-        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --copy-calibration --gemm {args.gemm}",
+        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --no-backward --copy-calibration "
+        f"--gemm {args.gemm}",
         f"python bench.py --summarize-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}{flag}",
         "```",
         "",
@@ -252,6 +259,60 @@ def cpu_baseline(w, seconds: float):
                   f"{nthreads} threads; value = 2*{ra}*{rb}*{w.K} flop / wall",
         "seconds": t,
     }
+
+
+def backward_mixed(cf, W, dev, stream, reps: int = 10):
+    """dX = Q_G(dY) Q_W(W) and dW = Q_G(dY)^T Q_A(X) of the 7B up-projection: dY quantized once
+    in E5C2 along its rows, W and X as their forward E4C3 codes.  Each GEMM call (prep,
+    expansions, MFMA GEMM) is timed with HIP events on the library's stream: median of `reps`
+    individually timed calls after warm-up.  Operands are quantized before timing."""
+    import numpy as np
+    import torch
+
+    out = {}
+    src = {}
+    for name in ("dgrad_mixed", "wgrad_mixed"):
+        w = W.get(name)
+        ops = []
+        for which, op in (("a", w.a), ("b", w.b)):
+            key = (op.seed, op.axis)
+            if key not in src:
+                x = torch.from_numpy(w.operand(which)).to(torch.bfloat16).to(dev)
+                src[key] = cf.curvefp_quantize(x, w.fmt_of(which), block_axis=op.axis)
+                del x
+            ops.append(src[key])
+        (ca, sa), (cb, sb) = ops
+        C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+        ws = cf.gemm_mixed_workspace(w.M, w.N, w.K, dev)
+
+        def call():
+            cf.curvefp_gemm_mixed(ca, sa, w.fmt_of("a"), w.a.trans, cb, sb, w.fmt_of("b"), w.b.trans,
+                                  w.M, w.N, w.K, c=C, workspace=ws)
+
+        for _ in range(3):
+            call()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            call()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        t = float(np.median(ts))
+        tf = w.flops() / t / 1e12
+        out[name.split("_")[0]] = {
+            "workload": w.name, "M": w.M, "N": w.N, "K": w.K,
+            "formats": f"{w.fmt_of('a')} x {w.fmt_of('b')}", "trans": [w.a.trans, w.b.trans],
+            "us": t * 1e6, "achieved": tf, "peak": F16_DENSE_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": tf / F16_DENSE_PEAK_TFLOPS, "mfma_pipe_frac": 3.0 * tf / F16_DENSE_PEAK_TFLOPS,
+            "timing": f"median of {reps} individually timed curvefp_gemm_mixed calls",
+        }
+        del C, ws
+    src.clear()
+    torch.cuda.empty_cache()
+    return out
 
 
 def main():
@@ -427,6 +488,9 @@ def main():
             "us_back_to_back": t_b2b * 1e6, "achieved_back_to_back": nbytes / t_b2b / 1e9,
         }
         del xs, cs, ss
+
+    if not args.no_backward:
+        result["backward_mixed"] = backward_mixed(cf, W, dev, stream)
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
