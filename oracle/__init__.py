@@ -37,6 +37,7 @@ from .quant import (
 from .gemm import (
     gemm_exact,
     gemm_exact_mixed,
+    mixed_lattice,
     expand_scales,
     product_address_mixed,
     gemm_exact_python,
@@ -49,7 +50,7 @@ __all__ = [
     "FORMATS", "Format", "get_format", "rational_format",
     "scale_exponents", "quantize", "quantize_axis0", "dequantize",
     "code_fields", "level_value_f64", "pack7", "unpack7", "POISON_SCALE",
-    "gemm_exact", "gemm_exact_mixed", "expand_scales", "product_address_mixed",
+    "gemm_exact", "gemm_exact_mixed", "mixed_lattice", "expand_scales", "product_address_mixed",
     "gemm_exact_python", "product_address", "phase_bins_one",
     "load_library",
 ]

@@ -234,26 +234,31 @@ int oracle_dot_phase_sums(const uint8_t* a, const int8_t* as, const uint8_t* b, 
 
 /*
  * Mixed-format GEMM (the backward recipe of Sec. 3.3: E5C2 output gradients times reused
- * E4C3 forward operands).  The paper states the closed product for one K; with binary radix
- * and curve counts K_x, K_w (powers of two) both indices are lifted to the finer lattice
- * L = max(K_x, K_w): n'_x = (L / K_x) n_x, n'_w = (L / K_w) n_w, so that each magnitude is
- * 2^(n' / L) exactly, and the product address is
- *   u = n'_x + n'_w,  h = u mod L,  t = a_x + a_w + floor(u / L),  delta = (-1)^(s_x xor s_w),
- * the single-format rule when K_x = K_w.  Scales are per element here (a_scales [M][kd],
- * b_scales [N][kd]): callers whose blocks lie along k expand them, and operands whose blocks
- * lie along the other axis (forward codes reused in a backward GEMM) are passed the same way.
+ * E4C3 forward operands).  The paper states the closed product for one lattice.  Operand x has
+ * magnitudes 2^(p_x n_x / N_x), N_x = q_x K_x; over the common denominator D = lcm(N_a, N_b)
+ * both exponents are integers over D: u_x = p_x (D / N_x) n_x, and the product's exponent is
+ * (u_a + u_b) / D, so its address is
+ *   u = u_a + u_b,  h = (u mod D) / g,  t = a_a + a_b + floor(u / D),  delta = (-1)^(s_a xor s_b),
+ * with g = gcd(p_a D / N_a, p_b D / N_b, D) and H = D / g phases: the single-format rule when
+ * the formats agree.  For binary radices (N = K, powers of two) D = max(K_a, K_b) and the lift
+ * is n' = (D / K) n.  Scales are per element here (a_scales [M][kd], b_scales [N][kd]): callers
+ * whose blocks lie along k expand them, and operands whose blocks lie along the other axis
+ * (forward codes reused in a backward GEMM) are passed the same way.
  */
-static void dot_bins_mixed(const fmt_t* fx, const fmt_t* fw, int L, hist_t* hs,
+typedef struct {
+    int D, g, H, la, lb;   /* common denominator, phase divisor, phases, exponent multipliers */
+} lattice_t;
+
+static void dot_bins_mixed(const fmt_t* fx, const fmt_t* fw, const lattice_t* L, hist_t* hs,
                            const uint8_t* a, const int8_t* as, const uint8_t* b, const int8_t* bs, int64_t kd) {
     const int ECx = fx->E + fx->C, ECw = fw->E + fw->C;
-    const int lx = L / fx->K, lw = L / fw->K;
     for (int64_t k = 0; k < kd; k++) {
         int ma = a[k] & fx->mag_mask, mb = b[k] & fw->mag_mask;
         if (ma == 0 || mb == 0) continue;
         int sx = (a[k] >> ECx) & 1, sw = (b[k] >> ECw) & 1;
-        int u = lx * (ma - fx->B) + lw * (mb - fw->B);
-        int h = floor_mod(u, L);
-        int t = as[k] + bs[k] + floor_div(u, L);
+        int u = L->la * (ma - fx->B) + L->lb * (mb - fw->B);
+        int h = floor_mod(u, L->D) / L->g;
+        int t = as[k] + bs[k] + floor_div(u, L->D);
         int rel = t - hs->t_min;
         hs->cnt[(size_t)h * hs->t_span + rel] += (sx ^ sw) ? -1 : 1;
         if (rel < hs->lo) hs->lo = rel;
@@ -261,15 +266,21 @@ static void dot_bins_mixed(const fmt_t* fx, const fmt_t* fw, int L, hist_t* hs,
     }
 }
 
-int oracle_gemm_exact_mixed(const uint8_t* a_codes, const int8_t* a_scales, int Ea, int Ca,
-                            const uint8_t* b_codes, const int8_t* b_scales, int Eb, int Cb,
+int oracle_gemm_exact_mixed(const uint8_t* a_codes, const int8_t* a_scales, int Ea, int Ca, int pa, int qa,
+                            const uint8_t* b_codes, const int8_t* b_scales, int Eb, int Cb, int pb, int qb,
                             int64_t M, int64_t N, int64_t kd, double* out, int nthreads, int32_t* max_count) {
     fmt_t fx, fw, fl;
-    if (make_fmt(Ea, Ca, 1, 1, &fx) || make_fmt(Eb, Cb, 1, 1, &fw) || M < 0 || N < 0 || kd < 0) return -1;
-    const int L = fx.K > fw.K ? fx.K : fw.K;
-    /* bins sized for the lifted lattice: |u| <= lx (B_x - 1) + lw (B_w - 1) */
-    fl.E = 0; fl.C = 0; fl.p = 1; fl.q = 1; fl.K = L; fl.QK = L; fl.g = 1; fl.H = L; fl.mag_mask = 0;
-    fl.B = ((L / fx.K) * (fx.B - 1) + (L / fw.K) * (fw.B - 1) + 1) / 2 + 1;
+    if (make_fmt(Ea, Ca, pa, qa, &fx) || make_fmt(Eb, Cb, pb, qb, &fw) || M < 0 || N < 0 || kd < 0) return -1;
+    lattice_t L;
+    L.D = fx.QK / gcd_i(fx.QK, fw.QK) * fw.QK;
+    L.la = pa * (L.D / fx.QK);
+    L.lb = pb * (L.D / fw.QK);
+    L.g = gcd_i(gcd_i(L.la, L.lb), L.D);
+    L.H = L.D / L.g;
+    if (L.H > 64 * 8) return -1;
+    /* bins sized for the common lattice: |u| <= la (B_a - 1) + lb (B_b - 1), phases H over D */
+    fl.E = 0; fl.C = 0; fl.p = 1; fl.q = 1; fl.K = L.D; fl.QK = L.D; fl.g = L.g; fl.H = L.H; fl.mag_mask = 0;
+    fl.B = (L.la * (fx.B - 1) + L.lb * (fw.B - 1) + 1) / 2 + 1;
     if (nthreads > 0) omp_set_num_threads(nthreads);
     int32_t gmax = 0;
     #pragma omp parallel
@@ -280,7 +291,7 @@ int oracle_gemm_exact_mixed(const uint8_t* a_codes, const int8_t* a_scales, int 
         #pragma omp for schedule(dynamic, 1)
         for (int64_t i = 0; i < M; i++) {
             for (int64_t j = 0; j < N; j++) {
-                dot_bins_mixed(&fx, &fw, L, &hs, a_codes + i * kd, a_scales + i * kd,
+                dot_bins_mixed(&fx, &fw, &L, &hs, a_codes + i * kd, a_scales + i * kd,
                                b_codes + j * kd, b_scales + j * kd, kd);
                 __float128 v = reduce_bins(&fl, &hs, &lmax, NULL);
                 out[i * N + j] = (double)v;

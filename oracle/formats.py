@@ -73,18 +73,21 @@ class Format:
         return self.bits + S / G
 
 
-# Tab. curvefp-formats: CurveFP7 E3C3, CurveFP8 E4C3 / E5C2, all binary radix.
+def rational_format(E: int, C: int, p: int, q: int) -> Format:
+    """A format with rational radix r = 2^(p/q) (Sec. 3.1, Tab. radix-frontier)."""
+    return Format(f"E{E}C{C}_r{p}/{q}", E, C, p, q)
+
+
+# Tab. curvefp-formats: CurveFP7 E3C3, CurveFP8 E4C3 / E5C2, all binary radix; and the two
+# E4C3 radices of Tab. radix-frontier, r = 2^(8/9) (9 phases) and r = 2^(3/4) (32 phases).
 FORMATS = {
     "E4C3": Format("E4C3", 4, 3),
     "E5C2": Format("E5C2", 5, 2),
     "E3C3": Format("E3C3", 3, 3),
+    "E4C3_r8/9": rational_format(4, 3, 8, 9),
+    "E4C3_r3/4": rational_format(4, 3, 3, 4),
 }
 
 
 def get_format(name: str) -> Format:
     return FORMATS[name]
-
-
-def rational_format(E: int, C: int, p: int, q: int) -> Format:
-    """A format with rational radix r = 2^(p/q) (Sec. 3.1, Tab. radix-frontier)."""
-    return Format(f"E{E}C{C}_r{p}/{q}", E, C, p, q)

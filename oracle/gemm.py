@@ -55,7 +55,7 @@ def load_library():
         lib.oracle_gemm_exact.restype = I
         lib.oracle_dot_phase_sums.argtypes = [P, P, P, P, I64, I, I, I, I, I, P, P, P]
         lib.oracle_dot_phase_sums.restype = I
-        lib.oracle_gemm_exact_mixed.argtypes = [P, P, I, I, P, P, I, I, I64, I64, I64, P, I, P]
+        lib.oracle_gemm_exact_mixed.argtypes = [P, P, I, I, I, I, P, P, I, I, I, I, I64, I64, I64, P, I, P]
         lib.oracle_gemm_exact_mixed.restype = I
         lib.oracle_max_threads.restype = I
         _lib = lib
@@ -90,13 +90,24 @@ def gemm_exact(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: int = 3
     return out
 
 
+def mixed_lattice(fmt_a: Format, fmt_b: Format):
+    """Common lattice of two formats: magnitudes 2^(p n / N) of both are integers u over
+    D = lcm(N_a, N_b), u_x = p_x (D / N_x) n_x.  Returns (D, la, lb, g, H) with g the gcd of
+    the multipliers and D, and H = D / g phases."""
+    D = fmt_a.N * fmt_b.N // gcd(fmt_a.N, fmt_b.N)
+    la = fmt_a.p * (D // fmt_a.N)
+    lb = fmt_b.p * (D // fmt_b.N)
+    g = gcd(gcd(la, lb), D)
+    return D, la, lb, g, D // g
+
+
 def gemm_exact_mixed(a_codes, a_scales, fmt_a: Format, b_codes, b_scales, fmt_b: Format,
                      nthreads: int = 0, return_max_count: bool = False):
-    """Exact GEMM of two operands in different binary-radix formats (the backward recipe of
-    Sec. 3.3), per-element scales: A codes/scales [M, K], B codes/scales [N, K] -> float64
-    [M, N].  Indices are lifted to the finer curve lattice L = max(K_a, K_b) and products
-    are binned at h = u mod L, t = a_x + a_w + floor(u / L) (see curvefp_oracle.c)."""
-    assert fmt_a.p == fmt_a.q == 1 and fmt_b.p == fmt_b.q == 1
+    """Exact GEMM of two operands in different formats (the backward recipe of Sec. 3.3),
+    per-element scales: A codes/scales [M, K], B codes/scales [N, K] -> float64 [M, N].
+    Both exponents are taken over the common lattice D = lcm(N_a, N_b) and products are binned
+    at h = (u mod D) / g, t = a_x + a_w + floor(u / D) (see curvefp_oracle.c); for binary
+    radices D = max(K_a, K_b)."""
     lib = load_library()
     a_codes = np.ascontiguousarray(a_codes, dtype=np.uint8)
     b_codes = np.ascontiguousarray(b_codes, dtype=np.uint8)
@@ -107,8 +118,8 @@ def gemm_exact_mixed(a_codes, a_scales, fmt_a: Format, b_codes, b_scales, fmt_b:
     assert kd == kd2 and a_scales.shape == (M, kd) and b_scales.shape == (N, kd)
     out = np.empty((M, N), dtype=np.float64)
     mc = np.zeros(1, dtype=np.int32)
-    rc = lib.oracle_gemm_exact_mixed(_ptr(a_codes), _ptr(a_scales), fmt_a.E, fmt_a.C,
-                                     _ptr(b_codes), _ptr(b_scales), fmt_b.E, fmt_b.C,
+    rc = lib.oracle_gemm_exact_mixed(_ptr(a_codes), _ptr(a_scales), fmt_a.E, fmt_a.C, fmt_a.p, fmt_a.q,
+                                     _ptr(b_codes), _ptr(b_scales), fmt_b.E, fmt_b.C, fmt_b.p, fmt_b.q,
                                      M, N, kd, _ptr(out), int(nthreads), _ptr(mc))
     if rc != 0:
         raise ValueError("oracle_gemm_exact_mixed rejected its arguments")
@@ -128,16 +139,16 @@ def expand_scales(scales, block: int = 32, axis: int = 1):
 
 
 def product_address_mixed(code_x: int, a_x: int, fmt_x: Format, code_w: int, a_w: int, fmt_w: Format):
-    """(delta, h, t) of one product of two binary-radix formats on the lattice L = max(K_x,
-    K_w), or None for a zero operand."""
-    L = max(fmt_x.K, fmt_w.K)
+    """(delta, h, t) of one product of two formats on their common lattice (mixed_lattice),
+    or None for a zero operand."""
+    D, lx, lw, g, _ = mixed_lattice(fmt_x, fmt_w)
     ex, ew = fmt_x.E + fmt_x.C, fmt_w.E + fmt_w.C
     mx, mw = code_x & ((1 << ex) - 1), code_w & ((1 << ew) - 1)
     if mx == 0 or mw == 0:
         return None
     sx, sw = (code_x >> ex) & 1, (code_w >> ew) & 1
-    u = (L // fmt_x.K) * (mx - fmt_x.B) + (L // fmt_w.K) * (mw - fmt_w.B)
-    return (-1 if (sx ^ sw) else 1), u % L, a_x + a_w + u // L
+    u = lx * (mx - fmt_x.B) + lw * (mw - fmt_w.B)
+    return (-1 if (sx ^ sw) else 1), (u % D) // g, a_x + a_w + u // D
 
 
 def phase_bins_one(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: int = 32):

@@ -34,10 +34,20 @@ SCALE_MIN = -127
 SCALE_MAX = 127
 
 
+_SIG_CACHE = {}
+
+
 def _sig_table(fmt: Format) -> np.ndarray:
-    """S[r] = 2^{r/N} for r in [0, N), N = qK: the fractional part of every level."""
+    """S[r] = 2^{r/N} for r in [0, N), N = qK: the fractional part of every level, each the
+    float64 nearest to the real value (evaluated with mpmath at 40 digits, then rounded once;
+    ``2.0 ** (r / N)`` would round r / N first whenever N is not a power of two)."""
     N = fmt.N
-    return np.array([2.0 ** (r / N) for r in range(N)], dtype=np.float64)
+    if N not in _SIG_CACHE:
+        import mpmath
+        with mpmath.workdps(40):
+            _SIG_CACHE[N] = np.array([float(mpmath.power(2, mpmath.mpf(r) / N)) for r in range(N)],
+                                     dtype=np.float64)
+    return _SIG_CACHE[N]
 
 
 def level_value_f64(fmt: Format, n):

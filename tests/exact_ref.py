@@ -78,7 +78,13 @@ def nearest_binary_radix(M: int, j: int, E: int, C: int, P: int = 160):
 
 def rn_f32_pow2(a: int, n: int, K: int, P: int = 200) -> float:
     """Nearest float32 (ties to even) to 2^(a + n/K), decided rigorously."""
-    e, k = divmod(n, K)
+    return rn_f32_level(a, n, 1, K, P)
+
+
+def rn_f32_level(a: int, n: int, p: int, N: int, P: int = 200) -> float:
+    """Nearest float32 (ties to even) to 2^(a + p n / N), decided rigorously."""
+    e, k = divmod(p * n, N)
+    K = N
     Ex = a + e                    # value = 2^Ex * 2^(k/K)
     if k == 0:
         if Ex > 127:
@@ -116,3 +122,73 @@ def rn_f32_pow2(a: int, n: int, K: int, P: int = 200) -> float:
 
 def f32_bits(x: float) -> int:
     return struct.unpack("<I", struct.pack("<f", x))[0]
+
+
+# ---------------------------------------------------------------- rational radix r = 2^(p/q)
+
+class Tie(Exception):
+    """y sits exactly on a decision point (possible only where the point is dyadic)."""
+
+
+def _level_parts(n: int, p: int, N: int):
+    """2^(p n / N) = 2^w * 2^(r / N), 0 <= r < N."""
+    return divmod(p * n, N)
+
+
+def _above_midpoint(M: int, j: int, n: int, p: int, N: int, P: int) -> bool:
+    """y = M 2^(j-23) > (L(n) + L(n+1)) / 2, L(n) = 2^(p n / N), decided with brackets
+    F(r) = floor(2^(r/N) 2^P), exact only for r = 0."""
+    w0, r0 = _level_parts(n, p, N)
+    w1, r1 = _level_parts(n + 1, p, N)
+    d = w1 - w0
+    assert d >= 0
+    S = frac_pow2_floor(r0, N, P) + (frac_pow2_floor(r1, N, P) << d)
+    width = (0 if r0 == 0 else 1) + (0 if r1 == 0 else (1 << d))
+    sh = j - 22 + P - w0
+    assert sh >= 0
+    lhs = M << sh                                  # 2 y 2^(P - w0)
+    if width == 0:
+        if lhs == S:
+            raise Tie((M, j, n))
+        return lhs > S
+    if lhs >= S + width:
+        return True
+    if lhs <= S:
+        return False
+    raise Undecided((M, j, n))
+
+
+def nearest_level(M: int, j: int, E: int, C: int, p: int, q: int, P: int = 240):
+    """Nearest element of {0} U {2^(p n / N)}, N = qK, to y = M 2^(j-23), M in [2^23, 2^24),
+    levels n in [-(B-1), B-1].  Returns n, or None for zero.  A tie between zero and the smallest
+    level (possible when its half is dyadic) goes to the level, the reading the library takes.
+    Raises Undecided if a bracket is too wide."""
+    assert (1 << 23) <= M < (1 << 24)
+    K = 1 << C
+    N = q * K
+    B = 1 << (E + C - 1)
+    n_min, n_max = -(B - 1), B - 1
+    # midpoints increase with n: the nearest level is n_min + #{n : y above midpoint n}
+    lo, hi = n_min, n_max            # find the count by bisection over the monotone predicate
+    while lo < hi:
+        mid = (lo + hi) // 2
+        if _above_midpoint(M, j, mid, p, N, P):
+            lo = mid + 1
+        else:
+            hi = mid
+    n = lo
+    if n > n_min:
+        return n
+    # zero or n_min: 2y against L(n_min)
+    w, r = _level_parts(n_min, p, N)
+    sh = j - 22 + P - w
+    assert sh >= 0
+    lhs = M << sh                    # 2 y 2^(P - w)
+    F = frac_pow2_floor(r, N, P)
+    if r == 0:
+        return n_min if lhs >= F else None     # lhs == F: the tie, to the level
+    if lhs >= F + 1:
+        return n_min
+    if lhs <= F:
+        return None
+    raise Undecided((M, j, "zero"))

@@ -20,6 +20,8 @@ from tests import exact_ref as X
 
 GOLD = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "paper_tables.json")))
 FMT_NAMES = ("E4C3", "E5C2", "E3C3")
+RADIX_NAMES = ("E4C3_r8/9", "E4C3_r3/4")      # Tab. radix-frontier
+ALL_NAMES = FMT_NAMES + RADIX_NAMES
 
 
 # ------------------------------------------------------------------ tables
@@ -258,7 +260,7 @@ def test_scale_rule_and_error_bound(name):
     assert np.all(n[nz] <= f.n_max)
 
 
-@pytest.mark.parametrize("name", FMT_NAMES)
+@pytest.mark.parametrize("name", ALL_NAMES)
 @pytest.mark.parametrize("a", [-100, -20, 0, 7, 100])
 def test_round_trip_all_codes(name, a):
     """quantize(dequantize(c)) == c for every canonical code (blocks holding the top code)."""
@@ -348,7 +350,7 @@ def _deq_exact64(codes, scales, f):
     return np.where(nz, np.where(s == 1, -v, v), 0.0)
 
 
-@pytest.mark.parametrize("name", FMT_NAMES)
+@pytest.mark.parametrize("name", ALL_NAMES)
 def test_gemm_matches_float64_matmul(name):
     """Phase-binned exact GEMM vs numpy float64 matmul of reconstructed values."""
     f = oracle.get_format(name)
@@ -365,7 +367,7 @@ def test_gemm_matches_float64_matmul(name):
     assert C.shape == (48, 40)
 
 
-@pytest.mark.parametrize("name", FMT_NAMES)
+@pytest.mark.parametrize("name", ALL_NAMES)
 def test_gemm_matches_python_mini_oracle(name):
     f = oracle.get_format(name)
     rng = np.random.default_rng(5)
@@ -400,7 +402,7 @@ def test_gemm_powers_of_two_exact():
             assert C[i, j] == float(tot)
 
 
-@pytest.mark.parametrize("name", FMT_NAMES)
+@pytest.mark.parametrize("name", ALL_NAMES)
 def test_gemm_sign_identity_and_zero(name):
     f = oracle.get_format(name)
     EC = f.E + f.C
@@ -456,6 +458,170 @@ def test_phase_sums_recombine():
     assert abs(val - ref) <= 1e-12 * abs(ref)
 
 
+# ------------------------------------------------------------------ rational radix (Tab. radix-frontier)
+
+def _rigorous_rank(M, j, f):
+    n = X.nearest_level(int(M), j, f.E, f.C, f.p, f.q)
+    return 0 if n is None else n + f.B
+
+
+def _rank_steps(j, f):
+    """The rigorous rank over the significands of octave j as a step function: [(first M, rank)]."""
+    lo_M, hi_M = 1 << 23, (1 << 24) - 1
+    steps = [(lo_M, _rigorous_rank(lo_M, j, f))]
+    r_end = _rigorous_rank(hi_M, j, f)
+    while steps[-1][1] != r_end:
+        cur = steps[-1][1]
+        lo, hi = steps[-1][0], hi_M
+        while lo < hi:                      # smallest M whose rank exceeds cur
+            mid = (lo + hi) // 2
+            if _rigorous_rank(mid, j, f) > cur:
+                hi = mid
+            else:
+                lo = mid + 1
+        steps.append((lo, _rigorous_rank(lo, j, f)))
+    return steps
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_format_parameters(name):
+    """Tab. radix-frontier variants: E4C3 element (8 bits, 127 positive magnitudes), levels
+    2^(p n / (qK)) (Sec. 3.2: r^(e + k/K) = 2^(p(eK + k)/(qK))), H from the printed table."""
+    f = oracle.get_format(name)
+    case = next(c for c in GOLD["radix_phases"]["cases"] if (c["p"], c["q"]) == (f.p, f.q))
+    assert (f.bits, f.E, f.C, f.positive_levels, f.H) == (8, case["E"], case["C"], 127, case["H"])
+    n = np.arange(f.n_min, f.n_max + 1)
+    v = oracle.level_value_f64(f, n)
+    r = 2.0 ** (f.p / f.q)
+    assert np.allclose(v, r ** (n / f.K), rtol=1e-14, atol=0)
+    assert np.all(np.diff(v) > 0)
+    # adjacent curve indices differ by r^(1/K), adjacent exponents by r (Sec. 3.1)
+    assert np.allclose(v[1:] / v[:-1], r ** (1 / f.K), rtol=1e-14)
+    assert np.allclose(v[f.K:] / v[:-f.K], r, rtol=1e-14)
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_nearest_level_exhaustive_octaves(name):
+    """Every fp32 significand of the interior octaves over one period of the level pattern
+    (1 octave for 2^(1/9) spacing, 3 for 2^(3/32)): oracle == rigorous nearest level."""
+    f = oracle.get_format(name)
+    period = f.p // math.gcd(f.p, f.N)
+    Ms = np.arange(1 << 23, 1 << 24, dtype=np.int64)
+    for j in range(period):
+        vals = np.ldexp(Ms.astype(np.float64), j - 23).astype(np.float32)
+        x, nb = _blocks_with_scale0(vals, f)
+        codes, scales = oracle.quantize(x, f)
+        assert np.all(scales == 0)
+        got = codes.reshape(nb, 32)[:, 1:].reshape(-1)[: len(Ms)].astype(np.int64)
+        steps = _rank_steps(j, f)
+        assert len(steps) >= 9                    # at least 9 levels' decisions per octave here
+        expect = np.zeros(len(Ms), np.int64)
+        for M0, r in steps:
+            expect[M0 - (1 << 23):] = r
+        assert np.array_equal(got, expect), j
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_nearest_level_edges(name):
+    """Octaves around the zero threshold, the smallest level and the top level."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(11)
+    w_min = (f.p * f.n_min) // f.N
+    w_max = (f.p * f.n_max) // f.N
+    lm = float(np.float32(oracle.level_value_f64(f, f.n_max)))
+    for j in (w_min - 3, w_min - 2, w_min - 1, w_min, w_min + 1, w_max - 1, w_max):
+        Ms = np.unique(np.concatenate([rng.integers(1 << 23, 1 << 24, 3000),
+                                       np.array([1 << 23, (1 << 23) + 1, (1 << 24) - 1])]))
+        vals = np.ldexp(Ms.astype(np.float64), j - 23).astype(np.float32)
+        keep = vals.astype(np.float64) <= lm
+        Ms, vals = Ms[keep], vals[keep]
+        x, nb = _blocks_with_scale0(vals, f)
+        codes, scales = oracle.quantize(x, f)
+        assert np.all(scales == 0)
+        got = codes.reshape(nb, 32)[:, 1:].reshape(-1)[: len(Ms)].astype(np.int64)
+        exp = np.array([_rigorous_rank(M, j, f) for M in Ms])
+        assert np.array_equal(got, exp), j
+
+
+def test_radix_zero_tie_goes_to_the_level():
+    """r = 2^(8/9): the smallest level is 2^(-7), so the zero/level decision point 2^(-8) is a
+    float and a tie can occur (with binary radix and r = 2^(3/4) it is irrational).  Reading: the
+    tie goes to the smallest level; one ulp below goes to zero."""
+    f = oracle.get_format("E4C3_r8/9")
+    assert oracle.level_value_f64(f, f.n_min) == 2.0 ** -7
+    half = np.float32(2.0 ** -8)
+    below = np.nextafter(half, np.float32(0))
+    x, nb = _blocks_with_scale0(np.array([half, below, -half], np.float32), f)
+    codes, scales = oracle.quantize(x, f)
+    assert scales[0, 0] == 0
+    assert list(codes[0, 1:4]) == [1, 0, 1 | (1 << (f.E + f.C))]
+    assert X.nearest_level(1 << 23, -8, f.E, f.C, f.p, f.q) == f.n_min
+    for name in ("E4C3", "E4C3_r3/4"):     # elsewhere the point is irrational: no tie
+        g = oracle.get_format(name)
+        _, r = divmod(g.p * g.n_min, g.N)
+        assert r != 0
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_scale_rule_and_error_bound(name):
+    """Ceil-absmax with the fp32 top level, and the interior bound |x - x_hat| <= |x| (rho - 1) /
+    (rho + 1) for the level ratio rho = r^(1/K)."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(12)
+    x = (rng.standard_normal((64, 1024)) * np.exp2(rng.uniform(-30, 30, (64, 1)))).astype(np.float32)
+    codes, scales = oracle.quantize(x, f)
+    lm = float(np.float32(oracle.level_value_f64(f, f.n_max)))
+    amax = np.abs(x.astype(np.float64)).reshape(64, 32, 32).max(-1)
+    y = np.ldexp(amax, -scales.astype(np.int64))
+    assert np.all(y <= lm) and np.all(y > lm / 2)
+    deq = oracle.dequantize(codes, scales, f).astype(np.float64)
+    xd = x.astype(np.float64)
+    rho = 2.0 ** (f.p / f.N)
+    bound = (rho - 1) / (rho + 1)
+    a = np.repeat(scales.astype(np.int64), 32, axis=1)
+    interior = np.abs(xd) >= np.ldexp(oracle.level_value_f64(f, f.n_min), a)
+    rel = np.abs(xd - deq)[interior] / np.abs(xd)[interior]
+    assert rel.max() <= bound * (1 + 1e-6)
+    nz, s, n = oracle.code_fields(codes, f)
+    assert np.all(n[nz] <= f.n_max)
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_dequantize_rigorous_all_codes_all_scales(name):
+    """fp32 reconstruction == rigorously rounded 2^(a + p n / N), every code and scale."""
+    f = oracle.get_format(name)
+    EC = f.E + f.C
+    mags = np.arange(1, 2 ** EC)
+    scales = np.arange(-127, 128)
+    pad = (-len(mags)) % 32
+    cpad = np.concatenate([np.tile(mags, (len(scales), 1)), np.zeros((len(scales), pad), np.int64)],
+                          axis=1).astype(np.uint8)
+    sc = np.repeat(scales[:, None], cpad.shape[1] // 32, axis=1).astype(np.int8)
+    got = oracle.dequantize(cpad, sc, f)[:, :len(mags)]
+    for ia, a in enumerate(scales):
+        for im, m in enumerate(mags):
+            exp = X.rn_f32_level(int(a), int(m) - f.B, f.p, f.N)
+            assert X.f32_bits(float(got[ia, im])) == X.f32_bits(exp), (a, m)
+
+
+@pytest.mark.parametrize("name", RADIX_NAMES)
+def test_radix_closed_product_values(name):
+    """Closure with a rational radix (Sec. 3.2): every code pair's (delta, h, t) gives
+    delta 2^t 2^(h/H) equal to the product of the two reconstructed values (mpmath)."""
+    import mpmath
+    mpmath.mp.dps = 40
+    f = oracle.get_format(name)
+    mags = np.arange(1, 2 ** (f.E + f.C))
+    r = mpmath.power(2, mpmath.mpf(f.p) / f.q)
+    for mx in mags[::3]:
+        for mw in mags[::5]:
+            d, h, t = oracle.product_address(int(mx), -3, int(mw | (1 << 7)), 5, f)
+            got = d * mpmath.power(2, t) * mpmath.power(2, mpmath.mpf(h) / f.H)
+            vx = mpmath.power(2, -3) * mpmath.power(r, mpmath.mpf(int(mx) - f.B) / f.K)
+            vw = -mpmath.power(2, 5) * mpmath.power(r, mpmath.mpf(int(mw) - f.B) / f.K)
+            assert abs(got - vx * vw) <= mpmath.mpf(10) ** -30 * abs(vx * vw)
+
+
 # ------------------------------------------------------------------ mixed formats (backward recipe)
 
 MIXED = [("E5C2", "E4C3"), ("E4C3", "E5C2"), ("E5C2", "E3C3")]
@@ -508,7 +674,7 @@ def test_mixed_equals_single_format_when_formats_agree():
     """With both operands in one format the lifted rule is the paper's single-format rule:
     the mixed oracle (per-element scales) must reproduce gemm_exact bit for bit."""
     rng = np.random.default_rng(12)
-    for name in FMT_NAMES:
+    for name in ALL_NAMES:
         f = oracle.get_format(name)
         A = (rng.standard_normal((9, 96)) * np.exp2(rng.uniform(-5, 5, (9, 1)))).astype(np.float32)
         B = rng.standard_normal((7, 96)).astype(np.float32)
@@ -557,3 +723,52 @@ def test_mixed_gemm_with_reused_forward_codes():
     absmm = np.abs(dg) @ np.abs(dw)
     assert C.shape == (24, 96)
     assert np.all(np.abs(C - ref) <= 1e-13 * absmm)
+
+
+RADIX_MIXED = [("E5C2", "E4C3_r8/9"), ("E4C3_r3/4", "E4C3_r8/9"), ("E4C3_r8/9", "E4C3"), ("E4C3_r3/4", "E3C3")]
+
+
+@pytest.mark.parametrize("pair", RADIX_MIXED, ids=lambda p: f"{p[0]}x{p[1]}")
+def test_mixed_rational_closure_all_pairs(pair):
+    """Two lattices 2^(p_x n / N_x) and 2^(p_w n / N_w): every pair of nonzero codes, both
+    signs, two scale pairs.  The product exponent, added as exact rationals, must equal
+    t + h / H of the address on the common lattice; every one of its H phases is occupied, and
+    H = lcm(N_x, N_w) / gcd of the lifted multipliers (8 for two binary radices, 36 for 2^(8/9)
+    with E5C2's 2^(1/4), 72 with 2^(3/32))."""
+    fx, fw = oracle.get_format(pair[0]), oracle.get_format(pair[1])
+    D, lx, lw, g, H = oracle.mixed_lattice(fx, fw)
+
+    def codes_of(f):
+        mags = np.arange(1, 2 ** (f.E + f.C))
+        return np.concatenate([mags, mags | (1 << (f.E + f.C))])
+
+    cx, cw = codes_of(fx), codes_of(fw)
+    _, sx, nx = oracle.code_fields(cx, fx)
+    _, sw, nw = oracle.code_fields(cw, fw)
+    phases = set()
+    for ax, aw in [(0, 0), (-7, 4)]:
+        for i in range(len(cx)):
+            for j in range(len(cw)):
+                d, h, t = oracle.product_address_mixed(int(cx[i]), ax, fx, int(cw[j]), aw, fw)
+                q = Fraction(ax + aw) + Fraction(fx.p * int(nx[i]), fx.N) + Fraction(fw.p * int(nw[j]), fw.N)
+                assert Fraction(t) + Fraction(h, H) == q
+                assert 0 <= h < H and d == (-1 if sx[i] ^ sw[j] else 1)
+                phases.add(h)
+    assert phases == set(range(H))
+    expect_H = {("E5C2", "E4C3_r8/9"): 36, ("E4C3_r3/4", "E4C3_r8/9"): 288, ("E4C3_r8/9", "E4C3"): 72,
+                ("E4C3_r3/4", "E3C3"): 32}[pair]
+    assert H == expect_H
+
+
+@pytest.mark.parametrize("pair", RADIX_MIXED, ids=lambda p: f"{p[0]}x{p[1]}")
+def test_mixed_rational_gemm_matches_float64_matmul(pair):
+    fa, fb = oracle.get_format(pair[0]), oracle.get_format(pair[1])
+    rng = np.random.default_rng(15)
+    A = (rng.standard_normal((24, 160)) * np.exp(rng.normal(0, 3, (24, 1)))).astype(np.float32)
+    B = (rng.standard_normal((20, 160)) * 0.02).astype(np.float32)
+    ca, sa = oracle.quantize(A, fa)
+    cb, sb = oracle.quantize(B, fb)
+    C = oracle.gemm_exact_mixed(ca, oracle.expand_scales(sa), fa, cb, oracle.expand_scales(sb), fb)
+    da, db = _deq_exact64(ca, sa, fa), _deq_exact64(cb, sb, fb)
+    absmm = np.abs(da) @ np.abs(db).T
+    assert np.all(np.abs(C - da @ db.T) <= 1e-13 * absmm)
