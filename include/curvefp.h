@@ -4,10 +4,11 @@
  *
  * CurveFP (arXiv 2608.10010) stores a block of G values with one signed
  * power-of-two scale exponent a_b and one (1+E+C)-bit code per element; a
- * nonzero element is (-1)^s 2^{a_b} 2^{e + k/K}, K = 2^C (Sec. 3.1,
+ * nonzero element is (-1)^s 2^{a_b} r^{e + k/K}, K = 2^C (Sec. 3.1,
  * Eq. curvefp-value).  The formats are those of Tab. curvefp-formats:
  * CurveFP8 E4C3 (forward operands), CurveFP8 E5C2 (gradients) and CurveFP7
- * E3C3 (compact inference), all with binary radix.
+ * E3C3 (compact inference), all with binary radix r = 2, and E4C3 with the
+ * radices r = 2^{8/9} and r = 2^{3/4} of Tab. radix-frontier.
  *
  * Conventions shared by every entry point
  *   - All data pointers are device pointers owned by the caller.  The library
@@ -28,6 +29,7 @@
  *
  * Element code layout (one byte per code for E4C3/E5C2, 7-bit packed for E3C3)
  *   code = s << (E+C) | m,  m = n + 2^{E+C-1},  n = e*K + k in [-(2^{E+C-1}-1), 2^{E+C-1}-1],
+ *   standing for r^{n/K} = 2^{p n / (qK)},
  *   m = 0 is the zero sentinel (the paper reserves magnitude index zero and drops
  *   the smallest exponent/curve combination, Sec. 3.1; App. C.1 gives the same
  *   rank layout for E4C3: sign in bit 7, rank in bits 6:0, q = m - 64).
@@ -47,9 +49,13 @@ extern "C" {
 #endif
 
 typedef enum {
-    CURVEFP_E4C3 = 0,   /* 8 bits, E=4, C=3, 127 levels, H=8 */
-    CURVEFP_E5C2 = 1,   /* 8 bits, E=5, C=2, 127 levels, H=4 */
-    CURVEFP_E3C3 = 2    /* 7 bits, E=3, C=3,  63 levels, H=8 */
+    CURVEFP_E4C3 = 0,       /* 8 bits, E=4, C=3, 127 levels, H=8 */
+    CURVEFP_E5C2 = 1,       /* 8 bits, E=5, C=2, 127 levels, H=4 */
+    CURVEFP_E3C3 = 2,       /* 7 bits, E=3, C=3,  63 levels, H=8 */
+    /* E4C3 with the rational radices of Tab. radix-frontier (Sec. 3.1: r = 2^{p/q},
+     * levels r^{n/K} = 2^{p n/(qK)}, Eq. phase-count H = qK / gcd(p, qK)) */
+    CURVEFP_E4C3_R8_9 = 3,  /* 8 bits, r = 2^{8/9}: levels 2^{n/9} in [2^-7, 2^7], H=9 */
+    CURVEFP_E4C3_R3_4 = 4   /* 8 bits, r = 2^{3/4}: levels 2^{3n/32} in [2^-5.906, 2^5.906], H=32 */
 } curvefp_format;
 
 typedef enum {
@@ -71,6 +77,10 @@ typedef enum {
  * count H = qK/gcd(p, qK) of Eq. phase-count (binary radix: H = K).  Any output
  * pointer may be NULL.  Returns CURVEFP_OK or CURVEFP_ERR_FORMAT. */
 int curvefp_format_info(int format, int* bits, int* E, int* C, int* phases);
+
+/* Radix r = 2^{p/q} of a format (p = q = 1: binary).  Returns CURVEFP_OK or
+ * CURVEFP_ERR_FORMAT. */
+int curvefp_format_radix(int format, int* p, int* q);
 
 /* Bytes of the code array for `outer` rows of `k` elements each
  * (outer*k for E4C3/E5C2, outer*(k/32)*28 for E3C3); negative status on bad input. */

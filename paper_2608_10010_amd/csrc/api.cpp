@@ -11,11 +11,23 @@ using namespace curvefp;
 
 namespace {
 
-constexpr int kBits[3] = {8, 8, 7};
-constexpr int kE[3] = {4, 5, 3};
-constexpr int kC[3] = {3, 2, 3};
+// per format id: element bits, E, C, radix r = 2^{P/Q}
+constexpr int kBits[NUM_FORMATS] = {8, 8, 7, 8, 8};
+constexpr int kE[NUM_FORMATS] = {4, 5, 3, 4, 4};
+constexpr int kC[NUM_FORMATS] = {3, 2, 3, 3, 3};
+constexpr int kP[NUM_FORMATS] = {1, 1, 1, 8, 3};
+constexpr int kQ[NUM_FORMATS] = {1, 1, 1, 9, 4};
 
-bool fmt_ok(int f) { return f >= 0 && f <= 2; }
+bool fmt_ok(int f) { return f >= 0 && f < NUM_FORMATS; }
+
+int gcd_i(int a, int b) {
+    while (b) {
+        const int r = a % b;
+        a = b;
+        b = r;
+    }
+    return a;
+}
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 std::mutex g_mu;
@@ -57,7 +69,15 @@ int curvefp_format_info(int format, int* bits, int* E, int* C, int* phases) {
     if (bits) *bits = kBits[format];
     if (E) *E = kE[format];
     if (C) *C = kC[format];
-    if (phases) *phases = 1 << kC[format];   // binary radix: H = qK / gcd(p, qK) = K
+    const int qk = kQ[format] << kC[format];
+    if (phases) *phases = qk / gcd_i(kP[format], qk);   // H = qK / gcd(p, qK)
+    return CURVEFP_OK;
+}
+
+int curvefp_format_radix(int format, int* p, int* q) {
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (p) *p = kP[format];
+    if (q) *q = kQ[format];
     return CURVEFP_OK;
 }
 

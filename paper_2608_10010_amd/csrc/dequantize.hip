@@ -1,10 +1,11 @@
-// CurveFP reconstruction x_hat = (-1)^s 2^{a_b} 2^{e + k/K} (Eq. curvefp-value),
-// written as the nearest fp32 value.
+// CurveFP reconstruction x_hat = (-1)^s 2^{a_b} r^{e + k/K} (Eq. curvefp-value),
+// written as the nearest fp32 value.  With r = 2^{P/Q} the magnitude is 2^{w + f/N},
+// w = floor(P n / N), f = P n mod N, N = QK (binary radix: w = e, f = k).
 //
 // In the normal range the result is exact bit assembly: the fp32 exponent is
-// e + a_b and the mantissa is that of fl32(2^{k/K}) (scaling by a power of two
+// w + a_b and the mantissa is that of fl32(2^{f/N}) (scaling by a power of two
 // commutes with rounding there).  Below 2^-126 the 62-bit significand of
-// 2^{k/K} is rounded once at the subnormal position.  HBM-bound: one byte (or 7
+// 2^{f/N} is rounded once at the subnormal position.  HBM-bound: one byte (or 7
 // bits) and 1/32 scale byte read, four bytes written per element.
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
@@ -13,37 +14,59 @@
 
 namespace curvefp {
 
-__device__ uint32_t g_mant[3][8];
-__device__ uint64_t g_sig62[3][8];
+__device__ uint32_t g_mant[NUM_FORMATS][8];
+__device__ uint64_t g_sig62[NUM_FORMATS][8];
+// rational radix: per magnitude rank, (w << 24) | mantissa of fl32(2^{f/N}) and floor(2^{f/N} 2^62)
+__device__ uint32_t g_dq_em[NUM_FORMATS][128];
+__device__ uint64_t g_dq_sig62[NUM_FORMATS][128];
 
 hipError_t dequantize_upload(const AllTables& t) {
-    uint32_t m[3][8];
-    uint64_t s[3][8];
-    for (int f = 0; f < 3; f++) {
+    uint32_t m[NUM_FORMATS][8];
+    uint64_t s[NUM_FORMATS][8];
+    static uint32_t em[NUM_FORMATS][128];
+    static uint64_t s62[NUM_FORMATS][128];
+    for (int f = 0; f < NUM_FORMATS; f++) {
         memcpy(m[f], t.f[f].mant, sizeof(m[f]));
         memcpy(s[f], t.f[f].sig62, sizeof(s[f]));
+        memcpy(em[f], t.f[f].dq_em, sizeof(em[f]));
+        memcpy(s62[f], t.f[f].dq_sig62, sizeof(s62[f]));
     }
     hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_mant), m, sizeof(m));
     if (e != hipSuccess) return e;
-    return hipMemcpyToSymbol(HIP_SYMBOL(g_sig62), s, sizeof(s));
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_sig62), s, sizeof(s));
+    if (e != hipSuccess) return e;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_dq_em), em, sizeof(em));
+    if (e != hipSuccess) return e;
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_dq_sig62), s62, sizeof(s62));
 }
 
 namespace {
 
+// binary radix: mant/sig indexed by the curve index k (8 entries); rational radix: by the
+// magnitude rank (128 entries, mant holding (w << 24) | mantissa)
 template <class F>
 __device__ __forceinline__ uint32_t value_bits(uint32_t code, int a, const uint32_t* mant, const uint64_t* sig) {
     const uint32_t m = code & F::MAG_MASK;
     if (m == 0) return 0u;
     const uint32_t s = (code >> F::EC) & 1u;
-    const int n = (int)m - F::B;
-    const int e = n >> F::C;                 // floor(n / K)
-    const int k = n & (F::K - 1);
-    const int ex = e + a;
+    int ex, k;
+    uint32_t mbits;
+    if (F::BINARY) {
+        const int n = (int)m - F::B;
+        k = n & (F::K - 1);
+        ex = (n >> F::C) + a;                // floor(n / K) + a
+        mbits = mant[k];
+    } else {
+        k = (int)m;
+        const uint32_t em = mant[m];
+        ex = ((int32_t)em >> 24) + a;        // floor(P n / N) + a
+        mbits = em & 0x7FFFFFu;
+    }
     uint32_t bits;
     if (ex > 127) {
         bits = 0x7F800000u;                  // beyond FLT_MAX: rounds to infinity
     } else if (ex >= -126) {
-        bits = ((uint32_t)(ex + 127) << 23) | mant[k];
+        bits = ((uint32_t)(ex + 127) << 23) | mbits;
     } else {
         const int sh = -87 - ex;             // 62 - (ex + 149), in [40, 56]
         const uint64_t v = sig[k];
@@ -63,11 +86,12 @@ template <class F>
 __global__ __launch_bounds__(256) void dequantize_kernel(
     const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
     Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx) {
-    __shared__ uint32_t mant[8];
-    __shared__ uint64_t sig[8];
-    if (threadIdx.x < 8) {
-        mant[threadIdx.x] = g_mant[fidx][threadIdx.x];
-        sig[threadIdx.x] = g_sig62[fidx][threadIdx.x];
+    constexpr int TAB = F::BINARY ? 8 : 128;
+    __shared__ uint32_t mant[TAB];
+    __shared__ uint64_t sig[TAB];
+    if (threadIdx.x < TAB) {
+        mant[threadIdx.x] = F::BINARY ? g_mant[fidx][threadIdx.x] : g_dq_em[fidx][threadIdx.x];
+        sig[threadIdx.x] = F::BINARY ? g_sig62[fidx][threadIdx.x] : g_dq_sig62[fidx][threadIdx.x];
     }
     __syncthreads();
     const bool dense = ld == (int64_t)cpr * 8;
@@ -143,7 +167,9 @@ hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format
     switch (format) {
         case 0: return launch_fmt<FmtE4C3>(codes, scales, outer, k, dst, ld_dst, 0, s);
         case 1: return launch_fmt<FmtE5C2>(codes, scales, outer, k, dst, ld_dst, 1, s);
-        default: return launch_fmt<FmtE3C3>(codes, scales, outer, k, dst, ld_dst, 2, s);
+        case 2: return launch_fmt<FmtE3C3>(codes, scales, outer, k, dst, ld_dst, 2, s);
+        case 3: return launch_fmt<FmtE4C3R89>(codes, scales, outer, k, dst, ld_dst, 3, s);
+        default: return launch_fmt<FmtE4C3R34>(codes, scales, outer, k, dst, ld_dst, 4, s);
     }
 }
 

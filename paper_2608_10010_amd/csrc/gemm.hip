@@ -4,8 +4,9 @@
 // product in the code domain and sums the products phase by phase,
 // sum_h 2^{h/H} N_h (Sec. 3.2, Eq. binned-accumulation).  Here the same sum is
 // evaluated on MFMA: every code is expanded once per workgroup into an fp16
-// pair (hi, lo) with hi + lo = 2^{x} 2^{k/K} to 22 significant bits, where the
-// exponent x = (a_b - alpha_row) + e + bias carries the block scale relative to
+// pair (hi, lo) with hi + lo = 2^{x} 2^{f/N} to 22 significant bits (the level
+// r^{n/K} = 2^{w + f/N}; binary radix: w = e, f/N = k/K), where the
+// exponent x = (a_b - alpha_row) + w + bias carries the block scale relative to
 // the largest block scale alpha_row of its row (a power of two, so no new
 // phase).  Three f16 MFMA products hi.hi + hi.lo + lo.hi accumulate in fp32,
 // and the epilogue multiplies by 2^{alpha_i + beta_j - 2 bias} exactly.
@@ -39,11 +40,11 @@
 
 namespace curvefp {
 
-__device__ uint32_t g_dec[3][GEMM_DEC_ENTRIES];
+__device__ uint32_t g_dec[NUM_FORMATS][GEMM_DEC_ENTRIES];
 
 hipError_t gemm_upload(const AllTables& t) {
-    uint32_t h[3][GEMM_DEC_ENTRIES];
-    for (int f = 0; f < 3; f++) memcpy(h[f], t.f[f].dec, sizeof(h[f]));
+    uint32_t h[NUM_FORMATS][GEMM_DEC_ENTRIES];
+    for (int f = 0; f < NUM_FORMATS; f++) memcpy(h[f], t.f[f].dec, sizeof(h[f]));
     return hipMemcpyToSymbol(HIP_SYMBOL(g_dec), h, sizeof(h));
 }
 
@@ -1227,27 +1228,35 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
 }
 
 // fp16 exponent offset of a format's expansion (the row's largest element lands near 2^15)
-int gemm_bias(int f) { return f == 0 ? FmtE4C3::GEMM_BIAS : f == 1 ? FmtE5C2::GEMM_BIAS : FmtE3C3::GEMM_BIAS; }
+int gemm_bias(int f) {
+    constexpr int bias[NUM_FORMATS] = {FmtE4C3::GEMM_BIAS, FmtE5C2::GEMM_BIAS, FmtE3C3::GEMM_BIAS,
+                                       FmtE4C3R89::GEMM_BIAS, FmtE4C3R34::GEMM_BIAS};
+    return bias[f];
+}
 
+// the GEMM kernel for the sum of the two operands' offsets: E4C3 and 2^(8/9) 8, E5C2 0, E3C3 12,
+// 2^(3/4) 10, so the sums of any two are 0, 8, 10, 12, 16, 18, 20, 22, 24
 hipError_t launch_gemm_ws_bias(int bias2, dim3 grid, hipStream_t s, const char* pa, const char* pb, const int* maxA,
                                const int* maxB, int64_t M, int64_t N, int64_t K, int64_t rta, int64_t rtb, float* c,
                                int64_t ldc, int splits, char* part, int* cnt) {
-    constexpr int E4 = FmtE4C3::GEMM_BIAS, E5 = FmtE5C2::GEMM_BIAS, E3 = FmtE3C3::GEMM_BIAS;
+    static_assert(FmtE4C3::GEMM_BIAS == 8 && FmtE5C2::GEMM_BIAS == 0 && FmtE3C3::GEMM_BIAS == 12 &&
+                      FmtE4C3R89::GEMM_BIAS == 8 && FmtE4C3R34::GEMM_BIAS == 10,
+                  "the bias sums listed below");
 #define CURVEFP_WS_GEMM(B2)                                                                                     \
     case B2:                                                                                                  \
         hipLaunchKernelGGL((gemm_ws_kernel<B2>), grid, dim3(NTHREADS), 0, s, pa, pb, maxA, maxB, M, N, K, rta, \
                            rtb, c, ldc, splits, part, cnt);                                                   \
         break;
-    static_assert(E4 + E5 != 2 * E4 && E4 + E3 != 2 * E3 && E5 + E3 != 2 * E5 && E4 + E5 != E5 + E3 &&
-                      E4 + E3 != 2 * E5 && E5 + E3 != 2 * E4,
-                  "distinct bias sums");
     switch (bias2) {
-        CURVEFP_WS_GEMM(2 * E4)
-        CURVEFP_WS_GEMM(2 * E5)
-        CURVEFP_WS_GEMM(2 * E3)
-        CURVEFP_WS_GEMM(E4 + E5)
-        CURVEFP_WS_GEMM(E4 + E3)
-        CURVEFP_WS_GEMM(E5 + E3)
+        CURVEFP_WS_GEMM(0)
+        CURVEFP_WS_GEMM(8)
+        CURVEFP_WS_GEMM(10)
+        CURVEFP_WS_GEMM(12)
+        CURVEFP_WS_GEMM(16)
+        CURVEFP_WS_GEMM(18)
+        CURVEFP_WS_GEMM(20)
+        CURVEFP_WS_GEMM(22)
+        CURVEFP_WS_GEMM(24)
         default: return hipErrorInvalidValue;
     }
 #undef CURVEFP_WS_GEMM
@@ -1380,7 +1389,10 @@ hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const 
     switch (format) {
         case 0: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, w, 0, s);
         case 1: return launch_ws_fmt<FmtE5C2>(a, as, b, bs, M, N, K, c, ldc, w, 1, s);
-        default: return launch_ws_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, w, 2, s);
+        case 2: return launch_ws_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, w, 2, s);
+        // 2^(8/9) shares E4C3's packing and exponent offset: its kernels, its own table
+        case 3: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, w, 3, s);
+        default: return launch_ws_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, c, ldc, w, 4, s);
     }
 }
 
@@ -1389,7 +1401,9 @@ hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int
     switch (format) {
         case 0: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, 0, s);
         case 1: return launch_fmt<FmtE5C2>(a, as, b, bs, M, N, K, c, ldc, 1, s);
-        default: return launch_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, 2, s);
+        case 2: return launch_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, 2, s);
+        case 3: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, 3, s);
+        default: return launch_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, c, ldc, 4, s);
     }
 }
 

@@ -1,7 +1,8 @@
 // CurveFP block quantization Q(X) on gfx950 (Sec. 3.1 of the CurveFP paper).
 //
 // For a block of 32 values with maximum magnitude amax:
-//   scale  a = smallest integer with amax <= 2^a * fl32(2^{n_max/K})  (ceil-absmax),
+//   scale  a = smallest integer with amax <= 2^a * fl32(L_max)  (ceil-absmax; L_max = r^{n_max/K},
+//          the top level, 2^{n_max/K} with binary radix),
 //          computed on the fp32 bit pattern: a = e(amax) - o_hi + [mant(amax) > mant(fl32(L_max))];
 //   element: y = |x| 2^{-a} is formed exactly by subtracting a from the exponent
 //          field; its rank is looked up in a per-format table indexed by the
@@ -19,17 +20,17 @@
 
 namespace curvefp {
 
-__device__ uint32_t g_qlut[3][QLUT_MAX];
+__device__ uint32_t g_qlut[NUM_FORMATS][QLUT_MAX];
 // bfloat16 sources: the low 16 bits of every scaled magnitude are zero, so the bucket's
 // decision point is never passed and the rank is the bucket's base rank alone (one byte)
-__device__ __attribute__((aligned(16))) uint8_t g_qlut8[3][QLUT_MAX];
-__device__ uint32_t g_lmax_mant[3];
+__device__ __attribute__((aligned(16))) uint8_t g_qlut8[NUM_FORMATS][QLUT_MAX];
+__device__ uint32_t g_lmax_mant[NUM_FORMATS];
 
 hipError_t quantize_upload(const AllTables& t) {
-    static uint32_t h[3][QLUT_MAX];
-    static uint8_t h8[3][QLUT_MAX];
-    uint32_t lm[3];
-    for (int f = 0; f < 3; f++) {
+    static uint32_t h[NUM_FORMATS][QLUT_MAX];
+    static uint8_t h8[NUM_FORMATS][QLUT_MAX];
+    uint32_t lm[NUM_FORMATS];
+    for (int f = 0; f < NUM_FORMATS; f++) {
         memcpy(h[f], t.f[f].qlut, sizeof(h[f]));
         for (int i = 0; i < QLUT_MAX; i++) h8[f][i] = (uint8_t)(t.f[f].qlut[i] >> 16);
         lm[f] = t.f[f].lmax_mant;
@@ -506,7 +507,9 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
     switch (format) {
         case 0: return launch_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, 0, codes, scales, s);
         case 1: return launch_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, 1, codes, scales, s);
-        default: return launch_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, codes, scales, s);
+        case 2: return launch_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, codes, scales, s);
+        case 3: return launch_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, 3, codes, scales, s);
+        default: return launch_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, 4, codes, scales, s);
     }
 }
 

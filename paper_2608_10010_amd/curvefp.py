@@ -15,7 +15,7 @@ import torch
 
 from . import build as _build
 
-FORMATS = {"E4C3": 0, "E5C2": 1, "E3C3": 2}
+FORMATS = {"E4C3": 0, "E5C2": 1, "E3C3": 2, "E4C3_r8/9": 3, "E4C3_r3/4": 4}
 DTYPES = {torch.float32: 0, torch.bfloat16: 1}
 STATUS = {0: "ok", -1: "ERR_NULL", -2: "ERR_SHAPE", -3: "ERR_FORMAT", -4: "ERR_BLOCK",
           -5: "ERR_ALIGN", -6: "ERR_HIP"}
@@ -45,6 +45,8 @@ def lib() -> ctypes.CDLL:
         IP = ctypes.POINTER(ctypes.c_int)
         L.curvefp_format_info.argtypes = [I, IP, IP, IP, IP]
         L.curvefp_format_info.restype = I
+        L.curvefp_format_radix.argtypes = [I, IP, IP]
+        L.curvefp_format_radix.restype = I
         L.curvefp_codes_bytes.argtypes = [I, I64, I64, I]
         L.curvefp_codes_bytes.restype = I64
         L.curvefp_scales_count.argtypes = [I64, I64, I]
@@ -91,6 +93,13 @@ def curvefp_format_info(fmt) -> Tuple[int, int, int, int]:
     _check(lib().curvefp_format_info(_fmt(fmt), ctypes.byref(b), ctypes.byref(e), ctypes.byref(c),
                                      ctypes.byref(h)), "curvefp_format_info")
     return b.value, e.value, c.value, h.value
+
+
+def curvefp_format_radix(fmt) -> Tuple[int, int]:
+    """(p, q) of the format's radix r = 2^(p/q)."""
+    p, q = ctypes.c_int(), ctypes.c_int()
+    _check(lib().curvefp_format_radix(_fmt(fmt), ctypes.byref(p), ctypes.byref(q)), "curvefp_format_radix")
+    return p.value, q.value
 
 
 def curvefp_codes_bytes(fmt, outer: int, k: int, block: int = 32) -> int:

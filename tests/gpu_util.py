@@ -12,7 +12,8 @@ import oracle
 from paper_2608_10010_amd import curvefp as cf
 
 DEV = "cuda:0"
-FMTS = ("E4C3", "E5C2", "E3C3")
+FMTS = ("E4C3", "E5C2", "E3C3", "E4C3_r8/9", "E4C3_r3/4")
+BINARY_FMTS = FMTS[:3]
 
 
 def say(*a):
@@ -56,10 +57,15 @@ def exact_values(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.ndarray:
     return np.where(nz, np.where(s == 1, -v, v), 0.0)
 
 
+def top_exponent(f) -> int:
+    """floor(log2) of the format's top level 2^{p n_max / (qK)} (binary radix: 2^{E-1} - 1)."""
+    return (f.p * f.n_max) // f.N
+
+
 def row_tops(codes, scales, fmt):
     """2^{alpha + e_max + 1}: the top of the range a row's block scales allow."""
     f = oracle.get_format(fmt)
-    e_max = 2 ** (f.E - 1) - 1
+    e_max = top_exponent(f)
     sc = scales.astype(np.int64)
     alpha = np.max(np.where(sc == oracle.POISON_SCALE, -127, sc), axis=1)
     return np.ldexp(1.0, alpha + e_max + 1)
@@ -113,7 +119,7 @@ def exact_values_elem(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.nda
 
 def row_tops_elem(scales: np.ndarray, fmt: str) -> np.ndarray:
     f = oracle.get_format(fmt)
-    e_max = 2 ** (f.E - 1) - 1
+    e_max = top_exponent(f)
     sc = scales.astype(np.int64)
     alpha = np.max(np.where(sc == oracle.POISON_SCALE, -127, sc), axis=1)
     return np.ldexp(1.0, alpha + e_max + 1)

@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 12
+    assert len(names) == 13
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -48,7 +48,13 @@ def test_format_info(L):
     assert cf.curvefp_format_info("E4C3") == (8, 4, 3, 8)
     assert cf.curvefp_format_info("E5C2") == (8, 5, 2, 4)
     assert cf.curvefp_format_info("E3C3") == (7, 3, 3, 8)
-    assert L.curvefp_format_info(3, None, None, None, None) == EFMT
+    # Tab. radix-frontier: E4C3 with r = 2^(8/9) and 2^(3/4) needs 9 and 32 phases
+    assert cf.curvefp_format_info("E4C3_r8/9") == (8, 4, 3, 9)
+    assert cf.curvefp_format_info("E4C3_r3/4") == (8, 4, 3, 32)
+    assert [cf.curvefp_format_radix(f) for f in ("E4C3", "E5C2", "E3C3", "E4C3_r8/9", "E4C3_r3/4")] == \
+        [(1, 1), (1, 1), (1, 1), (8, 9), (3, 4)]
+    assert L.curvefp_format_radix(5, None, None) == EFMT
+    assert L.curvefp_format_info(5, None, None, None, None) == EFMT
     assert L.curvefp_format_info(-1, None, None, None, None) == EFMT
 
 
@@ -60,6 +66,7 @@ def test_sizes(L):
     assert L.curvefp_codes_bytes(0, 10, 33, 32) == ESHAPE
     assert L.curvefp_codes_bytes(0, 10, 64, 16) == EBLOCK
     assert L.curvefp_codes_bytes(5, 10, 64, 32) == EFMT
+    assert cf.curvefp_codes_bytes("E4C3_r3/4", 10, 64) == 640
     assert L.curvefp_scales_count(10, 48, 32) == ESHAPE
     assert L.curvefp_scales_count(10, 64, 64) == EBLOCK
 
@@ -81,6 +88,7 @@ def test_quantize_validation(L):
     assert q(FAKE, 0, 4, 32, 32, 1, 0, 32, FAKE, None, None) == ENULL
     assert q(FAKE, 2, 4, 32, 32, 1, 0, 32, FAKE, FAKE, None) == EFMT       # dtype
     assert q(FAKE, 0, 4, 32, 32, 1, 7, 32, FAKE, FAKE, None) == EFMT       # format
+    assert q(FAKE, 0, 4, 32, 32, 1, 5, 32, FAKE, FAKE, None) == EFMT
     assert q(FAKE, 0, 4, 32, 32, 1, 0, 64, FAKE, FAKE, None) == EBLOCK     # block
     assert q(FAKE, 0, 4, 32, 32, 2, 0, 32, FAKE, FAKE, None) == EBLOCK     # axis
     assert q(FAKE, 0, 0, 32, 32, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # rows
@@ -98,7 +106,7 @@ def test_dequantize_validation(L):
     assert d(None, FAKE, 0, 4, 32, 32, FAKE, 32, None) == ENULL
     assert d(FAKE, None, 0, 4, 32, 32, FAKE, 32, None) == ENULL
     assert d(FAKE, FAKE, 0, 4, 32, 32, None, 32, None) == ENULL
-    assert d(FAKE, FAKE, 3, 4, 32, 32, FAKE, 32, None) == EFMT
+    assert d(FAKE, FAKE, 5, 4, 32, 32, FAKE, 32, None) == EFMT
     assert d(FAKE, FAKE, 0, 4, 32, 16, FAKE, 32, None) == EBLOCK
     assert d(FAKE, FAKE, 0, 4, 48, 32, FAKE, 48, None) == ESHAPE
     assert d(FAKE, FAKE, 0, 4, 32, 32, FAKE, 16, None) == ESHAPE
@@ -167,7 +175,7 @@ def test_gemm_mixed_validation(L):
         a = list(args)
         a[i] = None
         assert g(*a) == ENULL, i
-    for i, v in ((2, 3), (6, -1)):
+    for i, v in ((2, 5), (6, -1)):
         bad = list(args); bad[i] = v
         assert g(*bad) == EFMT, (i, v)
     for i, v in ((3, 2), (7, -1), (11, 16)):
