@@ -18,12 +18,14 @@ Infinity Cache) gives the HBM figure for the quantizer, and the two backward
 GEMMs of the 7B up-projection as the paper runs them (E5C2 output gradients
 times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
 `backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
-workload as `cpu_baseline`.
+workload as `cpu_baseline`.  `radix_variants` times the inference operands in
+E4C3 with the three radices of the paper's radix experiment.
 """
 
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -49,12 +51,16 @@ def parse():
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--no-backward", action="store_true",
                    help="skip the mixed-format backward GEMMs (E5C2 gradients x reused E4C3 codes)")
+    p.add_argument("--no-radix", action="store_true",
+                   help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 256 MiB device copy three times (counter calibration)")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
                    help="print the traffic summary of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) "
                         "of this script with --copy-calibration, then exit")
+    p.add_argument("--summarize-stream-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
+                   help="the same for the streaming quantize of the same runs, then exit")
     return p.parse_args()
 
 
@@ -134,6 +140,98 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
     return out
 
 
+def pmc_commands(gemm: str):
+    """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
+    run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix "
+           f"--copy-calibration --gemm {gemm}")
+    return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
+            for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
+
+
+# the bf16 -> E4C3 rows kernel with 8 chunks per thread (demangled with or without the default
+# radix arguments of Fmt)
+STREAM_KERNEL = re.compile(r"quantize_rows_kernel<curvefp::Fmt<4, 3(, 1, 1)?>, true, 8,")
+
+
+def stream_per_dispatch(d: str, counter: str):
+    """Mean per dispatch of `counter` for the streaming quantize and the calibration copy."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    per, copy_grid, rows = {}, 0, []
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            kind = "stream" if STREAM_KERNEL.search(name) else ("copy" if "copyBuffer" in name else None)
+            if kind is None:
+                continue
+            rows.append((kind, r))
+            if kind == "copy":
+                copy_grid = max(copy_grid, int(r["Grid_Size"]))
+    seen = set()
+    for kind, r in rows:
+        if kind == "copy" and int(r["Grid_Size"]) != copy_grid:
+            continue
+        inst = ((kind, r["Dispatch_Id"]), r.get("Counter_Value"), r.get("Start_Timestamp"))
+        if inst in seen:
+            continue
+        seen.add(inst)
+        key = (kind, r["Dispatch_Id"])
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for kind in ("stream", "copy"):
+        vals = [v for (k, _), v in per.items() if k == kind]
+        if not vals:
+            raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
+        out[kind] = (sum(vals) / len(vals), len(vals))
+    return out
+
+
+def summarize_stream_pmc(args):
+    fetch = stream_per_dispatch(args.summarize_stream_pmc[0], "FETCH_SIZE")
+    write = stream_per_dispatch(args.summarize_stream_pmc[1], "WRITE_SIZE")
+    f_fetch = fetch["copy"][0] * 1024.0 / COPY_BYTES
+    f_write = write["copy"][0] * 1024.0 / COPY_BYTES
+    fb = fetch["stream"][0] * 1024.0 / f_fetch
+    wb = write["stream"][0] * 1024.0 / f_write
+    elems = 32768 * 16384
+    lines = [
+        "# HBM traffic of the 1 GiB streaming quantize (32768 x 16384 bf16 -> E4C3)",
+        "",
+        "Commands (from the repository root on one MI355X, `export TMPDIR=/tmp` first; each pass is its own run):",
+        "",
+        "```",
+        *pmc_commands(args.gemm),
+        f"python bench.py --summarize-stream-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}",
+        "```",
+        "",
+        "Kernel: `quantize_rows_kernel<Fmt<4, 3>, true, 8, ...>` (bf16 -> E4C3, 8 chunks per thread), the "
+        "`quantize_stream` case of bench.py.",
+        "",
+        "| dispatch | count | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |",
+        "|---|---|---|---|",
+        f"| streaming quantize | {fetch['stream'][1]} + {write['stream'][1]} | {fetch['stream'][0]:.1f} | "
+        f"{write['stream'][0]:.1f} |",
+        f"| `__amd_rocclr_copyBuffer`, {COPY_BYTES >> 20} MiB device copy | {fetch['copy'][1]} + {write['copy'][1]} | "
+        f"{fetch['copy'][0]:.1f} | {write['copy'][0]:.1f} |",
+        "",
+        f"Calibration (same runs): the copy reads and writes {COPY_BYTES >> 20} MiB once each; the counters report "
+        f"{f_fetch:.4f}x (FETCH_SIZE) and {f_write:.4f}x (WRITE_SIZE) those bytes.",
+        f"Streaming quantize, calibrated: {fb / 1e6:.1f} MB read (algorithmic: the 1 GiB source, "
+        f"{elems * 2 / 1e6:.1f} MB) and {wb / 1e6:.1f} MB written (algorithmic: codes + scales, "
+        f"{elems * (1 + 1 / 32) / 1e6:.1f} MB).",
+        "",
+        f"fetch_bytes={fb:.0f}",
+        f"write_bytes={wb:.0f}",
+        f"kernel_source_sha256={kernel_source_digest(QUANTIZE_SOURCES)}",
+    ]
+    print("\n".join(lines))
+
+
 def summarize_pmc(args):
     fetch = pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE", args.gemm)
     write = pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE", args.gemm)
@@ -150,12 +248,7 @@ def summarize_pmc(args):
         "Commands (from the repository root on one MI355X; each pass is its own run):",
         "",
         "```",
-        f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch_{args.gemm} -o pmc -- "
-        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --no-backward --copy-calibration "
-        f"--gemm {args.gemm}",
-        f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write_{args.gemm} -o pmc -- "
-        f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-stream --no-backward --copy-calibration "
-        f"--gemm {args.gemm}",
+        *pmc_commands(args.gemm),
         f"python bench.py --summarize-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}{flag}",
         "```",
         "",
@@ -315,10 +408,62 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
     return out
 
 
+def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 10):
+    """The inference workload's operands quantized and multiplied in E4C3 with the radices of
+    Tab. radix-frontier (r = 2: 8 phases; 2^(8/9): 9; 2^(3/4): 32): per format the median of
+    `reps` individually timed calls of quantize(act), quantize(weight) and curvefp_gemm_ws."""
+    import numpy as np
+    import torch
+
+    out = {}
+    C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    ws = cf.gemm_workspace(w.M, w.N, w.K, dev)
+    for fmt in ("E4C3", "E4C3_r8/9", "E4C3_r3/4"):
+        ca, sa = cf.curvefp_quantize(ta, fmt, block_axis=w.a.axis)
+        cb, sb = cf.curvefp_quantize(tb, fmt, block_axis=w.b.axis)
+        calls = {
+            "quantize_act": lambda: cf.curvefp_quantize(ta, fmt, block_axis=w.a.axis, codes=ca, scales=sa),
+            "quantize_weight": lambda: cf.curvefp_quantize(tb, fmt, block_axis=w.b.axis, codes=cb, scales=sb),
+            "gemm": lambda: cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, fmt, c=C, workspace=ws),
+        }
+        t = {}
+        for name, fn in calls.items():
+            for _ in range(3):
+                fn()
+            torch.cuda.synchronize()
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+            t[name] = float(np.median(ts))
+        p, q = cf.curvefp_format_radix(fmt)
+        H = cf.curvefp_format_info(fmt)[3]
+        qa = w.M * w.K * quantize_bytes_per_elem(fmt, w.dtype)
+        qb = w.N * w.K * quantize_bytes_per_elem(fmt, w.dtype)
+        tf = w.flops() / t["gemm"] / 1e12
+        out[fmt] = {
+            "radix": f"2^({p}/{q})", "phases": H,
+            "us": {k: v * 1e6 for k, v in t.items()},
+            "quantize_gbps": {"act": qa / t["quantize_act"] / 1e9, "weight": qb / t["quantize_weight"] / 1e9},
+            "gemm_tflops": tf, "gemm_frac": tf / F16_DENSE_PEAK_TFLOPS,
+        }
+    out["workload"] = f"{w.name} operands ({w.M}x{w.K} act, {w.N}x{w.K} weight, bf16), block 32"
+    out["timing"] = f"median of {reps} individually timed calls each"
+    del C, ws
+    return out
+
+
 def main():
     args = parse()
     if args.summarize_pmc:
         summarize_pmc(args)
+        return
+    if args.summarize_stream_pmc:
+        summarize_stream_pmc(args)
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -488,6 +633,9 @@ def main():
             "us_back_to_back": t_b2b * 1e6, "achieved_back_to_back": nbytes / t_b2b / 1e9,
         }
         del xs, cs, ss
+
+    if not args.no_radix:
+        result["radix_variants"] = radix_variants(cf, w, ta, tb, dev, stream)
 
     if not args.no_backward:
         result["backward_mixed"] = backward_mixed(cf, W, dev, stream)
