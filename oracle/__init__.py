@@ -27,6 +27,10 @@ from .quant import (
     scale_exponents,
     quantize,
     quantize_axis0,
+    quantize_mse,
+    mse_candidates,
+    quantize_mse_axis0,
+    block_sq_error,
     dequantize,
     code_fields,
     level_value_f64,
@@ -48,7 +52,8 @@ from .gemm import (
 
 __all__ = [
     "FORMATS", "Format", "get_format", "rational_format",
-    "scale_exponents", "quantize", "quantize_axis0", "dequantize",
+    "scale_exponents", "quantize", "quantize_axis0", "quantize_mse", "quantize_mse_axis0", "mse_candidates",
+    "block_sq_error", "dequantize",
     "code_fields", "level_value_f64", "pack7", "unpack7", "POISON_SCALE",
     "gemm_exact", "gemm_exact_mixed", "mixed_lattice", "expand_scales", "product_address_mixed",
     "gemm_exact_python", "product_address", "phase_bins_one",

@@ -147,6 +147,89 @@ def quantize(x: np.ndarray, fmt: Format, block: int = 32):
     return codes.reshape(outer, k).astype(np.uint8), a.astype(np.int8)
 
 
+def _codes_at_scale(xb: np.ndarray, a: np.ndarray, fmt: Format) -> np.ndarray:
+    """Codes of finite blocks xb [..., block] (float64 copies of the source) at the block
+    scales a [...]: sign kept, magnitude nearest to |x| 2^-a, saturating (Sec. 3.1)."""
+    y = np.ldexp(np.abs(xb), -a[..., None])
+    is_zero, n = _nearest_index(y, fmt)
+    codes = (np.signbit(xb).astype(np.int64) << (fmt.E + fmt.C)) | (n + fmt.B)
+    return np.where(is_zero, 0, codes)
+
+
+def _reconstruct_f32(codes: np.ndarray, a: np.ndarray, fmt: Format) -> np.ndarray:
+    """fp32 reconstruction of block codes [..., block] at the block scales a [...]."""
+    nz, s, n = code_fields(codes, fmt)
+    mag = np.ldexp(level_value_f64(fmt, np.where(nz, n, 0)), a[..., None])
+    val = np.where(nz, np.where(s == 1, -mag, mag), 0.0)
+    with np.errstate(over="ignore"):
+        return val.astype(np.float32)
+
+
+def block_sq_error(xb: np.ndarray, xh: np.ndarray) -> np.ndarray:
+    """Reconstruction error of each block: sum over i of (x_i - x_hat_i)^2, each step one
+    float64 operation, i in index order (no fused multiply-add)."""
+    d = xb.astype(np.float64) - xh.astype(np.float64)
+    acc = np.zeros(d.shape[:-1], dtype=np.float64)
+    with np.errstate(over="ignore", invalid="ignore"):
+        for i in range(d.shape[-1]):
+            acc = acc + d[..., i] * d[..., i]
+    return acc
+
+
+def mse_candidates(fmt: Format, candidates: int):
+    """Scale offsets from the ceil-absmax scale a_c that the static search tries, in order:
+    0, -1, ..., -(candidates - 1) (``candidates`` counts the scales at or below a_c), then
+    +1, ..., +(P - 1), where P = p / gcd(p, qK) is the number
+    of octaves after which the level pattern 2^(p n / (qK)) repeats (1 for binary radix and
+    2^(8/9), 3 for 2^(3/4)).  A scale a_c + P + j is never better than a_c + j (j >= 0): its
+    levels are those of a_c + j shifted up by a whole pattern, so it keeps every level up to the
+    block's top and only drops levels at the bottom; within one pattern the lattices differ."""
+    period = fmt.p // fmt.g
+    return [-d for d in range(candidates)] + list(range(1, period))
+
+
+def quantize_mse(x: np.ndarray, fmt: Format, candidates: int = 4, block: int = 32):
+    """Q(X) with static-operand scales: each block takes the power-of-two scale among a_c + u,
+    u in mse_candidates(fmt, candidates) (a_c the ceil-absmax scale; scales outside [-127, 127]
+    are not tried), whose fp32 reconstruction has the least squared error (block_sq_error);
+    a tie keeps the scale tried first (Sec. 3.1: static operands choose a representable scale
+    by reconstruction-MSE search).  Zero blocks get scale 0, non-finite blocks -128, as in
+    quantize().  Returns (codes, scales) like quantize()."""
+    x = np.asarray(x)
+    assert x.dtype == np.float32 and x.ndim == 2 and 1 <= candidates <= 8
+    outer, k = x.shape
+    assert k % block == 0
+    xb = x.astype(np.float64).reshape(outer, k // block, block)
+    mag = np.abs(xb)
+    with np.errstate(invalid="ignore"):
+        finite_block = np.all(np.isfinite(xb), axis=-1)
+    amax = np.where(finite_block, np.max(np.where(np.isfinite(mag), mag, 0.0), axis=-1), np.inf)
+    a_c = scale_exponents(amax, fmt)
+    live = finite_block & (amax > 0)
+    xs = np.where(finite_block[..., None], xb, 0.0)
+    best_a = np.where(live, a_c, 0)
+    best_codes = _codes_at_scale(xs, best_a, fmt)
+    best_err = block_sq_error(xs, _reconstruct_f32(best_codes, best_a, fmt))
+    for u in mse_candidates(fmt, candidates)[1:]:
+        a = a_c + u
+        ok = live & (a >= SCALE_MIN) & (a <= SCALE_MAX)
+        a_try = np.where(ok, a, 0)
+        codes = _codes_at_scale(xs, a_try, fmt)
+        err = block_sq_error(xs, _reconstruct_f32(codes, a_try, fmt))
+        take = ok & (err < best_err)
+        best_a = np.where(take, a, best_a)
+        best_codes = np.where(take[..., None], codes, best_codes)
+        best_err = np.where(take, err, best_err)
+    codes = np.where(live[..., None], best_codes, 0)
+    scales = np.where(finite_block, best_a, POISON_SCALE)
+    return codes.reshape(outer, k).astype(np.uint8), scales.astype(np.int8)
+
+
+def quantize_mse_axis0(x: np.ndarray, fmt: Format, candidates: int = 4, block: int = 32):
+    """quantize_mse with blocks along the rows of x: codes [cols, rows]."""
+    return quantize_mse(np.ascontiguousarray(np.asarray(x).T), fmt, candidates, block)
+
+
 def quantize_axis0(x: np.ndarray, fmt: Format, block: int = 32):
     """Blocks along the rows of x: quantizes x^T, giving codes [cols, rows]."""
     return quantize(np.ascontiguousarray(np.asarray(x).T), fmt, block)

@@ -772,3 +772,133 @@ def test_mixed_rational_gemm_matches_float64_matmul(pair):
     da, db = _deq_exact64(ca, sa, fa), _deq_exact64(cb, sb, fb)
     absmm = np.abs(da) @ np.abs(db).T
     assert np.all(np.abs(C - da @ db.T) <= 1e-13 * absmm)
+
+
+# ------------------------------------------------------------------ static-operand MSE scales (Sec. 3.1)
+
+def _exact_block_error(block, a, f):
+    """Exact squared reconstruction error of one block at scale a (Fractions), with the codes from
+    the rigorous nearest-level rule and the fp32 reconstruction rounded rigorously."""
+    tot = Fraction(0)
+    for v in block:
+        v = float(v)
+        if v == 0.0:
+            continue
+        y = abs(v) * 2.0 ** (-a)                       # exact: a power-of-two rescale of an fp32
+        m, e = math.frexp(y)                            # y = m 2^e, m in [0.5, 1)
+        M, j = int(m * (1 << 24)), e - 1
+        n = X.nearest_level(M, j, f.E, f.C, f.p, f.q) if M >= (1 << 23) else None
+        xh = 0.0 if n is None else math.copysign(X.rn_f32_level(a, n, f.p, f.N), v)
+        if math.isinf(xh):
+            return None                                 # the reconstruction overflows fp32
+        tot += (Fraction(v) - Fraction(xh)) ** 2
+    return tot
+
+
+def _mse_blocks(seed):
+    """Blocks where a lower scale can win: heavy tails, single outliers, a clipped top."""
+    rng = np.random.default_rng(seed)
+    b = [rng.standard_t(2, (24, 32)), rng.standard_normal((24, 32)),
+         np.where(rng.random((24, 32)) < 0.05, 40.0, 1.0) * rng.standard_normal((24, 32))]
+    return (np.concatenate(b) * 0.03).astype(np.float32)
+
+
+@pytest.mark.parametrize("name", ALL_NAMES)
+def test_mse_scale_is_the_exact_argmin(name):
+    """The chosen scale minimizes the exact squared error over the candidates (a_c .. a_c - 3 and,
+    when the level pattern spans P > 1 octaves, a_c + 1 .. a_c + P - 1), computed with exact
+    Fractions of rigorously reconstructed values; a winner within 1e-12 of the best exact error
+    is accepted (the float64 sum decides near-ties), and an exact tie keeps the first tried."""
+    f = oracle.get_format(name)
+    offs = oracle.mse_candidates(f, 4)
+    assert offs[:4] == [0, -1, -2, -3] and len(offs) == 4 + (f.p // math.gcd(f.p, f.N)) - 1
+    x = _mse_blocks(21)
+    codes, scales = oracle.quantize_mse(x, f, candidates=4)
+    _, s_ceil = oracle.quantize(x, f)
+    moved = 0
+    for r in range(x.shape[0]):
+        ac = int(s_ceil[r, 0])
+        errs = {}
+        for u in offs:
+            e = _exact_block_error(x[r], ac + u, f)
+            if e is not None:
+                errs[ac + u] = e
+        best = min(errs.values())
+        got = int(scales[r, 0])
+        assert errs[got] <= best * (1 + Fraction(1, 10 ** 12)), (r, got, errs)
+        first = next(ac + u for u in offs if ac + u in errs and errs[ac + u] == errs[got])
+        assert got == first
+        moved += got != ac
+    # the search changes something on this data for the narrow formats
+    if name in ("E3C3", "E4C3_r3/4"):
+        assert moved > 0
+
+
+@pytest.mark.parametrize("name", ALL_NAMES)
+def test_mse_scales_beyond_the_candidates_never_better(name):
+    """The reading behind the candidate set: a scale one whole level pattern above a candidate
+    at or above a_c (a_c + P + j against a_c + j) never has a smaller exact error; and for binary
+    radix and 2^(8/9) (P = 1) this rules out every scale above a_c."""
+    f = oracle.get_format(name)
+    P = f.p // math.gcd(f.p, f.N)
+    x = _mse_blocks(22)[::3]
+    _, s_ceil = oracle.quantize(x, f)
+    for r in range(x.shape[0]):
+        ac = int(s_ceil[r, 0])
+        for j in range(P):
+            e0, e1 = _exact_block_error(x[r], ac + j, f), _exact_block_error(x[r], ac + j + P, f)
+            assert e0 is not None and e1 is not None and e1 >= e0, (r, j)
+
+
+@pytest.mark.parametrize("name", ALL_NAMES)
+def test_mse_special_cases(name):
+    """One candidate is ceil-absmax; a block of representable values gets ceil-absmax's scale and
+    codes (zero error, ties keep the first tried); zero and non-finite blocks as quantize()."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(23)
+    x = (rng.standard_normal((16, 256)) * np.exp2(rng.uniform(-20, 20, (16, 1)))).astype(np.float32)
+    P = f.p // math.gcd(f.p, f.N)
+    c1, s1 = oracle.quantize_mse(x, f, 1)
+    c0, s0 = oracle.quantize(x, f)
+    if P == 1:        # one candidate, and no scale above a_c to try: ceil-absmax itself
+        assert np.array_equal(c1, c0) and np.array_equal(s1, s0)
+    else:             # candidates counts the scales at or below a_c; a_c + 1 .. a_c + P - 1 remain
+        d = s1.astype(int) - s0.astype(int)
+        assert np.all((d >= 0) & (d < P))
+    codes, scales = oracle.quantize(x, f)
+    deq = oracle.dequantize(codes, scales, f)
+    # reconstructed values are representable, so the search finds a zero-error scale and the
+    # values come back exactly.  With P = 1 that scale is their own ceil-absmax scale (its
+    # lattice contains the one they came from), and ties keep it; with 2^(3/4) halving the scale
+    # moves the lattice, so ceil-absmax can lose them where the search does not
+    c1, s1 = oracle.quantize(deq, f)
+    c2, s2 = oracle.quantize_mse(deq, f, candidates=8)
+    assert np.array_equal(oracle.dequantize(c2, s2, f), deq)
+    if P == 1:
+        assert np.array_equal(s2, s1) and np.array_equal(c2, c1)
+    else:
+        assert not np.array_equal(oracle.dequantize(c1, s1, f), deq)
+    z = np.zeros((2, 64), np.float32)
+    z[1, 3] = np.nan
+    z[1, 40] = 1.0
+    cz, sz = oracle.quantize_mse(z, f)
+    assert list(sz[0]) == [0, 0] and list(sz[1]) == [-128, sz[1, 1]] and np.all(cz[:, :32] == 0)
+    a_c = int(oracle.quantize(z, f)[1][1, 1])
+    assert sz[1, 1] == a_c if P == 1 else a_c <= sz[1, 1] < a_c + P
+
+
+def test_mse_error_sum_order():
+    """block_sq_error is the float64 sum in index order: it differs from a reordered sum on data
+    built so the order matters, and matches a literal Python loop."""
+    x = np.array([[2.0 ** 27] + [1.0] * 31], np.float64)   # 2^54 then 31 ones: in index order
+    # each 1 is below half an ulp of the running sum and is lost; reversed, they add up first
+    xh = np.zeros_like(x)
+    e = oracle.block_sq_error(x, xh)[0]
+    acc = 0.0
+    for v in x[0]:
+        acc = acc + v * v
+    assert e == acc == 2.0 ** 54
+    rev = 0.0
+    for v in x[0][::-1]:
+        rev = rev + v * v
+    assert rev == 2.0 ** 54 + 32
