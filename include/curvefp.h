@@ -66,7 +66,7 @@ typedef enum {
 typedef enum {
     CURVEFP_OK = 0,
     CURVEFP_ERR_NULL = -1,     /* a required pointer is NULL */
-    CURVEFP_ERR_SHAPE = -2,    /* non-positive or inconsistent sizes, ld too small, blocked extent % 32 != 0 */
+    CURVEFP_ERR_SHAPE = -2,    /* non-positive or inconsistent sizes or counts, ld too small, blocked extent % 32 != 0 */
     CURVEFP_ERR_FORMAT = -3,   /* unknown format or dtype */
     CURVEFP_ERR_BLOCK = -4,    /* block != 32, or block_axis not 0/1 */
     CURVEFP_ERR_ALIGN = -5,    /* pointer or row not 16-byte aligned */
@@ -110,6 +110,24 @@ int curvefp_init(void);
 int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
                      int block_axis, int format, int block,
                      void* codes, int8_t* scales, void* stream);
+
+/*
+ * Block quantization with static-operand scales (Sec. 3.1: static operands choose a
+ * representable power-of-two scale by reconstruction-MSE search), for weights quantized
+ * once.  Same arguments, layouts and results as curvefp_quantize except the scale: each
+ * block tries the scales a_c + u, a_c its ceil-absmax scale, for u = 0, -1, ...,
+ * -(candidates - 1) and then, when the format's level pattern spans P > 1 octaves
+ * (P = p / gcd(p, qK): 3 for CURVEFP_E4C3_R3_4, else 1), u = 1 .. P - 1 (a scale a_c + P + j
+ * is never better than a_c + j); scales outside [-127, 127] are skipped.  Each candidate's
+ * codes are reconstructed to fp32 exactly as curvefp_dequantize does, the squared errors
+ * (x - x_hat)^2 are summed in fp64 over the block's 32 elements in index order, each
+ * product and sum rounded once, and the first candidate in the order above with the least
+ * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE.  Zero blocks get scale 0 and
+ * non-finite blocks -128 with zero codes, as in curvefp_quantize.
+ */
+int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                         int block_axis, int format, int block, int candidates,
+                         void* codes, int8_t* scales, void* stream);
 
 /*
  * Reconstruction x_hat = (-1)^s 2^{a_b} 2^{n/K} (Eq. curvefp-value), written as

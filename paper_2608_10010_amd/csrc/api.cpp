@@ -115,6 +115,26 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
                                       reinterpret_cast<hipStream_t>(stream)));
 }
 
+int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                         int block_axis, int format, int block, int candidates, void* codes, int8_t* scales,
+                         void* stream) {
+    if (!src || !codes || !scales) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
+    if (block != 32 || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
+    if (candidates < 1 || candidates > 8) return CURVEFP_ERR_SHAPE;
+    if (rows <= 0 || cols <= 0 || ld_src < cols) return CURVEFP_ERR_SHAPE;
+    if ((block_axis == 1 ? cols : rows) % 32) return CURVEFP_ERR_SHAPE;
+    if (rows * cols / 32 / 256 >= ((int64_t)1 << 31)) return CURVEFP_ERR_SHAPE;
+    const int esz = dtype == CURVEFP_F32 ? 4 : 2;
+    if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_quantize_mse(src, dtype, rows, cols, ld_src, block_axis, format, candidates, codes, scales,
+                                          reinterpret_cast<hipStream_t>(stream)));
+}
+
 int curvefp_dequantize(const void* codes, const int8_t* scales, int format, int64_t outer, int64_t k,
                        int block, float* dst, int64_t ld_dst, void* stream) {
     if (!codes || !scales || !dst) return CURVEFP_ERR_NULL;
@@ -193,7 +213,8 @@ const char* curvefp_status_string(int status) {
     switch (status) {
         case CURVEFP_OK: return "ok";
         case CURVEFP_ERR_NULL: return "null pointer argument";
-        case CURVEFP_ERR_SHAPE: return "invalid shape, leading dimension, or blocked extent not a multiple of 32";
+        case CURVEFP_ERR_SHAPE:
+            return "invalid shape, leading dimension, count, or blocked extent not a multiple of 32";
         case CURVEFP_ERR_FORMAT: return "unknown format or dtype";
         case CURVEFP_ERR_BLOCK: return "unsupported block size or block axis";
         case CURVEFP_ERR_ALIGN: return "pointer or row not 16-byte aligned";

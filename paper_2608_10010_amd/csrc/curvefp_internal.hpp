@@ -13,6 +13,7 @@
 namespace curvefp {
 
 constexpr int floor_div_c(int a, int b) { return a / b - ((a % b != 0) && ((a < 0) != (b < 0)) ? 1 : 0); }
+constexpr int gcd_c(int a, int b) { return b == 0 ? a : gcd_c(b, a % b); }
 
 template <int E_, int C_, int P_ = 1, int Q_ = 1>
 struct Fmt {
@@ -23,6 +24,8 @@ struct Fmt {
     static constexpr int K = 1 << C;
     static constexpr int N = Q * K;                 // exponent residues: 2^{P n / N}
     static constexpr bool BINARY = P == 1 && Q == 1;
+    // octaves after which the level pattern repeats (2^{P'} = r^{N'/K} in lowest terms)
+    static constexpr int PERIOD = P / gcd_c(P, N);
     static constexpr int EC = E + C;
     static constexpr int B = 1 << (EC - 1);
     static constexpr int NMAX = B - 1;
@@ -55,6 +58,7 @@ static_assert(FmtE4C3::OZ == -9 && FmtE5C2::OZ == -17 && FmtE3C3::OZ == -5, "zer
 static_assert(FmtE4C3::OHI == 7 && FmtE5C2::OHI == 15 && FmtE3C3::OHI == 3, "top octaves");
 static_assert(FmtE4C3R89::OZ == -8 && FmtE4C3R89::OHI == 7, "2^(8/9): levels 2^(n/9), 2^-7 .. 2^7");
 static_assert(FmtE4C3R34::OZ == -7 && FmtE4C3R34::OHI == 5, "2^(3/4): levels 2^(3n/32), 2^-5.9 .. 2^5.9");
+static_assert(FmtE4C3::PERIOD == 1 && FmtE4C3R89::PERIOD == 1 && FmtE4C3R34::PERIOD == 3, "pattern periods");
 
 // GEMM expansion table: one (lo16 << 16) | hi16 fp16 pair per code byte (sign included),
 // for a block whose scale equals its row's largest; other blocks are scaled by 2^-D in fp16.
@@ -65,6 +69,7 @@ constexpr int QLUT_MAX = FmtE5C2::QLUT_SIZE;   // the largest of the formats'
 // Host-built constant tables for one format (long double arithmetic, own derivation).
 struct FormatTables {
     int K = 0;
+    int P = 1, Q = 1;               // radix 2^{P/Q}
     int qlut_size = 0;
     uint32_t qlut[QLUT_MAX];        // (m_base << 16) | thr16, see quantize.hip
     uint32_t lmax_mant = 0;         // mantissa field of fl32 of the top level
@@ -89,6 +94,11 @@ hipError_t gemm_upload(const AllTables& t);
 
 hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
                            int axis, int format, void* codes, int8_t* scales, hipStream_t s);
+// static-operand scales: reconstruction-MSE search over `candidates` scales at or below the
+// ceil-absmax scale (and, for a level pattern spanning P > 1 octaves, the P - 1 above it)
+hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
+                               int axis, int format, int candidates, void* codes, int8_t* scales,
+                               hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
                              int64_t outer, int64_t k, float* dst, int64_t ld_dst, hipStream_t s);
 // workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)

@@ -12,6 +12,7 @@
 //          (nearest in absolute error, saturating at the endpoints) derived on the host.
 // Memory: HBM-bound; one pass, coalesced 16-byte loads, one byte (or 7 bits)
 // per code and one byte per block written.
+#include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
 
@@ -25,6 +26,10 @@ __device__ uint32_t g_qlut[NUM_FORMATS][QLUT_MAX];
 // decision point is never passed and the rank is the bucket's base rank alone (one byte)
 __device__ __attribute__((aligned(16))) uint8_t g_qlut8[NUM_FORMATS][QLUT_MAX];
 __device__ uint32_t g_lmax_mant[NUM_FORMATS];
+// reconstruction tables for the static-scale search (the dequantizer's, see codec.hpp): binary
+// radix 8 entries by curve index, rational radix 128 by magnitude rank
+__device__ uint32_t g_qr_mant[NUM_FORMATS][128];
+__device__ uint64_t g_qr_sig[NUM_FORMATS][128];
 
 hipError_t quantize_upload(const AllTables& t) {
     static uint32_t h[NUM_FORMATS][QLUT_MAX];
@@ -35,9 +40,22 @@ hipError_t quantize_upload(const AllTables& t) {
         for (int i = 0; i < QLUT_MAX; i++) h8[f][i] = (uint8_t)(t.f[f].qlut[i] >> 16);
         lm[f] = t.f[f].lmax_mant;
     }
+    static uint32_t rm[NUM_FORMATS][128];
+    static uint64_t rs[NUM_FORMATS][128];
+    for (int f = 0; f < NUM_FORMATS; f++) {
+        const bool binary = t.f[f].P == 1 && t.f[f].Q == 1;
+        for (int i = 0; i < 128; i++) {
+            rm[f][i] = binary ? (i < 8 ? t.f[f].mant[i] : 0u) : t.f[f].dq_em[i];
+            rs[f][i] = binary ? (i < 8 ? t.f[f].sig62[i] : 0ull) : t.f[f].dq_sig62[i];
+        }
+    }
     hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut), h, sizeof(h));
     if (e != hipSuccess) return e;
     e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut8), h8, sizeof(h8));
+    if (e != hipSuccess) return e;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qr_mant), rm, sizeof(rm));
+    if (e != hipSuccess) return e;
+    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qr_sig), rs, sizeof(rs));
     if (e != hipSuccess) return e;
     return hipMemcpyToSymbol(HIP_SYMBOL(g_lmax_mant), lm, sizeof(lm));
 }
@@ -500,6 +518,191 @@ hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, in
     return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, s);
 }
 
+// ---------------------------------------------------------------------------------------------
+// Static-operand scales (Sec. 3.1: static operands choose a representable power-of-two scale by
+// reconstruction-MSE search).  One thread per block of 32: the block is quantized at each
+// candidate scale a_c + u (a_c ceil-absmax; u = 0, -1, .., -(candidates - 1), then 1 .. P - 1
+// when the level pattern spans P > 1 octaves), each element reconstructed to fp32 exactly as the
+// dequantizer does, and the squared error summed in fp64 in index order; the first candidate
+// with the least error wins.  Offline work for weights: simple and compute-light (a few hundred
+// fp64 operations per block).
+
+// fp32 bits -> the same value in fp64, exactly, without the fp32 denormal mode's say
+__device__ __forceinline__ double f64_of_f32_bits(uint32_t b) {
+    const uint32_t e = (b >> 23) & 0xFFu, m = b & 0x7FFFFFu;
+    double v;
+    if (e == 0) {
+        v = (double)m * 0x1p-149;                    // exact: m < 2^23, a power-of-two scale
+    } else {
+        const uint64_t d = ((uint64_t)(e - 127 + 1023) << 52) | ((uint64_t)m << 29);
+        v = __builtin_bit_cast(double, d);
+    }
+    return (b >> 31) ? -v : v;
+}
+
+// acc + d * d as two roundings (no fused multiply-add), so the sum is the same everywhere
+__device__ __forceinline__ double add_square(double acc, double d) {
+#pragma clang fp contract(off)
+    const double sq = d * d;
+    return acc + sq;
+}
+
+// rank of one magnitude at scale a (the fast or the exact path of ranks_of)
+template <class F>
+__device__ __forceinline__ uint32_t rank_at(uint32_t mag, int a, const uint32_t* lut) {
+    return a >= F::A_FAST_MIN ? rank_fast<F>(mag, a, lut) : rank_exact<F>(mag, a, lut);
+}
+
+// squared reconstruction error of the block at scale a; codes are formed and dropped element by
+// element, so only the magnitudes stay in registers across candidates
+template <class F>
+__device__ __forceinline__ double block_error(const uint32_t* mag, uint32_t sgn, int a, const uint32_t* lut,
+                                              const uint32_t* mant, const uint64_t* sig) {
+    double acc = 0.0;
+#pragma unroll
+    for (int i = 0; i < 32; i++) {
+        const uint32_t s = (sgn >> i) & 1u;
+        const uint32_t rk = rank_at<F>(mag[i], a, lut);
+        const uint32_t code = rk | ((rk != 0 ? s : 0u) << F::EC);
+        const double x = f64_of_f32_bits(mag[i] | (s << 31));
+        const double xh = f64_of_f32_bits(value_bits<F>(code, a, mant, sig));
+        acc = add_square(acc, x - xh);
+    }
+    return acc;
+}
+
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void quantize_mse_kernel(
+    const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld, int axis, int candidates,
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    __shared__ uint32_t lut[F::QLUT_SIZE];
+    constexpr int RT = F::BINARY ? 8 : 128;
+    __shared__ uint32_t mant[RT];
+    __shared__ uint64_t sig[RT];
+    for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
+    if (threadIdx.x < RT) {
+        mant[threadIdx.x] = g_qr_mant[fidx][threadIdx.x];
+        sig[threadIdx.x] = g_qr_sig[fidx][threadIdx.x];
+    }
+    const uint32_t lmax_mant = g_lmax_mant[fidx];
+    __syncthreads();
+    // block b: axis 1 -> row b / (cols / 32), block b mod (cols / 32) of it; axis 0 -> column
+    // b mod cols, rows 32 (b / cols) ..: consecutive threads take consecutive columns
+    const int64_t nbr = axis == 1 ? cols / 32 : rows / 32;          // blocks per output row
+    const int64_t nb = axis == 1 ? rows * nbr : cols * nbr;
+    const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (b >= nb) return;
+    int64_t orow, oblk;                                             // output row and block in it
+    uint32_t mag[32], sgn = 0;
+    if (axis == 1) {
+        orow = b / nbr;
+        oblk = b - orow * nbr;
+        if (BF16) {
+            const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const uint16_t*>(src) + orow * ld + 32 * oblk);
+#pragma unroll
+            for (int t = 0; t < 4; t++) {
+                const uint4 v = p[t];
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    mag[8 * t + 2 * j] = (w[j] << 16) & 0x7FFF0000u;
+                    mag[8 * t + 2 * j + 1] = w[j] & 0x7FFF0000u;
+                    sgn |= ((w[j] >> 15) & 1u) << (8 * t + 2 * j);
+                    sgn |= (w[j] >> 31) << (8 * t + 2 * j + 1);
+                }
+            }
+        } else {
+            const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const uint32_t*>(src) + orow * ld + 32 * oblk);
+#pragma unroll
+            for (int t = 0; t < 8; t++) {
+                const uint4 v = p[t];
+                const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+                for (int j = 0; j < 4; j++) {
+                    mag[4 * t + j] = w[j] & 0x7FFFFFFFu;
+                    sgn |= (w[j] >> 31) << (4 * t + j);
+                }
+            }
+        }
+    } else {
+        const int64_t rb = b / cols;
+        orow = b - rb * cols;                                       // the source column
+        oblk = rb;
+#pragma unroll
+        for (int i = 0; i < 32; i++) {
+            const int64_t e = (32 * rb + i) * ld + orow;
+            const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[e] << 16)
+                                    : reinterpret_cast<const uint32_t*>(src)[e];
+            mag[i] = w & 0x7FFFFFFFu;
+            sgn |= (w >> 31) << i;
+        }
+    }
+    uint32_t amax = 0;
+#pragma unroll
+    for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
+    const int ac = scale_of<F>(amax, lmax_mant);
+    const bool live = ac != -128 && amax != 0;
+    int best_a = ac;
+    if (live) {
+        double best_err = block_error<F>(mag, sgn, ac, lut, mant, sig);
+        const int nc = candidates + F::PERIOD - 1;
+        for (int c = 1; c < nc; c++) {
+            const int a = c < candidates ? ac - c : ac + (c - candidates + 1);
+            if (a < -127 || a > 127) continue;
+            const double err = block_error<F>(mag, sgn, a, lut, mant, sig);
+            if (err < best_err) {
+                best_err = err;
+                best_a = a;
+            }
+        }
+    }
+    uint32_t cc[32];
+#pragma unroll
+    for (int i = 0; i < 32; i++) {
+        const uint32_t rk = live ? rank_at<F>(mag[i], best_a, lut) : 0u;
+        cc[i] = rk | ((rk != 0 ? (sgn >> i) & 1u : 0u) << F::EC);
+    }
+    if (!F::PACKED7) {
+        uint4* o = reinterpret_cast<uint4*>(codes + (orow * nbr + oblk) * 32);
+#pragma unroll
+        for (int q = 0; q < 2; q++) {
+            uint32_t k[4];
+#pragma unroll
+            for (int j = 0; j < 4; j++)
+                k[j] = cc[16 * q + 4 * j] | (cc[16 * q + 4 * j + 1] << 8) | (cc[16 * q + 4 * j + 2] << 16) |
+                       (cc[16 * q + 4 * j + 3] << 24);
+            o[q] = make_uint4(k[0], k[1], k[2], k[3]);
+        }
+    } else {
+        uint32_t wds[7] = {0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+        for (int i = 0; i < 32; i++) {
+            const int bit = 7 * i;
+            wds[bit >> 5] |= cc[i] << (bit & 31);
+            if ((bit & 31) > 25) wds[(bit >> 5) + 1] |= cc[i] >> (32 - (bit & 31));
+        }
+        uint32_t* o = reinterpret_cast<uint32_t*>(codes + (orow * nbr + oblk) * 28);
+#pragma unroll
+        for (int j = 0; j < 7; j++) o[j] = wds[j];
+    }
+    scales[orow * nbr + oblk] = (int8_t)best_a;
+}
+
+template <class F>
+hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                          int candidates, int fidx, void* codes, int8_t* scales, hipStream_t s) {
+    const int64_t nb = rows * cols / 32;
+    const dim3 grid((unsigned)((nb + 255) / 256));
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    if (dtype == 1)
+        hipLaunchKernelGGL((quantize_mse_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, axis, candidates,
+                           cp, scales, fidx);
+    else
+        hipLaunchKernelGGL((quantize_mse_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, axis, candidates,
+                           cp, scales, fidx);
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
@@ -510,6 +713,21 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
         case 2: return launch_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, codes, scales, s);
         case 3: return launch_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, 3, codes, scales, s);
         default: return launch_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, 4, codes, scales, s);
+    }
+}
+
+}  // namespace curvefp
+
+namespace curvefp {
+
+hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                               int format, int candidates, void* codes, int8_t* scales, hipStream_t s) {
+    switch (format) {
+        case 0: return launch_mse_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, candidates, 0, codes, scales, s);
+        case 1: return launch_mse_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, candidates, 1, codes, scales, s);
+        case 2: return launch_mse_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, candidates, 2, codes, scales, s);
+        case 3: return launch_mse_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, candidates, 3, codes, scales, s);
+        default: return launch_mse_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, candidates, 4, codes, scales, s);
     }
 }
 

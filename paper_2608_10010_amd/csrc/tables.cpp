@@ -158,6 +158,8 @@ bool build_format(int E, int C, int P, int Q, FormatTables* ft) {
     const int K = 1 << C, N = r.N;
     const int EC = E + C;
     ft->K = K;
+    ft->P = P;
+    ft->Q = Q;
     const int ohi = floor_div(P * r.nmax, N);           // octave of the top level
     const int oz = r.zero.o;                             // octave of the zero point
     ft->qlut_size = (ohi - oz + 1) * 128;

@@ -55,6 +55,8 @@ def lib() -> ctypes.CDLL:
         L.curvefp_init.restype = I
         L.curvefp_quantize.argtypes = [P, I, I64, I64, I64, I, I, I, P, P, P]
         L.curvefp_quantize.restype = I
+        L.curvefp_quantize_mse.argtypes = [P, I, I64, I64, I64, I, I, I, I, P, P, P]
+        L.curvefp_quantize_mse.restype = I
         L.curvefp_dequantize.argtypes = [P, P, I, I64, I64, I, P, I64, P]
         L.curvefp_dequantize.restype = I
         L.curvefp_gemm.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
@@ -143,6 +145,25 @@ def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 3
                                 block_axis, f, block, codes.data_ptr(), scales.data_ptr(),
                                 _stream(stream))
     _check(st, "curvefp_quantize")
+    return codes, scales
+
+
+def curvefp_quantize_mse(src: torch.Tensor, fmt, block_axis: int = 1, candidates: int = 4, block: int = 32,
+                         codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
+                         stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """curvefp_quantize with static-operand scales chosen by reconstruction-MSE search."""
+    assert src.dim() == 2 and src.stride(1) == 1
+    rows, cols = src.shape
+    outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
+    f = _fmt(fmt)
+    if codes is None:
+        shape = (outer, k // 32, 28) if f == 2 else (outer, k)
+        codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
+    if scales is None:
+        scales = torch.empty((outer, k // block), dtype=torch.int8, device=src.device)
+    st = lib().curvefp_quantize_mse(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), block_axis, f,
+                                    block, candidates, codes.data_ptr(), scales.data_ptr(), _stream(stream))
+    _check(st, "curvefp_quantize_mse")
     return codes, scales
 
 

@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 13
+    assert len(names) == 14
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -41,6 +41,37 @@ def test_exports_every_declared_symbol(L):
         assert hasattr(L, n)
     # nothing but the C ABI is exported under the library's prefix
     assert exported == set(names)
+
+
+def declared_signatures():
+    """name -> list of parameter types (as written) of every function the header declares."""
+    text = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for m in re.finditer(r"\b(?:int|int64_t|const char\*)\s+(curvefp_[a-z0-9_]+)\s*\(([^)]*)\)\s*;", text):
+        params = [p.strip() for p in m.group(2).split(",")]
+        out[m.group(1)] = [] if params == ["void"] else params
+    return out
+
+
+def test_binding_declares_every_signature(L):
+    """The ctypes binding gives every C function its argument and result types, with one ctypes
+    type of the right width per parameter: an undeclared function would get its 64-bit pointers
+    and sizes passed as 32-bit ints (truncated device addresses)."""
+    import ctypes
+    sigs = declared_signatures()
+    assert set(sigs) == set(declared_functions())
+    width = {"int": ctypes.c_int, "int64_t": ctypes.c_int64}
+    for name, params in sigs.items():
+        fn = getattr(L, name)
+        assert fn.argtypes is not None, f"{name}: no argtypes"
+        assert len(fn.argtypes) == len(params), (name, fn.argtypes, params)
+        for t, p in zip(fn.argtypes, params):
+            if "*" in p:
+                assert t in (ctypes.c_void_p,) or issubclass(t, ctypes._Pointer), (name, p, t)
+            else:
+                base = p.split()[0]
+                assert t is width[base], (name, p, t)
+        assert fn.restype is not None, name
 
 
 def test_format_info(L):
@@ -198,3 +229,26 @@ def test_gemm_mixed_validation(L):
         assert g(*bad) == EALIGN, i
     bad = list(args); bad[14] = WS + 64
     assert g(*bad) == EALIGN
+
+
+def test_quantize_mse_validation(L):
+    q = L.curvefp_quantize_mse
+    #       src   dt rows cols ld  axis fmt blk cand codes scales stream
+    args = [FAKE, 0, 4, 32, 32, 1, 0, 32, 4, FAKE, FAKE, None]
+    for i in (0, 9, 10):
+        a = list(args); a[i] = None
+        assert q(*a) == ENULL, i
+    for i, v in ((1, 2), (6, 5), (6, -1)):
+        a = list(args); a[i] = v
+        assert q(*a) == EFMT, (i, v)
+    for i, v in ((7, 64), (5, 2)):
+        a = list(args); a[i] = v
+        assert q(*a) == EBLOCK, (i, v)
+    for i, v in ((8, 0), (8, 9), (2, 0), (3, 40), (4, 16)):
+        a = list(args); a[i] = v
+        assert q(*a) == ESHAPE, (i, v)
+    a = list(args); a[5] = 0; a[2] = 40
+    assert q(*a) == ESHAPE                      # blocks down the columns need rows % 32 == 0
+    for i in (0, 9):
+        a = list(args); a[i] = MIS
+        assert q(*a) == EALIGN, i

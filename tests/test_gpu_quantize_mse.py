@@ -1,0 +1,105 @@
+"""GPU parity of curvefp_quantize_mse (static-operand scales by reconstruction-MSE search):
+codes and scales bit for bit against the oracle's quantize_mse on the same seeded sources."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2608_10010_amd import curvefp as cf
+from paper_2608_10010_amd import workloads as W
+from tests.gpu_util import DEV, FMTS, layout_codes, say, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def oracle_mse(x, fmt, axis, candidates):
+    f = oracle.get_format(fmt)
+    if axis == 1:
+        return oracle.quantize_mse(x, f, candidates)
+    return oracle.quantize_mse_axis0(x, f, candidates)
+
+
+def run_and_compare(x, fmt, dtype, axis, candidates, what, ld_pad=0):
+    """Quantize x on the GPU and with the oracle (bf16 sources: the same bf16-rounded values)."""
+    if dtype == "bf16":
+        x = W.bf16_round(x)
+    t = to_dev(x, dtype)
+    if ld_pad:
+        wide = torch.zeros((t.shape[0], t.shape[1] + ld_pad), dtype=t.dtype, device=DEV)
+        wide[:, : t.shape[1]] = t
+        t = wide[:, : x.shape[1]]
+    codes, scales = cf.curvefp_quantize_mse(t, fmt, block_axis=axis, candidates=candidates)
+    torch.cuda.synchronize()
+    oc, osc = oracle_mse(x, fmt, axis, candidates)
+    got_c = codes.cpu().numpy().reshape(-1)
+    exp_c = layout_codes(oc, fmt).reshape(-1)
+    got_s = scales.cpu().numpy()
+    assert np.array_equal(got_s, osc), f"{what}: {np.sum(got_s != osc)} scales differ"
+    assert np.array_equal(got_c, exp_c), f"{what}: {np.sum(got_c != exp_c)} code bytes differ"
+    return osc
+
+
+def heavy(shape, seed):
+    """Blocks where a lower (or, for 2^(3/4), a higher) scale can win: t(2) tails and outliers."""
+    rng = np.random.default_rng(seed)
+    x = rng.standard_t(2, shape) * 0.02
+    x = np.where(rng.random(shape) < 0.02, x * 30, x)
+    return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("axis,shape", [(1, (37, 352)), (0, (160, 45)), (1, (300, 1024))])
+@pytest.mark.parametrize("candidates", [1, 4, 8])
+def test_random(fmt, dtype, axis, shape, candidates):
+    say(f"[quantize_mse] fmt={fmt} dtype={dtype} axis={axis} shape={shape} candidates={candidates}")
+    x = heavy(shape, 7 * shape[0] + shape[1] + candidates)
+    s = run_and_compare(x, fmt, dtype, axis, candidates, f"{fmt} {dtype} axis={axis} {shape} c={candidates}")
+    if candidates == 1 and oracle.get_format(fmt).p == 1:
+        # one candidate and no scale above ceil-absmax worth trying: the plain quantizer's scales
+        s0 = oracle.quantize(x if axis == 1 else np.ascontiguousarray(x.T), oracle.get_format(fmt))[1] \
+            if dtype == "f32" else None
+        if s0 is not None:
+            assert np.array_equal(s, s0)
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("kind", W.EDGE_KINDS + ("nonfinite",))
+def test_edges(fmt, kind):
+    x = W.edge_tensor(kind, (64, 256), seed=13)
+    say(f"[quantize_mse] edge fmt={fmt} kind={kind}")
+    run_and_compare(x, fmt, "f32", 1, 4, f"edge {kind}")
+    run_and_compare(np.ascontiguousarray(x.T), fmt, "f32", 0, 4, f"edge {kind} axis0")
+
+
+@pytest.mark.parametrize("fmt", ["E3C3", "E4C3_r3/4"])
+def test_search_moves_scales(fmt):
+    """On heavy-tailed weights the narrow formats move some block scales off ceil-absmax."""
+    x = heavy((256, 1024), 99)
+    s = run_and_compare(x, fmt, "f32", 1, 4, f"moves {fmt}")
+    s0 = oracle.quantize(x, oracle.get_format(fmt))[1]
+    moved = np.mean(s != s0)
+    say(f"[quantize_mse] {fmt}: {moved:.3%} of block scales moved")
+    assert 0 < moved < 0.5
+
+
+def test_row_stride():
+    x = heavy((64, 256), 5)
+    run_and_compare(x, "E3C3", "bf16", 1, 4, "row stride", ld_pad=24)
+
+
+@pytest.mark.parametrize("fmt", ["E3C3", "E4C3"])
+def test_inference_weight_full_size(fmt):
+    """The inference workload's 4096 x 4096 bf16 weight, quantized as a static operand in the
+    launch the benchmark times; every 61st row against the oracle (blocks are row-local)."""
+    w = W.get("inference")
+    B = w.operand("b")
+    say(f"[quantize_mse] inference weight {B.shape} fmt={fmt}")
+    codes, scales = cf.curvefp_quantize_mse(to_dev(B, "bf16"), fmt, block_axis=1, candidates=4)
+    torch.cuda.synchronize()
+    rows = np.arange(0, B.shape[0], 61)
+    oc, osc = oracle.quantize_mse(np.ascontiguousarray(B[rows]), oracle.get_format(fmt), 4)
+    gc = codes.cpu().numpy()[rows].reshape(len(rows), -1)
+    assert np.array_equal(scales.cpu().numpy()[rows], osc)
+    assert np.array_equal(gc, layout_codes(oc, fmt).reshape(len(rows), -1))
