@@ -75,13 +75,17 @@ def test_edges(fmt, kind):
 
 @pytest.mark.parametrize("fmt", ["E3C3", "E4C3_r3/4"])
 def test_search_moves_scales(fmt):
-    """On heavy-tailed weights the narrow formats move some block scales off ceil-absmax."""
+    """On heavy-tailed weights the narrow formats move some block scales off ceil-absmax (with
+    2^(3/4) most of them: a_c + 1 and a_c + 2 carry different level lattices, so each block picks
+    the best of three placements)."""
     x = heavy((256, 1024), 99)
     s = run_and_compare(x, fmt, "f32", 1, 4, f"moves {fmt}")
     s0 = oracle.quantize(x, oracle.get_format(fmt))[1]
     moved = np.mean(s != s0)
     say(f"[quantize_mse] {fmt}: {moved:.3%} of block scales moved")
-    assert 0 < moved < 0.5
+    assert moved > 0
+    if fmt == "E3C3":      # only lower scales can win, and only where clipping the top pays
+        assert moved < 0.5
 
 
 def test_row_stride():
