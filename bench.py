@@ -19,7 +19,8 @@ GEMMs of the 7B up-projection as the paper runs them (E5C2 output gradients
 times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
 `backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
 workload as `cpu_baseline`.  `radix_variants` times the inference operands in
-E4C3 with the three radices of the paper's radix experiment.
+E4C3 with the three radices of the paper's radix experiment, and `static_scales`
+the inference weight quantized with reconstruction-MSE scale search.
 """
 
 import argparse
@@ -51,6 +52,8 @@ def parse():
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--no-backward", action="store_true",
                    help="skip the mixed-format backward GEMMs (E5C2 gradients x reused E4C3 codes)")
+    p.add_argument("--no-static", action="store_true",
+                   help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
                    help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -142,7 +145,7 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
 
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
-    run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix "
+    run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -408,6 +411,40 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
     return out
 
 
+def static_scales(cf, w, tb, dev, stream, reps: int = 10):
+    """The inference weight (4096 x 4096 bf16) quantized as a static operand: curvefp_quantize_mse
+    with 4 candidate scales, against curvefp_quantize (ceil-absmax) on the same tensor; median of
+    `reps` individually timed calls each, bytes as for quantize (source + codes + scales)."""
+    import numpy as np
+    import torch
+
+    out = {}
+    nbytes = w.N * w.K * quantize_bytes_per_elem(w.fmt, w.dtype)
+    cm, sm = cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4)
+    cc, sc = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
+    calls = {"mse_search": lambda: cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4,
+                                                          codes=cm, scales=sm),
+             "ceil_absmax": lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cc, scales=sc)}
+    for name, fn in calls.items():
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        t = float(np.median(ts))
+        out[name] = {"us": t * 1e6, "gbps": nbytes / t / 1e9}
+    out["scales_moved_frac"] = float((sm != sc).float().mean().item())
+    out["workload"] = f"{w.name} weight {w.N}x{w.K} {w.dtype} -> {w.fmt}, 4 candidate scales"
+    out["timing"] = f"median of {reps} individually timed calls each"
+    return out
+
+
 def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 10):
     """The inference workload's operands quantized and multiplied in E4C3 with the radices of
     Tab. radix-frontier (r = 2: 8 phases; 2^(8/9): 9; 2^(3/4): 32): per format the median of
@@ -633,6 +670,9 @@ def main():
             "us_back_to_back": t_b2b * 1e6, "achieved_back_to_back": nbytes / t_b2b / 1e9,
         }
         del xs, cs, ss
+
+    if not args.no_static:
+        result["static_scales"] = static_scales(cf, w, tb, dev, stream)
 
     if not args.no_radix:
         result["radix_variants"] = radix_variants(cf, w, ta, tb, dev, stream)
