@@ -198,6 +198,24 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
                     void* stream);
 
 /*
+ * The product of curvefp_gemm_ws (same operands, format, workspace and fp32 values), with
+ * the output requantized in the GEMM's epilogue instead of stored as fp32: the explicit
+ * output requantization of Sec. 3.2 (products are closed on widened coordinates; only the
+ * requantization to a finite destination may saturate).  C is quantized in blocks of 32
+ * consecutive outputs along each row into out_format with the rule of curvefp_quantize
+ * (ceil-absmax scale, nearest level), so out_codes / out_scales equal curvefp_quantize
+ * (block_axis = 1) of the fp32 C that curvefp_gemm_ws returns, bit for bit.
+ *   out_codes [M][N] bytes (E3C3: [M][N/32][28]), out_scales [M][N/32].
+ * N must be a multiple of 32 (CURVEFP_ERR_SHAPE otherwise); out_codes 16-byte aligned.
+ * Other errors as curvefp_gemm_ws.
+ */
+int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales,
+                         const void* b_codes, const int8_t* b_scales,
+                         int64_t M, int64_t N, int64_t K, int format, int block, int out_format,
+                         void* out_codes, int8_t* out_scales,
+                         void* workspace, int64_t workspace_bytes, void* stream);
+
+/*
  * Bytes of device workspace curvefp_gemm_mixed needs for an M x N x K product:
  * curvefp_gemm_workspace_bytes(M, N, K) plus, per operand, 4 bytes per
  * (256-row slab of K, 32 padded GEMM rows) for the column maxima of a reused

@@ -1,5 +1,7 @@
-// The CurveFP reconstruction x_hat = (-1)^s 2^{a_b} r^{e + k/K} (Eq. curvefp-value) as fp32 bits,
-// shared by the dequantize kernel and the static-scale (MSE) quantizer.
+// Element arithmetic shared by several kernels: the CurveFP reconstruction x_hat =
+// (-1)^s 2^{a_b} r^{e + k/K} (Eq. curvefp-value) as fp32 bits (dequantize kernel, static-scale
+// quantizer), and the block quantizer's rule with the format's constants given at run time
+// (the GEMM's output requantization).
 #pragma once
 
 #include <cstdint>
@@ -44,6 +46,45 @@ __device__ __forceinline__ uint32_t value_bits(uint32_t code, int a, const uint3
         bits = (uint32_t)q;
     }
     return bits | (s << 31);
+}
+
+// The quantizer of Sec. 3.1 with run-time format constants: the same decisions as the quantize
+// kernels (quantize.hip: block_scale, scale_of, rank_exact, rank_lookup), for kernels that
+// quantize values they have computed themselves.
+struct QRule {
+    int oz;               // octave of the zero threshold (first table octave)
+    int ohi;              // octave of the top level
+    int qsize;            // table entries, (ohi - oz + 1) * 128
+    int ec;               // E + C: the sign bit's position
+    uint32_t lmax_mant;   // mantissa field of fl32 of the top level
+};
+
+// ceil-absmax block scale from the largest magnitude's fp32 bits: -128 for a non-finite block
+__device__ __forceinline__ int qr_scale(uint32_t amax, const QRule& q) {
+    if (amax >= 0x7F800000u) return -128;
+    if (amax == 0) return 0;
+    const int ef = (int)(amax >> 23);
+    if (ef == 0) return -127;                        // subnormal maximum: below every clamp
+    const int a = ef - 127 - q.ohi + (((amax & 0x7FFFFFu) > q.lmax_mant) ? 1 : 0);
+    return min(max(a, -127), 127);
+}
+
+// magnitude rank of |x| (fp32 bits without the sign) at scale a, lut = the format's table
+__device__ __forceinline__ uint32_t qr_rank(uint32_t mag, int a, const uint32_t* lut, const QRule& q) {
+    if (a == -128 || mag == 0) return 0;
+    int32_t yb;
+    if ((mag >> 23) == 0) {                          // subnormal: normalize first
+        const int p = 31 - __clz(mag);
+        const uint32_t mn = mag << (23 - p);
+        yb = (int32_t)(((uint32_t)(p - 22 - a) << 23) | (mn & 0x7FFFFFu));
+    } else {
+        yb = (int32_t)mag - (a << 23);
+    }
+    int32_t idx = (yb >> 16) - ((127 + q.oz) << 7);
+    if (idx < 0) return 0;
+    idx = min(idx, q.qsize - 1);
+    const uint32_t e = lut[idx];
+    return (e >> 16) + ((((uint32_t)yb & 0xFFFFu) > (e & 0xFFFFu)) ? 1u : 0u);
 }
 
 }  // namespace curvefp

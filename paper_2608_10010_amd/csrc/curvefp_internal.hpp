@@ -105,6 +105,10 @@ hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                           int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s);
+// curvefp_gemm_ws with C requantized in the epilogue (blocks of 32 along each output row)
+hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
+                               int64_t K, int format, int out_format, void* out_codes, int8_t* out_scales, void* ws,
+                               hipStream_t s);
 // mixed formats / reused forward operands (trans: codes of a [K][R] tensor, blocks along R)
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,

@@ -33,7 +33,9 @@
 // Small problems split K in two (grid.z = 2) so the grid covers the 256
 // compute units; the two partial sums land in C through fp32 atomic adds on
 // a zero-filled C, which is order-independent for two terms.
+#include "codec.hpp"
 #include "curvefp_internal.hpp"
+#include "device_util.hpp"
 
 #include <cstring>
 #include <type_traits>
@@ -41,8 +43,23 @@
 namespace curvefp {
 
 __device__ uint32_t g_dec[NUM_FORMATS][GEMM_DEC_ENTRIES];
+// output requantization: the quantize tables of every format (the quantizer's, quantize.hip)
+__device__ uint32_t g_gq_lut[NUM_FORMATS][QLUT_MAX];
+// and the constants of its rule, kept on the host for the launch (the same on every device)
+static QRule g_qrule[NUM_FORMATS];
 
 hipError_t gemm_upload(const AllTables& t) {
+    static uint32_t q[NUM_FORMATS][QLUT_MAX];
+    for (int f = 0; f < NUM_FORMATS; f++) memcpy(q[f], t.f[f].qlut, sizeof(q[f]));
+    const int oz[NUM_FORMATS] = {FmtE4C3::OZ, FmtE5C2::OZ, FmtE3C3::OZ, FmtE4C3R89::OZ, FmtE4C3R34::OZ};
+    const int ohi[NUM_FORMATS] = {FmtE4C3::OHI, FmtE5C2::OHI, FmtE3C3::OHI, FmtE4C3R89::OHI, FmtE4C3R34::OHI};
+    const int ec[NUM_FORMATS] = {FmtE4C3::EC, FmtE5C2::EC, FmtE3C3::EC, FmtE4C3R89::EC, FmtE4C3R34::EC};
+    for (int f = 0; f < NUM_FORMATS; f++) {
+        if (t.f[f].qlut_size != (ohi[f] - oz[f] + 1) * 128) return hipErrorInvalidValue;
+        g_qrule[f] = QRule{oz[f], ohi[f], t.f[f].qlut_size, ec[f], t.f[f].lmax_mant};
+    }
+    hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_gq_lut), q, sizeof(q));
+    if (e != hipSuccess) return e;
     uint32_t h[NUM_FORMATS][GEMM_DEC_ENTRIES];
     for (int f = 0; f < NUM_FORMATS; f++) memcpy(h[f], t.f[f].dec, sizeof(h[f]));
     return hipMemcpyToSymbol(HIP_SYMBOL(g_dec), h, sizeof(h));
@@ -778,6 +795,123 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
     return w;
 }
 
+// ---------------------------------------------------------------------------------------------
+// Output requantization (Sec. 3.2: products are closed on widened coordinates; only the explicit
+// requantization to a finite destination may saturate).  The tile's fp32 values, exactly those
+// store_tile would write, are quantized in blocks of 32 along each output row by the quantizer's
+// rule (codec.hpp), so the codes equal curvefp_quantize of curvefp_gemm_ws's C bit for bit.  The
+// tile goes through LDS (the freed stages) in four slices of 64 rows: every wave writes its fp32
+// values of the slice (the 32 rows ti of both wave rows), then each thread quantizes two blocks
+// of 32 of the slice and stores their codes (32 contiguous bytes, or 28 packed) and scales.
+// The accumulators are only ever indexed by unrolled loop counters.
+struct ReqOut {
+    uint8_t* codes;        // [M][N] bytes, or [M][N/32][28] for 7-bit codes
+    int8_t* scales;        // [M][N/32]
+    QRule rule;
+    int fmt;               // output format (table row)
+    int packed7;
+};
+
+// float offset of (row, col) in a 64 x 256 fp32 slice: 16-byte chunks XOR-swizzled by row & 7,
+// so a thread reading its block's eight chunks and the lanes of a wave spread over the banks
+__device__ __forceinline__ int slice_off(int row, int col) {
+    return row * 256 + ((((col >> 2) ^ (row & 7))) << 2) + (col & 3);
+}
+
+template <int BIAS2, bool ADD>
+__device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sAlpha, const int* sBeta,
+                                             int64_t M, int64_t N, int64_t m0, int64_t n0, int wm, int wn,
+                                             int lane, int tid, const char* other_slot, int wbase, char* slice_mem,
+                                             char* aux, const ReqOut& ro) {
+    constexpr int BN = 256, WN = Tile<256>::WN, TN = Tile<256>::TN;
+    float* slice = reinterpret_cast<float*>(slice_mem);          // 64 rows x 256 fp32 (64 KB)
+    uint32_t* qlut = reinterpret_cast<uint32_t*>(aux);           // the output format's table
+    const QRule q = ro.rule;
+    __syncthreads();                                             // every wave is done with the stages
+    for (int i = tid; i < q.qsize; i += NTHREADS) qlut[i] = g_gq_lut[ro.fmt][i];
+    const __amdgpu_buffer_rsrc_t rq =
+        __builtin_amdgcn_make_buffer_rsrc((void*)other_slot, (short)0, ADD ? (int)BM * BN * 4 : 0, 0x00020000);
+    const int lrow = 4 * (lane >> 5);                            // row of the lane within a 32-row block
+    const int lcol = wn * WN + (lane & 31);
+    const int64_t nbr = N / 32;                                  // output blocks per row
+#pragma unroll
+    for (int ti = 0; ti < TM; ti++) {
+        // phase A: this wave's 32 rows of slice ti (slice rows wm * 32 ..) into LDS
+#pragma unroll
+        for (int tj = 0; tj < TN; tj++) {
+            const int beta = sBeta[lcol + 32 * tj] - BIAS2;
+#pragma unroll
+            for (int g = 0; g < 4; g++) {
+                const int4 al = *reinterpret_cast<const int4*>(sAlpha + wm * WM + 32 * ti + lrow + 8 * g);
+                const int alr[4] = {al.x, al.y, al.z, al.w};
+                f32x4 other;
+                if (ADD)
+                    other = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, wbase + ((ti * 4 + tj) * 4 + g) * 1024, 0,
+                                                                     AUX_DEVICE_COHERENT));
+#pragma unroll
+                for (int r = 0; r < 4; r++) {
+                    float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta);
+                    if (ADD) val += other[r];
+                    slice[slice_off(wm * 32 + lrow + 8 * g + r, lcol + 32 * tj)] = val;
+                }
+            }
+        }
+        __syncthreads();
+        // phase B: 64 rows x 8 blocks, two per thread (eight threads cover one row)
+        for (int bi = tid; bi < 64 * 8; bi += NTHREADS) {
+            const int srow = bi >> 3, cb = bi & 7;
+            const int64_t row = m0 + (srow >> 5) * WM + 32 * ti + (srow & 31);
+            const int64_t blk = n0 / 32 + cb;
+            if (row >= M || blk >= nbr) continue;
+            uint32_t bits[32];
+#pragma unroll
+            for (int c = 0; c < 8; c++) {
+                const float4 v = *reinterpret_cast<const float4*>(slice + slice_off(srow, 32 * cb + 4 * c));
+                bits[4 * c] = __builtin_bit_cast(uint32_t, v.x);
+                bits[4 * c + 1] = __builtin_bit_cast(uint32_t, v.y);
+                bits[4 * c + 2] = __builtin_bit_cast(uint32_t, v.z);
+                bits[4 * c + 3] = __builtin_bit_cast(uint32_t, v.w);
+            }
+            uint32_t amax = 0;
+#pragma unroll
+            for (int i = 0; i < 32; i++) amax = max(amax, bits[i] & 0x7FFFFFFFu);
+            const int a = qr_scale(amax, q);
+            uint32_t cd[32];
+#pragma unroll
+            for (int i = 0; i < 32; i++) {
+                const uint32_t rk = qr_rank(bits[i] & 0x7FFFFFFFu, a, qlut, q);
+                cd[i] = rk | ((rk != 0 ? bits[i] >> 31 : 0u) << q.ec);
+            }
+            if (!ro.packed7) {
+                uint4* dst = reinterpret_cast<uint4*>(ro.codes + row * N + 32 * blk);
+#pragma unroll
+                for (int h = 0; h < 2; h++) {
+                    uint32_t w[4];
+#pragma unroll
+                    for (int j = 0; j < 4; j++)
+                        w[j] = cd[16 * h + 4 * j] | (cd[16 * h + 4 * j + 1] << 8) | (cd[16 * h + 4 * j + 2] << 16) |
+                               (cd[16 * h + 4 * j + 3] << 24);
+                    dst[h] = make_uint4(w[0], w[1], w[2], w[3]);
+                }
+            } else {
+                uint32_t wd[7] = {0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+                for (int i = 0; i < 32; i++) {
+                    const int bit = 7 * i;
+                    wd[bit >> 5] |= cd[i] << (bit & 31);
+                    if ((bit & 31) > 25) wd[(bit >> 5) + 1] |= cd[i] >> (32 - (bit & 31));
+                }
+                uint32_t* dst = reinterpret_cast<uint32_t*>(ro.codes + (row * nbr + blk) * 28);
+#pragma unroll
+                for (int j = 0; j < 7; j++) dst[j] = wd[j];
+            }
+            ro.scales[row * nbr + blk] = (int8_t)a;
+        }
+        __syncthreads();                                         // the slice is free for the next ti
+    }
+}
+
 // GEMM on expanded planes: 256 x 256 tile per 256-thread workgroup as in the fused kernel (the
 // same MFMA order, so the same C bit for bit).  Two LDS stages; a step (one K block) is
 //   phase 1: the block's second fragment slice is read from LDS under the first slice's MFMAs;
@@ -786,11 +920,12 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
 //   phase 2: the copy of block s+2 into the stage just freed (buffer-to-LDS loads, 16 per
 //            thread) and the reads of block s+1's first slice go out under the second slice's MFMAs.
 // So each copy has a whole step to land, and the scheduler is held to this interleaving.
-template <int BIAS2>
+template <int BIAS2, bool REQ = false>
 __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     const char* __restrict__ PA, const char* __restrict__ PB, const int* __restrict__ maxA,
     const int* __restrict__ maxB, int64_t M, int64_t N, int64_t K, int64_t RTA, int64_t RTB,
-    float* __restrict__ C, int64_t ldc, int splits, char* __restrict__ part, int* __restrict__ cnt) {
+    float* __restrict__ C, int64_t ldc, int splits, char* __restrict__ part, int* __restrict__ cnt,
+    ReqOut ro) {
     using TL = Tile<256>;
     constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE;
     constexpr int MPS = TL::MFMA_PER_SUB;   // 48 MFMAs per 16-wide K slice
@@ -960,7 +1095,10 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
     }
 
     if (splits == 1) {
-        store_tile<BIAS2, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
+        if (REQ)
+            requant_tile<BIAS2, false>(acc, sAlpha, sBeta, M, N, m0, n0, wm, wn, lane, tid, nullptr, 0, st0, st1, ro);
+        else
+            store_tile<BIAS2, BN>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false);
         return;
     }
     // K split in two: each half publishes its scaled values (C = ldexp(D, alpha_i + beta_j -
@@ -1004,8 +1142,12 @@ __global__ __launch_bounds__(NTHREADS) void gemm_ws_kernel(
         sLast[0] = __hip_atomic_fetch_add(cnt + tile, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 1;
     __syncthreads();
     if (!sLast[0]) return;   // uniform: the other half arrives later and finishes the tile
-    store_tile<BIAS2, BN, true>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false,
-                            slots + (1 - wi.split) * PART_BYTES, wbase);
+    if (REQ)
+        requant_tile<BIAS2, true>(acc, sAlpha, sBeta, M, N, m0, n0, wm, wn, lane, tid,
+                                  slots + (1 - wi.split) * PART_BYTES, wbase, st0, st1, ro);
+    else
+        store_tile<BIAS2, BN, true>(acc, sAlpha, sBeta, C, ldc, M, N, m0, n0, wm, wn, lane, false,
+                                    slots + (1 - wi.split) * PART_BYTES, wbase);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -1223,7 +1365,37 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     const int64_t items = w.rta * w.rtb * splits;
     const int64_t grid = (items + 7) / 8 * 8;   // whole XCD shares; surplus workgroups return at once
     hipLaunchKernelGGL((gemm_ws_kernel<2 * F::GEMM_BIAS>), dim3((unsigned)grid), dim3(NTHREADS), 0, s, ws + w.planes_a,
-                       ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt);
+                       ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, c, ldc, splits, ws + w.part, cnt, ReqOut{});
+    return hipGetLastError();
+}
+
+// curvefp_gemm_ws with its epilogue requantizing C (see requant_tile): the same prep and
+// expansion launches, then gemm_ws_kernel<BIAS2, true>
+template <class F>
+hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
+                              int64_t N, int64_t K, char* ws, int fidx, int ofmt, uint8_t* qc, int8_t* qs,
+                              hipStream_t s) {
+    const WsLayout w = ws_layout(M, N, K);
+    const int64_t nkb = K / 32;
+    int* maxA = reinterpret_cast<int*>(ws + w.max_a);
+    int* maxB = reinterpret_cast<int*>(ws + w.max_b);
+    const int64_t tiles = w.rta * w.rtb;
+    const int splits = w.splits;
+    int* cnt = reinterpret_cast<int*>(ws + w.cnt);
+    const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
+                       nkb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
+    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx};
+    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx};
+    hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
+                       dim3(256), 0, s, opA, opB, nkb);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const ReqOut ro{qc, qs, g_qrule[ofmt], ofmt, ofmt == 2 ? 1 : 0};
+    const int64_t grid = (tiles * splits + 7) / 8 * 8;
+    hipLaunchKernelGGL((gemm_ws_kernel<2 * F::GEMM_BIAS, true>), dim3((unsigned)grid), dim3(NTHREADS), 0, s,
+                       ws + w.planes_a, ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, nullptr, N, splits,
+                       ws + w.part, cnt, ro);
     return hipGetLastError();
 }
 
@@ -1245,7 +1417,7 @@ hipError_t launch_gemm_ws_bias(int bias2, dim3 grid, hipStream_t s, const char* 
 #define CURVEFP_WS_GEMM(B2)                                                                                     \
     case B2:                                                                                                  \
         hipLaunchKernelGGL((gemm_ws_kernel<B2>), grid, dim3(NTHREADS), 0, s, pa, pb, maxA, maxB, M, N, K, rta, \
-                           rtb, c, ldc, splits, part, cnt);                                                   \
+                           rtb, c, ldc, splits, part, cnt, ReqOut{});                                         \
         break;
     switch (bias2) {
         CURVEFP_WS_GEMM(0)
@@ -1377,6 +1549,20 @@ hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout(M, N, K).bytes; }
 
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) { return mixed_layout(M, N, K).bytes; }
+
+hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
+                               int64_t K, int format, int out_format, void* out_codes, int8_t* out_scales, void* ws,
+                               hipStream_t s) {
+    char* w = reinterpret_cast<char*>(ws);
+    uint8_t* qc = reinterpret_cast<uint8_t*>(out_codes);
+    switch (format) {
+        case 0: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, w, 0, out_format, qc, out_scales, s);
+        case 1: return launch_requant_fmt<FmtE5C2>(a, as, b, bs, M, N, K, w, 1, out_format, qc, out_scales, s);
+        case 2: return launch_requant_fmt<FmtE3C3>(a, as, b, bs, M, N, K, w, 2, out_format, qc, out_scales, s);
+        case 3: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, w, 3, out_format, qc, out_scales, s);
+        default: return launch_requant_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, w, 4, out_format, qc, out_scales, s);
+    }
+}
 
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
                              int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, void* ws, hipStream_t s) {

@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 14
+    assert len(names) == 15
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -252,3 +252,27 @@ def test_quantize_mse_validation(L):
     for i in (0, 9):
         a = list(args); a[i] = MIS
         assert q(*a) == EALIGN, i
+
+
+def test_gemm_requant_validation(L):
+    need = L.curvefp_gemm_workspace_bytes(64, 64, 64)
+    WS = 1 << 24
+    g = L.curvefp_gemm_requant
+    #       a     as    b     bs    M   N   K  fmt blk ofmt codes scales ws  bytes stream
+    args = [FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 32, 2, FAKE, FAKE, WS, need, None]
+    for i in (0, 1, 2, 3, 10, 11, 12):
+        a = list(args); a[i] = None
+        assert g(*a) == ENULL, i
+    for i, v in ((7, 5), (9, 5), (9, -1)):
+        a = list(args); a[i] = v
+        assert g(*a) == EFMT, (i, v)
+    a = list(args); a[8] = 64
+    assert g(*a) == EBLOCK
+    for i, v in ((4, 0), (5, 40), (6, 48), (13, need - 1)):
+        a = list(args); a[i] = v
+        assert g(*a) == ESHAPE, (i, v)
+    for i in (0, 2, 10):
+        a = list(args); a[i] = MIS
+        assert g(*a) == EALIGN, i
+    a = list(args); a[12] = WS + 64
+    assert g(*a) == EALIGN
