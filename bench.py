@@ -19,8 +19,9 @@ GEMMs of the 7B up-projection as the paper runs them (E5C2 output gradients
 times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
 `backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
 workload as `cpu_baseline`.  `radix_variants` times the inference operands in
-E4C3 with the three radices of the paper's radix experiment, and `static_scales`
-the inference weight quantized with reconstruction-MSE scale search.
+E4C3 with the three radices of the paper's radix experiment, `static_scales`
+the inference weight quantized with reconstruction-MSE scale search, and
+`requant` the inference GEMM with its output requantized in the epilogue.
 """
 
 import argparse
@@ -52,6 +53,8 @@ def parse():
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--no-backward", action="store_true",
                    help="skip the mixed-format backward GEMMs (E5C2 gradients x reused E4C3 codes)")
+    p.add_argument("--no-requant", action="store_true",
+                   help="skip the GEMM with output requantization (fused epilogue vs GEMM + quantize)")
     p.add_argument("--no-static", action="store_true",
                    help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
@@ -145,7 +148,7 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
 
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
-    run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static "
+    run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -411,6 +414,51 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
     return out
 
 
+def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 10):
+    """The inference GEMM with its output requantized to E3C3 (the next layer's activation
+    format): curvefp_gemm_requant (fused epilogue) against curvefp_gemm_ws followed by
+    curvefp_quantize of the fp32 C; median of `reps` individually timed calls each."""
+    import numpy as np
+    import torch
+
+    ofmt = "E3C3"
+    ws = cf.gemm_workspace(w.M, w.N, w.K, dev)
+    C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    oc = torch.empty((w.M, w.N // 32, 28), dtype=torch.uint8, device=dev)
+    os_ = torch.empty((w.M, w.N // 32), dtype=torch.int8, device=dev)
+    oc2, os2 = torch.empty_like(oc), torch.empty_like(os_)
+
+    def fused():
+        cf.curvefp_gemm_requant(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, ofmt, out_codes=oc, out_scales=os_,
+                                workspace=ws)
+
+    def two_step():
+        cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws)
+        cf.curvefp_quantize(C, ofmt, codes=oc2, scales=os2)
+
+    out = {}
+    for name, fn in (("fused", fused), ("gemm_then_quantize", two_step)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        t = float(np.median(ts))
+        out[name] = {"us": t * 1e6, "tflops": w.flops() / t / 1e12}
+    torch.cuda.synchronize()
+    out["bit_exact"] = bool(torch.equal(oc, oc2) and torch.equal(os_, os2))
+    out["workload"] = f"{w.name}, output requantized to {ofmt} in blocks of 32 along its rows"
+    out["timing"] = f"median of {reps} individually timed calls each"
+    del ws, C
+    return out
+
+
 def static_scales(cf, w, tb, dev, stream, reps: int = 10):
     """The inference weight (4096 x 4096 bf16) quantized as a static operand: curvefp_quantize_mse
     with 4 candidate scales, against curvefp_quantize (ceil-absmax) on the same tensor; median of
@@ -670,6 +718,9 @@ def main():
             "us_back_to_back": t_b2b * 1e6, "achieved_back_to_back": nbytes / t_b2b / 1e9,
         }
         del xs, cs, ss
+
+    if not args.no_requant:
+        result["requant"] = requant(cf, w, ca, sa, cb, sb, dev, stream)
 
     if not args.no_static:
         result["static_scales"] = static_scales(cf, w, tb, dev, stream)

@@ -69,22 +69,29 @@ __device__ __forceinline__ int qr_scale(uint32_t amax, const QRule& q) {
     return min(max(a, -127), 127);
 }
 
-// magnitude rank of |x| (fp32 bits without the sign) at scale a, lut = the format's table
+// The rank of |x| (fp32 bits without the sign) at scale a in three steps, so that a caller can
+// make all its table lookups at once: the scaled magnitude's bits (subnormal inputs normalized
+// first), the table index, and the rank from the table entry (0 for zero, a poisoned scale, or a
+// magnitude below the table).  Branch-free.
+__device__ __forceinline__ int32_t qr_scaled(uint32_t mag, int a) {
+    const int p = 31 - __clz(mag | 1u);              // leading one of a subnormal input
+    const uint32_t mn = mag << max(23 - p, 0);
+    const int32_t ysub = (int32_t)(((uint32_t)(p - 22 - a) << 23) | (mn & 0x7FFFFFu));
+    return (mag >> 23) == 0 ? ysub : (int32_t)mag - (a << 23);
+}
+
+__device__ __forceinline__ int32_t qr_index(int32_t yb, const QRule& q) { return (yb >> 16) - ((127 + q.oz) << 7); }
+
+__device__ __forceinline__ uint32_t qr_from_entry(uint32_t e, int32_t yb, int32_t idx, uint32_t mag, int a) {
+    const uint32_t r = (e >> 16) + ((((uint32_t)yb & 0xFFFFu) > (e & 0xFFFFu)) ? 1u : 0u);
+    return (idx < 0 || mag == 0 || a == -128) ? 0u : r;
+}
+
+// magnitude rank of |x| at scale a, lut = the format's table
 __device__ __forceinline__ uint32_t qr_rank(uint32_t mag, int a, const uint32_t* lut, const QRule& q) {
-    if (a == -128 || mag == 0) return 0;
-    int32_t yb;
-    if ((mag >> 23) == 0) {                          // subnormal: normalize first
-        const int p = 31 - __clz(mag);
-        const uint32_t mn = mag << (23 - p);
-        yb = (int32_t)(((uint32_t)(p - 22 - a) << 23) | (mn & 0x7FFFFFu));
-    } else {
-        yb = (int32_t)mag - (a << 23);
-    }
-    int32_t idx = (yb >> 16) - ((127 + q.oz) << 7);
-    if (idx < 0) return 0;
-    idx = min(idx, q.qsize - 1);
-    const uint32_t e = lut[idx];
-    return (e >> 16) + ((((uint32_t)yb & 0xFFFFu) > (e & 0xFFFFu)) ? 1u : 0u);
+    const int32_t yb = qr_scaled(mag, a);
+    const int32_t idx = qr_index(yb, q);
+    return qr_from_entry(lut[min(max(idx, 0), q.qsize - 1)], yb, idx, mag, a);
 }
 
 }  // namespace curvefp

@@ -836,7 +836,18 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
     const int64_t nbr = N / 32;                                  // output blocks per row
 #pragma unroll
     for (int ti = 0; ti < TM; ti++) {
-        // phase A: this wave's 32 rows of slice ti (slice rows wm * 32 ..) into LDS
+        // phase A: this wave's 32 rows of slice ti (slice rows wm * 32 ..) into LDS; the other
+        // K half's sixteen partial vectors are all requested before the first is used
+        f32x4 other[TN][4];
+        if (ADD) {
+#pragma unroll
+            for (int tj = 0; tj < TN; tj++)
+#pragma unroll
+                for (int g = 0; g < 4; g++)
+                    other[tj][g] = __builtin_bit_cast(
+                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, wbase + ((ti * 4 + tj) * 4 + g) * 1024, 0,
+                                                                     AUX_DEVICE_COHERENT));
+        }
 #pragma unroll
         for (int tj = 0; tj < TN; tj++) {
             const int beta = sBeta[lcol + 32 * tj] - BIAS2;
@@ -844,15 +855,10 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
             for (int g = 0; g < 4; g++) {
                 const int4 al = *reinterpret_cast<const int4*>(sAlpha + wm * WM + 32 * ti + lrow + 8 * g);
                 const int alr[4] = {al.x, al.y, al.z, al.w};
-                f32x4 other;
-                if (ADD)
-                    other = __builtin_bit_cast(
-                        f32x4, __builtin_amdgcn_raw_buffer_load_b128(rq, wbase + ((ti * 4 + tj) * 4 + g) * 1024, 0,
-                                                                     AUX_DEVICE_COHERENT));
 #pragma unroll
                 for (int r = 0; r < 4; r++) {
                     float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta);
-                    if (ADD) val += other[r];
+                    if (ADD) val += other[tj][g][r];
                     slice[slice_off(wm * 32 + lrow + 8 * g + r, lcol + 32 * tj)] = val;
                 }
             }
@@ -864,48 +870,54 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
             const int64_t row = m0 + (srow >> 5) * WM + 32 * ti + (srow & 31);
             const int64_t blk = n0 / 32 + cb;
             if (row >= M || blk >= nbr) continue;
-            uint32_t bits[32];
-#pragma unroll
-            for (int c = 0; c < 8; c++) {
-                const float4 v = *reinterpret_cast<const float4*>(slice + slice_off(srow, 32 * cb + 4 * c));
-                bits[4 * c] = __builtin_bit_cast(uint32_t, v.x);
-                bits[4 * c + 1] = __builtin_bit_cast(uint32_t, v.y);
-                bits[4 * c + 2] = __builtin_bit_cast(uint32_t, v.z);
-                bits[4 * c + 3] = __builtin_bit_cast(uint32_t, v.w);
-            }
+            // pass 1: the block maximum; pass 2: each 16-byte chunk (re-read from LDS) quantized
+            // and packed into the output words, so only one chunk is held at a time
+            const float* rowp = slice + srow * 256;
+            auto chunk = [&](int c) {
+                return *reinterpret_cast<const uint4*>(rowp + (((8 * cb + c) ^ (srow & 7)) << 2));
+            };
             uint32_t amax = 0;
 #pragma unroll
-            for (int i = 0; i < 32; i++) amax = max(amax, bits[i] & 0x7FFFFFFFu);
+            for (int c = 0; c < 8; c++) {
+                const uint4 v = chunk(c);
+                amax = max(max(amax, max(v.x & 0x7FFFFFFFu, v.y & 0x7FFFFFFFu)),
+                           max(v.z & 0x7FFFFFFFu, v.w & 0x7FFFFFFFu));
+            }
             const int a = qr_scale(amax, q);
-            uint32_t cd[32];
+            // the packing is chosen once per block, so each loop below is straight-line code and
+            // its table lookups can be scheduled together
+            auto codes_of = [&](auto p7c) {
+                constexpr bool P7 = decltype(p7c)::value;
+                uint32_t wd[8] = {0, 0, 0, 0, 0, 0, 0, 0};
 #pragma unroll
-            for (int i = 0; i < 32; i++) {
-                const uint32_t rk = qr_rank(bits[i] & 0x7FFFFFFFu, a, qlut, q);
-                cd[i] = rk | ((rk != 0 ? bits[i] >> 31 : 0u) << q.ec);
-            }
-            if (!ro.packed7) {
-                uint4* dst = reinterpret_cast<uint4*>(ro.codes + row * N + 32 * blk);
+                for (int c = 0; c < 8; c++) {
+                    const uint4 v = chunk(c);
+                    const uint32_t b4[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
-                for (int h = 0; h < 2; h++) {
-                    uint32_t w[4];
-#pragma unroll
-                    for (int j = 0; j < 4; j++)
-                        w[j] = cd[16 * h + 4 * j] | (cd[16 * h + 4 * j + 1] << 8) | (cd[16 * h + 4 * j + 2] << 16) |
-                               (cd[16 * h + 4 * j + 3] << 24);
-                    dst[h] = make_uint4(w[0], w[1], w[2], w[3]);
+                    for (int j = 0; j < 4; j++) {
+                        const uint32_t rk = qr_rank(b4[j] & 0x7FFFFFFFu, a, qlut, q);
+                        const uint32_t code = rk | ((rk != 0 ? b4[j] >> 31 : 0u) << q.ec);
+                        if (!P7) {
+                            wd[c] |= code << (8 * j);
+                        } else {
+                            const int bit = 7 * (4 * c + j);
+                            wd[bit >> 5] |= code << (bit & 31);
+                            if ((bit & 31) > 25) wd[(bit >> 5) + 1] |= code >> (32 - (bit & 31));
+                        }
+                    }
                 }
-            } else {
-                uint32_t wd[7] = {0, 0, 0, 0, 0, 0, 0};
+                if (!P7) {
+                    uint4* dst = reinterpret_cast<uint4*>(ro.codes + row * N + 32 * blk);
+                    dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+                    dst[1] = make_uint4(wd[4], wd[5], wd[6], wd[7]);
+                } else {
+                    uint32_t* dst = reinterpret_cast<uint32_t*>(ro.codes + (row * nbr + blk) * 28);
 #pragma unroll
-                for (int i = 0; i < 32; i++) {
-                    const int bit = 7 * i;
-                    wd[bit >> 5] |= cd[i] << (bit & 31);
-                    if ((bit & 31) > 25) wd[(bit >> 5) + 1] |= cd[i] >> (32 - (bit & 31));
+                    for (int j = 0; j < 7; j++) dst[j] = wd[j];
                 }
-                uint32_t* dst = reinterpret_cast<uint32_t*>(ro.codes + (row * nbr + blk) * 28);
-#pragma unroll
-                for (int j = 0; j < 7; j++) dst[j] = wd[j];
-            }
+            };
+            if (ro.packed7) codes_of(std::true_type());
+            else codes_of(std::false_type());
             ro.scales[row * nbr + blk] = (int8_t)a;
         }
         __syncthreads();                                         // the slice is free for the next ti
