@@ -21,8 +21,14 @@
  *     negative curvefp_status; nothing is launched then.  Launch failures
  *     return CURVEFP_ERR_HIP.  Data-dependent conditions (non-finite inputs)
  *     are encoded in the outputs, never in the status.
- *   - block must be 32 (blocks of 32 consecutive elements along the
- *     contraction axis); the blocked extent must be a multiple of 32.
+ *   - block G is the number of consecutive elements along the blocked axis that
+ *     share one scale (Eq. effective-rate: R = 1 + E + C + S/G bits per value;
+ *     Sec. 3.1 evaluates fixed-size blocks, rowwise and tensorwise sharing):
+ *     any positive multiple of 32 (32, 64, ..., 512 for the block sizes the
+ *     paper sweeps; the blocked extent itself for rowwise scales), else
+ *     CURVEFP_ERR_BLOCK.  The blocked extent must be a multiple of G
+ *     (CURVEFP_ERR_SHAPE otherwise).  curvefp_quantize_mse takes G = 32 only,
+ *     and curvefp_gemm_requant's output uses G = 32 whatever its inputs use.
  *   - Code, output and (for blocks along rows) source pointers must be 16-byte
  *     aligned, and leading dimensions (in elements) must keep every row 16-byte
  *     aligned; the quantize-transpose source only needs element alignment.
@@ -33,11 +39,15 @@
  *   m = 0 is the zero sentinel (the paper reserves magnitude index zero and drops
  *   the smallest exponent/curve combination, Sec. 3.1; App. C.1 gives the same
  *   rank layout for E4C3: sign in bit 7, rank in bits 6:0, q = m - 64).
- *   E3C3 codes are packed LSB first: code i of a block of 32 occupies bits
- *   [7i, 7i+7) of a 224-bit little-endian string, i.e. 28 bytes per block.
+ *   Codes are laid out per group of 32 elements whatever G is.  E3C3 codes are
+ *   packed LSB first: code i of a group of 32 occupies bits [7i, 7i+7) of a
+ *   224-bit little-endian string, i.e. 28 bytes per group.
  *
- * Scales: int8 power-of-two exponents, one per block, row-major
- *   [outer][k / 32]; -128 marks a block that held a NaN or an infinity.
+ * Scales: int8 power-of-two exponents, one per block of G, row-major
+ *   [outer][k / G]; -128 marks a block that held a NaN or an infinity.  A block's
+ *   scale is the ceil-absmax rule applied to its largest magnitude, so a block of
+ *   G has the largest of the scales its groups of 32 would get on their own
+ *   (all-zero groups aside).
  */
 #ifndef CURVEFP_H
 #define CURVEFP_H
@@ -66,9 +76,9 @@ typedef enum {
 typedef enum {
     CURVEFP_OK = 0,
     CURVEFP_ERR_NULL = -1,     /* a required pointer is NULL */
-    CURVEFP_ERR_SHAPE = -2,    /* non-positive or inconsistent sizes or counts, ld too small, blocked extent % 32 != 0 */
+    CURVEFP_ERR_SHAPE = -2,    /* non-positive or inconsistent sizes or counts, ld too small, blocked extent % block != 0 */
     CURVEFP_ERR_FORMAT = -3,   /* unknown format or dtype */
-    CURVEFP_ERR_BLOCK = -4,    /* block != 32, or block_axis not 0/1 */
+    CURVEFP_ERR_BLOCK = -4,    /* block not a positive multiple of 32, or block_axis not 0/1 */
     CURVEFP_ERR_ALIGN = -5,    /* pointer or row not 16-byte aligned */
     CURVEFP_ERR_HIP = -6       /* a HIP call failed (launch, device query, table upload) */
 } curvefp_status;
@@ -96,10 +106,13 @@ int curvefp_init(void);
 /*
  * Block quantization Q(X) (Sec. 3.1).
  *   src     [rows][ld_src] elements of `dtype` (fp32 or bf16), row-major.
- *   block_axis = 1: blocks of 32 run along each row; codes are [rows][cols]
- *                   (E3C3: [rows][cols/32][28] bytes), scales [rows][cols/32].
+ *   block_axis = 1: blocks of G run along each row; codes are [rows][cols]
+ *                   (E3C3: [rows][cols/32][28] bytes), scales [rows][cols/G].
  *   block_axis = 0: blocks run down the columns (quantize-transpose); codes are
- *                   [cols][rows] (E3C3: [cols][rows/32][28]), scales [cols][rows/32].
+ *                   [cols][rows] (E3C3: [cols][rows/32][28]), scales [cols][rows/G].
+ *   Blocks of 32..512 (a power of two) along rows are quantized in one pass; any
+ *   other G, and every G > 32 down the columns, first write the block scales in
+ *   a pass of their own (the source is read twice).
  * Scale (dynamic, ceil-absmax): a_b is the smallest integer with
  *   max|x| <= 2^{a_b} * fl32(2^{n_max/K}), clamped to [-127, 127]; 0 for an
  *   all-zero block; -128 (and all-zero codes) for a block holding NaN/Inf.
@@ -122,8 +135,9 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
  * codes are reconstructed to fp32 exactly as curvefp_dequantize does, the squared errors
  * (x - x_hat)^2 are summed in fp64 over the block's 32 elements in index order, each
  * product and sum rounded once, and the first candidate in the order above with the least
- * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE.  Zero blocks get scale 0 and
- * non-finite blocks -128 with zero codes, as in curvefp_quantize.
+ * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE; block must be 32, else
+ * CURVEFP_ERR_BLOCK.  Zero blocks get scale 0 and non-finite blocks -128 with zero codes,
+ * as in curvefp_quantize.
  */
 int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
                          int block_axis, int format, int block, int candidates,
@@ -142,7 +156,7 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
 /*
  * CurveFP GEMM: C[M][N] = deq(A)[M][K] . deq(B)[N][K]^T in fp32, the forward
  * contract Q_A(X) Q_W(W)^T of Sec. 3.3 with both operands K-contiguous
- * (A codes [M][K], B codes [N][K], scales [.][K/32], one format for both).
+ * (A codes [M][K], B codes [N][K], scales [.][K/G], one format and one G for both).
  * c is [M][ldc] fp32, overwritten.
  *
  * Every nonzero product is, in the code domain, a sign xor, a curve-index sum
@@ -232,9 +246,11 @@ int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
  *   C[M][N] = deq(A)[M][K] . deq(B)[N][K]^T in fp32, c [M][ldc], overwritten.
  * Operand layouts (per operand, X = A with R = M or X = B with R = N):
  *   x_trans = 0: the codes and scales curvefp_quantize(block_axis = 1) makes of an
- *                [R][K] tensor: codes [R][K] (E3C3 [R][K/32][28]), scales [R][K/32];
+ *                [R][K] tensor: codes [R][K] (E3C3 [R][K/32][28]), scales [R][K/G];
  *   x_trans = 1: those it makes of a [K][R] tensor: codes [K][R] (E3C3 [K][R/32][28]),
- *                scales [K][R/32]; the blocks lie along R, so R % 32 == 0.
+ *                scales [K][R/G]; the blocks lie along R, so R % G == 0.
+ *   Both operands use the same block size G; K % 32 == 0, and K % G == 0 when an
+ *   operand is quantized along K.
  * Formats a_format, b_format are any of the three.  The product of two curve
  * values with curve counts K_a, K_b (both powers of two) is a value of the finer
  * lattice L = max(K_a, K_b): indices lift as n' = (L / K) n, the phase is
@@ -245,7 +261,7 @@ int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
  * stated for curvefp_gemm.  With a_trans = b_trans = 0 and a_format == b_format the
  * result equals curvefp_gemm_ws's bit for bit.
  * Errors: as curvefp_gemm_ws, plus CURVEFP_ERR_BLOCK for a trans flag other than
- * 0/1 and CURVEFP_ERR_SHAPE for a reused operand with R % 32 != 0, more than
+ * 0/1 and CURVEFP_ERR_SHAPE for a reused operand with R % G != 0, more than
  * 65535 256-row tiles of reused operands, or a workspace smaller than
  * curvefp_gemm_mixed_workspace_bytes(M, N, K).  The workspace (256-byte aligned)
  * is scratch: calls that share it must be ordered.

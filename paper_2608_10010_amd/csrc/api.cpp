@@ -20,6 +20,9 @@ constexpr int kQ[NUM_FORMATS] = {1, 1, 1, 9, 4};
 
 bool fmt_ok(int f) { return f >= 0 && f < NUM_FORMATS; }
 
+// elements per scale: a positive multiple of 32 (codes stay laid out per 32 elements)
+bool block_ok(int b) { return b >= 32 && b % 32 == 0 && b <= (1 << 30); }
+
 int gcd_i(int a, int b) {
     while (b) {
         const int r = a % b;
@@ -83,13 +86,13 @@ int curvefp_format_radix(int format, int* p, int* q) {
 
 int64_t curvefp_codes_bytes(int format, int64_t outer, int64_t k, int block) {
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32) return CURVEFP_ERR_BLOCK;
-    if (outer < 0 || k < 0 || k % 32) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (outer < 0 || k < 0 || k % block) return CURVEFP_ERR_SHAPE;
     return format == CURVEFP_E3C3 ? outer * (k / 32) * 28 : outer * k;
 }
 
 int64_t curvefp_scales_count(int64_t outer, int64_t k, int block) {
-    if (block != 32) return CURVEFP_ERR_BLOCK;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
     if (outer < 0 || k < 0 || k % block) return CURVEFP_ERR_SHAPE;
     return outer * (k / block);
 }
@@ -101,9 +104,9 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
                      void* stream) {
     if (!src || !codes || !scales) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
-    if (block != 32 || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
+    if (!block_ok(block) || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
     if (rows <= 0 || cols <= 0 || ld_src < cols) return CURVEFP_ERR_SHAPE;
-    if ((block_axis == 1 ? cols : rows) % 32) return CURVEFP_ERR_SHAPE;
+    if ((block_axis == 1 ? cols : rows) % block) return CURVEFP_ERR_SHAPE;
     const int esz = dtype == CURVEFP_F32 ? 4 : 2;
     // blocks along rows are read with 16-byte vector loads; the transpose path reads elements
     if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
@@ -111,7 +114,7 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
     if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_quantize(src, dtype, rows, cols, ld_src, block_axis, format, codes, scales,
+    return hip_status(launch_quantize(src, dtype, rows, cols, ld_src, block_axis, format, block, codes, scales,
                                       reinterpret_cast<hipStream_t>(stream)));
 }
 
@@ -139,12 +142,12 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format, int6
                        int block, float* dst, int64_t ld_dst, void* stream) {
     if (!codes || !scales || !dst) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32) return CURVEFP_ERR_BLOCK;
-    if (outer <= 0 || k <= 0 || k % 32 || ld_dst < k) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (outer <= 0 || k <= 0 || k % block || ld_dst < k) return CURVEFP_ERR_SHAPE;
     if (!aligned16(codes) || !aligned16(dst) || (ld_dst * 4) % 16) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_dequantize(codes, scales, format, outer, k, dst, ld_dst,
+    return hip_status(launch_dequantize(codes, scales, format, outer, k, block, dst, ld_dst,
                                         reinterpret_cast<hipStream_t>(stream)));
 }
 
@@ -153,12 +156,12 @@ int curvefp_gemm(const void* a_codes, const int8_t* a_scales, const void* b_code
                  void* stream) {
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_gemm(a_codes, a_scales, b_codes, b_scales, M, N, K, format, c, ldc,
+    return hip_status(launch_gemm(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc,
                                   reinterpret_cast<hipStream_t>(stream)));
 }
 
@@ -172,14 +175,14 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
                     void* workspace, int64_t workspace_bytes, void* stream) {
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c || !workspace) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_gemm_ws(a_codes, a_scales, b_codes, b_scales, M, N, K, format, c, ldc, workspace,
+    return hip_status(launch_gemm_ws(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc, workspace,
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
@@ -189,15 +192,15 @@ int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void
     if (!a_codes || !a_scales || !b_codes || !b_scales || !out_codes || !out_scales || !workspace)
         return CURVEFP_ERR_NULL;
     if (!fmt_ok(format) || !fmt_ok(out_format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || N % 32) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % block || N % 32) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(out_codes)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_gemm_requant(a_codes, a_scales, b_codes, b_scales, M, N, K, format, out_format, out_codes,
-                                          out_scales, workspace, reinterpret_cast<hipStream_t>(stream)));
+    return hip_status(launch_gemm_requant(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, out_format,
+                                          out_codes, out_scales, workspace, reinterpret_cast<hipStream_t>(stream)));
 }
 
 int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) {
@@ -211,11 +214,13 @@ int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format
                        void* workspace, int64_t workspace_bytes, void* stream) {
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c || !workspace) return CURVEFP_ERR_NULL;
     if (!fmt_ok(a_format) || !fmt_ok(b_format)) return CURVEFP_ERR_FORMAT;
-    if (block != 32 || (a_trans != 0 && a_trans != 1) || (b_trans != 0 && b_trans != 1)) return CURVEFP_ERR_BLOCK;
+    if (!block_ok(block) || (a_trans != 0 && a_trans != 1) || (b_trans != 0 && b_trans != 1)) return CURVEFP_ERR_BLOCK;
     if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
-    // a reused operand has its blocks along its GEMM rows; the expansion grid has one
-    // workgroup row per 256 GEMM rows of each reused operand (at most 65535 in all)
-    if ((a_trans && M % 32) || (b_trans && N % 32)) return CURVEFP_ERR_SHAPE;
+    // an operand quantized along K has its blocks along K; a reused operand has them along its
+    // GEMM rows; the expansion grid has one workgroup row per 256 GEMM rows of each reused
+    // operand (at most 65535 in all)
+    if ((!a_trans || !b_trans) && K % block) return CURVEFP_ERR_SHAPE;
+    if ((a_trans && M % block) || (b_trans && N % block)) return CURVEFP_ERR_SHAPE;
     if ((a_trans ? (M + 255) / 256 : 0) + (b_trans ? (N + 255) / 256 : 0) > 65535) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_mixed_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
@@ -223,7 +228,7 @@ int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format
     int st = ensure_tables();
     if (st) return st;
     return hip_status(launch_gemm_mixed(a_codes, a_scales, a_format, a_trans, b_codes, b_scales, b_format, b_trans,
-                                        M, N, K, c, ldc, workspace, reinterpret_cast<hipStream_t>(stream)));
+                                        M, N, K, block, c, ldc, workspace, reinterpret_cast<hipStream_t>(stream)));
 }
 
 const char* curvefp_status_string(int status) {
@@ -231,7 +236,7 @@ const char* curvefp_status_string(int status) {
         case CURVEFP_OK: return "ok";
         case CURVEFP_ERR_NULL: return "null pointer argument";
         case CURVEFP_ERR_SHAPE:
-            return "invalid shape, leading dimension, count, or blocked extent not a multiple of 32";
+            return "invalid shape, leading dimension, count, or blocked extent not a multiple of the block";
         case CURVEFP_ERR_FORMAT: return "unknown format or dtype";
         case CURVEFP_ERR_BLOCK: return "unsupported block size or block axis";
         case CURVEFP_ERR_ALIGN: return "pointer or row not 16-byte aligned";

@@ -92,29 +92,33 @@ hipError_t quantize_upload(const AllTables& t);
 hipError_t dequantize_upload(const AllTables& t);
 hipError_t gemm_upload(const AllTables& t);
 
+// `block` (a multiple of 32 dividing the blocked extent) is the number of consecutive elements
+// that share one scale in every launcher below; codes are laid out per 32 elements regardless
 hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
-                           int axis, int format, void* codes, int8_t* scales, hipStream_t s);
+                           int axis, int format, int block, void* codes, int8_t* scales, hipStream_t s);
 // static-operand scales: reconstruction-MSE search over `candidates` scales at or below the
 // ceil-absmax scale (and, for a level pattern spanning P > 1 octaves, the P - 1 above it)
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
                                int axis, int format, int candidates, void* codes, int8_t* scales,
                                hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
-                             int64_t outer, int64_t k, float* dst, int64_t ld_dst, hipStream_t s);
+                             int64_t outer, int64_t k, int block, float* dst, int64_t ld_dst, hipStream_t s);
 // workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                          int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s);
+                          int64_t N, int64_t K, int format, int block, float* c, int64_t ldc, void* ws,
+                          hipStream_t s);
 // curvefp_gemm_ws with C requantized in the epilogue (blocks of 32 along each output row)
 hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
-                               int64_t K, int format, int out_format, void* out_codes, int8_t* out_scales, void* ws,
-                               hipStream_t s);
+                               int64_t K, int format, int block, int out_format, void* out_codes, int8_t* out_scales,
+                               void* ws, hipStream_t s);
 // mixed formats / reused forward operands (trans: codes of a [K][R] tensor, blocks along R)
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
-                             int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, void* ws, hipStream_t s);
+                             int tb, int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc, void* ws,
+                             hipStream_t s);
 hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int8_t* bs,
-                       int64_t M, int64_t N, int64_t K, int format, float* c, int64_t ldc,
+                       int64_t M, int64_t N, int64_t K, int format, int block, float* c, int64_t ldc,
                        hipStream_t s);
 
 }  // namespace curvefp

@@ -49,7 +49,7 @@ namespace {
 template <class F>
 __global__ __launch_bounds__(256) void dequantize_kernel(
     const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
-    Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx) {
+    Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx, Div32 dgq) {
     constexpr int TAB = F::BINARY ? 8 : 128;
     __shared__ uint32_t mant[TAB];
     __shared__ uint64_t sig[TAB];
@@ -61,8 +61,8 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
     const bool dense = ld == (int64_t)cpr * 8;
     const uint32_t stride = gridDim.x * 256u;
     for (uint32_t g = blockIdx.x * 256u + threadIdx.x; g < nchunks; g += stride) {
-        const uint32_t b = g >> 2;
-        const int a = scales[b];
+        const uint32_t b = g >> 2;                  // 32-element group; its scale is that of block b / (G / 32)
+        const int a = scales[div32(b, dgq)];
         uint32_t c[8];
         if (!F::PACKED7) {
             const uint2 w = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
@@ -105,8 +105,9 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
 }
 
 template <class F>
-hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, int64_t k, float* dst,
+hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, int64_t k, int block, float* dst,
                       int64_t ld, int fidx, hipStream_t s) {
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
     const int64_t cpr = k / 8;
     const int64_t slab = ((int64_t)1 << 31) / cpr;   // 32-bit chunk indices per launch
     const uint8_t* cp = reinterpret_cast<const uint8_t*>(codes);
@@ -116,8 +117,8 @@ hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, in
         int64_t blocks = (nchunks + 255) / 256;
         blocks = blocks < 8192 ? blocks : 8192;
         hipLaunchKernelGGL((dequantize_kernel<F>), dim3((unsigned)blocks), dim3(256), 0, s,
-                           cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / 32),
-                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx);
+                           cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / block),
+                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx, dgq);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -127,13 +128,13 @@ hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, in
 }  // namespace
 
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format, int64_t outer,
-                             int64_t k, float* dst, int64_t ld_dst, hipStream_t s) {
+                             int64_t k, int block, float* dst, int64_t ld_dst, hipStream_t s) {
     switch (format) {
-        case 0: return launch_fmt<FmtE4C3>(codes, scales, outer, k, dst, ld_dst, 0, s);
-        case 1: return launch_fmt<FmtE5C2>(codes, scales, outer, k, dst, ld_dst, 1, s);
-        case 2: return launch_fmt<FmtE3C3>(codes, scales, outer, k, dst, ld_dst, 2, s);
-        case 3: return launch_fmt<FmtE4C3R89>(codes, scales, outer, k, dst, ld_dst, 3, s);
-        default: return launch_fmt<FmtE4C3R34>(codes, scales, outer, k, dst, ld_dst, 4, s);
+        case 0: return launch_fmt<FmtE4C3>(codes, scales, outer, k, block, dst, ld_dst, 0, s);
+        case 1: return launch_fmt<FmtE5C2>(codes, scales, outer, k, block, dst, ld_dst, 1, s);
+        case 2: return launch_fmt<FmtE3C3>(codes, scales, outer, k, block, dst, ld_dst, 2, s);
+        case 3: return launch_fmt<FmtE4C3R89>(codes, scales, outer, k, block, dst, ld_dst, 3, s);
+        default: return launch_fmt<FmtE4C3R34>(codes, scales, outer, k, block, dst, ld_dst, 4, s);
     }
 }
 

@@ -331,7 +331,7 @@ template <class F, int BN_>
 __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     const uint8_t* __restrict__ A, const int8_t* __restrict__ As,
     const uint8_t* __restrict__ B, const int8_t* __restrict__ Bs,
-    int64_t M, int64_t N, int64_t K, float* __restrict__ C, int64_t ldc, int fidx) {
+    int64_t M, int64_t N, int64_t K, float* __restrict__ C, int64_t ldc, int fidx, int64_t nsb, Div32 dgq) {
     using TL = Tile<BN_>;
     constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE, TASKS = TL::TASKS;
     constexpr int PLANE_B = TL::PLANE_B;
@@ -367,12 +367,14 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     // scales are read as aligned dwords (a 32-bit result keeps the compiler from extending a
     // byte at its load): the descriptors start at the dword below the tile's first scale and
     // end at the dword that holds its last one, all inside mapped pages
-    const uintptr_t sa0 = reinterpret_cast<uintptr_t>(As + m0 * nkb), sb0 = reinterpret_cast<uintptr_t>(Bs + n0 * nkb);
+    // (nsb scales per row, one per G = 32 (G / 32) elements: K block kb has scale kb / (G / 32))
+    const uintptr_t sa0 = reinterpret_cast<uintptr_t>(As + m0 * nsb), sb0 = reinterpret_cast<uintptr_t>(Bs + n0 * nsb);
     const int dA = (int)(sa0 & 3), dB = (int)(sb0 & 3);
     const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
-        reinterpret_cast<void*>(sa0 - dA), (short)0, (int)((dA + rowsA * nkb + 3) & ~3), 0x00020000);
+        reinterpret_cast<void*>(sa0 - dA), (short)0, (int)((dA + rowsA * nsb + 3) & ~3), 0x00020000);
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
-        reinterpret_cast<void*>(sb0 - dB), (short)0, (int)((dB + rowsB * nkb + 3) & ~3), 0x00020000);
+        reinterpret_cast<void*>(sb0 - dB), (short)0, (int)((dB + rowsB * nsb + 3) & ~3), 0x00020000);
+    auto sidx = [&](int64_t kb) { return (int)div32((uint32_t)kb, dgq); };
 
     // expansion tasks: rows (tid >> 2) + 64 j of A (j < 4) and rows (tid >> 2) + 64 (j - 4) of B
     // (4 <= j < TASKS), chunk q = tid & 3
@@ -381,9 +383,9 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     const int copy4 = (tid & (LUT_COPIES - 1)) * 4;
     const int off0 = swz(r0, q);                 // swz(r0 + 64 j, q) = off0 + 64 j * ROW_BYTES
     const int voff_code = (int)(r0 * row_bytes) + (F::PACKED7 ? 4 * ((7 * q) >> 2) : 8 * q);
-    // byte offset of task j's scale of block kb: xA/xB + 64 (j & 3) nkb + kb, where the middle
-    // term is a multiple of 4 and so moves only the dword
-    const int xA = dA + (int)(r0 * nkb), xB = dB + (int)(r0 * nkb);
+    // byte offset of task j's scale of block kb: xA/xB + 64 (j & 3) nsb + sidx(kb), where the
+    // middle term is a multiple of 4 and so moves only the dword
+    const int xA = dA + (int)(r0 * nsb), xB = dB + (int)(r0 * nsb);
     // the row maxima of this thread's tasks, one byte each (scales lie in [-128, 127])
     uint32_t alpha_pk[2] = {0u, 0u};   // filled once the maxima are known
     auto alpha_of = [&](int j) { return (int)__builtin_amdgcn_sbfe(alpha_pk[j >> 2], 8 * (j & 3), 8); };
@@ -406,16 +408,16 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     auto blocks = [&](int64_t kb_cur) {
         Blocks b;
         b.next = kb_cur + 1;
-        b.vA = (xA + (int)b.next) & ~3;
-        b.vB = (xB + (int)b.next) & ~3;
-        b.shA = 8 * ((xA + (int)kb_cur) & 3);
-        b.shB = 8 * ((xB + (int)kb_cur) & 3);
+        b.vA = (xA + sidx(b.next)) & ~3;
+        b.vB = (xB + sidx(b.next)) & ~3;
+        b.shA = 8 * ((xA + sidx(kb_cur)) & 3);
+        b.shB = 8 * ((xB + sidx(kb_cur)) & 3);
         return b;
     };
     auto fetch = [&](int j, int64_t kb, int vscl) {
         const int ro = 64 * (j & 3);
         load_raw<F>(j < 4 ? rcA : rcB, j < 4 ? rsA : rsB, voff_code,
-                    (int)(ro * row_bytes + kb * (F::PACKED7 ? 28 : 32)), vscl, (int)(ro * nkb), q, raw[j]);
+                    (int)(ro * row_bytes + kb * (F::PACKED7 ? 28 : 32)), vscl, (int)(ro * nsb), q, raw[j]);
     };
     // gather: task j's table entries into e, then the load of its next block; returns
     // D = (row maximum) - (block scale), and files min(D, 48) for the fixup pass
@@ -452,7 +454,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
 
     // codes of block 0 are requested before the maxima are computed, so both latencies overlap
 #pragma unroll
-    for (int j = 0; j < TASKS; j++) fetch(j, kb0, j < 4 ? (xA + (int)kb0) & ~3 : (xB + (int)kb0) & ~3);
+    for (int j = 0; j < TASKS; j++) fetch(j, kb0, j < 4 ? (xA + sidx(kb0)) & ~3 : (xB + sidx(kb0)) & ~3);
 
     // largest block scale of every A and B row of the tile (over all of K), 0 for rows past the
     // edge: one row per thread; up to 15 unaligned bytes at each end, 16-byte loads in between,
@@ -489,8 +491,8 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
         for (int i = 0; i < 15; i++) m = max(m, max(hb[i], tb[i]));
         return m;
     };
-    sAlpha[tid] = tid < rowsA ? row_max(As + (m0 + tid) * nkb, (int)nkb) : 0;
-    if (tid < BN) sBeta[tid] = tid < rowsB ? row_max(Bs + (n0 + tid) * nkb, (int)nkb) : 0;
+    sAlpha[tid] = tid < rowsA ? row_max(As + (m0 + tid) * nsb, (int)nsb) : 0;
+    if (tid < BN) sBeta[tid] = tid < rowsB ? row_max(Bs + (n0 + tid) * nsb, (int)nsb) : 0;
     __syncthreads();
 
 #pragma unroll
@@ -664,10 +666,10 @@ WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
 }
 
 // one launch before the expansion: row maxima of the block scales of A (workgroups
-// [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th scale of the row;
-// one more workgroup zeroes the per-tile arrival counters when K is split
+// [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th of the row's nsb
+// scales; one more workgroup zeroes the per-tile arrival counters when K is split
 __global__ __launch_bounds__(256) void prep_kernel(const int8_t* __restrict__ as, const int8_t* __restrict__ bs,
-                                                   int64_t M, int64_t N, int64_t nkb, int ga, int gb,
+                                                   int64_t M, int64_t N, int64_t nsb, int ga, int gb,
                                                    int* __restrict__ maxA, int* __restrict__ maxB,
                                                    int* __restrict__ cnt, int ncnt) {
     const int bid = (int)blockIdx.x;
@@ -683,9 +685,9 @@ __global__ __launch_bounds__(256) void prep_kernel(const int8_t* __restrict__ as
     const int part = threadIdx.x & 15;
     int m = -128;
     if (row < R) {
-        const int8_t* sp = s + row * nkb;
+        const int8_t* sp = s + row * nsb;
 #pragma unroll 8
-        for (int64_t kb = part; kb < nkb; kb += 16) m = max(m, (int)sp[kb]);
+        for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, (int)sp[sb]);
     }
 #pragma unroll
     for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
@@ -701,6 +703,8 @@ struct ExpandOperand {
     const int* rmax;
     char* planes;
     int fidx;                 // format: which expansion table
+    int64_t nsb;              // scales per row (K / G)
+    Div32 dgq;                // K block kb has scale kb / (G / 32)
 };
 
 // both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B (F fixes the code
@@ -725,16 +729,18 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     const int64_t rg = max((int64_t)0, min((int64_t)64, R - r0));
     const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(X + min(r0, R) * row_bytes), (short)0, (int)(rg * row_bytes), 0x00020000);
-    const uintptr_t s0 = reinterpret_cast<uintptr_t>(Xs + min(r0, R) * nkb);
+    const int64_t nsb = op.nsb;
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(Xs + min(r0, R) * nsb);
     const int ds = (int)(s0 & 3);
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-        reinterpret_cast<void*>(s0 - ds), (short)0, (int)((ds + rg * nkb + 3) & ~3), 0x00020000);
+        reinterpret_cast<void*>(s0 - ds), (short)0, (int)((ds + rg * nsb + 3) & ~3), 0x00020000);
     const int voff_code = (int)(lr * row_bytes) + (F::PACKED7 ? 4 * ((7 * q) >> 2) : 8 * q);
-    const int x = ds + (int)(lr * nkb);   // byte offset of the row's scales in rs
+    const int x = ds + (int)(lr * nsb);   // byte offset of the row's scales in rs
+    auto sidx = [&](int64_t kb) { return (int)div32((uint32_t)kb, op.dgq); };
     Raw<F> raw[4];
 #pragma unroll
     for (int t = 0; t < 4; t++)
-        load_raw<F>(rc, rs, voff_code, (int)((kbase + t) * (F::PACKED7 ? 28 : 32)), (x + (int)(kbase + t)) & ~3, 0, q,
+        load_raw<F>(rc, rs, voff_code, (int)((kbase + t) * (F::PACKED7 ? 28 : 32)), (x + sidx(kbase + t)) & ~3, 0, q,
                     raw[t]);
     const int alpha = rmax[row];
     __syncthreads();
@@ -742,7 +748,7 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     for (int t = 0; t < 4; t++) {
         const int64_t kb = kbase + t;
         if (kb >= nkb) break;
-        const Chunk c = settle<F>(raw[t], q, 8 * ((x + (int)kb) & 3));
+        const Chunk c = settle<F>(raw[t], q, 8 * ((x + sidx(kb)) & 3));
         uint32_t e[8];
 #pragma unroll
         for (int i = 0; i < 8; i++) e[i] = lut[chunk_code<F>(c, i)];
@@ -1202,6 +1208,8 @@ struct PrepOperand {
     int cgroups;    // trans: groups of 64 scale columns covering the tiles' tiles * 8 columns
     int* rmax;      // not trans: row maxima [tiles * 256], 0 past the last row
     int* colpart;   // trans: partial column maxima [nslab][tiles * 8]
+    int64_t nsb;    // scales per row (not trans: K / G) or per k-row (trans: rows / G)
+    Div32 dgq;      // trans: 32-row group j has scale column j / (G / 32)
 };
 
 // one launch before the expansion: for an operand quantized along K, the row maxima of its block
@@ -1221,14 +1229,14 @@ __global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOpe
     const PrepOperand& p = isA ? pa : pb;
     const int g = isA ? bid : bid - pa.groups;
     if (!p.trans) {
-        const int64_t nkb = p.K / 32;
+        const int64_t nsb = p.nsb;
         const int64_t row = (int64_t)g * 16 + (t >> 4);
         const int part = t & 15;
         int m = -128;
         if (row < p.rows) {
-            const int8_t* sp = p.scales + row * nkb;
+            const int8_t* sp = p.scales + row * nsb;
 #pragma unroll 8
-            for (int64_t kb = part; kb < nkb; kb += 16) m = max(m, (int)sp[kb]);
+            for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, (int)sp[sb]);
         }
 #pragma unroll
         for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
@@ -1241,10 +1249,10 @@ __global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOpe
     const int64_t k0 = (int64_t)slab * PREP_SLAB + (t >> 6) * 64;
     int m = -128;
     if (j < J) {
-        const int8_t* sp = p.scales + j;
+        const int8_t* sp = p.scales + div32((uint32_t)j, p.dgq);
         const int64_t kend = min(k0 + 64, p.K);
 #pragma unroll 8
-        for (int64_t k = k0; k < kend; k++) m = max(m, (int)sp[k * J]);
+        for (int64_t k = k0; k < kend; k++) m = max(m, (int)sp[k * p.nsb]);
     }
     red[t] = m;
     __syncthreads();
@@ -1254,13 +1262,15 @@ __global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOpe
 
 struct ExpandTOperand {
     const uint8_t* codes;    // [K][ld] bytes: codes of a [K][R] tensor quantized along R
-    const int8_t* scales;    // [K][R / 32]
+    const int8_t* scales;    // [K][R / G]
     int64_t rows, tiles, ld; // R, row tiles of 256, bytes per k-row (R, or R / 32 * 28 packed)
     const int* colpart;      // partial column maxima [nslab][tiles * 8]
     int64_t nslab;
     int* rmax;               // row maxima [tiles * 256], written by the first K block's workgroups
     char* planes;
     int fidx;
+    int64_t nsb;             // scales per k-row, R / G
+    Div32 dgq;               // 32-row group j has scale column j / (G / 32)
 };
 
 // expansion of a reused operand: one workgroup per (K block, tile of 256 rows).  The 32 k-rows
@@ -1285,7 +1295,7 @@ __global__ __launch_bounds__(256) void expand_t_kernel(ExpandTOperand opA, Expan
     lut[t] = g_dec[op.fidx][t];
     const int64_t rt = isA ? (int64_t)blockIdx.y : (int64_t)blockIdx.y - opA.tiles;
     const int64_t kb = blockIdx.x;
-    const int64_t R = op.rows, J = R / 32, J8 = op.tiles * 8;
+    const int64_t R = op.rows, J8 = op.tiles * 8;
     const int vrows = (int)min((int64_t)256, R - rt * 256);   // a multiple of 32
     const int vdw = P7 ? vrows / 32 * 7 : vrows / 4;           // valid dwords of a k-row
     const uint8_t* src = op.codes + kb * 32 * op.ld + rt * TB;
@@ -1300,7 +1310,7 @@ __global__ __launch_bounds__(256) void expand_t_kernel(ExpandTOperand opA, Expan
     {
         const int k = t >> 3, j = t & 7;
         int s = -128;
-        if (32 * j < vrows) s = op.scales[(kb * 32 + k) * J + rt * 8 + j];
+        if (32 * j < vrows) s = op.scales[(kb * 32 + k) * op.nsb + div32((uint32_t)(rt * 8 + j), op.dgq)];
         scT[j * 32 + k] = (int8_t)s;
     }
     {
@@ -1356,10 +1366,11 @@ __global__ __launch_bounds__(256) void expand_t_kernel(ExpandTOperand opA, Expan
 
 template <class F>
 hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                         int64_t N, int64_t K, float* c, int64_t ldc, char* ws, int fidx, hipStream_t s) {
+                         int64_t N, int64_t K, int block, float* c, int64_t ldc, char* ws, int fidx, hipStream_t s) {
     hipError_t e = hipSuccess;
     const WsLayout w = ws_layout(M, N, K);
-    const int64_t nkb = K / 32;
+    const int64_t nkb = K / 32, nsb = K / block;
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
     int* maxA = reinterpret_cast<int*>(ws + w.max_a);
     int* maxB = reinterpret_cast<int*>(ws + w.max_b);
     const int64_t tiles = w.rta * w.rtb;
@@ -1367,9 +1378,9 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
     hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
-                       nkb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
-    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx};
-    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx};
+                       nsb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
+    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
+    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
                        dim3(256), 0, s, opA, opB, nkb);
     e = hipGetLastError();
@@ -1385,10 +1396,11 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
 // expansion launches, then gemm_ws_kernel<BIAS2, true>
 template <class F>
 hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                              int64_t N, int64_t K, char* ws, int fidx, int ofmt, uint8_t* qc, int8_t* qs,
+                              int64_t N, int64_t K, int block, char* ws, int fidx, int ofmt, uint8_t* qc, int8_t* qs,
                               hipStream_t s) {
     const WsLayout w = ws_layout(M, N, K);
-    const int64_t nkb = K / 32;
+    const int64_t nkb = K / 32, nsb = K / block;
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
     int* maxA = reinterpret_cast<int*>(ws + w.max_a);
     int* maxB = reinterpret_cast<int*>(ws + w.max_b);
     const int64_t tiles = w.rta * w.rtb;
@@ -1396,9 +1408,9 @@ hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, co
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
     hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
-                       nkb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
-    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx};
-    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx};
+                       nsb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
+    const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
+    const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
                        dim3(256), 0, s, opA, opB, nkb);
     hipError_t e = hipGetLastError();
@@ -1448,10 +1460,12 @@ hipError_t launch_gemm_ws_bias(int bias2, dim3 grid, hipStream_t s, const char* 
 }
 
 hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
-                        int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, char* ws, hipStream_t s) {
+                        int tb, int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc, char* ws,
+                        hipStream_t s) {
     const MixedLayout x = mixed_layout(M, N, K);
     const WsLayout& w = x.w;
     const int64_t nkb = K / 32;
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
     int* maxA = reinterpret_cast<int*>(ws + w.max_a);
     int* maxB = reinterpret_cast<int*>(ws + w.max_b);
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
@@ -1468,6 +1482,8 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
         p.groups = tr ? (int)(p.cgroups * x.nslab) : (int)(RT * 16);
         p.rmax = rmax;
         p.colpart = reinterpret_cast<int*>(ws + colpart);
+        p.nsb = tr ? R / block : K / block;
+        p.dgq = dgq;
         return p;
     };
     const PrepOperand pa = prep_op(as, M, w.rta, ta, maxA, x.colpart_a);
@@ -1479,13 +1495,16 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
 
     // expansions: operands that share a kind (along K, or reused) and a code packing share a launch
     const bool p7a = fa == 2, p7b = fb == 2;
-    const ExpandOperand ka = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fa};
-    const ExpandOperand kbo = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fb};
+    const int64_t nsb = K / block;
+    const ExpandOperand ka = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fa, nsb, dgq};
+    const ExpandOperand kbo = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fb, nsb, dgq};
     auto ld_of = [](int f, int64_t R) { return f == 2 ? R / 32 * 28 : R; };
     const ExpandTOperand xa = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, ld_of(fa, M),
-                               reinterpret_cast<const int*>(ws + x.colpart_a), x.nslab, maxA, ws + w.planes_a, fa};
+                               reinterpret_cast<const int*>(ws + x.colpart_a), x.nslab, maxA, ws + w.planes_a, fa,
+                               M / block, dgq};
     const ExpandTOperand xb = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, ld_of(fb, N),
-                               reinterpret_cast<const int*>(ws + x.colpart_b), x.nslab, maxB, ws + w.planes_b, fb};
+                               reinterpret_cast<const int*>(ws + x.colpart_b), x.nslab, maxB, ws + w.planes_b, fb,
+                               N / block, dgq};
     auto expand_k = [&](const ExpandOperand& o1, const ExpandOperand& o2, bool p7) {
         const dim3 grid((unsigned)(4 * (o1.tiles + o2.tiles)), (unsigned)((nkb + 3) / 4));
         if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb);
@@ -1517,7 +1536,7 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
 
 template <class F, int BN_>
 hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                       int64_t N, int64_t K, float* c, int64_t ldc, int fidx, int splits, hipStream_t s) {
+                       int64_t N, int64_t K, int block, float* c, int64_t ldc, int fidx, int splits, hipStream_t s) {
     using TL = Tile<BN_>;
     // the dynamic-LDS limit is a per-function, per-device attribute: raise it once per device
     static bool attr_set[64] = {};
@@ -1541,7 +1560,7 @@ hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int
     dim3 grid((unsigned)((N + BN_ - 1) / BN_), (unsigned)((M + BM - 1) / BM), (unsigned)splits);
     hipLaunchKernelGGL((gemm_kernel<F, BN_>), grid, dim3(NTHREADS), TL::SMEM, s,
                        reinterpret_cast<const uint8_t*>(a), as, reinterpret_cast<const uint8_t*>(b), bs,
-                       M, N, K, c, ldc, fidx);
+                       M, N, K, c, ldc, fidx, K / block, make_div32((uint32_t)(block / 32)));
     return hipGetLastError();
 }
 
@@ -1550,10 +1569,10 @@ hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int
 // measured 17% slower on 2048 x 4096 x 4096.)
 template <class F>
 hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                      int64_t N, int64_t K, float* c, int64_t ldc, int fidx, hipStream_t s) {
+                      int64_t N, int64_t K, int block, float* c, int64_t ldc, int fidx, hipStream_t s) {
     const int64_t tiles = ((M + BM - 1) / BM) * ((N + 255) / 256);
     const int splits = (tiles < 256 && K / 32 >= 16) ? 2 : 1;
-    return launch_tile<F, 256>(a, as, b, bs, M, N, K, c, ldc, fidx, splits, s);
+    return launch_tile<F, 256>(a, as, b, bs, M, N, K, block, c, ldc, fidx, splits, s);
 }
 
 }  // namespace
@@ -1563,45 +1582,47 @@ int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) { return mixed_layout(M, N, K).bytes; }
 
 hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
-                               int64_t K, int format, int out_format, void* out_codes, int8_t* out_scales, void* ws,
-                               hipStream_t s) {
+                               int64_t K, int format, int block, int out_format, void* out_codes, int8_t* out_scales,
+                               void* ws, hipStream_t s) {
     char* w = reinterpret_cast<char*>(ws);
     uint8_t* qc = reinterpret_cast<uint8_t*>(out_codes);
     switch (format) {
-        case 0: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, w, 0, out_format, qc, out_scales, s);
-        case 1: return launch_requant_fmt<FmtE5C2>(a, as, b, bs, M, N, K, w, 1, out_format, qc, out_scales, s);
-        case 2: return launch_requant_fmt<FmtE3C3>(a, as, b, bs, M, N, K, w, 2, out_format, qc, out_scales, s);
-        case 3: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, w, 3, out_format, qc, out_scales, s);
-        default: return launch_requant_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, w, 4, out_format, qc, out_scales, s);
+        case 0: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 0, out_format, qc, out_scales, s);
+        case 1: return launch_requant_fmt<FmtE5C2>(a, as, b, bs, M, N, K, block, w, 1, out_format, qc, out_scales, s);
+        case 2: return launch_requant_fmt<FmtE3C3>(a, as, b, bs, M, N, K, block, w, 2, out_format, qc, out_scales, s);
+        case 3: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 3, out_format, qc, out_scales, s);
+        default: return launch_requant_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, block, w, 4, out_format, qc, out_scales, s);
     }
 }
 
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
-                             int tb, int64_t M, int64_t N, int64_t K, float* c, int64_t ldc, void* ws, hipStream_t s) {
-    return launch_mixed(a, as, fa, ta, b, bs, fb, tb, M, N, K, c, ldc, reinterpret_cast<char*>(ws), s);
+                             int tb, int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc, void* ws,
+                             hipStream_t s) {
+    return launch_mixed(a, as, fa, ta, b, bs, fb, tb, M, N, K, block, c, ldc, reinterpret_cast<char*>(ws), s);
 }
 
 hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                          int64_t N, int64_t K, int format, float* c, int64_t ldc, void* ws, hipStream_t s) {
+                          int64_t N, int64_t K, int format, int block, float* c, int64_t ldc, void* ws,
+                          hipStream_t s) {
     char* w = reinterpret_cast<char*>(ws);
     switch (format) {
-        case 0: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, w, 0, s);
-        case 1: return launch_ws_fmt<FmtE5C2>(a, as, b, bs, M, N, K, c, ldc, w, 1, s);
-        case 2: return launch_ws_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, w, 2, s);
+        case 0: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, c, ldc, w, 0, s);
+        case 1: return launch_ws_fmt<FmtE5C2>(a, as, b, bs, M, N, K, block, c, ldc, w, 1, s);
+        case 2: return launch_ws_fmt<FmtE3C3>(a, as, b, bs, M, N, K, block, c, ldc, w, 2, s);
         // 2^(8/9) shares E4C3's packing and exponent offset: its kernels, its own table
-        case 3: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, w, 3, s);
-        default: return launch_ws_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, c, ldc, w, 4, s);
+        case 3: return launch_ws_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, c, ldc, w, 3, s);
+        default: return launch_ws_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, block, c, ldc, w, 4, s);
     }
 }
 
 hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                       int64_t N, int64_t K, int format, float* c, int64_t ldc, hipStream_t s) {
+                       int64_t N, int64_t K, int format, int block, float* c, int64_t ldc, hipStream_t s) {
     switch (format) {
-        case 0: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, 0, s);
-        case 1: return launch_fmt<FmtE5C2>(a, as, b, bs, M, N, K, c, ldc, 1, s);
-        case 2: return launch_fmt<FmtE3C3>(a, as, b, bs, M, N, K, c, ldc, 2, s);
-        case 3: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, c, ldc, 3, s);
-        default: return launch_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, c, ldc, 4, s);
+        case 0: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, c, ldc, 0, s);
+        case 1: return launch_fmt<FmtE5C2>(a, as, b, bs, M, N, K, block, c, ldc, 1, s);
+        case 2: return launch_fmt<FmtE3C3>(a, as, b, bs, M, N, K, block, c, ldc, 2, s);
+        case 3: return launch_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, c, ldc, 3, s);
+        default: return launch_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, block, c, ldc, 4, s);
     }
 }
 

@@ -1,6 +1,6 @@
 // CurveFP block quantization Q(X) on gfx950 (Sec. 3.1 of the CurveFP paper).
 //
-// For a block of 32 values with maximum magnitude amax:
+// For a block of G values (G a multiple of 32; 32 by default) with maximum magnitude amax:
 //   scale  a = smallest integer with amax <= 2^a * fl32(L_max)  (ceil-absmax; L_max = r^{n_max/K},
 //          the top level, 2^{n_max/K} with binary radix),
 //          computed on the fp32 bit pattern: a = e(amax) - o_hi + [mant(amax) > mant(fl32(L_max))];
@@ -11,7 +11,11 @@
 //          point a table bucket can hold.  The table encodes the nearest-level rule
 //          (nearest in absolute error, saturating at the endpoints) derived on the host.
 // Memory: HBM-bound; one pass, coalesced 16-byte loads, one byte (or 7 bits)
-// per code and one byte per block written.
+// per code and one byte per block written.  Blocks of 64..512 along rows take their maximum
+// over the G/8 lanes that hold them; every other G first writes the block scales in a pass of
+// their own (the scale rule is monotone in amax, so the scale of a block is that of its
+// largest element), and the quantize pass then reads them.  Codes are laid out per 32
+// elements (E3C3: 28 bytes) whatever G is.
 #include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
@@ -148,19 +152,33 @@ __device__ __forceinline__ void unpack8(const uint4* v, uint32_t* mag, uint32_t*
     }
 }
 
-// quantize one chunk of 8 consecutive elements; four lanes (a quad) hold one block of 32
+// the maximum over the 2^lgl lanes (lgl in 2..6, aligned groups) that hold one block
+__device__ __forceinline__ uint32_t group_max_u32(uint32_t v, int lgl) {
+    v = quad_max_u32(v);
+    for (int o = 4; o < (1 << lgl); o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+    return v;
+}
+
+// quantize one chunk of 8 consecutive elements; 2^lgl consecutive lanes hold one block of
+// 8 * 2^lgl elements (a quad for 32).  lgl < 0: the block scales were written by the scale
+// pass, scale of chunk g at g / (G / 8) (dgl)
 template <class F, bool BF16, bool NTS, class T>
 __device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const T* lut,
                                                uint32_t lmax_mant, uint8_t* __restrict__ codes,
-                                               int8_t* __restrict__ scales) {
+                                               int8_t* __restrict__ scales, int lgl, Div32 dgl) {
     const int part = (int)(g & 3);
     uint32_t mag[8], sgn[8];
     unpack8<BF16>(v, mag, sgn);
-    uint32_t amax = 0;
+    int a;
+    if (lgl >= 0) {
+        uint32_t amax = 0;
 #pragma unroll
-    for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
-    amax = quad_max_u32(amax);
-    const int a = scale_of<F>(amax, lmax_mant);
+        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+        amax = lgl == 2 ? quad_max_u32(amax) : group_max_u32(amax, lgl);
+        a = scale_of<F>(amax, lmax_mant);
+    } else {
+        a = scales[div32(g, dgl)];
+    }
     uint32_t rk[8];
     ranks_of<F>(mag, 8, a, lut, rk);
     uint32_t c[8];
@@ -190,7 +208,7 @@ __device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const
             st4<NTS>(base + 6, (uint32_t)(chunk >> 24));
         }
     }
-    if (part == 0) scales[b] = (int8_t)a;
+    if (lgl >= 0 && (g & ((1u << lgl) - 1)) == 0) scales[g >> lgl] = (int8_t)a;
 }
 
 // blocks along rows: chunk g (8 elements) is chunk g mod cpr of row g / cpr; four consecutive
@@ -199,7 +217,7 @@ __device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const
 template <class F, bool BF16, int U, bool NT, bool NTS>
 __global__ __launch_bounds__(256) void quantize_rows_kernel(
     const void* __restrict__ src, uint32_t nchunks, uint32_t cpr, Div32 dcpr, int64_t ld,
-    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx, int lgl, Div32 dgl) {
     using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
     __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
     constexpr int ESZ = BF16 ? 2 : 4;
@@ -248,7 +266,7 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const uint32_t g = g0 + 256u * u;
-            if (g < nchunks) quantize_chunk<F, BF16, NTS>(v[u], g, lut, lmax_mant, codes, scales);
+            if (g < nchunks) quantize_chunk<F, BF16, NTS>(v[u], g, lut, lmax_mant, codes, scales, lgl, dgl);
         }
         if (!more) break;
 #pragma unroll
@@ -261,11 +279,13 @@ __global__ __launch_bounds__(256) void quantize_rows_kernel(
 
 // quantize-transpose: thread g takes column g mod cols and R consecutive blocks of 32 rows
 // (row group g / cols), so the loads of a wave read one contiguous span of a source row and
-// each thread writes R * 32 contiguous code bytes (R * 28 for E3C3) and R scales
+// each thread writes R * 32 contiguous code bytes (R * 28 for E3C3) and R scales.  given != 0:
+// blocks of G rows whose scales the scale pass wrote, [cols][nsb], 32-row block rb in G-block
+// rb / (G / 32) (dgq)
 template <class F, bool BF16, int R>
 __global__ __launch_bounds__(256) void quantize_cols_kernel(
     const void* __restrict__ src, uint32_t nthreads, uint32_t cols, Div32 dcols, int64_t rows, int64_t ld,
-    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx, int given, int64_t nsb, Div32 dgq) {
     __shared__ uint32_t lut[F::QLUT_SIZE];
     for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
     const uint32_t lmax_mant = g_lmax_mant[fidx];
@@ -288,10 +308,15 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(
             mag[i] = w & 0x7FFFFFFFu;
             sgn[i] = w >> 31;
         }
-        uint32_t amax = 0;
+        int a;
+        if (given) {
+            a = scales[(int64_t)c * nsb + div32((uint32_t)rb, dgq)];
+        } else {
+            uint32_t amax = 0;
 #pragma unroll
-        for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
-        const int a = scale_of<F>(amax, lmax_mant);
+            for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
+            a = scale_of<F>(amax, lmax_mant);
+        }
         uint32_t rk[32];
         ranks_of<F>(mag, 32, a, lut, rk);
         uint32_t cc[32];
@@ -319,13 +344,70 @@ __global__ __launch_bounds__(256) void quantize_cols_kernel(
 #pragma unroll
             for (int d = 0; d < 7; d++) st4<true>(o + d, w[d]);
         }
-        scales[(int64_t)c * rblocks + rb] = (int8_t)a;
+        if (!given) scales[(int64_t)c * rblocks + rb] = (int8_t)a;
+    }
+}
+
+// Scale pass (blocks the quantize kernels cannot reduce in one pass): the ceil-absmax scale of
+// every block of G elements.  Blocks along rows: one wave per block, 16-byte loads.
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void block_scales_rows_kernel(const void* __restrict__ src, int64_t nblocks,
+                                                                int64_t bpr, int64_t ld, int G,
+                                                                int8_t* __restrict__ scales, int fidx) {
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int NV = BF16 ? 1 : 2;   // 16-byte loads per chunk of 8 elements
+    const int64_t blk = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int lane = (int)(threadIdx.x & 63);
+    if (blk >= nblocks) return;        // whole waves
+    const int64_t r = blk / bpr, cb = blk - r * bpr;
+    const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) + (r * ld + cb * G) * ESZ);
+    uint32_t amax = 0;
+#pragma unroll 4
+    for (int c = lane; c < G / 8; c += 64) {
+        uint4 v[NV];
+#pragma unroll
+        for (int t = 0; t < NV; t++) v[t] = ld16<false>(p + NV * c + t);
+        uint32_t mag[8], sgn[8];
+        unpack8<BF16>(v, mag, sgn);
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, o));
+    if (lane == 0) scales[blk] = (int8_t)scale_of<F>(amax, g_lmax_mant[fidx]);
+}
+
+// blocks along columns (quantize-transpose): a workgroup takes 64 columns of one block of G
+// rows, in four row parts; scales [cols][rows / G]
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void block_scales_cols_kernel(const void* __restrict__ src, int64_t rows,
+                                                                int64_t cols, int64_t ld, int G, int64_t ncg,
+                                                                int8_t* __restrict__ scales, int fidx) {
+    __shared__ uint32_t red[256];
+    const int t = (int)threadIdx.x, j = t & 63, part = t >> 6;
+    const int64_t b = (int64_t)blockIdx.x / ncg, cg = (int64_t)blockIdx.x - b * ncg;
+    const int64_t c = cg * 64 + j;
+    uint32_t amax = 0;
+    if (c < cols) {
+#pragma unroll 8
+        for (int i = part; i < G; i += 4) {
+            const int64_t e = (b * G + i) * ld + c;
+            const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[e] << 16)
+                                    : reinterpret_cast<const uint32_t*>(src)[e];
+            amax = max(amax, w & 0x7FFFFFFFu);
+        }
+    }
+    red[t] = amax;
+    __syncthreads();
+    if (t < 64 && c < cols) {
+        const uint32_t m = max(max(red[t], red[t + 64]), max(red[t + 128], red[t + 192]));
+        scales[c * (rows / G) + b] = (int8_t)scale_of<F>(m, g_lmax_mant[fidx]);
     }
 }
 
 template <class F, bool BF16, int U>
 hipError_t launch_rows_u(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
-                         int8_t* scales, hipStream_t s) {
+                         int8_t* scales, int block, int lgl, Div32 dgl, hipStream_t s) {
     const int64_t cpr = cols / 8;
     // 32-bit chunk indices: slabs of at most 2^31 chunks
     const int64_t slab = ((int64_t)1 << 31) / cpr;
@@ -336,9 +418,9 @@ hipError_t launch_rows_u(const void* src, int64_t rows, int64_t cols, int64_t ld
         blocks = blocks < 32768 ? blocks : 32768;
         const void* sp = reinterpret_cast<const char*>(src) + r0 * ld * (BF16 ? 2 : 4);
         uint8_t* cp = codes + (F::PACKED7 ? r0 * (cols / 32) * 28 : r0 * cols);
-        int8_t* scp = scales + r0 * (cols / 32);
+        int8_t* scp = scales + r0 * (cols / block);
         hipLaunchKernelGGL((quantize_rows_kernel<F, BF16, U, true, true>), dim3(blocks), dim3(256), 0, s, sp,
-                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, cp, scp, fidx);
+                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, cp, scp, fidx, lgl, dgl);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -347,15 +429,27 @@ hipError_t launch_rows_u(const void* src, int64_t rows, int64_t cols, int64_t ld
 
 // Streams of at least 2048 workgroups at 128 (bf16) or 64 (fp32) bytes in flight per thread use
 // that depth (the shape that measured fastest on a 1 GiB stream); smaller tensors use 32 bytes
-// per thread, so that they still spread over every compute unit.
+// per thread, so that they still spread over every compute unit.  Blocks of 32..512 (a power of
+// two) are reduced over their lanes; any other block size runs the scale pass first.
 template <class F, bool BF16>
 hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
-                       int8_t* scales, hipStream_t s) {
+                       int8_t* scales, int block, hipStream_t s) {
     constexpr int UBIG = BF16 ? 8 : 2;
+    int lgl = -1;
+    if (block <= 512 && (block & (block - 1)) == 0)
+        for (lgl = 0; (8 << lgl) < block; lgl++) {}
+    const Div32 dgl = make_div32((uint32_t)(block / 8));
+    if (lgl < 0) {
+        const int64_t nb = rows * (cols / block);
+        hipLaunchKernelGGL((block_scales_rows_kernel<F, BF16>), dim3((unsigned)((nb + 3) / 4)), dim3(256), 0, s, src,
+                           nb, cols / block, ld, block, scales, fidx);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
     const int64_t nchunks = rows * (cols / 8);
     if (nchunks >= (int64_t)2048 * 256 * UBIG)
-        return launch_rows_u<F, BF16, UBIG>(src, rows, cols, ld, fidx, codes, scales, s);
-    return launch_rows_u<F, BF16, BF16 ? 2 : 1>(src, rows, cols, ld, fidx, codes, scales, s);
+        return launch_rows_u<F, BF16, UBIG>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
+    return launch_rows_u<F, BF16, BF16 ? 2 : 1>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
 }
 
 // quantize-transpose through LDS: a workgroup takes 128 rows (four blocks) x 64 columns.  The
@@ -369,7 +463,7 @@ constexpr int TT_OUT_STRIDE = 144;   // 128 code bytes + 16: the 16-byte writes 
 template <class F, bool BF16>
 __global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
     const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld,
-    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx, int given, int64_t nsb, Div32 dgq) {
     using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
     constexpr int ESZ = BF16 ? 2 : 4;
     constexpr int SEG = TT_COLS * ESZ / 16;            // 16-byte pieces per tile row
@@ -414,10 +508,15 @@ __global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
         mag[i] = w & 0x7FFFFFFFu;
         sgn[i] = w >> 31;
     }
-    uint32_t amax = 0;
+    int a = 0;
+    if (given) {
+        if (c0 + j < cols) a = scales[(c0 + j) * nsb + div32((uint32_t)(r0 / 32 + b), dgq)];
+    } else {
+        uint32_t amax = 0;
 #pragma unroll
-    for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
-    const int a = scale_of<F>(amax, lmax_mant);
+        for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
+        a = scale_of<F>(amax, lmax_mant);
+    }
     uint32_t rk[32];
     ranks_of<F>(mag, 32, a, lut, rk);
     uint32_t cc[32];
@@ -464,7 +563,7 @@ __global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
             }
         }
     }
-    {
+    if (!given) {
         const int jj = tid >> 2, bb = tid & 3;
         if (c0 + jj < cols) scales[(c0 + jj) * rblocks + r0 / 32 + bb] = scl[jj * 4 + bb];
     }
@@ -472,7 +571,9 @@ __global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
 
 template <class F, int R>
 hipError_t launch_cols(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int fidx,
-                       uint8_t* codes, int8_t* scales, hipStream_t s) {
+                       uint8_t* codes, int8_t* scales, int block, hipStream_t s) {
+    const int given = block > 32;
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
     // column slabs keep the thread count of one launch below 2^31
     const int64_t groups = rows / (32 * R);
     const int64_t slab = ((int64_t)1 << 31) / groups;
@@ -483,13 +584,15 @@ hipError_t launch_cols(const void* src, int dtype, int64_t rows, int64_t cols, i
         const int64_t esz = dtype == 1 ? 2 : 4;
         const void* sp = reinterpret_cast<const char*>(src) + c0 * esz;
         uint8_t* cp = codes + (F::PACKED7 ? c0 * (rows / 32) * 28 : c0 * rows);
-        int8_t* scp = scales + c0 * (rows / 32);
+        int8_t* scp = scales + c0 * (rows / block);
         if (dtype == 1)
             hipLaunchKernelGGL((quantize_cols_kernel<F, true, R>), dim3((unsigned)blocks), dim3(256), 0, s, sp,
-                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx);
+                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx,
+                               given, rows / block, dgq);
         else
             hipLaunchKernelGGL((quantize_cols_kernel<F, false, R>), dim3((unsigned)blocks), dim3(256), 0, s, sp,
-                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx);
+                               (uint32_t)nthreads, (uint32_t)nc, make_div32((uint32_t)nc), rows, ld, cp, scp, fidx,
+                               given, rows / block, dgq);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
@@ -498,11 +601,26 @@ hipError_t launch_cols(const void* src, int dtype, int64_t rows, int64_t cols, i
 
 template <class F>
 hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
-                      int fidx, void* codes, int8_t* scales, hipStream_t s) {
+                      int fidx, int block, void* codes, int8_t* scales, hipStream_t s) {
     uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
     if (axis == 1) {
-        return dtype == 1 ? launch_rows<F, true>(src, rows, cols, ld, fidx, cp, scales, s)
-                          : launch_rows<F, false>(src, rows, cols, ld, fidx, cp, scales, s);
+        return dtype == 1 ? launch_rows<F, true>(src, rows, cols, ld, fidx, cp, scales, block, s)
+                          : launch_rows<F, false>(src, rows, cols, ld, fidx, cp, scales, block, s);
+    }
+    // blocks of more than 32 rows: scale pass, then the quantize-transpose reads the scales
+    const int given = block > 32;
+    const Div32 dgq = make_div32((uint32_t)(block / 32));
+    if (given) {
+        const int64_t ncg = (cols + 63) / 64;
+        const dim3 grid((unsigned)(ncg * (rows / block)));
+        if (dtype == 1)
+            hipLaunchKernelGGL((block_scales_cols_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, block,
+                               ncg, scales, fidx);
+        else
+            hipLaunchKernelGGL((block_scales_cols_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, block,
+                               ncg, scales, fidx);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
     }
     const int64_t esz = dtype == 1 ? 2 : 4;
     const bool tiled = rows % TT_ROWS == 0 && cols % 8 == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
@@ -510,12 +628,14 @@ hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, in
     if (tiled) {
         const dim3 grid((unsigned)((cols + TT_COLS - 1) / TT_COLS), (unsigned)(rows / TT_ROWS));
         if (dtype == 1)
-            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, cp, scales, fidx);
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, cp,
+                               scales, fidx, given, rows / block, dgq);
         else
-            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, cp, scales, fidx);
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, cp,
+                               scales, fidx, given, rows / block, dgq);
         return hipGetLastError();
     }
-    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, s);
+    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, block, s);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -706,13 +826,13 @@ hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols
 }  // namespace
 
 hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
-                           int axis, int format, void* codes, int8_t* scales, hipStream_t s) {
+                           int axis, int format, int block, void* codes, int8_t* scales, hipStream_t s) {
     switch (format) {
-        case 0: return launch_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, 0, codes, scales, s);
-        case 1: return launch_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, 1, codes, scales, s);
-        case 2: return launch_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, codes, scales, s);
-        case 3: return launch_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, 3, codes, scales, s);
-        default: return launch_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, 4, codes, scales, s);
+        case 0: return launch_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, 0, block, codes, scales, s);
+        case 1: return launch_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, 1, block, codes, scales, s);
+        case 2: return launch_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, block, codes, scales, s);
+        case 3: return launch_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, 3, block, codes, scales, s);
+        default: return launch_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, 4, block, codes, scales, s);
     }
 }
 

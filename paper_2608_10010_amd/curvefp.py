@@ -129,8 +129,9 @@ def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 3
                      stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Q(X) of a 2-D fp32/bf16 device tensor (row stride may exceed its width).
 
-    block_axis=1: codes [rows, cols] (E3C3: [rows, cols/32, 28] bytes), scales [rows, cols/32].
-    block_axis=0: quantize-transpose, codes [cols, rows], scales [cols, rows/32].
+    block_axis=1: codes [rows, cols] (E3C3: [rows, cols/32, 28] bytes), scales [rows, cols/block].
+    block_axis=0: quantize-transpose, codes [cols, rows], scales [cols, rows/block].
+    block: elements per scale, a multiple of 32 dividing the blocked extent.
     """
     assert src.dim() == 2 and src.stride(1) == 1
     rows, cols = src.shape

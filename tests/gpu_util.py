@@ -47,11 +47,11 @@ def unpack_dev_codes(codes: torch.Tensor, fmt: str, k: int) -> np.ndarray:
     return c
 
 
-def exact_values(codes: np.ndarray, scales: np.ndarray, fmt: str) -> np.ndarray:
+def exact_values(codes: np.ndarray, scales: np.ndarray, fmt: str, block: int = 32) -> np.ndarray:
     """float64 reconstructed values 2^{a + n/K} (the oracle's level function)."""
     f = oracle.get_format(fmt)
     nz, s, n = oracle.code_fields(codes, f)
-    a = np.repeat(scales.astype(np.int64), 32, axis=1)
+    a = np.repeat(scales.astype(np.int64), block, axis=1)
     a = np.where(a == oracle.POISON_SCALE, 0, a)
     v = np.ldexp(oracle.level_value_f64(f, np.where(nz, n, 0)), a)
     return np.where(nz, np.where(s == 1, -v, v), 0.0)
@@ -71,7 +71,7 @@ def row_tops(codes, scales, fmt):
     return np.ldexp(1.0, alpha + e_max + 1)
 
 
-def gemm_tolerance(ca, sa, cb, sb, fmt):
+def gemm_tolerance(ca, sa, cb, sb, fmt, block: int = 32):
     """Element-wise bound for the MFMA GEMM against the exact sum.
 
     * 1e-5 sum_k |a_ik b_jk| covers the 22-bit fp16 high/low operand splits
@@ -81,7 +81,7 @@ def gemm_tolerance(ca, sa, cb, sb, fmt):
       scale range top = 2^{alpha + e_max + 1} (absolute error <= 2^-40 top);
     * 2^-148 covers an exact result that underflows fp32.
     """
-    va, vb = np.abs(exact_values(ca, sa, fmt)), np.abs(exact_values(cb, sb, fmt))
+    va, vb = np.abs(exact_values(ca, sa, fmt, block)), np.abs(exact_values(cb, sb, fmt, block))
     S = va @ vb.T
     ta, tb = row_tops(ca, sa, fmt), row_tops(cb, sb, fmt)
     flush = ta[:, None] * vb.sum(1)[None, :] + va.sum(1)[:, None] * tb[None, :]

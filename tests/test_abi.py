@@ -99,7 +99,17 @@ def test_sizes(L):
     assert L.curvefp_codes_bytes(5, 10, 64, 32) == EFMT
     assert cf.curvefp_codes_bytes("E4C3_r3/4", 10, 64) == 640
     assert L.curvefp_scales_count(10, 48, 32) == ESHAPE
-    assert L.curvefp_scales_count(10, 64, 64) == EBLOCK
+    # blocks of G = any positive multiple of 32 (Eq. effective-rate's G); the extent a multiple of G
+    assert L.curvefp_scales_count(10, 64, 64) == 10
+    assert L.curvefp_scales_count(10, 1024, 512) == 20
+    assert L.curvefp_scales_count(10, 288, 96) == 30
+    assert L.curvefp_scales_count(10, 4096, 4096) == 10          # rowwise
+    assert L.curvefp_scales_count(10, 96, 64) == ESHAPE
+    for bad in (0, 16, 48, -32):
+        assert L.curvefp_scales_count(10, 96, bad) == EBLOCK, bad
+        assert L.curvefp_codes_bytes(0, 10, 96, bad) == EBLOCK, bad
+    assert L.curvefp_codes_bytes(2, 10, 512, 512) == 10 * 16 * 28   # codes stay per group of 32
+    assert L.curvefp_codes_bytes(0, 10, 96, 64) == ESHAPE
 
 
 def test_status_strings(L):
@@ -120,7 +130,10 @@ def test_quantize_validation(L):
     assert q(FAKE, 2, 4, 32, 32, 1, 0, 32, FAKE, FAKE, None) == EFMT       # dtype
     assert q(FAKE, 0, 4, 32, 32, 1, 7, 32, FAKE, FAKE, None) == EFMT       # format
     assert q(FAKE, 0, 4, 32, 32, 1, 5, 32, FAKE, FAKE, None) == EFMT
-    assert q(FAKE, 0, 4, 32, 32, 1, 0, 64, FAKE, FAKE, None) == EBLOCK     # block
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 48, FAKE, FAKE, None) == EBLOCK     # block not a multiple of 32
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 0, FAKE, FAKE, None) == EBLOCK
+    assert q(FAKE, 0, 4, 32, 32, 1, 0, 64, FAKE, FAKE, None) == ESHAPE     # cols % block
+    assert q(FAKE, 0, 32, 64, 64, 0, 0, 64, FAKE, FAKE, None) == ESHAPE    # rows % block on axis 0
     assert q(FAKE, 0, 4, 32, 32, 2, 0, 32, FAKE, FAKE, None) == EBLOCK     # axis
     assert q(FAKE, 0, 0, 32, 32, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # rows
     assert q(FAKE, 0, 4, 40, 40, 1, 0, 32, FAKE, FAKE, None) == ESHAPE     # cols % 32
@@ -139,7 +152,9 @@ def test_dequantize_validation(L):
     assert d(FAKE, FAKE, 0, 4, 32, 32, None, 32, None) == ENULL
     assert d(FAKE, FAKE, 5, 4, 32, 32, FAKE, 32, None) == EFMT
     assert d(FAKE, FAKE, 0, 4, 32, 16, FAKE, 32, None) == EBLOCK
+    assert d(FAKE, FAKE, 0, 4, 32, 80, FAKE, 32, None) == EBLOCK
     assert d(FAKE, FAKE, 0, 4, 48, 32, FAKE, 48, None) == ESHAPE
+    assert d(FAKE, FAKE, 0, 4, 96, 64, FAKE, 96, None) == ESHAPE
     assert d(FAKE, FAKE, 0, 4, 32, 32, FAKE, 16, None) == ESHAPE
     assert d(FAKE, FAKE, 0, -1, 32, 32, FAKE, 32, None) == ESHAPE
     assert d(FAKE, FAKE, 0, 4, 32, 32, MIS, 32, None) == EALIGN
@@ -157,6 +172,8 @@ def test_gemm_validation(L):
     assert g(*bad) == EFMT
     bad = list(args); bad[8] = 16
     assert g(*bad) == EBLOCK
+    bad = list(args); bad[8] = 128                   # K % block
+    assert g(*bad) == ESHAPE
     for i, v in ((4, 0), (5, -3), (6, 0), (6, 48), (10, 32)):
         bad = list(args); bad[i] = v
         assert g(*bad) == ESHAPE, (i, v)
@@ -209,9 +226,15 @@ def test_gemm_mixed_validation(L):
     for i, v in ((2, 5), (6, -1)):
         bad = list(args); bad[i] = v
         assert g(*bad) == EFMT, (i, v)
-    for i, v in ((3, 2), (7, -1), (11, 16)):
+    for i, v in ((3, 2), (7, -1), (11, 16), (11, 40)):
         bad = list(args); bad[i] = v
         assert g(*bad) == EBLOCK, (i, v)
+    # K % block for an operand quantized along K; R % block for a reused one
+    bad = list(args); bad[11] = 128
+    assert g(*bad) == ESHAPE
+    bad = list(args); bad[3] = 1; bad[7] = 1; bad[8] = 96; bad[11] = 64; bad[10] = 128
+    bad[15] = L.curvefp_gemm_mixed_workspace_bytes(96, 64, 128)
+    assert g(*bad) == ESHAPE                          # M = 96 rows of a reused A, blocks of 64
     for i, v in ((8, 0), (9, -1), (10, 48), (13, 32), (15, need - 1)):
         bad = list(args); bad[i] = v
         assert g(*bad) == ESHAPE, (i, v)
@@ -266,8 +289,10 @@ def test_gemm_requant_validation(L):
     for i, v in ((7, 5), (9, 5), (9, -1)):
         a = list(args); a[i] = v
         assert g(*a) == EFMT, (i, v)
-    a = list(args); a[8] = 64
+    a = list(args); a[8] = 48
     assert g(*a) == EBLOCK
+    a = list(args); a[8] = 128                       # the inputs' K % block
+    assert g(*a) == ESHAPE
     for i, v in ((4, 0), (5, 40), (6, 48), (13, need - 1)):
         a = list(args); a[i] = v
         assert g(*a) == ESHAPE, (i, v)

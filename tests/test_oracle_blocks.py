@@ -1,0 +1,155 @@
+"""Oracle pins for block sizes G other than 32 (Eq. effective-rate's G; Sec. 3.1 evaluates
+fixed-size blocks and rowwise sharing, Sec. 4.2 uses G64 and G512).
+
+Each block of G consecutive elements gets one ceil-absmax scale and every element the nearest
+level at that scale.  These tests hold the oracle to that definition through facts that do
+not come from its own code:
+  * the scale rule is monotone in the block maximum, so a block's scale is the largest of the
+    scales its groups of 32 get alone (all-zero groups aside: their scale is 0 by convention);
+  * every code is the nearest level at the block scale, decided by the rigorous integer
+    brackets of tests/exact_ref.py;
+  * the exact GEMM over blocks of G equals numpy's float64 product of the dequantized operands
+    within fp64 rounding, and equals the exact GEMM at G = 32 with each scale repeated.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from tests import exact_ref
+
+NAMES = list(oracle.FORMATS)
+BLOCKS = [64, 128, 256, 512, 96, 160]
+
+
+def sample_input(rng, rows, cols):
+    """Groups of 32 with magnitudes spread over 2^-20 .. 2^20, some groups all zero."""
+    x = rng.standard_normal((rows, cols)) * np.exp2(rng.uniform(-20, 20, (rows, cols // 32, 1))).repeat(32, 1).reshape(
+        rows, cols // 32, 32).reshape(rows, cols)
+    zero = rng.random((rows, cols // 32)) < 0.15
+    x = np.where(np.repeat(zero, 32, axis=1), 0.0, x)
+    return x.astype(np.float32)
+
+
+def rigorous_code(x: float, a: int, f) -> int:
+    """Code of the nearest element of {0} U {2^(a + p n / (qK))} to x (exact_ref brackets)."""
+    if x == 0:
+        return 0
+    m, e = math.frexp(abs(x))            # |x| = m 2^e, m in [0.5, 1)
+    M = int(m * (1 << 24))               # exact: fp32 has 24 significand bits
+    n = exact_ref.nearest_level(M, e - 1 - a, f.E, f.C, f.p, f.q)
+    if n is None:
+        return 0
+    return ((1 if x < 0 else 0) << (f.E + f.C)) | (n + f.B)
+
+
+@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("G", BLOCKS + ["row"])
+def test_block_scale_is_largest_group_scale(name, G):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(40 + len(name))
+    cols = 960
+    G = cols if G == "row" else G
+    if cols % G:
+        cols = 2 * G * 3
+    x = sample_input(rng, 12, cols)
+    _, sg = oracle.quantize(x, f, G)
+    _, s32 = oracle.quantize(x, f, 32)
+    groups = np.abs(x).reshape(12, cols // 32, 32).max(-1) > 0
+    s32 = np.where(groups, s32.astype(np.int64), -1000).reshape(12, cols // G, G // 32)
+    expect = s32.max(-1)
+    expect = np.where(expect == -1000, 0, expect)
+    assert sg.shape == (12, cols // G)
+    assert np.array_equal(sg.astype(np.int64), expect)
+
+
+@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("G", [64, 512, 96])
+def test_block_codes_are_nearest_at_block_scale(name, G):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(7 + G)
+    cols = 2 * G * 3 if G == 96 else 2 * G
+    x = sample_input(rng, 4, cols)
+    codes, scales = oracle.quantize(x, f, G)
+    a = np.repeat(scales.astype(np.int64), G, axis=1)
+    idx = rng.choice(x.size, 400, replace=False)
+    for i in idx:
+        r, c = divmod(int(i), cols)
+        assert int(codes[r, c]) == rigorous_code(float(x[r, c]), int(a[r, c]), f), (r, c, float(x[r, c]))
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_block_round_trip(name):
+    """Quantizing the reconstruction of blocks of G: the largest element's level lies in the top
+    octave of the block's range or one octave lower, so the scale stays or drops by one (it can
+    drop when that level is a whole octave below the top: its value is at most
+    2^(a-1) fl32(L_max)); blocks that keep their scale give back their codes."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(3)
+    for G in (64, 256, 512):
+        x = sample_input(rng, 6, 1024)
+        c, s = oracle.quantize(x, f, G)
+        xh = oracle.dequantize(c, s, f, G)
+        c2, s2 = oracle.quantize(xh, f, G)
+        d = s.astype(np.int64) - s2.astype(np.int64)
+        assert set(np.unique(d)) <= {0, 1}, G
+        keep = np.repeat(d == 0, G, axis=1)
+        assert np.array_equal(np.where(keep, c, 0), np.where(keep, c2, 0)), G
+        assert (d == 0).mean() > 0.5, G
+
+
+def test_block_nonfinite_poisons_the_whole_block():
+    f = oracle.get_format("E4C3")
+    x = np.ones((2, 256), np.float32)
+    x[0, 200] = np.inf
+    codes, scales = oracle.quantize(x, f, 128)
+    assert scales[0, 1] == oracle.POISON_SCALE and not codes[0, 128:].any()
+    assert scales[0, 0] != oracle.POISON_SCALE and scales[1].tolist() == [scales[0, 0]] * 2
+
+
+@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("G", [64, 256, 96])
+def test_gemm_over_blocks_of_g(name, G):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(50 + G)
+    K = 3 * G if G == 96 else 2 * G
+    A = sample_input(rng, 9, K)
+    B = sample_input(rng, 7, K)
+    ca, sa = oracle.quantize(A, f, G)
+    cb, sb = oracle.quantize(B, f, G)
+    V = oracle.gemm_exact(ca, sa, cb, sb, f, block=G)
+    # the same products at G = 32 with each block scale repeated: the exact sums agree exactly
+    r = G // 32
+    V32 = oracle.gemm_exact(ca, np.repeat(sa, r, axis=1), cb, np.repeat(sb, r, axis=1), f, block=32)
+    assert np.array_equal(V, V32)
+    # and numpy's float64 product of the reconstructions, within fp64 rounding
+    da = oracle.dequantize(ca, sa, f, G).astype(np.float64)
+    db = oracle.dequantize(cb, sb, f, G).astype(np.float64)
+    # fp32 reconstruction differs from the exact level by at most 2^-24 relative per operand
+    ref = da @ db.T
+    bound = (2.0 ** -22 + K * 2.0 ** -52) * (np.abs(da) @ np.abs(db).T) + 2.0 ** -140
+    assert np.all(np.abs(V - ref) <= bound)
+
+
+@pytest.mark.parametrize("pair", [("E5C2", "E4C3"), ("E4C3_r3/4", "E4C3_r8/9")], ids=lambda p: f"{p[0]}x{p[1]}")
+def test_mixed_gemm_with_reused_operand_in_blocks_of_g(pair):
+    """The backward recipe with blocks of 64: A quantized along K, B a reused [K][N] operand whose
+    blocks of 64 run along N; per-element scales expand both."""
+    fa, fb = (oracle.get_format(n) for n in pair)
+    rng = np.random.default_rng(61)
+    G, M, N, K = 64, 5, 128, 128
+    A = sample_input(rng, M, K)
+    Bt = sample_input(rng, K, N)                  # [K][N], quantized along N
+    ca, sa = oracle.quantize(A, fa, G)
+    cbt, sbt = oracle.quantize(Bt, fb, G)
+    ea = oracle.expand_scales(sa, G, axis=1)
+    eb = oracle.expand_scales(sbt, G, axis=0)     # [N][K]
+    cb = np.ascontiguousarray(cbt.T)
+    V = oracle.gemm_exact_mixed(ca, ea, fa, cb, eb, fb)
+    da = oracle.dequantize(ca, sa, fa, G).astype(np.float64)
+    db = oracle.dequantize(cbt, sbt, fb, G).astype(np.float64).T
+    ref = da @ db.T
+    bound = (2.0 ** -22 + K * 2.0 ** -52) * (np.abs(da) @ np.abs(db).T) + 2.0 ** -140
+    assert np.all(np.abs(V - ref) <= bound)
