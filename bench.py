@@ -20,8 +20,9 @@ times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
 `backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
 workload as `cpu_baseline`.  `radix_variants` times the inference operands in
 E4C3 with the three radices of the paper's radix experiment, `static_scales`
-the inference weight quantized with reconstruction-MSE scale search, and
-`requant` the inference GEMM with its output requantized in the epilogue.
+the inference weight quantized with reconstruction-MSE scale search,
+`requant` the inference GEMM with its output requantized in the epilogue, and
+`block_sizes` the inference workload with one scale per 32, 64, 512 or K elements.
 """
 
 import argparse
@@ -55,6 +56,8 @@ def parse():
                    help="skip the mixed-format backward GEMMs (E5C2 gradients x reused E4C3 codes)")
     p.add_argument("--no-requant", action="store_true",
                    help="skip the GEMM with output requantization (fused epilogue vs GEMM + quantize)")
+    p.add_argument("--no-blocks", action="store_true",
+                   help="skip the block-size sweep (G = 32, 64, 512, K) of the inference workload")
     p.add_argument("--no-static", action="store_true",
                    help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
@@ -149,6 +152,7 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
     run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
+           f"--no-blocks "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -493,6 +497,60 @@ def static_scales(cf, w, tb, dev, stream, reps: int = 10):
     return out
 
 
+def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 10):
+    """The inference workload with one scale per G elements (Eq. effective-rate; Sec. 4.2's G64
+    and G512, and rowwise G = K): per G the median of `reps` individually timed calls of
+    quantize(act), quantize(weight) and curvefp_gemm_ws.  Quantize bytes are the algorithmic
+    source + codes + one scale byte per G elements; G = 4096 runs the scale pass first and reads
+    the source twice."""
+    import numpy as np
+    import torch
+
+    out = {}
+    C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+    ws = cf.gemm_workspace(w.M, w.N, w.K, dev)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return float(np.median(ts))
+
+    for G in (32, 64, 512, w.K):
+        ca, sa = cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, block=G)
+        cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, block=G)
+        per_elem = quantize_bytes_per_elem(w.fmt, w.dtype) - 1.0 / 32.0 + 1.0 / G
+        t_a = timed(lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, block=G, codes=ca, scales=sa))
+        t_b = timed(lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, block=G, codes=cb, scales=sb))
+        t_g = timed(lambda: cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, block=G, c=C, workspace=ws))
+        out[f"G{G}"] = {"quantize_act_gbps": w.M * w.K * per_elem / t_a / 1e9,
+                        "quantize_weight_gbps": w.N * w.K * per_elem / t_b / 1e9,
+                        "gemm_us": t_g * 1e6, "gemm_tflops": w.flops() / t_g / 1e12,
+                        "bits_per_value_int8_scales": (7.0 if w.fmt == "E3C3" else 8.0) + 8.0 / G}
+    # S-bit scale exponents at G64 (Sec. 4.2: S = 5 for activations, 4 for weights), same codes
+    # layout; bytes: source + codes + S/G bits of offset per element + one reference byte per row
+    for which, t, rows, S in (("act", ta, w.M, 5), ("weight", tb, w.N, 4)):
+        G = 64
+        cc, rr, oo = cf.curvefp_quantize_compact(t, w.fmt, G, S)
+        per_elem = quantize_bytes_per_elem(w.fmt, w.dtype) - 1.0 / 32.0 + S / 8.0 / G
+        tq = timed(lambda: cf.curvefp_quantize_compact(t, w.fmt, G, S, codes=cc, row_ref=rr, offsets=oo))
+        out[f"compact_G{G}_S{S}_{which}"] = {
+            "quantize_gbps": (rows * w.K * per_elem + rows) / tq / 1e9, "us": tq * 1e6,
+            "bits_per_value": (7.0 if w.fmt == "E3C3" else 8.0) + S / G}
+    out["workload"] = (f"{w.name}: act {w.M}x{w.K}, weight {w.N}x{w.K} {w.dtype} -> {w.fmt}, G = 32, 64, 512, K; "
+                       f"S-bit scales at G64 (S = 5 act, 4 weight)")
+    out["timing"] = f"median of {reps} individually timed calls each"
+    return out
+
+
 def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 10):
     """The inference workload's operands quantized and multiplied in E4C3 with the radices of
     Tab. radix-frontier (r = 2: 8 phases; 2^(8/9): 9; 2^(3/4): 32): per format the median of
@@ -727,6 +785,9 @@ def main():
 
     if not args.no_radix:
         result["radix_variants"] = radix_variants(cf, w, ta, tb, dev, stream)
+
+    if not args.no_blocks:
+        result["block_sizes"] = block_sizes(cf, w, ta, tb, dev, stream)
 
     if not args.no_backward:
         result["backward_mixed"] = backward_mixed(cf, W, dev, stream)

@@ -144,6 +144,37 @@ int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols,
                          void* codes, int8_t* scales, void* stream);
 
 /*
+ * Block quantization with S-bit scale exponents (Eq. effective-rate, R = 1 + E + C + S/G bits
+ * per value; Sec. 4.2 prices E3C3 weights at S = 4 and activations at S = 5), blocks of G along
+ * the rows of src.  The paper gives only the width; the layout taken here: each row keeps one
+ * int8 reference e_r, the largest ceil-absmax scale among its blocks that are finite and not all
+ * zero (0 if there is none), and each block an unsigned S-bit offset d = e_r - a', where
+ * a' = max(a_b, e_r - (2^S - 2)) and a_b is the block's ceil-absmax scale: a block whose scale
+ * lies more than 2^S - 2 below the reference is quantized at the raised scale a' (its smallest
+ * values lose resolution, none saturates).  d = 2^S - 1 marks a block that held a NaN or an
+ * infinity (its codes are zero); an all-zero block has d = 0.  Codes are curvefp_quantize's at
+ * the scales a' (identical to curvefp_quantize's codes wherever no block is raised).
+ *   codes    [rows][cols] bytes (E3C3: [rows][cols/32][28]), 16-byte aligned;
+ *   row_ref  [rows] int8;
+ *   offsets  [rows][curvefp_compact_offsets_bytes(1, cols, block, scale_bits)] bytes: offset j of
+ *            a row at bits [S j, S j + S) of a little-endian bit string, rows padded to bytes.
+ * scale_bits in [2, 8] and block a multiple of 32 (CURVEFP_ERR_BLOCK otherwise); cols % block
+ * == 0 and cols <= 131072 (CURVEFP_ERR_SHAPE otherwise); src and rows 16-byte aligned.
+ */
+int64_t curvefp_compact_offsets_bytes(int64_t rows, int64_t cols, int block, int scale_bits);
+int curvefp_quantize_compact(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                             int format, int block, int scale_bits, void* codes, int8_t* row_ref,
+                             uint8_t* offsets, void* stream);
+
+/*
+ * int8 block scales [rows][nblocks] from curvefp_quantize_compact's row references and packed
+ * offsets: e_r - d, or -128 for the marker 2^S - 1.  With them, every entry point that takes
+ * scales (dequantize, the GEMMs) consumes S-bit-scaled operands with block = G.
+ */
+int curvefp_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t rows, int64_t nblocks,
+                          int scale_bits, int8_t* scales, void* stream);
+
+/*
  * Reconstruction x_hat = (-1)^s 2^{a_b} 2^{n/K} (Eq. curvefp-value), written as
  * the nearest fp32 value (ties to even).  codes/scales as produced by
  * curvefp_quantize with block_axis = 1 for an [outer][k] tensor;

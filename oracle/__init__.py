@@ -36,6 +36,10 @@ from .quant import (
     level_value_f64,
     pack7,
     unpack7,
+    quantize_compact,
+    compact_scales,
+    pack_offsets,
+    unpack_offsets,
     POISON_SCALE,
 )
 from .gemm import (

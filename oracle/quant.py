@@ -280,3 +280,64 @@ def unpack7(packed: np.ndarray, k: int) -> np.ndarray:
     bits = np.unpackbits(packed, axis=-1, bitorder="little").reshape(outer, k // 32, 32, 7)
     weights = (1 << np.arange(7)).astype(np.uint16)
     return (bits.astype(np.uint16) * weights).sum(-1).reshape(outer, k).astype(np.uint8)
+
+
+# ---------------------------------------------------------------- S-bit scale exponents
+
+def quantize_compact(x: np.ndarray, fmt: Format, block: int, scale_bits: int):
+    """Block quantization with S-bit scale exponents (Eq. effective-rate: R = 1 + E + C + S/G;
+    Sec. 4.2 prices weights at S = 4 and activations at S = 5).  The paper gives only the bit
+    count; the reading taken here (blocks along the rows of x):
+
+    * each row keeps one int8 reference e_r: the largest ceil-absmax scale among its blocks that
+      are finite and not all zero (0 when it has none);
+    * each block keeps an unsigned S-bit offset d_b = e_r - a'_b, a'_b = max(a_b, e_r - W),
+      W = 2^S - 2: a block whose own scale lies more than W below the reference is quantized at
+      the raised scale a'_b (its smallest values lose resolution; nothing saturates);
+    * the offset 2^S - 1 marks a block that held a NaN or an infinity (all-zero codes); an
+      all-zero block has offset 0.
+
+    Returns (codes uint8 [rows, cols], row_ref int8 [rows], offsets int64 [rows, cols // block]).
+    """
+    x = np.asarray(x)
+    assert x.dtype == np.float32 and x.ndim == 2 and 2 <= scale_bits <= 8
+    rows, cols = x.shape
+    assert cols % block == 0
+    nb = cols // block
+    _, a = quantize(x, fmt, block)
+    a = a.astype(np.int64)
+    xb = x.astype(np.float64).reshape(rows, nb, block)
+    finite = a != POISON_SCALE
+    with np.errstate(invalid="ignore"):
+        live = finite & np.any(np.where(np.isfinite(xb), xb, 0.0) != 0, axis=-1)
+    ref = np.where(live.any(axis=1), np.max(np.where(live, a, SCALE_MIN - 1), axis=1), 0)
+    window = (1 << scale_bits) - 2
+    a_eff = np.where(live, np.maximum(a, ref[:, None] - window), ref[:, None])
+    codes = np.where(live[..., None], _codes_at_scale(np.where(live[..., None], xb, 0.0), a_eff, fmt), 0)
+    offsets = np.where(finite, ref[:, None] - a_eff, (1 << scale_bits) - 1)
+    return codes.reshape(rows, cols).astype(np.uint8), ref.astype(np.int8), offsets
+
+
+def compact_scales(row_ref: np.ndarray, offsets: np.ndarray, scale_bits: int) -> np.ndarray:
+    """int8 block scales [rows, nb] of S-bit offsets: e_r - d_b, or -128 for the marker 2^S - 1."""
+    ref = np.asarray(row_ref).astype(np.int64)[:, None]
+    d = np.asarray(offsets).astype(np.int64)
+    return np.where(d == (1 << scale_bits) - 1, POISON_SCALE, ref - d).astype(np.int8)
+
+
+def pack_offsets(offsets: np.ndarray, scale_bits: int) -> np.ndarray:
+    """S-bit offsets [rows, nb] packed LSB first, offset j of a row at bits [S j, S j + S) of a
+    little-endian bit string, each row padded to ceil(nb S / 8) bytes."""
+    d = np.asarray(offsets).astype(np.uint8)
+    rows, nb = d.shape
+    bits = np.unpackbits(d[..., None], axis=-1, bitorder="little")[..., :scale_bits].reshape(rows, nb * scale_bits)
+    pad = (-(nb * scale_bits)) % 8
+    bits = np.concatenate([bits, np.zeros((rows, pad), np.uint8)], axis=1)
+    return np.packbits(bits, axis=-1, bitorder="little")
+
+
+def unpack_offsets(packed: np.ndarray, nb: int, scale_bits: int) -> np.ndarray:
+    """Inverse of pack_offsets."""
+    p = np.asarray(packed, dtype=np.uint8)
+    bits = np.unpackbits(p, axis=-1, bitorder="little")[:, : nb * scale_bits].reshape(p.shape[0], nb, scale_bits)
+    return (bits.astype(np.int64) << np.arange(scale_bits)).sum(-1)

@@ -118,6 +118,39 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
                                       reinterpret_cast<hipStream_t>(stream)));
 }
 
+int64_t curvefp_compact_offsets_bytes(int64_t rows, int64_t cols, int block, int scale_bits) {
+    if (!block_ok(block) || scale_bits < 2 || scale_bits > 8) return CURVEFP_ERR_BLOCK;
+    if (rows < 0 || cols < 0 || cols % block) return CURVEFP_ERR_SHAPE;
+    return rows * ((cols / block * scale_bits + 7) / 8);
+}
+
+int curvefp_quantize_compact(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src, int format,
+                             int block, int scale_bits, void* codes, int8_t* row_ref, uint8_t* offsets,
+                             void* stream) {
+    if (!src || !codes || !row_ref || !offsets) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
+    if (!block_ok(block) || scale_bits < 2 || scale_bits > 8) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || cols <= 0 || ld_src < cols || cols % block) return CURVEFP_ERR_SHAPE;
+    if (cols > 131072 || rows > 0x7FFFFFFF) return CURVEFP_ERR_SHAPE;   // one workgroup per row
+    const int esz = dtype == CURVEFP_F32 ? 4 : 2;
+    if (!aligned16(codes) || !aligned16(src) || (ld_src * esz) % 16) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_quantize_compact(src, dtype, rows, cols, ld_src, format, block, scale_bits, codes,
+                                              row_ref, offsets, reinterpret_cast<hipStream_t>(stream)));
+}
+
+int curvefp_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t rows, int64_t nblocks,
+                          int scale_bits, int8_t* scales, void* stream) {
+    if (!row_ref || !offsets || !scales) return CURVEFP_ERR_NULL;
+    if (scale_bits < 2 || scale_bits > 8) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || nblocks <= 0 || rows * nblocks >= ((int64_t)1 << 39)) return CURVEFP_ERR_SHAPE;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_scales_unpack(row_ref, offsets, rows, nblocks, scale_bits, scales,
+                                           reinterpret_cast<hipStream_t>(stream)));
+}
+
 int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
                          int block_axis, int format, int block, int candidates, void* codes, int8_t* scales,
                          void* stream) {
@@ -238,7 +271,7 @@ const char* curvefp_status_string(int status) {
         case CURVEFP_ERR_SHAPE:
             return "invalid shape, leading dimension, count, or blocked extent not a multiple of the block";
         case CURVEFP_ERR_FORMAT: return "unknown format or dtype";
-        case CURVEFP_ERR_BLOCK: return "unsupported block size or block axis";
+        case CURVEFP_ERR_BLOCK: return "unsupported block size, block axis or scale width";
         case CURVEFP_ERR_ALIGN: return "pointer or row not 16-byte aligned";
         case CURVEFP_ERR_HIP: return "HIP error (launch, device query or table upload)";
         default: return "unknown status";

@@ -101,6 +101,12 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
                                int axis, int format, int candidates, void* codes, int8_t* scales,
                                hipStream_t s);
+// S-bit scale exponents: per row an int8 reference and packed S-bit offsets (blocks along rows)
+hipError_t launch_quantize_compact(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int format,
+                                  int block, int scale_bits, void* codes, int8_t* row_ref, uint8_t* offsets,
+                                  hipStream_t s);
+hipError_t launch_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t rows, int64_t nblocks,
+                                int scale_bits, int8_t* scales, hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
                              int64_t outer, int64_t k, int block, float* dst, int64_t ld_dst, hipStream_t s);
 // workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)

@@ -159,37 +159,23 @@ __device__ __forceinline__ uint32_t group_max_u32(uint32_t v, int lgl) {
     return v;
 }
 
-// quantize one chunk of 8 consecutive elements; 2^lgl consecutive lanes hold one block of
-// 8 * 2^lgl elements (a quad for 32).  lgl < 0: the block scales were written by the scale
-// pass, scale of chunk g at g / (G / 8) (dgl)
-template <class F, bool BF16, bool NTS, class T>
-__device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const T* lut,
-                                               uint32_t lmax_mant, uint8_t* __restrict__ codes,
-                                               int8_t* __restrict__ scales, int lgl, Div32 dgl) {
+// codes of chunk g (8 consecutive elements, magnitudes and signs) at scale a, stored at chunk g
+// of `codes`; E3C3 packs 7 bits per code over the quad that holds a group of 32
+template <class F, bool NTS, class T>
+__device__ __forceinline__ void encode_chunk(const uint32_t* mag, const uint32_t* sgn, int a, uint32_t g,
+                                             const T* lut, uint8_t* __restrict__ codes) {
     const int part = (int)(g & 3);
-    uint32_t mag[8], sgn[8];
-    unpack8<BF16>(v, mag, sgn);
-    int a;
-    if (lgl >= 0) {
-        uint32_t amax = 0;
-#pragma unroll
-        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
-        amax = lgl == 2 ? quad_max_u32(amax) : group_max_u32(amax, lgl);
-        a = scale_of<F>(amax, lmax_mant);
-    } else {
-        a = scales[div32(g, dgl)];
-    }
     uint32_t rk[8];
     ranks_of<F>(mag, 8, a, lut, rk);
     uint32_t c[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) c[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
-    const uint32_t b = g >> 2;   // block index (blocks are contiguous in the output)
+    const uint32_t b = g >> 2;   // group of 32 (groups are contiguous in the output)
     if (!F::PACKED7) {
         st8<NTS>(codes + (uint64_t)g * 8, c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
                  c[4] | (c[5] << 8) | (c[6] << 16) | (c[7] << 24));
     } else {
-        // 56-bit chunk of this lane; the block string is chunk0 | chunk1 << 56 | ...
+        // 56-bit chunk of this lane; the group's string is chunk0 | chunk1 << 56 | ...
         uint64_t chunk = 0;
 #pragma unroll
         for (int i = 0; i < 8; i++) chunk |= (uint64_t)c[i] << (7 * i);
@@ -208,6 +194,28 @@ __device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const
             st4<NTS>(base + 6, (uint32_t)(chunk >> 24));
         }
     }
+}
+
+// quantize one chunk of 8 consecutive elements; 2^lgl consecutive lanes hold one block of
+// 8 * 2^lgl elements (a quad for 32).  lgl < 0: the block scales were written by the scale
+// pass, scale of chunk g at g / (G / 8) (dgl)
+template <class F, bool BF16, bool NTS, class T>
+__device__ __forceinline__ void quantize_chunk(const uint4* v, uint32_t g, const T* lut,
+                                               uint32_t lmax_mant, uint8_t* __restrict__ codes,
+                                               int8_t* __restrict__ scales, int lgl, Div32 dgl) {
+    uint32_t mag[8], sgn[8];
+    unpack8<BF16>(v, mag, sgn);
+    int a;
+    if (lgl >= 0) {
+        uint32_t amax = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+        amax = lgl == 2 ? quad_max_u32(amax) : group_max_u32(amax, lgl);
+        a = scale_of<F>(amax, lmax_mant);
+    } else {
+        a = scales[div32(g, dgl)];
+    }
+    encode_chunk<F, NTS>(mag, sgn, a, g, lut, codes);
     if (lgl >= 0 && (g & ((1u << lgl) - 1)) == 0) scales[g >> lgl] = (int8_t)a;
 }
 
@@ -639,6 +647,137 @@ hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, in
 }
 
 // ---------------------------------------------------------------------------------------------
+// S-bit scale exponents (Eq. effective-rate with an S-bit scale field).  One workgroup per row:
+// pass 1 writes the row's maxima per group of 32 to LDS; the block scales follow, the row's
+// reference (the largest scale among its finite blocks that are not all zero, 0 if none), and
+// every block's scale is raised to at least reference - (2^S - 2); pass 2 reads the row again
+// (from the caches) and quantizes it at those scales.  The offsets reference - scale (2^S - 1
+// for a block that held a NaN or an infinity, 0 for an all-zero block) leave packed S bits
+// each, LSB first, each row padded to whole bytes.
+constexpr int COMPACT_MAX_GROUPS = 4096;   // up to 131072 elements per row
+constexpr int COMPACT_NONE = -1000;         // below every scale
+
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void quantize_compact_kernel(const void* __restrict__ src, int64_t cols, int64_t ld,
+                                                               int G, int S, uint8_t* __restrict__ codes,
+                                                               int8_t* __restrict__ row_ref,
+                                                               uint8_t* __restrict__ offsets, int64_t off_bytes,
+                                                               int fidx) {
+    using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int NV = BF16 ? 1 : 2;
+    __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
+    __shared__ uint32_t gmax[COMPACT_MAX_GROUPS];
+    __shared__ int bsc[COMPACT_MAX_GROUPS];
+    __shared__ uint8_t doff[COMPACT_MAX_GROUPS];
+    __shared__ int wred[4];
+    const int tid = (int)threadIdx.x;
+    const int64_t row = blockIdx.x;
+    const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) + row * ld * ESZ);
+    const int nchunks = (int)(cols / 8), nb = (int)(cols / G), gpb = G / 32;
+    if (BF16) {
+        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(g_qlut8[fidx]);
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lut);
+        for (int i = tid; i < F::QLUT_SIZE / 4; i += 256) l32[i] = s32[i];
+    } else {
+        for (int i = tid; i < F::QLUT_SIZE; i += 256) lut[i] = (T)g_qlut[fidx][i];
+    }
+    const uint32_t lmax_mant = g_lmax_mant[fidx];
+    // pass 1: group maxima (the four chunks of a group sit in one quad of lanes)
+    for (int c = tid; c < nchunks; c += 256) {
+        uint4 v[NV];
+#pragma unroll
+        for (int t = 0; t < NV; t++) v[t] = ld16<false>(p + NV * c + t);
+        uint32_t mag[8], sgn[8];
+        unpack8<BF16>(v, mag, sgn);
+        uint32_t amax = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+        amax = quad_max_u32(amax);
+        if ((c & 3) == 0) gmax[c >> 2] = amax;
+    }
+    __syncthreads();
+    // block scales and the row's reference
+    int lm = COMPACT_NONE;
+    for (int b = tid; b < nb; b += 256) {
+        uint32_t m = 0;
+        for (int j = 0; j < gpb; j++) m = max(m, gmax[b * gpb + j]);
+        const int a = scale_of<F>(m, lmax_mant);
+        bsc[b] = m == 0 ? COMPACT_NONE : a;          // all-zero blocks take no part
+        if (m != 0 && a != -128) lm = max(lm, a);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) lm = max(lm, __shfl_xor(lm, o));
+    if ((tid & 63) == 0) wred[tid >> 6] = lm;
+    __syncthreads();
+    const int top = max(max(wred[0], wred[1]), max(wred[2], wred[3]));
+    const int ref = top == COMPACT_NONE ? 0 : top;
+    const int window = (1 << S) - 2;
+    for (int b = tid; b < nb; b += 256) {
+        const int a = bsc[b];
+        int ae, d;
+        if (a == COMPACT_NONE) { ae = ref; d = 0; }                        // all zero
+        else if (a == -128) { ae = -128; d = window + 1; }                 // NaN / Inf
+        else { ae = max(a, ref - window); d = ref - ae; }
+        bsc[b] = ae;
+        doff[b] = (uint8_t)d;
+    }
+    __syncthreads();
+    // pass 2: the row at its blocks' scales
+    uint8_t* rc = codes + (F::PACKED7 ? row * (cols / 32) * 28 : row * cols);
+    for (int c = tid; c < nchunks; c += 256) {
+        uint4 v[NV];
+#pragma unroll
+        for (int t = 0; t < NV; t++) v[t] = ld16<false>(p + NV * c + t);
+        uint32_t mag[8], sgn[8];
+        unpack8<BF16>(v, mag, sgn);
+        encode_chunk<F, false>(mag, sgn, bsc[(8 * c) / G], (uint32_t)c, lut, rc);
+    }
+    // the offsets, one output byte per thread and step
+    uint8_t* ro = offsets + row * off_bytes;
+    for (int64_t j = tid; j < off_bytes; j += 256) {
+        uint32_t v = 0;
+        for (int bit = 0; bit < 8; bit++) {
+            const int64_t gb = 8 * j + bit;
+            const int64_t blk = gb / S;
+            if (blk < nb) v |= (uint32_t)((doff[blk] >> (gb - blk * S)) & 1) << bit;
+        }
+        ro[j] = (uint8_t)v;
+    }
+    if (tid == 0) row_ref[row] = (int8_t)ref;
+}
+
+// int8 block scales from S-bit offsets: reference - offset, -128 for the marker 2^S - 1
+__global__ __launch_bounds__(256) void scales_unpack_kernel(const int8_t* __restrict__ row_ref,
+                                                            const uint8_t* __restrict__ offsets, int64_t rows,
+                                                            int64_t nb, int64_t off_bytes, int S,
+                                                            int8_t* __restrict__ scales) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= rows * nb) return;
+    const int64_t r = i / nb, b = i - r * nb;
+    const uint8_t* ro = offsets + r * off_bytes;
+    const int64_t gb = b * S;
+    uint32_t w = ro[gb >> 3];
+    if ((gb & 7) + S > 8) w |= (uint32_t)ro[(gb >> 3) + 1] << 8;
+    const int d = (int)((w >> (gb & 7)) & ((1u << S) - 1));
+    scales[i] = (int8_t)(d == (1 << S) - 1 ? -128 : (int)row_ref[r] - d);
+}
+
+template <class F>
+hipError_t launch_compact_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int block, int S,
+                              int fidx, void* codes, int8_t* row_ref, uint8_t* offsets, hipStream_t s) {
+    const int64_t ob = (cols / block * S + 7) / 8;
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    if (dtype == 1)
+        hipLaunchKernelGGL((quantize_compact_kernel<F, true>), dim3((unsigned)rows), dim3(256), 0, s, src, cols, ld,
+                           block, S, cp, row_ref, offsets, ob, fidx);
+    else
+        hipLaunchKernelGGL((quantize_compact_kernel<F, false>), dim3((unsigned)rows), dim3(256), 0, s, src, cols, ld,
+                           block, S, cp, row_ref, offsets, ob, fidx);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------------
 // Static-operand scales (Sec. 3.1: static operands choose a representable power-of-two scale by
 // reconstruction-MSE search).  One thread per block of 32: the block is quantized at each
 // candidate scale a_c + u (a_c ceil-absmax; u = 0, -1, .., -(candidates - 1), then 1 .. P - 1
@@ -849,6 +988,26 @@ hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t
         case 3: return launch_mse_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, candidates, 3, codes, scales, s);
         default: return launch_mse_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, candidates, 4, codes, scales, s);
     }
+}
+
+hipError_t launch_quantize_compact(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int format,
+                                  int block, int scale_bits, void* codes, int8_t* row_ref, uint8_t* offsets,
+                                  hipStream_t s) {
+    switch (format) {
+        case 0: return launch_compact_fmt<FmtE4C3>(src, dtype, rows, cols, ld, block, scale_bits, 0, codes, row_ref, offsets, s);
+        case 1: return launch_compact_fmt<FmtE5C2>(src, dtype, rows, cols, ld, block, scale_bits, 1, codes, row_ref, offsets, s);
+        case 2: return launch_compact_fmt<FmtE3C3>(src, dtype, rows, cols, ld, block, scale_bits, 2, codes, row_ref, offsets, s);
+        case 3: return launch_compact_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, block, scale_bits, 3, codes, row_ref, offsets, s);
+        default: return launch_compact_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, block, scale_bits, 4, codes, row_ref, offsets, s);
+    }
+}
+
+hipError_t launch_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t rows, int64_t nblocks,
+                                int scale_bits, int8_t* scales, hipStream_t s) {
+    const int64_t n = rows * nblocks;
+    hipLaunchKernelGGL(scales_unpack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ref, offsets, rows,
+                       nblocks, (nblocks * scale_bits + 7) / 8, scale_bits, scales);
+    return hipGetLastError();
 }
 
 }  // namespace curvefp

@@ -57,6 +57,12 @@ def lib() -> ctypes.CDLL:
         L.curvefp_quantize.restype = I
         L.curvefp_quantize_mse.argtypes = [P, I, I64, I64, I64, I, I, I, I, P, P, P]
         L.curvefp_quantize_mse.restype = I
+        L.curvefp_compact_offsets_bytes.argtypes = [I64, I64, I, I]
+        L.curvefp_compact_offsets_bytes.restype = I64
+        L.curvefp_quantize_compact.argtypes = [P, I, I64, I64, I64, I, I, I, P, P, P, P]
+        L.curvefp_quantize_compact.restype = I
+        L.curvefp_scales_unpack.argtypes = [P, P, I64, I64, I, P, P]
+        L.curvefp_scales_unpack.restype = I
         L.curvefp_dequantize.argtypes = [P, P, I, I64, I64, I, P, I64, P]
         L.curvefp_dequantize.restype = I
         L.curvefp_gemm.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
@@ -168,6 +174,49 @@ def curvefp_quantize_mse(src: torch.Tensor, fmt, block_axis: int = 1, candidates
                                     block, candidates, codes.data_ptr(), scales.data_ptr(), _stream(stream))
     _check(st, "curvefp_quantize_mse")
     return codes, scales
+
+
+def curvefp_compact_offsets_bytes(rows: int, cols: int, block: int, scale_bits: int) -> int:
+    n = lib().curvefp_compact_offsets_bytes(rows, cols, block, scale_bits)
+    if n < 0:
+        raise CurveFPError(int(n), "curvefp_compact_offsets_bytes")
+    return int(n)
+
+
+def curvefp_quantize_compact(src: torch.Tensor, fmt, block: int, scale_bits: int,
+                             codes: Optional[torch.Tensor] = None, row_ref: Optional[torch.Tensor] = None,
+                             offsets: Optional[torch.Tensor] = None,
+                             stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """Q(X) with S-bit scale exponents along the rows of src: codes as curvefp_quantize's
+    (block_axis=1), an int8 reference per row, and packed S-bit offsets [rows, bytes per row]."""
+    assert src.dim() == 2 and src.stride(1) == 1
+    rows, cols = src.shape
+    f = _fmt(fmt)
+    if codes is None:
+        shape = (rows, cols // 32, 28) if f == 2 else (rows, cols)
+        codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
+    if row_ref is None:
+        row_ref = torch.empty((rows,), dtype=torch.int8, device=src.device)
+    if offsets is None:
+        ob = curvefp_compact_offsets_bytes(1, cols, block, scale_bits)
+        offsets = torch.empty((rows, ob), dtype=torch.uint8, device=src.device)
+    st = lib().curvefp_quantize_compact(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), f, block,
+                                        scale_bits, codes.data_ptr(), row_ref.data_ptr(), offsets.data_ptr(),
+                                        _stream(stream))
+    _check(st, "curvefp_quantize_compact")
+    return codes, row_ref, offsets
+
+
+def curvefp_scales_unpack(row_ref: torch.Tensor, offsets: torch.Tensor, nblocks: int, scale_bits: int,
+                          scales: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """int8 block scales [rows, nblocks] of S-bit offsets (reference - offset; -128 marks NaN/Inf)."""
+    rows = row_ref.shape[0]
+    if scales is None:
+        scales = torch.empty((rows, nblocks), dtype=torch.int8, device=row_ref.device)
+    st = lib().curvefp_scales_unpack(row_ref.data_ptr(), offsets.data_ptr(), rows, nblocks, scale_bits,
+                                     scales.data_ptr(), _stream(stream))
+    _check(st, "curvefp_scales_unpack")
+    return scales
 
 
 def curvefp_dequantize(codes: torch.Tensor, scales: torch.Tensor, fmt, outer: int, k: int,

@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 15
+    assert len(names) == 18
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -301,3 +301,35 @@ def test_gemm_requant_validation(L):
         assert g(*a) == EALIGN, i
     a = list(args); a[12] = WS + 64
     assert g(*a) == EALIGN
+
+
+def test_quantize_compact_validation(L):
+    q = L.curvefp_quantize_compact
+    #       src   dt rows cols ld  fmt blk S  codes ref   offs  stream
+    args = [FAKE, 0, 4, 256, 256, 2, 64, 4, FAKE, FAKE, FAKE, None]
+    for i in (0, 8, 9, 10):
+        a = list(args); a[i] = None
+        assert q(*a) == ENULL, i
+    for i, v in ((1, 2), (5, 5)):
+        a = list(args); a[i] = v
+        assert q(*a) == EFMT, (i, v)
+    for i, v in ((6, 48), (6, 0), (7, 1), (7, 9)):
+        a = list(args); a[i] = v
+        assert q(*a) == EBLOCK, (i, v)
+    for i, v in ((2, 0), (3, 96), (4, 128), (6, 512)):
+        a = list(args); a[i] = v
+        assert q(*a) == ESHAPE, (i, v)
+    a = list(args); a[3] = a[4] = 131072 + 64; a[6] = 64
+    assert q(*a) == ESHAPE                       # more than 4096 groups of 32 in a row
+    for i in (0, 8):
+        a = list(args); a[i] = MIS
+        assert q(*a) == EALIGN, i
+    assert L.curvefp_compact_offsets_bytes(3, 4096, 64, 4) == 3 * 32
+    assert L.curvefp_compact_offsets_bytes(3, 4096, 64, 5) == 3 * 40
+    assert L.curvefp_compact_offsets_bytes(2, 96, 32, 5) == 2 * 2      # 15 bits -> 2 bytes
+    assert L.curvefp_compact_offsets_bytes(2, 96, 32, 9) == EBLOCK
+    assert L.curvefp_compact_offsets_bytes(2, 96, 64, 4) == ESHAPE
+    u = L.curvefp_scales_unpack
+    assert u(None, FAKE, 4, 4, 4, FAKE, None) == ENULL
+    assert u(FAKE, FAKE, 4, 4, 1, FAKE, None) == EBLOCK
+    assert u(FAKE, FAKE, 0, 4, 4, FAKE, None) == ESHAPE

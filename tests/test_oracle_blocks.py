@@ -153,3 +153,78 @@ def test_mixed_gemm_with_reused_operand_in_blocks_of_g(pair):
     ref = da @ db.T
     bound = (2.0 ** -22 + K * 2.0 ** -52) * (np.abs(da) @ np.abs(db).T) + 2.0 ** -140
     assert np.all(np.abs(V - ref) <= bound)
+
+
+# ---------------------------------------------------------------- S-bit scale exponents
+
+def spread_rows(rng, rows, cols, G, spread):
+    """Blocks of G along rows with block magnitudes 2^U(0, spread) below a row top of 2^U(-5, 5)."""
+    top = rng.uniform(-5, 5, (rows, 1))
+    blk = top - rng.uniform(0, spread, (rows, cols // G))
+    x = rng.standard_normal((rows, cols)) * np.exp2(np.repeat(blk, G, axis=1))
+    return x.astype(np.float32)
+
+
+@pytest.mark.parametrize("name", NAMES)
+@pytest.mark.parametrize("S", [4, 5])
+def test_compact_within_window_is_the_block_quantizer(name, S):
+    """When every block's scale lies within 2^S - 2 of its row's largest, the S-bit form holds the
+    block quantizer's codes and scales exactly (reference - offset)."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(70 + S)
+    G = 64
+    x = spread_rows(rng, 8, 1024, G, (1 << S) - 6)
+    c, s = oracle.quantize(x, f, G)
+    cc, ref, d = oracle.quantize_compact(x, f, G, S)
+    assert np.array_equal(cc, c)
+    assert np.array_equal(oracle.compact_scales(ref, d, S), s)
+    assert ref.tolist() == s.astype(np.int64).max(axis=1).tolist()
+    assert d.max() <= (1 << S) - 2
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_compact_raised_blocks_are_nearest_at_the_raised_scale(name):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(77)
+    G, S = 64, 4
+    x = spread_rows(rng, 4, 512, G, 40)          # blocks far below the row top
+    cc, ref, d = oracle.quantize_compact(x, f, G, S)
+    _, s = oracle.quantize(x, f, G)
+    window = (1 << S) - 2
+    raised = s.astype(np.int64) < ref.astype(np.int64)[:, None] - window
+    assert raised.any() and np.all(d[raised] == window)
+    a = np.repeat(oracle.compact_scales(ref, d, S).astype(np.int64), G, axis=1)
+    for r, c in zip(*np.nonzero(np.repeat(raised, G, axis=1))):
+        if rng.random() < 0.25:
+            assert int(cc[r, c]) == rigorous_code(float(x[r, c]), int(a[r, c]), f), (r, c)
+
+
+def test_compact_markers_zero_blocks_and_rows():
+    f = oracle.get_format("E3C3")
+    x = np.ones((3, 256), np.float32) * np.float32(3.0)
+    x[0, 70] = np.nan                     # block 1 of row 0 poisoned
+    x[1, :64] = 0.0                       # block 0 of row 1 all zero
+    x[2, :] = 0.0                         # an all-zero row
+    x[1, 64:] = np.float32(2.0 ** -30)    # row 1's other blocks far below nothing: they set the reference
+    for S in (4, 5):
+        cc, ref, d = oracle.quantize_compact(x, f, 64, S)
+        _, s = oracle.quantize(x, f, 64)
+        assert d[0].tolist() == [0, (1 << S) - 1, 0, 0] and not cc[0, 64:128].any()
+        assert ref[0] == s[0, 0]
+        assert d[1, 0] == 0 and ref[1] == s[1, 1] and not cc[1, :64].any()
+        assert ref[2] == 0 and d[2].tolist() == [0, 0, 0, 0] and not cc[2].any()
+        assert oracle.compact_scales(ref, d, S)[0, 1] == oracle.POISON_SCALE
+
+
+def test_compact_offset_packing_layout():
+    """Offsets LSB first in a little-endian bit string, rows padded to whole bytes, worked by
+    hand: S = 4, offsets 1, 2, 15, 0, 7 -> 0x21 0x0F 0x07; S = 5, offsets 1, 2, 31, 4 -> bits 0
+    (1), 6 (2 << 5), 10..14 (31 << 10), 17 (4 << 15) -> 0x41 0x7C 0x02."""
+    assert oracle.pack_offsets(np.array([[1, 2, 15, 0, 7]]), 4).tolist() == [[0x21, 0x0F, 0x07]]
+    assert oracle.pack_offsets(np.array([[1, 2, 31, 4]]), 5).tolist() == [[0x41, 0x7C, 0x02]]
+    rng = np.random.default_rng(5)
+    for S in range(2, 9):
+        d = rng.integers(0, 1 << S, (3, 37))
+        p = oracle.pack_offsets(d, S)
+        assert p.shape == (3, (37 * S + 7) // 8)
+        assert np.array_equal(oracle.unpack_offsets(p, 37, S), d)
