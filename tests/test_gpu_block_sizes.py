@@ -92,7 +92,7 @@ def test_quantize_edges(fmt):
 def test_quantize_inference_activation_blocks(G):
     """The inference activation (2048 x 4096 bf16, outlier channels) with G512 and rowwise
     scales, in E3C3 (the paper's G sweep format)."""
-    a = W.get("inference").operand("act")
+    a = W.get("inference").operand("a")
     check_quantize(a, "E3C3", "bf16", 1, G, "inference_act")
 
 
@@ -196,3 +196,27 @@ def test_gemm_mixed(ta, tb, G):
     cb, sb = operand(B.astype(np.float32), fb, tb)
     V = oracle.gemm_exact_mixed(ca, sa, oracle.get_format(fa), cb, sb, oracle.get_format(fb))
     check_gemm(C, V, gemm_tolerance_mixed(ca, sa, fa, cb, sb, fb), f"mixed ta={ta} tb={tb} G={G}")
+
+
+@pytest.mark.parametrize("G", [512, 4096])
+def test_inference_full_size(G):
+    """The inference workload at its full size (2048 x 4096 x 4096 E3C3, bf16 sources) with G512
+    and rowwise scales, in the launch configuration bench.py times: the workspace GEMM equals the
+    G = 32 call on the same codes with repeated scales bit for bit, and 16 sampled rows equal the
+    exact oracle on the oracle's own quantization within the bound."""
+    w = W.get("inference")
+    A, B = w.operand("a"), w.operand("b")
+    say(f"[blocks] inference full size G={G}")
+    qa = cf.curvefp_quantize(to_dev(A, "bf16"), w.fmt, block=G)
+    qb = cf.curvefp_quantize(to_dev(B, "bf16"), w.fmt, block=G)
+    C = cf.curvefp_gemm_ws(qa[0], qa[1], qb[0], qb[1], w.M, w.N, w.K, w.fmt, block=G)
+    C32 = cf.curvefp_gemm_ws(qa[0], repeat32(qa[1], G), qb[0], repeat32(qb[1], G), w.M, w.N, w.K, w.fmt)
+    torch.cuda.synchronize()
+    C = C.cpu().numpy()
+    same_bits(C, C32.cpu().numpy(), f"inference G={G} vs G=32 repeated")
+    f = oracle.get_format(w.fmt)
+    rows = np.random.default_rng(G).choice(w.M, 16, replace=False)
+    ca, sa = oracle.quantize(np.ascontiguousarray(A[rows]), f, G)
+    cb, sb = oracle.quantize(B, f, G)
+    V = oracle.gemm_exact(ca, sa, cb, sb, f, block=G)
+    check_gemm(C[rows], V, gemm_tolerance(ca, sa, cb, sb, w.fmt, block=G), f"inference G={G} sampled rows")

@@ -66,9 +66,10 @@ def test_quantize_compact_edges(fmt):
     check_compact(spread_rows(rng, 2, 131072, 512, 20), fmt, "bf16", 512, 5, "long_rows")
 
 
-@pytest.mark.parametrize("which,S", [("act", 5), ("weight", 4)])
+@pytest.mark.parametrize("which,S", [("a", 5), ("b", 4)])
 def test_inference_operands(which, S):
-    """The inference operands in E3C3 with G64 and the paper's scale widths."""
+    """The inference operands in E3C3 with G64 and the paper's scale widths (S = 5 for the
+    activation, 4 for the weight)."""
     x = W.get("inference").operand(which)
     check_compact(x, "E3C3", "bf16", 64, S, f"inference_{which}")
 
