@@ -812,24 +812,23 @@ __device__ __forceinline__ uint32_t rank_at(uint32_t mag, int a, const uint32_t*
     return a >= F::A_FAST_MIN ? rank_fast<F>(mag, a, lut) : rank_exact<F>(mag, a, lut);
 }
 
-// squared reconstruction error of the block at scale a; codes are formed and dropped element by
-// element, so only the magnitudes stay in registers across candidates
+// squared reconstruction error of one element at scale a, added to acc (fp64, index order)
 template <class F>
-__device__ __forceinline__ double block_error(const uint32_t* mag, uint32_t sgn, int a, const uint32_t* lut,
-                                              const uint32_t* mant, const uint64_t* sig) {
-    double acc = 0.0;
-#pragma unroll
-    for (int i = 0; i < 32; i++) {
-        const uint32_t s = (sgn >> i) & 1u;
-        const uint32_t rk = rank_at<F>(mag[i], a, lut);
-        const uint32_t code = rk | ((rk != 0 ? s : 0u) << F::EC);
-        const double x = f64_of_f32_bits(mag[i] | (s << 31));
-        const double xh = f64_of_f32_bits(value_bits<F>(code, a, mant, sig));
-        acc = add_square(acc, x - xh);
-    }
-    return acc;
+__device__ __forceinline__ double add_element_error(double acc, uint32_t m, uint32_t s, double x, int a,
+                                                    const uint32_t* lut, const uint32_t* mant, const uint64_t* sig) {
+    const uint32_t rk = rank_at<F>(m, a, lut);
+    const uint32_t code = rk | ((rk != 0 ? s : 0u) << F::EC);
+    const double xh = f64_of_f32_bits(value_bits<F>(code, a, mant, sig));
+    return add_square(acc, x - xh);
 }
 
+// candidates per block at most: 8 below or at the ceil-absmax scale, P - 1 <= 2 above it
+constexpr int MSE_MAXC = 10;
+
+// One thread per block.  The block's magnitudes sit in LDS ([element][thread], so a wave's
+// reads of one element are conflict-free); one pass over the 32 elements updates every
+// candidate's error sum, each in index order, so each element is converted once and only the
+// sums stay in registers (the candidate loop is unrolled and guarded by the wave-uniform count).
 template <class F, bool BF16>
 __global__ __launch_bounds__(256) void quantize_mse_kernel(
     const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld, int axis, int candidates,
@@ -838,6 +837,7 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
     constexpr int RT = F::BINARY ? 8 : 128;
     __shared__ uint32_t mant[RT];
     __shared__ uint64_t sig[RT];
+    __shared__ uint32_t smag[32 * 256];
     for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
     if (threadIdx.x < RT) {
         mant[threadIdx.x] = g_qr_mant[fidx][threadIdx.x];
@@ -851,8 +851,9 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
     const int64_t nb = axis == 1 ? rows * nbr : cols * nbr;
     const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (b >= nb) return;
+    uint32_t* my = smag + threadIdx.x;                              // element i at my[256 i]
     int64_t orow, oblk;                                             // output row and block in it
-    uint32_t mag[32], sgn = 0;
+    uint32_t sgn = 0, amax = 0;
     if (axis == 1) {
         orow = b / nbr;
         oblk = b - orow * nbr;
@@ -864,8 +865,10 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
                 const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int j = 0; j < 4; j++) {
-                    mag[8 * t + 2 * j] = (w[j] << 16) & 0x7FFF0000u;
-                    mag[8 * t + 2 * j + 1] = w[j] & 0x7FFF0000u;
+                    const uint32_t m0 = (w[j] << 16) & 0x7FFF0000u, m1 = w[j] & 0x7FFF0000u;
+                    my[256 * (8 * t + 2 * j)] = m0;
+                    my[256 * (8 * t + 2 * j + 1)] = m1;
+                    amax = max(amax, max(m0, m1));
                     sgn |= ((w[j] >> 15) & 1u) << (8 * t + 2 * j);
                     sgn |= (w[j] >> 31) << (8 * t + 2 * j + 1);
                 }
@@ -878,7 +881,9 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
                 const uint32_t w[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                 for (int j = 0; j < 4; j++) {
-                    mag[4 * t + j] = w[j] & 0x7FFFFFFFu;
+                    const uint32_t m = w[j] & 0x7FFFFFFFu;
+                    my[256 * (4 * t + j)] = m;
+                    amax = max(amax, m);
                     sgn |= (w[j] >> 31) << (4 * t + j);
                 }
             }
@@ -892,33 +897,47 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
             const int64_t e = (32 * rb + i) * ld + orow;
             const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[e] << 16)
                                     : reinterpret_cast<const uint32_t*>(src)[e];
-            mag[i] = w & 0x7FFFFFFFu;
+            my[256 * i] = w & 0x7FFFFFFFu;
+            amax = max(amax, w & 0x7FFFFFFFu);
             sgn |= (w >> 31) << i;
         }
     }
-    uint32_t amax = 0;
-#pragma unroll
-    for (int i = 0; i < 32; i++) amax = max(amax, mag[i]);
     const int ac = scale_of<F>(amax, lmax_mant);
     const bool live = ac != -128 && amax != 0;
     int best_a = ac;
     if (live) {
-        double best_err = block_error<F>(mag, sgn, ac, lut, mant, sig);
         const int nc = candidates + F::PERIOD - 1;
-        for (int c = 1; c < nc; c++) {
-            const int a = c < candidates ? ac - c : ac + (c - candidates + 1);
-            if (a < -127 || a > 127) continue;
-            const double err = block_error<F>(mag, sgn, a, lut, mant, sig);
-            if (err < best_err) {
-                best_err = err;
-                best_a = a;
-            }
+        int acand[MSE_MAXC];
+        bool ok[MSE_MAXC];
+        double acc[MSE_MAXC];
+#pragma unroll
+        for (int c = 0; c < MSE_MAXC; c++) {
+            acand[c] = c < candidates ? ac - c : ac + (c - candidates + 1);
+            ok[c] = c < nc && acand[c] >= -127 && acand[c] <= 127;
+            acc[c] = 0.0;
         }
+#pragma unroll 2
+        for (int i = 0; i < 32; i++) {
+            const uint32_t m = my[256 * i];
+            const uint32_t s = (sgn >> i) & 1u;
+            const double x = f64_of_f32_bits(m | (s << 31));
+#pragma unroll
+            for (int c = 0; c < MSE_MAXC; c++)
+                if (c < nc && ok[c]) acc[c] = add_element_error<F>(acc[c], m, s, x, acand[c], lut, mant, sig);
+        }
+        // the first candidate in the order above with the least error
+        double best_err = acc[0];
+#pragma unroll
+        for (int c = 1; c < MSE_MAXC; c++)
+            if (c < nc && ok[c] && acc[c] < best_err) {
+                best_err = acc[c];
+                best_a = acand[c];
+            }
     }
     uint32_t cc[32];
 #pragma unroll
     for (int i = 0; i < 32; i++) {
-        const uint32_t rk = live ? rank_at<F>(mag[i], best_a, lut) : 0u;
+        const uint32_t rk = live ? rank_at<F>(my[256 * i], best_a, lut) : 0u;
         cc[i] = rk | ((rk != 0 ? (sgn >> i) & 1u : 0u) << F::EC);
     }
     if (!F::PACKED7) {
