@@ -545,8 +545,15 @@ def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 10):
         out[f"compact_G{G}_S{S}_{which}"] = {
             "quantize_gbps": (rows * w.K * per_elem + rows) / tq / 1e9, "us": tq * 1e6,
             "bits_per_value": (7.0 if w.fmt == "E3C3" else 8.0) + S / G}
+    # tensorwise: one scale per tensor (a max pass over the source, then the quantize pass)
+    for which, t, rows in (("act", ta, w.M), ("weight", tb, w.N)):
+        cc, ss = cf.curvefp_quantize_tensorwise(t, w.fmt)
+        wsw = torch.empty((1,), dtype=torch.int32, device=dev)
+        per_elem = quantize_bytes_per_elem(w.fmt, w.dtype) - 1.0 / 32.0
+        tq = timed(lambda: cf.curvefp_quantize_tensorwise(t, w.fmt, codes=cc, scales=ss, workspace=wsw))
+        out[f"tensorwise_{which}"] = {"quantize_gbps": (rows * w.K * per_elem + rows) / tq / 1e9, "us": tq * 1e6}
     out["workload"] = (f"{w.name}: act {w.M}x{w.K}, weight {w.N}x{w.K} {w.dtype} -> {w.fmt}, G = 32, 64, 512, K; "
-                       f"S-bit scales at G64 (S = 5 act, 4 weight)")
+                       f"S-bit scales at G64 (S = 5 act, 4 weight); tensorwise")
     out["timing"] = f"median of {reps} individually timed calls each"
     return out
 

@@ -144,6 +144,22 @@ int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols,
                          void* codes, int8_t* scales, void* stream);
 
 /*
+ * Tensorwise scale sharing (Sec. 3.1 evaluates tensorwise, rowwise and fixed-size blocks): one
+ * ceil-absmax scale for the whole tensor, i.e. the block is the tensor.  Codes as
+ * curvefp_quantize's for the same block_axis; the scale is written once per output row,
+ * scales [outer] (outer = rows for block_axis = 1, cols for 0), all equal, so every consumer
+ * takes the operand as rowwise-scaled (block = the blocked extent).  A NaN or infinity
+ * anywhere poisons the tensor (scale -128, zero codes).
+ *   workspace  one 32-bit word of device memory (4-byte aligned), scratch of the call:
+ *              calls that share it must be ordered.
+ * The blocked extent must be a multiple of 32 and at most 2^30 (CURVEFP_ERR_SHAPE).  The source
+ * is read twice (its maximum, then the codes).
+ */
+int curvefp_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                                int block_axis, int format, void* codes, int8_t* scales, void* workspace,
+                                void* stream);
+
+/*
  * Block quantization with S-bit scale exponents (Eq. effective-rate, R = 1 + E + C + S/G bits
  * per value; Sec. 4.2 prices E3C3 weights at S = 4 and activations at S = 5), blocks of G along
  * the rows of src.  The paper gives only the width; the layout taken here: each row keeps one

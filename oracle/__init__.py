@@ -37,6 +37,7 @@ from .quant import (
     pack7,
     unpack7,
     quantize_compact,
+    quantize_tensorwise,
     compact_scales,
     pack_offsets,
     unpack_offsets,

@@ -341,3 +341,16 @@ def unpack_offsets(packed: np.ndarray, nb: int, scale_bits: int) -> np.ndarray:
     p = np.asarray(packed, dtype=np.uint8)
     bits = np.unpackbits(p, axis=-1, bitorder="little")[:, : nb * scale_bits].reshape(p.shape[0], nb, scale_bits)
     return (bits.astype(np.int64) << np.arange(scale_bits)).sum(-1)
+
+
+# ---------------------------------------------------------------- tensorwise scales
+
+def quantize_tensorwise(x: np.ndarray, fmt: Format):
+    """Tensorwise scale sharing (Sec. 3.1): the whole tensor is one block, quantized at the
+    ceil-absmax scale of its largest magnitude.  Returns (codes uint8 [rows, cols], scales int8
+    [rows, 1]): the scale repeated once per row, the rowwise layout (block = cols)."""
+    x = np.asarray(x)
+    assert x.dtype == np.float32 and x.ndim == 2
+    rows, cols = x.shape
+    codes, s = quantize(np.ascontiguousarray(x.reshape(1, rows * cols)), fmt, rows * cols)
+    return codes.reshape(rows, cols), np.full((rows, 1), s[0, 0], dtype=np.int8)

@@ -118,6 +118,25 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
                                       reinterpret_cast<hipStream_t>(stream)));
 }
 
+int curvefp_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
+                                int block_axis, int format, void* codes, int8_t* scales, void* workspace,
+                                void* stream) {
+    if (!src || !codes || !scales || !workspace) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
+    if (block_axis != 0 && block_axis != 1) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || cols <= 0 || ld_src < cols) return CURVEFP_ERR_SHAPE;
+    if ((block_axis == 1 ? cols : rows) % 32 || (block_axis == 1 ? cols : rows) > (1 << 30)) return CURVEFP_ERR_SHAPE;
+    if (rows >= ((int64_t)1 << 31) || cols >= ((int64_t)1 << 31)) return CURVEFP_ERR_SHAPE;
+    const int esz = dtype == CURVEFP_F32 ? 4 : 2;
+    if (!aligned16(codes) || (reinterpret_cast<uintptr_t>(workspace) & 3)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
+    if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
+    int st = ensure_tables();
+    if (st) return st;
+    return hip_status(launch_quantize_tensorwise(src, dtype, rows, cols, ld_src, block_axis, format, codes, scales,
+                                                 workspace, reinterpret_cast<hipStream_t>(stream)));
+}
+
 int64_t curvefp_compact_offsets_bytes(int64_t rows, int64_t cols, int block, int scale_bits) {
     if (!block_ok(block) || scale_bits < 2 || scale_bits > 8) return CURVEFP_ERR_BLOCK;
     if (rows < 0 || cols < 0 || cols % block) return CURVEFP_ERR_SHAPE;

@@ -101,6 +101,9 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
                                int axis, int format, int candidates, void* codes, int8_t* scales,
                                hipStream_t s);
+// one scale for the whole tensor, written once per output row; workspace: one 32-bit word
+hipError_t launch_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                                     int format, void* codes, int8_t* scales, void* workspace, hipStream_t s);
 // S-bit scale exponents: per row an int8 reference and packed S-bit offsets (blocks along rows)
 hipError_t launch_quantize_compact(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int format,
                                   int block, int scale_bits, void* codes, int8_t* row_ref, uint8_t* offsets,

@@ -577,10 +577,10 @@ __global__ __launch_bounds__(256) void quantize_cols_tiled_kernel(
     }
 }
 
+// given != 0: the block scales (blocks of `block` rows) are already in `scales`
 template <class F, int R>
 hipError_t launch_cols(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int fidx,
-                       uint8_t* codes, int8_t* scales, int block, hipStream_t s) {
-    const int given = block > 32;
+                       uint8_t* codes, int8_t* scales, int block, int given, hipStream_t s) {
     const Div32 dgq = make_div32((uint32_t)(block / 32));
     // column slabs keep the thread count of one launch below 2^31
     const int64_t groups = rows / (32 * R);
@@ -643,7 +643,7 @@ hipError_t launch_fmt(const void* src, int dtype, int64_t rows, int64_t cols, in
                                scales, fidx, given, rows / block, dgq);
         return hipGetLastError();
     }
-    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, block, s);
+    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, block, given, s);
 }
 
 // ---------------------------------------------------------------------------------------------
@@ -761,6 +761,126 @@ __global__ __launch_bounds__(256) void scales_unpack_kernel(const int8_t* __rest
     if ((gb & 7) + S > 8) w |= (uint32_t)ro[(gb >> 3) + 1] << 8;
     const int d = (int)((w >> (gb & 7)) & ((1u << S) - 1));
     scales[i] = (int8_t)(d == (1 << S) - 1 ? -128 : (int)row_ref[r] - d);
+}
+
+// Tensorwise scales: one ceil-absmax scale for the whole tensor.  A 4-byte workspace word is
+// cleared, every workgroup folds the largest magnitude bits it reads into it (atomicMax on the
+// fp32 bit pattern: non-negative floats order as integers, NaN above infinity), the scale is
+// written once per output row (the rowwise layout, all entries equal), and the quantize kernels
+// then read it as the scale of a block spanning the whole blocked extent.
+__global__ void tensor_max_clear_kernel(uint32_t* __restrict__ word) { *word = 0u; }
+
+// VEC: rows 16-byte aligned with cols % 8 == 0, read in chunks of 8 elements (n = rows * cols / 8
+// chunks, row of chunk g = g / (cols / 8)); otherwise one element at a time (n = rows * cols).
+// n < 2^32 either way (the launcher checks).
+template <bool BF16, bool VEC>
+__global__ __launch_bounds__(256) void tensor_max_kernel(const void* __restrict__ src, uint32_t n, uint32_t per_row,
+                                                         Div32 dpr, int64_t ld, uint32_t* __restrict__ word) {
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int NV = BF16 ? 1 : 2;
+    uint32_t m = 0;
+    // four units in flight per thread: the grid is small (every workgroup ends in one atomic on
+    // the same word, and those serialize), so each thread streams many units
+#pragma unroll 4
+    for (uint32_t g = blockIdx.x * 256u + threadIdx.x; g < n; g += gridDim.x * 256u) {
+        const uint32_t r = div32(g, dpr), c = g - r * per_row;
+        if (VEC) {
+            const uint4* p = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) +
+                                                            ((int64_t)r * ld + 8 * (int64_t)c) * ESZ);
+            uint4 v[NV];
+#pragma unroll
+            for (int t = 0; t < NV; t++) v[t] = ld16<true>(p + t);
+            uint32_t mag[8], sgn[8];
+            unpack8<BF16>(v, mag, sgn);
+#pragma unroll
+            for (int i = 0; i < 8; i++) m = max(m, mag[i]);
+        } else {
+            const char* p = reinterpret_cast<const char*>(src) + ((int64_t)r * ld + c) * ESZ;
+            const uint32_t w = BF16 ? ((uint32_t)*reinterpret_cast<const uint16_t*>(p) << 16)
+                                    : *reinterpret_cast<const uint32_t*>(p);
+            m = max(m, w & 0x7FFFFFFFu);
+        }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, o));
+    __shared__ uint32_t wm[4];
+    if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = m;
+    __syncthreads();
+    if (threadIdx.x == 0) atomicMax(word, max(max(wm[0], wm[1]), max(wm[2], wm[3])));
+}
+
+template <class F>
+__global__ __launch_bounds__(256) void tensor_scale_kernel(const uint32_t* __restrict__ word, int64_t outer,
+                                                           int8_t* __restrict__ scales, int fidx) {
+    const int a = scale_of<F>(*word, g_lmax_mant[fidx]);
+    for (int64_t r = (int64_t)blockIdx.x * 256 + threadIdx.x; r < outer; r += (int64_t)gridDim.x * 256)
+        scales[r] = (int8_t)a;
+}
+
+template <class F>
+hipError_t launch_tensorwise_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                                 int fidx, void* codes, int8_t* scales, uint32_t* word, hipStream_t s) {
+    hipLaunchKernelGGL(tensor_max_clear_kernel, dim3(1), dim3(1), 0, s, word);
+    const int64_t esz0 = dtype == 1 ? 2 : 4;
+    const bool vec = cols % 8 == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 && (ld * esz0) % 16 == 0;
+    const int64_t per_row = vec ? cols / 8 : cols;
+    // slabs of rows keep the unit count of one launch at most 2^32 - 2^21, so the grid-stride
+    // index (stride at most 2^20) never wraps; per_row < 2^31 (checked by the caller)
+    const int64_t slab = (((int64_t)1 << 32) - ((int64_t)1 << 21)) / per_row;
+    for (int64_t r0 = 0; r0 < rows; r0 += slab) {
+        const int64_t nr = rows - r0 < slab ? rows - r0 : slab;
+        const uint32_t n = (uint32_t)(nr * per_row);
+        int64_t g = ((int64_t)n + 255) / 256;
+        g = g < 256 ? g : 256;                 // one workgroup per compute unit, 256 atomics
+        const void* sp = reinterpret_cast<const char*>(src) + r0 * ld * esz0;
+        const Div32 dpr = make_div32((uint32_t)per_row);
+        if (dtype == 1) {
+            if (vec) hipLaunchKernelGGL((tensor_max_kernel<true, true>), dim3((unsigned)g), dim3(256), 0, s, sp, n,
+                                        (uint32_t)per_row, dpr, ld, word);
+            else hipLaunchKernelGGL((tensor_max_kernel<true, false>), dim3((unsigned)g), dim3(256), 0, s, sp, n,
+                                    (uint32_t)per_row, dpr, ld, word);
+        } else {
+            if (vec) hipLaunchKernelGGL((tensor_max_kernel<false, true>), dim3((unsigned)g), dim3(256), 0, s, sp, n,
+                                        (uint32_t)per_row, dpr, ld, word);
+            else hipLaunchKernelGGL((tensor_max_kernel<false, false>), dim3((unsigned)g), dim3(256), 0, s, sp, n,
+                                    (uint32_t)per_row, dpr, ld, word);
+        }
+    }
+    const int64_t outer = axis == 1 ? rows : cols;
+    int64_t gs = (outer + 255) / 256;
+    gs = gs < 1024 ? gs : 1024;
+    hipLaunchKernelGGL((tensor_scale_kernel<F>), dim3((unsigned)gs), dim3(256), 0, s, word, outer, scales, fidx);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // the quantize pass with the scale given, one block per output row of the blocked extent
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    const int64_t esz = dtype == 1 ? 2 : 4;
+    if (axis == 1) {
+        const Div32 dgl = make_div32((uint32_t)(cols / 8));
+        const int64_t nchunks = rows * (cols / 8);
+        if (dtype == 1) {
+            if (nchunks >= (int64_t)2048 * 256 * 8)
+                return launch_rows_u<F, true, 8>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
+            return launch_rows_u<F, true, 2>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
+        }
+        if (nchunks >= (int64_t)2048 * 256 * 2)
+            return launch_rows_u<F, false, 2>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
+        return launch_rows_u<F, false, 1>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
+    }
+    const Div32 dgq = make_div32((uint32_t)(rows / 32));
+    const bool tiled = rows % TT_ROWS == 0 && cols % 8 == 0 && (reinterpret_cast<uintptr_t>(src) & 15) == 0 &&
+                       (ld * esz) % 16 == 0 && rows / TT_ROWS <= 65535;
+    if (tiled) {
+        const dim3 grid((unsigned)((cols + TT_COLS - 1) / TT_COLS), (unsigned)(rows / TT_ROWS));
+        if (dtype == 1)
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, cp,
+                               scales, fidx, 1, (int64_t)1, dgq);
+        else
+            hipLaunchKernelGGL((quantize_cols_tiled_kernel<F, false>), grid, dim3(256), 0, s, src, rows, cols, ld, cp,
+                               scales, fidx, 1, (int64_t)1, dgq);
+        return hipGetLastError();
+    }
+    return launch_cols<F, 1>(src, dtype, rows, cols, ld, fidx, cp, scales, (int)rows, 1, s);
 }
 
 template <class F>
@@ -1027,6 +1147,18 @@ hipError_t launch_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, i
     hipLaunchKernelGGL(scales_unpack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, row_ref, offsets, rows,
                        nblocks, (nblocks * scale_bits + 7) / 8, scale_bits, scales);
     return hipGetLastError();
+}
+
+hipError_t launch_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
+                                     int format, void* codes, int8_t* scales, void* workspace, hipStream_t s) {
+    uint32_t* w = reinterpret_cast<uint32_t*>(workspace);
+    switch (format) {
+        case 0: return launch_tensorwise_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, 0, codes, scales, w, s);
+        case 1: return launch_tensorwise_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, 1, codes, scales, w, s);
+        case 2: return launch_tensorwise_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, 2, codes, scales, w, s);
+        case 3: return launch_tensorwise_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, 3, codes, scales, w, s);
+        default: return launch_tensorwise_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, 4, codes, scales, w, s);
+    }
 }
 
 }  // namespace curvefp

@@ -57,6 +57,8 @@ def lib() -> ctypes.CDLL:
         L.curvefp_quantize.restype = I
         L.curvefp_quantize_mse.argtypes = [P, I, I64, I64, I64, I, I, I, I, P, P, P]
         L.curvefp_quantize_mse.restype = I
+        L.curvefp_quantize_tensorwise.argtypes = [P, I, I64, I64, I64, I, I, P, P, P, P]
+        L.curvefp_quantize_tensorwise.restype = I
         L.curvefp_compact_offsets_bytes.argtypes = [I64, I64, I, I]
         L.curvefp_compact_offsets_bytes.restype = I64
         L.curvefp_quantize_compact.argtypes = [P, I, I64, I64, I64, I, I, I, P, P, P, P]
@@ -173,6 +175,30 @@ def curvefp_quantize_mse(src: torch.Tensor, fmt, block_axis: int = 1, candidates
     st = lib().curvefp_quantize_mse(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), block_axis, f,
                                     block, candidates, codes.data_ptr(), scales.data_ptr(), _stream(stream))
     _check(st, "curvefp_quantize_mse")
+    return codes, scales
+
+
+def curvefp_quantize_tensorwise(src: torch.Tensor, fmt, block_axis: int = 1,
+                                codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
+                                workspace: Optional[torch.Tensor] = None,
+                                stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Q(X) with one scale for the whole tensor: codes as curvefp_quantize's, the scale repeated
+    once per output row (scales [outer], the rowwise layout: block = the blocked extent)."""
+    assert src.dim() == 2 and src.stride(1) == 1
+    rows, cols = src.shape
+    outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
+    f = _fmt(fmt)
+    if codes is None:
+        shape = (outer, k // 32, 28) if f == 2 else (outer, k)
+        codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
+    if scales is None:
+        scales = torch.empty((outer, 1), dtype=torch.int8, device=src.device)
+    if workspace is None:
+        workspace = torch.empty((1,), dtype=torch.int32, device=src.device)
+    st = lib().curvefp_quantize_tensorwise(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), block_axis,
+                                           f, codes.data_ptr(), scales.data_ptr(), workspace.data_ptr(),
+                                           _stream(stream))
+    _check(st, "curvefp_quantize_tensorwise")
     return codes, scales
 
 

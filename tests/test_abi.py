@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -333,3 +333,26 @@ def test_quantize_compact_validation(L):
     assert u(None, FAKE, 4, 4, 4, FAKE, None) == ENULL
     assert u(FAKE, FAKE, 4, 4, 1, FAKE, None) == EBLOCK
     assert u(FAKE, FAKE, 0, 4, 4, FAKE, None) == ESHAPE
+
+
+def test_quantize_tensorwise_validation(L):
+    q = L.curvefp_quantize_tensorwise
+    WS = FAKE
+    #       src   dt rows cols ld  axis fmt codes scales ws  stream
+    args = [FAKE, 0, 4, 64, 64, 1, 2, FAKE, FAKE, WS, None]
+    for i in (0, 7, 8, 9):
+        a = list(args); a[i] = None
+        assert q(*a) == ENULL, i
+    for i, v in ((1, 2), (6, 5)):
+        a = list(args); a[i] = v
+        assert q(*a) == EFMT, (i, v)
+    a = list(args); a[5] = 2
+    assert q(*a) == EBLOCK
+    for i, v in ((2, 0), (3, 40), (4, 32)):
+        a = list(args); a[i] = v
+        assert q(*a) == ESHAPE, (i, v)
+    a = list(args); a[5] = 0                     # blocked extent = rows = 4, not a multiple of 32
+    assert q(*a) == ESHAPE
+    for i, v in ((0, MIS), (7, MIS), (9, FAKE + 2)):
+        a = list(args); a[i] = v
+        assert q(*a) == EALIGN, (i, v)

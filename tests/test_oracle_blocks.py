@@ -228,3 +228,51 @@ def test_compact_offset_packing_layout():
         p = oracle.pack_offsets(d, S)
         assert p.shape == (3, (37 * S + 7) // 8)
         assert np.array_equal(oracle.unpack_offsets(p, 37, S), d)
+
+
+# ---------------------------------------------------------------- tensorwise scales
+
+@pytest.mark.parametrize("name", NAMES)
+def test_tensorwise_scale_is_largest_row_scale(name):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(80)
+    x = sample_input(rng, 9, 256)
+    x[3] = 0.0                                    # an all-zero row takes no part
+    c, s = oracle.quantize_tensorwise(x, f)
+    _, sr = oracle.quantize(x, f, 256)
+    live = np.abs(x).max(axis=1) > 0
+    assert s.shape == (9, 1) and np.all(s == s[0, 0])
+    assert int(s[0, 0]) == int(sr[live, 0].astype(np.int64).max())
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_tensorwise_codes_are_nearest_at_the_tensor_scale(name):
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(81)
+    x = sample_input(rng, 5, 512)
+    c, s = oracle.quantize_tensorwise(x, f)
+    a = int(s[0, 0])
+    for i in rng.choice(x.size, 300, replace=False):
+        r, k = divmod(int(i), 512)
+        assert int(c[r, k]) == rigorous_code(float(x[r, k]), a, f), (r, k)
+
+
+@pytest.mark.parametrize("name", NAMES)
+def test_tensorwise_equals_rowwise_when_rows_share_their_maximum(name):
+    """Rows scaled to the same largest magnitude: the tensor's scale is every row's."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(82)
+    x = rng.standard_normal((6, 128)).astype(np.float64)
+    x = x / np.abs(x).max(axis=1, keepdims=True) * 3.5
+    x = x.astype(np.float32)
+    c, s = oracle.quantize_tensorwise(x, f)
+    cr, sr = oracle.quantize(x, f, 128)
+    assert np.array_equal(c, cr) and np.array_equal(s, sr)
+
+
+def test_tensorwise_nonfinite_poisons_the_tensor():
+    f = oracle.get_format("E4C3")
+    x = np.ones((4, 64), np.float32)
+    x[2, 5] = np.inf
+    c, s = oracle.quantize_tensorwise(x, f)
+    assert np.all(s == oracle.POISON_SCALE) and not c.any()
