@@ -492,6 +492,24 @@ def static_scales(cf, w, tb, dev, stream, reps: int = 10):
         t = float(np.median(ts))
         out[name] = {"us": t * 1e6, "gbps": nbytes / t / 1e9}
     out["scales_moved_frac"] = float((sm != sc).float().mean().item())
+    # the same search over blocks of 64 (Sec. 4.2's PTQ setting), one thread per block of 64
+    cm64, sm64 = cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4, block=64)
+    fn64 = lambda: cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4, block=64,
+                                           codes=cm64, scales=sm64)
+    for _ in range(3):
+        fn64()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn64()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    t = float(np.median(ts))
+    nb64 = w.N * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - 1.0 / 32.0 + 1.0 / 64.0)
+    out["mse_search_G64"] = {"us": t * 1e6, "gbps": nb64 / t / 1e9}
     out["workload"] = f"{w.name} weight {w.N}x{w.K} {w.dtype} -> {w.fmt}, 4 candidate scales"
     out["timing"] = f"median of {reps} individually timed calls each"
     return out

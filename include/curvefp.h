@@ -27,8 +27,8 @@
  *     any positive multiple of 32 (32, 64, ..., 512 for the block sizes the
  *     paper sweeps; the blocked extent itself for rowwise scales), else
  *     CURVEFP_ERR_BLOCK.  The blocked extent must be a multiple of G
- *     (CURVEFP_ERR_SHAPE otherwise).  curvefp_quantize_mse takes G = 32 only,
- *     and curvefp_gemm_requant's output uses G = 32 whatever its inputs use.
+ *     (CURVEFP_ERR_SHAPE otherwise).  curvefp_gemm_requant's output uses G = 32
+ *     whatever its inputs use.
  *   - Code, output and (for blocks along rows) source pointers must be 16-byte
  *     aligned, and leading dimensions (in elements) must keep every row 16-byte
  *     aligned; the quantize-transpose source only needs element alignment.
@@ -135,9 +135,9 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
  * codes are reconstructed to fp32 exactly as curvefp_dequantize does, the squared errors
  * (x - x_hat)^2 are summed in fp64 over the block's 32 elements in index order, each
  * product and sum rounded once, and the first candidate in the order above with the least
- * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE; block must be 32, else
- * CURVEFP_ERR_BLOCK.  Zero blocks get scale 0 and non-finite blocks -128 with zero codes,
- * as in curvefp_quantize.
+ * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE.  Any block size of curvefp_quantize
+ * (the sums then run over the block's G elements in index order).  Zero blocks get scale 0 and
+ * non-finite blocks -128 with zero codes, as in curvefp_quantize.
  */
 int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
                          int block_axis, int format, int block, int candidates,

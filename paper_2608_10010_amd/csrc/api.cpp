@@ -175,10 +175,10 @@ int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols,
                          void* stream) {
     if (!src || !codes || !scales) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format) || (dtype != CURVEFP_F32 && dtype != CURVEFP_BF16)) return CURVEFP_ERR_FORMAT;
-    if (block != 32 || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
+    if (!block_ok(block) || (block_axis != 0 && block_axis != 1)) return CURVEFP_ERR_BLOCK;
     if (candidates < 1 || candidates > 8) return CURVEFP_ERR_SHAPE;
     if (rows <= 0 || cols <= 0 || ld_src < cols) return CURVEFP_ERR_SHAPE;
-    if ((block_axis == 1 ? cols : rows) % 32) return CURVEFP_ERR_SHAPE;
+    if ((block_axis == 1 ? cols : rows) % block) return CURVEFP_ERR_SHAPE;
     if (rows * cols / 32 / 256 >= ((int64_t)1 << 31)) return CURVEFP_ERR_SHAPE;
     const int esz = dtype == CURVEFP_F32 ? 4 : 2;
     if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
@@ -186,7 +186,8 @@ int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols,
     if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
-    return hip_status(launch_quantize_mse(src, dtype, rows, cols, ld_src, block_axis, format, candidates, codes, scales,
+    return hip_status(launch_quantize_mse(src, dtype, rows, cols, ld_src, block_axis, format, block, candidates, codes,
+                                          scales,
                                           reinterpret_cast<hipStream_t>(stream)));
 }
 

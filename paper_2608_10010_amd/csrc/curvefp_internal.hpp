@@ -99,7 +99,7 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 // static-operand scales: reconstruction-MSE search over `candidates` scales at or below the
 // ceil-absmax scale (and, for a level pattern spanning P > 1 octaves, the P - 1 above it)
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
-                               int axis, int format, int candidates, void* codes, int8_t* scales,
+                               int axis, int format, int block, int candidates, void* codes, int8_t* scales,
                                hipStream_t s);
 // one scale for the whole tensor, written once per output row; workspace: one 32-bit word
 hipError_t launch_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,

@@ -1086,12 +1086,168 @@ __global__ __launch_bounds__(256) void quantize_mse_kernel(
     scales[orow * nbr + oblk] = (int8_t)best_a;
 }
 
+// The same search for blocks of G > 32 elements (Sec. 4.2's PTQ weights use G64 and G512): one
+// thread per block streams it from memory three times (its maximum; every candidate's error
+// sum, element by element in index order; the codes at the winning scale, 32 at a time), so
+// only the candidates' sums stay in registers.  Blocks along rows are read 8 elements per
+// 16-byte load; blocks down the columns one element per load (consecutive threads take
+// consecutive columns).
+template <class F, bool BF16>
+__device__ __forceinline__ void mse_load8(const void* __restrict__ src, int axis, int64_t base, int64_t ld, int j,
+                                          uint32_t* mag, uint32_t& sgn8) {
+    sgn8 = 0;
+    if (axis == 1) {
+        const char* p = reinterpret_cast<const char*>(src) + (base + 8 * (int64_t)j) * (BF16 ? 2 : 4);
+        uint4 v[BF16 ? 1 : 2];
+#pragma unroll
+        for (int t = 0; t < (BF16 ? 1 : 2); t++) v[t] = ld16<false>(reinterpret_cast<const uint4*>(p) + t);
+        uint32_t sg[8];
+        unpack8<BF16>(v, mag, sg);
+#pragma unroll
+        for (int e = 0; e < 8; e++) sgn8 |= sg[e] << e;
+    } else {
+#pragma unroll
+        for (int e = 0; e < 8; e++) {
+            const int64_t idx = base + (8 * (int64_t)j + e) * ld;
+            const uint32_t w = BF16 ? ((uint32_t)reinterpret_cast<const uint16_t*>(src)[idx] << 16)
+                                    : reinterpret_cast<const uint32_t*>(src)[idx];
+            mag[e] = w & 0x7FFFFFFFu;
+            sgn8 |= (w >> 31) << e;
+        }
+    }
+}
+
+template <class F, bool BF16>
+__global__ __launch_bounds__(256) void quantize_mse_g_kernel(
+    const void* __restrict__ src, int64_t rows, int64_t cols, int64_t ld, int axis, int G, int candidates,
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int fidx) {
+    __shared__ uint32_t lut[F::QLUT_SIZE];
+    constexpr int RT = F::BINARY ? 8 : 128;
+    __shared__ uint32_t mant[RT];
+    __shared__ uint64_t sig[RT];
+    for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = g_qlut[fidx][i];
+    if (threadIdx.x < RT) {
+        mant[threadIdx.x] = g_qr_mant[fidx][threadIdx.x];
+        sig[threadIdx.x] = g_qr_sig[fidx][threadIdx.x];
+    }
+    const uint32_t lmax_mant = g_lmax_mant[fidx];
+    __syncthreads();
+    const int64_t k = axis == 1 ? cols : rows;                   // blocked extent
+    const int64_t nbr = k / G;                                    // blocks per output row
+    const int64_t nb = axis == 1 ? rows * nbr : cols * nbr;
+    const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (b >= nb) return;
+    int64_t orow, oblk, base;                                     // output row, block, first element
+    if (axis == 1) {
+        orow = b / nbr;
+        oblk = b - orow * nbr;
+        base = orow * ld + oblk * G;
+    } else {
+        oblk = b / cols;
+        orow = b - oblk * cols;                                   // the source column
+        base = oblk * G * ld + orow;
+    }
+    const int nch = G / 8;
+    uint32_t amax = 0;
+    for (int j = 0; j < nch; j++) {
+        uint32_t mag[8], sg;
+        mse_load8<F, BF16>(src, axis, base, ld, j, mag, sg);
+#pragma unroll
+        for (int e = 0; e < 8; e++) amax = max(amax, mag[e]);
+    }
+    const int ac = scale_of<F>(amax, lmax_mant);
+    const bool live = ac != -128 && amax != 0;
+    int best_a = ac;
+    if (live) {
+        const int nc = candidates + F::PERIOD - 1;
+        int acand[MSE_MAXC];
+        bool ok[MSE_MAXC];
+        double acc[MSE_MAXC];
+#pragma unroll
+        for (int c = 0; c < MSE_MAXC; c++) {
+            acand[c] = c < candidates ? ac - c : ac + (c - candidates + 1);
+            ok[c] = c < nc && acand[c] >= -127 && acand[c] <= 127;
+            acc[c] = 0.0;
+        }
+        for (int j = 0; j < nch; j++) {
+            uint32_t mag[8], sg;
+            mse_load8<F, BF16>(src, axis, base, ld, j, mag, sg);
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+                const uint32_t s = (sg >> e) & 1u;
+                const double x = f64_of_f32_bits(mag[e] | (s << 31));
+#pragma unroll
+                for (int c = 0; c < MSE_MAXC; c++)
+                    if (c < nc && ok[c])
+                        acc[c] = add_element_error<F>(acc[c], mag[e], s, x, acand[c], lut, mant, sig);
+            }
+        }
+        double best_err = acc[0];
+#pragma unroll
+        for (int c = 1; c < MSE_MAXC; c++)
+            if (c < nc && ok[c] && acc[c] < best_err) {
+                best_err = acc[c];
+                best_a = acand[c];
+            }
+    }
+    // codes, one group of 32 at a time
+    for (int grp = 0; grp < G / 32; grp++) {
+        uint32_t cc[32];
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            uint32_t mag[8], sg;
+            mse_load8<F, BF16>(src, axis, base, ld, 4 * grp + q, mag, sg);
+#pragma unroll
+            for (int e = 0; e < 8; e++) {
+                const uint32_t rk = live ? rank_at<F>(mag[e], best_a, lut) : 0u;
+                cc[8 * q + e] = rk | ((rk != 0 ? (sg >> e) & 1u : 0u) << F::EC);
+            }
+        }
+        const int64_t g32 = orow * (k / 32) + oblk * (G / 32) + grp;   // group of 32 in the output
+        if (!F::PACKED7) {
+            uint4* o = reinterpret_cast<uint4*>(codes + g32 * 32);
+#pragma unroll
+            for (int h = 0; h < 2; h++) {
+                uint32_t w4[4];
+#pragma unroll
+                for (int t = 0; t < 4; t++)
+                    w4[t] = cc[16 * h + 4 * t] | (cc[16 * h + 4 * t + 1] << 8) | (cc[16 * h + 4 * t + 2] << 16) |
+                            (cc[16 * h + 4 * t + 3] << 24);
+                o[h] = make_uint4(w4[0], w4[1], w4[2], w4[3]);
+            }
+        } else {
+            uint32_t wds[7] = {0, 0, 0, 0, 0, 0, 0};
+#pragma unroll
+            for (int i = 0; i < 32; i++) {
+                const int bit = 7 * i;
+                wds[bit >> 5] |= cc[i] << (bit & 31);
+                if ((bit & 31) > 25) wds[(bit >> 5) + 1] |= cc[i] >> (32 - (bit & 31));
+            }
+            uint32_t* o = reinterpret_cast<uint32_t*>(codes + g32 * 28);
+#pragma unroll
+            for (int t = 0; t < 7; t++) o[t] = wds[t];
+        }
+    }
+    scales[orow * nbr + oblk] = (int8_t)best_a;
+}
+
 template <class F>
 hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
-                          int candidates, int fidx, void* codes, int8_t* scales, hipStream_t s) {
+                          int block, int candidates, int fidx, void* codes, int8_t* scales, hipStream_t s) {
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    if (block > 32) {
+        const int64_t nbg = rows * cols / block;
+        const dim3 gg((unsigned)((nbg + 255) / 256));
+        if (dtype == 1)
+            hipLaunchKernelGGL((quantize_mse_g_kernel<F, true>), gg, dim3(256), 0, s, src, rows, cols, ld, axis, block,
+                               candidates, cp, scales, fidx);
+        else
+            hipLaunchKernelGGL((quantize_mse_g_kernel<F, false>), gg, dim3(256), 0, s, src, rows, cols, ld, axis, block,
+                               candidates, cp, scales, fidx);
+        return hipGetLastError();
+    }
     const int64_t nb = rows * cols / 32;
     const dim3 grid((unsigned)((nb + 255) / 256));
-    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
     if (dtype == 1)
         hipLaunchKernelGGL((quantize_mse_kernel<F, true>), grid, dim3(256), 0, s, src, rows, cols, ld, axis, candidates,
                            cp, scales, fidx);
@@ -1119,13 +1275,13 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 namespace curvefp {
 
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
-                               int format, int candidates, void* codes, int8_t* scales, hipStream_t s) {
+                               int format, int block, int candidates, void* codes, int8_t* scales, hipStream_t s) {
     switch (format) {
-        case 0: return launch_mse_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, candidates, 0, codes, scales, s);
-        case 1: return launch_mse_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, candidates, 1, codes, scales, s);
-        case 2: return launch_mse_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, candidates, 2, codes, scales, s);
-        case 3: return launch_mse_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, candidates, 3, codes, scales, s);
-        default: return launch_mse_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, candidates, 4, codes, scales, s);
+        case 0: return launch_mse_fmt<FmtE4C3>(src, dtype, rows, cols, ld, axis, block, candidates, 0, codes, scales, s);
+        case 1: return launch_mse_fmt<FmtE5C2>(src, dtype, rows, cols, ld, axis, block, candidates, 1, codes, scales, s);
+        case 2: return launch_mse_fmt<FmtE3C3>(src, dtype, rows, cols, ld, axis, block, candidates, 2, codes, scales, s);
+        case 3: return launch_mse_fmt<FmtE4C3R89>(src, dtype, rows, cols, ld, axis, block, candidates, 3, codes, scales, s);
+        default: return launch_mse_fmt<FmtE4C3R34>(src, dtype, rows, cols, ld, axis, block, candidates, 4, codes, scales, s);
     }
 }
 

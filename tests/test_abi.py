@@ -264,9 +264,11 @@ def test_quantize_mse_validation(L):
     for i, v in ((1, 2), (6, 5), (6, -1)):
         a = list(args); a[i] = v
         assert q(*a) == EFMT, (i, v)
-    for i, v in ((7, 64), (5, 2)):
+    for i, v in ((7, 48), (7, 0), (5, 2)):
         a = list(args); a[i] = v
         assert q(*a) == EBLOCK, (i, v)
+    a = list(args); a[7] = 64                      # cols % block
+    assert q(*a) == ESHAPE
     for i, v in ((8, 0), (8, 9), (2, 0), (3, 40), (4, 16)):
         a = list(args); a[i] = v
         assert q(*a) == ESHAPE, (i, v)

@@ -13,14 +13,14 @@ from tests.gpu_util import DEV, FMTS, layout_codes, say, to_dev
 pytestmark = pytest.mark.gpu
 
 
-def oracle_mse(x, fmt, axis, candidates):
+def oracle_mse(x, fmt, axis, candidates, block=32):
     f = oracle.get_format(fmt)
     if axis == 1:
-        return oracle.quantize_mse(x, f, candidates)
-    return oracle.quantize_mse_axis0(x, f, candidates)
+        return oracle.quantize_mse(x, f, candidates, block)
+    return oracle.quantize_mse_axis0(x, f, candidates, block)
 
 
-def run_and_compare(x, fmt, dtype, axis, candidates, what, ld_pad=0):
+def run_and_compare(x, fmt, dtype, axis, candidates, what, ld_pad=0, block=32):
     """Quantize x on the GPU and with the oracle (bf16 sources: the same bf16-rounded values)."""
     if dtype == "bf16":
         x = W.bf16_round(x)
@@ -29,9 +29,9 @@ def run_and_compare(x, fmt, dtype, axis, candidates, what, ld_pad=0):
         wide = torch.zeros((t.shape[0], t.shape[1] + ld_pad), dtype=t.dtype, device=DEV)
         wide[:, : t.shape[1]] = t
         t = wide[:, : x.shape[1]]
-    codes, scales = cf.curvefp_quantize_mse(t, fmt, block_axis=axis, candidates=candidates)
+    codes, scales = cf.curvefp_quantize_mse(t, fmt, block_axis=axis, candidates=candidates, block=block)
     torch.cuda.synchronize()
-    oc, osc = oracle_mse(x, fmt, axis, candidates)
+    oc, osc = oracle_mse(x, fmt, axis, candidates, block)
     got_c = codes.cpu().numpy().reshape(-1)
     exp_c = layout_codes(oc, fmt).reshape(-1)
     got_s = scales.cpu().numpy()
@@ -107,3 +107,21 @@ def test_inference_weight_full_size(fmt):
     gc = codes.cpu().numpy()[rows].reshape(len(rows), -1)
     assert np.array_equal(scales.cpu().numpy()[rows], osc)
     assert np.array_equal(gc, layout_codes(oc, fmt).reshape(len(rows), -1))
+
+
+@pytest.mark.parametrize("fmt", FMTS)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("axis,shape,G", [(1, (37, 1536), 64), (1, (21, 1536), 512), (1, (9, 1536), 96),
+                                          (0, (1536, 45), 64), (0, (1024, 40), 512), (1, (5, 1536), 1536)])
+def test_blocks_of_g(fmt, dtype, axis, shape, G):
+    """Static scales over blocks of G > 32 (Sec. 4.2's PTQ weights use G64 and G512): every
+    candidate's error summed over the block's G elements in index order."""
+    say(f"[quantize_mse] blocks of G={G} fmt={fmt} dtype={dtype} axis={axis} shape={shape}")
+    x = heavy(shape, shape[0] + G)
+    run_and_compare(x, fmt, dtype, axis, 4, f"{fmt} {dtype} axis={axis} {shape} G={G}", block=G)
+
+
+def test_inference_weight_g64():
+    """The first 512 rows of the inference weight (4096 columns, bf16) in E3C3 with G64."""
+    x = np.ascontiguousarray(W.get("inference").operand("b")[:512])
+    run_and_compare(x, "E3C3", "bf16", 1, 4, "inference weight G64", block=64)

@@ -276,3 +276,29 @@ def test_tensorwise_nonfinite_poisons_the_tensor():
     x[2, 5] = np.inf
     c, s = oracle.quantize_tensorwise(x, f)
     assert np.all(s == oracle.POISON_SCALE) and not c.any()
+
+
+# ---------------------------------------------------------------- static scales over blocks of G
+
+@pytest.mark.parametrize("name", NAMES)
+def test_mse_over_blocks_of_g_is_the_exact_argmin(name):
+    """Static-operand scales with G = 64 (Sec. 4.2's PTQ weights): the chosen scale minimizes the
+    exact squared error of the 64-element block over the candidates (exact Fractions of
+    rigorously reconstructed values, as for blocks of 32); an exact tie keeps the first tried."""
+    from fractions import Fraction
+    from tests.test_oracle_pins import _exact_block_error, _mse_blocks
+    f = oracle.get_format(name)
+    x = np.ascontiguousarray(_mse_blocks(31).reshape(-1, 64)[::2])     # two 32-blocks per row
+    offs = oracle.mse_candidates(f, 4)
+    codes, scales = oracle.quantize_mse(x, f, candidates=4, block=64)
+    _, s_ceil = oracle.quantize(x, f, 64)
+    for r in range(x.shape[0]):
+        ac = int(s_ceil[r, 0])
+        errs = {ac + u: e for u in offs if (e := _exact_block_error(x[r], ac + u, f)) is not None}
+        best = min(errs.values())
+        got = int(scales[r, 0])
+        assert errs[got] <= best * (1 + Fraction(1, 10 ** 12)), (r, got)
+        assert got == next(ac + u for u in offs if ac + u in errs and errs[ac + u] == errs[got])
+        # and the codes are the nearest levels at the chosen scale
+        for i in range(0, 64, 7):
+            assert int(codes[r, i]) == rigorous_code(float(x[r, i]), got, f), (r, i)
