@@ -428,36 +428,41 @@ def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 10):
     ofmt = "E3C3"
     ws = cf.gemm_workspace(w.M, w.N, w.K, dev)
     C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
-    oc = torch.empty((w.M, w.N // 32, 28), dtype=torch.uint8, device=dev)
-    os_ = torch.empty((w.M, w.N // 32), dtype=torch.int8, device=dev)
-    oc2, os2 = torch.empty_like(oc), torch.empty_like(os_)
-
-    def fused():
-        cf.curvefp_gemm_requant(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, ofmt, out_codes=oc, out_scales=os_,
-                                workspace=ws)
-
-    def two_step():
-        cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws)
-        cf.curvefp_quantize(C, ofmt, codes=oc2, scales=os2)
-
     out = {}
-    for name, fn in (("fused", fused), ("gemm_then_quantize", two_step)):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn()
-            e1.record(stream)
+    exact = True
+    # output blocks of 32, and of 64 (the activation block size of Sec. 4.2's G64 setting)
+    for G in (32, 64):
+        oc = torch.empty((w.M, w.N // 32, 28), dtype=torch.uint8, device=dev)
+        os_ = torch.empty((w.M, w.N // G), dtype=torch.int8, device=dev)
+        oc2, os2 = torch.empty_like(oc), torch.empty_like(os_)
+
+        def fused():
+            cf.curvefp_gemm_requant(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, ofmt, out_codes=oc, out_scales=os_,
+                                    workspace=ws, out_block=G)
+
+        def two_step():
+            cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws)
+            cf.curvefp_quantize(C, ofmt, block=G, codes=oc2, scales=os2)
+
+        for name, fn in (("fused", fused), ("gemm_then_quantize", two_step)):
+            for _ in range(3):
+                fn()
             torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e-3)
-        t = float(np.median(ts))
-        out[name] = {"us": t * 1e6, "tflops": w.flops() / t / 1e12}
-    torch.cuda.synchronize()
-    out["bit_exact"] = bool(torch.equal(oc, oc2) and torch.equal(os_, os2))
-    out["workload"] = f"{w.name}, output requantized to {ofmt} in blocks of 32 along its rows"
+            ts = []
+            for _ in range(reps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1) * 1e-3)
+            t = float(np.median(ts))
+            key = name if G == 32 else f"{name}_G{G}"
+            out[key] = {"us": t * 1e6, "tflops": w.flops() / t / 1e12}
+        torch.cuda.synchronize()
+        exact = exact and bool(torch.equal(oc, oc2) and torch.equal(os_, os2))
+    out["bit_exact"] = exact
+    out["workload"] = f"{w.name}, output requantized to {ofmt} in blocks of 32 (and of 64: *_G64) along its rows"
     out["timing"] = f"median of {reps} individually timed calls each"
     del ws, C
     return out

@@ -27,8 +27,8 @@
  *     any positive multiple of 32 (32, 64, ..., 512 for the block sizes the
  *     paper sweeps; the blocked extent itself for rowwise scales), else
  *     CURVEFP_ERR_BLOCK.  The blocked extent must be a multiple of G
- *     (CURVEFP_ERR_SHAPE otherwise).  curvefp_gemm_requant's output uses G = 32
- *     whatever its inputs use.
+ *     (CURVEFP_ERR_SHAPE otherwise).  curvefp_gemm_requant's output blocks are
+ *     chosen on their own (32, 64, 128 or 256).
  *   - Code, output and (for blocks along rows) source pointers must be 16-byte
  *     aligned, and leading dimensions (in elements) must keep every row 16-byte
  *     aligned; the quantize-transpose source only needs element alignment.
@@ -262,18 +262,20 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
  * The product of curvefp_gemm_ws (same operands, format, workspace and fp32 values), with
  * the output requantized in the GEMM's epilogue instead of stored as fp32: the explicit
  * output requantization of Sec. 3.2 (products are closed on widened coordinates; only the
- * requantization to a finite destination may saturate).  C is quantized in blocks of 32
- * consecutive outputs along each row into out_format with the rule of curvefp_quantize
- * (ceil-absmax scale, nearest level), so out_codes / out_scales equal curvefp_quantize
- * (block_axis = 1) of the fp32 C that curvefp_gemm_ws returns, bit for bit.
- *   out_codes [M][N] bytes (E3C3: [M][N/32][28]), out_scales [M][N/32].
- * N must be a multiple of 32 (CURVEFP_ERR_SHAPE otherwise); out_codes 16-byte aligned.
- * Other errors as curvefp_gemm_ws.
+ * requantization to a finite destination may saturate).  C is quantized in blocks of
+ * out_block consecutive outputs along each row into out_format with the rule of
+ * curvefp_quantize (ceil-absmax scale, nearest level), so out_codes / out_scales equal
+ * curvefp_quantize (block_axis = 1, block = out_block) of the fp32 C that curvefp_gemm_ws
+ * returns, bit for bit.
+ *   out_codes [M][N] bytes (E3C3: [M][N/32][28]), out_scales [M][N/out_block].
+ * out_block is 32, 64, 128 or 256 (an output block lies within one 256-column tile of the
+ * epilogue; CURVEFP_ERR_BLOCK otherwise); N must be a multiple of out_block
+ * (CURVEFP_ERR_SHAPE otherwise); out_codes 16-byte aligned.  Other errors as curvefp_gemm_ws.
  */
 int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales,
                          const void* b_codes, const int8_t* b_scales,
                          int64_t M, int64_t N, int64_t K, int format, int block, int out_format,
-                         void* out_codes, int8_t* out_scales,
+                         int out_block, void* out_codes, int8_t* out_scales,
                          void* workspace, int64_t workspace_bytes, void* stream);
 
 /*

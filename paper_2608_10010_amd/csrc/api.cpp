@@ -240,20 +240,24 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
 }
 
 int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void* b_codes, const int8_t* b_scales,
-                         int64_t M, int64_t N, int64_t K, int format, int block, int out_format, void* out_codes,
-                         int8_t* out_scales, void* workspace, int64_t workspace_bytes, void* stream) {
+                         int64_t M, int64_t N, int64_t K, int format, int block, int out_format, int out_block,
+                         void* out_codes, int8_t* out_scales, void* workspace, int64_t workspace_bytes,
+                         void* stream) {
     if (!a_codes || !a_scales || !b_codes || !b_scales || !out_codes || !out_scales || !workspace)
         return CURVEFP_ERR_NULL;
     if (!fmt_ok(format) || !fmt_ok(out_format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % block || N % 32) return CURVEFP_ERR_SHAPE;
+    // output blocks lie inside one 256-column tile of the epilogue
+    if (out_block != 32 && out_block != 64 && out_block != 128 && out_block != 256) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % block || N % out_block) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(out_codes)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
     int st = ensure_tables();
     if (st) return st;
     return hip_status(launch_gemm_requant(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, out_format,
-                                          out_codes, out_scales, workspace, reinterpret_cast<hipStream_t>(stream)));
+                                          out_block, out_codes, out_scales, workspace,
+                                          reinterpret_cast<hipStream_t>(stream)));
 }
 
 int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) {

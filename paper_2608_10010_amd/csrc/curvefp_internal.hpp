@@ -117,10 +117,10 @@ int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                           int64_t N, int64_t K, int format, int block, float* c, int64_t ldc, void* ws,
                           hipStream_t s);
-// curvefp_gemm_ws with C requantized in the epilogue (blocks of 32 along each output row)
+// curvefp_gemm_ws with C requantized in the epilogue (blocks of out_block <= 256 along each output row)
 hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
-                               int64_t K, int format, int block, int out_format, void* out_codes, int8_t* out_scales,
-                               void* ws, hipStream_t s);
+                               int64_t K, int format, int block, int out_format, int out_block, void* out_codes,
+                               int8_t* out_scales, void* ws, hipStream_t s);
 // mixed formats / reused forward operands (trans: codes of a [K][R] tensor, blocks along R)
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,

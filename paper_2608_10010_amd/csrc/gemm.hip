@@ -812,10 +812,11 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
 // The accumulators are only ever indexed by unrolled loop counters.
 struct ReqOut {
     uint8_t* codes;        // [M][N] bytes, or [M][N/32][28] for 7-bit codes
-    int8_t* scales;        // [M][N/32]
+    int8_t* scales;        // [M][N/G]
     QRule rule;
     int fmt;               // output format (table row)
     int packed7;
+    int glog;              // output blocks of G = 32 << glog elements along each row (G <= 256)
 };
 
 // float offset of (row, col) in a 64 x 256 fp32 slice: 16-byte chunks XOR-swizzled by row & 7,
@@ -870,12 +871,15 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
             }
         }
         __syncthreads();
-        // phase B: 64 rows x 8 blocks, two per thread (eight threads cover one row)
+        // phase B: 64 rows x 8 groups of 32, two per thread (eight adjacent lanes cover one row,
+        // so a block of G = 32 << glog is G/32 adjacent lanes)
         for (int bi = tid; bi < 64 * 8; bi += NTHREADS) {
             const int srow = bi >> 3, cb = bi & 7;
             const int64_t row = m0 + (srow >> 5) * WM + 32 * ti + (srow & 31);
             const int64_t blk = n0 / 32 + cb;
-            if (row >= M || blk >= nbr) continue;
+            // groups past M or N hold zeros; blocks never straddle N (N % G == 0), and every lane
+            // takes part in the block maximum before the invalid ones stop
+            const bool valid = row < M && blk < nbr;
             // pass 1: the block maximum; pass 2: each 16-byte chunk (re-read from LDS) quantized
             // and packed into the output words, so only one chunk is held at a time
             const float* rowp = slice + srow * 256;
@@ -889,6 +893,8 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
                 amax = max(max(amax, max(v.x & 0x7FFFFFFFu, v.y & 0x7FFFFFFFu)),
                            max(v.z & 0x7FFFFFFFu, v.w & 0x7FFFFFFFu));
             }
+            for (int o = 1; o < (1 << ro.glog); o <<= 1) amax = max(amax, (uint32_t)__shfl_xor((int)amax, o));
+            if (!valid) continue;
             const int a = qr_scale(amax, q);
             // the packing is chosen once per block, so each loop below is straight-line code and
             // its table lookups can be scheduled together
@@ -924,7 +930,7 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
             };
             if (ro.packed7) codes_of(std::true_type());
             else codes_of(std::false_type());
-            ro.scales[row * nbr + blk] = (int8_t)a;
+            if ((cb & ((1 << ro.glog) - 1)) == 0) ro.scales[row * (nbr >> ro.glog) + (blk >> ro.glog)] = (int8_t)a;
         }
         __syncthreads();                                         // the slice is free for the next ti
     }
@@ -1396,8 +1402,8 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
 // expansion launches, then gemm_ws_kernel<BIAS2, true>
 template <class F>
 hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
-                              int64_t N, int64_t K, int block, char* ws, int fidx, int ofmt, uint8_t* qc, int8_t* qs,
-                              hipStream_t s) {
+                              int64_t N, int64_t K, int block, char* ws, int fidx, int ofmt, int oblock, uint8_t* qc,
+                              int8_t* qs, hipStream_t s) {
     const WsLayout w = ws_layout(M, N, K);
     const int64_t nkb = K / 32, nsb = K / block;
     const Div32 dgq = make_div32((uint32_t)(block / 32));
@@ -1415,7 +1421,9 @@ hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, co
                        dim3(256), 0, s, opA, opB, nkb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    const ReqOut ro{qc, qs, g_qrule[ofmt], ofmt, ofmt == 2 ? 1 : 0};
+    int glog = 0;
+    while ((32 << glog) < oblock) glog++;
+    const ReqOut ro{qc, qs, g_qrule[ofmt], ofmt, ofmt == 2 ? 1 : 0, glog};
     const int64_t grid = (tiles * splits + 7) / 8 * 8;
     hipLaunchKernelGGL((gemm_ws_kernel<2 * F::GEMM_BIAS, true>), dim3((unsigned)grid), dim3(NTHREADS), 0, s,
                        ws + w.planes_a, ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, nullptr, N, splits,
@@ -1582,16 +1590,16 @@ int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) { return mixed_layout(M, N, K).bytes; }
 
 hipError_t launch_gemm_requant(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M, int64_t N,
-                               int64_t K, int format, int block, int out_format, void* out_codes, int8_t* out_scales,
-                               void* ws, hipStream_t s) {
+                               int64_t K, int format, int block, int out_format, int out_block, void* out_codes,
+                               int8_t* out_scales, void* ws, hipStream_t s) {
     char* w = reinterpret_cast<char*>(ws);
     uint8_t* qc = reinterpret_cast<uint8_t*>(out_codes);
     switch (format) {
-        case 0: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 0, out_format, qc, out_scales, s);
-        case 1: return launch_requant_fmt<FmtE5C2>(a, as, b, bs, M, N, K, block, w, 1, out_format, qc, out_scales, s);
-        case 2: return launch_requant_fmt<FmtE3C3>(a, as, b, bs, M, N, K, block, w, 2, out_format, qc, out_scales, s);
-        case 3: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 3, out_format, qc, out_scales, s);
-        default: return launch_requant_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, block, w, 4, out_format, qc, out_scales, s);
+        case 0: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 0, out_format, out_block, qc, out_scales, s);
+        case 1: return launch_requant_fmt<FmtE5C2>(a, as, b, bs, M, N, K, block, w, 1, out_format, out_block, qc, out_scales, s);
+        case 2: return launch_requant_fmt<FmtE3C3>(a, as, b, bs, M, N, K, block, w, 2, out_format, out_block, qc, out_scales, s);
+        case 3: return launch_requant_fmt<FmtE4C3>(a, as, b, bs, M, N, K, block, w, 3, out_format, out_block, qc, out_scales, s);
+        default: return launch_requant_fmt<FmtE4C3R34>(a, as, b, bs, M, N, K, block, w, 4, out_format, out_block, qc, out_scales, s);
     }
 }
 

@@ -73,7 +73,7 @@ def lib() -> ctypes.CDLL:
         L.curvefp_gemm_workspace_bytes.restype = I64
         L.curvefp_gemm_ws.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P, I64, P]
         L.curvefp_gemm_ws.restype = I
-        L.curvefp_gemm_requant.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, P, P, P, I64, P]
+        L.curvefp_gemm_requant.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, I, P, P, P, I64, P]
         L.curvefp_gemm_requant.restype = I
         L.curvefp_gemm_mixed_workspace_bytes.argtypes = [I64, I64, I64]
         L.curvefp_gemm_mixed_workspace_bytes.restype = I64
@@ -332,20 +332,22 @@ def curvefp_gemm_mixed(a_codes: torch.Tensor, a_scales: torch.Tensor, fmt_a, a_t
 def curvefp_gemm_requant(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.Tensor,
                          b_scales: torch.Tensor, M: int, N: int, K: int, fmt, out_fmt, block: int = 32,
                          out_codes: Optional[torch.Tensor] = None, out_scales: Optional[torch.Tensor] = None,
-                         workspace: Optional[torch.Tensor] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+                         workspace: Optional[torch.Tensor] = None, stream=None,
+                         out_block: int = 32) -> Tuple[torch.Tensor, torch.Tensor]:
     """curvefp_gemm_ws's product requantized in the epilogue: codes/scales of C in out_fmt,
-    blocks of 32 along each row (equal to curvefp_quantize of the fp32 C)."""
+    blocks of out_block (32, 64, 128 or 256) along each row (equal to curvefp_quantize of the
+    fp32 C with that block)."""
     fo = _fmt(out_fmt)
     if out_codes is None:
         shape = (M, N // 32, 28) if fo == 2 else (M, N)
         out_codes = torch.empty(shape, dtype=torch.uint8, device=a_codes.device)
     if out_scales is None:
-        out_scales = torch.empty((M, N // 32), dtype=torch.int8, device=a_codes.device)
+        out_scales = torch.empty((M, N // out_block), dtype=torch.int8, device=a_codes.device)
     if workspace is None:
         workspace = gemm_workspace(M, N, K, a_codes.device)
     st = lib().curvefp_gemm_requant(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
-                                    b_scales.data_ptr(), M, N, K, _fmt(fmt), block, fo, out_codes.data_ptr(),
-                                    out_scales.data_ptr(), workspace.data_ptr(),
+                                    b_scales.data_ptr(), M, N, K, _fmt(fmt), block, fo, out_block,
+                                    out_codes.data_ptr(), out_scales.data_ptr(), workspace.data_ptr(),
                                     workspace.numel() * workspace.element_size(), _stream(stream))
     _check(st, "curvefp_gemm_requant")
     return out_codes, out_scales

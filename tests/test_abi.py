@@ -283,25 +283,28 @@ def test_gemm_requant_validation(L):
     need = L.curvefp_gemm_workspace_bytes(64, 64, 64)
     WS = 1 << 24
     g = L.curvefp_gemm_requant
-    #       a     as    b     bs    M   N   K  fmt blk ofmt codes scales ws  bytes stream
-    args = [FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 32, 2, FAKE, FAKE, WS, need, None]
-    for i in (0, 1, 2, 3, 10, 11, 12):
+    #       a     as    b     bs    M   N   K  fmt blk ofmt oblk codes scales ws  bytes stream
+    args = [FAKE, FAKE, FAKE, FAKE, 64, 64, 64, 0, 32, 2, 32, FAKE, FAKE, WS, need, None]
+    for i in (0, 1, 2, 3, 11, 12, 13):
         a = list(args); a[i] = None
         assert g(*a) == ENULL, i
     for i, v in ((7, 5), (9, 5), (9, -1)):
         a = list(args); a[i] = v
         assert g(*a) == EFMT, (i, v)
-    a = list(args); a[8] = 48
-    assert g(*a) == EBLOCK
+    for i, v in ((8, 48), (10, 512), (10, 96), (10, 16)):
+        a = list(args); a[i] = v
+        assert g(*a) == EBLOCK, (i, v)
     a = list(args); a[8] = 128                       # the inputs' K % block
     assert g(*a) == ESHAPE
-    for i, v in ((4, 0), (5, 40), (6, 48), (13, need - 1)):
+    a = list(args); a[10] = 128                      # N % out_block
+    assert g(*a) == ESHAPE
+    for i, v in ((4, 0), (5, 40), (6, 48), (14, need - 1)):
         a = list(args); a[i] = v
         assert g(*a) == ESHAPE, (i, v)
-    for i in (0, 2, 10):
+    for i in (0, 2, 11):
         a = list(args); a[i] = MIS
         assert g(*a) == EALIGN, i
-    a = list(args); a[12] = WS + 64
+    a = list(args); a[13] = WS + 64
     assert g(*a) == EALIGN
 
 

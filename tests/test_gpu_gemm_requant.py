@@ -120,3 +120,24 @@ def test_inference_full_size(ofmt):
     qa, qb = quantized_operands(w.operand("a"), w.operand("b"), w.fmt, w.dtype)
     fused, ref, _ = fused_and_two_step(qa, qb, w.M, w.N, w.K, w.fmt, ofmt)
     same(fused, ref, f"inference -> {ofmt}")
+
+
+@pytest.mark.parametrize("ofmt", FMTS)
+@pytest.mark.parametrize("G,shape", [(64, (300, 576, 640)), (128, (200, 384, 1024)), (256, (130, 768, 512)),
+                                     (64, (2048, 4096, 4096)), (256, (4096, 4096, 128))])
+def test_output_blocks_of_g(ofmt, G, shape):
+    """Output blocks of 64, 128 and 256 (the next layer's activations at the paper's G64): equal
+    to curvefp_quantize of curvefp_gemm_ws's fp32 C with that block, bit for bit; ragged M, N a
+    multiple of G but not of 256, K split and not, and the full inference shape."""
+    M, N, K = shape
+    fmt = "E3C3"
+    A, B = sources(M, N, K, G + FMTS.index(ofmt))
+    say(f"[gemm_requant] out blocks of {G}: {fmt} -> {ofmt} M={M} N={N} K={K}")
+    qa, qb = quantized_operands(A, B, fmt)
+    ws = cf.gemm_workspace(M, N, K, DEV)
+    codes, scales = cf.curvefp_gemm_requant(qa[0], qa[1], qb[0], qb[1], M, N, K, fmt, ofmt, workspace=ws,
+                                            out_block=G)
+    C = cf.curvefp_gemm_ws(qa[0], qa[1], qb[0], qb[1], M, N, K, fmt, workspace=ws)
+    c2, s2 = cf.curvefp_quantize(C, ofmt, block=G)
+    torch.cuda.synchronize()
+    same((codes.cpu().numpy(), scales.cpu().numpy()), (c2.cpu().numpy(), s2.cpu().numpy()), f"G={G} -> {ofmt}")
