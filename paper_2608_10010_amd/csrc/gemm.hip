@@ -832,10 +832,14 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
                                              char* aux, const ReqOut& ro) {
     constexpr int BN = 256, WN = Tile<256>::WN, TN = Tile<256>::TN;
     float* slice = reinterpret_cast<float*>(slice_mem);          // 64 rows x 256 fp32 (64 KB)
-    uint32_t* qlut = reinterpret_cast<uint32_t*>(aux);           // the output format's table
+    // the output format's table behind one octave of rank-0 entries (base 0, threshold 0xFFFF):
+    // a magnitude scaled by ldexp lands in the pad or below it exactly when the quantizer's
+    // rule gives it rank 0, so the lookup needs no range tests
+    uint32_t* qlut = reinterpret_cast<uint32_t*>(aux);
     const QRule q = ro.rule;
     __syncthreads();                                             // every wave is done with the stages
-    for (int i = tid; i < q.qsize; i += NTHREADS) qlut[i] = g_gq_lut[ro.fmt][i];
+    for (int i = tid; i < q.qsize + 128; i += NTHREADS) qlut[i] = i < 128 ? 0xFFFFu : g_gq_lut[ro.fmt][i - 128];
+    const int ibase = (126 + q.oz) << 7, itop = q.qsize + 127;
     const __amdgpu_buffer_rsrc_t rq =
         __builtin_amdgcn_make_buffer_rsrc((void*)other_slot, (short)0, ADD ? (int)BM * BN * 4 : 0, 0x00020000);
     const int lrow = 4 * (lane >> 5);                            // row of the lane within a 32-row block
@@ -907,7 +911,12 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
                     const uint32_t b4[4] = {v.x, v.y, v.z, v.w};
 #pragma unroll
                     for (int j = 0; j < 4; j++) {
-                        const uint32_t rk = qr_rank(b4[j] & 0x7FFFFFFFu, a, qlut, q);
+                        // |x| 2^-a by v_ldexp_f32: exact wherever it can reach a nonzero level
+                        // (fp32 denormals are kept), below that it only needs to stay small
+                        const uint32_t yb = __builtin_bit_cast(
+                            uint32_t, __builtin_amdgcn_ldexpf(__builtin_bit_cast(float, b4[j] & 0x7FFFFFFFu), -a));
+                        const uint32_t e = qlut[min(max((int)(yb >> 16) - ibase, 0), itop)];
+                        const uint32_t rk = (e >> 16) + (((yb & 0xFFFFu) > (e & 0xFFFFu)) ? 1u : 0u);
                         const uint32_t code = rk | ((rk != 0 ? b4[j] >> 31 : 0u) << q.ec);
                         if (!P7) {
                             wd[c] |= code << (8 * j);
@@ -918,6 +927,10 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
                         }
                     }
                 }
+                // a block that held a NaN or an infinity (scale -128) keeps zero codes
+                const uint32_t keep = a == -128 ? 0u : ~0u;
+#pragma unroll
+                for (int t = 0; t < 8; t++) wd[t] &= keep;
                 if (!P7) {
                     uint4* dst = reinterpret_cast<uint4*>(ro.codes + row * N + 32 * blk);
                     dst[0] = make_uint4(wd[0], wd[1], wd[2], wd[3]);
