@@ -15,6 +15,9 @@ __device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
 constexpr int QP_XOR1 = 1 | (0 << 2) | (3 << 4) | (2 << 6);   // [1,0,3,2]
 constexpr int QP_XOR2 = 2 | (3 << 2) | (0 << 4) | (1 << 6);   // [2,3,0,1]
 constexpr int QP_NEXT = 1 | (2 << 2) | (3 << 4) | (3 << 6);   // [1,2,3,3]
+// lane i of each row of 16 reads lane 15 - i; of each half-row of 8, lane 7 - i
+constexpr int DPP_ROW_MIRROR = 0x140;
+constexpr int DPP_ROW_HALF_MIRROR = 0x141;
 
 __device__ __forceinline__ uint32_t quad_max_u32(uint32_t v) {
     v = max(v, dpp_u32<QP_XOR1>(v));

@@ -665,6 +665,9 @@ WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
     return w;
 }
 
+// rows of at most this many scales skip prep_kernel: the expansion scans them itself
+constexpr int64_t EXPAND_FOLD_MAX_SCALES = 128;
+
 // one launch before the expansion: row maxima of the block scales of A (workgroups
 // [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th of the row's nsb
 // scales; one more workgroup zeroes the per-tile arrival counters when K is split
@@ -700,7 +703,7 @@ struct ExpandOperand {
     const uint8_t* codes;
     const int8_t* scales;
     int64_t rows, tiles;      // rows, and row tiles of 256
-    const int* rmax;
+    int* rmax;                // row maxima: read, or written by the first K group when folded
     char* planes;
     int fidx;                 // format: which expansion table
     int64_t nsb;              // scales per row (K / G)
@@ -710,7 +713,12 @@ struct ExpandOperand {
 // both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B (F fixes the code
 // packing, which both share; each operand brings its own table)
 template <class F>
-__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb) {
+// fold != 0: no prep launch ran; every workgroup takes its rows' maxima itself (a quad of lanes
+// per row scans the row's scales), the first K group writes them for the GEMM's epilogue, and
+// workgroup (0, 0) clears the ncnt arrival counters.  Worth it while rows hold few scales: the
+// scan is repeated by every K group.
+__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb, int fold,
+                                                     int* __restrict__ cnt, int ncnt) {
     __shared__ uint32_t lut[GEMM_DEC_ENTRIES];
     const bool isA = (int64_t)blockIdx.x < 4 * opA.tiles;
     const ExpandOperand& op = isA ? opA : opB;
@@ -718,7 +726,7 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     const uint8_t* X = op.codes;
     const int8_t* Xs = op.scales;
     const int64_t R = op.rows, RT = op.tiles;
-    const int* rmax = op.rmax;
+    int* rmax = op.rmax;
     char* planes = op.planes;
     const int64_t row_bytes = F::PACKED7 ? nkb * 28 : nkb * 32;
     const int64_t r0 = (int64_t)(isA ? blockIdx.x : blockIdx.x - 4 * opA.tiles) * 64;
@@ -742,7 +750,30 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     for (int t = 0; t < 4; t++)
         load_raw<F>(rc, rs, voff_code, (int)((kbase + t) * (F::PACKED7 ? 28 : 32)), (x + sidx(kbase + t)) & ~3, 0, q,
                     raw[t]);
-    const int alpha = rmax[row];
+    int alpha;
+    if (fold) {
+        int m = -128;
+        if (row < R) {
+            // the row's scales are bytes [x, x + nsb) of rs: dword loads, a quad's lanes interleaved
+            const int lo = x, hi = x + (int)nsb;
+            for (int d = (lo >> 2) + q; d <= ((hi - 1) >> 2); d += 4) {
+                const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rs, 4 * d, 0, 0);
+#pragma unroll
+                for (int bb = 0; bb < 4; bb++) {
+                    const int pos = 4 * d + bb;
+                    if (pos >= lo && pos < hi) m = max(m, (int)(int8_t)(w >> (8 * bb)));
+                }
+            }
+        }
+        m = max(m, (int)dpp_u32<QP_XOR1>((uint32_t)m));
+        m = max(m, (int)dpp_u32<QP_XOR2>((uint32_t)m));
+        alpha = row < R ? m : 0;
+        if (blockIdx.y == 0 && q == 0) rmax[row] = alpha;      // the padded rows, as prep_kernel
+        if (blockIdx.x == 0 && blockIdx.y == 0)
+            for (int i = threadIdx.x; i < ncnt; i += 256) cnt[i] = 0;
+    } else {
+        alpha = rmax[row];
+    }
     __syncthreads();
 #pragma unroll
     for (int t = 0; t < 4; t++) {
@@ -1396,12 +1427,16 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     const int splits = w.splits;
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
-    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
-                       nsb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
+    // rows with few scales: the expansion takes the row maxima itself (one launch fewer)
+    const int fold = nsb <= EXPAND_FOLD_MAX_SCALES ? 1 : 0;
+    const int ncnt = splits > 1 ? (int)tiles : 0;
+    if (!fold)
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M,
+                           N, nsb, ga, gb, maxA, maxB, cnt, ncnt);
     const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
     const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
-                       dim3(256), 0, s, opA, opB, nkb);
+                       dim3(256), 0, s, opA, opB, nkb, fold, cnt, fold ? ncnt : 0);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t items = w.rta * w.rtb * splits;
@@ -1426,12 +1461,16 @@ hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, co
     const int splits = w.splits;
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
-    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
-                       nsb, ga, gb, maxA, maxB, cnt, (int)(splits > 1 ? tiles : 0));
+    // rows with few scales: the expansion takes the row maxima itself (one launch fewer)
+    const int fold = nsb <= EXPAND_FOLD_MAX_SCALES ? 1 : 0;
+    const int ncnt = splits > 1 ? (int)tiles : 0;
+    if (!fold)
+        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M,
+                           N, nsb, ga, gb, maxA, maxB, cnt, ncnt);
     const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
     const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
-                       dim3(256), 0, s, opA, opB, nkb);
+                       dim3(256), 0, s, opA, opB, nkb, fold, cnt, fold ? ncnt : 0);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int glog = 0;
@@ -1528,8 +1567,8 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
                                N / block, dgq};
     auto expand_k = [&](const ExpandOperand& o1, const ExpandOperand& o2, bool p7) {
         const dim3 grid((unsigned)(4 * (o1.tiles + o2.tiles)), (unsigned)((nkb + 3) / 4));
-        if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb);
-        else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, o1, o2, nkb);
+        if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb, 0, nullptr, 0);
+        else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, o1, o2, nkb, 0, nullptr, 0);
         return hipGetLastError();
     };
     auto expand_t = [&](const ExpandTOperand& o1, const ExpandTOperand& o2, bool p7) {

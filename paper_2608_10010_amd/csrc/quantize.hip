@@ -152,10 +152,14 @@ __device__ __forceinline__ void unpack8(const uint4* v, uint32_t* mag, uint32_t*
     }
 }
 
-// the maximum over the 2^lgl lanes (lgl in 2..6, aligned groups) that hold one block
+// the maximum over the 2^lgl lanes (lgl in 2..6, aligned groups, all active) that hold one
+// block: DPP within 16 lanes (after the quad maximum, a half-row mirror pairs each lane with
+// one of the other quad, a row mirror with one of the other half), shuffles beyond
 __device__ __forceinline__ uint32_t group_max_u32(uint32_t v, int lgl) {
     v = quad_max_u32(v);
-    for (int o = 4; o < (1 << lgl); o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
+    if (lgl >= 3) v = max(v, dpp_u32<DPP_ROW_HALF_MIRROR>(v));
+    if (lgl >= 4) v = max(v, dpp_u32<DPP_ROW_MIRROR>(v));
+    for (int o = 16; o < (1 << lgl); o <<= 1) v = max(v, (uint32_t)__shfl_xor((int)v, o));
     return v;
 }
 
