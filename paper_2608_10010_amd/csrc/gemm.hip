@@ -835,11 +835,13 @@ __device__ __forceinline__ WorkItem work_item(int tiles_y, int tiles_x, int spli
 // ---------------------------------------------------------------------------------------------
 // Output requantization (Sec. 3.2: products are closed on widened coordinates; only the explicit
 // requantization to a finite destination may saturate).  The tile's fp32 values, exactly those
-// store_tile would write, are quantized in blocks of 32 along each output row by the quantizer's
-// rule (codec.hpp), so the codes equal curvefp_quantize of curvefp_gemm_ws's C bit for bit.  The
-// tile goes through LDS (the freed stages) in four slices of 64 rows: every wave writes its fp32
-// values of the slice (the 32 rows ti of both wave rows), then each thread quantizes two blocks
-// of 32 of the slice and stores their codes (32 contiguous bytes, or 28 packed) and scales.
+// store_tile would write, are quantized in blocks of G (32, 64, 128 or 256) along each output row
+// by the quantizer's rule (codec.hpp), so the codes equal curvefp_quantize of curvefp_gemm_ws's C
+// with that block, bit for bit.  The tile goes through LDS (the freed stages) in four slices of
+// 64 rows: every wave writes its fp32 values of the slice (the 32 rows ti of both wave rows),
+// then each thread quantizes two groups of 32 of the slice (a block's G/32 groups sit in
+// adjacent lanes and share its maximum) and stores their codes (32 contiguous bytes, or 28
+// packed) and the block's scale.
 // The accumulators are only ever indexed by unrolled loop counters.
 struct ReqOut {
     uint8_t* codes;        // [M][N] bytes, or [M][N/32][28] for 7-bit codes

@@ -466,7 +466,8 @@ hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, 
 
 // quantize-transpose through LDS: a workgroup takes 128 rows (four blocks) x 64 columns.  The
 // tile is read with 16-byte loads along the source rows, each thread then quantizes one
-// column's block of 32 from LDS (a wave reads one contiguous row segment per step), and the
+// column's group of 32 from LDS (a wave reads one contiguous row segment per step; for blocks
+// of G > 32 rows the scale pass has written the block scales), and the
 // codes go back through LDS so every column's 128 code bytes (112 for E3C3) leave as whole
 // 16-byte stores.  Needs rows % 128 == 0, cols % 8 == 0 and a 16-byte aligned source.
 constexpr int TT_ROWS = 128, TT_COLS = 64;
@@ -903,12 +904,11 @@ hipError_t launch_compact_fmt(const void* src, int dtype, int64_t rows, int64_t 
 
 // ---------------------------------------------------------------------------------------------
 // Static-operand scales (Sec. 3.1: static operands choose a representable power-of-two scale by
-// reconstruction-MSE search).  One thread per block of 32: the block is quantized at each
+// reconstruction-MSE search).  One thread per block (of 32 here; larger blocks below): the block is quantized at each
 // candidate scale a_c + u (a_c ceil-absmax; u = 0, -1, .., -(candidates - 1), then 1 .. P - 1
 // when the level pattern spans P > 1 octaves), each element reconstructed to fp32 exactly as the
 // dequantizer does, and the squared error summed in fp64 in index order; the first candidate
-// with the least error wins.  Offline work for weights: simple and compute-light (a few hundred
-// fp64 operations per block).
+// with the least error wins.  Offline work for weights, run once per tensor.
 
 // fp32 bits -> the same value in fp64, exactly, without the fp32 denormal mode's say
 __device__ __forceinline__ double f64_of_f32_bits(uint32_t b) {

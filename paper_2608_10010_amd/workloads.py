@@ -7,7 +7,8 @@ distributions named for it, from ``numpy.random.default_rng(seed)`` in float64,
 rounded to float32 and then, for bf16 sources, to bfloat16 with
 round-to-nearest-even.  The same bytes feed both sides.
 
-GEMM convention: C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T, blocks of 32 along K.
+GEMM convention: C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T, blocks along K (32 unless a
+test or measurement names another size).
 An operand stored with K along its rows (e.g. a weight held as K x N) is
 quantized with ``axis=0`` (quantize-transpose).
 """
