@@ -140,7 +140,9 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
     for kind in CALL_KERNELS[path] + ("copy",):
         vals = [v for (k, _), v in per.items() if k == kind]
         if not vals:
-            if kind == "zero_rows_kernel":      # launched only when K is split
+            # zero_rows_kernel runs only when K is split; prep_kernel only when rows hold more
+            # than 128 scales (otherwise the expansion takes the row maxima itself)
+            if kind in ("zero_rows_kernel", "prep_kernel"):
                 out[kind] = (0.0, 0)
                 continue
             raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
@@ -266,6 +268,8 @@ def summarize_pmc(args):
         "|---|---|---|---|",
     ]
     for k in kernels:
+        if fetch[k][1] == 0:
+            continue                           # not launched by this call
         lines.append(f"| `{k}` | {fetch[k][1]} | {fetch[k][0]:.1f} | {write[k][0]:.1f} |")
     lines += [
         f"| one GEMM call (sum) | {fetch['gemm'][1]} | {fetch['gemm'][0]:.1f} | {write['gemm'][0]:.1f} |",
