@@ -744,7 +744,8 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "gemm call (" + ", ".join(CALL_KERNELS[args.gemm]) + ")",
+            "kernel": ("gemm call (expand_kernel, gemm_ws_kernel; prep_kernel first when rows hold more "
+                       "than 128 scales)" if args.gemm == "ws" else "gemm call (" + ", ".join(CALL_KERNELS["fused"]) + ")"),
             "achieved": gemm_tflops,
             "peak": F16_DENSE_PEAK_TFLOPS,
             "unit": "TFLOP/s",
