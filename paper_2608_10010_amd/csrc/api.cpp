@@ -1,8 +1,8 @@
-// C ABI of libcurvefp: argument validation, per-device table upload, dispatch.
+// C ABI of libcurvefp: argument validation and dispatch.
 // Validation runs before any HIP call, so every argument error is reported
-// without touching the device.
-#include <mutex>
-#include <vector>
+// without touching the device.  The library keeps no state: its constant tables
+// are compile-time __constant__ arrays of the kernel files, and a call does
+// nothing but validate its arguments and launch on the caller's stream.
 
 #include "../../include/curvefp.h"
 #include "curvefp_internal.hpp"
@@ -32,33 +32,6 @@ int gcd_i(int a, int b) {
     return a;
 }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-std::mutex g_mu;
-std::vector<char> g_ready;   // per device: tables uploaded
-AllTables* g_tables = nullptr;
-bool g_tables_bad = false;
-
-int ensure_tables() {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return CURVEFP_ERR_HIP;
-    std::lock_guard<std::mutex> lk(g_mu);
-    if ((int)g_ready.size() > dev && g_ready[dev]) return CURVEFP_OK;
-    if (g_tables_bad) return CURVEFP_ERR_HIP;
-    if (!g_tables) {
-        g_tables = new AllTables();
-        if (!build_tables(g_tables)) {
-            g_tables_bad = true;
-            return CURVEFP_ERR_HIP;
-        }
-    }
-    if (quantize_upload(*g_tables) != hipSuccess || dequantize_upload(*g_tables) != hipSuccess ||
-        gemm_upload(*g_tables) != hipSuccess)
-        return CURVEFP_ERR_HIP;
-    if (hipDeviceSynchronize() != hipSuccess) return CURVEFP_ERR_HIP;
-    if ((int)g_ready.size() <= dev) g_ready.resize(dev + 1, 0);
-    g_ready[dev] = 1;
-    return CURVEFP_OK;
-}
 
 int hip_status(hipError_t e) { return e == hipSuccess ? CURVEFP_OK : CURVEFP_ERR_HIP; }
 
@@ -97,8 +70,6 @@ int64_t curvefp_scales_count(int64_t outer, int64_t k, int block) {
     return outer * (k / block);
 }
 
-int curvefp_init(void) { return ensure_tables(); }
-
 int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
                      int block_axis, int format, int block, void* codes, int8_t* scales,
                      void* stream) {
@@ -112,8 +83,6 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
     if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_quantize(src, dtype, rows, cols, ld_src, block_axis, format, block, codes, scales,
                                       reinterpret_cast<hipStream_t>(stream)));
 }
@@ -131,8 +100,6 @@ int curvefp_quantize_tensorwise(const void* src, int dtype, int64_t rows, int64_
     if (!aligned16(codes) || (reinterpret_cast<uintptr_t>(workspace) & 3)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_quantize_tensorwise(src, dtype, rows, cols, ld_src, block_axis, format, codes, scales,
                                                  workspace, reinterpret_cast<hipStream_t>(stream)));
 }
@@ -153,8 +120,6 @@ int curvefp_quantize_compact(const void* src, int dtype, int64_t rows, int64_t c
     if (cols > 131072 || rows > 0x7FFFFFFF) return CURVEFP_ERR_SHAPE;   // one workgroup per row
     const int esz = dtype == CURVEFP_F32 ? 4 : 2;
     if (!aligned16(codes) || !aligned16(src) || (ld_src * esz) % 16) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_quantize_compact(src, dtype, rows, cols, ld_src, format, block, scale_bits, codes,
                                               row_ref, offsets, reinterpret_cast<hipStream_t>(stream)));
 }
@@ -164,8 +129,6 @@ int curvefp_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t
     if (!row_ref || !offsets || !scales) return CURVEFP_ERR_NULL;
     if (scale_bits < 2 || scale_bits > 8) return CURVEFP_ERR_BLOCK;
     if (rows <= 0 || nblocks <= 0 || rows * nblocks >= ((int64_t)1 << 39)) return CURVEFP_ERR_SHAPE;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_scales_unpack(row_ref, offsets, rows, nblocks, scale_bits, scales,
                                            reinterpret_cast<hipStream_t>(stream)));
 }
@@ -184,8 +147,6 @@ int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols,
     if (!aligned16(codes)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 1 && (!aligned16(src) || (ld_src * esz) % 16)) return CURVEFP_ERR_ALIGN;
     if (block_axis == 0 && (reinterpret_cast<uintptr_t>(src) % esz)) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_quantize_mse(src, dtype, rows, cols, ld_src, block_axis, format, block, candidates, codes,
                                           scales,
                                           reinterpret_cast<hipStream_t>(stream)));
@@ -198,8 +159,6 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format, int6
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
     if (outer <= 0 || k <= 0 || k % block || ld_dst < k) return CURVEFP_ERR_SHAPE;
     if (!aligned16(codes) || !aligned16(dst) || (ld_dst * 4) % 16) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_dequantize(codes, scales, format, outer, k, block, dst, ld_dst,
                                         reinterpret_cast<hipStream_t>(stream)));
 }
@@ -212,8 +171,6 @@ int curvefp_gemm(const void* a_codes, const int8_t* a_scales, const void* b_code
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
     if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_gemm(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc,
                                   reinterpret_cast<hipStream_t>(stream)));
 }
@@ -233,8 +190,6 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_gemm_ws(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc, workspace,
                                      reinterpret_cast<hipStream_t>(stream)));
 }
@@ -253,8 +208,6 @@ int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(out_codes)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_gemm_requant(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, out_format,
                                           out_block, out_codes, out_scales, workspace,
                                           reinterpret_cast<hipStream_t>(stream)));
@@ -282,8 +235,6 @@ int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format
     if (workspace_bytes < gemm_mixed_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
-    int st = ensure_tables();
-    if (st) return st;
     return hip_status(launch_gemm_mixed(a_codes, a_scales, a_format, a_trans, b_codes, b_scales, b_format, b_trans,
                                         M, N, K, block, c, ldc, workspace, reinterpret_cast<hipStream_t>(stream)));
 }
@@ -297,7 +248,7 @@ const char* curvefp_status_string(int status) {
         case CURVEFP_ERR_FORMAT: return "unknown format or dtype";
         case CURVEFP_ERR_BLOCK: return "unsupported block size, block axis or scale width";
         case CURVEFP_ERR_ALIGN: return "pointer or row not 16-byte aligned";
-        case CURVEFP_ERR_HIP: return "HIP error (launch, device query or table upload)";
+        case CURVEFP_ERR_HIP: return "HIP error (kernel launch)";
         default: return "unknown status";
     }
 }

@@ -10,36 +10,18 @@
 #include "curvefp_internal.hpp"
 #include "codec.hpp"
 #include "device_util.hpp"
+#include "curvefp_tables.inc"
 
 #include <cstring>
 
 namespace curvefp {
 
-__device__ uint32_t g_mant[NUM_FORMATS][8];
-__device__ uint64_t g_sig62[NUM_FORMATS][8];
+// compile-time tables (curvefp_tables.inc, written at build time by gen_tables)
+__constant__ uint32_t g_mant[NUM_FORMATS][8] = CURVEFP_MANT_INIT;
+__constant__ uint64_t g_sig62[NUM_FORMATS][8] = CURVEFP_SIG62_INIT;
 // rational radix: per magnitude rank, (w << 24) | mantissa of fl32(2^{f/N}) and floor(2^{f/N} 2^62)
-__device__ uint32_t g_dq_em[NUM_FORMATS][128];
-__device__ uint64_t g_dq_sig62[NUM_FORMATS][128];
-
-hipError_t dequantize_upload(const AllTables& t) {
-    uint32_t m[NUM_FORMATS][8];
-    uint64_t s[NUM_FORMATS][8];
-    static uint32_t em[NUM_FORMATS][128];
-    static uint64_t s62[NUM_FORMATS][128];
-    for (int f = 0; f < NUM_FORMATS; f++) {
-        memcpy(m[f], t.f[f].mant, sizeof(m[f]));
-        memcpy(s[f], t.f[f].sig62, sizeof(s[f]));
-        memcpy(em[f], t.f[f].dq_em, sizeof(em[f]));
-        memcpy(s62[f], t.f[f].dq_sig62, sizeof(s62[f]));
-    }
-    hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_mant), m, sizeof(m));
-    if (e != hipSuccess) return e;
-    e = hipMemcpyToSymbol(HIP_SYMBOL(g_sig62), s, sizeof(s));
-    if (e != hipSuccess) return e;
-    e = hipMemcpyToSymbol(HIP_SYMBOL(g_dq_em), em, sizeof(em));
-    if (e != hipSuccess) return e;
-    return hipMemcpyToSymbol(HIP_SYMBOL(g_dq_sig62), s62, sizeof(s62));
-}
+__constant__ uint32_t g_dq_em[NUM_FORMATS][128] = CURVEFP_DQ_EM_INIT;
+__constant__ uint64_t g_dq_sig62[NUM_FORMATS][128] = CURVEFP_DQ_SIG62_INIT;
 
 namespace {
 

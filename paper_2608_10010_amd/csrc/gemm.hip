@@ -36,34 +36,31 @@
 #include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
+#include "curvefp_tables.inc"
 
 #include <cstring>
 #include <type_traits>
 
 namespace curvefp {
 
-__device__ uint32_t g_dec[NUM_FORMATS][GEMM_DEC_ENTRIES];
+// compile-time tables (curvefp_tables.inc, written at build time by gen_tables)
+__constant__ uint32_t g_dec[NUM_FORMATS][GEMM_DEC_ENTRIES] = CURVEFP_DEC_INIT;
 // output requantization: the quantize tables of every format (the quantizer's, quantize.hip)
-__device__ uint32_t g_gq_lut[NUM_FORMATS][QLUT_MAX];
-// and the constants of its rule, kept on the host for the launch (the same on every device)
-static QRule g_qrule[NUM_FORMATS];
+__constant__ uint32_t g_gq_lut[NUM_FORMATS][QLUT_MAX] = CURVEFP_QLUT_INIT;
 
-hipError_t gemm_upload(const AllTables& t) {
-    static uint32_t q[NUM_FORMATS][QLUT_MAX];
-    for (int f = 0; f < NUM_FORMATS; f++) memcpy(q[f], t.f[f].qlut, sizeof(q[f]));
-    const int oz[NUM_FORMATS] = {FmtE4C3::OZ, FmtE5C2::OZ, FmtE3C3::OZ, FmtE4C3R89::OZ, FmtE4C3R34::OZ};
-    const int ohi[NUM_FORMATS] = {FmtE4C3::OHI, FmtE5C2::OHI, FmtE3C3::OHI, FmtE4C3R89::OHI, FmtE4C3R34::OHI};
-    const int ec[NUM_FORMATS] = {FmtE4C3::EC, FmtE5C2::EC, FmtE3C3::EC, FmtE4C3R89::EC, FmtE4C3R34::EC};
-    for (int f = 0; f < NUM_FORMATS; f++) {
-        if (t.f[f].qlut_size != (ohi[f] - oz[f] + 1) * 128) return hipErrorInvalidValue;
-        g_qrule[f] = QRule{oz[f], ohi[f], t.f[f].qlut_size, ec[f], t.f[f].lmax_mant};
-    }
-    hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_gq_lut), q, sizeof(q));
-    if (e != hipSuccess) return e;
-    uint32_t h[NUM_FORMATS][GEMM_DEC_ENTRIES];
-    for (int f = 0; f < NUM_FORMATS; f++) memcpy(h[f], t.f[f].dec, sizeof(h[f]));
-    return hipMemcpyToSymbol(HIP_SYMBOL(g_dec), h, sizeof(h));
+// the output quantizer's rule per format, for the launch
+constexpr uint32_t kLmaxMant[NUM_FORMATS] = CURVEFP_LMAX_MANT_INIT;
+constexpr int kQlutSize[NUM_FORMATS] = CURVEFP_QLUT_SIZE_INIT;
+constexpr int kOz[NUM_FORMATS] = {FmtE4C3::OZ, FmtE5C2::OZ, FmtE3C3::OZ, FmtE4C3R89::OZ, FmtE4C3R34::OZ};
+constexpr int kOhi[NUM_FORMATS] = {FmtE4C3::OHI, FmtE5C2::OHI, FmtE3C3::OHI, FmtE4C3R89::OHI, FmtE4C3R34::OHI};
+constexpr int kEc[NUM_FORMATS] = {FmtE4C3::EC, FmtE5C2::EC, FmtE3C3::EC, FmtE4C3R89::EC, FmtE4C3R34::EC};
+constexpr bool qlut_sizes_ok() {
+    for (int f = 0; f < NUM_FORMATS; f++)
+        if (kQlutSize[f] != (kOhi[f] - kOz[f] + 1) * 128) return false;
+    return true;
 }
+static_assert(qlut_sizes_ok(), "generated quantizer tables match the formats' octave ranges");
+constexpr QRule qrule(int f) { return QRule{kOz[f], kOhi[f], kQlutSize[f], kEc[f], kLmaxMant[f]}; }
 
 namespace {
 
@@ -1477,7 +1474,7 @@ hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, co
     if (e != hipSuccess) return e;
     int glog = 0;
     while ((32 << glog) < oblock) glog++;
-    const ReqOut ro{qc, qs, g_qrule[ofmt], ofmt, ofmt == 2 ? 1 : 0, glog};
+    const ReqOut ro{qc, qs, qrule(ofmt), ofmt, ofmt == 2 ? 1 : 0, glog};
     const int64_t grid = (tiles * splits + 7) / 8 * 8;
     hipLaunchKernelGGL((gemm_ws_kernel<2 * F::GEMM_BIAS, true>), dim3((unsigned)grid), dim3(NTHREADS), 0, s,
                        ws + w.planes_a, ws + w.planes_b, maxA, maxB, M, N, K, w.rta, w.rtb, nullptr, N, splits,

@@ -1,4 +1,4 @@
-// Host construction of libcurvefp's constant tables.
+// Host construction of libcurvefp's constant tables (run at build time by gen_tables.cpp).
 //
 // All irrational constants 2^{r/N} come from x87 80-bit exp2l (64-bit
 // significand).  Every integer decision taken from them (a threshold floor, a
@@ -22,7 +22,7 @@
 #include <cstdio>
 #include <cstring>
 
-#include "curvefp_internal.hpp"
+#include "tables.hpp"
 
 namespace curvefp {
 namespace {
@@ -201,6 +201,14 @@ bool build_format(int E, int C, int P, int Q, FormatTables* ft) {
     }
     // fl32 of the top level: the ceil-absmax comparison value (its exponent is ohi)
     ft->lmax_mant = ft->dq_em[(1 << EC) - 1] & 0x7FFFFFu;
+    ft->npoints = r.nmid;
+    for (int i = 0; i < r.nmid; i++) {
+        ft->point_o[i] = r.mid[i].o;
+        ft->point_T[i] = r.mid[i].T;
+    }
+    ft->zero_o = r.zero.o;
+    ft->zero_T = r.zero.T;
+    ft->zero_exact = r.zero.exact ? 1 : 0;
     if ((int)((int32_t)ft->dq_em[(1 << EC) - 1] >> 24) != ohi) return false;
     // GEMM expansion pairs: value (-1)^s 2^{w + bias} 2^{f/N}, bias = 15 - ohi (the row's top
     // element lands near 2^15), hi = RN16(v), lo = RN16(v - hi)
