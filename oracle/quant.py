@@ -12,7 +12,8 @@ Readings taken where the paper is silent (each is listed in the design doc):
 * ceil-absmax: a_b is the smallest integer a with amax <= 2^a * fl32(L_max),
   L_max = r^{n_max/K} the largest positive level.  fl32(L_max) is the value the
   top code actually reconstructs to, so a block that holds its own top code
-  keeps its scale (quantize(dequantize(c)) == c).  All-zero block -> a_b = 0.
+  keeps its scale (quantize(dequantize(c)) == c).  All-zero block: every integer
+  satisfies the inequality, so a_b is the bottom of the stored range, -127.
   a_b is stored as int8, clamped to [-127, 127].
 * non-finite inputs: a block holding NaN or +-Inf gets scale -128 and all-zero
   codes; it reconstructs to NaN.
@@ -73,8 +74,9 @@ def scale_exponents(amax: np.ndarray, fmt: Format) -> np.ndarray:
     """Ceil-absmax block scale: smallest integer a with amax <= 2^a * fl32(L_max).
 
     ``amax`` holds the block maxima of |x| in float64 (exact copies of fp32
-    values).  Zero blocks get 0, non-finite blocks get POISON_SCALE, the rest is
-    clamped to [-127, 127].  Returns int64.
+    values).  Zero blocks get SCALE_MIN (every a satisfies 0 <= 2^a fl32(L_max); the
+    smallest stored one), non-finite blocks get POISON_SCALE, the rest is clamped to
+    [-127, 127].  Returns int64.
     """
     amax = np.asarray(amax, dtype=np.float64)
     lm = top_level_fp32(fmt)
@@ -88,7 +90,7 @@ def scale_exponents(amax: np.ndarray, fmt: Format) -> np.ndarray:
         a = np.where(safe <= np.ldexp(lm, a - 1), a - 1, a)
     assert np.all(safe[pos] <= np.ldexp(lm, a[pos]))
     assert np.all(safe[pos] > np.ldexp(lm, a[pos] - 1))
-    a = np.where(pos, a, 0)
+    a = np.where(pos, a, SCALE_MIN)
     a = np.clip(a, SCALE_MIN, SCALE_MAX)
     a = np.where(finite, a, POISON_SCALE)
     return a.astype(np.int64)
@@ -192,8 +194,8 @@ def quantize_mse(x: np.ndarray, fmt: Format, candidates: int = 4, block: int = 3
     """Q(X) with static-operand scales: each block takes the power-of-two scale among a_c + u,
     u in mse_candidates(fmt, candidates) (a_c the ceil-absmax scale; scales outside [-127, 127]
     are not tried), whose fp32 reconstruction has the least squared error (block_sq_error);
-    a tie keeps the scale tried first (Sec. 3.1: static operands choose a representable scale
-    by reconstruction-MSE search).  Zero blocks get scale 0, non-finite blocks -128, as in
+    a tie keeps the scale tried first (Sec. 3.1: a static operand's power-of-two scale is the one
+    that minimizes the squared reconstruction error).  Zero blocks get scale -127, non-finite blocks -128, as in
     quantize().  Returns (codes, scales) like quantize()."""
     x = np.asarray(x)
     assert x.dtype == np.float32 and x.ndim == 2 and 1 <= candidates <= 8
@@ -207,7 +209,7 @@ def quantize_mse(x: np.ndarray, fmt: Format, candidates: int = 4, block: int = 3
     a_c = scale_exponents(amax, fmt)
     live = finite_block & (amax > 0)
     xs = np.where(finite_block[..., None], xb, 0.0)
-    best_a = np.where(live, a_c, 0)
+    best_a = np.where(live, a_c, SCALE_MIN)
     best_codes = _codes_at_scale(xs, best_a, fmt)
     best_err = block_sq_error(xs, _reconstruct_f32(best_codes, best_a, fmt))
     for u in mse_candidates(fmt, candidates)[1:]:

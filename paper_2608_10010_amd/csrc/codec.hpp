@@ -62,9 +62,8 @@ struct QRule {
 // ceil-absmax block scale from the largest magnitude's fp32 bits: -128 for a non-finite block
 __device__ __forceinline__ int qr_scale(uint32_t amax, const QRule& q) {
     if (amax >= 0x7F800000u) return -128;
-    if (amax == 0) return 0;
     const int ef = (int)(amax >> 23);
-    if (ef == 0) return -127;                        // subnormal maximum: below every clamp
+    if (ef == 0) return -127;                        // all zero, or a subnormal maximum
     const int a = ef - 127 - q.ohi + (((amax & 0x7FFFFFu) > q.lmax_mant) ? 1 : 0);
     return min(max(a, -127), 127);
 }

@@ -19,58 +19,32 @@
 #include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
+#include "curvefp_tables.inc"
 
 #include <cstring>
 #include <type_traits>
 
 namespace curvefp {
 
-__device__ uint32_t g_qlut[NUM_FORMATS][QLUT_MAX];
+// compile-time tables (curvefp_tables.inc, written at build time by gen_tables)
+__constant__ uint32_t g_qlut[NUM_FORMATS][QLUT_MAX] = CURVEFP_QLUT_INIT;
 // bfloat16 sources: the low 16 bits of every scaled magnitude are zero, so the bucket's
 // decision point is never passed and the rank is the bucket's base rank alone (one byte)
-__device__ __attribute__((aligned(16))) uint8_t g_qlut8[NUM_FORMATS][QLUT_MAX];
-__device__ uint32_t g_lmax_mant[NUM_FORMATS];
+__constant__ __attribute__((aligned(16))) uint8_t g_qlut8[NUM_FORMATS][QLUT_MAX] = CURVEFP_QLUT8_INIT;
+__constant__ uint32_t g_lmax_mant[NUM_FORMATS] = CURVEFP_LMAX_MANT_INIT;
 // reconstruction tables for the static-scale search (the dequantizer's, see codec.hpp): binary
 // radix 8 entries by curve index, rational radix 128 by magnitude rank
-__device__ uint32_t g_qr_mant[NUM_FORMATS][128];
-__device__ uint64_t g_qr_sig[NUM_FORMATS][128];
-
-hipError_t quantize_upload(const AllTables& t) {
-    static uint32_t h[NUM_FORMATS][QLUT_MAX];
-    static uint8_t h8[NUM_FORMATS][QLUT_MAX];
-    uint32_t lm[NUM_FORMATS];
-    for (int f = 0; f < NUM_FORMATS; f++) {
-        memcpy(h[f], t.f[f].qlut, sizeof(h[f]));
-        for (int i = 0; i < QLUT_MAX; i++) h8[f][i] = (uint8_t)(t.f[f].qlut[i] >> 16);
-        lm[f] = t.f[f].lmax_mant;
-    }
-    static uint32_t rm[NUM_FORMATS][128];
-    static uint64_t rs[NUM_FORMATS][128];
-    for (int f = 0; f < NUM_FORMATS; f++) {
-        const bool binary = t.f[f].P == 1 && t.f[f].Q == 1;
-        for (int i = 0; i < 128; i++) {
-            rm[f][i] = binary ? (i < 8 ? t.f[f].mant[i] : 0u) : t.f[f].dq_em[i];
-            rs[f][i] = binary ? (i < 8 ? t.f[f].sig62[i] : 0ull) : t.f[f].dq_sig62[i];
-        }
-    }
-    hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut), h, sizeof(h));
-    if (e != hipSuccess) return e;
-    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qlut8), h8, sizeof(h8));
-    if (e != hipSuccess) return e;
-    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qr_mant), rm, sizeof(rm));
-    if (e != hipSuccess) return e;
-    e = hipMemcpyToSymbol(HIP_SYMBOL(g_qr_sig), rs, sizeof(rs));
-    if (e != hipSuccess) return e;
-    return hipMemcpyToSymbol(HIP_SYMBOL(g_lmax_mant), lm, sizeof(lm));
-}
+__constant__ uint32_t g_qr_mant[NUM_FORMATS][128] = CURVEFP_QR_MANT_INIT;
+__constant__ uint64_t g_qr_sig[NUM_FORMATS][128] = CURVEFP_QR_SIG_INIT;
 
 namespace {
 
 template <class F>
 __device__ __forceinline__ int block_scale(uint32_t amax, uint32_t lmax_mant) {
-    if (amax == 0) return 0;
+    // an all-zero block (every integer a satisfies 0 <= 2^a fl32(L_max)) and a subnormal maximum
+    // both take the bottom of the scale range
     const int ef = (int)(amax >> 23);
-    if (ef == 0) return -127;                       // subnormal maximum: below every clamp
+    if (ef == 0) return -127;
     const int a = ef - 127 - F::OHI + (((amax & 0x7FFFFFu) > lmax_mant) ? 1 : 0);
     return min(max(a, -127), 127);
 }
@@ -903,8 +877,8 @@ hipError_t launch_compact_fmt(const void* src, int dtype, int64_t rows, int64_t 
 }
 
 // ---------------------------------------------------------------------------------------------
-// Static-operand scales (Sec. 3.1: static operands choose a representable power-of-two scale by
-// reconstruction-MSE search).  One thread per block (of 32 here; larger blocks below): the block is quantized at each
+// Static-operand scales (Sec. 3.1: weights quantized once pick, among representable powers of two,
+// the scale that minimizes the squared reconstruction error).  One thread per block (of 32 here; larger blocks below): the block is quantized at each
 // candidate scale a_c + u (a_c ceil-absmax; u = 0, -1, .., -(candidates - 1), then 1 .. P - 1
 // when the level pattern spans P > 1 octaves), each element reconstructed to fp32 exactly as the
 // dequantizer does, and the squared error summed in fp64 in index order; the first candidate

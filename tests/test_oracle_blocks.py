@@ -5,7 +5,8 @@ Each block of G consecutive elements gets one ceil-absmax scale and every elemen
 level at that scale.  These tests hold the oracle to that definition through facts that do
 not come from its own code:
   * the scale rule is monotone in the block maximum, so a block's scale is the largest of the
-    scales its groups of 32 get alone (all-zero groups aside: their scale is 0 by convention);
+    scales its groups of 32 get alone (an all-zero group takes the bottom of the range, -127:
+    every integer satisfies the ceil-absmax inequality for a zero maximum);
   * every code is the nearest level at the block scale, decided by the rigorous integer
     brackets of tests/exact_ref.py;
   * the exact GEMM over blocks of G equals numpy's float64 product of the dequantized operands
@@ -58,9 +59,8 @@ def test_block_scale_is_largest_group_scale(name, G):
     _, sg = oracle.quantize(x, f, G)
     _, s32 = oracle.quantize(x, f, 32)
     groups = np.abs(x).reshape(12, cols // 32, 32).max(-1) > 0
-    s32 = np.where(groups, s32.astype(np.int64), -1000).reshape(12, cols // G, G // 32)
-    expect = s32.max(-1)
-    expect = np.where(expect == -1000, 0, expect)
+    assert (~groups).any() and np.all(s32[~groups] == -127)
+    expect = s32.astype(np.int64).reshape(12, cols // G, G // 32).max(-1)
     assert sg.shape == (12, cols // G)
     assert np.array_equal(sg.astype(np.int64), expect)
 

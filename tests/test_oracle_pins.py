@@ -321,11 +321,15 @@ def test_nonfinite_blocks_poison():
 
 
 def test_zero_block_and_sign_of_zero():
+    """All-zero blocks (either sign of zero) give code 0 and the bottom scale -127: for a zero
+    maximum every integer a satisfies the ceil-absmax inequality, and -127 is the smallest stored
+    scale.  A block whose maximum is the smallest subnormal lands on the same scale."""
     f = oracle.get_format("E5C2")
-    x = np.zeros((1, 64), np.float32)
-    x[0, 32:] = -0.0
+    x = np.zeros((1, 96), np.float32)
+    x[0, 32:64] = -0.0
+    x[0, 64] = np.float32(2.0 ** -149)
     codes, scales = oracle.quantize(x, f)
-    assert np.all(codes == 0) and np.all(scales == 0)
+    assert np.all(codes[0, :64] == 0) and np.all(scales == -127)
 
 
 def test_pack7_layout():
@@ -882,7 +886,7 @@ def test_mse_special_cases(name):
     z[1, 3] = np.nan
     z[1, 40] = 1.0
     cz, sz = oracle.quantize_mse(z, f)
-    assert list(sz[0]) == [0, 0] and list(sz[1]) == [-128, sz[1, 1]] and np.all(cz[:, :32] == 0)
+    assert list(sz[0]) == [-127, -127] and list(sz[1]) == [-128, sz[1, 1]] and np.all(cz[:, :32] == 0)
     a_c = int(oracle.quantize(z, f)[1][1, 1])
     assert sz[1, 1] == a_c if P == 1 else a_c <= sz[1, 1] < a_c + P
 
