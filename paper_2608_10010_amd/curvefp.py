@@ -51,8 +51,6 @@ def lib() -> ctypes.CDLL:
         L.curvefp_codes_bytes.restype = I64
         L.curvefp_scales_count.argtypes = [I64, I64, I]
         L.curvefp_scales_count.restype = I64
-        L.curvefp_init.argtypes = []
-        L.curvefp_init.restype = I
         L.curvefp_quantize.argtypes = [P, I, I64, I64, I64, I, I, I, P, P, P]
         L.curvefp_quantize.restype = I
         L.curvefp_quantize_mse.argtypes = [P, I, I64, I64, I64, I, I, I, I, P, P, P]
@@ -100,6 +98,77 @@ def _check(st: int, what: str):
         raise CurveFPError(st, what)
 
 
+# ---------------------------------------------------------------- argument checks
+# The C ABI takes raw device pointers and sizes, so it cannot tell a host pointer or a buffer
+# that is too small from a good one: such a call would make the kernels read or write out of
+# bounds.  Every wrapper therefore checks, before anything reaches the library, that each tensor
+# is on the current GPU, has the dtype the library reads or writes, and spans at least the bytes
+# the call implies for its shape, format and block.  A failed check raises ValueError.
+
+# device types the checks accept (the tests of these checks add "meta", whose tensors have null
+# data pointers, which the library rejects before launching anything)
+_GPU_DEVICE_TYPES = ("cuda",)
+
+
+def _on_gpu(what: str, tensors, stream=None):
+    """All tensors on one GPU, the current device (and the stream's, when one is given)."""
+    dev = None
+    for name, t in tensors:
+        if not isinstance(t, torch.Tensor):
+            raise ValueError(f"{what}: {name} must be a torch.Tensor")
+        if t.device.type not in _GPU_DEVICE_TYPES:
+            raise ValueError(f"{what}: {name} is on {t.device}, not on a GPU")
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError(f"{what}: {name} is on {t.device}, the other operands on {dev}")
+    if dev is not None and dev.type == "cuda":
+        cur = torch.cuda.current_device()
+        if dev.index != cur:
+            raise ValueError(f"{what}: operands are on {dev}, the current device is cuda:{cur}")
+        if stream is not None and getattr(stream, "device", dev) != dev:
+            raise ValueError(f"{what}: the stream belongs to {stream.device}, the operands to {dev}")
+
+
+def _dense(what: str, name: str, t: torch.Tensor, nbytes: int, dtype=None):
+    """A contiguous buffer of at least nbytes (of dtype, when given)."""
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{what}: {name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{what}: {name} must be contiguous")
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what}: {name} holds {have} bytes, the call needs {nbytes}")
+
+
+def _matrix(what: str, name: str, t: torch.Tensor, rows: int, cols: int, dtypes):
+    """A 2-D row-major matrix of at least rows x cols elements (unit column stride; the row stride
+    is passed as the leading dimension)."""
+    if t.dtype not in dtypes:
+        raise ValueError(f"{what}: {name} must be one of {dtypes}, got {t.dtype}")
+    if t.dim() != 2 or t.stride(1) != 1:
+        raise ValueError(f"{what}: {name} must be 2-D with unit column stride")
+    if t.shape[0] < rows or t.shape[1] < cols:
+        raise ValueError(f"{what}: {name} is {tuple(t.shape)}, the call needs at least {rows} x {cols}")
+    if rows > 1 and t.stride(0) < cols:
+        raise ValueError(f"{what}: {name} rows overlap (row stride {t.stride(0)} < {cols})")
+
+
+def _codes_arg(what, name, t, f, outer, k, block):
+    _dense(what, name, t, curvefp_codes_bytes(f, outer, k, block), torch.uint8)
+
+
+def _scales_arg(what, name, t, outer, k, block):
+    _dense(what, name, t, curvefp_scales_count(outer, k, block), torch.int8)
+
+
+def _source_arg(what, src):
+    """A 2-D fp32 or bf16 source (its row stride is the library's ld_src)."""
+    if src.dim() != 2:
+        raise ValueError(f"{what}: src must be 2-D, got {src.dim()} dimensions")
+    _matrix(what, "src", src, src.shape[0], src.shape[1], tuple(DTYPES))
+
+
 def curvefp_format_info(fmt) -> Tuple[int, int, int, int]:
     b, e, c, h = (ctypes.c_int() for _ in range(4))
     _check(lib().curvefp_format_info(_fmt(fmt), ctypes.byref(b), ctypes.byref(e), ctypes.byref(c),
@@ -128,10 +197,6 @@ def curvefp_scales_count(outer: int, k: int, block: int = 32) -> int:
     return n
 
 
-def curvefp_init():
-    _check(lib().curvefp_init(), "curvefp_init")
-
-
 def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 32,
                      codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
                      stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
@@ -141,7 +206,9 @@ def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 3
     block_axis=0: quantize-transpose, codes [cols, rows], scales [cols, rows/block].
     block: elements per scale, a multiple of 32 dividing the blocked extent.
     """
-    assert src.dim() == 2 and src.stride(1) == 1
+    what = "curvefp_quantize"
+    _on_gpu(what, [("src", src)], stream)
+    _source_arg(what, src)
     rows, cols = src.shape
     outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
     f = _fmt(fmt)
@@ -152,6 +219,9 @@ def curvefp_quantize(src: torch.Tensor, fmt, block_axis: int = 1, block: int = 3
         assert codes.numel() == nbytes
     if scales is None:
         scales = torch.empty((outer, k // block), dtype=torch.int8, device=src.device)
+    _on_gpu(what, [("src", src), ("codes", codes), ("scales", scales)], stream)
+    _codes_arg(what, "codes", codes, f, outer, k, block)
+    _scales_arg(what, "scales", scales, outer, k, block)
     st = lib().curvefp_quantize(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0),
                                 block_axis, f, block, codes.data_ptr(), scales.data_ptr(),
                                 _stream(stream))
@@ -163,7 +233,9 @@ def curvefp_quantize_mse(src: torch.Tensor, fmt, block_axis: int = 1, candidates
                          codes: Optional[torch.Tensor] = None, scales: Optional[torch.Tensor] = None,
                          stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """curvefp_quantize with static-operand scales chosen by reconstruction-MSE search."""
-    assert src.dim() == 2 and src.stride(1) == 1
+    what = "curvefp_quantize_mse"
+    _on_gpu(what, [("src", src)], stream)
+    _source_arg(what, src)
     rows, cols = src.shape
     outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
     f = _fmt(fmt)
@@ -172,6 +244,9 @@ def curvefp_quantize_mse(src: torch.Tensor, fmt, block_axis: int = 1, candidates
         codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
     if scales is None:
         scales = torch.empty((outer, k // block), dtype=torch.int8, device=src.device)
+    _on_gpu(what, [("src", src), ("codes", codes), ("scales", scales)], stream)
+    _codes_arg(what, "codes", codes, f, outer, k, block)
+    _scales_arg(what, "scales", scales, outer, k, block)
     st = lib().curvefp_quantize_mse(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), block_axis, f,
                                     block, candidates, codes.data_ptr(), scales.data_ptr(), _stream(stream))
     _check(st, "curvefp_quantize_mse")
@@ -184,7 +259,9 @@ def curvefp_quantize_tensorwise(src: torch.Tensor, fmt, block_axis: int = 1,
                                 stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Q(X) with one scale for the whole tensor: codes as curvefp_quantize's, the scale repeated
     once per output row (scales [outer], the rowwise layout: block = the blocked extent)."""
-    assert src.dim() == 2 and src.stride(1) == 1
+    what = "curvefp_quantize_tensorwise"
+    _on_gpu(what, [("src", src)], stream)
+    _source_arg(what, src)
     rows, cols = src.shape
     outer, k = (rows, cols) if block_axis == 1 else (cols, rows)
     f = _fmt(fmt)
@@ -195,6 +272,10 @@ def curvefp_quantize_tensorwise(src: torch.Tensor, fmt, block_axis: int = 1,
         scales = torch.empty((outer, 1), dtype=torch.int8, device=src.device)
     if workspace is None:
         workspace = torch.empty((1,), dtype=torch.int32, device=src.device)
+    _on_gpu(what, [("src", src), ("codes", codes), ("scales", scales), ("workspace", workspace)], stream)
+    _codes_arg(what, "codes", codes, f, outer, k, 32)
+    _dense(what, "scales", scales, outer, torch.int8)
+    _dense(what, "workspace", workspace, 4)
     st = lib().curvefp_quantize_tensorwise(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), block_axis,
                                            f, codes.data_ptr(), scales.data_ptr(), workspace.data_ptr(),
                                            _stream(stream))
@@ -215,7 +296,9 @@ def curvefp_quantize_compact(src: torch.Tensor, fmt, block: int, scale_bits: int
                              stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """Q(X) with S-bit scale exponents along the rows of src: codes as curvefp_quantize's
     (block_axis=1), an int8 reference per row, and packed S-bit offsets [rows, bytes per row]."""
-    assert src.dim() == 2 and src.stride(1) == 1
+    what = "curvefp_quantize_compact"
+    _on_gpu(what, [("src", src)], stream)
+    _source_arg(what, src)
     rows, cols = src.shape
     f = _fmt(fmt)
     if codes is None:
@@ -226,6 +309,10 @@ def curvefp_quantize_compact(src: torch.Tensor, fmt, block: int, scale_bits: int
     if offsets is None:
         ob = curvefp_compact_offsets_bytes(1, cols, block, scale_bits)
         offsets = torch.empty((rows, ob), dtype=torch.uint8, device=src.device)
+    _on_gpu(what, [("src", src), ("codes", codes), ("row_ref", row_ref), ("offsets", offsets)], stream)
+    _codes_arg(what, "codes", codes, f, rows, cols, block)
+    _dense(what, "row_ref", row_ref, rows, torch.int8)
+    _dense(what, "offsets", offsets, curvefp_compact_offsets_bytes(rows, cols, block, scale_bits), torch.uint8)
     st = lib().curvefp_quantize_compact(src.data_ptr(), DTYPES[src.dtype], rows, cols, src.stride(0), f, block,
                                         scale_bits, codes.data_ptr(), row_ref.data_ptr(), offsets.data_ptr(),
                                         _stream(stream))
@@ -236,9 +323,16 @@ def curvefp_quantize_compact(src: torch.Tensor, fmt, block: int, scale_bits: int
 def curvefp_scales_unpack(row_ref: torch.Tensor, offsets: torch.Tensor, nblocks: int, scale_bits: int,
                           scales: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """int8 block scales [rows, nblocks] of S-bit offsets (reference - offset; -128 marks NaN/Inf)."""
-    rows = row_ref.shape[0]
+    what = "curvefp_scales_unpack"
+    _on_gpu(what, [("row_ref", row_ref), ("offsets", offsets)], stream)
+    rows = row_ref.numel()
     if scales is None:
         scales = torch.empty((rows, nblocks), dtype=torch.int8, device=row_ref.device)
+    _on_gpu(what, [("row_ref", row_ref), ("offsets", offsets), ("scales", scales)], stream)
+    _dense(what, "row_ref", row_ref, rows, torch.int8)
+    if 2 <= scale_bits <= 8 and nblocks > 0:   # otherwise the library rejects the call
+        _dense(what, "offsets", offsets, rows * ((nblocks * scale_bits + 7) // 8), torch.uint8)
+        _dense(what, "scales", scales, rows * nblocks, torch.int8)
     st = lib().curvefp_scales_unpack(row_ref.data_ptr(), offsets.data_ptr(), rows, nblocks, scale_bits,
                                      scales.data_ptr(), _stream(stream))
     _check(st, "curvefp_scales_unpack")
@@ -248,20 +342,43 @@ def curvefp_scales_unpack(row_ref: torch.Tensor, offsets: torch.Tensor, nblocks:
 def curvefp_dequantize(codes: torch.Tensor, scales: torch.Tensor, fmt, outer: int, k: int,
                        block: int = 32, dst: Optional[torch.Tensor] = None,
                        stream=None) -> torch.Tensor:
+    what = "curvefp_dequantize"
+    f = _fmt(fmt)
+    _on_gpu(what, [("codes", codes), ("scales", scales)], stream)
     if dst is None:
         dst = torch.empty((outer, k), dtype=torch.float32, device=codes.device)
+    _on_gpu(what, [("codes", codes), ("scales", scales), ("dst", dst)], stream)
+    _codes_arg(what, "codes", codes, f, outer, k, block)
+    _scales_arg(what, "scales", scales, outer, k, block)
+    _matrix(what, "dst", dst, outer, k, (torch.float32,))
     st = lib().curvefp_dequantize(codes.data_ptr(), scales.data_ptr(), _fmt(fmt), outer, k, block,
                                   dst.data_ptr(), dst.stride(0), _stream(stream))
     _check(st, "curvefp_dequantize")
     return dst
 
 
+def _gemm_args(what, a_codes, a_scales, b_codes, b_scales, M, N, K, f, block, c, stream):
+    """Operands of a single-format GEMM: A codes/scales of an [M, K] tensor, B of an [N, K]
+    tensor, blocks along K; c (if given) at least M x N fp32."""
+    ts = [("a_codes", a_codes), ("a_scales", a_scales), ("b_codes", b_codes), ("b_scales", b_scales)]
+    _on_gpu(what, ts + ([("c", c)] if c is not None else []), stream)
+    _codes_arg(what, "a_codes", a_codes, f, M, K, block)
+    _scales_arg(what, "a_scales", a_scales, M, K, block)
+    _codes_arg(what, "b_codes", b_codes, f, N, K, block)
+    _scales_arg(what, "b_scales", b_scales, N, K, block)
+    if c is not None:
+        _matrix(what, "c", c, M, N, (torch.float32,))
+
+
 def curvefp_gemm(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.Tensor,
                  b_scales: torch.Tensor, M: int, N: int, K: int, fmt, block: int = 32,
                  c: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
     """C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T in fp32."""
+    what = "curvefp_gemm"
     if c is None:
+        _on_gpu(what, [("a_codes", a_codes)], stream)
         c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    _gemm_args(what, a_codes, a_scales, b_codes, b_scales, M, N, K, _fmt(fmt), block, c, stream)
     st = lib().curvefp_gemm(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
                             b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
                             _stream(stream))
@@ -286,10 +403,15 @@ def curvefp_gemm_ws(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torc
                     c: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
                     stream=None) -> torch.Tensor:
     """The product of curvefp_gemm, through a workspace (codes expanded once)."""
+    what = "curvefp_gemm_ws"
+    _on_gpu(what, [("a_codes", a_codes)], stream)
     if c is None:
         c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
     if workspace is None:
         workspace = gemm_workspace(M, N, K, a_codes.device)
+    _gemm_args(what, a_codes, a_scales, b_codes, b_scales, M, N, K, _fmt(fmt), block, c, stream)
+    _on_gpu(what, [("a_codes", a_codes), ("workspace", workspace)], stream)
+    _dense(what, "workspace", workspace, curvefp_gemm_workspace_bytes(M, N, K))
     st = lib().curvefp_gemm_ws(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
                                b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
@@ -317,10 +439,21 @@ def curvefp_gemm_mixed(a_codes: torch.Tensor, a_scales: torch.Tensor, fmt_a, a_t
     """C[M, N] = deq(A)[M, K] . deq(B)[N, K]^T for operands of any two formats.  x_trans = 0:
     codes/scales of an [R, K] tensor quantized along K; x_trans = 1: those of a [K, R] tensor
     quantized along R (forward codes reused by a backward GEMM)."""
+    what = "curvefp_gemm_mixed"
+    _on_gpu(what, [("a_codes", a_codes)], stream)
     if c is None:
         c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
     if workspace is None:
         workspace = gemm_mixed_workspace(M, N, K, a_codes.device)
+    _on_gpu(what, [("a_codes", a_codes), ("a_scales", a_scales), ("b_codes", b_codes), ("b_scales", b_scales),
+                   ("c", c), ("workspace", workspace)], stream)
+    for x, codes, scales, fx, tx, R in (("a", a_codes, a_scales, fmt_a, a_trans, M),
+                                        ("b", b_codes, b_scales, fmt_b, b_trans, N)):
+        outer, k = (K, R) if int(tx) == 1 else (R, K)
+        _codes_arg(what, f"{x}_codes", codes, _fmt(fx), outer, k, block)
+        _scales_arg(what, f"{x}_scales", scales, outer, k, block)
+    _matrix(what, "c", c, M, N, (torch.float32,))
+    _dense(what, "workspace", workspace, curvefp_gemm_mixed_workspace_bytes(M, N, K))
     st = lib().curvefp_gemm_mixed(a_codes.data_ptr(), a_scales.data_ptr(), _fmt(fmt_a), int(a_trans),
                                   b_codes.data_ptr(), b_scales.data_ptr(), _fmt(fmt_b), int(b_trans),
                                   M, N, K, block, c.data_ptr(), c.stride(0), workspace.data_ptr(),
@@ -337,7 +470,9 @@ def curvefp_gemm_requant(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes:
     """curvefp_gemm_ws's product requantized in the epilogue: codes/scales of C in out_fmt,
     blocks of out_block (32, 64, 128 or 256) along each row (equal to curvefp_quantize of the
     fp32 C with that block)."""
+    what = "curvefp_gemm_requant"
     fo = _fmt(out_fmt)
+    _on_gpu(what, [("a_codes", a_codes)], stream)
     if out_codes is None:
         shape = (M, N // 32, 28) if fo == 2 else (M, N)
         out_codes = torch.empty(shape, dtype=torch.uint8, device=a_codes.device)
@@ -345,6 +480,12 @@ def curvefp_gemm_requant(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes:
         out_scales = torch.empty((M, N // out_block), dtype=torch.int8, device=a_codes.device)
     if workspace is None:
         workspace = gemm_workspace(M, N, K, a_codes.device)
+    _gemm_args(what, a_codes, a_scales, b_codes, b_scales, M, N, K, _fmt(fmt), block, None, stream)
+    _on_gpu(what, [("a_codes", a_codes), ("out_codes", out_codes), ("out_scales", out_scales),
+                   ("workspace", workspace)], stream)
+    _codes_arg(what, "out_codes", out_codes, fo, M, N, out_block)
+    _scales_arg(what, "out_scales", out_scales, M, N, out_block)
+    _dense(what, "workspace", workspace, curvefp_gemm_workspace_bytes(M, N, K))
     st = lib().curvefp_gemm_requant(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
                                     b_scales.data_ptr(), M, N, K, _fmt(fmt), block, fo, out_block,
                                     out_codes.data_ptr(), out_scales.data_ptr(), workspace.data_ptr(),
