@@ -14,9 +14,11 @@
  *   - All data pointers are device pointers owned by the caller.  The library
  *     never allocates, frees or keeps them.
  *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every call
- *     is asynchronous on that stream and never synchronizes it.  Constant
- *     tables are uploaded on the first call on each device (or by
- *     curvefp_init); that first call is synchronous.
+ *     is asynchronous on that stream and never synchronizes it.  The library
+ *     keeps no state: its constant tables (quantizer thresholds, reconstruction
+ *     and expansion values) are compile-time __constant__ arrays, generated
+ *     when the library is built, so no call uploads, allocates or waits, and
+ *     every call may be captured into a HIP graph.
  *   - Argument errors are detected before any HIP call and returned as a
  *     negative curvefp_status; nothing is launched then.  Launch failures
  *     return CURVEFP_ERR_HIP.  Data-dependent conditions (non-finite inputs)
@@ -46,8 +48,10 @@
  * Scales: int8 power-of-two exponents, one per block of G, row-major
  *   [outer][k / G]; -128 marks a block that held a NaN or an infinity.  A block's
  *   scale is the ceil-absmax rule applied to its largest magnitude, so a block of
- *   G has the largest of the scales its groups of 32 would get on their own
- *   (all-zero groups aside).
+ *   G has the largest of the scales its groups of 32 would get on their own.  An
+ *   all-zero block has scale -127, the bottom of the range (every integer satisfies
+ *   the rule's inequality for a zero maximum), so it never raises a row's largest
+ *   scale.
  */
 #ifndef CURVEFP_H
 #define CURVEFP_H
@@ -80,7 +84,7 @@ typedef enum {
     CURVEFP_ERR_FORMAT = -3,   /* unknown format or dtype */
     CURVEFP_ERR_BLOCK = -4,    /* block not a positive multiple of 32, or block_axis not 0/1 */
     CURVEFP_ERR_ALIGN = -5,    /* pointer or row not 16-byte aligned */
-    CURVEFP_ERR_HIP = -6       /* a HIP call failed (launch, device query, table upload) */
+    CURVEFP_ERR_HIP = -6       /* a kernel launch failed */
 } curvefp_status;
 
 /* Format parameters from Tab. curvefp-formats: element bits, E, C and the phase
@@ -99,10 +103,6 @@ int64_t curvefp_codes_bytes(int format, int64_t outer, int64_t k, int block);
 /* Number of int8 scales: outer * (k / block); negative status on bad input. */
 int64_t curvefp_scales_count(int64_t outer, int64_t k, int block);
 
-/* Upload the constant tables to the current device.  Optional: every entry
- * point does it on its first call on a device.  Synchronous. */
-int curvefp_init(void);
-
 /*
  * Block quantization Q(X) (Sec. 3.1).
  *   src     [rows][ld_src] elements of `dtype` (fp32 or bf16), row-major.
@@ -114,7 +114,7 @@ int curvefp_init(void);
  *   other G, and every G > 32 down the columns, first write the block scales in
  *   a pass of their own (the source is read twice).
  * Scale (dynamic, ceil-absmax): a_b is the smallest integer with
- *   max|x| <= 2^{a_b} * fl32(2^{n_max/K}), clamped to [-127, 127]; 0 for an
+ *   max|x| <= 2^{a_b} * fl32(2^{n_max/K}), clamped to [-127, 127]; -127 for an
  *   all-zero block; -128 (and all-zero codes) for a block holding NaN/Inf.
  * Element: the magnitude nearest to |x| 2^{-a_b} in absolute error among zero
  *   and the levels 2^{n/K}, saturating at the endpoints; the sign is kept,
@@ -125,8 +125,8 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
                      void* codes, int8_t* scales, void* stream);
 
 /*
- * Block quantization with static-operand scales (Sec. 3.1: static operands choose a
- * representable power-of-two scale by reconstruction-MSE search), for weights quantized
+ * Block quantization with static-operand scales (Sec. 3.1: a static operand takes the
+ * power-of-two scale whose reconstruction has the least squared error), for weights quantized
  * once.  Same arguments, layouts and results as curvefp_quantize except the scale: each
  * block tries the scales a_c + u, a_c its ceil-absmax scale, for u = 0, -1, ...,
  * -(candidates - 1) and then, when the format's level pattern spans P > 1 octaves
@@ -136,7 +136,7 @@ int curvefp_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int
  * (x - x_hat)^2 are summed in fp64 over the block's 32 elements in index order, each
  * product and sum rounded once, and the first candidate in the order above with the least
  * sum wins.  candidates in [1, 8], else CURVEFP_ERR_SHAPE.  Any block size of curvefp_quantize
- * (the sums then run over the block's G elements in index order).  Zero blocks get scale 0 and
+ * (the sums then run over the block's G elements in index order).  Zero blocks get scale -127 and
  * non-finite blocks -128 with zero codes, as in curvefp_quantize.
  */
 int curvefp_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld_src,
@@ -214,12 +214,21 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
  * an fp16 high/low pair (22 significant bits) carrying its block scale
  * relative to the row's largest block scale, three f16 MFMA products
  * (hi.hi + hi.lo + lo.hi) accumulate in fp32, and the epilogue applies the
- * row and column scale offsets exactly.  Error: each product is represented
- * to about 2^-21 relative; elements more than ~2^-29 below their row's largest
- * element keep fewer bits (fp16 subnormals) and those more than ~2^-39 below
- * it are flushed; accumulation is fp32.  Relative Frobenius error against the
- * exact phase-binned sum is about 1e-7 on the benchmark workloads.
- * Blocks with scale -128 contribute zero.
+ * row and column scale offsets exactly.  Accumulation is fp32.  Relative
+ * Frobenius error against the exact phase-binned sum is about 1e-7 on the
+ * benchmark workloads.  Blocks with scale -128 contribute zero.
+ *
+ * Scale-spread limit (the one place where the result can depart from the exact
+ * sum by more than rounding).  Let alpha be the largest block scale of a row of
+ * A (or of B) and top = 2^{alpha + e_max + 1}, e_max = floor(log2) of the
+ * format's top level (7 for E4C3, 15 for E5C2, 3 for E3C3; all-zero blocks,
+ * scale -127, and poisoned blocks never set alpha).  An element v of that row
+ *   - with |v| >= 2^-18 top keeps 22 significant bits (each product is good
+ *     to about 2^-21 relative);
+ *   - with |v| < 2^-18 top keeps an absolute error of at most 2^-39 top;
+ *   - with |v| < 2^-41 top is flushed: it contributes nothing.
+ * A block loses all of its contribution only when its scale lies more than 41
+ * binades below alpha; tests/test_gpu_accuracy_contract.py pins each clause.
  *
  * This entry point allocates nothing: the expansion happens inside the GEMM
  * kernel, once per workgroup that needs a code.  curvefp_gemm_ws below does the

@@ -65,6 +65,11 @@ def lognormal_rows(shape, seed: int, sigma: float = 3.0) -> np.ndarray:
 
 # ---------------------------------------------------------------- workloads
 
+# the last few operands drawn, shared by workloads built from the same recipe and seed (the
+# sweep's formats reuse one layer's tensors): callers must treat operands as read-only
+_RECENT: Dict[tuple, np.ndarray] = {}
+_RECENT_MAX = 4
+
 @dataclass
 class Operand:
     name: str
@@ -93,10 +98,16 @@ class Workload:
         """The source tensor (float32 array; bf16-representable when dtype is bf16)."""
         if which not in self._cache:
             op = self.a if which == "a" else self.b
-            x = op.make(op.seed)
-            assert x.shape == op.shape, (x.shape, op.shape)
-            if self.dtype == "bf16":
-                x = bf16_round(x)
+            key = (op.name, op.shape, op.seed, self.dtype, self.note)
+            x = _RECENT.get(key)
+            if x is None:
+                x = op.make(op.seed)
+                assert x.shape == op.shape, (x.shape, op.shape)
+                if self.dtype == "bf16":
+                    x = bf16_round(x)
+                _RECENT[key] = x
+                while len(_RECENT) > _RECENT_MAX:
+                    _RECENT.pop(next(iter(_RECENT)))
             self._cache[which] = x
         return self._cache[which]
 

@@ -71,21 +71,36 @@ def row_tops(codes, scales, fmt):
     return np.ldexp(1.0, alpha + e_max + 1)
 
 
+# An element is expanded relative to the top of its row's scale range, top = 2^{alpha + e_max + 1}
+# (alpha = the row's largest block scale): it keeps 22 significant bits while it stays above
+# fp16's normal range in those units, and otherwise an absolute error of at most about 2^-39 top
+# (elements below about 2^-41 top are flushed to zero).  FLUSH_REL is that absolute bound with a
+# factor of two to spare.
+FLUSH_REL = 2.0 ** -38
+
+
+def element_loss(v: np.ndarray, tops: np.ndarray) -> np.ndarray:
+    """Per-element bound on what the expansion can lose beyond the relative 2^-21: at most the
+    element itself, and at most FLUSH_REL of its row's top."""
+    return np.minimum(v, FLUSH_REL * tops[:, None])
+
+
 def gemm_tolerance(ca, sa, cb, sb, fmt, block: int = 32):
     """Element-wise bound for the MFMA GEMM against the exact sum.
 
     * 1e-5 sum_k |a_ik b_jk| covers the 22-bit fp16 high/low operand splits
       (about 3 * 2^-22 per product) and fp32 accumulation;
-    * 2^-38 (top_i ||b_j||_1 + top_j ||a_i||_1) covers elements that fall below
-      fp16's normal range when expressed relative to the top of their row's
-      scale range top = 2^{alpha + e_max + 1} (absolute error <= 2^-40 top);
+    * sum_k (la_ik |b_jk| + |a_ik| lb_jk + la_ik lb_jk), with la = element_loss(|a|) (and lb
+      for B), covers the elements that fall below fp16's normal range relative to their row's
+      top: each such element may lose at most itself and at most 2^-38 of its row's top, so
+      the term admits the loss of exactly those contributions and no more;
     * 2^-148 covers an exact result that underflows fp32.
     """
     va, vb = np.abs(exact_values(ca, sa, fmt, block)), np.abs(exact_values(cb, sb, fmt, block))
+    la, lb = element_loss(va, row_tops(ca, sa, fmt)), element_loss(vb, row_tops(cb, sb, fmt))
     S = va @ vb.T
-    ta, tb = row_tops(ca, sa, fmt), row_tops(cb, sb, fmt)
-    flush = ta[:, None] * vb.sum(1)[None, :] + va.sum(1)[:, None] * tb[None, :]
-    return 1e-5 * S + 2.0 ** -38 * flush + 2.0 ** -148
+    loss = la @ vb.T + va @ lb.T + la @ lb.T
+    return 1e-5 * S + loss + 2.0 ** -148
 
 
 def check_gemm(C_dev: np.ndarray, V: np.ndarray, tol: np.ndarray, what: str, frobenius: bool = True):
@@ -130,7 +145,7 @@ def gemm_tolerance_mixed(ca, sa, fa, cb, sb, fb):
     elements are expanded relative to the top of its own row's scale range, with its own
     format's largest exponent."""
     va, vb = np.abs(exact_values_elem(ca, sa, fa)), np.abs(exact_values_elem(cb, sb, fb))
+    la, lb = element_loss(va, row_tops_elem(sa, fa)), element_loss(vb, row_tops_elem(sb, fb))
     S = va @ vb.T
-    ta, tb = row_tops_elem(sa, fa), row_tops_elem(sb, fb)
-    flush = ta[:, None] * vb.sum(1)[None, :] + va.sum(1)[:, None] * tb[None, :]
-    return 1e-5 * S + 2.0 ** -38 * flush + 2.0 ** -148
+    loss = la @ vb.T + va @ lb.T + la @ lb.T
+    return 1e-5 * S + loss + 2.0 ** -148

@@ -147,7 +147,8 @@ def test_output_row_stride():
     assert np.all(got[:, 40:] == 5.0)
 
 
-WL = ["tiny", "inference", "fwd", "dgrad", "wgrad", "sweep_o_E5C2", "sweep_down_E3C3"]
+SWEEPS = [f"sweep_{layer}_{fmt}" for layer in ("qkv", "o", "gateup", "down") for fmt in ("E4C3", "E5C2", "E3C3")]
+WL = ["tiny", "inference", "fwd", "dgrad", "wgrad"] + SWEEPS
 
 
 @pytest.mark.parametrize("name", WL)

@@ -87,7 +87,10 @@ def test_workspace_reuse_and_row_stride():
     assert np.all(got[:, 40:] == 5.0)
 
 
-WL = ["inference", "fwd", "dgrad", "wgrad", "sweep_o_E5C2", "sweep_down_E3C3"]
+# every configuration the benchmark runs: the inference GEMM, the 7B forward / dgrad / wgrad, and
+# the 8B layer sweep (QKV, O, gate/up, down) in each of the three formats
+SWEEPS = [f"sweep_{layer}_{fmt}" for layer in ("qkv", "o", "gateup", "down") for fmt in ("E4C3", "E5C2", "E3C3")]
+WL = ["inference", "fwd", "dgrad", "wgrad"] + SWEEPS
 
 
 @pytest.mark.parametrize("name", WL)

@@ -90,7 +90,8 @@ def test_all_fp32_significands_one_octave(fmt):
     run_and_compare(x, fmt, "f32", 1, "octave_sweep")
 
 
-WL_SAMPLED = ["tiny", "inference", "fwd", "dgrad", "wgrad", "sweep_gateup_E4C3", "sweep_down_E3C3"]
+SWEEPS = [f"sweep_{layer}_{fmt}" for layer in ("qkv", "o", "gateup", "down") for fmt in ("E4C3", "E5C2", "E3C3")]
+WL_SAMPLED = ["tiny", "inference", "fwd", "dgrad", "wgrad"] + SWEEPS
 
 
 @pytest.mark.parametrize("name", WL_SAMPLED)
