@@ -267,6 +267,29 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
                     float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
                     void* stream);
 
+/* Bytes of the device scratch curvefp_gemm_ws_static uses on each GPU. */
+#define CURVEFP_STATIC_SCRATCH_BYTES ((int64_t)128 << 20)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid hipMalloc): curvefp_gemm_ws with the library's own static
+ * device scratch as its workspace.  Same operands, result (bit for bit) and errors as
+ * curvefp_gemm_ws, without the workspace arguments.  The scratch is one 256-byte aligned array
+ * of CURVEFP_STATIC_SCRATCH_BYTES per GPU, part of the library's code object: each GPU the
+ * entry point runs on holds it from the first call on that device until the process ends.
+ * The call makes no hipMalloc, hipFree or other allocation; its first call on a device looks
+ * up the array's device address (hipGetSymbolAddress) and keeps it.
+ *   Limit: curvefp_gemm_workspace_bytes(M, N, K) <= CURVEFP_STATIC_SCRATCH_BYTES, else
+ *   CURVEFP_ERR_SHAPE (before any HIP call).
+ *   Every call on one GPU uses that GPU's array, and everything the kernels need cleared is
+ *   cleared by the call itself; calls that overlap on one GPU (different streams, or host
+ *   threads without ordering) race on the array and may return wrong results.
+ */
+int curvefp_gemm_ws_static(const void* a_codes, const int8_t* a_scales,
+                           const void* b_codes, const int8_t* b_scales,
+                           int64_t M, int64_t N, int64_t K, int format, int block,
+                           float* c, int64_t ldc, void* stream);
+
 /*
  * The product of curvefp_gemm_ws (same operands, format, workspace and fp32 values), with
  * the output requantized in the GEMM's epilogue instead of stored as fp32: the explicit

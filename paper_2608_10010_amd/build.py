@@ -21,7 +21,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(BUILD, "libcurvefp.so")
-SOURCES = ["api.cpp", "quantize.hip", "dequantize.hip", "gemm.hip"]
+SOURCES = ["api.cpp", "quantize.hip", "dequantize.hip", "gemm.hip", "scratch.hip"]
 GEN_SOURCES = ["gen_tables.cpp", "tables.cpp"]
 GEN_DIR = os.path.join(BUILD, "gen")
 TABLES_INC = os.path.join(GEN_DIR, "curvefp_tables.inc")

@@ -194,6 +194,21 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
+int curvefp_gemm_ws_static(const void* a_codes, const int8_t* a_scales, const void* b_codes,
+                           const int8_t* b_scales, int64_t M, int64_t N, int64_t K, int format, int block, float* c,
+                           int64_t ldc, void* stream) {
+    if (!a_codes || !a_scales || !b_codes || !b_scales || !c) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (gemm_workspace_bytes(M, N, K) > CURVEFP_STATIC_SCRATCH_BYTES) return CURVEFP_ERR_SHAPE;
+    if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
+    void* ws = nullptr;
+    if (static_scratch(&ws) != hipSuccess) return CURVEFP_ERR_HIP;
+    return hip_status(launch_gemm_ws(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc, ws,
+                                     reinterpret_cast<hipStream_t>(stream)));
+}
+
 int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void* b_codes, const int8_t* b_scales,
                          int64_t M, int64_t N, int64_t K, int format, int block, int out_format, int out_block,
                          void* out_codes, int8_t* out_scales, void* workspace, int64_t workspace_bytes,

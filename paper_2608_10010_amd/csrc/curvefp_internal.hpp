@@ -51,6 +51,9 @@ int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_gemm_mixed(const void* a, const int8_t* as, int fa, int ta, const void* b, const int8_t* bs, int fb,
                              int tb, int64_t M, int64_t N, int64_t K, int block, float* c, int64_t ldc, void* ws,
                              hipStream_t s);
+// the calling device's static scratch (CURVEFP_STATIC_SCRATCH_BYTES, 256-byte aligned), looked up
+// on the device's first call and kept
+hipError_t static_scratch(void** out);
 hipError_t launch_gemm(const void* a, const int8_t* as, const void* b, const int8_t* bs,
                        int64_t M, int64_t N, int64_t K, int format, int block, float* c, int64_t ldc,
                        hipStream_t s);

@@ -71,6 +71,8 @@ def lib() -> ctypes.CDLL:
         L.curvefp_gemm_workspace_bytes.restype = I64
         L.curvefp_gemm_ws.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P, I64, P]
         L.curvefp_gemm_ws.restype = I
+        L.curvefp_gemm_ws_static.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
+        L.curvefp_gemm_ws_static.restype = I
         L.curvefp_gemm_requant.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, I, P, P, P, I64, P]
         L.curvefp_gemm_requant.restype = I
         L.curvefp_gemm_mixed_workspace_bytes.argtypes = [I64, I64, I64]
@@ -417,6 +419,23 @@ def curvefp_gemm_ws(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torc
                                workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                _stream(stream))
     _check(st, "curvefp_gemm_ws")
+    return c
+
+
+def curvefp_gemm_ws_static(a_codes: torch.Tensor, a_scales: torch.Tensor, b_codes: torch.Tensor,
+                           b_scales: torch.Tensor, M: int, N: int, K: int, fmt, block: int = 32,
+                           c: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """curvefp_gemm_ws on the library's static device scratch (no workspace, no allocation by
+    the library; c is allocated here only when not given)."""
+    what = "curvefp_gemm_ws_static"
+    if c is None:
+        _on_gpu(what, [("a_codes", a_codes)], stream)
+        c = torch.empty((M, N), dtype=torch.float32, device=a_codes.device)
+    _gemm_args(what, a_codes, a_scales, b_codes, b_scales, M, N, K, _fmt(fmt), block, c, stream)
+    st = lib().curvefp_gemm_ws_static(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
+                                      b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
+                                      _stream(stream))
+    _check(st, what)
     return c
 
 
