@@ -1,8 +1,8 @@
 """Benchmark of the CurveFP hot path on one MI355X.
 
-One step = one pass of the whole path over one batch of the CurveFP7 E3C3
-inference workload (activations 2048 x 4096 bf16, Student-t(4) * 0.5 with 0.1 %
-outlier channels x20; weights 4096 x 4096 bf16 N(0, 0.02), both block 32):
+One step = one pass of the whole path over one batch of the largest workload,
+the 8B-shaped gate/up projection in CurveFP8 E4C3 (activations 8192 x 4096 bf16
+N(0,1), weights 14336 x 4096 bf16 N(0, 0.02), both block 32; 962.1 GFLOP):
 
     quantize(activations) -> quantize(weights) -> CurveFP GEMM -> dequantize(activation codes)
 
@@ -13,16 +13,27 @@ that is allocated before the timed region, like C); --gemm fused times the
 allocation-free curvefp_gemm instead.  Per-call times come from HIP events
 recorded on the stream the library launches on.  The roofline object is for the
 GEMM call (the dominant part: its expansion and GEMM kernels together).
-A separate streaming quantize case (1 GiB bf16 source, larger than the 256 MB
-Infinity Cache) gives the HBM figure for the quantizer, and the two backward
-GEMMs of the 7B up-projection as the paper runs them (E5C2 output gradients
-times the reused E4C3 forward codes, curvefp_gemm_mixed) are timed as
-`backward_mixed`.  The CPU oracle is timed on a bounded row sample of the same
-workload as `cpu_baseline`.  `radix_variants` times the inference operands in
-E4C3 with the three radices of the paper's radix experiment, `static_scales`
-the inference weight quantized with reconstruction-MSE scale search,
-`requant` the inference GEMM with its output requantized in the epilogue, and
-`block_sizes` the inference workload with one scale per 32, 64, 512 or K elements.
+
+Also reported, each in a key of its own:
+  configs          every configuration of the workload set timed on its own: the tiny
+                   E4C3 case, the E3C3 inference GEMM, the 7B up-projection forward
+                   (E4C3, weights quantize-transposed), its E5C2 dgrad and wgrad, and the
+                   12 GEMMs of the 8B layer sweep (QKV, O, gate/up, down x E4C3, E5C2,
+                   E3C3): quantize GB/s of both operands and GEMM TFLOP/s and roofline
+                   fraction, each the median of individually timed calls;
+  quantize_stream  a 1 GiB bf16 source (larger than the 256 MB Infinity Cache)
+                   quantized to E4C3, against 8 TB/s and against a measured 1 GiB
+                   device copy in the same run;
+  backward_mixed   the two backward GEMMs of the 7B up-projection as the paper runs
+                   them (E5C2 output gradients times the reused E4C3 forward codes);
+  radix_variants, static_scales, requant, block_sizes
+                   the inference workload in the E4C3 radix variants, with
+                   reconstruction-error scale search, with its output requantized in
+                   the epilogue, and with one scale per 32, 64, 512 or K elements;
+  cpu_baseline     the CPU oracle on a bounded row sample of the headline workload,
+                   with the host's CPU model, affinity and thread count.
+--cpu-baseline-table times the oracle on every configuration instead (full size
+for the two smallest, every 32nd row of A for the rest) and prints that table.
 """
 
 import argparse
@@ -36,6 +47,11 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "CurveFP GEMM TFLOP/s + quantize GB/s (1×MI355X, % roofline), oracle-exact"
+# the largest single-GPU configuration: the 8B gate/up projection in the forward format
+HEADLINE = "sweep_gateup_E4C3"
+SWEEPS = [f"sweep_{layer}_{fmt}" for layer in ("qkv", "o", "gateup", "down") for fmt in ("E4C3", "E5C2", "E3C3")]
+# every configuration of the workload set, in order: tiny, inference, 7B forward, dgrad, wgrad, 8B sweep
+CONFIGS = ["tiny", "inference", "fwd", "dgrad", "wgrad"] + SWEEPS
 HBM_PEAK_GBS = 8000.0
 F16_DENSE_PEAK_TFLOPS = 2500.0   # MI355X dense fp16/bf16 MFMA
 
@@ -45,7 +61,7 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
-    p.add_argument("--workload", default="inference")
+    p.add_argument("--workload", default=HEADLINE)
     p.add_argument("--gemm", choices=["ws", "fused"], default="ws",
                    help="ws: curvefp_gemm_ws with a workspace allocated before the timed region "
                         "(codes expanded once, then the GEMM); fused: curvefp_gemm (expansion inside "
@@ -62,7 +78,12 @@ def parse():
                    help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
                    help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
+    p.add_argument("--no-configs", action="store_true",
+                   help="skip the per-configuration timings (every workload of the set)")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
+    p.add_argument("--cpu-baseline-table", action="store_true",
+                   help="time the CPU oracle on every configuration (full size for the tiny and "
+                        "inference cases, every 32nd row of A otherwise), print the table, then exit")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 256 MiB device copy three times (counter calibration)")
     p.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"),
@@ -154,7 +175,7 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
     run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
-           f"--no-blocks "
+           f"--no-blocks --no-configs "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -172,7 +193,7 @@ def stream_per_dispatch(d: str, counter: str):
     files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
     if not files:
         raise SystemExit(f"no counter_collection.csv under {d}")
-    per, copy_grid, rows = {}, 0, []
+    per, copy_grid, stream_grid, rows = {}, 0, 0, []
     for f in files:
         for r in csv.DictReader(open(f)):
             if r["Counter_Name"] != counter:
@@ -184,9 +205,13 @@ def stream_per_dispatch(d: str, counter: str):
             rows.append((kind, r))
             if kind == "copy":
                 copy_grid = max(copy_grid, int(r["Grid_Size"]))
+            else:
+                stream_grid = max(stream_grid, int(r["Grid_Size"]))
     seen = set()
     for kind, r in rows:
-        if kind == "copy" and int(r["Grid_Size"]) != copy_grid:
+        # the streaming case is the largest launch of its kernel (the step's own quantizes of
+        # bf16 -> E4C3 operands use the same instantiation with smaller grids)
+        if int(r["Grid_Size"]) != (copy_grid if kind == "copy" else stream_grid):
             continue
         inst = ((kind, r["Dispatch_Id"]), r.get("Counter_Value"), r.get("Start_Timestamp"))
         if inst in seen:
@@ -325,47 +350,207 @@ def dequantize_bytes_per_elem(fmt: str) -> float:
     return (7.0 / 8.0 if fmt == "E3C3" else 1.0) + 1.0 / 32.0 + 4.0
 
 
-def cpu_baseline(w, seconds: float):
-    """The oracle, as it stands, on a row sample of the same step (quantize both
-    sampled operands, exact GEMM, dequantize); scaled to GEMM TFLOP/s."""
-    import numpy as np
-    import oracle
+def host_cpu():
+    """The host the oracle runs on: CPU model, cores this process may use, nproc."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = os.cpu_count()
+    import subprocess
+    try:
+        nproc = int(subprocess.run(["nproc"], capture_output=True, text=True, check=True).stdout.strip())
+    except (OSError, ValueError, subprocess.CalledProcessError):
+        nproc = None
+    return {"cpu_model": model, "sched_getaffinity": affinity, "nproc": nproc,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
-    f = oracle.get_format(w.fmt)
+
+def oracle_step(f, A, B):
+    """The oracle's whole step on operands A [ra, K] and B [rb, K] (K along rows): quantize both,
+    the exact phase-binned GEMM, dequantize the activation codes.  Wall time of each phase."""
+    import oracle
+    t = {}
+    t0 = time.perf_counter()
+    ca, sa = oracle.quantize(A, f)
+    t["quantize_a"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    cb, sb = oracle.quantize(B, f)
+    t["quantize_b"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.gemm_exact(ca, sa, cb, sb, f)
+    t["gemm"] = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.dequantize(ca, sa, f)
+    t["dequantize"] = time.perf_counter() - t0
+    t["total"] = sum(t.values())
+    return t
+
+
+def gemm_operands_rows(w):
+    """A and B of a workload with K along their rows (the layout the oracle quantizes)."""
+    import numpy as np
     A, B = w.operand("a"), w.operand("b")
     A = A if w.a.axis == 1 else np.ascontiguousarray(A.T)
     B = B if w.b.axis == 1 else np.ascontiguousarray(B.T)
+    return A, B
+
+
+def sampled_rows(X, step: int):
+    import numpy as np
+    return np.ascontiguousarray(X[::step]) if step > 1 else X
+
+
+def extrapolate(t, w, sa: int, sb: int):
+    """Full-step time from a run on every sa-th row of A and every sb-th row of B: the quantize
+    and dequantize phases scale with their operand's rows, the GEMM with the product count."""
+    ra, rb = -(-w.M // sa), -(-w.N // sb)
+    return (t["quantize_a"] * w.M / ra + t["quantize_b"] * w.N / rb + t["gemm"] * (w.M * w.N) / (ra * rb)
+            + t["dequantize"] * w.M / ra)
+
+
+def cpu_baseline(w, seconds: float):
+    """The oracle, as it stands, on a bounded sample of the same step: every s-th row of A and of
+    B (s a power of two, lowered until one run takes about `seconds`) -- quantize both, exact
+    phase-binned GEMM, dequantize; value = the sampled GEMM's 2 ra rb K flop over the wall time."""
+    import oracle
+
+    f = oracle.get_format(w.fmt)
+    A, B = gemm_operands_rows(w)
     nthreads = oracle.load_library().oracle_max_threads()
-
-    def run(ra, rb):
-        t0 = time.perf_counter()
-        ca, sa = oracle.quantize(np.ascontiguousarray(A[:ra]), f)
-        cb, sb = oracle.quantize(np.ascontiguousarray(B[:rb]), f)
-        oracle.gemm_exact(ca, sa, cb, sb, f)
-        oracle.dequantize(ca, sa, f)
-        return time.perf_counter() - t0
-
-    # grow the sample until one run takes about `seconds` (at most the whole workload)
-    ra, rb = 16, 64
-    t = run(ra, rb)
-    for _ in range(4):
-        if t >= 0.6 * seconds or (ra >= w.M and rb >= w.N):
+    step = 1
+    while step < 4096 and (w.M // step) * (w.N // step) * w.K > 2.0e8:
+        step *= 2
+    while True:
+        t = oracle_step(f, sampled_rows(A, step), sampled_rows(B, step))
+        if t["total"] >= 0.4 * seconds or step == 1:
             break
-        scale = min(8.0, max(1.2, (seconds / max(t, 1e-3)) ** 0.5))
-        ra = int(min(w.M, max(16, ra * scale)))
-        rb = int(min(w.N, max(64, rb * scale)))
-        t = run(ra, rb)
+        step //= 2
+    ra, rb = -(-w.M // step), -(-w.N // step)
     flops = 2.0 * ra * rb * w.K
-    return {
-        "value": flops / t / 1e12,
+    out = {
+        "value": flops / t["total"] / 1e12,
         "unit": "TFLOP/s",
         "cores": nthreads,
         "kind": "oracle",
-        "sample": f"{ra} activation rows x {rb} weight rows of {w.name} (K={w.K}): oracle quantize "
-                  f"of both samples, exact phase-binned GEMM, dequantize; {t:.1f} s wall on "
-                  f"{nthreads} threads; value = 2*{ra}*{rb}*{w.K} flop / wall",
-        "seconds": t,
+        "sample": f"every {step}th row of A and of B of {w.name} ({ra} x {rb} of the {w.M} x {w.N} outputs, "
+                  f"K={w.K}): oracle quantize of both samples, exact phase-binned GEMM, dequantize; "
+                  f"{t['total']:.1f} s wall on {nthreads} threads; value = 2*{ra}*{rb}*{w.K} flop / wall",
+        "seconds": t["total"],
+        "phases_seconds": {k: v for k, v in t.items() if k != "total"},
+        "full_step_seconds_extrapolated": extrapolate(t, w, step, step),
     }
+    out.update(host_cpu())
+    return out
+
+
+def cpu_baseline_table():
+    """The oracle's step timed on every configuration: full size for the tiny and inference cases;
+    every 32nd row of A and of B for the rest (1/1024 of the products, 1/32 of each operand's
+    quantize), with the full-size time extrapolated phase by phase."""
+    import oracle
+    from paper_2608_10010_amd import workloads as W
+
+    nthreads = oracle.load_library().oracle_max_threads()
+    rows = []
+    for name in CONFIGS:
+        w = W.get(name)
+        f = oracle.get_format(w.fmt)
+        A, B = gemm_operands_rows(w)
+        step = 1 if name in ("tiny", "inference") else 32
+        t = oracle_step(f, sampled_rows(A, step), sampled_rows(B, step))
+        ra, rb = -(-w.M // step), -(-w.N // step)
+        products = float(ra) * rb * w.K
+        rows.append({"workload": w.name, "format": w.fmt, "M": w.M, "N": w.N, "K": w.K,
+                     "row_step": step, "rows_a": ra, "rows_b": rb, "seconds": t["total"],
+                     "phases_seconds": {k: v for k, v in t.items() if k != "total"},
+                     "gemm_products_per_s": products / t["gemm"],
+                     "seconds_full": t["total"] if step == 1 else None,
+                     "seconds_full_extrapolated": extrapolate(t, w, step, step)})
+        print(json.dumps(rows[-1]), flush=True)
+    out = {"kind": "oracle", "threads": nthreads, "configs": rows}
+    out.update(host_cpu())
+    return out
+
+
+def timed_median(fn, stream, reps: int = 10, warm: int = 3):
+    """Median of `reps` individually timed calls (HIP events on the library's stream)."""
+    import numpy as np
+    import torch
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1) * 1e-3)
+    return float(np.median(ts))
+
+
+def copy_peak(dev, stream, nbytes: int = 1 << 30, reps: int = 10):
+    """A plain 1 GiB device-to-device copy (read once, written once): the achievable HBM rate on
+    this box, median of individually timed copies."""
+    import torch
+    x = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    y = torch.empty_like(x)
+    x.fill_(1)
+    t = timed_median(lambda: y.copy_(x), stream, reps)
+    del x, y
+    return {"bytes_moved": 2 * nbytes, "us": t * 1e6, "gbps": 2 * nbytes / t / 1e9,
+            "what": f"torch copy_ of a {nbytes >> 20} MiB device buffer (read + write), median of {reps}"}
+
+
+def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
+    """Every configuration timed on its own: quantize of each operand (GB/s, algorithmic bytes)
+    and the GEMM call (TFLOP/s, fraction of dense fp16 peak); medians of `reps` calls each."""
+    import torch
+    out = {}
+    for name in CONFIGS:
+        w = W.get(name)
+        tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        ta = torch.from_numpy(w.operand("a")).to(tdt).to(dev)
+        tb = torch.from_numpy(w.operand("b")).to(tdt).to(dev)
+        ca, sa = cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis)
+        cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
+        C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
+        ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if gemm_path == "ws" else None
+        t_a = timed_median(lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa),
+                           stream, reps)
+        t_b = timed_median(lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb),
+                           stream, reps)
+        if gemm_path == "ws":
+            t_g = timed_median(lambda: cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws),
+                               stream, reps)
+        else:
+            t_g = timed_median(lambda: cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C), stream, reps)
+        bpe = quantize_bytes_per_elem(w.fmt, w.dtype)
+        tf = w.flops() / t_g / 1e12
+        out[name] = {
+            "workload": w.name, "format": w.fmt, "M": w.M, "N": w.N, "K": w.K,
+            "quantize_a": {"us": t_a * 1e6, "gbps": w.M * w.K * bpe / t_a / 1e9,
+                           "axis": w.a.axis},
+            "quantize_b": {"us": t_b * 1e6, "gbps": w.N * w.K * bpe / t_b / 1e9,
+                           "axis": w.b.axis},
+            "gemm": {"us": t_g * 1e6, "gflop": w.flops() / 1e9, "tflops": tf,
+                     "frac": tf / F16_DENSE_PEAK_TFLOPS},
+        }
+        del ta, tb, ca, sa, cb, sb, C, ws
+        torch.cuda.empty_cache()
+    out["timing"] = f"median of {reps} individually timed calls each (HIP events), inputs resident in HBM"
+    out["roofline"] = (f"quantize against {HBM_PEAK_GBS / 1000:.0f} TB/s (algorithmic bytes: source + codes + "
+                       f"scales); GEMM against {F16_DENSE_PEAK_TFLOPS / 1000:.1f} PFLOP/s dense fp16 (2MNK flop)")
+    return out
 
 
 def backward_mixed(cf, W, dev, stream, reps: int = 10):
@@ -642,6 +827,9 @@ def main():
     if args.summarize_stream_pmc:
         summarize_stream_pmc(args)
         return
+    if args.cpu_baseline_table:
+        print(json.dumps(cpu_baseline_table()), flush=True)
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures one GPU only: this build has no multi-GPU path "
@@ -835,6 +1023,10 @@ def main():
         t_b2b = e0.elapsed_time(e1) / reps * 1e-3
         nbytes = xs.numel() * quantize_bytes_per_elem("E4C3", "bf16")
         gbs = nbytes / t_q / 1e9
+        del xs, cs, ss
+        torch.cuda.empty_cache()
+        # (not in the counter runs: their calibration copies must be the largest copy dispatches)
+        cp = None if args.copy_calibration else copy_peak(dev, stream)
         result["quantize_stream"] = {
             "shape": [32768, 16384], "format": "E4C3", "source_dtype": "bf16",
             "us": t_q * 1e6, "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
@@ -842,20 +1034,35 @@ def main():
             "traffic": measured_stream_traffic(),
             "timing": "median of 20 individually timed calls",
             "us_back_to_back": t_b2b * 1e6, "achieved_back_to_back": nbytes / t_b2b / 1e9,
+            "copy": cp, "frac_of_copy": gbs / cp["gbps"] if cp else None,
+            "frac_of_copy_back_to_back": nbytes / t_b2b / 1e9 / cp["gbps"] if cp else None,
         }
-        del xs, cs, ss
 
-    if not args.no_requant:
-        result["requant"] = requant(cf, w, ca, sa, cb, sb, dev, stream)
+    # the headline's buffers are no longer needed
+    del ta, tb, ca, sa, cb, sb, C, D, ws
+    torch.cuda.empty_cache()
 
-    if not args.no_static:
-        result["static_scales"] = static_scales(cf, w, tb, dev, stream)
+    if not args.no_configs:
+        result["configs"] = config_sweep(cf, W, dev, stream, args.gemm)
 
-    if not args.no_radix:
-        result["radix_variants"] = radix_variants(cf, w, ta, tb, dev, stream)
-
-    if not args.no_blocks:
-        result["block_sizes"] = block_sizes(cf, w, ta, tb, dev, stream)
+    # the adjacent variants run on the inference workload (E3C3, 2048 x 4096 x 4096)
+    if not (args.no_requant and args.no_static and args.no_radix and args.no_blocks):
+        wi = W.get("inference")
+        ti = torch.from_numpy(wi.operand("a")).to(torch.bfloat16).to(dev)
+        tw = torch.from_numpy(wi.operand("b")).to(torch.bfloat16).to(dev)
+        if not args.no_requant:
+            cia, sia = cf.curvefp_quantize(ti, wi.fmt, block_axis=wi.a.axis)
+            ciw, siw = cf.curvefp_quantize(tw, wi.fmt, block_axis=wi.b.axis)
+            result["requant"] = requant(cf, wi, cia, sia, ciw, siw, dev, stream)
+            del cia, sia, ciw, siw
+        if not args.no_static:
+            result["static_scales"] = static_scales(cf, wi, tw, dev, stream)
+        if not args.no_radix:
+            result["radix_variants"] = radix_variants(cf, wi, ti, tw, dev, stream)
+        if not args.no_blocks:
+            result["block_sizes"] = block_sizes(cf, wi, ti, tw, dev, stream)
+        del ti, tw
+        torch.cuda.empty_cache()
 
     if not args.no_backward:
         result["backward_mixed"] = backward_mixed(cf, W, dev, stream)
