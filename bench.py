@@ -78,6 +78,8 @@ def parse():
                    help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
                    help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
+    p.add_argument("--no-reference", action="store_true",
+                   help="skip the vendor fp16 GEMM (torch.matmul) of the same M, N and 3K")
     p.add_argument("--no-configs", action="store_true",
                    help="skip the per-configuration timings (every workload of the set)")
     p.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -175,7 +177,7 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
     run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
-           f"--no-blocks --no-configs "
+           f"--no-blocks --no-configs --no-reference "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -509,6 +511,25 @@ def copy_peak(dev, stream, nbytes: int = 1 << 30, reps: int = 10):
     del x, y
     return {"bytes_moved": 2 * nbytes, "us": t * 1e6, "gbps": 2 * nbytes / t / 1e9,
             "what": f"torch copy_ of a {nbytes >> 20} MiB device buffer (read + write), median of {reps}"}
+
+
+def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 10):
+    """Context for the GEMM's roofline fraction: the vendor library's plain fp16 GEMM (torch.matmul,
+    hipBLASLt) on M x N with 3K, the same matrix-core work as the CurveFP GEMM's three fp16
+    products per useful product; median of `reps` individually timed calls."""
+    import torch
+    M, N, K = w.M, w.N, 3 * w.K
+    a = torch.randn(M, K, device=dev, dtype=torch.float32).to(torch.float16).contiguous()
+    b = torch.randn(K, N, device=dev, dtype=torch.float32).to(torch.float16).contiguous()
+    c = torch.empty((M, N), device=dev, dtype=torch.float16)
+    t = timed_median(lambda: torch.matmul(a, b, out=c), stream, reps)
+    tf = 2.0 * M * N * K / t / 1e12
+    del a, b, c
+    torch.cuda.empty_cache()
+    return {"what": f"torch.matmul fp16 {M}x{N}x{K} (hipBLASLt), median of {reps}", "us": t * 1e6,
+            "tflops": tf, "frac": tf / F16_DENSE_PEAK_TFLOPS,
+            "curvefp_gemm_matrix_core_tflops": 3.0 * gemm_tflops,
+            "curvefp_vs_vendor": 3.0 * gemm_tflops / tf}
 
 
 def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
@@ -866,21 +887,31 @@ def main():
         else:
             cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
+    # The step on two streams (both at the default priority).  Its HBM-bound parts run side by
+    # side: the activations are quantized and their codes reconstructed on the main stream while
+    # the weights are quantized on the side stream; the GEMM (MFMA-bound, every SIMD's registers
+    # taken by its waves) then runs alone on the main stream once both operands' codes are there.
+    side = torch.cuda.Stream(device=dev)
+
+    def rec(ev, key, s):
+        if ev is not None:
+            ev[key].record(s)
+
     def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa)
-        if ev is not None:
-            ev[1].record(stream)
-        cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb)
-        if ev is not None:
-            ev[2].record(stream)
+        side.wait_stream(stream)
+        rec(ev, "qa0", stream)
+        cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa, stream=stream)
+        rec(ev, "qa1", stream)
+        rec(ev, "qb0", side)
+        cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb, stream=side)
+        rec(ev, "qb1", side)
+        rec(ev, "d0", stream)
+        cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D, stream=stream)
+        rec(ev, "d1", stream)
+        stream.wait_stream(side)
+        rec(ev, "g0", stream)
         gemm()
-        if ev is not None:
-            ev[3].record(stream)
-        cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D)
-        if ev is not None:
-            ev[4].record(stream)
+        rec(ev, "g1", stream)
 
     for _ in range(args.warmup):
         step()
@@ -888,7 +919,8 @@ def main():
 
     # timed region: exactly `steps` steps, synchronized on both sides; HIP events are
     # recorded on the stream the library launches on, around every kernel of every step
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    keys = ("qa", "qb", "g", "d")
+    evs = [{k + e: torch.cuda.Event(enable_timing=True) for k in keys for e in "01"} for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -896,9 +928,9 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
-    names = ["quantize_a", "quantize_b", "gemm", "dequantize"]
-    per = {n: float(np.mean([evs[i][j].elapsed_time(evs[i][j + 1]) for i in range(args.steps)]))
-           for j, n in enumerate(names)}
+    names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
+    per = {n: float(np.mean([evs[i][k + "0"].elapsed_time(evs[i][k + "1"]) for i in range(args.steps)]))
+           for n, k in names.items()}
 
     flops = w.flops()
     gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
@@ -924,7 +956,7 @@ def main():
             "format": w.fmt,
             "source_dtype": w.dtype,
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
-            "step": "quantize(act) + quantize(weight) + gemm + dequantize(act codes)",
+            "step": "[quantize(act) -> dequantize(act codes)] || quantize(weight) on two streams, then gemm",
             "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
             "gemm_path": ("curvefp_gemm_ws: codes expanded once into a workspace, then the GEMM"
                           if args.gemm == "ws" else "curvefp_gemm: expansion inside the GEMM kernel"),
@@ -942,6 +974,8 @@ def main():
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
+        "kernels_us_note": "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
+                           "gemm: main; quantize_b: side, alongside quantize_a and dequantize)",
         "gemm_tflops": gemm_tflops,
         "quantize_gbps": {
             "act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
@@ -1037,6 +1071,9 @@ def main():
             "copy": cp, "frac_of_copy": gbs / cp["gbps"] if cp else None,
             "frac_of_copy_back_to_back": nbytes / t_b2b / 1e9 / cp["gbps"] if cp else None,
         }
+
+    if not args.no_reference:
+        result["vendor_fp16_gemm_reference"] = vendor_reference(w, dev, stream, gemm_tflops)
 
     # the headline's buffers are no longer needed
     del ta, tb, ca, sa, cb, sb, C, D, ws
