@@ -216,7 +216,12 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
  * (hi.hi + hi.lo + lo.hi) accumulate in fp32, and the epilogue applies the
  * row and column scale offsets exactly.  Accumulation is fp32.  Relative
  * Frobenius error against the exact phase-binned sum is about 1e-7 on the
- * benchmark workloads.  Blocks with scale -128 contribute zero.
+ * benchmark workloads.
+ *
+ * Non-finite sources: a block with scale -128 (it held a NaN or an infinity)
+ * reconstructs to NaN, so, as deq(A) deq(B)^T in IEEE arithmetic (0 * NaN is
+ * NaN), every output in a row of A or a column (row of B) that holds such a
+ * block is NaN; the other outputs are unaffected.
  *
  * Scale-spread limit (the one place where the result can depart from the exact
  * sum by more than rounding).  Let alpha be the largest block scale of a row of
@@ -340,7 +345,8 @@ int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K);
  * cores as in curvefp_gemm_ws: every element is expanded once to an fp16 high/low
  * pair carrying its own scale relative to its row's largest, with the error bound
  * stated for curvefp_gemm.  With a_trans = b_trans = 0 and a_format == b_format the
- * result equals curvefp_gemm_ws's bit for bit.
+ * result equals curvefp_gemm_ws's bit for bit.  A GEMM row (of A or B) any of whose
+ * elements lies in a block with scale -128 gives NaN outputs, as in curvefp_gemm.
  * Errors: as curvefp_gemm_ws, plus CURVEFP_ERR_BLOCK for a trans flag other than
  * 0/1 and CURVEFP_ERR_SHAPE for a reused operand with R % G != 0, more than
  * 65535 256-row tiles of reused operands, or a workspace smaller than

@@ -21,7 +21,7 @@ from math import gcd
 import numpy as np
 
 from .formats import Format
-from .quant import code_fields
+from .quant import POISON_SCALE, code_fields
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "curvefp_oracle.c")
@@ -85,8 +85,21 @@ def gemm_exact(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: int = 3
                                _ptr(out), int(nthreads), _ptr(mc))
     if rc != 0:
         raise ValueError("oracle_gemm_exact rejected its arguments")
+    poison_rows_cols(out, a_scales, b_scales)
     if return_max_count:
         return out, int(mc[0])
+    return out
+
+
+def poison_rows_cols(out, a_scales, b_scales):
+    """C = deq(A) deq(B)^T where a block that held a NaN or an infinity reconstructs to NaN
+    (scale POISON_SCALE, Eq. curvefp-value with the non-finite reading): in IEEE arithmetic
+    every dot product that meets a NaN is NaN, zero partners included, so each row of A and
+    each row of B with a poisoned scale makes its whole row / column of C NaN."""
+    pa = np.any(np.asarray(a_scales) == POISON_SCALE, axis=1)
+    pb = np.any(np.asarray(b_scales) == POISON_SCALE, axis=1)
+    out[pa, :] = np.nan
+    out[:, pb] = np.nan
     return out
 
 
@@ -123,6 +136,7 @@ def gemm_exact_mixed(a_codes, a_scales, fmt_a: Format, b_codes, b_scales, fmt_b:
                                      M, N, kd, _ptr(out), int(nthreads), _ptr(mc))
     if rc != 0:
         raise ValueError("oracle_gemm_exact_mixed rejected its arguments")
+    poison_rows_cols(out, a_scales, b_scales)
     if return_max_count:
         return out, int(mc[0])
     return out
@@ -222,4 +236,6 @@ def gemm_exact_python(a_codes, a_scales, b_codes, b_scales, fmt: Format, block: 
                          Fraction(0))
                 v += weights[h] * mpmath.mpf(nh.numerator) / nh.denominator
             out[i, j] = float(v)
-    return out
+    blocks_a = np.asarray(a_scales)[:, : kd // block]
+    blocks_b = np.asarray(b_scales)[:, : kd // block]
+    return poison_rows_cols(out, blocks_a, blocks_b)

@@ -98,6 +98,17 @@ struct Tile {
 // sched_group_barrier masks
 constexpr int SG_VALU = 0x002, SG_MFMA = 0x008, SG_DS_RD = 0x100;
 
+// Row maxima of block scales are taken over keys: a block that held a NaN or an infinity (scale
+// -128) counts as POISON_KEY, above every scale, so a row's maximum is at least POISON_KEY exactly
+// when one of its blocks is poisoned.  Such a row's expansion then flushes every element (its
+// offsets to the maximum are hundreds of binades), and the epilogue writes NaN for each output in
+// that row or column: C = deq(A) deq(B)^T with the poisoned blocks reconstructing to NaN.
+constexpr int POISON_KEY = 0x4000;
+__device__ __forceinline__ int scale_key(int s) { return s == -128 ? POISON_KEY : s; }
+__device__ __forceinline__ float poisoned(float v, int row_max, int col_max) {
+    return (row_max >= POISON_KEY || col_max >= POISON_KEY) ? __builtin_nanf("") : v;
+}
+
 // byte offset of 16-byte chunk q (k = 8q .. 8q+7) of tile row r
 __device__ __forceinline__ int swz(int r, int q) { return r * ROW_BYTES + 16 * (q ^ (((r >> 1) ^ (r >> 3)) & 3)); }
 
@@ -244,11 +255,12 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
         const int lrow = wm * WM + 4 * (lane >> 5);
         const int lcol = wn * WN + (lane & 31);
         const int voff = (lrow * (int)ldc + lcol) * 4;
-        int beta[TN];
+        int beta[TN], bmax[TN];
         bool colok[TN];
 #pragma unroll
         for (int tj = 0; tj < TN; tj++) {
-            beta[tj] = sBeta[lcol + 32 * tj] - BIAS2;
+            bmax[tj] = sBeta[lcol + 32 * tj];
+            beta[tj] = bmax[tj] - BIAS2;
             colok[tj] = lcol + 32 * tj < colsC;
         }
         // one straight-line store sequence per case (split or not, edge columns or not)
@@ -277,6 +289,7 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
                             if (EDGE && !colok[tj]) continue;
                             float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta[tj]);
                             if (ADD) val += other[tj][r];
+                            val = poisoned(val, alr[r], bmax[tj]);
                             if (SPLIT)
                                 __builtin_amdgcn_raw_ptr_buffer_atomic_fadd_f32(val, rc, voff + 128 * tj, soff, 0);
                             else
@@ -316,6 +329,7 @@ __device__ __forceinline__ void store_tile(f32x16 (&acc)[TM][Tile<BN_>::TN], con
                                 float, __builtin_amdgcn_raw_buffer_load_b32(
                                            rq, wbase + ((ti * 4 + tj) * 4 + v / 4) * 1024 + 4 * (v % 4), 0,
                                            AUX_DEVICE_COHERENT));
+                        val = poisoned(val, sAlpha[li], beta);
                         if (split) unsafeAtomicAdd(C + gi * ldc + gj, val);
                         else C[gi * ldc + gj] = val;
                     }
@@ -460,7 +474,7 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
         int m = -128;
         auto max4 = [&](uint32_t w) {
 #pragma unroll
-            for (int bb = 0; bb < 4; bb++) m = max(m, (int)(int8_t)(w >> (8 * bb)));
+            for (int bb = 0; bb < 4; bb++) m = max(m, scale_key((int)(int8_t)(w >> (8 * bb))));
         };
         const int head = min((int)((16 - (reinterpret_cast<uintptr_t>(sp) & 15)) & 15), n);
         const int nch = (n - head) >> 4;
@@ -468,14 +482,15 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
         int hb[15], tb[15];
 #pragma unroll
         for (int i = 0; i < 15; i++) {
-            hb[i] = i < head ? (int)sp[i] : -128;
-            tb[i] = i < tail ? (int)sp[head + 16 * nch + i] : -128;
+            hb[i] = i < head ? scale_key((int)sp[i]) : -127;
+            tb[i] = i < tail ? scale_key((int)sp[head + 16 * nch + i]) : -127;
         }
         const uint4* ab = reinterpret_cast<const uint4*>(sp + head);
         for (int c = 0; c < nch; c += 8) {
             uint4 v[8];
 #pragma unroll
-            for (int u = 0; u < 8; u++) v[u] = c + u < nch ? ab[c + u] : make_uint4(0x80808080u, 0x80808080u, 0x80808080u, 0x80808080u);
+            // padding of -127: below or at every real key (scales are at least -127, -128 is the key)
+            for (int u = 0; u < 8; u++) v[u] = c + u < nch ? ab[c + u] : make_uint4(0x81818181u, 0x81818181u, 0x81818181u, 0x81818181u);
 #pragma unroll
             for (int u = 0; u < 8; u++) {
                 max4(v[u].x);
@@ -494,7 +509,10 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
 
 #pragma unroll
     for (int j = 0; j < TASKS; j++) {
-        const int al = j < 4 ? sAlpha[r0 + 64 * j] : sBeta[r0 + 64 * (j - 4)];
+        // a poisoned row expands against the largest scale (every offset D = 127 - a stays in
+        // [0, 255]); its outputs are NaN whatever it accumulates
+        const int am = j < 4 ? sAlpha[r0 + 64 * j] : sBeta[r0 + 64 * (j - 4)];
+        const int al = am >= POISON_KEY ? 127 : am;
         alpha_pk[j >> 2] |= ((uint32_t)al & 0xFFu) << (8 * (j & 3));
     }
 
@@ -687,7 +705,7 @@ __global__ __launch_bounds__(256) void prep_kernel(const int8_t* __restrict__ as
     if (row < R) {
         const int8_t* sp = s + row * nsb;
 #pragma unroll 8
-        for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, (int)sp[sb]);
+        for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, scale_key((int)sp[sb]));
     }
 #pragma unroll
     for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
@@ -758,7 +776,7 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
 #pragma unroll
                 for (int bb = 0; bb < 4; bb++) {
                     const int pos = 4 * d + bb;
-                    if (pos >= lo && pos < hi) m = max(m, (int)(int8_t)(w >> (8 * bb)));
+                    if (pos >= lo && pos < hi) m = max(m, scale_key((int)(int8_t)(w >> (8 * bb))));
                 }
             }
         }
@@ -900,6 +918,7 @@ __device__ __forceinline__ void requant_tile(f32x16 (&acc)[TM][4], const int* sA
                 for (int r = 0; r < 4; r++) {
                     float val = __builtin_amdgcn_ldexpf(acc[ti][tj][4 * g + r], alr[r] + beta);
                     if (ADD) val += other[tj][g][r];
+                    val = poisoned(val, alr[r], beta + BIAS2);
                     slice[slice_off(wm * 32 + lrow + 8 * g + r, lcol + 32 * tj)] = val;
                 }
             }
@@ -1285,7 +1304,7 @@ __global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOpe
         if (row < p.rows) {
             const int8_t* sp = p.scales + row * nsb;
 #pragma unroll 8
-            for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, (int)sp[sb]);
+            for (int64_t sb = part; sb < nsb; sb += 16) m = max(m, scale_key((int)sp[sb]));
         }
 #pragma unroll
         for (int o = 8; o > 0; o >>= 1) m = max(m, __shfl_xor(m, o, 16));
@@ -1301,7 +1320,7 @@ __global__ __launch_bounds__(256) void prep_mixed_kernel(PrepOperand pa, PrepOpe
         const int8_t* sp = p.scales + div32((uint32_t)j, p.dgq);
         const int64_t kend = min(k0 + 64, p.K);
 #pragma unroll 8
-        for (int64_t k = k0; k < kend; k++) m = max(m, (int)sp[k * p.nsb]);
+        for (int64_t k = k0; k < kend; k++) m = max(m, scale_key((int)sp[k * p.nsb]));
     }
     red[t] = m;
     __syncthreads();

@@ -906,3 +906,32 @@ def test_mse_error_sum_order():
     for v in x[0][::-1]:
         rev = rev + v * v
     assert rev == 2.0 ** 54 + 32
+
+
+@pytest.mark.parametrize("name", ["E4C3", "E5C2", "E3C3"])
+def test_gemm_nonfinite_rows_are_nan(name):
+    """A NaN or infinity in a block poisons it (scale -128, zero codes) and it reconstructs to
+    NaN; the exact GEMM is deq(A) deq(B)^T in IEEE terms, so every output in a row of A or a
+    column of B that holds a poisoned block is NaN (0 * NaN is NaN), and the other outputs are
+    the products of the finite rows, as a float64 matmul of the reconstructed values gives."""
+    f = oracle.get_format(name)
+    rng = np.random.default_rng(17)
+    A = rng.standard_normal((12, 96)).astype(np.float32)
+    B = rng.standard_normal((10, 96)).astype(np.float32)
+    A[3, 5] = np.nan
+    A[7, 70] = np.inf
+    B[2, 40] = -np.inf
+    B[:, :32] = 0.0                       # B zero under A's poisoned block of row 3
+    ca, sa = oracle.quantize(A, f)
+    cb, sb = oracle.quantize(B, f)
+    V = oracle.gemm_exact(ca, sa, cb, sb, f)
+    da, db = oracle.dequantize(ca, sa, f), oracle.dequantize(cb, sb, f)
+    nan_rows, nan_cols = np.isnan(da).any(1), np.isnan(db).any(1)
+    assert list(np.nonzero(nan_rows)[0]) == [3, 7] and list(np.nonzero(nan_cols)[0]) == [2]
+    assert np.array_equal(np.isnan(V), nan_rows[:, None] | nan_cols[None, :])
+    keep_r, keep_c = ~nan_rows, ~nan_cols
+    ref = _deq_exact64(ca[keep_r], sa[keep_r], f) @ _deq_exact64(cb[keep_c], sb[keep_c], f).T
+    assert np.allclose(V[keep_r][:, keep_c], ref, rtol=1e-13, atol=0)
+    # the tiny pure-Python oracle follows the same rule
+    Vp = oracle.gemm_exact_python(ca[:5], sa[:5], cb[:4], sb[:4], f)
+    assert np.array_equal(np.isnan(Vp), np.isnan(V[:5, :4]))
