@@ -78,6 +78,8 @@ def parse():
                    help="skip the static-scale (reconstruction-MSE search) quantize of the inference weight")
     p.add_argument("--no-radix", action="store_true",
                    help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
+    p.add_argument("--serial-step", action="store_true",
+                   help="run the step's calls one after another on one stream")
     p.add_argument("--no-reference", action="store_true",
                    help="skip the vendor fp16 GEMM (torch.matmul) of the same M, N and 3K")
     p.add_argument("--no-configs", action="store_true",
@@ -163,9 +165,8 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
     for kind in CALL_KERNELS[path] + ("copy",):
         vals = [v for (k, _), v in per.items() if k == kind]
         if not vals:
-            # zero_rows_kernel runs only when K is split; prep_kernel only when rows hold more
-            # than 128 scales (otherwise the expansion takes the row maxima itself)
-            if kind in ("zero_rows_kernel", "prep_kernel"):
+            # zero_rows_kernel runs only when K is split (fused path)
+            if kind == "zero_rows_kernel":
                 out[kind] = (0.0, 0)
                 continue
             raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
@@ -897,7 +898,24 @@ def main():
         if ev is not None:
             ev[key].record(s)
 
+    def step_serial(ev=None):
+        rec(ev, "qa0", stream)
+        cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa, stream=stream)
+        rec(ev, "qa1", stream)
+        rec(ev, "qb0", stream)
+        cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb, stream=stream)
+        rec(ev, "qb1", stream)
+        rec(ev, "d0", stream)
+        cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D, stream=stream)
+        rec(ev, "d1", stream)
+        rec(ev, "g0", stream)
+        gemm()
+        rec(ev, "g1", stream)
+
     def step(ev=None):
+        if args.serial_step:
+            step_serial(ev)
+            return
         side.wait_stream(stream)
         rec(ev, "qa0", stream)
         cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa, stream=stream)
@@ -964,8 +982,8 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": ("gemm call (expand_kernel, gemm_ws_kernel; prep_kernel first when rows hold more "
-                       "than 128 scales)" if args.gemm == "ws" else "gemm call (" + ", ".join(CALL_KERNELS["fused"]) + ")"),
+            "kernel": ("gemm call (prep_kernel, expand_kernel, gemm_ws_kernel)" if args.gemm == "ws"
+                       else "gemm call (" + ", ".join(CALL_KERNELS["fused"]) + ")"),
             "achieved": gemm_tflops,
             "peak": F16_DENSE_PEAK_TFLOPS,
             "unit": "TFLOP/s",

@@ -347,7 +347,9 @@ __global__ __launch_bounds__(NTHREADS) void gemm_kernel(
     constexpr int BN = TL::BN, WN = TL::WN, TN = TL::TN, STAGE = TL::STAGE, TASKS = TL::TASKS;
     constexpr int PLANE_B = TL::PLANE_B;
     constexpr int MFMA_PER_SUB = TL::MFMA_PER_SUB, MPG = TL::MFMA_PER_GROUP;
-    extern __shared__ __attribute__((aligned(16))) char smem[];
+    // static LDS (146 KB for 256 x 256 tiles): gfx950 has 160 KB per workgroup, and a static
+    // array needs no per-device launch attribute
+    __shared__ __attribute__((aligned(16))) char smem[TL::SMEM];
     const char* lut = smem;
     char* stage0 = smem + LUT_BYTES;
     char* stage1 = stage0 + STAGE;
@@ -680,9 +682,6 @@ WsLayout ws_layout(int64_t M, int64_t N, int64_t K) {
     return w;
 }
 
-// rows of at most this many scales skip prep_kernel: the expansion scans them itself
-constexpr int64_t EXPAND_FOLD_MAX_SCALES = 128;
-
 // one launch before the expansion: row maxima of the block scales of A (workgroups
 // [0, ga)) and of B ([ga, ga + gb)), 16 lanes per row, each over every 16th of the row's nsb
 // scales; one more workgroup zeroes the per-tile arrival counters when K is split
@@ -718,7 +717,7 @@ struct ExpandOperand {
     const uint8_t* codes;
     const int8_t* scales;
     int64_t rows, tiles;      // rows, and row tiles of 256
-    int* rmax;                // row maxima: read, or written by the first K group when folded
+    const int* rmax;          // row maxima (keys of the block scales), from prep_kernel
     char* planes;
     int fidx;                 // format: which expansion table
     int64_t nsb;              // scales per row (K / G)
@@ -727,13 +726,11 @@ struct ExpandOperand {
 
 // both operands in one launch: workgroups [0, 4 A.tiles) take A, the rest B (F fixes the code
 // packing, which both share; each operand brings its own table)
+// The row maxima come from prep_kernel (one launch over the scales): taking them inside the
+// expansion instead, by every K group over the whole row, measured slower on the large shapes
+// (8192 x 14336 x 4096: 118 us against 87 + 4 us) and even on 2048 x 4096 x 4096.
 template <class F>
-// fold != 0: no prep launch ran; every workgroup takes its rows' maxima itself (a quad of lanes
-// per row scans the row's scales), the first K group writes them for the GEMM's epilogue, and
-// workgroup (0, 0) clears the ncnt arrival counters.  Worth it while rows hold few scales: the
-// scan is repeated by every K group.
-__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb, int fold,
-                                                     int* __restrict__ cnt, int ncnt) {
+__global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOperand opB, int64_t nkb) {
     __shared__ uint32_t lut[GEMM_DEC_ENTRIES];
     const bool isA = (int64_t)blockIdx.x < 4 * opA.tiles;
     const ExpandOperand& op = isA ? opA : opB;
@@ -741,7 +738,6 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     const uint8_t* X = op.codes;
     const int8_t* Xs = op.scales;
     const int64_t R = op.rows, RT = op.tiles;
-    int* rmax = op.rmax;
     char* planes = op.planes;
     const int64_t row_bytes = F::PACKED7 ? nkb * 28 : nkb * 32;
     const int64_t r0 = (int64_t)(isA ? blockIdx.x : blockIdx.x - 4 * opA.tiles) * 64;
@@ -765,30 +761,7 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
     for (int t = 0; t < 4; t++)
         load_raw<F>(rc, rs, voff_code, (int)((kbase + t) * (F::PACKED7 ? 28 : 32)), (x + sidx(kbase + t)) & ~3, 0, q,
                     raw[t]);
-    int alpha;
-    if (fold) {
-        int m = -128;
-        if (row < R) {
-            // the row's scales are bytes [x, x + nsb) of rs: dword loads, a quad's lanes interleaved
-            const int lo = x, hi = x + (int)nsb;
-            for (int d = (lo >> 2) + q; d <= ((hi - 1) >> 2); d += 4) {
-                const uint32_t w = __builtin_amdgcn_raw_buffer_load_b32(rs, 4 * d, 0, 0);
-#pragma unroll
-                for (int bb = 0; bb < 4; bb++) {
-                    const int pos = 4 * d + bb;
-                    if (pos >= lo && pos < hi) m = max(m, scale_key((int)(int8_t)(w >> (8 * bb))));
-                }
-            }
-        }
-        m = max(m, (int)dpp_u32<QP_XOR1>((uint32_t)m));
-        m = max(m, (int)dpp_u32<QP_XOR2>((uint32_t)m));
-        alpha = row < R ? m : 0;
-        if (blockIdx.y == 0 && q == 0) rmax[row] = alpha;      // the padded rows, as prep_kernel
-        if (blockIdx.x == 0 && blockIdx.y == 0)
-            for (int i = threadIdx.x; i < ncnt; i += 256) cnt[i] = 0;
-    } else {
-        alpha = rmax[row];
-    }
+    const int alpha = op.rmax[row];   // the padded rows hold 0
     __syncthreads();
 #pragma unroll
     for (int t = 0; t < 4; t++) {
@@ -1445,16 +1418,13 @@ hipError_t launch_ws_fmt(const void* a, const int8_t* as, const void* b, const i
     const int splits = w.splits;
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
-    // rows with few scales: the expansion takes the row maxima itself (one launch fewer)
-    const int fold = nsb <= EXPAND_FOLD_MAX_SCALES ? 1 : 0;
     const int ncnt = splits > 1 ? (int)tiles : 0;
-    if (!fold)
-        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M,
-                           N, nsb, ga, gb, maxA, maxB, cnt, ncnt);
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
+                       nsb, ga, gb, maxA, maxB, cnt, ncnt);
     const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
     const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
-                       dim3(256), 0, s, opA, opB, nkb, fold, cnt, fold ? ncnt : 0);
+                       dim3(256), 0, s, opA, opB, nkb);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     const int64_t items = w.rta * w.rtb * splits;
@@ -1479,16 +1449,13 @@ hipError_t launch_requant_fmt(const void* a, const int8_t* as, const void* b, co
     const int splits = w.splits;
     int* cnt = reinterpret_cast<int*>(ws + w.cnt);
     const int ga = (int)(w.rta * BM / 16), gb = (int)(w.rtb * BM / 16);
-    // rows with few scales: the expansion takes the row maxima itself (one launch fewer)
-    const int fold = nsb <= EXPAND_FOLD_MAX_SCALES ? 1 : 0;
     const int ncnt = splits > 1 ? (int)tiles : 0;
-    if (!fold)
-        hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M,
-                           N, nsb, ga, gb, maxA, maxB, cnt, ncnt);
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)(ga + gb + (splits > 1 ? 1 : 0))), dim3(256), 0, s, as, bs, M, N,
+                       nsb, ga, gb, maxA, maxB, cnt, ncnt);
     const ExpandOperand opA = {reinterpret_cast<const uint8_t*>(a), as, M, w.rta, maxA, ws + w.planes_a, fidx, nsb, dgq};
     const ExpandOperand opB = {reinterpret_cast<const uint8_t*>(b), bs, N, w.rtb, maxB, ws + w.planes_b, fidx, nsb, dgq};
     hipLaunchKernelGGL((expand_kernel<F>), dim3((unsigned)(4 * (w.rta + w.rtb)), (unsigned)((nkb + 3) / 4)),
-                       dim3(256), 0, s, opA, opB, nkb, fold, cnt, fold ? ncnt : 0);
+                       dim3(256), 0, s, opA, opB, nkb);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     int glog = 0;
@@ -1585,8 +1552,8 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
                                N / block, dgq};
     auto expand_k = [&](const ExpandOperand& o1, const ExpandOperand& o2, bool p7) {
         const dim3 grid((unsigned)(4 * (o1.tiles + o2.tiles)), (unsigned)((nkb + 3) / 4));
-        if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb, 0, nullptr, 0);
-        else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, o1, o2, nkb, 0, nullptr, 0);
+        if (p7) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, o1, o2, nkb);
+        else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, o1, o2, nkb);
         return hipGetLastError();
     };
     auto expand_t = [&](const ExpandTOperand& o1, const ExpandTOperand& o2, bool p7) {
@@ -1615,19 +1582,7 @@ hipError_t launch_mixed(const void* a, const int8_t* as, int fa, int ta, const v
 template <class F, int BN_>
 hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int8_t* bs, int64_t M,
                        int64_t N, int64_t K, int block, float* c, int64_t ldc, int fidx, int splits, hipStream_t s) {
-    using TL = Tile<BN_>;
-    // the dynamic-LDS limit is a per-function, per-device attribute: raise it once per device
-    static bool attr_set[64] = {};
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return e;
-    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-    if (!attr_set[dev]) {
-        e = hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_kernel<F, BN_>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, TL::SMEM);
-        if (e != hipSuccess) return e;
-        attr_set[dev] = true;
-    }
+    hipError_t e = hipSuccess;
     if (splits > 1) {
         int64_t zb = (M * N + 255) / 256;
         zb = zb < 4096 ? zb : 4096;
@@ -1636,7 +1591,7 @@ hipError_t launch_tile(const void* a, const int8_t* as, const void* b, const int
         if (e != hipSuccess) return e;
     }
     dim3 grid((unsigned)((N + BN_ - 1) / BN_), (unsigned)((M + BM - 1) / BM), (unsigned)splits);
-    hipLaunchKernelGGL((gemm_kernel<F, BN_>), grid, dim3(NTHREADS), TL::SMEM, s,
+    hipLaunchKernelGGL((gemm_kernel<F, BN_>), grid, dim3(NTHREADS), 0, s,
                        reinterpret_cast<const uint8_t*>(a), as, reinterpret_cast<const uint8_t*>(b), bs,
                        M, N, K, c, ldc, fidx, K / block, make_div32((uint32_t)(block / 32)));
     return hipGetLastError();
