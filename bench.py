@@ -145,6 +145,8 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
             kind = next((k for k in CALL_KERNELS[path] if k + "<" in name or k + "(" in name), None)
             if kind is None and "copyBuffer" in name:
                 kind = "copy"
+            if kind is None and name.startswith("Cijk_"):
+                kind = "vendor"      # the vendor fp16 GEMM of the same matrix-core work
             if kind is None:
                 continue
             rows.append((kind, r))
@@ -172,13 +174,16 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
             raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
         out[kind] = (sum(vals) / len(vals), len(vals))
     out["gemm"] = (sum(out[k][0] for k in CALL_KERNELS[path]), max(out[k][1] for k in CALL_KERNELS[path]))
+    vend = [v for (k, _), v in per.items() if k == "vendor"]
+    if vend:
+        out["vendor"] = (sum(vend) / len(vend), len(vend))
     return out
 
 
 def pmc_commands(gemm: str):
     """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
     run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
-           f"--no-blocks --no-configs --no-reference "
+           f"--no-blocks --no-configs "
            f"--copy-calibration --gemm {gemm}")
     return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
@@ -283,7 +288,7 @@ def summarize_pmc(args):
     kernels = CALL_KERNELS[args.gemm]
     flag = "" if args.gemm == "ws" else " --gemm fused"
     lines = [
-        f"# HBM traffic of one CurveFP GEMM call ({args.gemm} path), {args.workload} workload",
+        f"# Memory traffic of one CurveFP GEMM call ({args.gemm} path), {args.workload} workload",
         "",
         "Commands (from the repository root on one MI355X; each pass is its own run):",
         "",
@@ -307,8 +312,24 @@ def summarize_pmc(args):
         f"Calibration: the copy reads and writes {COPY_BYTES >> 20} MiB once each; the counters "
         f"report {f_fetch:.4f}x (FETCH_SIZE) and {f_write:.4f}x (WRITE_SIZE) those bytes, and the "
         f"GEMM's counts are divided by the same factors.",
-        f"HBM traffic per GEMM call: {gemm_fetch / 1e6:.2f} MB read + {gemm_write / 1e6:.2f} MB written.",
+        f"Traffic past the L2s per GEMM call (FETCH_SIZE / WRITE_SIZE count the L2s' requests to the "
+        f"fabric, served by the 256 MB MALL or by HBM): {gemm_fetch / 1e6:.2f} MB read + "
+        f"{gemm_write / 1e6:.2f} MB written.",
         "",
+    ]
+    if "vendor" in fetch and "vendor" in write:
+        from paper_2608_10010_amd import workloads as W
+        w = W.get(args.workload)
+        vf, vw = fetch["vendor"][0] * 1024.0 / f_fetch, write["vendor"][0] * 1024.0 / f_write
+        alg = 2.0 * (w.M * 3 * w.K + 3 * w.K * w.N + w.M * w.N)
+        lines += [
+            f"For comparison, the vendor fp16 GEMM of the same matrix-core work in the same runs (torch.matmul "
+            f"{w.M} x {w.N} x {3 * w.K}, `Cijk_...`, {fetch['vendor'][1]} dispatches): {vf / 1e6:.2f} MB read + "
+            f"{vw / 1e6:.2f} MB written per call, {(vf + vw) / alg:.2f}x its own algorithmic bytes (fp16 A, B and "
+            f"C, {alg / 1e6:.1f} MB).",
+            "",
+        ]
+    lines += [
         f"traffic_bytes_per_launch={gemm_fetch + gemm_write:.0f}",
         f"fetch_bytes_per_launch={gemm_fetch:.0f}",
         f"write_bytes_per_launch={gemm_write:.0f}",
