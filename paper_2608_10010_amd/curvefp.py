@@ -112,8 +112,8 @@ def _check(st: int, what: str):
 _GPU_DEVICE_TYPES = ("cuda",)
 
 
-def _on_gpu(what: str, tensors, stream=None):
-    """All tensors on one GPU, the current device (and the stream's, when one is given)."""
+def _device_error(what, tensors, stream):
+    """The slow path of _on_gpu: name the first violation."""
     dev = None
     for name, t in tensors:
         if not isinstance(t, torch.Tensor):
@@ -130,6 +130,24 @@ def _on_gpu(what: str, tensors, stream=None):
             raise ValueError(f"{what}: operands are on {dev}, the current device is cuda:{cur}")
         if stream is not None and getattr(stream, "device", dev) != dev:
             raise ValueError(f"{what}: the stream belongs to {stream.device}, the operands to {dev}")
+
+
+def _on_gpu(what: str, tensors, stream=None):
+    """All tensors on one GPU, the current device (and the stream's, when one is given)."""
+    idx = None
+    for _, t in tensors:
+        if not isinstance(t, torch.Tensor) or not t.is_cuda:
+            if isinstance(t, torch.Tensor) and t.device.type in _GPU_DEVICE_TYPES:
+                continue             # a device the tests of these checks admit (no GPU index)
+            return _device_error(what, tensors, stream)
+        d = t.get_device()
+        if idx is None:
+            idx = d
+        elif d != idx:
+            return _device_error(what, tensors, stream)
+    if idx is not None and (idx != torch.cuda.current_device()
+                            or (stream is not None and getattr(stream, "device_index", idx) != idx)):
+        return _device_error(what, tensors, stream)
 
 
 def _dense(what: str, name: str, t: torch.Tensor, nbytes: int, dtype=None):
@@ -156,12 +174,20 @@ def _matrix(what: str, name: str, t: torch.Tensor, rows: int, cols: int, dtypes)
         raise ValueError(f"{what}: {name} rows overlap (row stride {t.stride(0)} < {cols})")
 
 
+def _codes_bytes(f: int, outer: int, k: int, block: int) -> int:
+    """curvefp_codes_bytes without the library call (the arguments' own errors are the library's
+    to report: this only sizes the buffer check)."""
+    if f == FORMATS["E3C3"]:
+        return outer * (k // 32) * 28
+    return outer * k
+
+
 def _codes_arg(what, name, t, f, outer, k, block):
-    _dense(what, name, t, curvefp_codes_bytes(f, outer, k, block), torch.uint8)
+    _dense(what, name, t, _codes_bytes(f, outer, k, block), torch.uint8)
 
 
 def _scales_arg(what, name, t, outer, k, block):
-    _dense(what, name, t, curvefp_scales_count(outer, k, block), torch.int8)
+    _dense(what, name, t, outer * (k // block) if block > 0 else 0, torch.int8)
 
 
 def _source_arg(what, src):
