@@ -504,8 +504,35 @@ def cpu_baseline_table():
     return out
 
 
-def timed_median(fn, stream, reps: int = 10, warm: int = 3):
-    """Median of `reps` individually timed calls (HIP events on the library's stream)."""
+_HOLD_CYCLES = None
+
+
+def gpu_hold(stream, us: float = 300.0):
+    """Enqueue a short spin kernel (torch's) on `stream`, so that the host has enqueued the timed
+    call and its events before the GPU reaches them: the interval between the events is then the
+    call's GPU time, without the host's time to marshal and launch it (which a caller from C or
+    from a captured graph does not pay)."""
+    import torch
+    global _HOLD_CYCLES
+    if _HOLD_CYCLES is None:
+        n = 200000
+        with torch.cuda.stream(stream):
+            torch.cuda._sleep(1000)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            torch.cuda._sleep(n)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        us_per_cycle = max(e0.elapsed_time(e1) * 1e3 / n, 1e-5)
+        _HOLD_CYCLES = int(min(max(us / us_per_cycle, 1e4), 1e8))
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(_HOLD_CYCLES)
+
+
+def timed_median(fn, stream, reps: int = 10, warm: int = 3, before=None):
+    """Median of `reps` individually timed calls: HIP events on the library's stream around each
+    call, the GPU held back by gpu_hold until both events and the call are enqueued; `before`
+    (e.g. a cache flush) runs ahead of the hold each time."""
     import numpy as np
     import torch
     for _ in range(warm):
@@ -513,6 +540,9 @@ def timed_median(fn, stream, reps: int = 10, warm: int = 3):
     torch.cuda.synchronize()
     ts = []
     for _ in range(reps):
+        if before is not None:
+            before()
+        gpu_hold(stream)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         fn()
@@ -624,18 +654,7 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
             cf.curvefp_gemm_mixed(ca, sa, w.fmt_of("a"), w.a.trans, cb, sb, w.fmt_of("b"), w.b.trans,
                                   w.M, w.N, w.K, c=C, workspace=ws)
 
-        for _ in range(3):
-            call()
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            call()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e-3)
-        t = float(np.median(ts))
+        t = timed_median(call, stream, reps)
         tf = w.flops() / t / 1e12
         out[name.split("_")[0]] = {
             "workload": w.name, "M": w.M, "N": w.N, "K": w.K,
@@ -677,18 +696,7 @@ def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 10):
             cf.curvefp_quantize(C, ofmt, block=G, codes=oc2, scales=os2)
 
         for name, fn in (("fused", fused), ("gemm_then_quantize", two_step)):
-            for _ in range(3):
-                fn()
-            torch.cuda.synchronize()
-            ts = []
-            for _ in range(reps):
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-                fn()
-                e1.record(stream)
-                torch.cuda.synchronize()
-                ts.append(e0.elapsed_time(e1) * 1e-3)
-            t = float(np.median(ts))
+            t = timed_median(fn, stream, reps)
             key = name if G == 32 else f"{name}_G{G}"
             out[key] = {"us": t * 1e6, "tflops": w.flops() / t / 1e12}
         torch.cuda.synchronize()
@@ -715,36 +723,14 @@ def static_scales(cf, w, tb, dev, stream, reps: int = 10):
                                                           codes=cm, scales=sm),
              "ceil_absmax": lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cc, scales=sc)}
     for name, fn in calls.items():
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e-3)
-        t = float(np.median(ts))
+        t = timed_median(fn, stream, reps)
         out[name] = {"us": t * 1e6, "gbps": nbytes / t / 1e9}
     out["scales_moved_frac"] = float((sm != sc).float().mean().item())
     # the same search over blocks of 64 (Sec. 4.2's PTQ setting), one thread per block of 64
     cm64, sm64 = cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4, block=64)
     fn64 = lambda: cf.curvefp_quantize_mse(tb, w.fmt, block_axis=w.b.axis, candidates=4, block=64,
                                            codes=cm64, scales=sm64)
-    for _ in range(3):
-        fn64()
-    torch.cuda.synchronize()
-    ts = []
-    for _ in range(reps):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        fn64()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ts.append(e0.elapsed_time(e1) * 1e-3)
-    t = float(np.median(ts))
+    t = timed_median(fn64, stream, reps)
     nb64 = w.N * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - 1.0 / 32.0 + 1.0 / 64.0)
     out["mse_search_G64"] = {"us": t * 1e6, "gbps": nb64 / t / 1e9}
     out["workload"] = f"{w.name} weight {w.N}x{w.K} {w.dtype} -> {w.fmt}, 4 candidate scales"
@@ -766,18 +752,7 @@ def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 10):
     ws = cf.gemm_workspace(w.M, w.N, w.K, dev)
 
     def timed(fn):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(reps):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1) * 1e-3)
-        return float(np.median(ts))
+        return timed_median(fn, stream, reps)
 
     for G in (32, 64, 512, w.K):
         ca, sa = cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, block=G)
@@ -833,18 +808,7 @@ def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 10):
         }
         t = {}
         for name, fn in calls.items():
-            for _ in range(3):
-                fn()
-            torch.cuda.synchronize()
-            ts = []
-            for _ in range(reps):
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                e0.record(stream)
-                fn()
-                e1.record(stream)
-                torch.cuda.synchronize()
-                ts.append(e0.elapsed_time(e1) * 1e-3)
-            t[name] = float(np.median(ts))
+            t[name] = timed_median(fn, stream, reps)
         p, q = cf.curvefp_format_radix(fmt)
         H = cf.curvefp_format_info(fmt)[3]
         qa = w.M * w.K * quantize_bytes_per_elem(fmt, w.dtype)
@@ -1015,6 +979,10 @@ def main():
         "kernels_us": {n: per[n] * 1e3 for n in names},
         "kernels_us_note": "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
                            "gemm: main; quantize_b: side, alongside quantize_a and dequantize)",
+        "per_call_timing": "outside the step, every figure timed per call is the median of calls each "
+                           "between HIP events on the library's stream, enqueued behind a ~0.3 ms spin "
+                           "kernel so that the GPU reaches the first event only after the host has "
+                           "enqueued the call: GPU time, without the Python binding's host time",
         "gemm_tflops": gemm_tflops,
         "quantize_gbps": {
             "act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
@@ -1035,17 +1003,7 @@ def main():
     }
     cold = {}
     for n, fn in cold_calls.items():
-        ts = []
-        for _ in range(10):
-            flush.zero_()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            fn()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            ts.append(e0.elapsed_time(e1))
-        cold[n] = float(np.median(ts)) * 1e3
+        cold[n] = timed_median(fn, stream, 10, warm=0, before=flush.zero_) * 1e6
     del flush
     result["kernels_us_cold"] = cold
     result["cold_cache"] = {
@@ -1071,21 +1029,10 @@ def main():
         xs = torch.randn((32768, 16384), generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
         cs, ss = cf.curvefp_quantize(xs, "E4C3")
         torch.cuda.synchronize()
-        # the survey's protocol: median of >= 20 individually timed calls after warm-up (each
-        # call starts from an idle stream); the mean of 10 back-to-back calls is reported too
+        # median of >= 20 individually timed calls after warm-up (each call alone on the GPU,
+        # enqueued behind a spin kernel); the mean of 10 back-to-back calls is reported too
         # (it runs hotter: on long back-to-back runs the per-call time rises by up to ~40%)
-        for _ in range(3):
-            cf.curvefp_quantize(xs, "E4C3", codes=cs, scales=ss)
-        torch.cuda.synchronize()
-        per_call = []
-        for _ in range(20):
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            cf.curvefp_quantize(xs, "E4C3", codes=cs, scales=ss)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            per_call.append(e0.elapsed_time(e1) * 1e-3)
-        t_q = float(np.median(per_call))
+        t_q = timed_median(lambda: cf.curvefp_quantize(xs, "E4C3", codes=cs, scales=ss), stream, 20)
         reps = 10
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
