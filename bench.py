@@ -62,10 +62,11 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--workload", default=HEADLINE)
-    p.add_argument("--gemm", choices=["ws", "fused"], default="ws",
-                   help="ws: curvefp_gemm_ws with a workspace allocated before the timed region "
-                        "(codes expanded once, then the GEMM); fused: curvefp_gemm (expansion inside "
-                        "the GEMM kernel, no workspace)")
+    p.add_argument("--gemm", choices=["prepared", "ws", "fused"], default="prepared",
+                   help="prepared: each operand expanded by curvefp_prepare as soon as it is quantized (on "
+                        "its own stream), then curvefp_gemm_prepared; ws: curvefp_gemm_ws (both expansions "
+                        "and the GEMM in one call) with a workspace allocated before the timed region; "
+                        "fused: curvefp_gemm (expansion inside the GEMM kernel)")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-stream", action="store_true")
     p.add_argument("--no-backward", action="store_true",
@@ -123,7 +124,11 @@ def traffic_file(workload: str, path: str = "ws") -> str:
 
 # the kernels one GEMM call launches, by path
 CALL_KERNELS = {"ws": ("prep_kernel", "expand_kernel", "gemm_ws_kernel"),
+                "prepared": ("prep_kernel", "expand_kernel", "gemm_ws_kernel"),
                 "fused": ("zero_rows_kernel", "gemm_kernel")}
+# the kernel whose traffic the roofline carries: the whole call, or (prepared operands) the
+# GEMM kernel alone, the expansions being calls of their own
+ROOFLINE_KERNELS = {"ws": CALL_KERNELS["ws"], "prepared": ("gemm_ws_kernel",), "fused": CALL_KERNELS["fused"]}
 
 
 def pmc_per_dispatch(d: str, counter: str, path: str):
@@ -164,6 +169,12 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
         seen.add(inst)
         per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
     out = {}
+    # per GEMM call: a kernel's total over its dispatches / the GEMM kernel's dispatch count (the
+    # prepared path launches prep_kernel and expand_kernel once per operand, twice per call)
+    main_kernel = CALL_KERNELS[path][-1]
+    ncalls = len([1 for (k, _) in per if k == main_kernel])
+    if ncalls == 0:
+        raise SystemExit(f"no {main_kernel} dispatches with {counter} in {d}")
     for kind in CALL_KERNELS[path] + ("copy",):
         vals = [v for (k, _), v in per.items() if k == kind]
         if not vals:
@@ -172,8 +183,9 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
                 out[kind] = (0.0, 0)
                 continue
             raise SystemExit(f"no {kind} dispatches with {counter} in {d}")
-        out[kind] = (sum(vals) / len(vals), len(vals))
-    out["gemm"] = (sum(out[k][0] for k in CALL_KERNELS[path]), max(out[k][1] for k in CALL_KERNELS[path]))
+        out[kind] = (sum(vals) / (len(vals) if kind == "copy" else ncalls), len(vals))
+    out["gemm"] = (sum(out[k][0] for k in CALL_KERNELS[path]), ncalls)
+    out["roofline"] = (sum(out[k][0] for k in ROOFLINE_KERNELS[path]), ncalls)
     vend = [v for (k, _), v in per.items() if k == "vendor"]
     if vend:
         out["vendor"] = (sum(vend) / len(vend), len(vend))
@@ -286,7 +298,9 @@ def summarize_pmc(args):
     gemm_fetch = fetch["gemm"][0] * 1024.0 / f_fetch
     gemm_write = write["gemm"][0] * 1024.0 / f_write
     kernels = CALL_KERNELS[args.gemm]
-    flag = "" if args.gemm == "ws" else " --gemm fused"
+    flag = f" --gemm {args.gemm}"
+    roof_fetch = fetch["roofline"][0] * 1024.0 / f_fetch
+    roof_write = write["roofline"][0] * 1024.0 / f_write
     lines = [
         f"# Memory traffic of one CurveFP GEMM call ({args.gemm} path), {args.workload} workload",
         "",
@@ -297,7 +311,7 @@ def summarize_pmc(args):
         f"python bench.py --summarize-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}{flag}",
         "```",
         "",
-        "| kernel | dispatches | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |",
+        "| kernel | dispatches | FETCH_SIZE KiB per call | WRITE_SIZE KiB per call |",
         "|---|---|---|---|",
     ]
     for k in kernels:
@@ -317,6 +331,14 @@ def summarize_pmc(args):
         f"{gemm_write / 1e6:.2f} MB written.",
         "",
     ]
+    if args.gemm == "prepared":
+        lines += [
+            f"The prepared path's call is curvefp_prepare of A, curvefp_prepare of B (one `prep_kernel` and one "
+            f"`expand_kernel` each: two dispatches of each per call, summed above) and curvefp_gemm_prepared "
+            f"(`gemm_ws_kernel`). The GEMM kernel alone, whose traffic the roofline carries: "
+            f"{roof_fetch / 1e6:.2f} MB read + {roof_write / 1e6:.2f} MB written.",
+            "",
+        ]
     if "vendor" in fetch and "vendor" in write:
         from paper_2608_10010_amd import workloads as W
         w = W.get(args.workload)
@@ -330,9 +352,10 @@ def summarize_pmc(args):
             "",
         ]
     lines += [
-        f"traffic_bytes_per_launch={gemm_fetch + gemm_write:.0f}",
-        f"fetch_bytes_per_launch={gemm_fetch:.0f}",
-        f"write_bytes_per_launch={gemm_write:.0f}",
+        f"traffic_bytes_per_launch={roof_fetch + roof_write:.0f}",
+        f"fetch_bytes_per_launch={roof_fetch:.0f}",
+        f"write_bytes_per_launch={roof_write:.0f}",
+        f"call_traffic_bytes={gemm_fetch + gemm_write:.0f}",
         f"kernel_source_sha256={kernel_source_digest()}",
     ]
     print("\n".join(lines))
@@ -586,7 +609,9 @@ def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 10):
 
 def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
     """Every configuration timed on its own: quantize of each operand (GB/s, algorithmic bytes)
-    and the GEMM call (TFLOP/s, fraction of dense fp16 peak); medians of `reps` calls each."""
+    and the GEMM call (TFLOP/s, fraction of dense fp16 peak: curvefp_gemm_ws, expansion included,
+    or curvefp_gemm); with prepared operands also each operand's curvefp_prepare and the
+    curvefp_gemm_prepared call alone; medians of `reps` calls each."""
     import torch
     out = {}
     for name in CONFIGS:
@@ -597,12 +622,12 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
         ca, sa = cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis)
         cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
         C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
-        ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if gemm_path == "ws" else None
+        ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if gemm_path in ("ws", "prepared") else None
         t_a = timed_median(lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa),
                            stream, reps)
         t_b = timed_median(lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb),
                            stream, reps)
-        if gemm_path == "ws":
+        if gemm_path in ("ws", "prepared"):
             t_g = timed_median(lambda: cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws),
                                stream, reps)
         else:
@@ -618,6 +643,21 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
             "gemm": {"us": t_g * 1e6, "gflop": w.flops() / 1e9, "tflops": tf,
                      "frac": tf / F16_DENSE_PEAK_TFLOPS},
         }
+        if gemm_path == "prepared":
+            pa = cf.curvefp_prepare(ca, sa, w.M, w.K, w.fmt)
+            pb = cf.curvefp_prepare(cb, sb, w.N, w.K, w.fmt)
+            nws = cf.curvefp_gemm_prepared_workspace_bytes(w.M, w.N, w.K)
+            gws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
+            t_pa = timed_median(lambda: cf.curvefp_prepare(ca, sa, w.M, w.K, w.fmt, prepared=pa), stream, reps)
+            t_pb = timed_median(lambda: cf.curvefp_prepare(cb, sb, w.N, w.K, w.fmt, prepared=pb), stream, reps)
+            t_gp = timed_median(lambda: cf.curvefp_gemm_prepared(pa, w.fmt, pb, w.fmt, w.M, w.N, w.K, c=C,
+                                                                 workspace=gws), stream, reps)
+            tfp = w.flops() / t_gp / 1e12
+            out[name].update({
+                "prepare_a": {"us": t_pa * 1e6}, "prepare_b": {"us": t_pb * 1e6},
+                "gemm_prepared": {"us": t_gp * 1e6, "tflops": tfp, "frac": tfp / F16_DENSE_PEAK_TFLOPS},
+            })
+            del pa, pb, gws
         del ta, tb, ca, sa, cb, sb, C, ws
         torch.cuda.empty_cache()
     out["timing"] = f"median of {reps} individually timed calls each (HIP events), inputs resident in HBM"
@@ -864,19 +904,35 @@ def main():
     cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
     C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
     D = torch.empty((outer_a, ka), dtype=torch.float32, device=dev)
-    # the workspace is allocated once, like C: the timed calls only use it
+    # workspaces and prepared buffers are allocated once, like C: the timed calls only use them
+    prepared = args.gemm == "prepared"
     ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if args.gemm == "ws" else None
+    pa = pb = gws = None
+    if prepared:
+        pa = torch.empty(cf.curvefp_prepared_bytes(w.M, w.K), dtype=torch.uint8, device=dev)
+        pb = torch.empty(cf.curvefp_prepared_bytes(w.N, w.K), dtype=torch.uint8, device=dev)
+        nws = cf.curvefp_gemm_prepared_workspace_bytes(w.M, w.N, w.K)
+        gws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
+
+    def prepare_a(s=None):
+        cf.curvefp_prepare(ca, sa, w.M, w.K, w.fmt, prepared=pa, stream=s)
+
+    def prepare_b(s=None):
+        cf.curvefp_prepare(cb, sb, w.N, w.K, w.fmt, prepared=pb, stream=s)
 
     def gemm():
-        if args.gemm == "ws":
+        if prepared:
+            cf.curvefp_gemm_prepared(pa, w.fmt, pb, w.fmt, w.M, w.N, w.K, c=C, workspace=gws)
+        elif args.gemm == "ws":
             cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws)
         else:
             cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
     # The step on two streams (both at the default priority).  Its HBM-bound parts run side by
-    # side: the activations are quantized and their codes reconstructed on the main stream while
-    # the weights are quantized on the side stream; the GEMM (MFMA-bound, every SIMD's registers
-    # taken by its waves) then runs alone on the main stream once both operands' codes are there.
+    # side: the activations are quantized, expanded for the GEMM (prepared path) and their codes
+    # reconstructed on the main stream while the weights are quantized and expanded on the side
+    # stream; the GEMM (MFMA-bound, every SIMD's registers taken by its waves) then runs alone on
+    # the main stream once both operands are there.
     side = torch.cuda.Stream(device=dev)
 
     def rec(ev, key, s):
@@ -890,6 +946,13 @@ def main():
         rec(ev, "qb0", stream)
         cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb, stream=stream)
         rec(ev, "qb1", stream)
+        if prepared:
+            rec(ev, "pa0", stream)
+            prepare_a(stream)
+            rec(ev, "pa1", stream)
+            rec(ev, "pb0", stream)
+            prepare_b(stream)
+            rec(ev, "pb1", stream)
         rec(ev, "d0", stream)
         cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D, stream=stream)
         rec(ev, "d1", stream)
@@ -908,6 +971,13 @@ def main():
         rec(ev, "qb0", side)
         cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb, stream=side)
         rec(ev, "qb1", side)
+        if prepared:
+            rec(ev, "pa0", stream)
+            prepare_a(stream)
+            rec(ev, "pa1", stream)
+            rec(ev, "pb0", side)
+            prepare_b(side)
+            rec(ev, "pb1", side)
         rec(ev, "d0", stream)
         cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D, stream=stream)
         rec(ev, "d1", stream)
@@ -922,7 +992,7 @@ def main():
 
     # timed region: exactly `steps` steps, synchronized on both sides; HIP events are
     # recorded on the stream the library launches on, around every kernel of every step
-    keys = ("qa", "qb", "g", "d")
+    keys = ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
     evs = [{k + e: torch.cuda.Event(enable_timing=True) for k in keys for e in "01"} for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -932,6 +1002,8 @@ def main():
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
     names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
+    if prepared:
+        names.update({"prepare_a": "pa", "prepare_b": "pb"})
     per = {n: float(np.mean([evs[i][k + "0"].elapsed_time(evs[i][k + "1"]) for i in range(args.steps)]))
            for n, k in names.items()}
 
@@ -940,6 +1012,12 @@ def main():
     qa_bytes = outer_a * ka * quantize_bytes_per_elem(w.fmt, w.dtype)
     qb_bytes = w.N * w.K * quantize_bytes_per_elem(w.fmt, w.dtype)
     dq_bytes = outer_a * ka * dequantize_bytes_per_elem(w.fmt)
+    # a prepared operand's algorithmic bytes: its codes and scales read, its planes (4 bytes per
+    # element of the rows padded to 256) and row maxima written
+    pa_bytes = w.M * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - (2.0 if w.dtype == "bf16" else 4.0)) + \
+        cf.curvefp_prepared_bytes(w.M, w.K)
+    pb_bytes = w.N * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - (2.0 if w.dtype == "bf16" else 4.0)) + \
+        cf.curvefp_prepared_bytes(w.N, w.K)
 
     result = {
         "metric": METRIC,
@@ -959,16 +1037,21 @@ def main():
             "format": w.fmt,
             "source_dtype": w.dtype,
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
-            "step": "[quantize(act) -> dequantize(act codes)] || quantize(weight) on two streams, then gemm",
+            "step": ("[quantize(act) -> prepare(act) -> dequantize(act codes)] || [quantize(weight) -> "
+                     "prepare(weight)] on two streams, then gemm_prepared" if prepared else
+                     "[quantize(act) -> dequantize(act codes)] || quantize(weight) on two streams, then gemm"),
             "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
-            "gemm_path": ("curvefp_gemm_ws: codes expanded once into a workspace, then the GEMM"
-                          if args.gemm == "ws" else "curvefp_gemm: expansion inside the GEMM kernel"),
+            "gemm_path": {"prepared": "curvefp_prepare of each operand (its codes expanded once into fp16 "
+                                      "hi/lo planes), then curvefp_gemm_prepared",
+                          "ws": "curvefp_gemm_ws: codes expanded once into a workspace, then the GEMM",
+                          "fused": "curvefp_gemm: expansion inside the GEMM kernel"}[args.gemm],
             "parallelism": "single GPU",
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": ("gemm call (prep_kernel, expand_kernel, gemm_ws_kernel)" if args.gemm == "ws"
-                       else "gemm call (" + ", ".join(CALL_KERNELS["fused"]) + ")"),
+            "kernel": {"prepared": "gemm_ws_kernel (the curvefp_gemm_prepared call)",
+                       "ws": "gemm call (prep_kernel, expand_kernel, gemm_ws_kernel)",
+                       "fused": "gemm call (" + ", ".join(CALL_KERNELS["fused"]) + ")"}[args.gemm],
             "achieved": gemm_tflops,
             "peak": F16_DENSE_PEAK_TFLOPS,
             "unit": "TFLOP/s",
@@ -977,8 +1060,11 @@ def main():
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
-        "kernels_us_note": "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
-                           "gemm: main; quantize_b: side, alongside quantize_a and dequantize)",
+        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_a, prepare_a, "
+                            "dequantize, gemm: main; quantize_b, prepare_b: side, alongside the main "
+                            "stream's calls before the GEMM)" if prepared else
+                            "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
+                            "gemm: main; quantize_b: side, alongside quantize_a and dequantize)"),
         "per_call_timing": "outside the step, every figure timed per call is the median of calls each "
                            "between HIP events on the library's stream, enqueued behind a ~0.3 ms spin "
                            "kernel so that the GPU reaches the first event only after the host has "
@@ -990,6 +1076,10 @@ def main():
         },
         "dequantize_gbps": dq_bytes / (per["dequantize"] * 1e-3) / 1e9,
     }
+    if prepared:
+        result["prepare_gbps"] = {"act": pa_bytes / (per["prepare_a"] * 1e-3) / 1e9,
+                                  "weight": pb_bytes / (per["prepare_b"] * 1e-3) / 1e9,
+                                  "bytes": "codes + scales read, planes + row maxima written"}
 
     # The step above runs back to back on the same inputs, so sources that fit the 256 MB MALL
     # may be served from it.  Each call again on its own after a 512 MiB write that evicts the
@@ -1001,6 +1091,8 @@ def main():
         "gemm": gemm,
         "dequantize": lambda: cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D),
     }
+    if prepared:
+        cold_calls.update({"prepare_a": prepare_a, "prepare_b": prepare_b})
     cold = {}
     for n, fn in cold_calls.items():
         cold[n] = timed_median(fn, stream, 10, warm=0, before=flush.zero_) * 1e6
@@ -1013,6 +1105,9 @@ def main():
         "dequantize_gbps": dq_bytes / (cold["dequantize"] * 1e-6) / 1e9,
         "protocol": "each call alone after a 512 MiB device write (MALL and L2 evicted), median of 10",
     }
+    if prepared:
+        result["cold_cache"]["prepare_gbps"] = {"act": pa_bytes / (cold["prepare_a"] * 1e-6) / 1e9,
+                                                "weight": pb_bytes / (cold["prepare_b"] * 1e-6) / 1e9}
 
     if args.copy_calibration:
         xc = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)

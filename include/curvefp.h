@@ -272,6 +272,62 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
                     float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
                     void* stream);
 
+/*
+ * Prepared operands: the staging step of curvefp_gemm_ws as a call of its own.  The GEMM
+ * (Sec. 3.3, Eq. binned-accumulation) needs each operand's codes expanded into fp16 high/low
+ * planes relative to its rows' largest block scales; that expansion depends on the operand
+ * alone.  curvefp_prepare writes it for one operand into a caller-owned buffer, and
+ * curvefp_gemm_prepared multiplies two prepared operands.  An operand that several products
+ * share (static weights, Sec. 3.1) is then expanded once, and the two operands of one product
+ * can be expanded on two streams, each as soon as it is quantized.
+ * prepare(A), prepare(B), gemm_prepared give the C of curvefp_gemm_ws (and, for two formats,
+ * of curvefp_gemm_mixed with trans_a = trans_b = 0) bit for bit.
+ *
+ * curvefp_prepared_bytes: bytes of the prepared form of a [rows][k] operand (4 bytes per
+ * element with rows padded to a multiple of 256, plus one int32 per padded row).  Returns
+ * CURVEFP_ERR_SHAPE for non-positive sizes or k not a multiple of 32.
+ */
+int64_t curvefp_prepared_bytes(int64_t rows, int64_t k);
+
+/*
+ * Expand one operand: codes [rows][k] (k-contiguous; E3C3 28 bytes per 32 codes) and block
+ * scales [rows][k/block] of a tensor quantized along k by curvefp_quantize, in `format`, into
+ * `prepared` (device, 256-byte aligned, at least curvefp_prepared_bytes(rows, k) bytes,
+ * passed in prepared_size).  The buffer is overwritten with the expansion of the codes and
+ * scales as they are when the call runs; it does not record its shape or format, so the GEMM
+ * that reads it must be given the same rows (M or N), k and format.  Asynchronous on `stream`
+ * (null: the null stream).
+ * Errors: CURVEFP_ERR_NULL, _FORMAT, _BLOCK (block not a positive multiple of 32), _SHAPE
+ * (non-positive sizes, k % block, prepared_size too small), _ALIGN (codes not 16-byte or
+ * prepared not 256-byte aligned), _HIP (a launch failed).
+ */
+int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t k,
+                    int format, int block, void* prepared, int64_t prepared_size, void* stream);
+
+/*
+ * Bytes of device workspace curvefp_gemm_prepared needs for an M x N x K product: 0 unless K
+ * is split in two (fewer than 256 output tiles of 256 x 256 and K >= 512; then one arrival
+ * counter per tile and 512 KiB of partial sums per tile).  CURVEFP_ERR_SHAPE for non-positive
+ * sizes or K not a multiple of 32.
+ */
+int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K);
+
+/*
+ * C[M][N] = deq(A) deq(B)^T in fp32 (the contract of curvefp_gemm, including its non-finite
+ * and scale-spread clauses) from A prepared as [M][K] in format_a and B prepared as [N][K] in
+ * format_b (each by curvefp_prepare; the two formats may differ).  c is [M][ldc] fp32,
+ * overwritten.  workspace: at least curvefp_gemm_prepared_workspace_bytes(M, N, K) bytes,
+ * 256-byte aligned (may be null when that is 0); its contents are scratch, so calls that share
+ * it must be ordered.  The prepared buffers are only read: one prepared operand may serve
+ * concurrent calls.  Errors: CURVEFP_ERR_NULL, _FORMAT, _SHAPE (non-positive sizes, K % 32,
+ * ldc < N, workspace too small), _ALIGN (prepared buffers or workspace not 256-byte aligned,
+ * c not 16-byte aligned), _HIP.
+ */
+int curvefp_gemm_prepared(const void* a_prepared, int format_a,
+                          const void* b_prepared, int format_b,
+                          int64_t M, int64_t N, int64_t K, float* c, int64_t ldc,
+                          void* workspace, int64_t workspace_bytes, void* stream);
+
 /* Bytes of the device scratch curvefp_gemm_ws_static uses on each GPU. */
 #define CURVEFP_STATIC_SCRATCH_BYTES ((int64_t)128 << 20)
 

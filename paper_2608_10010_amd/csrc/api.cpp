@@ -194,6 +194,44 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
+int64_t curvefp_prepared_bytes(int64_t rows, int64_t k) {
+    if (rows <= 0 || k <= 0 || k % 32) return CURVEFP_ERR_SHAPE;
+    return prepared_bytes(rows, k);
+}
+
+int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t k, int format, int block,
+                    void* prepared, int64_t prepared_size, void* stream) {
+    if (!codes || !scales || !prepared) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || k <= 0 || k % block) return CURVEFP_ERR_SHAPE;
+    if (prepared_size < prepared_bytes(rows, k)) return CURVEFP_ERR_SHAPE;
+    if (!aligned16(codes) || reinterpret_cast<uintptr_t>(prepared) % 256) return CURVEFP_ERR_ALIGN;
+    return hip_status(launch_prepare(codes, scales, rows, k, format, block, prepared,
+                                     reinterpret_cast<hipStream_t>(stream)));
+}
+
+int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) {
+    if (M <= 0 || N <= 0 || K <= 0 || K % 32) return CURVEFP_ERR_SHAPE;
+    return gemm_prepared_workspace_bytes(M, N, K);
+}
+
+int curvefp_gemm_prepared(const void* a_prepared, int format_a, const void* b_prepared, int format_b, int64_t M,
+                          int64_t N, int64_t K, float* c, int64_t ldc, void* workspace, int64_t workspace_bytes,
+                          void* stream) {
+    if (!a_prepared || !b_prepared || !c) return CURVEFP_ERR_NULL;
+    if (!fmt_ok(format_a) || !fmt_ok(format_b)) return CURVEFP_ERR_FORMAT;
+    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    const int64_t need = gemm_prepared_workspace_bytes(M, N, K);
+    if (need > 0 && !workspace) return CURVEFP_ERR_NULL;
+    if (workspace_bytes < need) return CURVEFP_ERR_SHAPE;
+    if (reinterpret_cast<uintptr_t>(a_prepared) % 256 || reinterpret_cast<uintptr_t>(b_prepared) % 256 ||
+        !aligned16(c) || reinterpret_cast<uintptr_t>(workspace) % 256)
+        return CURVEFP_ERR_ALIGN;
+    return hip_status(launch_gemm_prepared(a_prepared, format_a, b_prepared, format_b, M, N, K, c, ldc, workspace,
+                                           reinterpret_cast<hipStream_t>(stream)));
+}
+
 int curvefp_gemm_ws_static(const void* a_codes, const int8_t* a_scales, const void* b_codes,
                            const int8_t* b_scales, int64_t M, int64_t N, int64_t K, int format, int block, float* c,
                            int64_t ldc, void* stream) {

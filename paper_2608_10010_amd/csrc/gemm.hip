@@ -1608,9 +1608,98 @@ hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8
     return launch_tile<F, 256>(a, as, b, bs, M, N, K, block, c, ldc, fidx, splits, s);
 }
 
+// Prepared operands: one operand's expansion in a buffer of its own, so that an operand several
+// GEMMs share (static weights) is expanded once, and the two operands can be expanded on two
+// streams as soon as each is quantized.  Layout for [rows][K] codes quantized along K: the planes
+// [K/32][RT][hi, lo][256 rows][64 B] (RT = ceil(rows / 256)), exactly the workspace path's
+// planes of that operand, then the row maxima of its block scales (prep_kernel's keys), RT * 256
+// int32.  The expansion depends on the operand alone, so prepare(A), prepare(B) and
+// gemm_prepared give curvefp_gemm_ws's C bit for bit.
+struct PreparedLayout {
+    int64_t rt, planes, rmax, bytes;
+};
+
+PreparedLayout prepared_layout(int64_t rows, int64_t K) {
+    PreparedLayout p;
+    p.rt = (rows + BM - 1) / BM;
+    p.planes = 0;
+    p.rmax = (K / 32) * p.rt * 2 * PLANE;
+    p.bytes = p.rmax + p.rt * BM * 4;
+    return p;
+}
+
+// the workspace of a GEMM on prepared operands: nothing unless K is split (then the arrival
+// counters and partial-sum slots of the workspace path)
+struct PreparedGemmLayout {
+    int64_t cnt, part, bytes;
+    int splits;
+};
+
+PreparedGemmLayout prepared_gemm_layout(int64_t M, int64_t N, int64_t K) {
+    const WsLayout w = ws_layout(M, N, K);
+    PreparedGemmLayout g;
+    g.splits = w.splits;
+    g.cnt = g.part = g.bytes = 0;
+    if (g.splits > 1) {
+        const int64_t tiles = w.rta * w.rtb;
+        g.part = (tiles * 4 + 255) & ~(int64_t)255;
+        g.bytes = g.part + tiles * g.splits * PART_BYTES;
+    }
+    return g;
+}
+
 }  // namespace
 
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout(M, N, K).bytes; }
+
+int64_t prepared_bytes(int64_t rows, int64_t K) { return prepared_layout(rows, K).bytes; }
+
+int64_t gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) { return prepared_gemm_layout(M, N, K).bytes; }
+
+hipError_t launch_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t K, int format, int block,
+                          void* prepared, hipStream_t s) {
+    const PreparedLayout p = prepared_layout(rows, K);
+    const int64_t nkb = K / 32, nsb = K / block;
+    char* base = reinterpret_cast<char*>(prepared);
+    int* rmax = reinterpret_cast<int*>(base + p.rmax);
+    const int groups = (int)(p.rt * BM / 16);
+    hipLaunchKernelGGL(prep_kernel, dim3((unsigned)groups), dim3(256), 0, s, scales, (const int8_t*)nullptr, rows,
+                       (int64_t)0, nsb, groups, 0, rmax, (int*)nullptr, (int*)nullptr, 0);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const ExpandOperand op = {reinterpret_cast<const uint8_t*>(codes), scales, rows, p.rt, rmax, base + p.planes,
+                              format, nsb, make_div32((uint32_t)(block / 32))};
+    ExpandOperand none = op;
+    none.tiles = 0;   // no second operand: no workgroups
+    // the kernel's format parameter fixes only the code packing; the table is the operand's
+    const dim3 grid((unsigned)(4 * p.rt), (unsigned)((nkb + 3) / 4));
+    if (format == 2) hipLaunchKernelGGL((expand_kernel<FmtE3C3>), grid, dim3(256), 0, s, op, none, nkb);
+    else hipLaunchKernelGGL((expand_kernel<FmtE4C3>), grid, dim3(256), 0, s, op, none, nkb);
+    return hipGetLastError();
+}
+
+hipError_t launch_gemm_prepared(const void* pa, int fa, const void* pb, int fb, int64_t M, int64_t N, int64_t K,
+                                float* c, int64_t ldc, void* ws, hipStream_t s) {
+    const PreparedLayout la = prepared_layout(M, K), lb = prepared_layout(N, K);
+    const PreparedGemmLayout g = prepared_gemm_layout(M, N, K);
+    const char* a = reinterpret_cast<const char*>(pa);
+    const char* b = reinterpret_cast<const char*>(pb);
+    const int64_t tiles = la.rt * lb.rt;
+    char* w = reinterpret_cast<char*>(ws);
+    int* cnt = g.splits > 1 ? reinterpret_cast<int*>(w + g.cnt) : nullptr;
+    if (g.splits > 1) {
+        // prep_kernel with no operands: its one extra workgroup clears the arrival counters
+        hipLaunchKernelGGL(prep_kernel, dim3(1), dim3(256), 0, s, (const int8_t*)nullptr, (const int8_t*)nullptr,
+                           (int64_t)0, (int64_t)0, (int64_t)0, 0, 0, (int*)nullptr, (int*)nullptr, cnt, (int)tiles);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    const int64_t items = tiles * g.splits;
+    const dim3 grid((unsigned)((items + 7) / 8 * 8));
+    return launch_gemm_ws_bias(gemm_bias(fa) + gemm_bias(fb), grid, s, a + la.planes, b + lb.planes,
+                               reinterpret_cast<const int*>(a + la.rmax), reinterpret_cast<const int*>(b + lb.rmax),
+                               M, N, K, la.rt, lb.rt, c, ldc, g.splits, g.splits > 1 ? w + g.part : nullptr, cnt);
+}
 
 int64_t gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) { return mixed_layout(M, N, K).bytes; }
 

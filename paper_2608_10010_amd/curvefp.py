@@ -73,6 +73,14 @@ def lib() -> ctypes.CDLL:
         L.curvefp_gemm_ws.restype = I
         L.curvefp_gemm_ws_static.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
         L.curvefp_gemm_ws_static.restype = I
+        L.curvefp_prepared_bytes.argtypes = [I64, I64]
+        L.curvefp_prepared_bytes.restype = I64
+        L.curvefp_prepare.argtypes = [P, P, I64, I64, I, I, P, I64, P]
+        L.curvefp_prepare.restype = I
+        L.curvefp_gemm_prepared_workspace_bytes.argtypes = [I64, I64, I64]
+        L.curvefp_gemm_prepared_workspace_bytes.restype = I64
+        L.curvefp_gemm_prepared.argtypes = [P, I, P, I, I64, I64, I64, P, I64, P, I64, P]
+        L.curvefp_gemm_prepared.restype = I
         L.curvefp_gemm_requant.argtypes = [P, P, P, P, I64, I64, I64, I, I, I, I, P, P, P, I64, P]
         L.curvefp_gemm_requant.restype = I
         L.curvefp_gemm_mixed_workspace_bytes.argtypes = [I64, I64, I64]
@@ -461,6 +469,65 @@ def curvefp_gemm_ws_static(a_codes: torch.Tensor, a_scales: torch.Tensor, b_code
     st = lib().curvefp_gemm_ws_static(a_codes.data_ptr(), a_scales.data_ptr(), b_codes.data_ptr(),
                                       b_scales.data_ptr(), M, N, K, _fmt(fmt), block, c.data_ptr(), c.stride(0),
                                       _stream(stream))
+    _check(st, what)
+    return c
+
+
+def curvefp_prepared_bytes(rows: int, k: int) -> int:
+    n = lib().curvefp_prepared_bytes(rows, k)
+    if n < 0:
+        raise CurveFPError(n, "curvefp_prepared_bytes")
+    return n
+
+
+def curvefp_prepare(codes: torch.Tensor, scales: torch.Tensor, rows: int, k: int, fmt, block: int = 32,
+                    prepared: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The expansion of one GEMM operand (codes of a [rows, k] tensor quantized along k) into a
+    prepared buffer (uint8, allocated here when not given) for curvefp_gemm_prepared."""
+    what = "curvefp_prepare"
+    f = _fmt(fmt)
+    if prepared is None:
+        _on_gpu(what, [("codes", codes)], stream)
+        prepared = torch.empty(curvefp_prepared_bytes(rows, k), dtype=torch.uint8, device=codes.device)
+    _on_gpu(what, [("codes", codes), ("scales", scales), ("prepared", prepared)], stream)
+    _codes_arg(what, "codes", codes, f, rows, k, block)
+    _scales_arg(what, "scales", scales, rows, k, block)
+    _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k))
+    st = lib().curvefp_prepare(codes.data_ptr(), scales.data_ptr(), rows, k, f, block, prepared.data_ptr(),
+                               prepared.numel() * prepared.element_size(), _stream(stream))
+    _check(st, what)
+    return prepared
+
+
+def curvefp_gemm_prepared_workspace_bytes(M: int, N: int, K: int) -> int:
+    n = lib().curvefp_gemm_prepared_workspace_bytes(M, N, K)
+    if n < 0:
+        raise CurveFPError(n, "curvefp_gemm_prepared_workspace_bytes")
+    return n
+
+
+def curvefp_gemm_prepared(a_prepared: torch.Tensor, fmt_a, b_prepared: torch.Tensor, fmt_b, M: int, N: int,
+                          K: int, c: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                          stream=None) -> torch.Tensor:
+    """C[M, N] = deq(A) deq(B)^T from A prepared as [M, K] in fmt_a and B as [N, K] in fmt_b."""
+    what = "curvefp_gemm_prepared"
+    _on_gpu(what, [("a_prepared", a_prepared)], stream)
+    if c is None:
+        c = torch.empty((M, N), dtype=torch.float32, device=a_prepared.device)
+    need = curvefp_gemm_prepared_workspace_bytes(M, N, K)
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=a_prepared.device)
+    ts = [("a_prepared", a_prepared), ("b_prepared", b_prepared), ("c", c)]
+    _on_gpu(what, ts + ([("workspace", workspace)] if workspace is not None else []), stream)
+    _dense(what, "a_prepared", a_prepared, curvefp_prepared_bytes(M, K))
+    _dense(what, "b_prepared", b_prepared, curvefp_prepared_bytes(N, K))
+    _matrix(what, "c", c, M, N, (torch.float32,))
+    ws_ptr, ws_bytes = 0, 0
+    if workspace is not None:
+        _dense(what, "workspace", workspace, need)
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    st = lib().curvefp_gemm_prepared(a_prepared.data_ptr(), _fmt(fmt_a), b_prepared.data_ptr(), _fmt(fmt_b), M, N,
+                                     K, c.data_ptr(), c.stride(0), ws_ptr or None, ws_bytes, _stream(stream))
     _check(st, what)
     return c
 

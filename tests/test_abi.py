@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 19
+    assert len(names) == 23
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -203,6 +203,56 @@ def test_gemm_ws_validation(L):
     assert g(*bad) == EFMT
     bad = list(args); bad[6] = 40
     assert g(*bad) == ESHAPE
+
+
+def test_prepared_validation(L):
+    assert L.curvefp_prepared_bytes(0, 64) == ESHAPE
+    assert L.curvefp_prepared_bytes(10, 48) == ESHAPE
+    # rows padded to 256: 256 rows x K x 4 bytes of planes + one int32 per padded row
+    assert L.curvefp_prepared_bytes(10, 64) == 256 * 64 * 4 + 256 * 4
+    assert L.curvefp_prepared_bytes(300, 64) == 512 * 64 * 4 + 512 * 4
+    need = L.curvefp_prepared_bytes(64, 64)
+    PR = 1 << 24                     # 256-byte aligned, never dereferenced
+    p = L.curvefp_prepare
+    args = [FAKE, FAKE, 64, 64, 0, 32, PR, need, None]
+    for i in (0, 1, 6):
+        a = list(args)
+        a[i] = None
+        assert p(*a) == ENULL, i
+    bad = list(args); bad[7] = need - 1
+    assert p(*bad) == ESHAPE
+    bad = list(args); bad[6] = PR + 128
+    assert p(*bad) == EALIGN
+    bad = list(args); bad[4] = 5
+    assert p(*bad) == EFMT
+    bad = list(args); bad[5] = 48
+    assert p(*bad) == EBLOCK
+    bad = list(args); bad[3] = 96                  # K % block
+    assert p(*bad) == ESHAPE
+    # the GEMM on prepared operands: no workspace unless K is split
+    assert L.curvefp_gemm_prepared_workspace_bytes(64, 64, 0) == ESHAPE
+    assert L.curvefp_gemm_prepared_workspace_bytes(64, 64, 64) == 0
+    assert L.curvefp_gemm_prepared_workspace_bytes(64, 64, 1024) > 0          # one tile, K split in two
+    assert L.curvefp_gemm_prepared_workspace_bytes(4096, 4096, 1024) == 0     # 256 tiles: no split
+    g = L.curvefp_gemm_prepared
+    args = [PR, 0, PR, 1, 64, 64, 64, FAKE, 64, None, 0, None]
+    for i in (0, 2, 7):
+        a = list(args)
+        a[i] = None
+        assert g(*a) == ENULL, i
+    bad = list(args); bad[3] = 7
+    assert g(*bad) == EFMT
+    bad = list(args); bad[8] = 63                   # ldc < N
+    assert g(*bad) == ESHAPE
+    bad = list(args); bad[6] = 48
+    assert g(*bad) == ESHAPE
+    bad = list(args); bad[2] = PR + 16
+    assert g(*bad) == EALIGN
+    need = L.curvefp_gemm_prepared_workspace_bytes(64, 64, 1024)
+    split = list(args); split[6] = 1024
+    assert g(*split) == ENULL                       # a split K needs its workspace
+    split[9], split[10] = PR, need - 1
+    assert g(*split) == ESHAPE
 
 
 def test_gemm_mixed_validation(L):

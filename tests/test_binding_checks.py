@@ -138,6 +138,33 @@ def test_gemm_checks(meta):
                                 out_scales=meta((M, 2), torch.int8), stream=STREAM)
 
 
+def test_prepared_checks(meta):
+    M, N, K = 64, 96, 256
+    a, sa = meta((M, K), torch.uint8), meta((M, K // 32), torch.int8)
+    passes_checks(lambda: cf.curvefp_prepare(a, sa, M, K, "E4C3", stream=STREAM))
+    with pytest.raises(ValueError, match="scales"):
+        cf.curvefp_prepare(a, sa[:-1], M, K, "E4C3", stream=STREAM)
+    with pytest.raises(ValueError, match="prepared"):
+        cf.curvefp_prepare(a, sa, M, K, "E4C3", prepared=meta((1024,), torch.uint8), stream=STREAM)
+    with pytest.raises(ValueError, match="not on a GPU"):
+        cf.curvefp_prepare(a, sa, M, K, "E4C3", prepared=torch.zeros(1 << 18, dtype=torch.uint8), stream=STREAM)
+    pa = meta((cf.curvefp_prepared_bytes(M, K),), torch.uint8)
+    pb = meta((cf.curvefp_prepared_bytes(N, K),), torch.uint8)
+    passes_checks(lambda: cf.curvefp_gemm_prepared(pa, "E5C2", pb, "E4C3", M, N, K, stream=STREAM))
+    with pytest.raises(ValueError, match="b_prepared"):   # N = 300 pads to 512 rows
+        cf.curvefp_gemm_prepared(pa, "E5C2", pb, "E4C3", M, 300, K, stream=STREAM)
+    with pytest.raises(ValueError, match="c is"):
+        cf.curvefp_gemm_prepared(pa, "E4C3", pb, "E4C3", M, N, K, c=meta((M, N - 1), torch.float32),
+                                 stream=STREAM)
+    # K split in two (one output tile, K = 1024): the workspace is required and checked
+    pa2 = meta((cf.curvefp_prepared_bytes(M, 1024),), torch.uint8)
+    pb2 = meta((cf.curvefp_prepared_bytes(N, 1024),), torch.uint8)
+    passes_checks(lambda: cf.curvefp_gemm_prepared(pa2, "E4C3", pb2, "E4C3", M, N, 1024, stream=STREAM))
+    with pytest.raises(ValueError, match="workspace"):
+        cf.curvefp_gemm_prepared(pa2, "E4C3", pb2, "E4C3", M, N, 1024, workspace=meta((64,), torch.uint8),
+                                 stream=STREAM)
+
+
 def test_mixed_gemm_checks(meta):
     M, N, K = 64, 96, 256
     # A = dY codes [M][K] along K; B = reused forward codes of a [K][N] tensor, blocks along N
