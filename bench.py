@@ -929,8 +929,8 @@ def main():
             cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
     # The step on two streams (both at the default priority).  Its HBM-bound parts run side by
-    # side: the activations are quantized, expanded for the GEMM (prepared path) and their codes
-    # reconstructed on the main stream while the weights are quantized and expanded on the side
+    # side: the activations are quantized, their codes reconstructed and (prepared path) expanded
+    # for the GEMM on the main stream while the weights are quantized and expanded on the side
     # stream; the GEMM (MFMA-bound, every SIMD's registers taken by its waves) then runs alone on
     # the main stream once both operands are there.
     side = torch.cuda.Stream(device=dev)
@@ -972,15 +972,17 @@ def main():
         cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb, stream=side)
         rec(ev, "qb1", side)
         if prepared:
-            rec(ev, "pa0", stream)
-            prepare_a(stream)
-            rec(ev, "pa1", stream)
             rec(ev, "pb0", side)
             prepare_b(side)
             rec(ev, "pb1", side)
         rec(ev, "d0", stream)
         cf.curvefp_dequantize(ca, sa, w.fmt, outer_a, ka, dst=D, stream=stream)
         rec(ev, "d1", stream)
+        if prepared:
+            # the activations' expansion after their reconstruction (measured the fastest order)
+            rec(ev, "pa0", stream)
+            prepare_a(stream)
+            rec(ev, "pa1", stream)
         stream.wait_stream(side)
         rec(ev, "g0", stream)
         gemm()
@@ -1037,7 +1039,7 @@ def main():
             "format": w.fmt,
             "source_dtype": w.dtype,
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
-            "step": ("[quantize(act) -> prepare(act) -> dequantize(act codes)] || [quantize(weight) -> "
+            "step": ("[quantize(act) -> dequantize(act codes) -> prepare(act)] || [quantize(weight) -> "
                      "prepare(weight)] on two streams, then gemm_prepared" if prepared else
                      "[quantize(act) -> dequantize(act codes)] || quantize(weight) on two streams, then gemm"),
             "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
@@ -1060,8 +1062,8 @@ def main():
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
-        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_a, prepare_a, "
-                            "dequantize, gemm: main; quantize_b, prepare_b: side, alongside the main "
+        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_a, dequantize, "
+                            "prepare_a, gemm: main; quantize_b, prepare_b: side, alongside the main "
                             "stream's calls before the GEMM)" if prepared else
                             "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
                             "gemm: main; quantize_b: side, alongside quantize_a and dequantize)"),
