@@ -60,7 +60,7 @@ def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=50)
-    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default=HEADLINE)
     p.add_argument("--gemm", choices=["prepared", "ws", "fused"], default="prepared",
                    help="prepared: each operand expanded by curvefp_prepare as soon as it is quantized (on "
