@@ -201,9 +201,9 @@ def pmc_commands(gemm: str):
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
 
 
-# the bf16 -> E4C3 rows kernel with 8 chunks per thread (demangled with or without the default
+# the bf16 -> E4C3 rows kernel with 2 chunks per thread (demangled with or without the default
 # radix arguments of Fmt)
-STREAM_KERNEL = re.compile(r"quantize_rows_kernel<curvefp::Fmt<4, 3(, 1, 1)?>, true, 8,")
+STREAM_KERNEL = re.compile(r"quantize_rows_kernel<curvefp::Fmt<4, 3(, 1, 1)?>, true, 2,")
 
 
 def stream_per_dispatch(d: str, counter: str):
@@ -266,7 +266,7 @@ def summarize_stream_pmc(args):
         f"python bench.py --summarize-stream-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}",
         "```",
         "",
-        "Kernel: `quantize_rows_kernel<Fmt<4, 3>, true, 8, ...>` (bf16 -> E4C3, 8 chunks per thread), the "
+        "Kernel: `quantize_rows_kernel<Fmt<4, 3>, true, 2, ...>` (bf16 -> E4C3, 2 chunks per thread), the "
         "`quantize_stream` case of bench.py.",
         "",
         "| dispatch | count | FETCH_SIZE KiB/dispatch | WRITE_SIZE KiB/dispatch |",

@@ -413,14 +413,15 @@ hipError_t launch_rows_u(const void* src, int64_t rows, int64_t cols, int64_t ld
     return hipSuccess;
 }
 
-// Streams of at least 2048 workgroups at 128 (bf16) or 64 (fp32) bytes in flight per thread use
-// that depth (the shape that measured fastest on a 1 GiB stream); smaller tensors use 32 bytes
-// per thread, so that they still spread over every compute unit.  Blocks of 32..512 (a power of
-// two) are reduced over their lanes; any other block size runs the scale pass first.
+// bf16 sources: two chunks (32 bytes) in flight per thread at every size.  Measured against eight
+// and one on 8192 x 4096, 14336 x 4096, 16384 x 8192, 32768 x 8192 and 32768 x 16384 sources, calls
+// alternating in one process: eight 6-9% slower on all but 16384 x 8192 (2.5%), one 10-20% slower.
+// fp32 sources: 64 bytes per thread from 2048 workgroups on, 32 below, so that smaller tensors
+// still spread over every compute unit.  Blocks of 32..512 (a power of two) are reduced over their
+// lanes; any other block size runs the scale pass first.
 template <class F, bool BF16>
 hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, int fidx, uint8_t* codes,
                        int8_t* scales, int block, hipStream_t s) {
-    constexpr int UBIG = BF16 ? 8 : 2;
     int lgl = -1;
     if (block <= 512 && (block & (block - 1)) == 0)
         for (lgl = 0; (8 << lgl) < block; lgl++) {}
@@ -433,9 +434,9 @@ hipError_t launch_rows(const void* src, int64_t rows, int64_t cols, int64_t ld, 
         if (e != hipSuccess) return e;
     }
     const int64_t nchunks = rows * (cols / 8);
-    if (nchunks >= (int64_t)2048 * 256 * UBIG)
-        return launch_rows_u<F, BF16, UBIG>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
-    return launch_rows_u<F, BF16, BF16 ? 2 : 1>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
+    if (BF16 || nchunks >= (int64_t)2048 * 256 * 2)
+        return launch_rows_u<F, BF16, 2>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
+    return launch_rows_u<F, BF16, 1>(src, rows, cols, ld, fidx, codes, scales, block, lgl, dgl, s);
 }
 
 // quantize-transpose through LDS: a workgroup takes 128 rows (four blocks) x 64 columns.  The
@@ -837,11 +838,8 @@ hipError_t launch_tensorwise_fmt(const void* src, int dtype, int64_t rows, int64
     if (axis == 1) {
         const Div32 dgl = make_div32((uint32_t)(cols / 8));
         const int64_t nchunks = rows * (cols / 8);
-        if (dtype == 1) {
-            if (nchunks >= (int64_t)2048 * 256 * 8)
-                return launch_rows_u<F, true, 8>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
+        if (dtype == 1)   // bf16: two chunks per thread at every size, as curvefp_quantize
             return launch_rows_u<F, true, 2>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
-        }
         if (nchunks >= (int64_t)2048 * 256 * 2)
             return launch_rows_u<F, false, 2>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
         return launch_rows_u<F, false, 1>(src, rows, cols, ld, fidx, cp, scales, (int)cols, -1, dgl, s);
