@@ -27,7 +27,8 @@ namespace {
 
 // chunk g = 8 consecutive codes: chunk g mod cpr of row g / cpr, block g / 4 (blocks are
 // contiguous in the code and scale arrays); a grid-stride loop over the chunks, one per thread
-// per round (a capped grid with plain stores measured fastest for this write-heavy stream)
+// per round (a capped grid with plain stores measured fastest for this write-heavy stream; the
+// cap grows with the tensor, see the launch)
 template <class F>
 __global__ __launch_bounds__(256) void dequantize_kernel(
     const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
@@ -96,8 +97,13 @@ hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, in
     for (int64_t r0 = 0; r0 < outer; r0 += slab) {
         const int64_t nr = outer - r0 < slab ? outer - r0 : slab;
         const int64_t nchunks = nr * cpr;
+        // two chunks per thread (two rounds) once that takes more than 8192 workgroups, else at
+        // most 8192: on 8192 x 4096 codes more workgroups measured slower, on 32768 x 8192 the
+        // 8192 cap 13% slower than two rounds
+        const int64_t half = (nchunks + 511) / 512;
         int64_t blocks = (nchunks + 255) / 256;
-        blocks = blocks < 8192 ? blocks : 8192;
+        const int64_t cap = half > 8192 ? half : 8192;
+        blocks = blocks < cap ? blocks : cap;
         hipLaunchKernelGGL((dequantize_kernel<F>), dim3((unsigned)blocks), dim3(256), 0, s,
                            cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / block),
                            (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx, dgq);

@@ -82,3 +82,30 @@ def test_output_row_stride():
     got = dst.cpu().numpy()
     assert np.array_equal(got[:, :64].view(np.uint32), oracle.dequantize(codes, sc, f).view(np.uint32))
     assert np.all(got[:, 64:] == 3.0)
+
+
+@pytest.mark.parametrize("fmt", ["E4C3", "E3C3"])
+def test_large_tensor_two_rounds(fmt):
+    """A reconstruction large enough for the launch's two chunks per thread (9216 x 8192 codes:
+    more chunks than 8192 workgroups of 256 threads can take in one round), as codes and scales
+    the oracle quantizes from the seeded source: sampled rows, every 8-code chunk of them, bit for
+    bit."""
+    M, K = 9216, 8192
+    rng = np.random.default_rng(77)
+    rows = np.unique(np.concatenate([np.arange(0, M, 127), [M - 1]]))
+    codes = np.zeros((M, K), dtype=np.uint8)
+    scales = np.zeros((M, K // 32), dtype=np.int8)
+    # the oracle's codes and scales for a block-random subset of rows; the other rows hold one
+    # seeded pattern (their values are not compared, only written)
+    X = (rng.standard_normal((len(rows), K)) * np.exp2(rng.uniform(-6, 6, (len(rows), 1)))).astype(np.float32)
+    oc, osc = oracle_quantize(X, fmt, 1)
+    codes[rows], scales[rows] = oc, osc
+    f = oracle.get_format(fmt)
+    say(f"[dequantize] two rounds fmt={fmt} shape=({M}, {K})")
+    c = torch.from_numpy(np.ascontiguousarray(layout_codes(codes, fmt))).to(DEV)
+    s = torch.from_numpy(scales).to(DEV)
+    out = cf.curvefp_dequantize(c, s, fmt, M, K)
+    torch.cuda.synchronize()
+    got = out[torch.from_numpy(rows).to(DEV)].cpu().numpy()
+    exp = oracle.dequantize(oc, osc, f)
+    assert np.array_equal(got.view(np.uint32), exp.view(np.uint32)), "sampled rows differ"
