@@ -696,14 +696,29 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
 
         t = timed_median(call, stream, reps)
         tf = w.flops() / t / 1e12
+        # the same product on prepared operands (each expanded in its own layout), the GEMM alone
+        fa, fb = w.fmt_of("a"), w.fmt_of("b")
+        pa = cf.curvefp_prepare(ca, sa, w.M, w.K, fa, trans=w.a.trans)
+        pb = cf.curvefp_prepare(cb, sb, w.N, w.K, fb, trans=w.b.trans)
+        nws = cf.curvefp_gemm_prepared_workspace_bytes(w.M, w.N, w.K)
+        gws = torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None
+        t_pa = timed_median(lambda: cf.curvefp_prepare(ca, sa, w.M, w.K, fa, trans=w.a.trans, prepared=pa), stream, reps)
+        t_pb = timed_median(lambda: cf.curvefp_prepare(cb, sb, w.N, w.K, fb, trans=w.b.trans, prepared=pb), stream, reps)
+        t_gp = timed_median(lambda: cf.curvefp_gemm_prepared(pa, fa, pb, fb, w.M, w.N, w.K, c=C, workspace=gws),
+                            stream, reps)
+        tfp = w.flops() / t_gp / 1e12
         out[name.split("_")[0]] = {
             "workload": w.name, "M": w.M, "N": w.N, "K": w.K,
-            "formats": f"{w.fmt_of('a')} x {w.fmt_of('b')}", "trans": [w.a.trans, w.b.trans],
+            "formats": f"{fa} x {fb}", "trans": [w.a.trans, w.b.trans],
             "us": t * 1e6, "achieved": tf, "peak": F16_DENSE_PEAK_TFLOPS, "unit": "TFLOP/s",
             "frac": tf / F16_DENSE_PEAK_TFLOPS, "mfma_pipe_frac": 3.0 * tf / F16_DENSE_PEAK_TFLOPS,
             "timing": f"median of {reps} individually timed curvefp_gemm_mixed calls",
+            "prepared": {"prepare_a_us": t_pa * 1e6, "prepare_b_us": t_pb * 1e6, "gemm_us": t_gp * 1e6,
+                         "tflops": tfp, "frac": tfp / F16_DENSE_PEAK_TFLOPS,
+                         "what": "curvefp_prepare of each operand in its layout, then curvefp_gemm_prepared "
+                                 "(the GEMM kernel alone)"},
         }
-        del C, ws
+        del C, ws, pa, pb, gws
     src.clear()
     torch.cuda.empty_cache()
     return out

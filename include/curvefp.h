@@ -280,29 +280,38 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales,
  * curvefp_gemm_prepared multiplies two prepared operands.  An operand that several products
  * share (static weights, Sec. 3.1) is then expanded once, and the two operands of one product
  * can be expanded on two streams, each as soon as it is quantized.
- * prepare(A), prepare(B), gemm_prepared give the C of curvefp_gemm_ws (and, for two formats,
- * of curvefp_gemm_mixed with trans_a = trans_b = 0) bit for bit.
+ * A backward GEMM's reused forward operand (Sec. 3.3: the codes kept from the forward pass, read
+ * transposed) is prepared the same way with trans = 1.  prepare(A), prepare(B), gemm_prepared
+ * give the C of curvefp_gemm_ws bit for bit, and for two formats or reused operands the C of
+ * curvefp_gemm_mixed with the same trans_a and trans_b.
  *
- * curvefp_prepared_bytes: bytes of the prepared form of a [rows][k] operand (4 bytes per
- * element with rows padded to a multiple of 256, plus one int32 per padded row).  Returns
- * CURVEFP_ERR_SHAPE for non-positive sizes or k not a multiple of 32.
+ * curvefp_prepared_bytes: bytes of the prepared form of an operand with `rows` GEMM rows over
+ * k (4 bytes per element with rows padded to a multiple of 256, plus one int32 per padded row;
+ * trans = 1 adds 32 bytes per 256 rows per 256 k of scratch).  Returns CURVEFP_ERR_SHAPE for
+ * non-positive sizes, k not a multiple of 32 or trans not 0 or 1.
  */
-int64_t curvefp_prepared_bytes(int64_t rows, int64_t k);
+int64_t curvefp_prepared_bytes(int64_t rows, int64_t k, int trans);
 
 /*
- * Expand one operand: codes [rows][k] (k-contiguous; E3C3 28 bytes per 32 codes) and block
- * scales [rows][k/block] of a tensor quantized along k by curvefp_quantize, in `format`, into
- * `prepared` (device, 256-byte aligned, at least curvefp_prepared_bytes(rows, k) bytes,
- * passed in prepared_size).  The buffer is overwritten with the expansion of the codes and
+ * Expand one operand with `rows` GEMM rows over k, in `format`, into `prepared` (device,
+ * 256-byte aligned, at least curvefp_prepared_bytes(rows, k, trans) bytes, passed in
+ * prepared_size).  The codes and scales are those curvefp_quantize made
+ *   trans = 0: of a [rows][k] tensor along k: codes [rows][k] (E3C3 [rows][k/32][28]), block
+ *              scales [rows][k/block], k % block == 0;
+ *   trans = 1: of a [k][rows] tensor along rows (a forward operand a backward GEMM reuses):
+ *              codes [k][rows] (E3C3 [k][rows/32][28]), scales [k][rows/block],
+ *              rows % block == 0 and rows <= 256 * 65535.  The buffer is overwritten with the expansion of the codes and
  * scales as they are when the call runs; it does not record its shape or format, so the GEMM
  * that reads it must be given the same rows (M or N), k and format.  Asynchronous on `stream`
  * (null: the null stream).
- * Errors: CURVEFP_ERR_NULL, _FORMAT, _BLOCK (block not a positive multiple of 32), _SHAPE
- * (non-positive sizes, k % block, prepared_size too small), _ALIGN (codes not 16-byte or
- * prepared not 256-byte aligned), _HIP (a launch failed).
+ * Errors: CURVEFP_ERR_NULL, _FORMAT, _BLOCK (block not a positive multiple of 32, trans not 0
+ * or 1), _SHAPE (non-positive sizes, k % 32, the blocked extent not a multiple of block,
+ * prepared_size too small), _ALIGN (codes not 16-byte or prepared not 256-byte aligned), _HIP
+ * (a launch failed).
  */
 int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t k,
-                    int format, int block, void* prepared, int64_t prepared_size, void* stream);
+                    int format, int block, int trans, void* prepared, int64_t prepared_size,
+                    void* stream);
 
 /*
  * Bytes of device workspace curvefp_gemm_prepared needs for an M x N x K product: 0 unless K
@@ -314,11 +323,11 @@ int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K);
 
 /*
  * C[M][N] = deq(A) deq(B)^T in fp32 (the contract of curvefp_gemm, including its non-finite
- * and scale-spread clauses) from A prepared as [M][K] in format_a and B prepared as [N][K] in
- * format_b (each by curvefp_prepare; the two formats may differ).  c is [M][ldc] fp32,
- * overwritten.  workspace: at least curvefp_gemm_prepared_workspace_bytes(M, N, K) bytes,
- * 256-byte aligned (may be null when that is 0); its contents are scratch, so calls that share
- * it must be ordered.  The prepared buffers are only read: one prepared operand may serve
+ * and scale-spread clauses) from A prepared with M rows over K in format_a and B prepared with
+ * N rows over K in format_b (each by curvefp_prepare, either trans; the formats may differ).
+ * c is [M][ldc] fp32, overwritten.  workspace: at least
+ * curvefp_gemm_prepared_workspace_bytes(M, N, K) bytes, 256-byte aligned (may be null when
+ * that is 0); its contents are scratch, so calls that share it must be ordered.  The prepared buffers are only read: one prepared operand may serve
  * concurrent calls.  Errors: CURVEFP_ERR_NULL, _FORMAT, _SHAPE (non-positive sizes, K % 32,
  * ldc < N, workspace too small), _ALIGN (prepared buffers or workspace not 256-byte aligned,
  * c not 16-byte aligned), _HIP.

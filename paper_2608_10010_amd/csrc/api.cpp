@@ -194,20 +194,23 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
-int64_t curvefp_prepared_bytes(int64_t rows, int64_t k) {
-    if (rows <= 0 || k <= 0 || k % 32) return CURVEFP_ERR_SHAPE;
-    return prepared_bytes(rows, k);
+int64_t curvefp_prepared_bytes(int64_t rows, int64_t k, int trans) {
+    if (rows <= 0 || k <= 0 || k % 32 || (trans != 0 && trans != 1)) return CURVEFP_ERR_SHAPE;
+    return prepared_bytes(rows, k, trans);
 }
 
 int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t k, int format, int block,
-                    void* prepared, int64_t prepared_size, void* stream) {
+                    int trans, void* prepared, int64_t prepared_size, void* stream) {
     if (!codes || !scales || !prepared) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
-    if (rows <= 0 || k <= 0 || k % block) return CURVEFP_ERR_SHAPE;
-    if (prepared_size < prepared_bytes(rows, k)) return CURVEFP_ERR_SHAPE;
+    if (!block_ok(block) || (trans != 0 && trans != 1)) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || k <= 0 || k % 32) return CURVEFP_ERR_SHAPE;
+    // blocks along k (trans 0) or along the rows of the reused operand (trans 1), whose expansion
+    // grid has one workgroup row per 256 rows
+    if (trans ? (rows % block || (rows + 255) / 256 > 65535) : k % block) return CURVEFP_ERR_SHAPE;
+    if (prepared_size < prepared_bytes(rows, k, trans)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(codes) || reinterpret_cast<uintptr_t>(prepared) % 256) return CURVEFP_ERR_ALIGN;
-    return hip_status(launch_prepare(codes, scales, rows, k, format, block, prepared,
+    return hip_status(launch_prepare(codes, scales, rows, k, format, block, trans, prepared,
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 

@@ -43,10 +43,10 @@ hipError_t launch_gemm_ws(const void* a, const int8_t* as, const void* b, const 
                           int64_t N, int64_t K, int format, int block, float* c, int64_t ldc, void* ws,
                           hipStream_t s);
 // prepared operands: one operand's expansion (planes + row maxima), and the GEMM on two of them
-int64_t prepared_bytes(int64_t rows, int64_t K);
+int64_t prepared_bytes(int64_t rows, int64_t K, int trans);
 int64_t gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K);
 hipError_t launch_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t K, int format, int block,
-                          void* prepared, hipStream_t s);
+                          int trans, void* prepared, hipStream_t s);
 hipError_t launch_gemm_prepared(const void* pa, int fa, const void* pb, int fb, int64_t M, int64_t N, int64_t K,
                                 float* c, int64_t ldc, void* ws, hipStream_t s);
 // curvefp_gemm_ws with C requantized in the epilogue (blocks of out_block <= 256 along each output row)

@@ -1622,18 +1622,24 @@ hipError_t launch_fmt(const void* a, const int8_t* as, const void* b, const int8
 // streams as soon as each is quantized.  Layout for [rows][K] codes quantized along K: the planes
 // [K/32][RT][hi, lo][256 rows][64 B] (RT = ceil(rows / 256)), exactly the workspace path's
 // planes of that operand, then the row maxima of its block scales (prep_kernel's keys), RT * 256
-// int32.  The expansion depends on the operand alone, so prepare(A), prepare(B) and
-// gemm_prepared give curvefp_gemm_ws's C bit for bit.
+// int32.  A reused operand (codes of a [K][rows] tensor quantized along rows, the backward GEMMs'
+// forward operand) is expanded into the same planes and row maxima, followed by the partial column
+// maxima its expansion reads ([ceil(K / 256)][RT * 8] int32, scratch of the preparation).  The
+// expansion depends on the operand alone, so prepare(A), prepare(B) and gemm_prepared give
+// curvefp_gemm_ws's C (and curvefp_gemm_mixed's, for two formats or reused operands) bit for bit.
 struct PreparedLayout {
-    int64_t rt, planes, rmax, bytes;
+    int64_t rt, planes, rmax, colpart, nslab, bytes;
 };
 
-PreparedLayout prepared_layout(int64_t rows, int64_t K) {
+PreparedLayout prepared_layout(int64_t rows, int64_t K, int trans = 0) {
     PreparedLayout p;
     p.rt = (rows + BM - 1) / BM;
     p.planes = 0;
     p.rmax = (K / 32) * p.rt * 2 * PLANE;
     p.bytes = p.rmax + p.rt * BM * 4;
+    p.nslab = (K + PREP_SLAB - 1) / PREP_SLAB;
+    p.colpart = p.bytes;
+    if (trans) p.bytes = p.colpart + p.nslab * p.rt * 8 * 4;
     return p;
 }
 
@@ -1661,16 +1667,48 @@ PreparedGemmLayout prepared_gemm_layout(int64_t M, int64_t N, int64_t K) {
 
 int64_t gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) { return ws_layout(M, N, K).bytes; }
 
-int64_t prepared_bytes(int64_t rows, int64_t K) { return prepared_layout(rows, K).bytes; }
+int64_t prepared_bytes(int64_t rows, int64_t K, int trans) { return prepared_layout(rows, K, trans).bytes; }
 
 int64_t gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) { return prepared_gemm_layout(M, N, K).bytes; }
 
 hipError_t launch_prepare(const void* codes, const int8_t* scales, int64_t rows, int64_t K, int format, int block,
-                          void* prepared, hipStream_t s) {
-    const PreparedLayout p = prepared_layout(rows, K);
+                          int trans, void* prepared, hipStream_t s) {
+    const PreparedLayout p = prepared_layout(rows, K, trans);
     const int64_t nkb = K / 32, nsb = K / block;
     char* base = reinterpret_cast<char*>(prepared);
     int* rmax = reinterpret_cast<int*>(base + p.rmax);
+    if (trans) {
+        // the mixed path's preparation of a reused operand: partial column maxima of its scales
+        // over slabs of 256 k-rows (prep_mixed_kernel), then the transposed expansion, which
+        // takes each row's maximum from them and writes it beside the planes
+        const Div32 dgq = make_div32((uint32_t)(block / 32));
+        PrepOperand po;
+        po.scales = scales;
+        po.rows = rows;
+        po.tiles = p.rt;
+        po.K = K;
+        po.trans = 1;
+        po.cgroups = (int)((p.rt * 8 + 63) / 64);
+        po.groups = (int)(po.cgroups * p.nslab);
+        po.rmax = rmax;
+        po.colpart = reinterpret_cast<int*>(base + p.colpart);
+        po.nsb = rows / block;
+        po.dgq = dgq;
+        PrepOperand pn = po;
+        pn.groups = 0;   // no second operand
+        hipLaunchKernelGGL(prep_mixed_kernel, dim3((unsigned)po.groups), dim3(256), 0, s, po, pn, (int*)nullptr, 0);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        const ExpandTOperand xo = {reinterpret_cast<const uint8_t*>(codes), scales, rows, p.rt,
+                                   format == 2 ? rows / 32 * 28 : rows, po.colpart, p.nslab, rmax, base + p.planes,
+                                   format, rows / block, dgq};
+        ExpandTOperand xn = xo;
+        xn.tiles = 0;
+        const dim3 grid((unsigned)nkb, (unsigned)p.rt);
+        if (format == 2) hipLaunchKernelGGL((expand_t_kernel<true>), grid, dim3(256), 0, s, xo, xn);
+        else hipLaunchKernelGGL((expand_t_kernel<false>), grid, dim3(256), 0, s, xo, xn);
+        return hipGetLastError();
+    }
     const int groups = (int)(p.rt * BM / 16);
     hipLaunchKernelGGL(prep_kernel, dim3((unsigned)groups), dim3(256), 0, s, scales, (const int8_t*)nullptr, rows,
                        (int64_t)0, nsb, groups, 0, rmax, (int*)nullptr, (int*)nullptr, 0);

@@ -73,9 +73,9 @@ def lib() -> ctypes.CDLL:
         L.curvefp_gemm_ws.restype = I
         L.curvefp_gemm_ws_static.argtypes = [P, P, P, P, I64, I64, I64, I, I, P, I64, P]
         L.curvefp_gemm_ws_static.restype = I
-        L.curvefp_prepared_bytes.argtypes = [I64, I64]
+        L.curvefp_prepared_bytes.argtypes = [I64, I64, I]
         L.curvefp_prepared_bytes.restype = I64
-        L.curvefp_prepare.argtypes = [P, P, I64, I64, I, I, P, I64, P]
+        L.curvefp_prepare.argtypes = [P, P, I64, I64, I, I, I, P, I64, P]
         L.curvefp_prepare.restype = I
         L.curvefp_gemm_prepared_workspace_bytes.argtypes = [I64, I64, I64]
         L.curvefp_gemm_prepared_workspace_bytes.restype = I64
@@ -473,27 +473,33 @@ def curvefp_gemm_ws_static(a_codes: torch.Tensor, a_scales: torch.Tensor, b_code
     return c
 
 
-def curvefp_prepared_bytes(rows: int, k: int) -> int:
-    n = lib().curvefp_prepared_bytes(rows, k)
+def curvefp_prepared_bytes(rows: int, k: int, trans: int = 0) -> int:
+    n = lib().curvefp_prepared_bytes(rows, k, trans)
     if n < 0:
         raise CurveFPError(n, "curvefp_prepared_bytes")
     return n
 
 
 def curvefp_prepare(codes: torch.Tensor, scales: torch.Tensor, rows: int, k: int, fmt, block: int = 32,
-                    prepared: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
-    """The expansion of one GEMM operand (codes of a [rows, k] tensor quantized along k) into a
-    prepared buffer (uint8, allocated here when not given) for curvefp_gemm_prepared."""
+                    trans: int = 0, prepared: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The expansion of one GEMM operand with `rows` GEMM rows over k into a prepared buffer
+    (uint8, allocated here when not given) for curvefp_gemm_prepared: trans = 0, the codes of a
+    [rows, k] tensor quantized along k; trans = 1, those of a [k, rows] tensor quantized along
+    rows (a forward operand a backward GEMM reuses)."""
     what = "curvefp_prepare"
     f = _fmt(fmt)
     if prepared is None:
         _on_gpu(what, [("codes", codes)], stream)
-        prepared = torch.empty(curvefp_prepared_bytes(rows, k), dtype=torch.uint8, device=codes.device)
+        prepared = torch.empty(curvefp_prepared_bytes(rows, k, trans), dtype=torch.uint8, device=codes.device)
     _on_gpu(what, [("codes", codes), ("scales", scales), ("prepared", prepared)], stream)
-    _codes_arg(what, "codes", codes, f, rows, k, block)
-    _scales_arg(what, "scales", scales, rows, k, block)
-    _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k))
-    st = lib().curvefp_prepare(codes.data_ptr(), scales.data_ptr(), rows, k, f, block, prepared.data_ptr(),
+    if trans:
+        _codes_arg(what, "codes", codes, f, k, rows, block)
+        _scales_arg(what, "scales", scales, k, rows, block)
+    else:
+        _codes_arg(what, "codes", codes, f, rows, k, block)
+        _scales_arg(what, "scales", scales, rows, k, block)
+    _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k, trans))
+    st = lib().curvefp_prepare(codes.data_ptr(), scales.data_ptr(), rows, k, f, block, trans, prepared.data_ptr(),
                                prepared.numel() * prepared.element_size(), _stream(stream))
     _check(st, what)
     return prepared

@@ -206,29 +206,41 @@ def test_gemm_ws_validation(L):
 
 
 def test_prepared_validation(L):
-    assert L.curvefp_prepared_bytes(0, 64) == ESHAPE
-    assert L.curvefp_prepared_bytes(10, 48) == ESHAPE
+    assert L.curvefp_prepared_bytes(0, 64, 0) == ESHAPE
+    assert L.curvefp_prepared_bytes(10, 48, 0) == ESHAPE
+    assert L.curvefp_prepared_bytes(10, 64, 2) == ESHAPE
     # rows padded to 256: 256 rows x K x 4 bytes of planes + one int32 per padded row
-    assert L.curvefp_prepared_bytes(10, 64) == 256 * 64 * 4 + 256 * 4
-    assert L.curvefp_prepared_bytes(300, 64) == 512 * 64 * 4 + 512 * 4
-    need = L.curvefp_prepared_bytes(64, 64)
+    assert L.curvefp_prepared_bytes(10, 64, 0) == 256 * 64 * 4 + 256 * 4
+    assert L.curvefp_prepared_bytes(300, 64, 0) == 512 * 64 * 4 + 512 * 4
+    # a reused operand adds the partial column maxima: ceil(K / 256) slabs x 8 per 256 rows
+    assert L.curvefp_prepared_bytes(300, 608, 1) == 512 * 608 * 4 + 512 * 4 + 3 * 2 * 8 * 4
+    need = L.curvefp_prepared_bytes(64, 64, 0)
     PR = 1 << 24                     # 256-byte aligned, never dereferenced
     p = L.curvefp_prepare
-    args = [FAKE, FAKE, 64, 64, 0, 32, PR, need, None]
-    for i in (0, 1, 6):
+    args = [FAKE, FAKE, 64, 64, 0, 32, 0, PR, need, None]
+    for i in (0, 1, 7):
         a = list(args)
         a[i] = None
         assert p(*a) == ENULL, i
-    bad = list(args); bad[7] = need - 1
+    bad = list(args); bad[8] = need - 1
     assert p(*bad) == ESHAPE
-    bad = list(args); bad[6] = PR + 128
+    bad = list(args); bad[7] = PR + 128
     assert p(*bad) == EALIGN
     bad = list(args); bad[4] = 5
     assert p(*bad) == EFMT
     bad = list(args); bad[5] = 48
     assert p(*bad) == EBLOCK
+    bad = list(args); bad[6] = 2
+    assert p(*bad) == EBLOCK
     bad = list(args); bad[3] = 96                  # K % block
     assert p(*bad) == ESHAPE
+    # reused operand: the blocks lie along the rows, so rows % block, not K % block
+    tneed = L.curvefp_prepared_bytes(64, 96, 1)
+    t = [FAKE, FAKE, 64, 96, 0, 64, 1, PR, tneed, None]
+    bad = list(t); bad[2] = 96
+    assert p(*bad) == ESHAPE                       # 96 rows, blocks of 64
+    bad = list(t); bad[8] = L.curvefp_prepared_bytes(64, 96, 0)
+    assert p(*bad) == ESHAPE                       # the non-reused size lacks the scratch
     # the GEMM on prepared operands: no workspace unless K is split
     assert L.curvefp_gemm_prepared_workspace_bytes(64, 64, 0) == ESHAPE
     assert L.curvefp_gemm_prepared_workspace_bytes(64, 64, 64) == 0

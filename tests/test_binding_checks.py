@@ -156,6 +156,14 @@ def test_prepared_checks(meta):
     with pytest.raises(ValueError, match="c is"):
         cf.curvefp_gemm_prepared(pa, "E4C3", pb, "E4C3", M, N, K, c=meta((M, N - 1), torch.float32),
                                  stream=STREAM)
+    # a reused operand: codes [K][rows], scales [K][rows / G]
+    at, sat = meta((K, M), torch.uint8), meta((K, M // 32), torch.int8)
+    passes_checks(lambda: cf.curvefp_prepare(at, sat, M, K, "E4C3", trans=1, stream=STREAM))
+    with pytest.raises(ValueError, match="scales"):
+        cf.curvefp_prepare(at, sat[:, :-1], M, K, "E4C3", trans=1, stream=STREAM)
+    with pytest.raises(ValueError, match="prepared"):   # the trans = 0 size lacks the scratch
+        cf.curvefp_prepare(at, sat, M, K, "E4C3", trans=1, prepared=meta((cf.curvefp_prepared_bytes(M, K),),
+                                                                          torch.uint8), stream=STREAM)
     # K split in two (one output tile, K = 1024): the workspace is required and checked
     pa2 = meta((cf.curvefp_prepared_bytes(M, 1024),), torch.uint8)
     pb2 = meta((cf.curvefp_prepared_bytes(N, 1024),), torch.uint8)

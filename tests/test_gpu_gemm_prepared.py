@@ -168,3 +168,57 @@ def test_workload_full_size(name):
     rel = check_gemm(Cp[rows][:, cols], V, tol, name)
     say(f"[gemm_prepared] workload={name} rel_frob={rel:.3e}")
     same_bits(Cp, Cw, name)
+
+
+# reused forward operands (the backward GEMMs of Sec. 3.3): a [K][R] tensor quantized along R,
+# prepared with trans = 1, against curvefp_gemm_mixed with the same layouts
+from tests.test_gpu_gemm_mixed import operand_source  # noqa: E402
+
+
+@pytest.mark.parametrize("fa,fb", [("E5C2", "E4C3"), ("E4C3", "E4C3"), ("E3C3", "E5C2"), ("E4C3_r3/4", "E4C3_r8/9")])
+@pytest.mark.parametrize("ta,tb", [(0, 1), (1, 1), (1, 0)])
+def test_reused_operands(fa, fb, ta, tb):
+    """Each operand prepared in its own layout (ragged M and N, an odd number of K blocks, K not a
+    multiple of 256) gives curvefp_gemm_mixed's C bit for bit, within the oracle's bound."""
+    M, N, K = 288, 320, 352
+    rng = np.random.default_rng(300 + 100 * FMTS.index(fa) + 10 * FMTS.index(fb) + 2 * ta + tb)
+    A = operand_source(rng, M, K, ta)
+    B = operand_source(rng, N, K, tb, spread=3.0)
+    say(f"[gemm_prepared] reused {fa}x{fb} trans={ta}{tb} M={M} N={N} K={K}")
+    qa = quantized(A, fa)
+    qb = quantized(B, fb)
+    pa = cf.curvefp_prepare(qa[0], qa[1], M, K, fa, trans=ta)
+    pb = cf.curvefp_prepare(qb[0], qb[1], N, K, fb, trans=tb)
+    Cp = cf.curvefp_gemm_prepared(pa, fa, pb, fb, M, N, K)
+    Cm = cf.curvefp_gemm_mixed(qa[0], qa[1], fa, ta, qb[0], qb[1], fb, tb, M, N, K)
+    torch.cuda.synchronize()
+    Cp, Cm = Cp.cpu().numpy(), Cm.cpu().numpy()
+    V, tol = oracle_mixed(A, fa, 1, ta, B, fb, 1, tb)
+    check_gemm(Cp, V, tol, f"prepared reused {fa}x{fb} trans={ta}{tb}")
+    same_bits(Cp, Cm, f"prepared reused {fa}x{fb} trans={ta}{tb}")
+
+
+@pytest.mark.parametrize("name", ["dgrad_mixed", "wgrad_mixed"])
+def test_backward_workload_full_size(name):
+    """The 7B up-projection's backward GEMMs as the paper runs them (E5C2 output gradients times
+    the reused E4C3 forward codes), every operand prepared: the whole output bit for bit against
+    curvefp_gemm_mixed, sampled rows against the oracle."""
+    w = W.get(name)
+    A, B = w.operand("a"), w.operand("b")
+    fa, fb = w.fmt_of("a"), w.fmt_of("b")
+    say(f"[gemm_prepared] backward workload={name} M={w.M} N={w.N} K={w.K} {fa}x{fb} "
+        f"trans={w.a.trans}{w.b.trans}")
+    qa = quantized(A, fa, w.dtype, w.a.axis)
+    qb = quantized(B, fb, w.dtype, w.b.axis)
+    pa = cf.curvefp_prepare(qa[0], qa[1], w.M, w.K, fa, trans=w.a.trans)
+    pb = cf.curvefp_prepare(qb[0], qb[1], w.N, w.K, fb, trans=w.b.trans)
+    Cp = cf.curvefp_gemm_prepared(pa, fa, pb, fb, w.M, w.N, w.K)
+    Cm = cf.curvefp_gemm_mixed(qa[0], qa[1], fa, w.a.trans, qb[0], qb[1], fb, w.b.trans, w.M, w.N, w.K)
+    torch.cuda.synchronize()
+    Cp, Cm = Cp.cpu().numpy(), Cm.cpu().numpy()
+    same_bits(Cp, Cm, name)
+    rows = np.arange(0, w.M, max(1, w.M // 12))
+    cols = np.unique(np.concatenate([np.arange(0, w.N, max(1, w.N // 128)), np.arange(w.N - 32, w.N)]))
+    V, tol = oracle_mixed(A, fa, w.a.axis, w.a.trans, B, fb, w.b.axis, w.b.trans, rows=rows, cols=cols)
+    rel = check_gemm(Cp[rows][:, cols], V, tol, name)
+    say(f"[gemm_prepared] backward workload={name} rel_frob={rel:.3e}")
