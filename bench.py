@@ -951,7 +951,7 @@ def main():
     side = torch.cuda.Stream(device=dev)
 
     def rec(ev, key, s):
-        if ev is not None:
+        if ev is not None and key in ev:
             ev[key].record(s)
 
     def step_serial(ev=None):
@@ -1007,10 +1007,13 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # timed region: exactly `steps` steps, synchronized on both sides; HIP events are
-    # recorded on the stream the library launches on, around every kernel of every step
+    # timed region: exactly `steps` steps, synchronized on both sides; HIP events on the main
+    # stream bracket the GEMM of every step (the roofline's kernel).  Events around the other
+    # calls would add their own latency to the step (each record is a barrier packet: ~0.9% of
+    # the step with events around all six calls), so those are timed in the steps after it.
     keys = ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
-    evs = [{k + e: torch.cuda.Event(enable_timing=True) for k in keys for e in "01"} for _ in range(args.steps)]
+    evs = [{"g0": torch.cuda.Event(enable_timing=True), "g1": torch.cuda.Event(enable_timing=True)}
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
@@ -1018,11 +1021,17 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
+    ndiag = min(args.steps, 10)
+    diag = [{k + e: torch.cuda.Event(enable_timing=True) for k in keys for e in "01"} for _ in range(ndiag)]
+    for i in range(ndiag):
+        step(diag[i])
+    torch.cuda.synchronize()
     names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
     if prepared:
         names.update({"prepare_a": "pa", "prepare_b": "pb"})
-    per = {n: float(np.mean([evs[i][k + "0"].elapsed_time(evs[i][k + "1"]) for i in range(args.steps)]))
+    per = {n: float(np.mean([diag[i][k + "0"].elapsed_time(diag[i][k + "1"]) for i in range(ndiag)]))
            for n, k in names.items()}
+    per["gemm"] = float(np.mean([evs[i]["g0"].elapsed_time(evs[i]["g1"]) for i in range(args.steps)]))
 
     flops = w.flops()
     gemm_tflops = flops / (per["gemm"] * 1e-3) / 1e12
@@ -1079,9 +1088,12 @@ def main():
         "kernels_us": {n: per[n] * 1e3 for n in names},
         "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_a, dequantize, "
                             "prepare_a, gemm: main; quantize_b, prepare_b: side, alongside the main "
-                            "stream's calls before the GEMM)" if prepared else
+                            "stream's calls before the GEMM); gemm: mean over the timed steps; the "
+                            "others: over 10 steps right after them with events around every call"
+                            if prepared else
                             "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
-                            "gemm: main; quantize_b: side, alongside quantize_a and dequantize)"),
+                            "gemm: main; quantize_b: side, alongside quantize_a and dequantize); gemm: "
+                            "mean over the timed steps; the others: over 10 steps right after them"),
         "per_call_timing": "outside the step, every figure timed per call is the median of calls each "
                            "between HIP events on the library's stream, enqueued behind a ~0.3 ms spin "
                            "kernel so that the GPU reaches the first event only after the host has "
