@@ -192,12 +192,18 @@ def pmc_per_dispatch(d: str, counter: str, path: str):
     return out
 
 
-def pmc_commands(gemm: str):
-    """The two counter runs both traffic summaries come from (GEMM call and streaming quantize)."""
+def pmc_dir(kind: str, gemm: str, workload: str = HEADLINE) -> str:
+    return f"gpurun_out/pmc_{kind}_{gemm}" + ("" if workload == HEADLINE else f"_{workload}")
+
+
+def pmc_commands(gemm: str, workload: str = HEADLINE):
+    """The two counter runs a traffic summary comes from (on the headline workload: the GEMM call's
+    and the streaming quantize's)."""
+    other = "" if workload == HEADLINE else f" --workload {workload} --no-stream --no-reference"
     run = (f"python bench.py --steps 3 --warmup 1 --no-cpu-baseline --no-backward --no-radix --no-static --no-requant "
            f"--no-blocks --no-configs "
-           f"--copy-calibration --gemm {gemm}")
-    return [f"rocprofv3 --pmc {c} --output-format csv -d gpurun_out/pmc_{d}_{gemm} -o pmc -- {run}"
+           f"--copy-calibration --gemm {gemm}{other}")
+    return [f"rocprofv3 --pmc {c} --output-format csv -d {pmc_dir(d, gemm, workload)} -o pmc -- {run}"
             for c, d in (("FETCH_SIZE", "fetch"), ("WRITE_SIZE", "write"))]
 
 
@@ -263,7 +269,7 @@ def summarize_stream_pmc(args):
         "",
         "```",
         *pmc_commands(args.gemm),
-        f"python bench.py --summarize-stream-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}",
+        f"python bench.py --summarize-stream-pmc {pmc_dir('fetch', args.gemm)} {pmc_dir('write', args.gemm)}",
         "```",
         "",
         "Kernel: `quantize_rows_kernel<Fmt<4, 3>, true, 2, ...>` (bf16 -> E4C3, 2 chunks per thread), the "
@@ -298,7 +304,7 @@ def summarize_pmc(args):
     gemm_fetch = fetch["gemm"][0] * 1024.0 / f_fetch
     gemm_write = write["gemm"][0] * 1024.0 / f_write
     kernels = CALL_KERNELS[args.gemm]
-    flag = f" --gemm {args.gemm}"
+    flag = f" --gemm {args.gemm}" + ("" if args.workload == HEADLINE else f" --workload {args.workload}")
     roof_fetch = fetch["roofline"][0] * 1024.0 / f_fetch
     roof_write = write["roofline"][0] * 1024.0 / f_write
     lines = [
@@ -307,8 +313,9 @@ def summarize_pmc(args):
         "Commands (from the repository root on one MI355X; each pass is its own run):",
         "",
         "```",
-        *pmc_commands(args.gemm),
-        f"python bench.py --summarize-pmc gpurun_out/pmc_fetch_{args.gemm} gpurun_out/pmc_write_{args.gemm}{flag}",
+        *pmc_commands(args.gemm, args.workload),
+        f"python bench.py --summarize-pmc {pmc_dir('fetch', args.gemm, args.workload)} "
+        f"{pmc_dir('write', args.gemm, args.workload)}{flag}",
         "```",
         "",
         "| kernel | dispatches | FETCH_SIZE KiB per call | WRITE_SIZE KiB per call |",
