@@ -201,6 +201,17 @@ int curvefp_dequantize(const void* codes, const int8_t* scales, int format,
                        float* dst, int64_t ld_dst, void* stream);
 
 /*
+ * Size limits of the GEMM entry points (curvefp_gemm, curvefp_gemm_ws, the prepared calls,
+ * curvefp_gemm_ws_static, curvefp_gemm_requant, curvefp_gemm_mixed and their byte counts):
+ * K <= CURVEFP_MAX_K, and for curvefp_gemm also M <= CURVEFP_MAX_M_FUSED; larger sizes return
+ * CURVEFP_ERR_SHAPE before anything is launched.  The expansion's grid has one workgroup row per
+ * four K blocks of 32 and the fused kernel's one per 256 rows of A, at most 65535 each; within
+ * these limits every kernel's byte offsets inside a tile of 256 rows stay below 2^31.
+ */
+#define CURVEFP_MAX_K ((int64_t)8388480)        /* 32 * 4 * 65535 */
+#define CURVEFP_MAX_M_FUSED ((int64_t)16776960) /* 256 * 65535 */
+
+/*
  * CurveFP GEMM: C[M][N] = deq(A)[M][K] . deq(B)[N][K]^T in fp32, the forward
  * contract Q_A(X) Q_W(W)^T of Sec. 3.3 with both operands K-contiguous
  * (A codes [M][K], B codes [N][K], scales [.][K/G], one format and one G for both).

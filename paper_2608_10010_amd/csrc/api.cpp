@@ -35,6 +35,9 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int hip_status(hipError_t e) { return e == hipSuccess ? CURVEFP_OK : CURVEFP_ERR_HIP; }
 
+// contraction length of the GEMM entry points: positive, whole groups of 32, at most CURVEFP_MAX_K
+bool gemm_k_ok(int64_t K) { return K > 0 && K % 32 == 0 && K <= CURVEFP_MAX_K; }
+
 }  // namespace
 
 #pragma GCC visibility push(default)
@@ -169,14 +172,15 @@ int curvefp_gemm(const void* a_codes, const int8_t* a_scales, const void* b_code
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M > CURVEFP_MAX_M_FUSED) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     return hip_status(launch_gemm(a_codes, a_scales, b_codes, b_scales, M, N, K, format, block, c, ldc,
                                   reinterpret_cast<hipStream_t>(stream)));
 }
 
 int64_t curvefp_gemm_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K)) return CURVEFP_ERR_SHAPE;
     return gemm_workspace_bytes(M, N, K);
 }
 
@@ -186,7 +190,7 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c || !workspace) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
@@ -195,7 +199,7 @@ int curvefp_gemm_ws(const void* a_codes, const int8_t* a_scales, const void* b_c
 }
 
 int64_t curvefp_prepared_bytes(int64_t rows, int64_t k, int trans) {
-    if (rows <= 0 || k <= 0 || k % 32 || (trans != 0 && trans != 1)) return CURVEFP_ERR_SHAPE;
+    if (rows <= 0 || !gemm_k_ok(k) || (trans != 0 && trans != 1)) return CURVEFP_ERR_SHAPE;
     return prepared_bytes(rows, k, trans);
 }
 
@@ -204,7 +208,7 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
     if (!codes || !scales || !prepared) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block) || (trans != 0 && trans != 1)) return CURVEFP_ERR_BLOCK;
-    if (rows <= 0 || k <= 0 || k % 32) return CURVEFP_ERR_SHAPE;
+    if (rows <= 0 || !gemm_k_ok(k)) return CURVEFP_ERR_SHAPE;
     // blocks along k (trans 0) or along the rows of the reused operand (trans 1), whose expansion
     // grid has one workgroup row per 256 rows
     if (trans ? (rows % block || (rows + 255) / 256 > 65535) : k % block) return CURVEFP_ERR_SHAPE;
@@ -215,7 +219,7 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
 }
 
 int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K)) return CURVEFP_ERR_SHAPE;
     return gemm_prepared_workspace_bytes(M, N, K);
 }
 
@@ -224,7 +228,7 @@ int curvefp_gemm_prepared(const void* a_prepared, int format_a, const void* b_pr
                           void* stream) {
     if (!a_prepared || !b_prepared || !c) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format_a) || !fmt_ok(format_b)) return CURVEFP_ERR_FORMAT;
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || ldc < N) return CURVEFP_ERR_SHAPE;
     const int64_t need = gemm_prepared_workspace_bytes(M, N, K);
     if (need > 0 && !workspace) return CURVEFP_ERR_NULL;
     if (workspace_bytes < need) return CURVEFP_ERR_SHAPE;
@@ -241,7 +245,7 @@ int curvefp_gemm_ws_static(const void* a_codes, const int8_t* a_scales, const vo
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c) return CURVEFP_ERR_NULL;
     if (!fmt_ok(format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || K % block || ldc < N) return CURVEFP_ERR_SHAPE;
     if (gemm_workspace_bytes(M, N, K) > CURVEFP_STATIC_SCRATCH_BYTES) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(c)) return CURVEFP_ERR_ALIGN;
     void* ws = nullptr;
@@ -260,7 +264,7 @@ int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void
     if (!block_ok(block)) return CURVEFP_ERR_BLOCK;
     // output blocks lie inside one 256-column tile of the epilogue
     if (out_block != 32 && out_block != 64 && out_block != 128 && out_block != 256) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % block || N % out_block) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || K % block || N % out_block) return CURVEFP_ERR_SHAPE;
     if (workspace_bytes < gemm_workspace_bytes(M, N, K)) return CURVEFP_ERR_SHAPE;
     if (!aligned16(a_codes) || !aligned16(b_codes) || !aligned16(out_codes)) return CURVEFP_ERR_ALIGN;
     if (reinterpret_cast<uintptr_t>(workspace) % 256) return CURVEFP_ERR_ALIGN;
@@ -270,7 +274,7 @@ int curvefp_gemm_requant(const void* a_codes, const int8_t* a_scales, const void
 }
 
 int64_t curvefp_gemm_mixed_workspace_bytes(int64_t M, int64_t N, int64_t K) {
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K)) return CURVEFP_ERR_SHAPE;
     return gemm_mixed_workspace_bytes(M, N, K);
 }
 
@@ -281,7 +285,7 @@ int curvefp_gemm_mixed(const void* a_codes, const int8_t* a_scales, int a_format
     if (!a_codes || !a_scales || !b_codes || !b_scales || !c || !workspace) return CURVEFP_ERR_NULL;
     if (!fmt_ok(a_format) || !fmt_ok(b_format)) return CURVEFP_ERR_FORMAT;
     if (!block_ok(block) || (a_trans != 0 && a_trans != 1) || (b_trans != 0 && b_trans != 1)) return CURVEFP_ERR_BLOCK;
-    if (M <= 0 || N <= 0 || K <= 0 || K % 32 || ldc < N) return CURVEFP_ERR_SHAPE;
+    if (M <= 0 || N <= 0 || !gemm_k_ok(K) || ldc < N) return CURVEFP_ERR_SHAPE;
     // an operand quantized along K has its blocks along K; a reused operand has them along its
     // GEMM rows; the expansion grid has one workgroup row per 256 GEMM rows of each reused
     // operand (at most 65535 in all)

@@ -370,6 +370,49 @@ def test_gemm_requant_validation(L):
     assert g(*a) == EALIGN
 
 
+def header_define(name):
+    text = open(os.path.join(ROOT, "include", "curvefp.h")).read()
+    return int(re.search(rf"#define {name} \(\(int64_t\)(\d+)\)", text).group(1))
+
+
+def test_gemm_size_limits(L):
+    # K <= CURVEFP_MAX_K for every GEMM entry point and M <= CURVEFP_MAX_M_FUSED for the fused one;
+    # a size at the limit passes the shape checks (a misaligned pointer then stops the call)
+    KMAX, MMAX = header_define("CURVEFP_MAX_K"), header_define("CURVEFP_MAX_M_FUSED")
+    assert KMAX == 32 * 4 * 65535 and MMAX == 256 * 65535
+    KBIG = KMAX + 32
+    for f in (L.curvefp_gemm_workspace_bytes, L.curvefp_gemm_prepared_workspace_bytes,
+              L.curvefp_gemm_mixed_workspace_bytes):
+        assert f(64, 64, KMAX) >= 0
+        assert f(64, 64, KBIG) == ESHAPE
+    for t in (0, 1):
+        assert L.curvefp_prepared_bytes(64, KMAX, t) > 0
+        assert L.curvefp_prepared_bytes(64, KBIG, t) == ESHAPE
+    g = L.curvefp_gemm
+    assert g(FAKE, FAKE, FAKE, FAKE, 64, 64, KBIG, 0, 32, FAKE, 64, None) == ESHAPE
+    assert g(MIS, FAKE, FAKE, FAKE, 64, 64, KMAX, 0, 32, FAKE, 64, None) == EALIGN
+    assert g(FAKE, FAKE, FAKE, FAKE, MMAX + 1, 64, 64, 0, 32, FAKE, 64, None) == ESHAPE
+    assert g(MIS, FAKE, FAKE, FAKE, MMAX, 64, 64, 0, 32, FAKE, 64, None) == EALIGN
+    WS = 1 << 24
+    BIG = 1 << 62                      # a workspace size no check can find too small
+    assert L.curvefp_gemm_ws(FAKE, FAKE, FAKE, FAKE, 64, 64, KBIG, 0, 32, FAKE, 64, WS, BIG, None) == ESHAPE
+    assert L.curvefp_gemm_ws(MIS, FAKE, FAKE, FAKE, 64, 64, KMAX, 0, 32, FAKE, 64, WS, BIG, None) == EALIGN
+    assert L.curvefp_gemm_ws_static(FAKE, FAKE, FAKE, FAKE, 64, 64, KBIG, 0, 32, FAKE, 64, None) == ESHAPE
+    p = L.curvefp_prepare
+    assert p(FAKE, FAKE, 64, KBIG, 0, 32, 0, WS, BIG, None) == ESHAPE
+    assert p(MIS, FAKE, 64, KMAX, 0, 32, 0, WS, BIG, None) == EALIGN
+    assert p(FAKE, FAKE, 64, KBIG, 0, 32, 1, WS, BIG, None) == ESHAPE
+    gp = L.curvefp_gemm_prepared
+    assert gp(WS, 0, WS, 0, 64, 64, KBIG, FAKE, 64, WS, BIG, None) == ESHAPE
+    assert gp(WS, 0, WS, 0, 64, 64, KMAX, MIS, 64, WS, BIG, None) == EALIGN
+    rq = L.curvefp_gemm_requant
+    assert rq(FAKE, FAKE, FAKE, FAKE, 64, 64, KBIG, 0, 32, 2, 32, FAKE, FAKE, WS, BIG, None) == ESHAPE
+    assert rq(MIS, FAKE, FAKE, FAKE, 64, 64, KMAX, 0, 32, 2, 32, FAKE, FAKE, WS, BIG, None) == EALIGN
+    gm = L.curvefp_gemm_mixed
+    assert gm(FAKE, FAKE, 1, 0, FAKE, FAKE, 0, 1, 64, 64, KBIG, 32, FAKE, 64, WS, BIG, None) == ESHAPE
+    assert gm(MIS, FAKE, 1, 0, FAKE, FAKE, 0, 1, 64, 64, KMAX, 32, FAKE, 64, WS, BIG, None) == EALIGN
+
+
 def test_quantize_compact_validation(L):
     q = L.curvefp_quantize_compact
     #       src   dt rows cols ld  fmt blk S  codes ref   offs  stream
