@@ -325,6 +325,28 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
                     void* stream);
 
 /*
+ * Quantize and prepare in one pass: Q(X) of Sec. 3.1 for a [rows][k] source with blocks along
+ * k (curvefp_quantize with block_axis = 1), the result's prepared form for the GEMM (Sec. 3.3:
+ * what curvefp_prepare writes from these codes with trans = 0) and, when dst is not null, its
+ * reconstruction (Eq. curvefp-value: what curvefp_dequantize writes), from one read of the
+ * source.  codes, scales, prepared and dst are bit for bit those of the three separate calls.
+ *   src      [rows][ld_src] fp32 (dtype 0) or bf16 (dtype 1), 16-byte aligned rows.
+ *   codes    [rows][k] (E3C3 [rows][k/32][28]), scales [rows][k/block], 16-byte aligned codes.
+ *   prepared at least curvefp_prepared_bytes(rows, k, 0) bytes (prepared_size), 256-byte aligned.
+ *   dst      null, or [rows][ld_dst] fp32 with 16-byte aligned rows.
+ * Each row is held in on-chip memory between reading and writing, which bounds k: k <= 16384
+ * for bf16 and k <= 8192 for fp32 sources, and block is 32, 64, 128, 256 or 512 (longer rows
+ * and other G: curvefp_quantize, curvefp_prepare and curvefp_dequantize).  Errors:
+ * CURVEFP_ERR_NULL (src, codes, scales or prepared), _FORMAT (dtype or format), _BLOCK, _SHAPE
+ * (non-positive sizes, k % block, k beyond the bound, ld_src < k, ld_dst < k, prepared_size
+ * too small, rows >= 2^31), _ALIGN, _HIP.
+ */
+int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld_src,
+                             int format, int block, void* codes, int8_t* scales,
+                             void* prepared, int64_t prepared_size, float* dst, int64_t ld_dst,
+                             void* stream);
+
+/*
  * Bytes of device workspace curvefp_gemm_prepared needs for an M x N x K product: 0 unless K
  * is split in two (fewer than 256 output tiles of 256 x 256 and K >= 512; then one arrival
  * counter per tile and 512 KiB of partial sums per tile).  CURVEFP_ERR_SHAPE for non-positive

@@ -218,6 +218,26 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
                                      reinterpret_cast<hipStream_t>(stream)));
 }
 
+int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld_src, int format,
+                             int block, void* codes, int8_t* scales, void* prepared, int64_t prepared_size, float* dst,
+                             int64_t ld_dst, void* stream) {
+    if (!src || !codes || !scales || !prepared) return CURVEFP_ERR_NULL;
+    if ((dtype != 0 && dtype != 1) || !fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    // a block's maximum is reduced over the 4 .. 64 lanes that hold it
+    if (block != 32 && block != 64 && block != 128 && block != 256 && block != 512) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || rows >= ((int64_t)1 << 31) || k <= 0 || k % block || ld_src < k) return CURVEFP_ERR_SHAPE;
+    // one row per wave, held in LDS between the two passes
+    if (k > (dtype == 1 ? 16384 : 8192)) return CURVEFP_ERR_SHAPE;
+    if (dst && ld_dst < k) return CURVEFP_ERR_SHAPE;
+    if (prepared_size < prepared_bytes(rows, k, 0)) return CURVEFP_ERR_SHAPE;
+    const int64_t esz = dtype == 1 ? 2 : 4;
+    if (!aligned16(src) || (ld_src * esz) % 16 || !aligned16(codes) || reinterpret_cast<uintptr_t>(prepared) % 256)
+        return CURVEFP_ERR_ALIGN;
+    if (dst && (!aligned16(dst) || (ld_dst * 4) % 16)) return CURVEFP_ERR_ALIGN;
+    return hip_status(launch_quantize_prepare(src, dtype, rows, k, ld_src, format, block, codes, scales, prepared, dst,
+                                              ld_dst, reinterpret_cast<hipStream_t>(stream)));
+}
+
 int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) {
     if (M <= 0 || N <= 0 || !gemm_k_ok(K)) return CURVEFP_ERR_SHAPE;
     return gemm_prepared_workspace_bytes(M, N, K);

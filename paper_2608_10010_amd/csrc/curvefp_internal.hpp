@@ -35,6 +35,11 @@ hipError_t launch_quantize_compact(const void* src, int dtype, int64_t rows, int
                                   hipStream_t s);
 hipError_t launch_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, int64_t rows, int64_t nblocks,
                                 int scale_bits, int8_t* scales, hipStream_t s);
+// quantize [rows][k] along k and write the result's prepared form (launch_prepare's layout, trans 0)
+// and, if dst is not null, its reconstruction; block in 32..512 (a power of two), k % block == 0
+hipError_t launch_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format,
+                                  int block, void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst,
+                                  hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
                              int64_t outer, int64_t k, int block, float* dst, int64_t ld_dst, hipStream_t s);
 // workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)

@@ -36,6 +36,7 @@
 #include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
+#include "planes.hpp"
 #include "curvefp_tables.inc"
 
 #include <cstring>
@@ -65,18 +66,14 @@ constexpr QRule qrule(int f) { return QRule{kOz[f], kOhi[f], kQlutSize[f], kEc[f
 namespace {
 
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
-typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = 256, BK = 32;
 constexpr int NTHREADS = 256;
 constexpr int WM = 128, TM = 4;
 constexpr int LUT_COPIES = 16;
 constexpr int LUT_BYTES = GEMM_DEC_ENTRIES * LUT_COPIES * 4;
-constexpr int ROW_BYTES = BK * 2;                 // one fp16 plane row: 32 halves
-constexpr int PLANE = BM * ROW_BYTES;             // 16 KB: one hi or lo plane of A
 
 // tile shape: 256 x BN_ outputs, four waves of 128 x BN_/2 (BN_ = 256 or 128)
 template <int BN_>
@@ -98,24 +95,10 @@ struct Tile {
 // sched_group_barrier masks
 constexpr int SG_VALU = 0x002, SG_MFMA = 0x008, SG_DS_RD = 0x100;
 
-// Row maxima of block scales are taken over keys: a block that held a NaN or an infinity (scale
-// -128) counts as POISON_KEY, above every scale, so a row's maximum is at least POISON_KEY exactly
-// when one of its blocks is poisoned.  Such a row's expansion then flushes every element (its
-// offsets to the maximum are hundreds of binades), and the epilogue writes NaN for each output in
-// that row or column: C = deq(A) deq(B)^T with the poisoned blocks reconstructing to NaN.
-constexpr int POISON_KEY = 0x4000;
-__device__ __forceinline__ int scale_key(int s) { return s == -128 ? POISON_KEY : s; }
+// the epilogue's NaN for an output whose row or column holds a poisoned block (row maxima at or
+// above POISON_KEY): C = deq(A) deq(B)^T with the poisoned blocks reconstructing to NaN
 __device__ __forceinline__ float poisoned(float v, int row_max, int col_max) {
     return (row_max >= POISON_KEY || col_max >= POISON_KEY) ? __builtin_nanf("") : v;
-}
-
-// byte offset of 16-byte chunk q (k = 8q .. 8q+7) of tile row r
-__device__ __forceinline__ int swz(int r, int q) { return r * ROW_BYTES + 16 * (q ^ (((r >> 1) ^ (r >> 3)) & 3)); }
-
-__device__ __forceinline__ uint32_t f16_pow2_neg(int d) {
-    // bits of the fp16 value 2^-d for 0 <= d <= 24 (exact: subnormal below 2^-14)
-    const _Float16 m = __builtin_amdgcn_ldexph((_Float16)1.0f, -d);
-    return (uint32_t)__builtin_bit_cast(uint16_t, m);
 }
 
 template <class F>
@@ -179,10 +162,6 @@ __device__ __forceinline__ uint32_t chunk_code(const Chunk& r, int i) {
     if (!F::PACKED7) return (r.w[i >> 2] >> (8 * (i & 3))) & 0xFFu;
     const uint64_t v = (uint64_t)r.w[0] | ((uint64_t)r.w[1] << 32);
     return (uint32_t)(v >> (7 * i)) & 0x7Fu;
-}
-
-__device__ __forceinline__ uint32_t pk_mul(uint32_t x, half2v m) {
-    return __builtin_bit_cast(uint32_t, __builtin_bit_cast(half2v, x) * m);
 }
 
 // expansion of one task, in two parts so the table gathers of the next task can be in flight
@@ -775,22 +754,8 @@ __global__ __launch_bounds__(256) void expand_kernel(ExpandOperand opA, ExpandOp
         uint32_t e[8];
 #pragma unroll
         for (int i = 0; i < 8; i++) e[i] = lut[chunk_code<F>(c, i)];
-        const int D = alpha - c.a;
-        const half2v m1 = __builtin_bit_cast(half2v, f16_pow2_neg(min(max(D, 0), 24)) * 0x10001u);
         uint32_t hv[4], lv[4];
-#pragma unroll
-        for (int p = 0; p < 4; p++) {
-            hv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x05040100u), m1);
-            lv[p] = pk_mul(__builtin_amdgcn_perm(e[2 * p + 1], e[2 * p], 0x07060302u), m1);
-        }
-        if (D > 24) {   // a block more than 24 binades below its row's top: second multiply
-            const half2v m2 = __builtin_bit_cast(half2v, f16_pow2_neg(min(D - 24, 24)) * 0x10001u);
-#pragma unroll
-            for (int p = 0; p < 4; p++) {
-                hv[p] = pk_mul(hv[p], m2);
-                lv[p] = pk_mul(lv[p], m2);
-            }
-        }
+        expand_chunk8(e, alpha - c.a, hv, lv);
         char* dst = planes + (kb * RT + row / BM) * (2 * PLANE) + swz((int)(row % BM), q);
         *reinterpret_cast<uint4*>(dst) = make_uint4(hv[0], hv[1], hv[2], hv[3]);
         *reinterpret_cast<uint4*>(dst + PLANE) = make_uint4(lv[0], lv[1], lv[2], lv[3]);

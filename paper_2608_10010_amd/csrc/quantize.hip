@@ -19,6 +19,7 @@
 #include "codec.hpp"
 #include "curvefp_internal.hpp"
 #include "device_util.hpp"
+#include "planes.hpp"
 #include "curvefp_tables.inc"
 
 #include <cstring>
@@ -36,6 +37,8 @@ __constant__ uint32_t g_lmax_mant[NUM_FORMATS] = CURVEFP_LMAX_MANT_INIT;
 // radix 8 entries by curve index, rational radix 128 by magnitude rank
 __constant__ uint32_t g_qr_mant[NUM_FORMATS][128] = CURVEFP_QR_MANT_INIT;
 __constant__ uint64_t g_qr_sig[NUM_FORMATS][128] = CURVEFP_QR_SIG_INIT;
+// the GEMM operands' expansion pairs (the GEMM's table, gemm.hip), for quantize-and-prepare
+__constant__ uint32_t g_qp_dec[NUM_FORMATS][GEMM_DEC_ENTRIES] = CURVEFP_DEC_INIT;
 
 namespace {
 
@@ -137,17 +140,21 @@ __device__ __forceinline__ uint32_t group_max_u32(uint32_t v, int lgl) {
     return v;
 }
 
-// codes of chunk g (8 consecutive elements, magnitudes and signs) at scale a, stored at chunk g
-// of `codes`; E3C3 packs 7 bits per code over the quad that holds a group of 32
-template <class F, bool NTS, class T>
-__device__ __forceinline__ void encode_chunk(const uint32_t* mag, const uint32_t* sgn, int a, uint32_t g,
-                                             const T* lut, uint8_t* __restrict__ codes) {
-    const int part = (int)(g & 3);
+// the codes of 8 consecutive elements (magnitudes and signs) at scale a
+template <class F, class T>
+__device__ __forceinline__ void chunk_codes(const uint32_t* mag, const uint32_t* sgn, int a, const T* lut,
+                                            uint32_t* c) {
     uint32_t rk[8];
     ranks_of<F>(mag, 8, a, lut, rk);
-    uint32_t c[8];
 #pragma unroll
     for (int i = 0; i < 8; i++) c[i] = rk[i] | ((rk[i] != 0 ? sgn[i] : 0u) << F::EC);
+}
+
+// codes c of chunk g stored at chunk g of `codes`; E3C3 packs 7 bits per code over the quad that
+// holds a group of 32
+template <class F, bool NTS>
+__device__ __forceinline__ void store_codes(const uint32_t* c, uint32_t g, uint8_t* __restrict__ codes) {
+    const int part = (int)(g & 3);
     const uint32_t b = g >> 2;   // group of 32 (groups are contiguous in the output)
     if (!F::PACKED7) {
         st8<NTS>(codes + (uint64_t)g * 8, c[0] | (c[1] << 8) | (c[2] << 16) | (c[3] << 24),
@@ -172,6 +179,16 @@ __device__ __forceinline__ void encode_chunk(const uint32_t* mag, const uint32_t
             st4<NTS>(base + 6, (uint32_t)(chunk >> 24));
         }
     }
+}
+
+// codes of chunk g (8 consecutive elements, magnitudes and signs) at scale a, stored at chunk g
+// of `codes`
+template <class F, bool NTS, class T>
+__device__ __forceinline__ void encode_chunk(const uint32_t* mag, const uint32_t* sgn, int a, uint32_t g,
+                                             const T* lut, uint8_t* __restrict__ codes) {
+    uint32_t c[8];
+    chunk_codes<F>(mag, sgn, a, lut, c);
+    store_codes<F, NTS>(c, g, codes);
 }
 
 // quantize one chunk of 8 consecutive elements; 2^lgl consecutive lanes hold one block of
@@ -1233,6 +1250,189 @@ hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols
     return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------------------------
+// Quantize and prepare in one launch: Q(X) of Sec. 3.1 with blocks along the rows, then the
+// result's staging as a GEMM operand (Sec. 3.3) -- the planes and row maxima that curvefp_prepare
+// writes from these codes (planes.hpp) -- and, when dst is given, the reconstruction of
+// Eq. curvefp-value that curvefp_dequantize writes.  One wave per row, in two passes over the
+// row's chunks (8 elements; chunk g = 64 UL s + 64 u + lane in segment s, UL chunks per lane in
+// flight): the first reads the source from HBM once, takes every block's scale and the row's
+// largest scale key alpha and keeps the chunks in LDS (up to 64 U per wave); the second takes
+// them back from LDS and writes.  Slots past the row's end hold zeros (scale -127, the bottom key,
+// so alpha is unchanged) and store nothing.  Waves of the padding rows (up to the next multiple
+// of 256) write zero planes and a zero row maximum, as the expansion does past the operand.
+template <class F, bool BF16, int U>
+__global__ __launch_bounds__(256) void quantize_prepare_kernel(
+    const void* __restrict__ src, int64_t rows, int64_t ld, uint32_t cpr, int64_t code_row_bytes,
+    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int64_t nsb, char* __restrict__ planes,
+    int* __restrict__ rmax, int64_t RT, float* __restrict__ dst, int64_t ld_dst, int fidx, int lgl) {
+    using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
+    constexpr int ESZ = BF16 ? 2 : 4;
+    constexpr int NV = BF16 ? 1 : 2;   // 16-byte loads per chunk
+    constexpr int UL = U < 4 ? U : 4;
+    static_assert(GEMM_DEC_ENTRIES == 256, "one expansion entry per thread");
+    __shared__ __attribute__((aligned(16))) uint4 rowbuf[4 * 64 * U * NV];
+    __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
+    __shared__ uint32_t dec[GEMM_DEC_ENTRIES];
+    __shared__ uint32_t qmant[128];
+    __shared__ uint64_t qsig[128];
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const bool real = row < rows;
+    uint4* wbuf = rowbuf + (threadIdx.x >> 6) * (64 * U * NV);
+    const uint4* srow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) + (real ? row : 0) * ld * ESZ);
+    const uint32_t nseg = (cpr + 64 * UL - 1) / (64 * UL);
+    auto load = [&](uint32_t seg, uint4 (*v)[NV]) {
+#pragma unroll
+        for (int u = 0; u < UL; u++) {
+            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+#pragma unroll
+            for (int t = 0; t < NV; t++) v[u][t] = make_uint4(0u, 0u, 0u, 0u);
+            if (real && g < cpr) {
+#pragma unroll
+                for (int t = 0; t < NV; t++) v[u][t] = ld16<true>(srow + NV * g + t);
+            }
+        }
+    };
+    // the first segment is requested before the tables are filled, so both latencies overlap
+    uint4 cur[UL][NV];
+    load(0, cur);
+    if (BF16) {
+        const uint32_t* s32 = reinterpret_cast<const uint32_t*>(g_qlut8[fidx]);
+        uint32_t* l32 = reinterpret_cast<uint32_t*>(lut);
+        for (int i = threadIdx.x; i < F::QLUT_SIZE / 4; i += blockDim.x) l32[i] = s32[i];
+    } else {
+        for (int i = threadIdx.x; i < F::QLUT_SIZE; i += blockDim.x) lut[i] = (T)g_qlut[fidx][i];
+    }
+    dec[threadIdx.x] = g_qp_dec[fidx][threadIdx.x];
+    if (dst != nullptr && threadIdx.x < 128) {
+        qmant[threadIdx.x] = g_qr_mant[fidx][threadIdx.x];
+        qsig[threadIdx.x] = g_qr_sig[fidx][threadIdx.x];
+    }
+    const uint32_t lmax_mant = g_lmax_mant[fidx];
+    __syncthreads();
+
+    const int64_t rt = row / BM;
+    const int rr = (int)(row - rt * BM);
+    if (!real) {
+        if (row < RT * BM) {
+            for (uint32_t g = (uint32_t)lane; g < cpr; g += 64) {
+                char* pd = planes + ((int64_t)(g >> 2) * RT + rt) * (2 * PLANE) + swz(rr, (int)(g & 3));
+                *reinterpret_cast<uint4*>(pd) = make_uint4(0u, 0u, 0u, 0u);
+                *reinterpret_cast<uint4*>(pd + PLANE) = make_uint4(0u, 0u, 0u, 0u);
+            }
+            if (lane == 0) rmax[row] = 0;
+        }
+        return;
+    }
+
+    // the block scale of a chunk: the 2^lgl lanes of a block share its largest magnitude
+    auto chunk_scale = [&](const uint4* v) {
+        uint32_t mag[8], sgn[8];
+        unpack8<BF16>(v, mag, sgn);
+        uint32_t amax = 0;
+#pragma unroll
+        for (int i = 0; i < 8; i++) amax = max(amax, mag[i]);
+        amax = lgl == 2 ? quad_max_u32(amax) : group_max_u32(amax, lgl);
+        return scale_of<F>(amax, lmax_mant);
+    };
+
+    // pass 1: the row's top key; the chunks go to LDS
+    int key = -128;
+    for (uint32_t seg = 0; seg < nseg; seg++) {
+        uint4 nxt[UL][NV];
+        if (seg + 1 < nseg) load(seg + 1, nxt);
+#pragma unroll
+        for (int u = 0; u < UL; u++) {
+            key = max(key, scale_key(chunk_scale(cur[u])));
+            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+#pragma unroll
+            for (int t = 0; t < NV; t++) wbuf[NV * g + t] = cur[u][t];
+        }
+#pragma unroll
+        for (int u = 0; u < UL; u++)
+#pragma unroll
+            for (int t = 0; t < NV; t++) cur[u][t] = nxt[u][t];
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o));
+    const int alpha = key;
+
+    // pass 2: codes and scales, both planes, the reconstruction
+    uint8_t* crow = codes + row * code_row_bytes;
+    int8_t* scrow = scales + row * nsb;
+    for (uint32_t seg = 0; seg < nseg; seg++) {
+#pragma unroll
+        for (int u = 0; u < UL; u++) {
+            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+            uint4 v[NV];
+#pragma unroll
+            for (int t = 0; t < NV; t++) v[t] = wbuf[NV * g + t];
+            const int a = chunk_scale(v);
+            if (g >= cpr) continue;   // whole blocks: cpr is a multiple of a block's lanes
+            uint32_t mag[8], sgn[8];
+            unpack8<BF16>(v, mag, sgn);
+            uint32_t c[8];
+            chunk_codes<F>(mag, sgn, a, lut, c);
+            store_codes<F, true>(c, g, crow);
+            if ((g & ((1u << lgl) - 1)) == 0) scrow[g >> lgl] = (int8_t)a;
+            uint32_t e[8];
+#pragma unroll
+            for (int i = 0; i < 8; i++) e[i] = dec[c[i]];
+            uint32_t hv[4], lv[4];
+            expand_chunk8(e, alpha - a, hv, lv);
+            char* pd = planes + ((int64_t)(g >> 2) * RT + rt) * (2 * PLANE) + swz(rr, (int)(g & 3));
+            *reinterpret_cast<uint4*>(pd) = make_uint4(hv[0], hv[1], hv[2], hv[3]);
+            *reinterpret_cast<uint4*>(pd + PLANE) = make_uint4(lv[0], lv[1], lv[2], lv[3]);
+            if (dst != nullptr) {
+                uint32_t o[8];
+#pragma unroll
+                for (int i = 0; i < 8; i++) o[i] = a == -128 ? 0x7FC00000u : value_bits<F>(c[i], a, qmant, qsig);
+                uint4* out = reinterpret_cast<uint4*>(dst + row * ld_dst + (int64_t)g * 8);
+                out[0] = make_uint4(o[0], o[1], o[2], o[3]);
+                out[1] = make_uint4(o[4], o[5], o[6], o[7]);
+            }
+        }
+    }
+    if (lane == 0) rmax[row] = alpha;
+}
+
+template <class F, bool BF16, int U>
+hipError_t launch_qp_u(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
+                       int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
+    const int64_t RT = (rows + BM - 1) / BM;
+    int lgl = 0;
+    while ((8 << lgl) < block) lgl++;
+    const int64_t code_row_bytes = F::PACKED7 ? k / 32 * 28 : k;
+    char* rmax = planes + (k / 32) * RT * 2 * PLANE;   // the prepared layout: planes, then row maxima
+    hipLaunchKernelGGL((quantize_prepare_kernel<F, BF16, U>), dim3((unsigned)(RT * 64)), dim3(256), 0, s, src, rows,
+                       ld, (uint32_t)(k / 8), code_row_bytes, codes, scales, k / block, planes,
+                       reinterpret_cast<int*>(rmax), RT, dst, ld_dst, fidx, lgl);
+    return hipGetLastError();
+}
+
+// chunks per lane: the fewest of 2, 4, ..., 32 that hold a row of k / 8 chunks in one wave
+template <class F, bool BF16>
+hipError_t launch_qp(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
+                     int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
+    const int64_t cpr = k / 8;
+    if (cpr <= 128) return launch_qp_u<F, BF16, 2>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 256) return launch_qp_u<F, BF16, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 512) return launch_qp_u<F, BF16, 8>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 1024 || !BF16)
+        return launch_qp_u<F, BF16, 16>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    return launch_qp_u<F, BF16, (BF16 ? 32 : 16)>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+}
+
+template <class F>
+hipError_t launch_qp_fmt(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int fidx, int block,
+                         void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst, hipStream_t s) {
+    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
+    char* pp = reinterpret_cast<char*>(prepared);
+    return dtype == 1 ? launch_qp<F, true>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s)
+                      : launch_qp<F, false>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s);
+}
 }  // namespace
 
 hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld,
@@ -1249,6 +1449,20 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 }  // namespace curvefp
 
 namespace curvefp {
+
+hipError_t launch_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format,
+                                  int block, void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst,
+                                  hipStream_t s) {
+    switch (format) {
+        case 0: return launch_qp_fmt<FmtE4C3>(src, dtype, rows, k, ld, 0, block, codes, scales, prepared, dst, ld_dst, s);
+        case 1: return launch_qp_fmt<FmtE5C2>(src, dtype, rows, k, ld, 1, block, codes, scales, prepared, dst, ld_dst, s);
+        case 2: return launch_qp_fmt<FmtE3C3>(src, dtype, rows, k, ld, 2, block, codes, scales, prepared, dst, ld_dst, s);
+        case 3:
+            return launch_qp_fmt<FmtE4C3R89>(src, dtype, rows, k, ld, 3, block, codes, scales, prepared, dst, ld_dst, s);
+        default:
+            return launch_qp_fmt<FmtE4C3R34>(src, dtype, rows, k, ld, 4, block, codes, scales, prepared, dst, ld_dst, s);
+    }
+}
 
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,
                                int format, int block, int candidates, void* codes, int8_t* scales, hipStream_t s) {

@@ -77,6 +77,8 @@ def lib() -> ctypes.CDLL:
         L.curvefp_prepared_bytes.restype = I64
         L.curvefp_prepare.argtypes = [P, P, I64, I64, I, I, I, P, I64, P]
         L.curvefp_prepare.restype = I
+        L.curvefp_quantize_prepare.argtypes = [P, I, I64, I64, I64, I, I, P, P, P, I64, P, I64, P]
+        L.curvefp_quantize_prepare.restype = I
         L.curvefp_gemm_prepared_workspace_bytes.argtypes = [I64, I64, I64]
         L.curvefp_gemm_prepared_workspace_bytes.restype = I64
         L.curvefp_gemm_prepared.argtypes = [P, I, P, I, I64, I64, I64, P, I64, P, I64, P]
@@ -503,6 +505,42 @@ def curvefp_prepare(codes: torch.Tensor, scales: torch.Tensor, rows: int, k: int
                                prepared.numel() * prepared.element_size(), _stream(stream))
     _check(st, what)
     return prepared
+
+
+def curvefp_quantize_prepare(src: torch.Tensor, fmt, block: int = 32, codes: Optional[torch.Tensor] = None,
+                             scales: Optional[torch.Tensor] = None, prepared: Optional[torch.Tensor] = None,
+                             dst: Optional[torch.Tensor] = None, dequantize: bool = False, stream=None):
+    """curvefp_quantize (blocks along the rows of a [rows, k] fp32/bf16 source), curvefp_prepare of
+    the result (trans = 0) and, with dequantize=True or a dst given, curvefp_dequantize of it, in
+    one launch.  Returns (codes, scales, prepared), plus dst when it is written."""
+    what = "curvefp_quantize_prepare"
+    _on_gpu(what, [("src", src)], stream)
+    _source_arg(what, src)
+    rows, k = src.shape
+    f = _fmt(fmt)
+    if codes is None:
+        shape = (rows, k // 32, 28) if f == 2 else (rows, k)
+        codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
+    if scales is None:
+        scales = torch.empty((rows, k // block), dtype=torch.int8, device=src.device)
+    if prepared is None:
+        prepared = torch.empty(curvefp_prepared_bytes(rows, k, 0), dtype=torch.uint8, device=src.device)
+    if dst is None and dequantize:
+        dst = torch.empty((rows, k), dtype=torch.float32, device=src.device)
+    ts = [("src", src), ("codes", codes), ("scales", scales), ("prepared", prepared)]
+    _on_gpu(what, ts + ([("dst", dst)] if dst is not None else []), stream)
+    _codes_arg(what, "codes", codes, f, rows, k, block)
+    _scales_arg(what, "scales", scales, rows, k, block)
+    _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k, 0))
+    if dst is not None:
+        _matrix(what, "dst", dst, rows, k, (torch.float32,))
+    st = lib().curvefp_quantize_prepare(src.data_ptr(), DTYPES[src.dtype], rows, k, src.stride(0), f, block,
+                                        codes.data_ptr(), scales.data_ptr(), prepared.data_ptr(),
+                                        prepared.numel() * prepared.element_size(),
+                                        dst.data_ptr() if dst is not None else None,
+                                        dst.stride(0) if dst is not None else 0, _stream(stream))
+    _check(st, what)
+    return (codes, scales, prepared) if dst is None else (codes, scales, prepared, dst)
 
 
 def curvefp_gemm_prepared_workspace_bytes(M: int, N: int, K: int) -> int:

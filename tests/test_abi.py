@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 23
+    assert len(names) == 24
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -265,6 +265,48 @@ def test_prepared_validation(L):
     assert g(*split) == ENULL                       # a split K needs its workspace
     split[9], split[10] = PR, need - 1
     assert g(*split) == ESHAPE
+
+
+def test_quantize_prepare_validation(L):
+    q = L.curvefp_quantize_prepare
+    need = L.curvefp_prepared_bytes(64, 256, 0)
+    PR = 1 << 24                     # 256-byte aligned, never dereferenced
+    #       src   dt rows k    ld   fmt blk codes scales prep need  dst   ldd  stream
+    args = [FAKE, 1, 64, 256, 256, 0, 32, FAKE, FAKE, PR, need, FAKE, 256, None]
+    for i in (0, 7, 8, 9):
+        a = list(args); a[i] = None
+        assert q(*a) == ENULL, i
+    for i, v in ((1, 2), (5, 5), (5, -1)):
+        a = list(args); a[i] = v
+        assert q(*a) == EFMT, (i, v)
+    for v in (16, 48, 96, 1024, 0):              # 32 .. 512, powers of two
+        a = list(args); a[6] = v
+        assert q(*a) == EBLOCK, v
+    for i, v in ((2, 0), (3, 0), (3, 48), (4, 128), (10, need - 1), (12, 128)):
+        a = list(args); a[i] = v
+        assert q(*a) == ESHAPE, (i, v)
+    a = list(args); a[6] = 512                   # k % block
+    assert q(*a) == ESHAPE
+    # the row is held on chip: k <= 16384 (bf16), k <= 8192 (fp32)
+    big = list(args); big[3] = big[4] = big[12] = 16384 + 32
+    big[10] = L.curvefp_prepared_bytes(64, 16384 + 32, 0)
+    assert q(*big) == ESHAPE
+    ok = list(big); ok[3] = ok[4] = ok[12] = 16384; ok[10] = L.curvefp_prepared_bytes(64, 16384, 0); ok[0] = MIS
+    assert q(*ok) == EALIGN                      # at the bound the shape passes
+    f32 = list(ok); f32[1] = 0
+    assert q(*f32) == ESHAPE
+    f32[3] = f32[4] = f32[12] = 8192; f32[10] = L.curvefp_prepared_bytes(64, 8192, 0)
+    assert q(*f32) == EALIGN
+    a = list(args); a[2] = 1 << 31
+    assert q(*a) == ESHAPE
+    a = list(args); a[11] = None; a[12] = 0      # no reconstruction: ld_dst unused
+    a[0] = MIS
+    assert q(*a) == EALIGN
+    for i, v in ((0, MIS), (7, MIS), (9, PR + 16), (11, MIS), (4, 260), (12, 257)):
+        a = list(args); a[i] = v
+        if i == 4:
+            a[3] = 256                           # a bf16 row stride of 520 bytes
+        assert q(*a) == EALIGN, (i, v)
 
 
 def test_gemm_mixed_validation(L):

@@ -173,6 +173,28 @@ def test_prepared_checks(meta):
                                  stream=STREAM)
 
 
+def test_quantize_prepare_checks(meta):
+    M, K = 64, 256
+    src = meta((M, K), torch.bfloat16)
+    passes_checks(lambda: cf.curvefp_quantize_prepare(src, "E4C3", stream=STREAM))
+    passes_checks(lambda: cf.curvefp_quantize_prepare(src, "E3C3", block=64, dequantize=True, stream=STREAM))
+    with pytest.raises(ValueError, match="codes"):
+        cf.curvefp_quantize_prepare(src, "E4C3", codes=meta((M, K - 32), torch.uint8), stream=STREAM)
+    with pytest.raises(ValueError, match="scales"):
+        cf.curvefp_quantize_prepare(src, "E4C3", block=64, scales=meta((M, K // 32 - 1), torch.int8)[:, :3],
+                                    stream=STREAM)
+    with pytest.raises(ValueError, match="prepared"):
+        cf.curvefp_quantize_prepare(src, "E4C3", prepared=meta((1024,), torch.uint8), stream=STREAM)
+    with pytest.raises(ValueError, match="dst"):
+        cf.curvefp_quantize_prepare(src, "E4C3", dst=meta((M, K), torch.bfloat16), stream=STREAM)
+    with pytest.raises(ValueError, match="dst"):
+        cf.curvefp_quantize_prepare(src, "E4C3", dst=meta((M - 1, K), torch.float32), stream=STREAM)
+    with pytest.raises(ValueError, match="not on a GPU"):
+        cf.curvefp_quantize_prepare(src, "E4C3", dst=torch.zeros((M, K)), stream=STREAM)
+    with pytest.raises(ValueError, match="not on a GPU"):
+        cf.curvefp_quantize_prepare(torch.zeros((M, K)), "E4C3", stream=STREAM)
+
+
 def test_mixed_gemm_checks(meta):
     M, N, K = 64, 96, 256
     # A = dY codes [M][K] along K; B = reused forward codes of a [K][N] tensor, blocks along N
