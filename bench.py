@@ -81,6 +81,9 @@ def parse():
                    help="skip the E4C3 radix variants (r = 2, 2^(8/9), 2^(3/4)) on the inference operands")
     p.add_argument("--serial-step", action="store_true",
                    help="run the step's calls one after another on one stream")
+    p.add_argument("--separate-step", action="store_true",
+                   help="prepared path: quantize, dequantize and prepare as separate calls instead of "
+                        "curvefp_quantize_prepare (one launch per operand)")
     p.add_argument("--no-reference", action="store_true",
                    help="skip the vendor fp16 GEMM (torch.matmul) of the same M, N and 3K")
     p.add_argument("--no-configs", action="store_true",
@@ -617,7 +620,8 @@ def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 10):
 def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
     """Every configuration timed on its own: quantize of each operand (GB/s, algorithmic bytes)
     and the GEMM call (TFLOP/s, fraction of dense fp16 peak: curvefp_gemm_ws, expansion included,
-    or curvefp_gemm); with prepared operands also each operand's curvefp_prepare and the
+    or curvefp_gemm); with prepared operands also each operand's curvefp_prepare, its
+    curvefp_quantize_prepare (quantize and prepare in one launch, where the shape allows) and the
     curvefp_gemm_prepared call alone; medians of `reps` calls each."""
     import torch
     out = {}
@@ -664,6 +668,13 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
                 "prepare_a": {"us": t_pa * 1e6}, "prepare_b": {"us": t_pb * 1e6},
                 "gemm_prepared": {"us": t_gp * 1e6, "tflops": tfp, "frac": tfp / F16_DENSE_PEAK_TFLOPS},
             })
+            # one launch per operand where it applies (blocks along K)
+            if w.a.axis == 1 and w.b.axis == 1:
+                t_qpa = timed_median(lambda: cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa),
+                                     stream, reps)
+                t_qpb = timed_median(lambda: cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb),
+                                     stream, reps)
+                out[name].update({"quantize_prepare_a": {"us": t_qpa * 1e6}, "quantize_prepare_b": {"us": t_qpb * 1e6}})
             del pa, pb, gws
         del ta, tb, ca, sa, cb, sb, C, ws
         torch.cuda.empty_cache()
@@ -928,6 +939,8 @@ def main():
     D = torch.empty((outer_a, ka), dtype=torch.float32, device=dev)
     # workspaces and prepared buffers are allocated once, like C: the timed calls only use them
     prepared = args.gemm == "prepared"
+    # one launch per operand (curvefp_quantize_prepare): both operands with blocks along K
+    fused_step = prepared and not args.separate_step and not args.serial_step and w.a.axis == 1 and w.b.axis == 1
     ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if args.gemm == "ws" else None
     pa = pb = gws = None
     if prepared:
@@ -951,10 +964,13 @@ def main():
             cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
     # The step on two streams (both at the default priority).  Its HBM-bound parts run side by
-    # side: the activations are quantized, their codes reconstructed and (prepared path) expanded
-    # for the GEMM on the main stream while the weights are quantized and expanded on the side
-    # stream; the GEMM (MFMA-bound, every SIMD's registers taken by its waves) then runs alone on
-    # the main stream once both operands are there.
+    # side, then the GEMM (MFMA-bound, every SIMD's registers taken by its waves) runs alone on the
+    # main stream once both operands are there.  Default (prepared path): one
+    # curvefp_quantize_prepare per operand -- the weights quantized and expanded on the main
+    # stream, the activations quantized, expanded and reconstructed on the side stream (the
+    # faster of the two assignments).  Separate calls: the activations are quantized, their
+    # codes reconstructed and (prepared path) expanded on the main stream while the weights are
+    # quantized and expanded on the side stream.
     side = torch.cuda.Stream(device=dev)
 
     def rec(ev, key, s):
@@ -982,7 +998,23 @@ def main():
         gemm()
         rec(ev, "g1", stream)
 
+    def step_fused(ev=None):
+        side.wait_stream(stream)
+        rec(ev, "qpb0", stream)
+        cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb, stream=stream)
+        rec(ev, "qpb1", stream)
+        rec(ev, "qpa0", side)
+        cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa, dst=D, stream=side)
+        rec(ev, "qpa1", side)
+        stream.wait_stream(side)
+        rec(ev, "g0", stream)
+        gemm()
+        rec(ev, "g1", stream)
+
     def step(ev=None):
+        if fused_step:
+            step_fused(ev)
+            return
         if args.serial_step:
             step_serial(ev)
             return
@@ -1018,7 +1050,7 @@ def main():
     # stream bracket the GEMM of every step (the roofline's kernel).  Events around the other
     # calls would add their own latency to the step (each record is a barrier packet: ~0.9% of
     # the step with events around all six calls), so those are timed in the steps after it.
-    keys = ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
+    keys = ("qpa", "qpb", "g") if fused_step else ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
     evs = [{"g0": torch.cuda.Event(enable_timing=True), "g1": torch.cuda.Event(enable_timing=True)}
            for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -1033,9 +1065,12 @@ def main():
     for i in range(ndiag):
         step(diag[i])
     torch.cuda.synchronize()
-    names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
-    if prepared:
-        names.update({"prepare_a": "pa", "prepare_b": "pb"})
+    if fused_step:
+        names = {"quantize_prepare_a": "qpa", "quantize_prepare_b": "qpb", "gemm": "g"}
+    else:
+        names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
+        if prepared:
+            names.update({"prepare_a": "pa", "prepare_b": "pb"})
     per = {n: float(np.mean([diag[i][k + "0"].elapsed_time(diag[i][k + "1"]) for i in range(ndiag)]))
            for n, k in names.items()}
     per["gemm"] = float(np.mean([evs[i]["g0"].elapsed_time(evs[i]["g1"]) for i in range(args.steps)]))
@@ -1051,6 +1086,10 @@ def main():
         cf.curvefp_prepared_bytes(w.M, w.K)
     pb_bytes = w.N * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - (2.0 if w.dtype == "bf16" else 4.0)) + \
         cf.curvefp_prepared_bytes(w.N, w.K)
+    # one curvefp_quantize_prepare: source read, codes + scales, planes + row maxima (and, for the
+    # activations, the fp32 reconstruction) written
+    qpa_bytes = qa_bytes + cf.curvefp_prepared_bytes(w.M, w.K) + 4.0 * w.M * w.K
+    qpb_bytes = qb_bytes + cf.curvefp_prepared_bytes(w.N, w.K)
 
     result = {
         "metric": METRIC,
@@ -1070,7 +1109,10 @@ def main():
             "format": w.fmt,
             "source_dtype": w.dtype,
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
-            "step": ("[quantize(act) -> dequantize(act codes) -> prepare(act)] || [quantize(weight) -> "
+            "step": ("quantize_prepare(weight) || quantize_prepare(act, with its reconstruction) on two "
+                     "streams (one launch each: quantize, dequantize and prepare fused), then gemm_prepared"
+                     if fused_step else
+                     "[quantize(act) -> dequantize(act codes) -> prepare(act)] || [quantize(weight) -> "
                      "prepare(weight)] on two streams, then gemm_prepared" if prepared else
                      "[quantize(act) -> dequantize(act codes)] || quantize(weight) on two streams, then gemm"),
             "gemm_arith": "fp16 hi/lo operand split, 3 MFMA f32_32x32x16_f16 per k-slice, fp32 accumulate",
@@ -1093,7 +1135,12 @@ def main():
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
-        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_a, dequantize, "
+        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_prepare_b, "
+                            "gemm: main; quantize_prepare_a: side, alongside quantize_prepare_b); gemm: "
+                            "mean over the timed steps; the others: over 10 steps right after them with "
+                            "events around every call"
+                            if fused_step else
+                            "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
                             "prepare_a, gemm: main; quantize_b, prepare_b: side, alongside the main "
                             "stream's calls before the GEMM); gemm: mean over the timed steps; the "
                             "others: over 10 steps right after them with events around every call"
@@ -1106,13 +1153,18 @@ def main():
                            "kernel so that the GPU reaches the first event only after the host has "
                            "enqueued the call: GPU time, without the Python binding's host time",
         "gemm_tflops": gemm_tflops,
-        "quantize_gbps": {
-            "act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
-            "weight": qb_bytes / (per["quantize_b"] * 1e-3) / 1e9,
-        },
-        "dequantize_gbps": dq_bytes / (per["dequantize"] * 1e-3) / 1e9,
     }
-    if prepared:
+    if fused_step:
+        result["quantize_prepare_gbps"] = {
+            "act": qpa_bytes / (per["quantize_prepare_a"] * 1e-3) / 1e9,
+            "weight": qpb_bytes / (per["quantize_prepare_b"] * 1e-3) / 1e9,
+            "bytes": "source read; codes, scales, planes and row maxima written (act: and its fp32 "
+                     "reconstruction)"}
+    else:
+        result["quantize_gbps"] = {"act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
+                                   "weight": qb_bytes / (per["quantize_b"] * 1e-3) / 1e9}
+        result["dequantize_gbps"] = dq_bytes / (per["dequantize"] * 1e-3) / 1e9
+    if prepared and not fused_step:
         result["prepare_gbps"] = {"act": pa_bytes / (per["prepare_a"] * 1e-3) / 1e9,
                                   "weight": pb_bytes / (per["prepare_b"] * 1e-3) / 1e9,
                                   "bytes": "codes + scales read, planes + row maxima written"}
@@ -1129,6 +1181,11 @@ def main():
     }
     if prepared:
         cold_calls.update({"prepare_a": prepare_a, "prepare_b": prepare_b})
+    if fused_step:
+        cold_calls.update({
+            "quantize_prepare_a": lambda: cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa,
+                                                                      dst=D),
+            "quantize_prepare_b": lambda: cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb)})
     cold = {}
     for n, fn in cold_calls.items():
         cold[n] = timed_median(fn, stream, 10, warm=0, before=flush.zero_) * 1e6
@@ -1144,6 +1201,10 @@ def main():
     if prepared:
         result["cold_cache"]["prepare_gbps"] = {"act": pa_bytes / (cold["prepare_a"] * 1e-6) / 1e9,
                                                 "weight": pb_bytes / (cold["prepare_b"] * 1e-6) / 1e9}
+    if fused_step:
+        result["cold_cache"]["quantize_prepare_gbps"] = {
+            "act": qpa_bytes / (cold["quantize_prepare_a"] * 1e-6) / 1e9,
+            "weight": qpb_bytes / (cold["quantize_prepare_b"] * 1e-6) / 1e9}
 
     if args.copy_calibration:
         xc = torch.empty(COPY_BYTES, dtype=torch.uint8, device=dev)

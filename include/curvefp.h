@@ -334,12 +334,15 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
  *   codes    [rows][k] (E3C3 [rows][k/32][28]), scales [rows][k/block], 16-byte aligned codes.
  *   prepared at least curvefp_prepared_bytes(rows, k, 0) bytes (prepared_size), 256-byte aligned.
  *   dst      null, or [rows][ld_dst] fp32 with 16-byte aligned rows.
- * Each row is held in on-chip memory between reading and writing, which bounds k: k <= 16384
- * for bf16 and k <= 8192 for fp32 sources, and block is 32, 64, 128, 256 or 512 (longer rows
- * and other G: curvefp_quantize, curvefp_prepare and curvefp_dequantize).  Errors:
+ * Rows of up to 8192 bf16 or 4096 fp32 elements (bf16 rows of up to 16384 in tensors of at most
+ * 2^26 elements) take one launch: a wave or a workgroup reads its row once, holds it in LDS while
+ * it takes the block scales and the row's largest scale, then writes every output.  Other shapes
+ * run the quantize, expansion and reconstruction kernels in turn (the same outputs; measured
+ * faster there).  block is 32, 64, 128, 256 or 512 (other G: curvefp_quantize,
+ * curvefp_prepare and curvefp_dequantize); k <= CURVEFP_MAX_K.  Errors:
  * CURVEFP_ERR_NULL (src, codes, scales or prepared), _FORMAT (dtype or format), _BLOCK, _SHAPE
- * (non-positive sizes, k % block, k beyond the bound, ld_src < k, ld_dst < k, prepared_size
- * too small, rows >= 2^31), _ALIGN, _HIP.
+ * (non-positive sizes, k % block, k > CURVEFP_MAX_K, ld_src < k, ld_dst < k, prepared_size too
+ * small, rows >= 2^31), _ALIGN, _HIP.
  */
 int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld_src,
                              int format, int block, void* codes, int8_t* scales,

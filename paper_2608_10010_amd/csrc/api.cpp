@@ -226,8 +226,7 @@ int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k
     // a block's maximum is reduced over the 4 .. 64 lanes that hold it
     if (block != 32 && block != 64 && block != 128 && block != 256 && block != 512) return CURVEFP_ERR_BLOCK;
     if (rows <= 0 || rows >= ((int64_t)1 << 31) || k <= 0 || k % block || ld_src < k) return CURVEFP_ERR_SHAPE;
-    // one row per wave, held in LDS between the two passes
-    if (k > (dtype == 1 ? 16384 : 8192)) return CURVEFP_ERR_SHAPE;
+    if (k > CURVEFP_MAX_K) return CURVEFP_ERR_SHAPE;   // the prepared form's bound
     if (dst && ld_dst < k) return CURVEFP_ERR_SHAPE;
     if (prepared_size < prepared_bytes(rows, k, 0)) return CURVEFP_ERR_SHAPE;
     const int64_t esz = dtype == 1 ? 2 : 4;

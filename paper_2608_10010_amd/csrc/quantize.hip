@@ -1255,14 +1255,17 @@ hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols
 // Quantize and prepare in one launch: Q(X) of Sec. 3.1 with blocks along the rows, then the
 // result's staging as a GEMM operand (Sec. 3.3) -- the planes and row maxima that curvefp_prepare
 // writes from these codes (planes.hpp) -- and, when dst is given, the reconstruction of
-// Eq. curvefp-value that curvefp_dequantize writes.  One wave per row, in two passes over the
-// row's chunks (8 elements; chunk g = 64 UL s + 64 u + lane in segment s, UL chunks per lane in
-// flight): the first reads the source from HBM once, takes every block's scale and the row's
-// largest scale key alpha and keeps the chunks in LDS (up to 64 U per wave); the second takes
-// them back from LDS and writes.  Slots past the row's end hold zeros (scale -127, the bottom key,
-// so alpha is unchanged) and store nothing.  Waves of the padding rows (up to the next multiple
-// of 256) write zero planes and a zero row maximum, as the expansion does past the operand.
-template <class F, bool BF16, int U>
+// Eq. curvefp-value that curvefp_dequantize writes.  WPR waves take one row (four rows per
+// workgroup, or one), in two passes over its chunks (8 elements; in segment s, chunk
+// g = 64 WPR (UL s + u) + 64 w + lane for wave w of the row, UL chunks per lane in flight): the
+// first reads the source once, takes every block's scale and the row's largest scale key alpha
+// (over the row's waves through LDS when WPR > 1) and keeps the chunks in LDS (64 WPR U per row,
+// 32 KB per workgroup at most, so that several workgroups share a compute unit); the second
+// takes them back and writes.  Slots past the row's end hold zeros (scale -127, the bottom key,
+// so alpha is unchanged) and store nothing.  Workgroups of the padding rows (up to the next
+// multiple of 256) write zero planes and a zero row maximum, as the expansion does past the
+// operand.
+template <class F, bool BF16, int U, int WPR>
 __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     const void* __restrict__ src, int64_t rows, int64_t ld, uint32_t cpr, int64_t code_row_bytes,
     uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int64_t nsb, char* __restrict__ planes,
@@ -1271,22 +1274,28 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     constexpr int ESZ = BF16 ? 2 : 4;
     constexpr int NV = BF16 ? 1 : 2;   // 16-byte loads per chunk
     constexpr int UL = U < 4 ? U : 4;
+    constexpr uint32_t SPAN = 64u * WPR;   // chunks of a row per u step
+    static_assert(WPR == 1 || WPR == 4, "one wave per row or one workgroup per row");
     static_assert(GEMM_DEC_ENTRIES == 256, "one expansion entry per thread");
+    static_assert(4 * 64 * U * NV * 16 <= 32768, "LDS staging of at most 32 KB per workgroup");
     __shared__ __attribute__((aligned(16))) uint4 rowbuf[4 * 64 * U * NV];
     __shared__ __attribute__((aligned(16))) T lut[F::QLUT_SIZE];
     __shared__ uint32_t dec[GEMM_DEC_ENTRIES];
     __shared__ uint32_t qmant[128];
     __shared__ uint64_t qsig[128];
-    const int lane = (int)(threadIdx.x & 63);
-    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    const bool real = row < rows;
-    uint4* wbuf = rowbuf + (threadIdx.x >> 6) * (64 * U * NV);
+    __shared__ int wkey[4];
+    const int lane = (int)(threadIdx.x & 63), wave = (int)(threadIdx.x >> 6);
+    const int wr = wave % WPR;                               // this wave's part of its row
+    const int64_t row = ((int64_t)blockIdx.x * 4 + wave) / WPR;
+    const bool real = row < rows;                            // uniform over the waves of a row
+    uint4* wbuf = rowbuf + (wave / WPR) * (SPAN * U * NV);
     const uint4* srow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) + (real ? row : 0) * ld * ESZ);
-    const uint32_t nseg = (cpr + 64 * UL - 1) / (64 * UL);
+    const uint32_t nseg = (cpr + SPAN * UL - 1) / (SPAN * UL);
+    auto chunk_of = [&](uint32_t seg, int u) { return SPAN * (UL * seg + (uint32_t)u) + 64u * wr + (uint32_t)lane; };
     auto load = [&](uint32_t seg, uint4 (*v)[NV]) {
 #pragma unroll
         for (int u = 0; u < UL; u++) {
-            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+            const uint32_t g = chunk_of(seg, u);
 #pragma unroll
             for (int t = 0; t < NV; t++) v[u][t] = make_uint4(0u, 0u, 0u, 0u);
             if (real && g < cpr) {
@@ -1315,14 +1324,14 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
 
     const int64_t rt = row / BM;
     const int rr = (int)(row - rt * BM);
-    if (!real) {
+    if (!real) {   // the whole row's waves (and, for WPR = 4, the workgroup) leave here
         if (row < RT * BM) {
-            for (uint32_t g = (uint32_t)lane; g < cpr; g += 64) {
+            for (uint32_t g = 64u * wr + (uint32_t)lane; g < cpr; g += SPAN) {
                 char* pd = planes + ((int64_t)(g >> 2) * RT + rt) * (2 * PLANE) + swz(rr, (int)(g & 3));
                 *reinterpret_cast<uint4*>(pd) = make_uint4(0u, 0u, 0u, 0u);
                 *reinterpret_cast<uint4*>(pd + PLANE) = make_uint4(0u, 0u, 0u, 0u);
             }
-            if (lane == 0) rmax[row] = 0;
+            if (wr == 0 && lane == 0) rmax[row] = 0;
         }
         return;
     }
@@ -1346,7 +1355,7 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
 #pragma unroll
         for (int u = 0; u < UL; u++) {
             key = max(key, scale_key(chunk_scale(cur[u])));
-            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+            const uint32_t g = chunk_of(seg, u);
 #pragma unroll
             for (int t = 0; t < NV; t++) wbuf[NV * g + t] = cur[u][t];
         }
@@ -1357,6 +1366,11 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     }
 #pragma unroll
     for (int o = 32; o > 0; o >>= 1) key = max(key, __shfl_xor(key, o));
+    if (WPR > 1) {
+        if (lane == 0) wkey[wave] = key;
+        __syncthreads();
+        key = max(max(wkey[0], wkey[1]), max(wkey[2], wkey[3]));
+    }
     const int alpha = key;
 
     // pass 2: codes and scales, both planes, the reconstruction
@@ -1365,7 +1379,7 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     for (uint32_t seg = 0; seg < nseg; seg++) {
 #pragma unroll
         for (int u = 0; u < UL; u++) {
-            const uint32_t g = seg * (64u * UL) + 64u * u + (uint32_t)lane;
+            const uint32_t g = chunk_of(seg, u);
             uint4 v[NV];
 #pragma unroll
             for (int t = 0; t < NV; t++) v[t] = wbuf[NV * g + t];
@@ -1395,10 +1409,10 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
             }
         }
     }
-    if (lane == 0) rmax[row] = alpha;
+    if (wr == 0 && lane == 0) rmax[row] = alpha;
 }
 
-template <class F, bool BF16, int U>
+template <class F, bool BF16, int U, int WPR>
 hipError_t launch_qp_u(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
                        int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
     const int64_t RT = (rows + BM - 1) / BM;
@@ -1406,23 +1420,30 @@ hipError_t launch_qp_u(const void* src, int64_t rows, int64_t k, int64_t ld, int
     while ((8 << lgl) < block) lgl++;
     const int64_t code_row_bytes = F::PACKED7 ? k / 32 * 28 : k;
     char* rmax = planes + (k / 32) * RT * 2 * PLANE;   // the prepared layout: planes, then row maxima
-    hipLaunchKernelGGL((quantize_prepare_kernel<F, BF16, U>), dim3((unsigned)(RT * 64)), dim3(256), 0, s, src, rows,
-                       ld, (uint32_t)(k / 8), code_row_bytes, codes, scales, k / block, planes,
+    hipLaunchKernelGGL((quantize_prepare_kernel<F, BF16, U, WPR>), dim3((unsigned)(RT * 64 * WPR)), dim3(256), 0, s,
+                       src, rows, ld, (uint32_t)(k / 8), code_row_bytes, codes, scales, k / block, planes,
                        reinterpret_cast<int*>(rmax), RT, dst, ld_dst, fidx, lgl);
     return hipGetLastError();
 }
 
-// chunks per lane: the fewest of 2, 4, ..., 32 that hold a row of k / 8 chunks in one wave
+// Rows of up to 512 chunks (bf16; 256 fp32: 2, 4 or 8 chunks per lane) take one wave each,
+// rows of up to 2048 bf16 (512 fp32) chunks one workgroup each, staged in at most 32 KB of LDS
+// per workgroup; qp_fused_rows decides which rows go here at all.
 template <class F, bool BF16>
 hipError_t launch_qp(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
                      int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
     const int64_t cpr = k / 8;
-    if (cpr <= 128) return launch_qp_u<F, BF16, 2>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-    if (cpr <= 256) return launch_qp_u<F, BF16, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-    if (cpr <= 512) return launch_qp_u<F, BF16, 8>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-    if (cpr <= 1024 || !BF16)
-        return launch_qp_u<F, BF16, 16>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-    return launch_qp_u<F, BF16, (BF16 ? 32 : 16)>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 128) return launch_qp_u<F, BF16, 2, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 256) return launch_qp_u<F, BF16, 4, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if constexpr (BF16) {
+        if (cpr <= 512)
+            return launch_qp_u<F, BF16, 8, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+        if (cpr <= 1024)
+            return launch_qp_u<F, BF16, 4, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+        return launch_qp_u<F, BF16, 8, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    } else {
+        return launch_qp_u<F, BF16, 2, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    }
 }
 
 template <class F>
@@ -1432,6 +1453,19 @@ hipError_t launch_qp_fmt(const void* src, int dtype, int64_t rows, int64_t k, in
     char* pp = reinterpret_cast<char*>(prepared);
     return dtype == 1 ? launch_qp<F, true>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s)
                       : launch_qp<F, false>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s);
+}
+
+// Which shapes take the fused kernel: rows of up to 1024 chunks (bf16; 512 fp32), and bf16 rows of
+// up to 2048 chunks in tensors of at most 2^26 elements; the others run the quantize, expansion and
+// reconstruction kernels in turn.  Measured on bf16 sources against those kernels in one call:
+// 8192 x 8192 (a workgroup per row, 4 chunks per lane) 101 against 123 us; 4096 x 11008 and
+// 4096 x 14336 (8 chunks per lane) 74.5 and 85.6 against 81.6 and 95.5 us, but 8192 x 14336
+// 226 against 201 us.  (Rows staged in 96-128 KB of LDS per workgroup, or read twice from the L2
+// by one wave, were 15-40% slower on those shapes.)
+bool qp_fused_rows(int dtype, int64_t rows, int64_t k) {
+    const int64_t cpr = k / 8;
+    if (dtype != 1) return cpr <= 512;
+    return cpr <= 1024 || (cpr <= 2048 && rows * k <= ((int64_t)1 << 26));
 }
 }  // namespace
 
@@ -1453,6 +1487,13 @@ namespace curvefp {
 hipError_t launch_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format,
                                   int block, void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst,
                                   hipStream_t s) {
+    if (!qp_fused_rows(dtype, rows, k)) {
+        // longer rows: the three kernels in turn, on the same outputs
+        hipError_t e = launch_quantize(src, dtype, rows, k, ld, 1, format, block, codes, scales, s);
+        if (e == hipSuccess) e = launch_prepare(codes, scales, rows, k, format, block, 0, prepared, s);
+        if (e == hipSuccess && dst != nullptr) e = launch_dequantize(codes, scales, format, rows, k, block, dst, ld_dst, s);
+        return e;
+    }
     switch (format) {
         case 0: return launch_qp_fmt<FmtE4C3>(src, dtype, rows, k, ld, 0, block, codes, scales, prepared, dst, ld_dst, s);
         case 1: return launch_qp_fmt<FmtE5C2>(src, dtype, rows, k, ld, 1, block, codes, scales, prepared, dst, ld_dst, s);

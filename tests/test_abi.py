@@ -287,15 +287,13 @@ def test_quantize_prepare_validation(L):
         assert q(*a) == ESHAPE, (i, v)
     a = list(args); a[6] = 512                   # k % block
     assert q(*a) == ESHAPE
-    # the row is held on chip: k <= 16384 (bf16), k <= 8192 (fp32)
-    big = list(args); big[3] = big[4] = big[12] = 16384 + 32
-    big[10] = L.curvefp_prepared_bytes(64, 16384 + 32, 0)
+    # k up to CURVEFP_MAX_K, the prepared form's bound
+    KMAX = header_define("CURVEFP_MAX_K")
+    big = list(args); big[3] = big[4] = big[12] = KMAX + 32; big[10] = 1 << 62
     assert q(*big) == ESHAPE
-    ok = list(big); ok[3] = ok[4] = ok[12] = 16384; ok[10] = L.curvefp_prepared_bytes(64, 16384, 0); ok[0] = MIS
+    ok = list(big); ok[3] = ok[4] = ok[12] = KMAX; ok[0] = MIS
     assert q(*ok) == EALIGN                      # at the bound the shape passes
     f32 = list(ok); f32[1] = 0
-    assert q(*f32) == ESHAPE
-    f32[3] = f32[4] = f32[12] = 8192; f32[10] = L.curvefp_prepared_bytes(64, 8192, 0)
     assert q(*f32) == EALIGN
     a = list(args); a[2] = 1 << 31
     assert q(*a) == ESHAPE

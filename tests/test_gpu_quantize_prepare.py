@@ -3,7 +3,8 @@ scales bit-exact against the oracle's quantizer and the reconstruction against t
 dequantizer; codes, scales, prepared bytes and reconstruction identical to curvefp_quantize,
 curvefp_prepare and curvefp_dequantize on the same source; products of fused-prepared operands
 identical to curvefp_gemm_ws and within the GEMM bound of the exact phase-binned oracle.  Shapes span
-every row length class (2 .. 32 chunks per lane), padding rows up to the next tile of 256, blocks of
+every row length class (a wave or a workgroup per row, with 2, 4 or 8 chunks per lane staged in LDS;
+longer rows through the separate kernels), padding rows up to the next tile of 256, blocks of
 32 .. 512, row strides, the edge tensors and non-finite blocks."""
 
 import numpy as np
@@ -79,10 +80,12 @@ def test_random(fmt, dtype, rows, k, block):
 
 
 @pytest.mark.parametrize("fmt", ["E4C3", "E3C3", "E5C2"])
-@pytest.mark.parametrize("dtype,k", [("bf16", 16384), ("bf16", 14336), ("bf16", 8224), ("f32", 8192), ("f32", 4128)])
+@pytest.mark.parametrize("dtype,k", [("bf16", 32768), ("bf16", 16384), ("bf16", 14336), ("bf16", 8224), ("bf16", 8192),
+                                     ("bf16", 4160), ("f32", 8192), ("f32", 4128), ("f32", 4096), ("f32", 2080)])
 def test_long_rows(fmt, dtype, k):
-    """Rows of 16 and 32 chunks per lane, full and partly filled."""
-    rows = 40
+    """Rows staged per workgroup (whole and partial segments), and rows too long for that (the three
+    kernels in turn)."""
+    rows = 40 if k <= 16384 else 8
     rng = np.random.default_rng(k)
     x = (rng.standard_normal((rows, k)) * np.exp2(rng.uniform(-8, 8, (rows, k // 32)).repeat(32, axis=1))).astype(
         np.float32)
