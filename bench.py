@@ -103,10 +103,10 @@ def parse():
 
 
 COPY_BYTES = 256 << 20
-KERNEL_SOURCES = ("gemm.hip", "curvefp_internal.hpp", "device_util.hpp")
+KERNEL_SOURCES = ("gemm.hip", "curvefp_internal.hpp", "device_util.hpp", "planes.hpp", "codec.hpp")
 
 
-QUANTIZE_SOURCES = ("quantize.hip", "curvefp_internal.hpp", "device_util.hpp")
+QUANTIZE_SOURCES = ("quantize.hip", "curvefp_internal.hpp", "device_util.hpp", "planes.hpp", "codec.hpp")
 STREAM_TRAFFIC = os.path.join(ROOT, "profiles", "quantize_stream_e4c3_1gib_traffic.md")
 
 
@@ -298,7 +298,143 @@ def summarize_stream_pmc(args):
     print("\n".join(lines))
 
 
+def pmc_by_grid(d: str, counter: str, kinds):
+    """Mean per dispatch of `counter` (summed over its instances) for each (kernel, grid size) of the
+    given kernels, for the vendor GEMM and for the largest copy (the calibration copy)."""
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    per, seen, copy_grid, rows = {}, set(), 0, []
+    for f in files:
+        for r in csv.DictReader(open(f)):
+            if r["Counter_Name"] != counter:
+                continue
+            name = r["Kernel_Name"]
+            kind = next((k for k in kinds if k + "<" in name or k + "(" in name), None)
+            if kind is None and "copyBuffer" in name:
+                kind = "copy"
+                copy_grid = max(copy_grid, int(r["Grid_Size"]))
+            if kind is None and name.startswith("Cijk_"):
+                kind = "vendor"
+            if kind is not None:
+                rows.append((kind, r))
+    for kind, r in rows:
+        if kind == "copy" and int(r["Grid_Size"]) != copy_grid:
+            continue
+        inst = ((kind, r["Dispatch_Id"]), r.get("Counter_Value"), r.get("Start_Timestamp"))
+        if inst in seen:
+            continue
+        seen.add(inst)
+        key = (kind, int(r["Grid_Size"]), r["Dispatch_Id"])
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (kind, grid, _), v in per.items():
+        s, n = out.get((kind, grid), (0.0, 0))
+        out[(kind, grid)] = (s + v, n + 1)
+    return {k: (s / n, n) for k, (s, n) in out.items()}
+
+
+def summarize_pmc_prepared(args):
+    """The prepared step's kernels: one curvefp_quantize_prepare per operand (quantize, expansion and,
+    for the activations, reconstruction in one launch) and the GEMM kernel on the prepared operands."""
+    from paper_2608_10010_amd import curvefp as cf
+    from paper_2608_10010_amd import workloads as W
+    w = W.get(args.workload)
+    kinds = ("quantize_prepare_kernel", "gemm_ws_kernel")
+    fetch = pmc_by_grid(args.summarize_pmc[0], "FETCH_SIZE", kinds)
+    write = pmc_by_grid(args.summarize_pmc[1], "WRITE_SIZE", kinds)
+    cf_ = [v for (k, _), v in fetch.items() if k == "copy"][0]
+    cw_ = [v for (k, _), v in write.items() if k == "copy"][0]
+    f_fetch, f_write = cf_[0] * 1024.0 / COPY_BYTES, cw_[0] * 1024.0 / COPY_BYTES
+    rt = lambda rows: (rows + 255) // 256
+    # the quantize_prepare grids of the two operands (a workgroup per 4 rows, or per row for rows
+    # longer than 4096 bf16 elements): told apart by their tiles of 256 rows
+    qp_grids = {}
+    for (k, grid) in fetch:
+        if k == "quantize_prepare_kernel":
+            tiles = grid // (64 * 256)
+            for nm, rows in (("act", w.M), ("weight", w.N)):
+                if tiles in (rt(rows), 4 * rt(rows)):
+                    qp_grids[nm] = grid
+    bpe = quantize_bytes_per_elem(w.fmt, w.dtype)
+    alg = {"act": w.M * w.K * (bpe + 4.0) + cf.curvefp_prepared_bytes(w.M, w.K),
+           "weight": w.N * w.K * bpe + cf.curvefp_prepared_bytes(w.N, w.K)}
+    lines = [
+        f"# Memory traffic of the prepared step's kernels, {args.workload} workload",
+        "",
+        "Commands (from the repository root on one MI355X; each pass is its own run):",
+        "",
+        "```",
+        *pmc_commands(args.gemm, args.workload),
+        f"python bench.py --summarize-pmc {pmc_dir('fetch', args.gemm, args.workload)} "
+        f"{pmc_dir('write', args.gemm, args.workload)} --gemm prepared"
+        + ("" if args.workload == HEADLINE else f" --workload {args.workload}"),
+        "```",
+        "",
+        "Per dispatch, each counter summed over its instances; MB = the counter scaled by what it reads for "
+        f"the {COPY_BYTES >> 20} MiB device copy of the same run ({f_fetch:.4f}x FETCH_SIZE, {f_write:.4f}x "
+        "WRITE_SIZE of the bytes the copy moves).  FETCH_SIZE / WRITE_SIZE count the L2s' requests to the "
+        "fabric, served by the 256 MB MALL or by HBM.",
+        "",
+        "| kernel | grid (work-items) | dispatches | FETCH_SIZE KiB | WRITE_SIZE KiB | MB read | MB written | "
+        "algorithmic MB |",
+        "|---|---|---|---|---|---|---|---|",
+    ]
+    step = 0.0
+    for nm in ("weight", "act"):
+        g = qp_grids.get(nm)
+        if g is None:
+            continue
+        fb, wb = fetch[("quantize_prepare_kernel", g)][0] * 1024 / f_fetch, write[("quantize_prepare_kernel", g)][0] * 1024 / f_write
+        step += fb + wb
+        what = "quantize_prepare (" + nm + (", with its fp32 reconstruction)" if nm == "act" else ")")
+        lines.append(f"| `{what}` | {g} | {fetch[('quantize_prepare_kernel', g)][1]} | "
+                     f"{fetch[('quantize_prepare_kernel', g)][0]:.1f} | {write[('quantize_prepare_kernel', g)][0]:.1f} | "
+                     f"{fb / 1e6:.1f} | {wb / 1e6:.1f} | {alg[nm] / 1e6:.1f} |")
+    gk = [k for k in fetch if k[0] == "gemm_ws_kernel"]
+    gk = max(gk, key=lambda k: fetch[k][1])          # the headline GEMM's grid: the most dispatches
+    gf, gw = fetch[gk][0] * 1024 / f_fetch, write[gk][0] * 1024 / f_write
+    step += gf + gw
+    planes = cf.curvefp_prepared_bytes(w.M, w.K) + cf.curvefp_prepared_bytes(w.N, w.K)
+    lines.append(f"| `gemm_ws_kernel` (curvefp_gemm_prepared) | {gk[1]} | {fetch[gk][1]} | {fetch[gk][0]:.1f} | "
+                 f"{write[gk][0]:.1f} | {gf / 1e6:.1f} | {gw / 1e6:.1f} | {(planes + 4.0 * w.M * w.N) / 1e6:.1f} |")
+    lines += [
+        "",
+        "Algorithmic bytes: quantize_prepare reads the source and writes codes, scales, the prepared planes "
+        "and row maxima (4 bytes per element of the rows padded to 256) and, for the activations, the fp32 "
+        "reconstruction; the GEMM's column is its prepared operands read once and C written once.  The GEMM "
+        "kernel reads its planes repeatedly (each 256-row panel once per output tile that needs it; the L2s "
+        "serve most re-reads): its traffic is what the roofline carries.",
+        "",
+    ]
+    vend = fetch.get(next((k for k in fetch if k[0] == "vendor"), None))
+    vendw = write.get(next((k for k in write if k[0] == "vendor"), None))
+    if vend and vendw:
+        vf, vw = vend[0] * 1024.0 / f_fetch, vendw[0] * 1024.0 / f_write
+        valg = 2.0 * (w.M * 3 * w.K + 3 * w.K * w.N + w.M * w.N)
+        lines += [
+            f"For comparison, the vendor fp16 GEMM of the same matrix-core work in the same runs (torch.matmul "
+            f"{w.M} x {w.N} x {3 * w.K}, `Cijk_...`, {vend[1]} dispatches): {vf / 1e6:.2f} MB read + "
+            f"{vw / 1e6:.2f} MB written per call, {(vf + vw) / valg:.2f}x its own algorithmic bytes (fp16 A, B and "
+            f"C, {valg / 1e6:.1f} MB).",
+            "",
+        ]
+    lines += [
+        f"traffic_bytes_per_launch={gf + gw:.0f}",
+        f"fetch_bytes_per_launch={gf:.0f}",
+        f"write_bytes_per_launch={gw:.0f}",
+        f"call_traffic_bytes={step:.0f}",
+        f"kernel_source_sha256={kernel_source_digest()}",
+    ]
+    print("\n".join(lines))
+
+
 def summarize_pmc(args):
+    if args.gemm == "prepared":
+        summarize_pmc_prepared(args)
+        return
     fetch = pmc_per_dispatch(args.summarize_pmc[0], "FETCH_SIZE", args.gemm)
     write = pmc_per_dispatch(args.summarize_pmc[1], "WRITE_SIZE", args.gemm)
     # KiB the counter reads per byte a plain copy moves (read and written once each)
