@@ -349,18 +349,19 @@ def summarize_pmc_prepared(args):
     cw_ = [v for (k, _), v in write.items() if k == "copy"][0]
     f_fetch, f_write = cf_[0] * 1024.0 / COPY_BYTES, cw_[0] * 1024.0 / COPY_BYTES
     rt = lambda rows: (rows + 255) // 256
-    # the quantize_prepare grids of the two operands (a workgroup per 4 rows, or per row for rows
-    # longer than 4096 bf16 elements): told apart by their tiles of 256 rows
+    # the quantize_prepare grids (a workgroup per 4 rows, or per row for rows longer than 4096 bf16
+    # elements): one operand alone, or both in one launch (the step), told apart by their tiles
     qp_grids = {}
     for (k, grid) in fetch:
         if k == "quantize_prepare_kernel":
             tiles = grid // (64 * 256)
-            for nm, rows in (("act", w.M), ("weight", w.N)):
-                if tiles in (rt(rows), 4 * rt(rows)):
+            for nm, t in (("act", rt(w.M)), ("weight", rt(w.N)), ("pair", rt(w.M) + rt(w.N))):
+                if tiles in (t, 4 * t):
                     qp_grids[nm] = grid
     bpe = quantize_bytes_per_elem(w.fmt, w.dtype)
     alg = {"act": w.M * w.K * (bpe + 4.0) + cf.curvefp_prepared_bytes(w.M, w.K),
            "weight": w.N * w.K * bpe + cf.curvefp_prepared_bytes(w.N, w.K)}
+    alg["pair"] = alg["act"] + alg["weight"]
     lines = [
         f"# Memory traffic of the prepared step's kernels, {args.workload} workload",
         "",
@@ -383,13 +384,16 @@ def summarize_pmc_prepared(args):
         "|---|---|---|---|---|---|---|---|",
     ]
     step = 0.0
-    for nm in ("weight", "act"):
+    for nm in ("pair", "weight", "act"):
         g = qp_grids.get(nm)
         if g is None:
             continue
         fb, wb = fetch[("quantize_prepare_kernel", g)][0] * 1024 / f_fetch, write[("quantize_prepare_kernel", g)][0] * 1024 / f_write
-        step += fb + wb
-        what = "quantize_prepare (" + nm + (", with its fp32 reconstruction)" if nm == "act" else ")")
+        if nm == "pair" or "pair" not in qp_grids:
+            step += fb + wb                   # the step's launch(es)
+        what = {"pair": "quantize_prepare_pair (both operands, the activations with their reconstruction: the step)",
+                "act": "quantize_prepare (act, with its fp32 reconstruction)",
+                "weight": "quantize_prepare (weight)"}[nm]
         lines.append(f"| `{what}` | {g} | {fetch[('quantize_prepare_kernel', g)][1]} | "
                      f"{fetch[('quantize_prepare_kernel', g)][0]:.1f} | {write[('quantize_prepare_kernel', g)][0]:.1f} | "
                      f"{fb / 1e6:.1f} | {wb / 1e6:.1f} | {alg[nm] / 1e6:.1f} |")
@@ -1099,14 +1103,12 @@ def main():
         else:
             cf.curvefp_gemm(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C)
 
-    # The step on two streams (both at the default priority).  Its HBM-bound parts run side by
-    # side, then the GEMM (MFMA-bound, every SIMD's registers taken by its waves) runs alone on the
-    # main stream once both operands are there.  Default (prepared path): one
-    # curvefp_quantize_prepare per operand -- the weights quantized and expanded on the main
-    # stream, the activations quantized, expanded and reconstructed on the side stream (the
-    # faster of the two assignments).  Separate calls: the activations are quantized, their
-    # codes reconstructed and (prepared path) expanded on the main stream while the weights are
-    # quantized and expanded on the side stream.
+    # Default (prepared path): one curvefp_quantize_prepare_pair launch quantizes and expands both
+    # operands (the activations also reconstructed), then the GEMM (MFMA-bound, every SIMD's
+    # registers taken by its waves) runs alone; one stream.  Separate calls: on two streams (both
+    # at the default priority) the activations are quantized, their codes reconstructed and
+    # (prepared path) expanded on the main stream while the weights are quantized and expanded on
+    # the side stream; the GEMM then runs on the main stream once both operands are there.
     side = torch.cuda.Stream(device=dev)
 
     def rec(ev, key, s):
@@ -1135,14 +1137,9 @@ def main():
         rec(ev, "g1", stream)
 
     def step_fused(ev=None):
-        side.wait_stream(stream)
-        rec(ev, "qpb0", stream)
-        cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb, stream=stream)
-        rec(ev, "qpb1", stream)
-        rec(ev, "qpa0", side)
-        cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa, dst=D, stream=side)
-        rec(ev, "qpa1", side)
-        stream.wait_stream(side)
+        rec(ev, "qp0", stream)
+        cf.curvefp_quantize_prepare_pair(ta, tb, w.fmt, out_a=(ca, sa, pa, D), out_b=(cb, sb, pb), stream=stream)
+        rec(ev, "qp1", stream)
         rec(ev, "g0", stream)
         gemm()
         rec(ev, "g1", stream)
@@ -1186,7 +1183,7 @@ def main():
     # stream bracket the GEMM of every step (the roofline's kernel).  Events around the other
     # calls would add their own latency to the step (each record is a barrier packet: ~0.9% of
     # the step with events around all six calls), so those are timed in the steps after it.
-    keys = ("qpa", "qpb", "g") if fused_step else ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
+    keys = ("qp", "g") if fused_step else ("qa", "qb", "g", "d") + (("pa", "pb") if prepared else ())
     evs = [{"g0": torch.cuda.Event(enable_timing=True), "g1": torch.cuda.Event(enable_timing=True)}
            for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -1202,7 +1199,7 @@ def main():
         step(diag[i])
     torch.cuda.synchronize()
     if fused_step:
-        names = {"quantize_prepare_a": "qpa", "quantize_prepare_b": "qpb", "gemm": "g"}
+        names = {"quantize_prepare_pair": "qp", "gemm": "g"}
     else:
         names = {"quantize_a": "qa", "quantize_b": "qb", "gemm": "g", "dequantize": "d"}
         if prepared:
@@ -1222,8 +1219,8 @@ def main():
         cf.curvefp_prepared_bytes(w.M, w.K)
     pb_bytes = w.N * w.K * (quantize_bytes_per_elem(w.fmt, w.dtype) - (2.0 if w.dtype == "bf16" else 4.0)) + \
         cf.curvefp_prepared_bytes(w.N, w.K)
-    # one curvefp_quantize_prepare: source read, codes + scales, planes + row maxima (and, for the
-    # activations, the fp32 reconstruction) written
+    # quantize-prepare: source read, codes + scales, planes + row maxima (and, for the activations,
+    # the fp32 reconstruction) written
     qpa_bytes = qa_bytes + cf.curvefp_prepared_bytes(w.M, w.K) + 4.0 * w.M * w.K
     qpb_bytes = qb_bytes + cf.curvefp_prepared_bytes(w.N, w.K)
 
@@ -1245,8 +1242,8 @@ def main():
             "format": w.fmt,
             "source_dtype": w.dtype,
             "M": w.M, "N": w.N, "K": w.K, "block": 32,
-            "step": ("quantize_prepare(weight) || quantize_prepare(act, with its reconstruction) on two "
-                     "streams (one launch each: quantize, dequantize and prepare fused), then gemm_prepared"
+            "step": ("quantize_prepare_pair(act with its reconstruction, weight) -- quantize, dequantize and "
+                     "prepare of both operands in one launch -- then gemm_prepared, one stream"
                      if fused_step else
                      "[quantize(act) -> dequantize(act codes) -> prepare(act)] || [quantize(weight) -> "
                      "prepare(weight)] on two streams, then gemm_prepared" if prepared else
@@ -1271,10 +1268,8 @@ def main():
             "mfma_pipe_frac": 3.0 * gemm_tflops / F16_DENSE_PEAK_TFLOPS,
         },
         "kernels_us": {n: per[n] * 1e3 for n in names},
-        "kernels_us_note": ("each call between HIP events on the stream it runs on (quantize_prepare_b, "
-                            "gemm: main; quantize_prepare_a: side, alongside quantize_prepare_b); gemm: "
-                            "mean over the timed steps; the others: over 10 steps right after them with "
-                            "events around every call"
+        "kernels_us_note": ("each call between HIP events on the stream; gemm: mean over the timed steps; "
+                            "quantize_prepare_pair: over 10 steps right after them with events around both calls"
                             if fused_step else
                             "each call between HIP events on the stream it runs on (quantize_a, dequantize, "
                             "prepare_a, gemm: main; quantize_b, prepare_b: side, alongside the main "
@@ -1292,10 +1287,9 @@ def main():
     }
     if fused_step:
         result["quantize_prepare_gbps"] = {
-            "act": qpa_bytes / (per["quantize_prepare_a"] * 1e-3) / 1e9,
-            "weight": qpb_bytes / (per["quantize_prepare_b"] * 1e-3) / 1e9,
-            "bytes": "source read; codes, scales, planes and row maxima written (act: and its fp32 "
-                     "reconstruction)"}
+            "pair": (qpa_bytes + qpb_bytes) / (per["quantize_prepare_pair"] * 1e-3) / 1e9,
+            "bytes": "both sources read; codes, scales, planes and row maxima written, and the activations' "
+                     "fp32 reconstruction"}
     else:
         result["quantize_gbps"] = {"act": qa_bytes / (per["quantize_a"] * 1e-3) / 1e9,
                                    "weight": qb_bytes / (per["quantize_b"] * 1e-3) / 1e9}
@@ -1319,6 +1313,8 @@ def main():
         cold_calls.update({"prepare_a": prepare_a, "prepare_b": prepare_b})
     if fused_step:
         cold_calls.update({
+            "quantize_prepare_pair": lambda: cf.curvefp_quantize_prepare_pair(
+                ta, tb, w.fmt, out_a=(ca, sa, pa, D), out_b=(cb, sb, pb)),
             "quantize_prepare_a": lambda: cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa,
                                                                       dst=D),
             "quantize_prepare_b": lambda: cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb)})
@@ -1339,6 +1335,7 @@ def main():
                                                 "weight": pb_bytes / (cold["prepare_b"] * 1e-6) / 1e9}
     if fused_step:
         result["cold_cache"]["quantize_prepare_gbps"] = {
+            "pair": (qpa_bytes + qpb_bytes) / (cold["quantize_prepare_pair"] * 1e-6) / 1e9,
             "act": qpa_bytes / (cold["quantize_prepare_a"] * 1e-6) / 1e9,
             "weight": qpb_bytes / (cold["quantize_prepare_b"] * 1e-6) / 1e9}
 

@@ -350,6 +350,24 @@ int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k
                              void* stream);
 
 /*
+ * curvefp_quantize_prepare of the two operands of one GEMM in one launch (Sec. 3.3: both operands
+ * of Q_A(X) Q_W(W)^T are quantized along the contraction axis k; one format, one block size and
+ * one source type for both): A [rows_a][ld_a] and B [rows_b][ld_b], each with its own codes,
+ * scales, prepared buffer (prepared_a_size / prepared_b_size bytes) and optional reconstruction
+ * (dst_a / dst_b, null for none).  The outputs are those of two curvefp_quantize_prepare calls,
+ * bit for bit; one launch spreads both operands over the whole GPU and needs no second stream.
+ * Errors: those of curvefp_quantize_prepare for either operand, and CURVEFP_ERR_SHAPE for
+ * rows_a + rows_b >= 2^31.
+ */
+int curvefp_quantize_prepare_pair(const void* src_a, int64_t rows_a, int64_t ld_a, void* codes_a,
+                                  int8_t* scales_a, void* prepared_a, int64_t prepared_a_size,
+                                  float* dst_a, int64_t ld_dst_a,
+                                  const void* src_b, int64_t rows_b, int64_t ld_b, void* codes_b,
+                                  int8_t* scales_b, void* prepared_b, int64_t prepared_b_size,
+                                  float* dst_b, int64_t ld_dst_b,
+                                  int dtype, int64_t k, int format, int block, void* stream);
+
+/*
  * Bytes of device workspace curvefp_gemm_prepared needs for an M x N x K product: 0 unless K
  * is split in two (fewer than 256 output tiles of 256 x 256 and K >= 512; then one arrival
  * counter per tile and 512 KiB of partial sums per tile).  CURVEFP_ERR_SHAPE for non-positive

@@ -38,6 +38,25 @@ int hip_status(hipError_t e) { return e == hipSuccess ? CURVEFP_OK : CURVEFP_ERR
 // contraction length of the GEMM entry points: positive, whole groups of 32, at most CURVEFP_MAX_K
 bool gemm_k_ok(int64_t K) { return K > 0 && K % 32 == 0 && K <= CURVEFP_MAX_K; }
 
+// one operand of curvefp_quantize_prepare(_pair): the status of its arguments
+int qp_check(int dtype, int64_t k, int format, int block, const void* src, int64_t rows, int64_t ld_src,
+             const void* codes, const int8_t* scales, const void* prepared, int64_t prepared_size, const float* dst,
+             int64_t ld_dst) {
+    if (!src || !codes || !scales || !prepared) return CURVEFP_ERR_NULL;
+    if ((dtype != 0 && dtype != 1) || !fmt_ok(format)) return CURVEFP_ERR_FORMAT;
+    // a block's maximum is reduced over the 4 .. 64 lanes that hold it
+    if (block != 32 && block != 64 && block != 128 && block != 256 && block != 512) return CURVEFP_ERR_BLOCK;
+    if (rows <= 0 || rows >= ((int64_t)1 << 31) || k <= 0 || k % block || ld_src < k) return CURVEFP_ERR_SHAPE;
+    if (k > CURVEFP_MAX_K) return CURVEFP_ERR_SHAPE;   // the prepared form's bound
+    if (dst && ld_dst < k) return CURVEFP_ERR_SHAPE;
+    if (prepared_size < prepared_bytes(rows, k, 0)) return CURVEFP_ERR_SHAPE;
+    const int64_t esz = dtype == 1 ? 2 : 4;
+    if (!aligned16(src) || (ld_src * esz) % 16 || !aligned16(codes) || reinterpret_cast<uintptr_t>(prepared) % 256)
+        return CURVEFP_ERR_ALIGN;
+    if (dst && (!aligned16(dst) || (ld_dst * 4) % 16)) return CURVEFP_ERR_ALIGN;
+    return CURVEFP_OK;
+}
+
 }  // namespace
 
 #pragma GCC visibility push(default)
@@ -221,20 +240,28 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
 int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld_src, int format,
                              int block, void* codes, int8_t* scales, void* prepared, int64_t prepared_size, float* dst,
                              int64_t ld_dst, void* stream) {
-    if (!src || !codes || !scales || !prepared) return CURVEFP_ERR_NULL;
-    if ((dtype != 0 && dtype != 1) || !fmt_ok(format)) return CURVEFP_ERR_FORMAT;
-    // a block's maximum is reduced over the 4 .. 64 lanes that hold it
-    if (block != 32 && block != 64 && block != 128 && block != 256 && block != 512) return CURVEFP_ERR_BLOCK;
-    if (rows <= 0 || rows >= ((int64_t)1 << 31) || k <= 0 || k % block || ld_src < k) return CURVEFP_ERR_SHAPE;
-    if (k > CURVEFP_MAX_K) return CURVEFP_ERR_SHAPE;   // the prepared form's bound
-    if (dst && ld_dst < k) return CURVEFP_ERR_SHAPE;
-    if (prepared_size < prepared_bytes(rows, k, 0)) return CURVEFP_ERR_SHAPE;
-    const int64_t esz = dtype == 1 ? 2 : 4;
-    if (!aligned16(src) || (ld_src * esz) % 16 || !aligned16(codes) || reinterpret_cast<uintptr_t>(prepared) % 256)
-        return CURVEFP_ERR_ALIGN;
-    if (dst && (!aligned16(dst) || (ld_dst * 4) % 16)) return CURVEFP_ERR_ALIGN;
+    const int st = qp_check(dtype, k, format, block, src, rows, ld_src, codes, scales, prepared, prepared_size, dst,
+                            ld_dst);
+    if (st != CURVEFP_OK) return st;
     return hip_status(launch_quantize_prepare(src, dtype, rows, k, ld_src, format, block, codes, scales, prepared, dst,
                                               ld_dst, reinterpret_cast<hipStream_t>(stream)));
+}
+
+int curvefp_quantize_prepare_pair(const void* src_a, int64_t rows_a, int64_t ld_a, void* codes_a, int8_t* scales_a,
+                                  void* prepared_a, int64_t prepared_a_size, float* dst_a, int64_t ld_dst_a,
+                                  const void* src_b, int64_t rows_b, int64_t ld_b, void* codes_b, int8_t* scales_b,
+                                  void* prepared_b, int64_t prepared_b_size, float* dst_b, int64_t ld_dst_b,
+                                  int dtype, int64_t k, int format, int block, void* stream) {
+    int st = qp_check(dtype, k, format, block, src_a, rows_a, ld_a, codes_a, scales_a, prepared_a, prepared_a_size,
+                      dst_a, ld_dst_a);
+    if (st != CURVEFP_OK) return st;
+    st = qp_check(dtype, k, format, block, src_b, rows_b, ld_b, codes_b, scales_b, prepared_b, prepared_b_size, dst_b,
+                  ld_dst_b);
+    if (st != CURVEFP_OK) return st;
+    if (rows_a + rows_b >= ((int64_t)1 << 31)) return CURVEFP_ERR_SHAPE;
+    return hip_status(launch_quantize_prepare_pair(src_a, rows_a, ld_a, codes_a, scales_a, prepared_a, dst_a, ld_dst_a,
+                                                   src_b, rows_b, ld_b, codes_b, scales_b, prepared_b, dst_b, ld_dst_b,
+                                                   dtype, k, format, block, reinterpret_cast<hipStream_t>(stream)));
 }
 
 int64_t curvefp_gemm_prepared_workspace_bytes(int64_t M, int64_t N, int64_t K) {

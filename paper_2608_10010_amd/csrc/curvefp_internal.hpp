@@ -40,6 +40,12 @@ hipError_t launch_scales_unpack(const int8_t* row_ref, const uint8_t* offsets, i
 hipError_t launch_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format,
                                   int block, void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst,
                                   hipStream_t s);
+// the same for the two operands of one GEMM (same k, dtype, format and block) in one launch
+hipError_t launch_quantize_prepare_pair(const void* src_a, int64_t rows_a, int64_t ld_a, void* codes_a,
+                                       int8_t* scales_a, void* prepared_a, float* dst_a, int64_t ld_dst_a,
+                                       const void* src_b, int64_t rows_b, int64_t ld_b, void* codes_b,
+                                       int8_t* scales_b, void* prepared_b, float* dst_b, int64_t ld_dst_b, int dtype,
+                                       int64_t k, int format, int block, hipStream_t s);
 hipError_t launch_dequantize(const void* codes, const int8_t* scales, int format,
                              int64_t outer, int64_t k, int block, float* dst, int64_t ld_dst, hipStream_t s);
 // workspace path: bytes it needs, and the launch (expansion kernels, then the GEMM)

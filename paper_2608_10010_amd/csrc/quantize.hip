@@ -1264,12 +1264,24 @@ hipError_t launch_mse_fmt(const void* src, int dtype, int64_t rows, int64_t cols
 // takes them back and writes.  Slots past the row's end hold zeros (scale -127, the bottom key,
 // so alpha is unchanged) and store nothing.  Workgroups of the padding rows (up to the next
 // multiple of 256) write zero planes and a zero row maximum, as the expansion does past the
-// operand.
+// operand.  Two operands of one GEMM (same k, format and source type) can share a launch:
+// workgroups [0, blocks_a) take A, the rest B.
+struct QPOperand {
+    const void* src;
+    int64_t rows, ld;
+    uint8_t* codes;
+    int8_t* scales;
+    char* planes;
+    int* rmax;          // the prepared layout's row maxima, after the planes
+    int64_t RT;         // tiles of 256 rows
+    float* dst;         // the reconstruction, or null
+    int64_t ld_dst;
+};
+
 template <class F, bool BF16, int U, int WPR>
-__global__ __launch_bounds__(256) void quantize_prepare_kernel(
-    const void* __restrict__ src, int64_t rows, int64_t ld, uint32_t cpr, int64_t code_row_bytes,
-    uint8_t* __restrict__ codes, int8_t* __restrict__ scales, int64_t nsb, char* __restrict__ planes,
-    int* __restrict__ rmax, int64_t RT, float* __restrict__ dst, int64_t ld_dst, int fidx, int lgl) {
+__global__ __launch_bounds__(256) void quantize_prepare_kernel(QPOperand opA, QPOperand opB, int64_t blocks_a,
+                                                               uint32_t cpr, int64_t code_row_bytes, int64_t nsb,
+                                                               int fidx, int lgl) {
     using T = typename std::conditional<BF16, uint8_t, uint32_t>::type;
     constexpr int ESZ = BF16 ? 2 : 4;
     constexpr int NV = BF16 ? 1 : 2;   // 16-byte loads per chunk
@@ -1285,11 +1297,17 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     __shared__ uint64_t qsig[128];
     __shared__ int wkey[4];
     const int lane = (int)(threadIdx.x & 63), wave = (int)(threadIdx.x >> 6);
+    const bool isA = (int64_t)blockIdx.x < blocks_a;
+    const QPOperand& op = isA ? opA : opB;
+    const int64_t bid = isA ? (int64_t)blockIdx.x : (int64_t)blockIdx.x - blocks_a;
+    const int64_t rows = op.rows, ld = op.ld, RT = op.RT, ld_dst = op.ld_dst;
+    char* __restrict__ planes = op.planes;
+    float* __restrict__ dst = op.dst;
     const int wr = wave % WPR;                               // this wave's part of its row
-    const int64_t row = ((int64_t)blockIdx.x * 4 + wave) / WPR;
+    const int64_t row = (bid * 4 + wave) / WPR;
     const bool real = row < rows;                            // uniform over the waves of a row
     uint4* wbuf = rowbuf + (wave / WPR) * (SPAN * U * NV);
-    const uint4* srow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(src) + (real ? row : 0) * ld * ESZ);
+    const uint4* srow = reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(op.src) + (real ? row : 0) * ld * ESZ);
     const uint32_t nseg = (cpr + SPAN * UL - 1) / (SPAN * UL);
     auto chunk_of = [&](uint32_t seg, int u) { return SPAN * (UL * seg + (uint32_t)u) + 64u * wr + (uint32_t)lane; };
     auto load = [&](uint32_t seg, uint4 (*v)[NV]) {
@@ -1331,7 +1349,7 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
                 *reinterpret_cast<uint4*>(pd) = make_uint4(0u, 0u, 0u, 0u);
                 *reinterpret_cast<uint4*>(pd + PLANE) = make_uint4(0u, 0u, 0u, 0u);
             }
-            if (wr == 0 && lane == 0) rmax[row] = 0;
+            if (wr == 0 && lane == 0) op.rmax[row] = 0;
         }
         return;
     }
@@ -1374,8 +1392,8 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
     const int alpha = key;
 
     // pass 2: codes and scales, both planes, the reconstruction
-    uint8_t* crow = codes + row * code_row_bytes;
-    int8_t* scrow = scales + row * nsb;
+    uint8_t* crow = op.codes + row * code_row_bytes;
+    int8_t* scrow = op.scales + row * nsb;
     for (uint32_t seg = 0; seg < nseg; seg++) {
 #pragma unroll
         for (int u = 0; u < UL; u++) {
@@ -1409,50 +1427,59 @@ __global__ __launch_bounds__(256) void quantize_prepare_kernel(
             }
         }
     }
-    if (wr == 0 && lane == 0) rmax[row] = alpha;
+    if (wr == 0 && lane == 0) op.rmax[row] = alpha;
+}
+
+// an operand of a launch: its buffers and tiles (rows = 0: none)
+QPOperand qp_operand(const void* src, int64_t rows, int64_t k, int64_t ld, void* codes, int8_t* scales, void* prepared,
+                     float* dst, int64_t ld_dst) {
+    QPOperand o;
+    o.src = src;
+    o.rows = rows;
+    o.ld = ld;
+    o.codes = reinterpret_cast<uint8_t*>(codes);
+    o.scales = scales;
+    o.planes = reinterpret_cast<char*>(prepared);
+    o.RT = (rows + BM - 1) / BM;
+    // the prepared layout: planes, then the row maxima
+    o.rmax = rows > 0 ? reinterpret_cast<int*>(o.planes + (k / 32) * o.RT * 2 * PLANE) : nullptr;
+    o.dst = dst;
+    o.ld_dst = ld_dst;
+    return o;
 }
 
 template <class F, bool BF16, int U, int WPR>
-hipError_t launch_qp_u(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
-                       int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
-    const int64_t RT = (rows + BM - 1) / BM;
+hipError_t launch_qp_u(const QPOperand& a, const QPOperand& b, int64_t k, int fidx, int block, hipStream_t s) {
     int lgl = 0;
     while ((8 << lgl) < block) lgl++;
     const int64_t code_row_bytes = F::PACKED7 ? k / 32 * 28 : k;
-    char* rmax = planes + (k / 32) * RT * 2 * PLANE;   // the prepared layout: planes, then row maxima
-    hipLaunchKernelGGL((quantize_prepare_kernel<F, BF16, U, WPR>), dim3((unsigned)(RT * 64 * WPR)), dim3(256), 0, s,
-                       src, rows, ld, (uint32_t)(k / 8), code_row_bytes, codes, scales, k / block, planes,
-                       reinterpret_cast<int*>(rmax), RT, dst, ld_dst, fidx, lgl);
+    const int64_t blocks_a = a.RT * 64 * WPR, blocks_b = b.RT * 64 * WPR;
+    hipLaunchKernelGGL((quantize_prepare_kernel<F, BF16, U, WPR>), dim3((unsigned)(blocks_a + blocks_b)), dim3(256), 0,
+                       s, a, b, blocks_a, (uint32_t)(k / 8), code_row_bytes, k / block, fidx, lgl);
     return hipGetLastError();
 }
 
 // Rows of up to 512 chunks (bf16; 256 fp32: 2, 4 or 8 chunks per lane) take one wave each,
-// rows of up to 2048 bf16 (512 fp32) chunks one workgroup each, staged in at most 32 KB of LDS
+// rows of up to 1024 bf16 (512 fp32) chunks one workgroup each, staged in at most 32 KB of LDS
 // per workgroup; qp_fused_rows decides which rows go here at all.
 template <class F, bool BF16>
-hipError_t launch_qp(const void* src, int64_t rows, int64_t k, int64_t ld, int fidx, int block, uint8_t* codes,
-                     int8_t* scales, char* planes, float* dst, int64_t ld_dst, hipStream_t s) {
+hipError_t launch_qp(const QPOperand& a, const QPOperand& b, int64_t k, int fidx, int block, hipStream_t s) {
     const int64_t cpr = k / 8;
-    if (cpr <= 128) return launch_qp_u<F, BF16, 2, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-    if (cpr <= 256) return launch_qp_u<F, BF16, 4, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+    if (cpr <= 128) return launch_qp_u<F, BF16, 2, 1>(a, b, k, fidx, block, s);
+    if (cpr <= 256) return launch_qp_u<F, BF16, 4, 1>(a, b, k, fidx, block, s);
     if constexpr (BF16) {
-        if (cpr <= 512)
-            return launch_qp_u<F, BF16, 8, 1>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-        if (cpr <= 1024)
-            return launch_qp_u<F, BF16, 4, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
-        return launch_qp_u<F, BF16, 8, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+        if (cpr <= 512) return launch_qp_u<F, BF16, 8, 1>(a, b, k, fidx, block, s);
+        if (cpr <= 1024) return launch_qp_u<F, BF16, 4, 4>(a, b, k, fidx, block, s);
+        return launch_qp_u<F, BF16, 8, 4>(a, b, k, fidx, block, s);
     } else {
-        return launch_qp_u<F, BF16, 2, 4>(src, rows, k, ld, fidx, block, codes, scales, planes, dst, ld_dst, s);
+        return launch_qp_u<F, BF16, 2, 4>(a, b, k, fidx, block, s);
     }
 }
 
 template <class F>
-hipError_t launch_qp_fmt(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int fidx, int block,
-                         void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst, hipStream_t s) {
-    uint8_t* cp = reinterpret_cast<uint8_t*>(codes);
-    char* pp = reinterpret_cast<char*>(prepared);
-    return dtype == 1 ? launch_qp<F, true>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s)
-                      : launch_qp<F, false>(src, rows, k, ld, fidx, block, cp, scales, pp, dst, ld_dst, s);
+hipError_t launch_qp_fmt(const QPOperand& a, const QPOperand& b, int dtype, int64_t k, int fidx, int block,
+                         hipStream_t s) {
+    return dtype == 1 ? launch_qp<F, true>(a, b, k, fidx, block, s) : launch_qp<F, false>(a, b, k, fidx, block, s);
 }
 
 // Which shapes take the fused kernel: rows of up to 1024 chunks (bf16; 512 fp32), and bf16 rows of
@@ -1484,25 +1511,55 @@ hipError_t launch_quantize(const void* src, int dtype, int64_t rows, int64_t col
 
 namespace curvefp {
 
+namespace {
+
+// the three kernels in turn for one operand (shapes the fused kernel does not take)
+hipError_t qp_separate(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format, int block,
+                       void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst, hipStream_t s) {
+    hipError_t e = launch_quantize(src, dtype, rows, k, ld, 1, format, block, codes, scales, s);
+    if (e == hipSuccess) e = launch_prepare(codes, scales, rows, k, format, block, 0, prepared, s);
+    if (e == hipSuccess && dst != nullptr) e = launch_dequantize(codes, scales, format, rows, k, block, dst, ld_dst, s);
+    return e;
+}
+
+hipError_t qp_launch(const QPOperand& a, const QPOperand& b, int dtype, int64_t k, int format, int block,
+                     hipStream_t s) {
+    switch (format) {
+        case 0: return launch_qp_fmt<FmtE4C3>(a, b, dtype, k, 0, block, s);
+        case 1: return launch_qp_fmt<FmtE5C2>(a, b, dtype, k, 1, block, s);
+        case 2: return launch_qp_fmt<FmtE3C3>(a, b, dtype, k, 2, block, s);
+        case 3: return launch_qp_fmt<FmtE4C3R89>(a, b, dtype, k, 3, block, s);
+        default: return launch_qp_fmt<FmtE4C3R34>(a, b, dtype, k, 4, block, s);
+    }
+}
+
+}  // namespace
+
 hipError_t launch_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k, int64_t ld, int format,
                                   int block, void* codes, int8_t* scales, void* prepared, float* dst, int64_t ld_dst,
                                   hipStream_t s) {
-    if (!qp_fused_rows(dtype, rows, k)) {
-        // longer rows: the three kernels in turn, on the same outputs
-        hipError_t e = launch_quantize(src, dtype, rows, k, ld, 1, format, block, codes, scales, s);
-        if (e == hipSuccess) e = launch_prepare(codes, scales, rows, k, format, block, 0, prepared, s);
-        if (e == hipSuccess && dst != nullptr) e = launch_dequantize(codes, scales, format, rows, k, block, dst, ld_dst, s);
-        return e;
+    if (!qp_fused_rows(dtype, rows, k))
+        return qp_separate(src, dtype, rows, k, ld, format, block, codes, scales, prepared, dst, ld_dst, s);
+    const QPOperand none = qp_operand(nullptr, 0, k, 0, nullptr, nullptr, nullptr, nullptr, 0);
+    return qp_launch(qp_operand(src, rows, k, ld, codes, scales, prepared, dst, ld_dst), none, dtype, k, format, block,
+                     s);
+}
+
+hipError_t launch_quantize_prepare_pair(const void* src_a, int64_t rows_a, int64_t ld_a, void* codes_a,
+                                       int8_t* scales_a, void* prepared_a, float* dst_a, int64_t ld_dst_a,
+                                       const void* src_b, int64_t rows_b, int64_t ld_b, void* codes_b,
+                                       int8_t* scales_b, void* prepared_b, float* dst_b, int64_t ld_dst_b, int dtype,
+                                       int64_t k, int format, int block, hipStream_t s) {
+    if (!qp_fused_rows(dtype, rows_a + rows_b, k)) {
+        hipError_t e = qp_separate(src_a, dtype, rows_a, k, ld_a, format, block, codes_a, scales_a, prepared_a, dst_a,
+                                   ld_dst_a, s);
+        if (e != hipSuccess) return e;
+        return qp_separate(src_b, dtype, rows_b, k, ld_b, format, block, codes_b, scales_b, prepared_b, dst_b, ld_dst_b,
+                           s);
     }
-    switch (format) {
-        case 0: return launch_qp_fmt<FmtE4C3>(src, dtype, rows, k, ld, 0, block, codes, scales, prepared, dst, ld_dst, s);
-        case 1: return launch_qp_fmt<FmtE5C2>(src, dtype, rows, k, ld, 1, block, codes, scales, prepared, dst, ld_dst, s);
-        case 2: return launch_qp_fmt<FmtE3C3>(src, dtype, rows, k, ld, 2, block, codes, scales, prepared, dst, ld_dst, s);
-        case 3:
-            return launch_qp_fmt<FmtE4C3R89>(src, dtype, rows, k, ld, 3, block, codes, scales, prepared, dst, ld_dst, s);
-        default:
-            return launch_qp_fmt<FmtE4C3R34>(src, dtype, rows, k, ld, 4, block, codes, scales, prepared, dst, ld_dst, s);
-    }
+    return qp_launch(qp_operand(src_a, rows_a, k, ld_a, codes_a, scales_a, prepared_a, dst_a, ld_dst_a),
+                     qp_operand(src_b, rows_b, k, ld_b, codes_b, scales_b, prepared_b, dst_b, ld_dst_b), dtype, k,
+                     format, block, s);
 }
 
 hipError_t launch_quantize_mse(const void* src, int dtype, int64_t rows, int64_t cols, int64_t ld, int axis,

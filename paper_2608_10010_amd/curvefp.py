@@ -79,6 +79,9 @@ def lib() -> ctypes.CDLL:
         L.curvefp_prepare.restype = I
         L.curvefp_quantize_prepare.argtypes = [P, I, I64, I64, I64, I, I, P, P, P, I64, P, I64, P]
         L.curvefp_quantize_prepare.restype = I
+        L.curvefp_quantize_prepare_pair.argtypes = [P, I64, I64, P, P, P, I64, P, I64,
+                                                    P, I64, I64, P, P, P, I64, P, I64, I, I64, I, I, P]
+        L.curvefp_quantize_prepare_pair.restype = I
         L.curvefp_gemm_prepared_workspace_bytes.argtypes = [I64, I64, I64]
         L.curvefp_gemm_prepared_workspace_bytes.restype = I64
         L.curvefp_gemm_prepared.argtypes = [P, I, P, I, I64, I64, I64, P, I64, P, I64, P]
@@ -507,17 +510,11 @@ def curvefp_prepare(codes: torch.Tensor, scales: torch.Tensor, rows: int, k: int
     return prepared
 
 
-def curvefp_quantize_prepare(src: torch.Tensor, fmt, block: int = 32, codes: Optional[torch.Tensor] = None,
-                             scales: Optional[torch.Tensor] = None, prepared: Optional[torch.Tensor] = None,
-                             dst: Optional[torch.Tensor] = None, dequantize: bool = False, stream=None):
-    """curvefp_quantize (blocks along the rows of a [rows, k] fp32/bf16 source), curvefp_prepare of
-    the result (trans = 0) and, with dequantize=True or a dst given, curvefp_dequantize of it, in
-    one launch.  Returns (codes, scales, prepared), plus dst when it is written."""
-    what = "curvefp_quantize_prepare"
+def _qp_outputs(what, src, f, block, codes, scales, prepared, dst, dequantize, stream):
+    """The outputs of one operand of quantize-prepare (allocated here when not given), checked."""
     _on_gpu(what, [("src", src)], stream)
     _source_arg(what, src)
     rows, k = src.shape
-    f = _fmt(fmt)
     if codes is None:
         shape = (rows, k // 32, 28) if f == 2 else (rows, k)
         codes = torch.empty(shape, dtype=torch.uint8, device=src.device)
@@ -534,6 +531,26 @@ def curvefp_quantize_prepare(src: torch.Tensor, fmt, block: int = 32, codes: Opt
     _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k, 0))
     if dst is not None:
         _matrix(what, "dst", dst, rows, k, (torch.float32,))
+    return codes, scales, prepared, dst
+
+
+def _qp_args(src, codes, scales, prepared, dst):
+    """One operand's pointer and size arguments, in the ABI's order."""
+    return [src.data_ptr(), src.shape[0], src.stride(0), codes.data_ptr(), scales.data_ptr(), prepared.data_ptr(),
+            prepared.numel() * prepared.element_size(), dst.data_ptr() if dst is not None else None,
+            dst.stride(0) if dst is not None else 0]
+
+
+def curvefp_quantize_prepare(src: torch.Tensor, fmt, block: int = 32, codes: Optional[torch.Tensor] = None,
+                             scales: Optional[torch.Tensor] = None, prepared: Optional[torch.Tensor] = None,
+                             dst: Optional[torch.Tensor] = None, dequantize: bool = False, stream=None):
+    """curvefp_quantize (blocks along the rows of a [rows, k] fp32/bf16 source), curvefp_prepare of
+    the result (trans = 0) and, with dequantize=True or a dst given, curvefp_dequantize of it, in
+    one launch.  Returns (codes, scales, prepared), plus dst when it is written."""
+    what = "curvefp_quantize_prepare"
+    f = _fmt(fmt)
+    codes, scales, prepared, dst = _qp_outputs(what, src, f, block, codes, scales, prepared, dst, dequantize, stream)
+    rows, k = src.shape
     st = lib().curvefp_quantize_prepare(src.data_ptr(), DTYPES[src.dtype], rows, k, src.stride(0), f, block,
                                         codes.data_ptr(), scales.data_ptr(), prepared.data_ptr(),
                                         prepared.numel() * prepared.element_size(),
@@ -541,6 +558,27 @@ def curvefp_quantize_prepare(src: torch.Tensor, fmt, block: int = 32, codes: Opt
                                         dst.stride(0) if dst is not None else 0, _stream(stream))
     _check(st, what)
     return (codes, scales, prepared) if dst is None else (codes, scales, prepared, dst)
+
+
+def curvefp_quantize_prepare_pair(src_a: torch.Tensor, src_b: torch.Tensor, fmt, block: int = 32,
+                                  out_a: Optional[Tuple] = None, out_b: Optional[Tuple] = None,
+                                  dequantize_a: bool = False, dequantize_b: bool = False, stream=None):
+    """curvefp_quantize_prepare of both operands of one GEMM ([rows_a, k] and [rows_b, k] sources of one
+    dtype) in one launch.  out_a / out_b: (codes, scales, prepared[, dst]) to write into, else
+    allocated.  Returns the two operands' tuples, as curvefp_quantize_prepare does."""
+    what = "curvefp_quantize_prepare_pair"
+    f = _fmt(fmt)
+    if src_a.dim() == 2 and src_b.dim() == 2 and (src_a.shape[1] != src_b.shape[1] or src_a.dtype != src_b.dtype):
+        raise ValueError(f"{what}: the sources must share k and dtype, got {tuple(src_a.shape)} {src_a.dtype} and "
+                         f"{tuple(src_b.shape)} {src_b.dtype}")
+    oa = (list(out_a) + [None] * (4 - len(out_a))) if out_a is not None else [None] * 4
+    ob = (list(out_b) + [None] * (4 - len(out_b))) if out_b is not None else [None] * 4
+    a = _qp_outputs(what, src_a, f, block, *oa, dequantize_a, stream)
+    b = _qp_outputs(what, src_b, f, block, *ob, dequantize_b, stream)
+    st = lib().curvefp_quantize_prepare_pair(*_qp_args(src_a, *a), *_qp_args(src_b, *b), DTYPES[src_a.dtype],
+                                             src_a.shape[1], f, block, _stream(stream))
+    _check(st, what)
+    return tuple((x[:3] if x[3] is None else x) for x in (a, b))
 
 
 def curvefp_gemm_prepared_workspace_bytes(M: int, N: int, K: int) -> int:

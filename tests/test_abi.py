@@ -33,7 +33,7 @@ def L():
 
 def test_exports_every_declared_symbol(L):
     names = declared_functions()
-    assert len(names) == 24
+    assert len(names) == 25
     out = subprocess.run(["nm", "-D", "--defined-only", B.LIB], capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT (curvefp_[a-z0-9_]+)$", out, flags=re.M))
     for n in names:
@@ -305,6 +305,33 @@ def test_quantize_prepare_validation(L):
         if i == 4:
             a[3] = 256                           # a bf16 row stride of 520 bytes
         assert q(*a) == EALIGN, (i, v)
+
+
+def test_quantize_prepare_pair_validation(L):
+    q = L.curvefp_quantize_prepare_pair
+    PR = 1 << 24
+    na, nb = L.curvefp_prepared_bytes(64, 256, 0), L.curvefp_prepared_bytes(300, 256, 0)
+    #       src   rows ld   codes scales prep need dst   ldd
+    A = [FAKE, 64, 256, FAKE, FAKE, PR, na, FAKE, 256]
+    B = [FAKE, 300, 256, FAKE, FAKE, PR, nb, None, 0]
+    tail = [1, 256, 0, 32, None]                 # dtype, k, format, block, stream
+    for part, i in [(0, 0), (0, 3), (0, 4), (0, 5), (1, 0), (1, 3), (1, 4), (1, 5)]:
+        a, b = list(A), list(B)
+        (a if part == 0 else b)[i] = None
+        assert q(*a, *b, *tail) == ENULL, (part, i)
+    for part, i, v in [(0, 6, na - 1), (1, 6, nb - 1), (0, 1, 0), (1, 1, -1), (1, 2, 128), (0, 8, 100)]:
+        a, b = list(A), list(B)
+        (a if part == 0 else b)[i] = v
+        assert q(*a, *b, *tail) == ESHAPE, (part, i, v)
+    for i, v, st in [(0, 2, EFMT), (2, 5, EFMT), (3, 48, EBLOCK), (1, 320, ESHAPE)]:
+        t = list(tail); t[i] = v
+        assert q(*A, *B, *t) == st, (i, v)
+    big = list(B); big[1] = (1 << 31) - 64; big[6] = 1 << 62
+    assert q(*A, *big, *tail) == ESHAPE          # rows_a + rows_b >= 2^31
+    a = list(A); a[0] = MIS
+    assert q(*a, *B, *tail) == EALIGN
+    b = list(B); b[5] = PR + 16
+    assert q(*A, *b, *tail) == EALIGN
 
 
 def test_gemm_mixed_validation(L):

@@ -195,6 +195,23 @@ def test_quantize_prepare_checks(meta):
         cf.curvefp_quantize_prepare(torch.zeros((M, K)), "E4C3", stream=STREAM)
 
 
+def test_quantize_prepare_pair_checks(meta):
+    K = 256
+    a, b = meta((64, K), torch.bfloat16), meta((300, K), torch.bfloat16)
+    passes_checks(lambda: cf.curvefp_quantize_prepare_pair(a, b, "E4C3", dequantize_a=True, stream=STREAM))
+    with pytest.raises(ValueError, match="share k and dtype"):
+        cf.curvefp_quantize_prepare_pair(a, meta((300, K + 32), torch.bfloat16), "E4C3", stream=STREAM)
+    with pytest.raises(ValueError, match="share k and dtype"):
+        cf.curvefp_quantize_prepare_pair(a, meta((300, K), torch.float32), "E4C3", stream=STREAM)
+    with pytest.raises(ValueError, match="prepared"):
+        cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_b=(None, None, meta((1024,), torch.uint8)), stream=STREAM)
+    with pytest.raises(ValueError, match="dst"):
+        cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_a=(None, None, None, meta((63, K), torch.float32)),
+                                         stream=STREAM)
+    with pytest.raises(ValueError, match="not on a GPU"):
+        cf.curvefp_quantize_prepare_pair(a, torch.zeros((300, K), dtype=torch.bfloat16), "E4C3", stream=STREAM)
+
+
 def test_mixed_gemm_checks(meta):
     M, N, K = 64, 96, 256
     # A = dY codes [M][K] along K; B = reused forward codes of a [K][N] tensor, blocks along N

@@ -169,3 +169,49 @@ def test_workload_full_size(name):
     Cw = cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt)
     torch.cuda.synchronize()
     assert torch.equal(C.view(torch.int32), Cw.view(torch.int32)), f"{name}: fused-prepared GEMM differs"
+
+
+@pytest.mark.parametrize("fmt", ["E4C3", "E5C2", "E3C3", "E4C3_r8/9"])
+@pytest.mark.parametrize("dtype,ra,rb,k,block", [("bf16", 300, 520, 640, 32), ("bf16", 1, 257, 4096, 64),
+                                                  ("f32", 129, 64, 2048, 128), ("bf16", 40, 24, 8192, 32),
+                                                  ("bf16", 16, 8, 32768, 32)])
+def test_pair(fmt, dtype, ra, rb, k, block):
+    """Both operands in one launch (a wave or a workgroup per row, or the separate kernels for the
+    longest rows): the outputs of two single calls, byte for byte, and the GEMM on them that of the
+    workspace GEMM."""
+    rng = np.random.default_rng(ra * 7 + rb + k)
+    A = (rng.standard_normal((ra, k)) * np.exp2(rng.uniform(-20, 20, (ra, 1)))).astype(np.float32)
+    B = (rng.standard_normal((rb, k)) * 0.02).astype(np.float32)
+    if dtype == "bf16":
+        A, B = W.bf16_round(A), W.bf16_round(B)
+    ta, tb = source(A, dtype), source(B, dtype)
+    say(f"[quantize_prepare] pair fmt={fmt} dtype={dtype} rows={ra}+{rb} k={k} G={block}")
+    pa, pb = cf.curvefp_quantize_prepare_pair(ta, tb, fmt, block=block, dequantize_a=True)
+    sa_ = cf.curvefp_quantize_prepare(ta, fmt, block=block, dequantize=True)
+    sb_ = cf.curvefp_quantize_prepare(tb, fmt, block=block)
+    torch.cuda.synchronize()
+    assert len(pa) == 4 and len(pb) == 3
+    for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
+                                            "prepared B")):
+        same_bytes(x, y, f"pair {fmt} {ra}+{rb}x{k}: {n}")
+    oracle_check(A, fmt, block, pa[0], pa[1], pa[3], f"pair {fmt} A")
+    if k <= 8192:
+        C = cf.curvefp_gemm_prepared(pa[2], fmt, pb[2], fmt, ra, rb, k)
+        Cw = cf.curvefp_gemm_ws(pa[0], pa[1], pb[0], pb[1], ra, rb, k, fmt, block=block)
+        torch.cuda.synchronize()
+        same_bits(C.cpu().numpy(), Cw.cpu().numpy(), f"pair {fmt} gemm")
+
+
+def test_pair_benchmark_operands():
+    """The benchmark's step: both gate/up operands in one launch equal two single calls."""
+    w = W.get("sweep_gateup_E4C3")
+    ta = torch.from_numpy(w.operand("a")).to(torch.bfloat16).to(DEV)
+    tb = torch.from_numpy(w.operand("b")).to(torch.bfloat16).to(DEV)
+    say("[quantize_prepare] pair on the gate/up operands")
+    pa, pb = cf.curvefp_quantize_prepare_pair(ta, tb, w.fmt, dequantize_a=True)
+    sa_ = cf.curvefp_quantize_prepare(ta, w.fmt, dequantize=True)
+    sb_ = cf.curvefp_quantize_prepare(tb, w.fmt)
+    torch.cuda.synchronize()
+    for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
+                                            "prepared B")):
+        same_bytes(x, y, f"gate/up pair: {n}")
