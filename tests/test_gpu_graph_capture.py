@@ -1,7 +1,8 @@
 """The path under HIP graph capture: the library's calls only launch kernels on the caller's stream
 (no allocation, upload, memset or synchronization), so a caller can capture a whole step --
-quantize, dequantize, prepare both operands, the GEMM on prepared operands; and the workspace GEMM
-on the library's static scratch -- into a graph and replay it.  Every replay follows new inputs
+quantize, dequantize, prepare both operands, the GEMM on prepared operands; the workspace GEMM on
+the library's static scratch; and the benchmark's step, quantize-prepare of both operands in one
+launch then the prepared GEMM -- into a graph and replay it.  Every replay follows new inputs
 written eagerly into the captured buffers (with synchronizations in between) and is compared bit for
 bit with the same calls made eagerly on those inputs."""
 
@@ -42,6 +43,9 @@ def test_captured_step_replays(fmt):
     gws = torch.empty(cf.curvefp_gemm_prepared_workspace_bytes(M, N, K), dtype=torch.uint8, device=DEV)
     C = torch.empty((M, N), dtype=torch.float32, device=DEV)
     C2 = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    C3 = torch.empty((M, N), dtype=torch.float32, device=DEV)
+    # the benchmark's step writes its own operand buffers
+    (qca, qsa, qpa, qD), (qcb, qsb, qpb) = cf.curvefp_quantize_prepare_pair(x, wt, fmt, dequantize_a=True)
 
     def step():
         cf.curvefp_quantize(x, fmt, codes=ca, scales=sa)
@@ -51,6 +55,8 @@ def test_captured_step_replays(fmt):
         cf.curvefp_prepare(cb, sb, N, K, fmt, prepared=pb)
         cf.curvefp_gemm_prepared(pa, fmt, pb, fmt, M, N, K, c=C, workspace=gws)
         cf.curvefp_gemm_ws_static(ca, sa, cb, sb, M, N, K, fmt, c=C2)
+        cf.curvefp_quantize_prepare_pair(x, wt, fmt, out_a=(qca, qsa, qpa, qD), out_b=(qcb, qsb, qpb))
+        cf.curvefp_gemm_prepared(qpa, fmt, qpb, fmt, M, N, K, c=C3, workspace=gws)
 
     step()                               # the static scratch's address is looked up before capture
     torch.cuda.synchronize()
@@ -69,7 +75,7 @@ def test_captured_step_replays(fmt):
         torch.cuda.synchronize()
         g.replay()
         torch.cuda.synchronize()
-        got = [t.clone() for t in (ca, sa, cb, sb, D, C, C2)]
+        got = [t.clone() for t in (ca, sa, cb, sb, D, C, C2, qca, qsa, qD, qcb, qsb, C3)]
         # the same calls eagerly, on the same inputs, into fresh outputs
         ea, esa = cf.curvefp_quantize(x, fmt)
         eb, esb = cf.curvefp_quantize(wt, fmt)
@@ -77,7 +83,8 @@ def test_captured_step_replays(fmt):
         eC = cf.curvefp_gemm_ws(ea, esa, eb, esb, M, N, K, fmt)
         torch.cuda.synchronize()
         say(f"[graph] replay seed={seed} fmt={fmt}")
-        for t, e, what in zip(got, (ea, esa, eb, esb, eD, eC, eC),
+        for t, e, what in zip(got, (ea, esa, eb, esb, eD, eC, eC, ea, esa, eD, eb, esb, eC),
                               ("codes A", "scales A", "codes B", "scales B", "dequantize", "prepared GEMM",
-                               "static-scratch GEMM")):
+                               "static-scratch GEMM", "pair codes A", "pair scales A", "pair reconstruction",
+                               "pair codes B", "pair scales B", "GEMM on the pair's operands")):
             same(t, e, f"replay seed={seed} {fmt}: {what}")
