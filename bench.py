@@ -761,8 +761,9 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
     """Every configuration timed on its own: quantize of each operand (GB/s, algorithmic bytes)
     and the GEMM call (TFLOP/s, fraction of dense fp16 peak: curvefp_gemm_ws, expansion included,
     or curvefp_gemm); with prepared operands also each operand's curvefp_prepare, its
-    curvefp_quantize_prepare (quantize and prepare in one launch, where the shape allows) and the
-    curvefp_gemm_prepared call alone; medians of `reps` calls each."""
+    curvefp_quantize_prepare (quantize and prepare in one launch, where the shape allows), the
+    curvefp_gemm_prepared call alone, and the whole step (both operands quantized and prepared,
+    then the prepared GEMM); medians of `reps` calls each."""
     import torch
     out = {}
     for name in CONFIGS:
@@ -809,12 +810,30 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
                 "gemm_prepared": {"us": t_gp * 1e6, "tflops": tfp, "frac": tfp / F16_DENSE_PEAK_TFLOPS},
             })
             # one launch per operand where it applies (blocks along K)
-            if w.a.axis == 1 and w.b.axis == 1:
+            fused = w.a.axis == 1 and w.b.axis == 1
+            if fused:
                 t_qpa = timed_median(lambda: cf.curvefp_quantize_prepare(ta, w.fmt, codes=ca, scales=sa, prepared=pa),
                                      stream, reps)
                 t_qpb = timed_median(lambda: cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb),
                                      stream, reps)
                 out[name].update({"quantize_prepare_a": {"us": t_qpa * 1e6}, "quantize_prepare_b": {"us": t_qpb * 1e6}})
+
+            # the whole step on this configuration, as the headline runs it: quantize and prepare
+            # both operands (one pair launch; quantize-transposed operands: quantize and prepare
+            # each), then the GEMM on the prepared operands; one stream, median of `reps` steps
+            def step():
+                if fused:
+                    cf.curvefp_quantize_prepare_pair(ta, tb, w.fmt, out_a=(ca, sa, pa), out_b=(cb, sb, pb))
+                else:
+                    cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa)
+                    cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb)
+                    cf.curvefp_prepare(ca, sa, w.M, w.K, w.fmt, prepared=pa)
+                    cf.curvefp_prepare(cb, sb, w.N, w.K, w.fmt, prepared=pb)
+                cf.curvefp_gemm_prepared(pa, w.fmt, pb, w.fmt, w.M, w.N, w.K, c=C, workspace=gws)
+            t_step = timed_median(step, stream, reps)
+            tfs = w.flops() / t_step / 1e12
+            out[name]["step"] = {"us": t_step * 1e6, "tflops": tfs, "what": "quantize_prepare_pair + gemm_prepared"
+                                 if fused else "quantize x2 (transpose) + prepare x2 + gemm_prepared"}
             del pa, pb, gws
         del ta, tb, ca, sa, cb, sb, C, ws
         torch.cuda.empty_cache()
