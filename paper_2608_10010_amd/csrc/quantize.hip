@@ -1551,11 +1551,12 @@ hipError_t launch_quantize_prepare_pair(const void* src_a, int64_t rows_a, int64
                                        int8_t* scales_b, void* prepared_b, float* dst_b, int64_t ld_dst_b, int dtype,
                                        int64_t k, int format, int block, hipStream_t s) {
     if (!qp_fused_rows(dtype, rows_a + rows_b, k)) {
-        hipError_t e = qp_separate(src_a, dtype, rows_a, k, ld_a, format, block, codes_a, scales_a, prepared_a, dst_a,
-                                   ld_dst_a, s);
+        // too large together: each operand on its own (the fused kernel where it takes it alone)
+        hipError_t e = launch_quantize_prepare(src_a, dtype, rows_a, k, ld_a, format, block, codes_a, scales_a,
+                                               prepared_a, dst_a, ld_dst_a, s);
         if (e != hipSuccess) return e;
-        return qp_separate(src_b, dtype, rows_b, k, ld_b, format, block, codes_b, scales_b, prepared_b, dst_b, ld_dst_b,
-                           s);
+        return launch_quantize_prepare(src_b, dtype, rows_b, k, ld_b, format, block, codes_b, scales_b, prepared_b,
+                                       dst_b, ld_dst_b, s);
     }
     return qp_launch(qp_operand(src_a, rows_a, k, ld_a, codes_a, scales_a, prepared_a, dst_a, ld_dst_a),
                      qp_operand(src_b, rows_b, k, ld_b, codes_b, scales_b, prepared_b, dst_b, ld_dst_b), dtype, k,

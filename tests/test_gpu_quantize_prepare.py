@@ -215,3 +215,30 @@ def test_pair_benchmark_operands():
     for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
                                             "prepared B")):
         same_bytes(x, y, f"gate/up pair: {n}")
+
+
+def test_pair_too_large_together():
+    """Operands of 16384-element rows too large to share a launch (over 2^26 elements together):
+    each is taken on its own -- the larger by the separate kernels, the smaller by the fused one --
+    with the outputs of two single calls, byte for byte."""
+    ra, rb, k = 5000, 1000, 16384
+    g = torch.Generator(device=DEV)
+    g.manual_seed(9)
+    ta = (torch.randn((ra, k), generator=g, device=DEV) * 3.0).to(torch.bfloat16)
+    tb = (torch.randn((rb, k), generator=g, device=DEV) * 0.02).to(torch.bfloat16)
+    say(f"[quantize_prepare] pair too large together rows={ra}+{rb} k={k}")
+    pa, pb = cf.curvefp_quantize_prepare_pair(ta, tb, "E4C3", dequantize_a=True)
+    sa_ = cf.curvefp_quantize_prepare(ta, "E4C3", dequantize=True)
+    sb_ = cf.curvefp_quantize_prepare(tb, "E4C3")
+    torch.cuda.synchronize()
+    for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
+                                            "prepared B")):
+        same_bytes(x, y, f"large pair: {n}")
+    rows = torch.tensor([0, 1, 2500, ra - 1], device=DEV)
+    xa = ta[rows].float().cpu().numpy()
+    oracle_check(xa, "E4C3", 32, pa[0][rows], pa[1][rows], pa[3][rows], "large pair A sampled rows")
+    rows_b = torch.tensor([0, rb - 1], device=DEV)
+    xb = tb[rows_b].float().cpu().numpy()
+    f = oracle.get_format("E4C3")
+    oc, os_ = oracle.quantize(xb, f)
+    assert np.array_equal(pb[1][rows_b].cpu().numpy(), os_) and np.array_equal(pb[0][rows_b].cpu().numpy(), oc)
