@@ -510,10 +510,11 @@ def curvefp_prepare(codes: torch.Tensor, scales: torch.Tensor, rows: int, k: int
     return prepared
 
 
-def _qp_outputs(what, src, f, block, codes, scales, prepared, dst, dequantize, stream):
-    """The outputs of one operand of quantize-prepare (allocated here when not given), checked."""
-    _on_gpu(what, [("src", src)], stream)
-    _source_arg(what, src)
+def _qp_outputs(what, src, f, block, codes, scales, prepared, dst, dequantize, stream, tag=""):
+    """The outputs of one operand of quantize-prepare (allocated here when not given), checked;
+    `tag` prefixes the tensor names in error messages (the pair's operands)."""
+    _on_gpu(what, [(tag + "src", src)], stream)
+    _source_arg(what + (f" ({tag.rstrip('_')})" if tag else ""), src)
     rows, k = src.shape
     if codes is None:
         shape = (rows, k // 32, 28) if f == 2 else (rows, k)
@@ -524,13 +525,13 @@ def _qp_outputs(what, src, f, block, codes, scales, prepared, dst, dequantize, s
         prepared = torch.empty(curvefp_prepared_bytes(rows, k, 0), dtype=torch.uint8, device=src.device)
     if dst is None and dequantize:
         dst = torch.empty((rows, k), dtype=torch.float32, device=src.device)
-    ts = [("src", src), ("codes", codes), ("scales", scales), ("prepared", prepared)]
-    _on_gpu(what, ts + ([("dst", dst)] if dst is not None else []), stream)
-    _codes_arg(what, "codes", codes, f, rows, k, block)
-    _scales_arg(what, "scales", scales, rows, k, block)
-    _dense(what, "prepared", prepared, curvefp_prepared_bytes(rows, k, 0))
+    ts = [(tag + "src", src), (tag + "codes", codes), (tag + "scales", scales), (tag + "prepared", prepared)]
+    _on_gpu(what, ts + ([(tag + "dst", dst)] if dst is not None else []), stream)
+    _codes_arg(what, tag + "codes", codes, f, rows, k, block)
+    _scales_arg(what, tag + "scales", scales, rows, k, block)
+    _dense(what, tag + "prepared", prepared, curvefp_prepared_bytes(rows, k, 0))
     if dst is not None:
-        _matrix(what, "dst", dst, rows, k, (torch.float32,))
+        _matrix(what, tag + "dst", dst, rows, k, (torch.float32,))
     return codes, scales, prepared, dst
 
 
@@ -573,8 +574,8 @@ def curvefp_quantize_prepare_pair(src_a: torch.Tensor, src_b: torch.Tensor, fmt,
                          f"{tuple(src_b.shape)} {src_b.dtype}")
     oa = (list(out_a) + [None] * (4 - len(out_a))) if out_a is not None else [None] * 4
     ob = (list(out_b) + [None] * (4 - len(out_b))) if out_b is not None else [None] * 4
-    a = _qp_outputs(what, src_a, f, block, *oa, dequantize_a, stream)
-    b = _qp_outputs(what, src_b, f, block, *ob, dequantize_b, stream)
+    a = _qp_outputs(what, src_a, f, block, *oa, dequantize_a, stream, tag="a_")
+    b = _qp_outputs(what, src_b, f, block, *ob, dequantize_b, stream, tag="b_")
     st = lib().curvefp_quantize_prepare_pair(*_qp_args(src_a, *a), *_qp_args(src_b, *b), DTYPES[src_a.dtype],
                                              src_a.shape[1], f, block, _stream(stream))
     _check(st, what)

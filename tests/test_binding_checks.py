@@ -203,9 +203,9 @@ def test_quantize_prepare_pair_checks(meta):
         cf.curvefp_quantize_prepare_pair(a, meta((300, K + 32), torch.bfloat16), "E4C3", stream=STREAM)
     with pytest.raises(ValueError, match="share k and dtype"):
         cf.curvefp_quantize_prepare_pair(a, meta((300, K), torch.float32), "E4C3", stream=STREAM)
-    with pytest.raises(ValueError, match="prepared"):
+    with pytest.raises(ValueError, match="b_prepared"):
         cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_b=(None, None, meta((1024,), torch.uint8)), stream=STREAM)
-    with pytest.raises(ValueError, match="dst"):
+    with pytest.raises(ValueError, match="a_dst"):
         cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_a=(None, None, None, meta((63, K), torch.float32)),
                                          stream=STREAM)
     with pytest.raises(ValueError, match="not on a GPU"):
