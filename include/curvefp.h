@@ -335,7 +335,8 @@ int curvefp_prepare(const void* codes, const int8_t* scales, int64_t rows, int64
  *   prepared at least curvefp_prepared_bytes(rows, k, 0) bytes (prepared_size), 256-byte aligned.
  *   dst      null, or [rows][ld_dst] fp32 with 16-byte aligned rows.
  * Rows of up to 8192 bf16 or 4096 fp32 elements (bf16 rows of up to 16384 in tensors of at most
- * 2^26 elements) take one launch: a wave or a workgroup reads its row once, holds it in LDS while
+ * 2^26 elements), in tensors of fewer than 2^23 rows, take one launch: a wave or a workgroup
+ * reads its row once, holds it in LDS while
  * it takes the block scales and the row's largest scale, then writes every output.  Other shapes
  * run the quantize, expansion and reconstruction kernels in turn (the same outputs; measured
  * faster there).  block is 32, 64, 128, 256 or 512 (other G: curvefp_quantize,
@@ -356,6 +357,8 @@ int curvefp_quantize_prepare(const void* src, int dtype, int64_t rows, int64_t k
  * scales, prepared buffer (prepared_a_size / prepared_b_size bytes) and optional reconstruction
  * (dst_a / dst_b, null for none).  The outputs are those of two curvefp_quantize_prepare calls,
  * bit for bit; one launch spreads both operands over the whole GPU and needs no second stream.
+ * When the two together fall outside the one-launch shapes above (rows_a + rows_b rows over k),
+ * each operand runs as curvefp_quantize_prepare would run it, A then B, on the same stream.
  * Errors: those of curvefp_quantize_prepare for either operand, and CURVEFP_ERR_SHAPE for
  * rows_a + rows_b >= 2^31.
  */

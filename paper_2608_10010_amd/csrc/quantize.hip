@@ -1491,6 +1491,8 @@ hipError_t launch_qp_fmt(const QPOperand& a, const QPOperand& b, int dtype, int6
 // by one wave, were 15-40% slower on those shapes.)
 bool qp_fused_rows(int dtype, int64_t rows, int64_t k) {
     const int64_t cpr = k / 8;
+    // the launch's work-items (up to 256 per row, the padding rows included) stay below 2^32
+    if (rows >= ((int64_t)1 << 23)) return false;
     if (dtype != 1) return cpr <= 512;
     return cpr <= 1024 || (cpr <= 2048 && rows * k <= ((int64_t)1 << 26));
 }
