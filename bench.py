@@ -702,7 +702,7 @@ def gpu_hold(stream, us: float = 300.0):
         torch.cuda._sleep(_HOLD_CYCLES)
 
 
-def timed_median(fn, stream, reps: int = 10, warm: int = 3, before=None):
+def timed_median(fn, stream, reps: int = 20, warm: int = 3, before=None):
     """Median of `reps` individually timed calls: HIP events on the library's stream around each
     call, the GPU held back by gpu_hold until both events and the call are enqueued; `before`
     (e.g. a cache flush) runs ahead of the hold each time."""
@@ -725,7 +725,7 @@ def timed_median(fn, stream, reps: int = 10, warm: int = 3, before=None):
     return float(np.median(ts))
 
 
-def copy_peak(dev, stream, nbytes: int = 1 << 30, reps: int = 10):
+def copy_peak(dev, stream, nbytes: int = 1 << 30, reps: int = 20):
     """A plain 1 GiB device-to-device copy (read once, written once): the achievable HBM rate on
     this box, median of individually timed copies."""
     import torch
@@ -738,7 +738,7 @@ def copy_peak(dev, stream, nbytes: int = 1 << 30, reps: int = 10):
             "what": f"torch copy_ of a {nbytes >> 20} MiB device buffer (read + write), median of {reps}"}
 
 
-def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 10):
+def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 20):
     """Context for the GEMM's roofline fraction: the vendor library's plain fp16 GEMM (torch.matmul,
     hipBLASLt) on M x N with 3K, the same matrix-core work as the CurveFP GEMM's three fp16
     products per useful product; median of `reps` individually timed calls."""
@@ -757,7 +757,7 @@ def vendor_reference(w, dev, stream, gemm_tflops: float, reps: int = 10):
             "curvefp_vs_vendor": 3.0 * gemm_tflops / tf}
 
 
-def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
+def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 20):
     """Every configuration timed on its own: quantize of each operand (GB/s, algorithmic bytes)
     and the GEMM call (TFLOP/s, fraction of dense fp16 peak: curvefp_gemm_ws, expansion included,
     or curvefp_gemm); with prepared operands also each operand's curvefp_prepare, its
@@ -766,6 +766,8 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
     then the prepared GEMM); medians of `reps` calls each."""
     import torch
     out = {}
+    # written before each cold call: 512 MiB evicts the 256 MB MALL and the L2s
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     for name in CONFIGS:
         w = W.get(name)
         tdt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
@@ -775,10 +777,11 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
         cb, sb = cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis)
         C = torch.empty((w.M, w.N), dtype=torch.float32, device=dev)
         ws = cf.gemm_workspace(w.M, w.N, w.K, dev) if gemm_path in ("ws", "prepared") else None
-        t_a = timed_median(lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa),
-                           stream, reps)
-        t_b = timed_median(lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb),
-                           stream, reps)
+        q_a = lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa)
+        q_b = lambda: cf.curvefp_quantize(tb, w.fmt, block_axis=w.b.axis, codes=cb, scales=sb)
+        t_a, t_b = timed_median(q_a, stream, reps), timed_median(q_b, stream, reps)
+        t_a_cold = timed_median(q_a, stream, reps, warm=0, before=flush.zero_)
+        t_b_cold = timed_median(q_b, stream, reps, warm=0, before=flush.zero_)
         if gemm_path in ("ws", "prepared"):
             t_g = timed_median(lambda: cf.curvefp_gemm_ws(ca, sa, cb, sb, w.M, w.N, w.K, w.fmt, c=C, workspace=ws),
                                stream, reps)
@@ -789,8 +792,10 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
         out[name] = {
             "workload": w.name, "format": w.fmt, "M": w.M, "N": w.N, "K": w.K,
             "quantize_a": {"us": t_a * 1e6, "gbps": w.M * w.K * bpe / t_a / 1e9,
+                           "us_cold": t_a_cold * 1e6, "gbps_cold": w.M * w.K * bpe / t_a_cold / 1e9,
                            "axis": w.a.axis},
             "quantize_b": {"us": t_b * 1e6, "gbps": w.N * w.K * bpe / t_b / 1e9,
+                           "us_cold": t_b_cold * 1e6, "gbps_cold": w.N * w.K * bpe / t_b_cold / 1e9,
                            "axis": w.b.axis},
             "gemm": {"us": t_g * 1e6, "gflop": w.flops() / 1e9, "tflops": tf,
                      "frac": tf / F16_DENSE_PEAK_TFLOPS},
@@ -837,13 +842,14 @@ def config_sweep(cf, W, dev, stream, gemm_path: str, reps: int = 10):
             del pa, pb, gws
         del ta, tb, ca, sa, cb, sb, C, ws
         torch.cuda.empty_cache()
-    out["timing"] = f"median of {reps} individually timed calls each (HIP events), inputs resident in HBM"
+    out["timing"] = (f"median of {reps} individually timed calls each (HIP events), inputs resident in HBM; "
+                     f"*_cold: each call after a 512 MiB write that evicts the MALL and the L2s")
     out["roofline"] = (f"quantize against {HBM_PEAK_GBS / 1000:.0f} TB/s (algorithmic bytes: source + codes + "
                        f"scales); GEMM against {F16_DENSE_PEAK_TFLOPS / 1000:.1f} PFLOP/s dense fp16 (2MNK flop)")
     return out
 
 
-def backward_mixed(cf, W, dev, stream, reps: int = 10):
+def backward_mixed(cf, W, dev, stream, reps: int = 20):
     """dX = Q_G(dY) Q_W(W) and dW = Q_G(dY)^T Q_A(X) of the 7B up-projection: dY quantized once
     in E5C2 along its rows, W and X as their forward E4C3 codes.  Each GEMM call (prep,
     expansions, MFMA GEMM) is timed with HIP events on the library's stream: median of `reps`
@@ -901,7 +907,7 @@ def backward_mixed(cf, W, dev, stream, reps: int = 10):
     return out
 
 
-def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 10):
+def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 20):
     """The inference GEMM with its output requantized to E3C3 (the next layer's activation
     format): curvefp_gemm_requant (fused epilogue) against curvefp_gemm_ws followed by
     curvefp_quantize of the fp32 C; median of `reps` individually timed calls each."""
@@ -940,7 +946,7 @@ def requant(cf, w, ca, sa, cb, sb, dev, stream, reps: int = 10):
     return out
 
 
-def static_scales(cf, w, tb, dev, stream, reps: int = 10):
+def static_scales(cf, w, tb, dev, stream, reps: int = 20):
     """The inference weight (4096 x 4096 bf16) quantized as a static operand: curvefp_quantize_mse
     with 4 candidate scales, against curvefp_quantize (ceil-absmax) on the same tensor; median of
     `reps` individually timed calls each, bytes as for quantize (source + codes + scales)."""
@@ -970,7 +976,7 @@ def static_scales(cf, w, tb, dev, stream, reps: int = 10):
     return out
 
 
-def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 10):
+def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 20):
     """The inference workload with one scale per G elements (Eq. effective-rate; Sec. 4.2's G64
     and G512, and rowwise G = K): per G the median of `reps` individually timed calls of
     quantize(act), quantize(weight) and curvefp_gemm_ws.  Quantize bytes are the algorithmic
@@ -1020,7 +1026,7 @@ def block_sizes(cf, w, ta, tb, dev, stream, reps: int = 10):
     return out
 
 
-def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 10):
+def radix_variants(cf, w, ta, tb, dev, stream, reps: int = 20):
     """The inference workload's operands quantized and multiplied in E4C3 with the radices of
     Tab. radix-frontier (r = 2: 8 phases; 2^(8/9): 9; 2^(3/4): 32): per format the median of
     `reps` individually timed calls of quantize(act), quantize(weight) and curvefp_gemm_ws."""
@@ -1320,7 +1326,7 @@ def main():
 
     # The step above runs back to back on the same inputs, so sources that fit the 256 MB MALL
     # may be served from it.  Each call again on its own after a 512 MiB write that evicts the
-    # MALL and the L2s (median of 10): the cold-cache figures, inputs from HBM.
+    # MALL and the L2s (median of 20): the cold-cache figures, inputs from HBM.
     flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     cold_calls = {
         "quantize_a": lambda: cf.curvefp_quantize(ta, w.fmt, block_axis=w.a.axis, codes=ca, scales=sa),
@@ -1339,7 +1345,7 @@ def main():
             "quantize_prepare_b": lambda: cf.curvefp_quantize_prepare(tb, w.fmt, codes=cb, scales=sb, prepared=pb)})
     cold = {}
     for n, fn in cold_calls.items():
-        cold[n] = timed_median(fn, stream, 10, warm=0, before=flush.zero_) * 1e6
+        cold[n] = timed_median(fn, stream, 20, warm=0, before=flush.zero_) * 1e6
     del flush
     result["kernels_us_cold"] = cold
     result["cold_cache"] = {
@@ -1347,7 +1353,7 @@ def main():
         "quantize_gbps": {"act": qa_bytes / (cold["quantize_a"] * 1e-6) / 1e9,
                           "weight": qb_bytes / (cold["quantize_b"] * 1e-6) / 1e9},
         "dequantize_gbps": dq_bytes / (cold["dequantize"] * 1e-6) / 1e9,
-        "protocol": "each call alone after a 512 MiB device write (MALL and L2 evicted), median of 10",
+        "protocol": "each call alone after a 512 MiB device write (MALL and L2 evicted), median of 20",
     }
     if prepared:
         result["cold_cache"]["prepare_gbps"] = {"act": pa_bytes / (cold["prepare_a"] * 1e-6) / 1e9,
