@@ -63,8 +63,10 @@ def parse():
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--workload", default=HEADLINE)
     p.add_argument("--gemm", choices=["prepared", "ws", "fused"], default="prepared",
-                   help="prepared: each operand expanded by curvefp_prepare as soon as it is quantized (on "
-                        "its own stream), then curvefp_gemm_prepared; ws: curvefp_gemm_ws (both expansions "
+                   help="prepared: both operands quantized and expanded for the GEMM by one "
+                        "curvefp_quantize_prepare_pair launch (--separate-step: quantize, prepare and "
+                        "dequantize calls on two streams), then curvefp_gemm_prepared; ws: quantize calls, then "
+                        "curvefp_gemm_ws (both expansions "
                         "and the GEMM in one call) with a workspace allocated before the timed region; "
                         "fused: curvefp_gemm (expansion inside the GEMM kernel)")
     p.add_argument("--no-cpu-baseline", action="store_true")
@@ -1077,7 +1079,7 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only: this build has no multi-GPU path "
+        print(f"bench.py measures one GPU only: the library has no multi-GPU path "
               f"(asked for --gpus {args.gpus}, WORLD_SIZE={world}).", file=sys.stderr)
         sys.exit(2)
 
