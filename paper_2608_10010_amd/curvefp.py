@@ -572,6 +572,9 @@ def curvefp_quantize_prepare_pair(src_a: torch.Tensor, src_b: torch.Tensor, fmt,
     if src_a.dim() == 2 and src_b.dim() == 2 and (src_a.shape[1] != src_b.shape[1] or src_a.dtype != src_b.dtype):
         raise ValueError(f"{what}: the sources must share k and dtype, got {tuple(src_a.shape)} {src_a.dtype} and "
                          f"{tuple(src_b.shape)} {src_b.dtype}")
+    for tag, out in (("out_a", out_a), ("out_b", out_b)):
+        if out is not None and not 3 <= len(out) <= 4:
+            raise ValueError(f"{what}: {tag} is (codes, scales, prepared[, dst]), got {len(out)} entries")
     oa = (list(out_a) + [None] * (4 - len(out_a))) if out_a is not None else [None] * 4
     ob = (list(out_b) + [None] * (4 - len(out_b))) if out_b is not None else [None] * 4
     a = _qp_outputs(what, src_a, f, block, *oa, dequantize_a, stream, tag="a_")

@@ -210,6 +210,10 @@ def test_quantize_prepare_pair_checks(meta):
                                          stream=STREAM)
     with pytest.raises(ValueError, match="not on a GPU"):
         cf.curvefp_quantize_prepare_pair(a, torch.zeros((300, K), dtype=torch.bfloat16), "E4C3", stream=STREAM)
+    with pytest.raises(ValueError, match="out_b is"):
+        cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_b=(None, None), stream=STREAM)
+    with pytest.raises(ValueError, match="out_a is"):
+        cf.curvefp_quantize_prepare_pair(a, b, "E4C3", out_a=(None,) * 5, stream=STREAM)
 
 
 def test_mixed_gemm_checks(meta):
