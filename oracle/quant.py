@@ -258,7 +258,9 @@ def dequantize(codes: np.ndarray, scales: np.ndarray, fmt: Format, block: int = 
     mag = np.ldexp(level_value_f64(fmt, np.where(nz, n, 0)), a)
     val = np.where(s == 1, -mag, mag)
     val = np.where(nz, val, 0.0)
-    out = val.astype(np.float32)
+    # magnitudes past the fp32 range round to +-inf, as round-to-nearest does (no warning wanted)
+    with np.errstate(over="ignore"):
+        out = val.astype(np.float32)
     out = np.where(a == POISON_SCALE, np.float32(np.nan), out)
     return out.astype(np.float32)
 
