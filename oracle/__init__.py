@@ -18,8 +18,8 @@ Everything here is written from the paper (arXiv 2608.10010, "CurveFP"):
                                App. A.1 (bin addressing)
 * storage rate              -- Sec. 3.3, Eq. (effective-rate)
 
-Readings of points the paper leaves open are listed in the design doc and repeated
-at the function that takes them.
+Readings of points the paper leaves open are stated at the function that takes
+them.
 """
 
 from .formats import FORMATS, Format, get_format, rational_format

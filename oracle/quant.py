@@ -7,7 +7,7 @@ Plain numpy in float64.  Each function follows the paper's definition directly:
                   error, saturate at the endpoints                 (Sec. 3.1)
 * block scale     dynamic operands use ceil-absmax scaling         (Sec. 3.1, App. A.2)
 
-Readings taken where the paper is silent (each is listed in the design doc):
+Readings taken where the paper is silent:
 
 * ceil-absmax: a_b is the smallest integer a with amax <= 2^a * fl32(L_max),
   L_max = r^{n_max/K} the largest positive level.  fl32(L_max) is the value the

@@ -14,7 +14,7 @@ def pytest_configure(config):
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests run on the GPU machine only; elsewhere they are skipped with a reason.
+    # GPU tests run only where a GPU is present; elsewhere they are skipped with a reason.
     try:
         import torch
         has_gpu = torch.cuda.is_available()
