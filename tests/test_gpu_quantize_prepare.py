@@ -202,6 +202,30 @@ def test_pair(fmt, dtype, ra, rb, k, block):
         same_bits(C.cpu().numpy(), Cw.cpu().numpy(), f"pair {fmt} gemm")
 
 
+@pytest.mark.parametrize("dtype,k", [("bf16", 1024), ("f32", 4096), ("bf16", 8192)])
+def test_pair_both_reconstructed(dtype, k):
+    """Both operands with their reconstruction (the second operand's dst included), against single
+    calls byte for byte and against the oracle."""
+    ra, rb = 70, 33
+    rng = np.random.default_rng(k + 3)
+    A = (rng.standard_normal((ra, k)) * np.exp2(rng.uniform(-30, 30, (ra, 1)))).astype(np.float32)
+    B = (rng.standard_normal((rb, k)) * np.exp2(rng.uniform(-30, 30, (rb, 1)))).astype(np.float32)
+    if dtype == "bf16":
+        A, B = W.bf16_round(A), W.bf16_round(B)
+    ta, tb = source(A, dtype), source(B, dtype)
+    say(f"[quantize_prepare] pair, both reconstructed, dtype={dtype} rows={ra}+{rb} k={k}")
+    pa, pb = cf.curvefp_quantize_prepare_pair(ta, tb, "E3C3", dequantize_a=True, dequantize_b=True)
+    sa_ = cf.curvefp_quantize_prepare(ta, "E3C3", dequantize=True)
+    sb_ = cf.curvefp_quantize_prepare(tb, "E3C3", dequantize=True)
+    torch.cuda.synchronize()
+    assert len(pa) == 4 and len(pb) == 4
+    for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
+                                            "prepared B", "dst B")):
+        same_bytes(x, y, f"pair both reconstructed {dtype} k={k}: {n}")
+    oracle_check(A, "E3C3", 32, pa[0], pa[1], pa[3], "pair both reconstructed A")
+    oracle_check(B, "E3C3", 32, pb[0], pb[1], pb[3], "pair both reconstructed B")
+
+
 def test_pair_benchmark_operands():
     """The benchmark's step: both gate/up operands in one launch equal two single calls."""
     w = W.get("sweep_gateup_E4C3")
