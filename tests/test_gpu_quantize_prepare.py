@@ -226,6 +226,33 @@ def test_pair_both_reconstructed(dtype, k):
     oracle_check(B, "E3C3", 32, pb[0], pb[1], pb[3], "pair both reconstructed B")
 
 
+@pytest.mark.parametrize("k", [512, 4096])
+def test_pair_row_strides(k):
+    """Both operands read from row-strided views and reconstructed into row-strided outputs: the
+    padding columns of the sources are never read and those of the outputs never written."""
+    ra, rb = 45, 130
+    rng = np.random.default_rng(k)
+    A = W.bf16_round(rng.standard_normal((ra, k)).astype(np.float32))
+    B = W.bf16_round((rng.standard_normal((rb, k)) * 0.02).astype(np.float32))
+    fa = to_dev(np.concatenate([A, np.full((ra, 64), 7.0e30, np.float32)], axis=1), "bf16")
+    fb = to_dev(np.concatenate([B, np.full((rb, 32), -3.0e30, np.float32)], axis=1), "bf16")
+    ta, tb = fa[:, :k], fb[:, :k]
+    da = torch.full((ra, k + 16), 5.0, dtype=torch.float32, device=DEV)
+    db = torch.full((rb, k + 8), 6.0, dtype=torch.float32, device=DEV)
+    say(f"[quantize_prepare] pair on row-strided views k={k}")
+    pa, pb = cf.curvefp_quantize_prepare_pair(ta, tb, "E4C3", out_a=(None, None, None, da[:, :k]),
+                                              out_b=(None, None, None, db[:, :k]))
+    sa_ = cf.curvefp_quantize_prepare(ta.contiguous(), "E4C3", dequantize=True)
+    sb_ = cf.curvefp_quantize_prepare(tb.contiguous(), "E4C3", dequantize=True)
+    torch.cuda.synchronize()
+    for x, y, n in zip(pa + pb, sa_ + sb_, ("codes A", "scales A", "prepared A", "dst A", "codes B", "scales B",
+                                            "prepared B", "dst B")):
+        same_bytes(x, y, f"strided pair k={k}: {n}")
+    assert bool((da[:, k:] == 5.0).all()) and bool((db[:, k:] == 6.0).all()), "padding columns written"
+    oracle_check(A, "E4C3", 32, pa[0], pa[1], pa[3], "strided pair A")
+    oracle_check(B, "E4C3", 32, pb[0], pb[1], pb[3], "strided pair B")
+
+
 def test_pair_benchmark_operands():
     """The benchmark's step: both gate/up operands in one launch equal two single calls."""
     w = W.get("sweep_gateup_E4C3")
