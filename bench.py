@@ -1338,6 +1338,8 @@ def main():
     }
     if prepared:
         cold_calls.update({"prepare_a": prepare_a, "prepare_b": prepare_b})
+    # the whole step, its sources and operands read from HBM
+    cold_calls["step"] = step
     if fused_step:
         cold_calls.update({
             "quantize_prepare_pair": lambda: cf.curvefp_quantize_prepare_pair(
@@ -1351,6 +1353,7 @@ def main():
     del flush
     result["kernels_us_cold"] = cold
     result["cold_cache"] = {
+        "step_tflops": flops / (cold["step"] * 1e-6) / 1e12,
         "gemm_tflops": flops / (cold["gemm"] * 1e-6) / 1e12,
         "quantize_gbps": {"act": qa_bytes / (cold["quantize_a"] * 1e-6) / 1e9,
                           "weight": qb_bytes / (cold["quantize_b"] * 1e-6) / 1e9},
