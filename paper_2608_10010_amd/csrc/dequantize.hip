@@ -28,8 +28,9 @@ namespace {
 // chunk g = 8 consecutive codes: chunk g mod cpr of row g / cpr, block g / 4 (blocks are
 // contiguous in the code and scale arrays); a grid-stride loop over the chunks, one per thread
 // per round (a capped grid with plain stores measured fastest for this write-heavy stream; the
-// cap grows with the tensor, see the launch)
-template <class F>
+// cap grows with the tensor, see the launch), or with TWO, two rounds per pass whose loads are
+// all issued before the first chunk is written
+template <class F, bool TWO>
 __global__ __launch_bounds__(256) void dequantize_kernel(
     const uint8_t* __restrict__ codes, const int8_t* __restrict__ scales, uint32_t nchunks, uint32_t cpr,
     Div32 dcpr, int64_t ld, float* __restrict__ dst, int fidx, Div32 dgq) {
@@ -43,25 +44,36 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
     __syncthreads();
     const bool dense = ld == (int64_t)cpr * 8;
     const uint32_t stride = gridDim.x * 256u;
-    for (uint32_t g = blockIdx.x * 256u + threadIdx.x; g < nchunks; g += stride) {
+    // the words of chunk g (8 codes) and its block's scale
+    auto fetch = [&](uint32_t g, uint2& w, uint32_t& w2, int& a) {
         const uint32_t b = g >> 2;                  // 32-element group; its scale is that of block b / (G / 32)
-        const int a = scales[div32(b, dgq)];
+        a = scales[div32(b, dgq)];
+        if (!F::PACKED7) {
+            w = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
+            w2 = 0u;
+        } else {
+            // bytes [7 part, 7 part + 7) of the block's 28 bytes; parts 1 and 2 (bytes 7..13 and
+            // 14..20) straddle three dwords, parts 0 and 3 two
+            const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + (uint64_t)b * 28);
+            const int part = (int)(g & 3);
+            const int d0 = (7 * part) >> 2;
+            w = make_uint2(base[d0], base[d0 + 1]);
+            w2 = (part == 1 || part == 2) ? base[d0 + 2] : 0u;
+        }
+    };
+    auto emit = [&](uint32_t g, uint2 w, uint32_t w2, int a) {
         uint32_t c[8];
         if (!F::PACKED7) {
-            const uint2 w = *reinterpret_cast<const uint2*>(codes + (uint64_t)g * 8);
 #pragma unroll
             for (int i = 0; i < 4; i++) {
                 c[i] = (w.x >> (8 * i)) & 0xFFu;
                 c[4 + i] = (w.y >> (8 * i)) & 0xFFu;
             }
         } else {
-            // bytes [7 part, 7 part + 7) of the block's 28 bytes; parts 1 and 2 (bytes 7..13 and
-            // 14..20) straddle three dwords, parts 0 and 3 two
-            const uint32_t* base = reinterpret_cast<const uint32_t*>(codes + (uint64_t)b * 28);
             const int part = (int)(g & 3);
-            const int d0 = (7 * part) >> 2, off = 7 * part - 4 * d0;
-            const uint64_t lo = (uint64_t)base[d0] | ((uint64_t)base[d0 + 1] << 32);
-            const uint64_t hi = (part == 1 || part == 2) ? (uint64_t)base[d0 + 2] : 0ull;
+            const int off = 7 * part - 4 * ((7 * part) >> 2);
+            const uint64_t lo = (uint64_t)w.x | ((uint64_t)w.y << 32);
+            const uint64_t hi = w2;
             const uint64_t chunk = off ? ((lo >> (8 * off)) | (hi << (64 - 8 * off))) : lo;
 #pragma unroll
             for (int i = 0; i < 8; i++) c[i] = (uint32_t)(chunk >> (7 * i)) & 0x7Fu;
@@ -84,6 +96,30 @@ __global__ __launch_bounds__(256) void dequantize_kernel(
         uint4* out = reinterpret_cast<uint4*>(dst + e);
         out[0] = make_uint4(o[0], o[1], o[2], o[3]);
         out[1] = make_uint4(o[4], o[5], o[6], o[7]);
+    };
+    if (!TWO) {
+        for (uint32_t g = blockIdx.x * 256u + threadIdx.x; g < nchunks; g += stride) {
+            uint2 w;
+            uint32_t x;
+            int a;
+            fetch(g, w, x, a);
+            emit(g, w, x, a);
+        }
+        return;
+    }
+    // large grids: two chunks per thread and pass (g and g + stride), both requested before either
+    // is written (64-bit positions: g + 2 stride can pass 2^32)
+    for (uint64_t p = (uint64_t)blockIdx.x * 256u + threadIdx.x; p < nchunks; p += 2ull * stride) {
+        const uint32_t g0 = (uint32_t)p;
+        const bool two = p + stride < nchunks;
+        const uint32_t g1 = two ? (uint32_t)(p + stride) : g0;
+        uint2 w0, w1 = make_uint2(0u, 0u);
+        uint32_t x0, x1 = 0u;
+        int a0, a1 = 0;
+        fetch(g0, w0, x0, a0);
+        if (two) fetch(g1, w1, x1, a1);
+        emit(g0, w0, x0, a0);
+        if (two) emit(g1, w1, x1, a1);
     }
 }
 
@@ -104,9 +140,17 @@ hipError_t launch_fmt(const void* codes, const int8_t* scales, int64_t outer, in
         int64_t blocks = (nchunks + 255) / 256;
         const int64_t cap = half > 8192 ? half : 8192;
         blocks = blocks < cap ? blocks : cap;
-        hipLaunchKernelGGL((dequantize_kernel<F>), dim3((unsigned)blocks), dim3(256), 0, s,
-                           cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k), scales + r0 * (k / block),
-                           (uint32_t)nchunks, (uint32_t)cpr, make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx, dgq);
+        // the two rounds of large grids with both chunks' loads in flight at once (16% faster on
+        // 32768 x 8192 from HBM; on grids of at most 8192 workgroups the plain loop measured faster)
+        const uint8_t* cr = cp + (F::PACKED7 ? r0 * (k / 32) * 28 : r0 * k);
+        if (half > 8192)
+            hipLaunchKernelGGL((dequantize_kernel<F, true>), dim3((unsigned)blocks), dim3(256), 0, s, cr,
+                               scales + r0 * (k / block), (uint32_t)nchunks, (uint32_t)cpr,
+                               make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx, dgq);
+        else
+            hipLaunchKernelGGL((dequantize_kernel<F, false>), dim3((unsigned)blocks), dim3(256), 0, s, cr,
+                               scales + r0 * (k / block), (uint32_t)nchunks, (uint32_t)cpr,
+                               make_div32((uint32_t)cpr), ld, dst + r0 * ld, fidx, dgq);
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }

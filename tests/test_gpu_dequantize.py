@@ -85,12 +85,12 @@ def test_output_row_stride():
 
 
 @pytest.mark.parametrize("fmt", ["E4C3", "E3C3"])
-def test_large_tensor_two_rounds(fmt):
-    """A reconstruction large enough for the launch's two chunks per thread (9216 x 8192 codes:
-    more chunks than 8192 workgroups of 256 threads can take in one round), as codes and scales
-    the oracle quantizes from the seeded source: sampled rows, every 8-code chunk of them, bit for
-    bit."""
-    M, K = 9216, 8192
+@pytest.mark.parametrize("M,K", [(9216, 8192), (8100, 4160)])
+def test_large_tensor_two_rounds(fmt, M, K):
+    """A reconstruction large enough for the launch's two chunks per thread (more chunks than 8192
+    workgroups of 256 threads can take in one round; 8100 x 4160 leaves the last threads one chunk),
+    as codes and scales the oracle quantizes from the seeded source: sampled rows, every 8-code
+    chunk of them, bit for bit."""
     rng = np.random.default_rng(77)
     rows = np.unique(np.concatenate([np.arange(0, M, 127), [M - 1]]))
     codes = np.zeros((M, K), dtype=np.uint8)
